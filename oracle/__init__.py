@@ -1,0 +1,231 @@
+"""OSCAR CPU oracle -- test infrastructure only.
+
+Loads ``liboscar_oracle.so`` (plain C, fp64; see ``oscar_oracle.c``) through
+ctypes and exposes numpy-in / numpy-out wrappers.  Only the test suite, the
+package smoke check and the benchmark's CPU-baseline leg use this module; the
+GPU library never imports or links it.
+
+What it computes (arXiv 2605.17757):
+  * ``kv_append``     -- rotate, clip, asymmetric-INT2 quantize and pack new K/V
+                         rows (Sec. 4 "KV Cache Update"; App. "Scale
+                         Determination and Per-token Clipping Details").
+  * ``decode``        -- attention over the packed cache, fp64, rotated basis
+                         (Alg. 1 DecodeStep; Sec. 2 attention).
+  * ``decode_brute``  -- the same in the original basis (dequantize, rotate back,
+                         plain softmax attention); tiny inputs only.
+  * ``bf16_decode``   -- plain fp64 attention over a bf16 paged cache.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+import subprocess
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+_SRC = os.path.join(_HERE, "oscar_oracle.c")
+_LIB = os.path.join(_HERE, "liboscar_oracle.so")
+
+CFLAGS = ["-O2", "-std=c11", "-fopenmp", "-ffp-contract=off", "-fno-fast-math",
+          "-fPIC", "-shared", "-Wall", "-Wno-unused-function"]
+
+
+def build(force: bool = False) -> str:
+    """Compile the oracle with gcc (IEEE arithmetic, no FMA contraction)."""
+    if force or not os.path.exists(_LIB) or os.path.getmtime(_LIB) < os.path.getmtime(_SRC):
+        tmp = _LIB + ".tmp%d" % os.getpid()
+        subprocess.run(["gcc", *CFLAGS, _SRC, "-o", tmp, "-lm"], check=True)
+        os.replace(tmp, _LIB)
+    return _LIB
+
+
+_lib = None
+
+
+def lib():
+    global _lib
+    if _lib is None:
+        build()
+        L = ctypes.CDLL(_LIB)
+        P = ctypes.c_void_p
+        i32, i64, f32, f64 = ctypes.c_int, ctypes.c_int64, ctypes.c_float, ctypes.c_double
+        L.oracle_page_head_bytes.restype = ctypes.c_size_t
+        L.oracle_page_head_bytes.argtypes = [i32, i32, i32]
+        L.oracle_rotate_row.argtypes = [P, P, i32, P]
+        L.oracle_quantize_row.restype = i32
+        L.oracle_quantize_row.argtypes = [P, i32, i32, f32, P, P, P]
+        L.oracle_kv_append.restype = i64
+        L.oracle_kv_append.argtypes = [i32, i32, i32, i32, i64, P, P, P, P, i32, P, P, f32, f32]
+        L.oracle_read_token.argtypes = [i32, i32, i32, i32, P, i64, i32, i32, i32, P, P, P]
+        L.oracle_decode.restype = i32
+        L.oracle_decode.argtypes = [i32, i32, i32, i32, i64, P, P, i32, i32, P, i32, P, P, P,
+                                    f64, P, i32, P]
+        L.oracle_decode_brute.restype = i32
+        L.oracle_decode_brute.argtypes = [i32, i32, i32, i32, i64, P, P, i32, i32, P, i32, P,
+                                          P, P, f64, P]
+        L.oracle_bf16_decode.restype = i32
+        L.oracle_bf16_decode.argtypes = [i32, i32, i32, i64, P, P, i32, i32, P, i32, P, f64,
+                                         P, i32, P]
+        L.oracle_bf16_append.restype = i32
+        L.oracle_bf16_append.argtypes = [i32, i32, i32, i64, P, P, P, P, i32]
+        L.oracle_f32_to_f16_rne.restype = ctypes.c_uint16
+        L.oracle_f32_to_f16_rne.argtypes = [f32]
+        L.oracle_f16_to_f32.restype = f32
+        L.oracle_f16_to_f32.argtypes = [ctypes.c_uint16]
+        L.oracle_bf16_to_f32.restype = f32
+        L.oracle_bf16_to_f32.argtypes = [ctypes.c_uint16]
+        L.oracle_num_threads.restype = i32
+        _lib = L
+    return _lib
+
+
+def _ptr(a: np.ndarray):
+    assert a.flags["C_CONTIGUOUS"], "oracle inputs must be C-contiguous"
+    return a.ctypes.data_as(ctypes.c_void_p)
+
+
+def _c(a, dtype):
+    return np.ascontiguousarray(a, dtype=dtype)
+
+
+def num_threads() -> int:
+    return int(lib().oracle_num_threads())
+
+
+def page_head_bytes(d: int, P: int, G: int) -> int:
+    return int(lib().oracle_page_head_bytes(d, P, G))
+
+
+def f32_to_f16_bits(x: float) -> int:
+    return int(lib().oracle_f32_to_f16_rne(float(x)))
+
+
+def f16_bits_to_f32(h: int) -> float:
+    return float(lib().oracle_f16_to_f32(int(h)))
+
+
+def rotate_row(x: np.ndarray, R: np.ndarray) -> np.ndarray:
+    """x~ = x R (fp64 accumulation, one rounding to fp32)."""
+    x = _c(x, np.float32)
+    R = _c(R, np.float32)
+    d = x.shape[0]
+    out = np.empty(d, np.float32)
+    lib().oracle_rotate_row(_ptr(x), _ptr(R), d, _ptr(out))
+    return out
+
+
+def quantize_row(xt: np.ndarray, G: int, rho: float):
+    """Clip + asymmetric INT2 of one rotated row -> (codes[d], s16[d/G], z16[d/G], n_sat)."""
+    xt = _c(xt, np.float32)
+    d = xt.shape[0]
+    codes = np.zeros(d, np.uint8)
+    s16 = np.zeros(d // G, np.uint16)
+    z16 = np.zeros(d // G, np.uint16)
+    sat = lib().oracle_quantize_row(_ptr(xt), d, G, float(rho), _ptr(codes), _ptr(s16), _ptr(z16))
+    return codes, s16, z16, int(sat)
+
+
+def kv_append(pages: np.ndarray, *, d: int, Hkv: int, P: int, G: int, k: np.ndarray,
+              v: np.ndarray, slot_mapping: np.ndarray, Rk: np.ndarray, Rv: np.ndarray,
+              clip_k: float, clip_v: float) -> int:
+    """Quantize rows into ``pages`` (uint8, modified in place).  Returns the
+    number of saturated fp16 stores."""
+    assert pages.dtype == np.uint8 and pages.flags["C_CONTIGUOUS"]
+    k = _c(k, np.uint16)
+    v = _c(v, np.uint16)
+    slots = _c(slot_mapping, np.int64)
+    n_tok = slots.shape[0]
+    assert k.size == n_tok * Hkv * d and v.size == n_tok * Hkv * d
+    num_pages = pages.size // (Hkv * page_head_bytes(d, P, G))
+    rc = lib().oracle_kv_append(d, Hkv, P, G, num_pages, _ptr(pages), _ptr(k), _ptr(v),
+                                _ptr(slots), n_tok, _ptr(_c(Rk, np.float32)),
+                                _ptr(_c(Rv, np.float32)), float(clip_k), float(clip_v))
+    if rc < 0:
+        raise ValueError("oracle kv_append: slot outside the page pool")
+    return int(rc)
+
+
+def read_token(pages: np.ndarray, *, d: int, Hkv: int, P: int, G: int, page: int, h: int,
+               t: int, is_v: bool):
+    codes = np.zeros(d, np.uint8)
+    s16 = np.zeros(d // G, np.uint16)
+    z16 = np.zeros(d // G, np.uint16)
+    lib().oracle_read_token(d, Hkv, P, G, _ptr(pages), page, h, t, int(is_v), _ptr(codes),
+                            _ptr(s16), _ptr(z16))
+    return codes, s16, z16
+
+
+def decode(pages: np.ndarray, *, d: int, Hkv: int, P: int, G: int, q: np.ndarray,
+           block_table: np.ndarray, seq_lens: np.ndarray, Rk: np.ndarray, Rv: np.ndarray,
+           sm_scale: float, pairs=None) -> np.ndarray:
+    """fp64 decode attention.  q: bf16 bits [B, Hq, d].  Returns [B, Hq, d], or
+    [n_pairs, d] when ``pairs`` (an [n, 2] array of (b, h)) is given."""
+    q = _c(q, np.uint16)
+    B, Hq = q.shape[0], q.shape[1]
+    bt = _c(block_table, np.int32)
+    sl = _c(seq_lens, np.int32)
+    num_pages = pages.size // (Hkv * page_head_bytes(d, P, G))
+    if pairs is None:
+        out = np.zeros((B, Hq, d), np.float64)
+        pp, n = None, 0
+    else:
+        pr = _c(pairs, np.int32).reshape(-1, 2)
+        out = np.zeros((pr.shape[0], d), np.float64)
+        pp, n = _ptr(pr), pr.shape[0]
+    rc = lib().oracle_decode(d, Hkv, P, G, num_pages, _ptr(pages), _ptr(q), B, Hq, _ptr(bt),
+                             bt.shape[1], _ptr(sl), _ptr(_c(Rk, np.float32)),
+                             _ptr(_c(Rv, np.float32)), float(sm_scale), pp, n, _ptr(out))
+    if rc:
+        raise ValueError("oracle decode: bad page id, length or head")
+    return out
+
+
+def decode_brute(pages: np.ndarray, *, d: int, Hkv: int, P: int, G: int, q: np.ndarray,
+                 block_table: np.ndarray, seq_lens: np.ndarray, Rk: np.ndarray,
+                 Rv: np.ndarray, sm_scale: float) -> np.ndarray:
+    q = _c(q, np.uint16)
+    B, Hq = q.shape[0], q.shape[1]
+    bt = _c(block_table, np.int32)
+    sl = _c(seq_lens, np.int32)
+    num_pages = pages.size // (Hkv * page_head_bytes(d, P, G))
+    out = np.zeros((B, Hq, d), np.float64)
+    rc = lib().oracle_decode_brute(d, Hkv, P, G, num_pages, _ptr(pages), _ptr(q), B, Hq,
+                                   _ptr(bt), bt.shape[1], _ptr(sl), _ptr(_c(Rk, np.float32)),
+                                   _ptr(_c(Rv, np.float32)), float(sm_scale), _ptr(out))
+    if rc:
+        raise ValueError("oracle decode_brute: bad page id or length")
+    return out
+
+
+def bf16_append(pages: np.ndarray, *, d: int, Hkv: int, P: int, k: np.ndarray, v: np.ndarray,
+                slot_mapping: np.ndarray) -> None:
+    assert pages.dtype == np.uint16 and pages.flags["C_CONTIGUOUS"]
+    slots = _c(slot_mapping, np.int64)
+    num_pages = pages.size // (Hkv * 2 * P * d)
+    rc = lib().oracle_bf16_append(d, Hkv, P, num_pages, _ptr(pages), _ptr(_c(k, np.uint16)),
+                                  _ptr(_c(v, np.uint16)), _ptr(slots), slots.shape[0])
+    if rc:
+        raise ValueError("oracle bf16_append: slot outside the page pool")
+
+
+def bf16_decode(pages: np.ndarray, *, d: int, Hkv: int, P: int, q: np.ndarray,
+                block_table: np.ndarray, seq_lens: np.ndarray, sm_scale: float,
+                pairs=None) -> np.ndarray:
+    q = _c(q, np.uint16)
+    B, Hq = q.shape[0], q.shape[1]
+    bt = _c(block_table, np.int32)
+    sl = _c(seq_lens, np.int32)
+    num_pages = pages.size // (Hkv * 2 * P * d)
+    if pairs is None:
+        out = np.zeros((B, Hq, d), np.float64)
+        pp, n = None, 0
+    else:
+        pr = _c(pairs, np.int32).reshape(-1, 2)
+        out = np.zeros((pr.shape[0], d), np.float64)
+        pp, n = _ptr(pr), pr.shape[0]
+    rc = lib().oracle_bf16_decode(d, Hkv, P, num_pages, _ptr(pages), _ptr(q), B, Hq, _ptr(bt),
+                                  bt.shape[1], _ptr(sl), float(sm_scale), pp, n, _ptr(out))
+    if rc:
+        raise ValueError("oracle bf16_decode: bad page id, length or head")
+    return out

@@ -1,0 +1,501 @@
+/*
+ * OSCAR CPU oracle -- TEST INFRASTRUCTURE ONLY.
+ *
+ * A plain, slow, obviously-correct CPU implementation of what the OSCAR serving
+ * hot path computes (arXiv 2605.17757):
+ *   - the cache update: rotate a bf16 key/value row by a fixed orthogonal matrix,
+ *     clip it, quantize it to asymmetric INT2 per channel group with an fp16
+ *     scale and zero, and pack four 2-bit codes per byte into a page
+ *     (Sec. 4 "KV Cache Update"; App. "Scale Determination and Per-token
+ *     Clipping Details"; Alg. 1 QuantizeAndWrite);
+ *   - decode attention over the packed cache (Alg. 1 DecodeStep; Sec. 2
+ *     attention definition), evaluated in fp64 in the rotated basis, plus a
+ *     brute-force evaluation in the original basis;
+ *   - plain fp64 attention over a bf16 paged cache (the bf16 baseline).
+ *
+ * Only the test suite, the package smoke check and the benchmark's CPU-baseline
+ * leg may load this library.  It shares no code, header or table with the GPU
+ * library; the page byte layout is re-implemented here from its written
+ * definition.
+ *
+ * Build: gcc -O2 -std=c11 -fopenmp -ffp-contract=off -fno-fast-math -shared -fPIC
+ * (no FMA contraction, IEEE single/double arithmetic on SSE2).
+ */
+#include <math.h>
+#include <stdint.h>
+#include <stdlib.h>
+#include <string.h>
+#ifdef _OPENMP
+#include <omp.h>
+#endif
+
+/* ------------------------------------------------------------------------- */
+/* Number formats (IEEE 754 binary16, bfloat16), written from the definitions */
+/* ------------------------------------------------------------------------- */
+
+static float f32_from_bits(uint32_t u) { float f; memcpy(&f, &u, 4); return f; }
+static uint32_t bits_from_f32(float f) { uint32_t u; memcpy(&u, &f, 4); return u; }
+
+/* bfloat16 is the upper half of a binary32: widening is exact. */
+float oracle_bf16_to_f32(uint16_t h) { return f32_from_bits(((uint32_t)h) << 16); }
+
+/* binary16 -> binary32 (exact). */
+float oracle_f16_to_f32(uint16_t h) {
+  uint32_t sign = (uint32_t)(h >> 15) & 1u;
+  int32_t exp = (h >> 10) & 0x1f;
+  uint32_t man = h & 0x3ffu;
+  double v;
+  if (exp == 0x1f) {
+    if (man) return f32_from_bits(0x7fc00000u | (sign << 31));
+    return sign ? -INFINITY : INFINITY;
+  }
+  if (exp == 0) v = ldexp((double)man, -24);                 /* subnormal: man * 2^-24 */
+  else v = ldexp((double)(man | 0x400u), exp - 25);          /* (1.man) * 2^(exp-15) */
+  return (float)(sign ? -v : v);
+}
+
+/* binary32 -> binary16, round to nearest, ties to even.  Values whose rounded
+ * magnitude exceeds the largest finite binary16 become infinity (IEEE). */
+uint16_t oracle_f32_to_f16_rne(float f) {
+  uint32_t u = bits_from_f32(f);
+  uint16_t sign = (uint16_t)((u >> 16) & 0x8000u);
+  double a = fabs((double)f);                  /* exact */
+  if (isnan(f)) return (uint16_t)(sign | 0x7e00u);
+  if (isinf(f)) return (uint16_t)(sign | 0x7c00u);
+  /* Quantum of the binary16 grid at magnitude a: 2^-24 below 2^-14 (subnormal
+   * range), else 2^(floor(log2 a) - 10). */
+  int e;
+  frexp(a, &e);                                /* a = m * 2^e, m in [0.5,1) */
+  int q_exp = (a < ldexp(1.0, -14)) ? -24 : (e - 1) - 10;
+  double q = ldexp(1.0, q_exp);
+  double n = a / q;                            /* exact: power-of-two division */
+  double fl = floor(n);
+  double r = n - fl;                           /* exact */
+  double k = fl;
+  if (r > 0.5 || (r == 0.5 && fmod(fl, 2.0) != 0.0)) k = fl + 1.0;
+  double res = k * q;                          /* exact */
+  if (res > 65504.0) return (uint16_t)(sign | 0x7c00u);
+  if (res == 0.0) return sign;
+  /* Encode res (a multiple of q, representable in binary16). */
+  if (res < ldexp(1.0, -14)) {
+    uint16_t man = (uint16_t)(res / ldexp(1.0, -24));
+    return (uint16_t)(sign | man);
+  }
+  int re;
+  double rm = frexp(res, &re);                 /* res = rm * 2^re, rm in [0.5,1) */
+  int ebias = (re - 1) + 15;
+  uint16_t man = (uint16_t)((rm * 2.0 - 1.0) * 1024.0);
+  return (uint16_t)(sign | (uint16_t)(ebias << 10) | man);
+}
+
+/* Saturating binary16 conversion used for stored scale and zero: finite values
+ * beyond +-65504 are clamped to +-65504 first, then rounded. */
+static uint16_t f16_sat(float f) {
+  if (f > 65504.0f) f = 65504.0f;
+  if (f < -65504.0f) f = -65504.0f;
+  return oracle_f32_to_f16_rne(f);
+}
+
+/* ------------------------------------------------------------------------- */
+/* Page layout (the ABI, re-implemented from its definition)                  */
+/* ------------------------------------------------------------------------- */
+/*
+ * The pool is num_pages pages; each page holds P token slots of Hkv heads.
+ * Page-head block (page p, kv-head h) starts at byte (p*Hkv + h) * B_ph where
+ * B_ph = 2*P*d/4 + 2*(d/G)*P*4.  Inside a block:
+ *   [K codes]  P*d/4 bytes, token-major: byte t*(d/4) + c/4
+ *   [V codes]  P*d/4 bytes, quad-major:  byte (c/4)*P + t
+ *   [K s,z]    (d/G)*P entries of 4 bytes, group-major: entry g*P + t
+ *   [V s,z]    same
+ * A code byte holds channels 4j..4j+3 of one token, channel c in bits 2*(c%4)
+ * (least significant first).  An s,z entry is two little-endian binary16
+ * values: scale, then zero.
+ */
+size_t oracle_page_head_bytes(int d, int P, int G) {
+  return (size_t)2 * P * (d / 4) + (size_t)2 * (d / G) * P * 4;
+}
+
+typedef struct { int d, Hkv, P, G; } geo_t;
+
+static size_t kcode_off(geo_t g, int t, int c) { return (size_t)t * (g.d / 4) + (size_t)(c / 4); }
+static size_t vcode_off(geo_t g, int t, int c) {
+  return (size_t)g.P * (g.d / 4) + (size_t)(c / 4) * g.P + (size_t)t;
+}
+static size_t sz_off(geo_t g, int is_v, int grp, int t) {
+  size_t base = (size_t)2 * g.P * (g.d / 4) + (is_v ? (size_t)(g.d / g.G) * g.P * 4 : 0);
+  return base + ((size_t)grp * g.P + (size_t)t) * 4;
+}
+static uint8_t *block_ptr(geo_t g, uint8_t *pages, int64_t page, int h) {
+  return pages + ((size_t)page * g.Hkv + (size_t)h) * oracle_page_head_bytes(g.d, g.P, g.G);
+}
+
+static void put_code(geo_t g, uint8_t *blk, int is_v, int t, int c, unsigned code) {
+  size_t off = is_v ? vcode_off(g, t, c) : kcode_off(g, t, c);
+  unsigned sh = 2u * (unsigned)(c % 4);
+  blk[off] = (uint8_t)((blk[off] & ~(3u << sh)) | ((code & 3u) << sh));
+}
+static unsigned get_code(geo_t g, const uint8_t *blk, int is_v, int t, int c) {
+  size_t off = is_v ? vcode_off(g, t, c) : kcode_off(g, t, c);
+  return (blk[off] >> (2u * (unsigned)(c % 4))) & 3u;
+}
+static void put_sz(geo_t g, uint8_t *blk, int is_v, int grp, int t, uint16_t s, uint16_t z) {
+  uint8_t *p = blk + sz_off(g, is_v, grp, t);
+  p[0] = (uint8_t)(s & 0xff); p[1] = (uint8_t)(s >> 8);
+  p[2] = (uint8_t)(z & 0xff); p[3] = (uint8_t)(z >> 8);
+}
+static void get_sz(geo_t g, const uint8_t *blk, int is_v, int grp, int t, uint16_t *s, uint16_t *z) {
+  const uint8_t *p = blk + sz_off(g, is_v, grp, t);
+  *s = (uint16_t)(p[0] | (p[1] << 8));
+  *z = (uint16_t)(p[2] | (p[3] << 8));
+}
+
+/* ------------------------------------------------------------------------- */
+/* Cache update                                                               */
+/* ------------------------------------------------------------------------- */
+
+/* Rotation x~ = x R in row-vector convention (Sec. 2; App. scale determination):
+ * x~_j = sum_c x_c R[c][j].  Products of a bf16-exact input and an fp32 matrix
+ * entry are exact in fp64; they are summed in fp64 in ascending c and the sum is
+ * rounded once to fp32. */
+void oracle_rotate_row(const float *x, const float *R, int d, float *out) {
+  for (int j = 0; j < d; ++j) {
+    double acc = 0.0;
+    for (int c = 0; c < d; ++c) acc = acc + (double)x[c] * (double)R[(size_t)c * d + j];
+    out[j] = (float)acc;
+  }
+}
+
+/* Clip and quantize one rotated row (App. scale determination, per token and
+ * per group of G channels):
+ *   tau = rho * max|x~| over the group, y = clip(x~, -tau, tau)
+ *   a = min y, b = max y, s = (b - a)/3, z = -a/s
+ *   code = clip(round(y/s + z), 0, 3)
+ * s and z are stored as binary16 and the codes are computed with the stored
+ * values, so that dequantizing a code and quantizing it again returns it.
+ * A group whose stored scale would be zero gets s = 1, z = -a, codes 0.
+ * A zero point of zero is stored as +0.  Returns the number of saturated binary16 stores. */
+int oracle_quantize_row(const float *xt, int d, int G, float rho,
+                        uint8_t *codes, uint16_t *s_out, uint16_t *z_out) {
+  int sat = 0;
+  for (int grp = 0; grp < d / G; ++grp) {
+    const float *x = xt + grp * G;
+    float m = 0.0f;
+    for (int c = 0; c < G; ++c) { float ax = fabsf(x[c]); if (ax > m) m = ax; }
+    float tau = rho * m;
+    float a = 0.0f, b = 0.0f;
+    for (int c = 0; c < G; ++c) {
+      float y = fminf(fmaxf(x[c], -tau), tau);
+      if (c == 0 || y < a) a = y;
+      if (c == 0 || y > b) b = y;
+    }
+    float s = (b - a) / 3.0f;
+    if (fabsf(s) > 65504.0f) ++sat;
+    uint16_t s16 = f16_sat(s);
+    uint16_t z16;
+    if ((s16 & 0x7fffu) == 0) {
+      s16 = 0x3c00u;                                  /* 1.0 */
+      float na = -a + 0.0f;                           /* +0, never -0 */
+      if (fabsf(na) > 65504.0f) ++sat;
+      z16 = f16_sat(na);
+      for (int c = 0; c < G; ++c) codes[grp * G + c] = 0;
+    } else {
+      float sf = oracle_f16_to_f32(s16);
+      float z = -a / sf;
+      z = z + 0.0f;                                   /* +0, never -0 */
+      if (fabsf(z) > 65504.0f) ++sat;
+      z16 = f16_sat(z);
+      float zf = oracle_f16_to_f32(z16);
+      for (int c = 0; c < G; ++c) {
+        float y = fminf(fmaxf(x[c], -tau), tau);
+        float u = y / sf;
+        u = u + zf;
+        float r = rintf(u);                           /* ties to even */
+        if (r < 0.0f) r = 0.0f;
+        if (r > 3.0f) r = 3.0f;
+        codes[grp * G + c] = (uint8_t)r;
+      }
+    }
+    s_out[grp] = s16;
+    z_out[grp] = z16;
+  }
+  return sat;
+}
+
+/* Quantize n_tok new rows into the paged cache (Alg. 1 QuantizeAndWrite; the
+ * fused cache-write of Sec. 4).  k, v: bf16 [n_tok, Hkv, d]; slot_mapping[i] =
+ * page*P + offset.  Rk, Rv: fp32 [d, d] row-major.  Returns the number of
+ * saturated binary16 stores, or -1 on a slot outside the pool. */
+int64_t oracle_kv_append(int d, int Hkv, int P, int G, int64_t num_pages, uint8_t *pages,
+                         const uint16_t *k, const uint16_t *v, const int64_t *slot_mapping,
+                         int n_tok, const float *Rk, const float *Rv, float clip_k, float clip_v) {
+  geo_t g = {d, Hkv, P, G};
+  int64_t sat = 0, bad = 0;
+#pragma omp parallel for reduction(+ : sat, bad) schedule(static)
+  for (int i = 0; i < n_tok; ++i) {
+    int64_t slot = slot_mapping[i];
+    if (slot < 0 || slot >= num_pages * (int64_t)P) { bad += 1; continue; }
+    int64_t page = slot / P;
+    int t = (int)(slot % P);
+    float *x = (float *)malloc(sizeof(float) * (size_t)d * 2);
+    float *xt = x + d;
+    uint8_t *codes = (uint8_t *)malloc((size_t)d);
+    uint16_t *s16 = (uint16_t *)malloc(sizeof(uint16_t) * (size_t)(d / G) * 2);
+    uint16_t *z16 = s16 + d / G;
+    for (int h = 0; h < Hkv; ++h) {
+      uint8_t *blk = block_ptr(g, pages, page, h);
+      for (int is_v = 0; is_v < 2; ++is_v) {
+        const uint16_t *src = (is_v ? v : k) + ((size_t)i * Hkv + (size_t)h) * d;
+        for (int c = 0; c < d; ++c) x[c] = oracle_bf16_to_f32(src[c]);
+        oracle_rotate_row(x, is_v ? Rv : Rk, d, xt);
+        sat += oracle_quantize_row(xt, d, G, is_v ? clip_v : clip_k, codes, s16, z16);
+        for (int c = 0; c < d; ++c) put_code(g, blk, is_v, t, c, codes[c]);
+        for (int grp = 0; grp < d / G; ++grp) put_sz(g, blk, is_v, grp, t, s16[grp], z16[grp]);
+      }
+    }
+    free(x); free(codes); free(s16);
+  }
+  return bad ? -1 : sat;
+}
+
+/* Read one token's codes and stored s,z back out of the cache (for tests). */
+void oracle_read_token(int d, int Hkv, int P, int G, const uint8_t *pages, int64_t page, int h,
+                       int t, int is_v, uint8_t *codes, uint16_t *s16, uint16_t *z16) {
+  geo_t g = {d, Hkv, P, G};
+  const uint8_t *blk = block_ptr(g, (uint8_t *)pages, page, h);
+  for (int c = 0; c < d; ++c) codes[c] = (uint8_t)get_code(g, blk, is_v, t, c);
+  for (int grp = 0; grp < d / G; ++grp) get_sz(g, blk, is_v, grp, t, &s16[grp], &z16[grp]);
+}
+
+/* Dequantized rotated row Q(x~)_c = s*(code - z) in fp64 (App. scale
+ * determination, dequantization map). */
+static void dequant_rotated(geo_t g, const uint8_t *blk, int is_v, int t, double *out) {
+  for (int grp = 0; grp < g.d / g.G; ++grp) {
+    uint16_t s16, z16;
+    get_sz(g, blk, is_v, grp, t, &s16, &z16);
+    double s = (double)oracle_f16_to_f32(s16), z = (double)oracle_f16_to_f32(z16);
+    for (int c = grp * g.G; c < (grp + 1) * g.G; ++c)
+      out[c] = s * ((double)get_code(g, blk, is_v, t, c) - z);
+  }
+}
+
+/* ------------------------------------------------------------------------- */
+/* Decode attention                                                           */
+/* ------------------------------------------------------------------------- */
+/*
+ * One decode step for B sequences (Alg. 1 DecodeStep; attention of Sec. 2).
+ * Query head h reads KV head h / (Hq/Hkv).  Sequence b attends to its tokens
+ * t < seq_lens[b]; token t lives in page block_table[b*max_pages + t/P] at slot
+ * t % P.  The cached keys and values are K^ = Q(K~) Rk^T and V^ = Q(V~) Rv^T,
+ * and the output is softmax(sm_scale * q K^T) V^.
+ *
+ * oracle_decode evaluates it in the rotated basis, using q K^T = (q Rk) Q(K~)^T
+ * and S V^ = (S Q(V~)) Rv^T, all in fp64.  Output o[pair][d] (fp64) for the
+ * listed (b, h) pairs; pairs == NULL means every (b, h) in order b-major.
+ * Returns 0, or -1 on a page id outside the pool / a bad length.
+ */
+static int decode_pair(geo_t g, const uint8_t *pages, int64_t num_pages, const uint16_t *q,
+                       int Hq, const int32_t *block_table, int max_pages,
+                       const int32_t *seq_lens, const float *Rk, const float *Rv,
+                       double sm_scale, int b, int h, double *o) {
+  int d = g.d, group = Hq / g.Hkv, kvh = h / group;
+  int len = seq_lens[b];
+  if (len < 1 || len > max_pages * g.P) return -1;
+  double *qt = (double *)calloc((size_t)d, sizeof(double));
+  double *ot = (double *)calloc((size_t)d, sizeof(double));
+  double *row = (double *)malloc(sizeof(double) * (size_t)d);
+  double *score = (double *)malloc(sizeof(double) * (size_t)len);
+  int rc = 0;
+  const uint16_t *qr = q + ((size_t)b * Hq + (size_t)h) * d;
+  for (int j = 0; j < d; ++j) {
+    double acc = 0.0;
+    for (int c = 0; c < d; ++c) acc += (double)oracle_bf16_to_f32(qr[c]) * (double)Rk[(size_t)c * d + j];
+    qt[j] = acc;
+  }
+  double m = -INFINITY;
+  for (int t = 0; t < len; ++t) {
+    int32_t page = block_table[(size_t)b * max_pages + t / g.P];
+    if (page < 0 || page >= num_pages) { rc = -1; goto done; }
+    dequant_rotated(g, block_ptr(g, (uint8_t *)pages, page, kvh), 0, t % g.P, row);
+    double acc = 0.0;
+    for (int c = 0; c < d; ++c) acc += qt[c] * row[c];
+    score[t] = sm_scale * acc;
+    if (score[t] > m) m = score[t];
+  }
+  double l = 0.0;
+  for (int t = 0; t < len; ++t) {
+    double p = exp(score[t] - m);
+    l += p;
+    int32_t page = block_table[(size_t)b * max_pages + t / g.P];
+    dequant_rotated(g, block_ptr(g, (uint8_t *)pages, page, kvh), 1, t % g.P, row);
+    for (int c = 0; c < d; ++c) ot[c] += p * row[c];
+  }
+  /* o = (ot / l) Rv^T, i.e. o_j = sum_c ot_c Rv[j][c] / l */
+  for (int j = 0; j < d; ++j) {
+    double acc = 0.0;
+    for (int c = 0; c < d; ++c) acc += ot[c] * (double)Rv[(size_t)j * d + c];
+    o[j] = acc / l;
+  }
+done:
+  free(qt); free(ot); free(row); free(score);
+  return rc;
+}
+
+int oracle_decode(int d, int Hkv, int P, int G, int64_t num_pages, const uint8_t *pages,
+                  const uint16_t *q, int B, int Hq, const int32_t *block_table, int max_pages,
+                  const int32_t *seq_lens, const float *Rk, const float *Rv, double sm_scale,
+                  const int32_t *pairs, int n_pairs, double *out) {
+  geo_t g = {d, Hkv, P, G};
+  if (Hq % Hkv) return -1;
+  int n = pairs ? n_pairs : B * Hq;
+  int bad = 0;
+#pragma omp parallel for reduction(+ : bad) schedule(dynamic, 1)
+  for (int i = 0; i < n; ++i) {
+    int b = pairs ? pairs[2 * i] : i / Hq;
+    int h = pairs ? pairs[2 * i + 1] : i % Hq;
+    if (b < 0 || b >= B || h < 0 || h >= Hq) { bad += 1; continue; }
+    if (decode_pair(g, pages, num_pages, q, Hq, block_table, max_pages, seq_lens, Rk, Rv,
+                    sm_scale, b, h, out + (size_t)i * d))
+      bad += 1;
+  }
+  return bad ? -1 : 0;
+}
+
+/* Brute force in the original basis, following Alg. 1 DecodeStep literally:
+ * dequantize the history, rotate it back (k^ = Q(k~) Rk^T, v^ = Q(v~) Rv^T),
+ * then o = softmax(sm_scale * q k^T) v^.  O(len * d^2) per pair: tiny inputs. */
+int oracle_decode_brute(int d, int Hkv, int P, int G, int64_t num_pages, const uint8_t *pages,
+                        const uint16_t *q, int B, int Hq, const int32_t *block_table,
+                        int max_pages, const int32_t *seq_lens, const float *Rk,
+                        const float *Rv, double sm_scale, double *out) {
+  geo_t g = {d, Hkv, P, G};
+  if (Hq % Hkv) return -1;
+  int group = Hq / Hkv;
+  double *rot = (double *)malloc(sizeof(double) * (size_t)d);
+  double *khat = (double *)malloc(sizeof(double) * (size_t)d);
+  int rc = 0;
+  for (int b = 0; b < B && !rc; ++b) {
+    int len = seq_lens[b];
+    if (len < 1 || len > max_pages * P) { rc = -1; break; }
+    double *vhat = (double *)malloc(sizeof(double) * (size_t)len * d);
+    double *score = (double *)malloc(sizeof(double) * (size_t)len);
+    for (int h = 0; h < Hq && !rc; ++h) {
+      int kvh = h / group;
+      const uint16_t *qr = q + ((size_t)b * Hq + h) * d;
+      double m = -INFINITY;
+      for (int t = 0; t < len; ++t) {
+        int32_t page = block_table[(size_t)b * max_pages + t / P];
+        if (page < 0 || page >= num_pages) { rc = -1; break; }
+        const uint8_t *blk = block_ptr(g, (uint8_t *)pages, page, kvh);
+        dequant_rotated(g, blk, 0, t % P, rot);
+        for (int j = 0; j < d; ++j) {          /* k^_j = sum_c Q(k~)_c Rk[j][c] */
+          double acc = 0.0;
+          for (int c = 0; c < d; ++c) acc += rot[c] * (double)Rk[(size_t)j * d + c];
+          khat[j] = acc;
+        }
+        dequant_rotated(g, blk, 1, t % P, rot);
+        for (int j = 0; j < d; ++j) {
+          double acc = 0.0;
+          for (int c = 0; c < d; ++c) acc += rot[c] * (double)Rv[(size_t)j * d + c];
+          vhat[(size_t)t * d + j] = acc;
+        }
+        double s = 0.0;
+        for (int j = 0; j < d; ++j) s += (double)oracle_bf16_to_f32(qr[j]) * khat[j];
+        score[t] = sm_scale * s;
+        if (score[t] > m) m = score[t];
+      }
+      if (rc) break;
+      double l = 0.0;
+      double *o = out + ((size_t)b * Hq + h) * d;
+      for (int j = 0; j < d; ++j) o[j] = 0.0;
+      for (int t = 0; t < len; ++t) {
+        double p = exp(score[t] - m);
+        l += p;
+        for (int j = 0; j < d; ++j) o[j] += p * vhat[(size_t)t * d + j];
+      }
+      for (int j = 0; j < d; ++j) o[j] /= l;
+    }
+    free(vhat); free(score);
+  }
+  free(rot); free(khat);
+  return rc;
+}
+
+/* ------------------------------------------------------------------------- */
+/* bf16 baseline: plain attention over a bf16 paged cache                     */
+/* ------------------------------------------------------------------------- */
+/* bf16 page-head block (page p, kv-head h) at element (p*Hkv + h) * 2*P*d:
+ * [K: P x d bf16, token-major][V: P x d bf16, token-major]. */
+int oracle_bf16_decode(int d, int Hkv, int P, int64_t num_pages, const uint16_t *pages,
+                       const uint16_t *q, int B, int Hq, const int32_t *block_table,
+                       int max_pages, const int32_t *seq_lens, double sm_scale,
+                       const int32_t *pairs, int n_pairs, double *out) {
+  if (Hq % Hkv) return -1;
+  int group = Hq / Hkv;
+  int n = pairs ? n_pairs : B * Hq;
+  int bad = 0;
+#pragma omp parallel for reduction(+ : bad) schedule(dynamic, 1)
+  for (int i = 0; i < n; ++i) {
+    int b = pairs ? pairs[2 * i] : i / Hq;
+    int h = pairs ? pairs[2 * i + 1] : i % Hq;
+    int len = (b >= 0 && b < B) ? seq_lens[b] : 0;
+    if (h < 0 || h >= Hq || len < 1 || len > max_pages * P) { bad += 1; continue; }
+    int kvh = h / group;
+    const uint16_t *qr = q + ((size_t)b * Hq + h) * d;
+    double *score = (double *)malloc(sizeof(double) * (size_t)len);
+    double *o = out + (size_t)i * d;
+    double m = -INFINITY;
+    int ok = 1;
+    for (int t = 0; t < len && ok; ++t) {
+      int32_t page = block_table[(size_t)b * max_pages + t / P];
+      if (page < 0 || page >= num_pages) { ok = 0; break; }
+      const uint16_t *kr = pages + (((size_t)page * Hkv + kvh) * 2 * P + (size_t)(t % P)) * d;
+      double s = 0.0;
+      for (int c = 0; c < d; ++c) s += (double)oracle_bf16_to_f32(qr[c]) * (double)oracle_bf16_to_f32(kr[c]);
+      score[t] = sm_scale * s;
+      if (score[t] > m) m = score[t];
+    }
+    if (ok) {
+      double l = 0.0;
+      for (int j = 0; j < d; ++j) o[j] = 0.0;
+      for (int t = 0; t < len; ++t) {
+        int32_t page = block_table[(size_t)b * max_pages + t / P];
+        const uint16_t *vr = pages + (((size_t)page * Hkv + kvh) * 2 * P + P + (size_t)(t % P)) * d;
+        double p = exp(score[t] - m);
+        l += p;
+        for (int j = 0; j < d; ++j) o[j] += p * (double)oracle_bf16_to_f32(vr[j]);
+      }
+      for (int j = 0; j < d; ++j) o[j] /= l;
+    } else {
+      bad += 1;
+    }
+    free(score);
+  }
+  return bad ? -1 : 0;
+}
+
+/* Write bf16 rows into the bf16 paged cache (plain copy at slot_mapping). */
+int oracle_bf16_append(int d, int Hkv, int P, int64_t num_pages, uint16_t *pages,
+                       const uint16_t *k, const uint16_t *v, const int64_t *slot_mapping,
+                       int n_tok) {
+  for (int i = 0; i < n_tok; ++i) {
+    int64_t slot = slot_mapping[i];
+    if (slot < 0 || slot >= num_pages * (int64_t)P) return -1;
+    int64_t page = slot / P;
+    int t = (int)(slot % P);
+    for (int h = 0; h < Hkv; ++h) {
+      uint16_t *kd = pages + (((size_t)page * Hkv + h) * 2 * P + (size_t)t) * d;
+      uint16_t *vd = pages + (((size_t)page * Hkv + h) * 2 * P + P + (size_t)t) * d;
+      memcpy(kd, k + ((size_t)i * Hkv + h) * d, sizeof(uint16_t) * (size_t)d);
+      memcpy(vd, v + ((size_t)i * Hkv + h) * d, sizeof(uint16_t) * (size_t)d);
+    }
+  }
+  return 0;
+}
+
+int oracle_num_threads(void) {
+#ifdef _OPENMP
+  return omp_get_max_threads();
+#else
+  return 1;
+#endif
+}

@@ -1,0 +1,517 @@
+"""Pins of the CPU oracle against what the paper and the mathematics fix.
+
+Each test checks the oracle against something other than itself: values the
+paper prints (the appendix worked example), closed forms, exact special cases
+that reduce to plain attention, an independent library (numpy) for the number
+formats, and invariants (orthogonality, round trips, page-order invariance).
+A plausible mistake in the oracle -- a dropped term, a wrong sign, a transposed
+rotation, a wrong byte offset or bit position, a wrong GQA head map -- fails at
+least one of them.
+"""
+import math
+import os
+
+import numpy as np
+import pytest
+
+import oracle
+import workloads as W
+
+GOLDEN = os.path.join(os.path.dirname(__file__), "golden", "worked_example_layer10_token5.txt")
+
+
+def _golden():
+    rows = {}
+    for line in open(GOLDEN):
+        if line.startswith("#") or not line.strip():
+            continue
+        name, *vals = line.split()
+        rows[name] = np.array([float(v) for v in vals], np.float64)
+    return rows
+
+
+# ---------------------------------------------------------------------------
+# Number formats: pinned to numpy's independent binary16 implementation
+# ---------------------------------------------------------------------------
+
+def test_f16_to_f32_all_codes_match_numpy():
+    codes = np.arange(65536, dtype=np.uint16)
+    ref = codes.view(np.float16).astype(np.float32)
+    got = np.array([oracle.f16_bits_to_f32(int(c)) for c in codes], np.float32)
+    finite = np.isfinite(ref)
+    assert np.array_equal(got[finite].view(np.uint32), ref[finite].view(np.uint32))
+    assert np.array_equal(np.isnan(got), np.isnan(ref))
+    assert np.array_equal(got[np.isinf(ref)], ref[np.isinf(ref)])
+
+
+def test_f32_to_f16_rne_matches_numpy_incl_ties_subnormals_overflow():
+    rng = np.random.default_rng(1)
+    vals = [0.0, -0.0, 65504.0, 65519.99, 65520.0, -65520.0, 1e6, 2.0 ** -24, 2.0 ** -25,
+            3 * 2.0 ** -26, 2.0 ** -14, 2.0 ** -14 - 2.0 ** -25, 1.0 + 2.0 ** -11,
+            1.0 + 3 * 2.0 ** -11, 2049.0, 2051.0, 1e-8, 6e-8]
+    # exact ties between adjacent binary16 values, normal and subnormal
+    h = rng.integers(0, 0x7bff, size=4000).astype(np.uint16)
+    lo = h.view(np.float16).astype(np.float64)
+    hi = (h + 1).view(np.float16).astype(np.float64)
+    ties = ((lo + hi) / 2).astype(np.float32)
+    rnd = (rng.standard_normal(20000) * 10.0 ** rng.uniform(-9, 5, 20000)).astype(np.float32)
+    x = np.concatenate([np.array(vals, np.float32), ties, -ties, rnd])
+    with np.errstate(over="ignore"):
+        ref = x.astype(np.float16).view(np.uint16)
+    got = np.array([oracle.f32_to_f16_bits(float(v)) for v in x], np.uint16)
+    assert np.array_equal(got, ref)
+
+
+def test_input_bf16_rounding_matches_torch():
+    import torch
+    x = (np.random.default_rng(2).standard_normal(50000) * 30).astype(np.float32)
+    ref = torch.from_numpy(x).to(torch.bfloat16).view(torch.int16).numpy().view(np.uint16)
+    assert np.array_equal(W.f32_to_bf16_bits(x), ref)
+
+
+# ---------------------------------------------------------------------------
+# Rotation: the paper's worked example and the row-vector convention
+# ---------------------------------------------------------------------------
+
+# Inputs are printed to 2 decimals (error <= 0.005 each).  For an orthonormal
+# mixing matrix with entries +-1/sqrt(128) the induced output error is a sum of
+# 128 independent terms of std 0.005/sqrt(3)/sqrt(128) -> std 0.0029; over 128
+# outputs the max is ~3.3 std ~= 0.0095, plus 0.005 output print rounding.
+PRINT_TOL = 0.02
+
+
+def test_worked_example_hadamard_step():
+    g = _golden()
+    H = W.sylvester_hadamard(128).astype(np.float32)
+    out = oracle.rotate_row(g["step1_k_uq"], H)
+    assert np.max(np.abs(out - g["step2_k_uq_h"])) <= PRINT_TOL
+    out2 = oracle.rotate_row(g["raw_k"], H)
+    assert np.max(np.abs(out2 - g["pure_hadamard_k_h"])) <= PRINT_TOL
+
+
+def test_worked_example_bit_reversal_step_is_exact():
+    g = _golden()
+    Pbr = W.bit_reversal_matrix(128).astype(np.float32)
+    out = oracle.rotate_row(g["step2_k_uq_h"].astype(np.float32), Pbr)
+    assert np.array_equal(out, g["step3_k_uq_h_pbr"].astype(np.float32))
+    # bit-reversal placement printed in the paper: top-1..8 -> 0,64,32,96,16,80,48,112
+    placed = [int(np.argmax(Pbr[k])) for k in range(8)]
+    assert placed == [0, 64, 32, 96, 16, 80, 48, 112]
+
+
+def test_rotation_row_vector_convention_with_nonsymmetric_permutation():
+    # R[c][(c+1) % d] = -1**c: x~ = x R gives x~_j = (-1)^(j-1) x_{j-1}.
+    d = 128
+    R = np.zeros((d, d), np.float32)
+    for c in range(d):
+        R[c, (c + 1) % d] = -1.0 if c % 2 else 1.0
+    x = np.arange(1, d + 1, dtype=np.float32)
+    out = oracle.rotate_row(x, R)
+    expect = np.array([x[(j - 1) % d] * (-1.0 if (j - 1) % 2 else 1.0) for j in range(d)],
+                      np.float32)
+    assert np.array_equal(out, expect)
+
+
+def test_rotation_preserves_norm_and_generated_R_is_orthogonal():
+    for seed in (11, 12, 13):
+        for compose in (False, True):
+            R = W.rotation(seed, compose=compose)
+            assert np.max(np.abs(R.T.astype(np.float64) @ R - np.eye(128))) <= 1e-6
+    g = _golden()
+    R = W.rotation(5)
+    out = oracle.rotate_row(g["raw_k"], R).astype(np.float64)
+    assert abs(np.linalg.norm(out) - np.linalg.norm(g["raw_k"])) <= 1e-4
+    # the paper's five printed vectors all have norm 38.13 +- 0.01
+    for name in g:
+        assert abs(np.linalg.norm(g[name]) - 38.13) <= 0.01
+
+
+def test_lemma1_hadamard_equalizes_diagonal():
+    # (H^T Lambda H)_ii = tr(Lambda)/d for any diagonal Lambda (Lemma 1).
+    H = W.sylvester_hadamard(128)
+    lam = np.diag(W.paper_like_spectrum())
+    dg = np.diag(H.T @ lam @ H)
+    assert np.max(np.abs(dg - np.trace(lam) / 128)) <= 1e-12
+
+
+# ---------------------------------------------------------------------------
+# Quantizer: the worked example's group ranges and closed-form properties
+# ---------------------------------------------------------------------------
+
+def _f16(bits):
+    return float(np.uint16(bits).view(np.float16))
+
+
+@pytest.mark.parametrize("name,ranges", [
+    ("raw_k", (44.81, 7.19)), ("step1_k_uq", (7.16, 37.85)), ("step2_k_uq_h", (13.52, 13.58)),
+    ("step3_k_uq_h_pbr", (13.82, 9.36)), ("pure_hadamard_k_h", (13.12, 14.01))])
+def test_worked_example_group_ranges(name, ranges):
+    # G_K = 64, no clipping: the stored scale is (max - min)/3 per group.
+    x = _golden()[name].astype(np.float32)
+    codes, s16, z16, sat = oracle.quantize_row(x, 64, 1.0)
+    assert sat == 0
+    for grp, printed in enumerate(ranges):
+        s = _f16(s16[grp])
+        # caption printed to 2 decimals (+-0.005), entries printed to 2 decimals
+        # (range +-0.01), stored scale rounded to binary16 (3 * half ulp)
+        half_ulp = 2.0 ** (math.floor(math.log2(s)) - 11)
+        assert abs(3 * s - printed) <= 0.015 + 3 * half_ulp + 1e-6
+        # the group minimum is recovered as -z*s
+        gx = x[grp * 64:(grp + 1) * 64]
+        a = -_f16(z16[grp]) * s
+        assert abs(a - gx.min()) <= 0.02
+    # argmin -> code 0, argmax -> code 3 (channels 50 and 42 of the raw token are
+    # the printed outliers -30.62 and 14.19)
+    if name == "raw_k":
+        assert codes[50] == 0 and codes[42] == 3
+
+
+def _bits(t):
+    """uint16 view of a bf16 torch tensor."""
+    import torch
+    return t.contiguous().view(torch.int16).numpy().view(np.uint16)
+
+
+def _rand_rows(n, seed, scale=3.0):
+    rng = np.random.default_rng(seed)
+    return (rng.standard_normal((n, 128)) * scale).astype(np.float32)
+
+
+@pytest.mark.parametrize("rho", [1.0, 0.9, 0.5])
+def test_quantizer_invariants(rho):
+    rows = _rand_rows(300, 7)
+    rows[:, 5] *= 40.0                               # an outlier channel
+    for x in rows:
+        codes, s16, z16, sat = oracle.quantize_row(x, 32, rho)
+        assert sat == 0 and codes.max() <= 3
+        for grp in range(4):
+            gx = x[grp * 32:(grp + 1) * 32]
+            gc = codes[grp * 32:(grp + 1) * 32]
+            s, z = _f16(s16[grp]), _f16(z16[grp])
+            tau = np.float32(rho) * np.float32(np.abs(gx).max())
+            y = np.clip(gx, -tau, tau)
+            # nondegenerate group: the minimum maps to 0, the maximum to 3
+            assert gc[np.argmin(y)] == 0 and gc[np.argmax(y)] == 3
+            # round trip: quantizing a dequantized code returns the code
+            for c in range(4):
+                deq = np.float32(s) * (np.float32(c) - np.float32(z))
+                u = np.float32(np.float32(deq / np.float32(s)) + np.float32(z))
+                assert int(np.clip(np.rint(u), 0, 3)) == c
+            # reconstruction error of clipped values is at most half a step,
+            # allowing for the binary16 rounding of s and z
+            deq = s * (gc.astype(np.float64) - z)
+            slack = 0.5 * s + 4 * abs(s) * 2.0 ** -11 * (3 + abs(z))
+            assert np.max(np.abs(deq - y)) <= slack
+            # clipping bound
+            assert np.all(np.abs(y) <= tau)
+            if rho == 1.0:
+                assert abs(-z * s - gx.min()) <= 4 * s * 2.0 ** -11 * (1 + abs(z))
+
+
+def test_quantizer_degenerate_groups():
+    x = np.zeros(128, np.float32)
+    x[32:64] = 2.5                                    # constant group
+    x[64:96] = -1.25
+    codes, s16, z16, sat = oracle.quantize_row(x, 32, 0.9)
+    assert list(s16) == [0x3C00] * 4                  # s = 1
+    # z = -a, stored +0 for a zero group; clipped constant group a = 0.9*2.5
+    assert z16[0] == 0x0000
+    assert _f16(z16[1]) == np.float16(-np.float32(0.9) * np.float32(2.5))
+    assert _f16(z16[2]) == np.float16(-(np.float32(-0.9) * np.float32(-1.25) * -1))
+    assert np.all(codes == 0)
+    # reconstruction s*(0 - z) = a
+    assert _f16(s16[1]) * (0 - _f16(z16[1])) == pytest.approx(0.9 * 2.5, rel=1e-3)
+
+
+def test_quantizer_saturates_huge_zero_point():
+    # a > 0 with a tiny range: z = -a/s is far outside binary16 -> saturated
+    x = np.full(128, 1000.0, np.float32)
+    x[:32] = np.float32(1000.0) + np.arange(32, dtype=np.float32) * np.float32(2.0 ** -10)
+    codes, s16, z16, sat = oracle.quantize_row(x, 32, 1.0)
+    assert sat >= 1 and _f16(z16[0]) == -65504.0
+
+
+# ---------------------------------------------------------------------------
+# Page layout: hand-computed bytes from the written layout definition
+# ---------------------------------------------------------------------------
+
+def test_append_bytes_at_hand_computed_offsets():
+    d, Hkv, P, G = 128, 2, 64, 32
+    bph = oracle.page_head_bytes(d, P, G)
+    assert bph == 2 * 64 * 32 + 2 * 4 * 64 * 4 == 6144
+    num_pages = 3
+    pages = np.full(num_pages * Hkv * bph, 0x5A, np.uint8)
+    eye = np.eye(d, dtype=np.float32)
+    # K row: group 0 = 0,1,2,3,0,1,2,3,... (a=0,b=3 -> s=1, z=0, codes = values)
+    k_row = np.zeros(d, np.float32)
+    k_row[:32] = np.tile([0, 1, 2, 3], 8)
+    # V row: group 1 = -1.5,-0.5,0.5,1.5 repeated (s=1, z=1.5, codes 0..3)
+    v_row = np.zeros(d, np.float32)
+    v_row[32:64] = np.tile([-1.5, -0.5, 0.5, 1.5], 8)
+    k = np.zeros((1, Hkv, d), np.uint16)
+    v = np.zeros((1, Hkv, d), np.uint16)
+    k[0, 1] = W.f32_to_bf16_bits(k_row)
+    v[0, 1] = W.f32_to_bf16_bits(v_row)
+    slot = np.array([1 * P + 5], np.int64)            # page 1, token 5
+    oracle.kv_append(pages, d=d, Hkv=Hkv, P=P, G=G, k=k, v=v, slot_mapping=slot, Rk=eye,
+                     Rv=eye, clip_k=1.0, clip_v=1.0)
+    base = (1 * Hkv + 1) * bph                        # page 1, kv-head 1
+    t = 5
+    # K codes token-major: bytes t*32 + j; channels 0..3 = codes 0,1,2,3 -> 0xE4
+    assert list(pages[base + t * 32: base + t * 32 + 8]) == [0xE4] * 8
+    assert list(pages[base + t * 32 + 8: base + t * 32 + 32]) == [0] * 24
+    # V codes quad-major: byte 2048 + j*64 + t; group 1 = quads 8..15 -> 0xE4
+    vb = [pages[base + 2048 + j * 64 + t] for j in range(32)]
+    assert vb[8:16] == [0xE4] * 8 and vb[:8] == [0] * 8 and vb[16:] == [0] * 16
+    # K s,z group-major: entry (g*64 + t)*4 at 4096; group 0: s=1.0 (0x3C00), z=+0
+    e = base + 4096 + (0 * 64 + t) * 4
+    assert list(pages[e:e + 4]) == [0x00, 0x3C, 0x00, 0x00]
+    # zero groups are degenerate: s = 1, z = +0
+    e = base + 4096 + (1 * 64 + t) * 4
+    assert list(pages[e:e + 4]) == [0x00, 0x3C, 0x00, 0x00]
+    # V s,z at 4096 + 1024; group 1: s = 1.0, z = 1.5 (0x3E00)
+    e = base + 5120 + (1 * 64 + t) * 4
+    assert list(pages[e:e + 4]) == [0x00, 0x3C, 0x00, 0x3E]
+    # kv-head 0 got an all-zero row: codes 0, every group degenerate (s=1, z=+0)
+    base0 = (1 * Hkv + 0) * bph
+    assert list(pages[base0 + t * 32: base0 + t * 32 + 32]) == [0] * 32
+    assert [pages[base0 + 2048 + j * 64 + t] for j in range(32)] == [0] * 32
+    for gg in range(4):
+        for off in (4096, 5120):
+            e = base0 + off + (gg * 64 + t) * 4
+            assert list(pages[e:e + 4]) == [0x00, 0x3C, 0x00, 0x00]
+    # nothing else in the pool was touched
+    touched = np.zeros(pages.size, bool)
+    for bb in (base, base0):
+        touched[bb + t * 32: bb + t * 32 + 32] = True
+        for j in range(32):
+            touched[bb + 2048 + j * 64 + t] = True
+        for gg in range(4):
+            for off in (4096, 5120):
+                e = bb + off + (gg * 64 + t) * 4
+                touched[e:e + 4] = True
+    assert np.all(pages[~touched] == 0x5A)
+
+
+def test_append_order_independent_and_readback():
+    cfg = W.config(0)
+    Rk, Rv = W.rotations(cfg)
+    k, v = W.cache_kv(cfg, 0)
+    kb = _bits(k)
+    vb = _bits(v)
+    table, num_pages = W.block_table(cfg)
+    slots = W.slots_for(table, 0, np.arange(256))
+    bph = oracle.page_head_bytes(128, 64, 32)
+    a = np.zeros(num_pages * bph, np.uint8)
+    b = np.zeros(num_pages * bph, np.uint8)
+    kw = dict(d=128, Hkv=1, P=64, G=32, Rk=Rk, Rv=Rv, clip_k=0.9, clip_v=0.9)
+    oracle.kv_append(a, k=kb, v=vb, slot_mapping=slots, **kw)
+    perm = np.random.default_rng(3).permutation(256)
+    oracle.kv_append(b, k=kb[perm], v=vb[perm], slot_mapping=slots[perm], **kw)
+    assert np.array_equal(a, b)
+    # read back one token and compare with quantizing its rotated row directly
+    t = 77
+    page = int(table[0, t // 64])
+    codes, s16, z16 = oracle.read_token(a, d=128, Hkv=1, P=64, G=32, page=page, h=0, t=t % 64,
+                                        is_v=False)
+    xt = oracle.rotate_row(W.bf16_bits_to_f32(kb[t, 0]), Rk)
+    c2, s2, z2, _ = oracle.quantize_row(xt, 32, 0.9)
+    assert np.array_equal(codes, c2) and np.array_equal(s16, s2) and np.array_equal(z16, z2)
+
+
+# ---------------------------------------------------------------------------
+# Decode: exact special cases, brute force, invariances
+# ---------------------------------------------------------------------------
+
+def _signed_cyclic(d, shift, seed):
+    signs = np.random.default_rng(seed).choice([-1.0, 1.0], size=d)
+    R = np.zeros((d, d), np.float32)
+    for c in range(d):
+        R[c, (c + shift) % d] = signs[c]
+    return R
+
+
+def _exact_rows(n, seed, d=128):
+    """Rotated-basis rows whose every 32-group is exactly representable by the
+    INT2 quantizer with rho=1: values a + k*s, k in 0..3, min and max present,
+    s and a dyadic so that s, z = -a/s and s*(k - z) are exact."""
+    rng = np.random.default_rng(seed)
+    out = np.zeros((n, d), np.float32)
+    for i in range(n):
+        for g in range(d // 32):
+            s = 2.0 ** int(rng.integers(-2, 2))
+            a = s * float(rng.integers(-3, 1))
+            ks = rng.integers(0, 4, size=32)
+            ks[rng.permutation(32)[:2]] = [0, 3]
+            out[i, g * 32:(g + 1) * 32] = a + s * ks
+    return out
+
+
+def _build_exact_cache(B, Hq, Hkv, lens, seed):
+    """Keys/values that the INT2 cache stores exactly (with signed-permutation
+    rotations), so decode must equal plain softmax attention on them."""
+    d, P, G = 128, 64, 32
+    Rk = _signed_cyclic(d, 5, seed)
+    Rv = _signed_cyclic(d, 11, seed + 1)
+    mp = int(math.ceil(max(lens) / P)) + 1
+    num_pages = B * mp
+    table = np.random.default_rng(seed).permutation(num_pages).astype(np.int32).reshape(B, mp)
+    bph = oracle.page_head_bytes(d, P, G)
+    pages = np.zeros(num_pages * Hkv * bph, np.uint8)
+    K = []
+    V = []
+    for b in range(B):
+        n = lens[b]
+        kt = _exact_rows(n * Hkv, seed + 10 + b).reshape(n, Hkv, d)
+        vt = _exact_rows(n * Hkv, seed + 20 + b).reshape(n, Hkv, d)
+        k = kt @ Rk.T                                  # k = k~ Rk^T, exact (signed permutation)
+        v = vt @ Rv.T
+        K.append(k.astype(np.float64))
+        V.append(v.astype(np.float64))
+        slots = W.slots_for(table, b, np.arange(n))
+        oracle.kv_append(pages, d=d, Hkv=Hkv, P=P, G=G, k=W.f32_to_bf16_bits(k),
+                         v=W.f32_to_bf16_bits(v), slot_mapping=slots, Rk=Rk, Rv=Rv, clip_k=1.0,
+                         clip_v=1.0)
+    q = W.f32_to_bf16_bits(np.random.default_rng(seed + 99).standard_normal((B, Hq, d)).astype(
+        np.float32))
+    return pages, table, q, Rk, Rv, K, V
+
+
+def _plain_attention(q, K, V, lens, Hq, Hkv, sm_scale):
+    B = q.shape[0]
+    out = np.zeros((B, Hq, 128))
+    qf = W.bf16_bits_to_f32(q).astype(np.float64)
+    for b in range(B):
+        for h in range(Hq):
+            kvh = h // (Hq // Hkv)
+            s = sm_scale * (K[b][:, kvh, :] @ qf[b, h])
+            p = np.exp(s - s.max())
+            out[b, h] = p @ V[b][:, kvh, :] / p.sum()
+    return out
+
+
+def test_decode_exact_cache_equals_plain_attention_gqa():
+    B, Hq, Hkv = 3, 8, 2
+    lens = [1, 70, 129]
+    pages, table, q, Rk, Rv, K, V = _build_exact_cache(B, Hq, Hkv, lens, 5)
+    kw = dict(d=128, Hkv=Hkv, P=64, G=32, q=q, block_table=table,
+              seq_lens=np.array(lens, np.int32), Rk=Rk, Rv=Rv, sm_scale=1 / math.sqrt(128))
+    got = oracle.decode(pages, **kw)
+    ref = _plain_attention(q, K, V, lens, Hq, Hkv, 1 / math.sqrt(128))
+    assert np.max(np.abs(got - ref)) <= 1e-12
+    # length 1: the output is the single cached value row
+    assert np.max(np.abs(got[0] - V[0][0, np.arange(Hq) // 4, :])) <= 1e-12
+    brute = oracle.decode_brute(pages, **kw)
+    assert np.max(np.abs(brute - ref)) <= 1e-12
+
+
+def test_decode_identical_keys_gives_mean_value():
+    B, Hq, Hkv, n = 1, 4, 1, 100
+    pages, table, q, Rk, Rv, K, V = _build_exact_cache(B, Hq, Hkv, [n], 8)
+    # overwrite every key with the key of token 0 (re-append)
+    k0 = K[0][0:1].repeat(n, axis=0)
+    slots = W.slots_for(table, 0, np.arange(n))
+    d = 128
+    # rebuild with identical keys
+    bph = oracle.page_head_bytes(d, 64, 32)
+    pages2 = np.zeros_like(pages)
+    oracle.kv_append(pages2, d=d, Hkv=1, P=64, G=32, k=W.f32_to_bf16_bits(k0.astype(np.float32)),
+                     v=W.f32_to_bf16_bits(V[0].astype(np.float32)), slot_mapping=slots, Rk=Rk,
+                     Rv=Rv, clip_k=1.0, clip_v=1.0)
+    got = oracle.decode(pages2, d=d, Hkv=1, P=64, G=32, q=q, block_table=table,
+                        seq_lens=np.array([n], np.int32), Rk=Rk, Rv=Rv, sm_scale=0.0884)
+    assert bph > 0
+    assert np.max(np.abs(got[0] - V[0][:, 0, :].mean(axis=0)[None, :])) <= 1e-12
+
+
+def test_decode_brute_force_matches_rotated_basis_on_config0():
+    cfg = W.config(0)
+    Rk, Rv = W.rotations(cfg)
+    k, v = W.cache_kv(cfg, 0)
+    kb, vb = _bits(k), _bits(v)
+    table, num_pages = W.block_table(cfg)
+    pages = np.zeros(num_pages * oracle.page_head_bytes(128, 64, 32), np.uint8)
+    oracle.kv_append(pages, d=128, Hkv=1, P=64, G=32, k=kb, v=vb,
+                     slot_mapping=W.slots_for(table, 0, np.arange(256)), Rk=Rk, Rv=Rv,
+                     clip_k=cfg.clip_k, clip_v=cfg.clip_v)
+    q = _bits(W.queries(cfg))
+    kw = dict(d=128, Hkv=1, P=64, G=32, q=q, block_table=table, seq_lens=cfg.lens, Rk=Rk,
+              Rv=Rv, sm_scale=cfg.sm_scale)
+    a = oracle.decode(pages, **kw)
+    b = oracle.decode_brute(pages, **kw)
+    assert np.max(np.abs(a - b)) <= 1e-12
+
+
+def test_decode_unquantized_rotation_invariance():
+    # With an orthogonal R and a cache that stores the rotated rows exactly,
+    # (q R)(k R)^T = q k^T: generic orthogonal R, exactly-representable rotated
+    # rows, decode equals plain attention on the back-rotated rows.
+    d = 128
+    Rk = W.rotation(21)
+    Rv = W.rotation(22)
+    n = 90
+    kt = _exact_rows(n, 31)
+    vt = _exact_rows(n, 32)
+    # rows k with k Rk == kt exactly are not bf16 in general; instead check the
+    # rotated-basis identity directly: the oracle's decode against brute force
+    # on a cache built from kt via an identity rotation composed into Rk.
+    eye = np.eye(d, dtype=np.float32)
+    table = np.arange(2, dtype=np.int32).reshape(1, 2)
+    pages = np.zeros(2 * oracle.page_head_bytes(d, 64, 32), np.uint8)
+    oracle.kv_append(pages, d=d, Hkv=1, P=64, G=32, k=W.f32_to_bf16_bits(kt),
+                     v=W.f32_to_bf16_bits(vt), slot_mapping=np.arange(n), Rk=eye, Rv=eye,
+                     clip_k=1.0, clip_v=1.0)
+    q = W.f32_to_bf16_bits(np.random.default_rng(4).standard_normal((1, 4, d)).astype(np.float32))
+    # The cache holds kt exactly.  Decoding it with (Rk, Rv) means keys kt Rk^T and
+    # values vt Rv^T; plain attention with those rows must match to fp64 rounding.
+    got = oracle.decode(pages, d=d, Hkv=1, P=64, G=32, q=q, block_table=table,
+                        seq_lens=np.array([n], np.int32), Rk=Rk, Rv=Rv, sm_scale=0.1)
+    Kf = kt.astype(np.float64) @ Rk.astype(np.float64).T
+    Vf = vt.astype(np.float64) @ Rv.astype(np.float64).T
+    ref = _plain_attention(q, [Kf[:, None, :]], [Vf[:, None, :]], [n], 4, 1, 0.1)
+    assert np.max(np.abs(got - ref)) <= 1e-10
+
+
+def test_decode_page_shuffle_invariance():
+    B, Hq, Hkv = 2, 4, 1
+    lens = [200, 130]
+    pages, table, q, Rk, Rv, K, V = _build_exact_cache(B, Hq, Hkv, lens, 13)
+    bph = oracle.page_head_bytes(128, 64, 32)
+    num_pages = table.size
+    perm = np.random.default_rng(0).permutation(num_pages)
+    # move page p to position perm[p]
+    moved = np.zeros_like(pages)
+    for p in range(num_pages):
+        moved[perm[p] * bph:(perm[p] + 1) * bph] = pages[p * bph:(p + 1) * bph]
+    table2 = perm[table].astype(np.int32)
+    kw = dict(d=128, Hkv=Hkv, P=64, G=32, q=q, seq_lens=np.array(lens, np.int32), Rk=Rk, Rv=Rv,
+              sm_scale=0.09)
+    a = oracle.decode(pages, block_table=table, **kw)
+    b = oracle.decode(moved, block_table=table2, **kw)
+    assert np.array_equal(a, b)
+    # pairs selection returns the same rows
+    pairs = np.array([[1, 3], [0, 2]], np.int32)
+    c = oracle.decode(pages, block_table=table, pairs=pairs, **kw)
+    assert np.array_equal(c[0], a[1, 3]) and np.array_equal(c[1], a[0, 2])
+
+
+def test_bf16_decode_equals_plain_attention():
+    rng = np.random.default_rng(6)
+    d, P, Hkv, Hq, B = 128, 64, 2, 6, 2
+    lens = [65, 3]
+    mp = 2
+    table = rng.permutation(B * mp).astype(np.int32).reshape(B, mp)
+    pages = np.zeros(B * mp * Hkv * 2 * P * d, np.uint16)
+    K, V = [], []
+    for b in range(B):
+        k = W.f32_to_bf16_bits(rng.standard_normal((lens[b], Hkv, d)).astype(np.float32))
+        v = W.f32_to_bf16_bits(rng.standard_normal((lens[b], Hkv, d)).astype(np.float32))
+        oracle.bf16_append(pages, d=d, Hkv=Hkv, P=P, k=k, v=v,
+                           slot_mapping=W.slots_for(table, b, np.arange(lens[b])))
+        K.append(W.bf16_bits_to_f32(k).astype(np.float64))
+        V.append(W.bf16_bits_to_f32(v).astype(np.float64))
+    q = W.f32_to_bf16_bits(rng.standard_normal((B, Hq, d)).astype(np.float32))
+    got = oracle.bf16_decode(pages, d=d, Hkv=Hkv, P=P, q=q, block_table=table,
+                             seq_lens=np.array(lens, np.int32), sm_scale=0.088)
+    ref = _plain_attention(q, K, V, lens, Hq, Hkv, 0.088)
+    assert np.max(np.abs(got - ref)) <= 1e-12
