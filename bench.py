@@ -1,0 +1,307 @@
+#!/usr/bin/env python3
+"""Benchmark of the OSCAR INT2 decode path on one MI355X.
+
+One step = one decode step of one attention layer for B sequences:
+  kv_append of each sequence's newest token (rotate, clip, INT2, pack)
+  + decode prepare (q~ = q R_k) + split (paged split-K attention over the INT2
+  cache) + reduce (log-sum-exp merge, o = o~ R_v^T),
+all on one HIP stream with the inputs already resident in HBM.  The default
+workload is the Qwen3-8B-shaped layer: 32 query / 8 KV heads, head dim 128,
+batch 64, per-sequence context lengths uniform in [16384, 32768], page size 64,
+shuffled non-contiguous pages.
+
+Prints one JSON line.  `value` is the step's algorithmic HBM bytes divided by
+the step time (GB/s).  `roofline` is the split kernel (the dominant kernel),
+timed with HIP events on the library's stream inside the timed loop.
+`cpu_baseline` is the CPU oracle timed on a bounded sample of the same
+workload.  `bf16_baseline` is the bf16 paged-decode kernel on the same
+sequences.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = ("INT2 paged decode attn: µs/step, HBM GB/s & % of peak "
+          "(Qwen3-8B shape, 32k ctx)")
+HBM_PEAK_GBS = 8000.0
+INT2_BYTES_PER_TOKEN_HEAD = 96          # 32 B K codes + 32 B V codes + 16 B K (s,z) + 16 B V (s,z)
+BF16_BYTES_PER_TOKEN_HEAD = 512
+
+
+def parse():
+    ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=10)
+    ap.add_argument("--config", type=int, default=2, help="workload index 0..4 (default 2)")
+    ap.add_argument("--batch", type=int, default=None, help="batch override (config 2: 64)")
+    ap.add_argument("--num-splits", type=int, default=0, help="0 = library default")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-bf16-baseline", action="store_true")
+    ap.add_argument("--cpu-seconds", type=float, default=10.0,
+                    help="target CPU time for the oracle baseline sample")
+    return ap.parse_args()
+
+
+def main():
+    args = parse()
+    world = int(os.environ.get("WORLD_SIZE", "1"))
+    if args.gpus != 1 or world != 1:
+        print("bench.py measures one GPU only: this build runs the decode path on a single "
+              "MI355X (no multi-GPU path); run with --gpus 1", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+
+    import paper_2605_17757_amd as ok
+    import workloads as W
+
+    if not torch.cuda.is_available():
+        print("bench.py needs a GPU", file=sys.stderr)
+        sys.exit(1)
+    torch.cuda.set_device(0)
+    dev = "cuda"
+    cfg = W.config(args.config, batch=args.batch if args.batch else (64 if args.config == 2 else None))
+    B, Hq, Hkv, d = cfg.B, cfg.Hq, cfg.Hkv, cfg.d
+    lens = cfg.lens.astype(np.int64)
+    table, num_pages = W.block_table(cfg)
+    lay = ok.Layout(num_kv_heads=Hkv, num_pages=num_pages)
+    Rk_np, Rv_np = W.rotations(cfg)
+    Rk = torch.from_numpy(Rk_np).to(dev)
+    Rv = torch.from_numpy(Rv_np).to(dev)
+    bt = torch.from_numpy(table).to(dev)
+    sl = torch.from_numpy(cfg.lens).to(dev)
+    q = W.queries(cfg, device=dev)
+    S = args.num_splits or ok.default_num_splits(lay, B, Hq, int(table.shape[1]) * 64)
+    if cfg.min_splits and S < cfg.min_splits:
+        S = cfg.min_splits
+
+    # ---- setup (untimed): build the INT2 and bf16 caches from the same rows ----
+    t0 = time.time()
+    pool = ok.alloc_pool(lay)
+    bf_pool = None
+    if not args.no_bf16_baseline:
+        bf_pool = torch.zeros(ok.bf16_pool_bytes(lay) // 2, dtype=torch.bfloat16, device=dev)
+    new_k = torch.empty(B, Hkv, d, dtype=torch.bfloat16, device=dev)
+    new_v = torch.empty_like(new_k)
+    new_slots = np.zeros(B, np.int64)
+    for b in range(B):
+        k, v = W.cache_kv(cfg, b, device=dev)
+        n = int(lens[b])
+        slots = torch.from_numpy(W.slots_for(table, b, np.arange(n))).to(dev)
+        # the cache holds tokens 0 .. n-2; token n-1 is the step's new token
+        ok.kv_append(lay, pool, k[:n - 1], v[:n - 1], slots[:n - 1], Rk, Rv, cfg.clip_k,
+                     cfg.clip_v)
+        if bf_pool is not None:
+            ok.bf16_kv_append(lay, bf_pool, k, v, slots)
+        new_k[b] = k[n - 1]
+        new_v[b] = v[n - 1]
+        new_slots[b] = int(W.slots_for(table, b, [n - 1])[0])
+        del k, v
+    new_slots_t = torch.from_numpy(new_slots).to(dev)
+    ws = ok.alloc_workspace(lay, B, Hq, S)
+    out = torch.empty(B, Hq, d, dtype=torch.bfloat16, device=dev)
+    torch.cuda.synchronize()
+    setup_s = time.time() - t0
+    print("setup %.1fs: %s B=%d Hq=%d Hkv=%d splits=%d mean_len=%.0f" %
+          (setup_s, cfg.name, B, Hq, Hkv, S, lens.mean()), file=sys.stderr, flush=True)
+
+    stream = torch.cuda.current_stream()
+
+    def step(ev=None):
+        if ev: ev[0].record(stream)
+        ok.kv_append(lay, pool, new_k, new_v, new_slots_t, Rk, Rv, cfg.clip_k, cfg.clip_v)
+        if ev: ev[1].record(stream)
+        ok.decode_prepare(lay, q, Rk, cfg.sm_scale, S, ws)
+        if ev: ev[2].record(stream)
+        ok.decode_split(lay, pool, B, Hq, bt, sl, S, ws)
+        if ev: ev[3].record(stream)
+        ok.decode_reduce(lay, B, Hq, Rv, S, ws, out)
+        if ev: ev[4].record(stream)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(5)] for _ in range(args.steps)]
+    torch.cuda.synchronize()
+    w0 = time.perf_counter()
+    for i in range(args.steps):
+        step(evs[i])
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - w0
+    seg = np.array([[evs[i][j].elapsed_time(evs[i][j + 1]) for j in range(4)]
+                    for i in range(args.steps)]) * 1e3               # us
+    step_us = np.array([evs[i][0].elapsed_time(evs[i][4]) for i in range(args.steps)]) * 1e3
+    us_step = wall / args.steps * 1e6
+
+    # ---- algorithmic bytes ----
+    pages_used = int(np.sum((lens + 63) // 64))
+    kv_bytes = int(lens.sum()) * Hkv * INT2_BYTES_PER_TOKEN_HEAD
+    table_bytes = pages_used * 4 + B * 4
+    split_bytes = kv_bytes + table_bytes
+    qo_bytes = 2 * B * Hq * d * 2
+    append_bytes = 2 * B * Hkv * d * 2 + B * Hkv * INT2_BYTES_PER_TOKEN_HEAD + B * 8 + 2 * d * d * 4
+    step_bytes = split_bytes + qo_bytes + append_bytes + 2 * d * d * 4
+    split_us = float(np.mean(seg[:, 2]))
+    achieved = split_bytes / (split_us * 1e-6) / 1e9
+
+    res = {
+        "metric": METRIC,
+        "value": round(step_bytes / (us_step * 1e-6) / 1e9, 1),
+        "unit": "GB/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(us_step / 1e3, 4),
+        "us_per_step": round(us_step, 2),
+        "frac_of_peak": round(step_bytes / (us_step * 1e-6) / 1e9 / HBM_PEAK_GBS, 4),
+        "tokens_per_s": round(B / (us_step * 1e-6), 1),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f32",
+        "data": "synthetic",
+        "config": {
+            "workload": cfg.name, "batch": B, "q_heads": Hq, "kv_heads": Hkv, "head_dim": d,
+            "page_size": 64, "group_size": 32, "clip": cfg.clip_k,
+            "seq_len_mean": float(lens.mean()), "seq_len_min": int(lens.min()),
+            "seq_len_max": int(lens.max()), "num_splits": S, "new_tokens_per_step": B,
+        },
+        "kernels_us": {
+            "kv_append": round(float(np.mean(seg[:, 0])), 2),
+            "decode_prepare": round(float(np.mean(seg[:, 1])), 2),
+            "decode_split": round(split_us, 2),
+            "decode_reduce": round(float(np.mean(seg[:, 3])), 2),
+            "step_events_median": round(float(np.median(step_us)), 2),
+            "step_events_p10": round(float(np.percentile(step_us, 10)), 2),
+            "step_events_p90": round(float(np.percentile(step_us, 90)), 2),
+        },
+        "roofline": {
+            "kernel": "decode_split", "bound": "hbm", "achieved": round(achieved, 1),
+            "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4),
+            "traffic": None, "bytes_per_launch": split_bytes,
+        },
+        "bytes": {"int2_kv": kv_bytes, "block_table": table_bytes, "q_and_out": qo_bytes,
+                  "append": append_bytes, "step_total": step_bytes,
+                  "bf16_kv_equivalent": int(lens.sum()) * Hkv * BF16_BYTES_PER_TOKEN_HEAD},
+    }
+
+    # ---- bf16 paged-decode baseline on the same sequences ----
+    if bf_pool is not None:
+        bf_out = torch.empty_like(out)
+        bws = torch.empty(ok.decode_workspace_bytes(lay, B, Hq, S), dtype=torch.uint8,
+                          device=dev)
+        for _ in range(args.warmup):
+            ok.bf16_decode_attn(lay, bf_pool, q, bt, sl, cfg.sm_scale, S, bws, bf_out)
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        e0.record(stream)
+        for _ in range(args.steps):
+            ok.bf16_decode_attn(lay, bf_pool, q, bt, sl, cfg.sm_scale, S, bws, bf_out)
+        e1.record(stream)
+        torch.cuda.synchronize()
+        bus = e0.elapsed_time(e1) * 1e3 / args.steps
+        bbytes = int(lens.sum()) * Hkv * BF16_BYTES_PER_TOKEN_HEAD + table_bytes + qo_bytes
+        int2_decode_us = float(np.mean(seg[:, 1] + seg[:, 2] + seg[:, 3]))
+        res["bf16_baseline"] = {
+            "us_per_decode": round(bus, 2), "GBps": round(bbytes / (bus * 1e-6) / 1e9, 1),
+            "frac_of_peak": round(bbytes / (bus * 1e-6) / 1e9 / HBM_PEAK_GBS, 4),
+            "int2_decode_us": round(int2_decode_us, 2),
+            "int2_speedup": round(bus / int2_decode_us, 3),
+            "kv_footprint_ratio": round(BF16_BYTES_PER_TOKEN_HEAD / INT2_BYTES_PER_TOKEN_HEAD, 3),
+        }
+        del bf_pool
+
+    # ---- device copy probe (achievable HBM bandwidth) ----
+    src = torch.empty(1 << 30, dtype=torch.uint8, device=dev)
+    dst = torch.empty_like(src)
+    for _ in range(3):
+        dst.copy_(src)
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record(stream)
+    for _ in range(10):
+        dst.copy_(src)
+    e1.record(stream)
+    torch.cuda.synchronize()
+    res["copy_probe_GBps"] = round(2 * src.numel() * 10 / (e0.elapsed_time(e1) * 1e-3) / 1e9, 1)
+    del src, dst
+
+    # ---- CPU oracle baseline on a bounded sample ----
+    if not args.no_cpu_baseline:
+        res["cpu_baseline"] = cpu_baseline(cfg, table, Rk_np, Rv_np, q, args.cpu_seconds)
+
+    print(json.dumps(res), flush=True)
+
+
+def cpu_baseline(cfg, table, Rk_np, Rv_np, q, seconds, max_seqs=4):
+    """The CPU oracle (plain C, fp64, OpenMP over (sequence, head)) decoding whole
+    sequences of the same workload.  The sample is the first `max_seqs`
+    sequences; the oracle builds its own cache for them with its own append
+    (untimed), then decodes them repeatedly until about `seconds` of decode time.
+    Reported in the metric's unit (GB/s of algorithmic INT2 bytes)."""
+    import torch
+
+    import oracle
+    import workloads as W
+
+    def u16(t):
+        return t.detach().contiguous().cpu().view(torch.int16).numpy().view(np.uint16)
+
+    qh = u16(q)
+    Hkv, d = cfg.Hkv, cfg.d
+    bph = oracle.page_head_bytes(d, 64, 32)
+    sample = []
+    for b in range(min(cfg.B, max_seqs)):
+        n = int(cfg.lens[b])
+        k, v = W.cache_kv(cfg, b, device="cuda")
+        kb, vb = u16(k), u16(v)
+        del k, v
+        npg = (n + 63) // 64
+        pool = np.zeros(npg * Hkv * bph, np.uint8)
+        oracle.kv_append(pool, d=d, Hkv=Hkv, P=64, G=32, k=kb, v=vb,
+                         slot_mapping=np.arange(n, dtype=np.int64), Rk=Rk_np, Rv=Rv_np,
+                         clip_k=cfg.clip_k, clip_v=cfg.clip_v)
+        sample.append((b, n, pool, np.arange(npg, dtype=np.int32)[None, :]))
+    spent, nbytes, passes = 0.0, 0, 0
+    while spent < seconds:
+        for b, n, pool, loc in sample:
+            t0 = time.perf_counter()
+            oracle.decode(pool, d=d, Hkv=Hkv, P=64, G=32, q=qh[b:b + 1], block_table=loc,
+                          seq_lens=np.array([n], np.int32), Rk=Rk_np, Rv=Rv_np,
+                          sm_scale=cfg.sm_scale)
+            spent += time.perf_counter() - t0
+            nbytes += n * Hkv * INT2_BYTES_PER_TOKEN_HEAD
+        passes += 1
+    ntok = sum(n for _, n, _, _ in sample)
+    return {
+        "value": round(nbytes / spent / 1e9, 4), "unit": "GB/s",
+        "cores": oracle.num_threads(), "kind": "oracle",
+        "us_per_step_equiv": round(spent / (passes * len(sample)) * cfg.B * 1e6, 1),
+        "sample": "decode of sequences 0-%d (%d tokens, %d q-heads each) of the same "
+                  "workload, %d passes, %.1f s of oracle time" % (len(sample) - 1, ntok, cfg.Hq,
+                                                                  passes, spent),
+        "cpu_model": _cpu_model(),
+    }
+
+
+def _cpu_model():
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,198 @@
+/*
+ * liboscar -- INT2 KV-cache append and paged decode attention for OSCAR
+ * (arXiv 2605.17757) on AMD Instinct MI355X (gfx950).
+ *
+ * The cache stores every key and value row rotated by a fixed orthogonal matrix,
+ * clipped, and quantized to asymmetric 2-bit codes per group of G channels with
+ * a binary16 scale and zero (Sec. 4 "KV Cache Update"; App. "Scale
+ * Determination and Per-token Clipping Details").  Decode attention reads the
+ * codes through a block table (paged cache, Sec. 4 "KV Cache Layout") and
+ * computes softmax(q K^T / sqrt(d)) V against the reconstructed rows
+ * K^ = Q(K R_k) R_k^T, V^ = Q(V R_v) R_v^T (Sec. 2 quantization notation;
+ * Alg. 1 DecodeStep) as a split-K flash-decoding pass with a log-sum-exp merge
+ * (Sec. 4 "Decoding Attention Kernel").
+ *
+ * Plain C, no HIP include: load it with any FFI.
+ *
+ * Conventions for every entry point
+ *   - Pointers named in the argument lists are DEVICE pointers unless marked
+ *     "host".  The caller owns and allocates every buffer: pages, inputs,
+ *     rotation matrices, workspace and output.  The library never allocates.
+ *   - Calls are asynchronous on `stream` (a hipStream_t passed as void*; NULL
+ *     is the default stream).  OSCAR_OK means "validated and launched".
+ *     OSCAR_ERR_HIP reports a launch error (hipGetLastError right after the
+ *     launch); asynchronous faults surface at the caller's next synchronization.
+ *   - Host arguments are validated before anything is launched; on any error
+ *     nothing is launched and no memory is touched.  Device-resident indices
+ *     (slot_mapping, block_table, seq_lens) are not validated: they must lie in
+ *     range (slot < num_pages*page_size, 0 <= page id < num_pages,
+ *     1 <= seq_lens[b] <= max_pages_per_seq*page_size).
+ *   - Inputs must be finite.  Scales and zeros that fall outside the binary16
+ *     range are saturated to +-65504.
+ *   - Supported shapes: head_dim 128, page_size 64, group_size 32.  Other values
+ *     return OSCAR_ERR_UNSUPPORTED.
+ *
+ * Page byte layout (an ABI: any producer/consumer of the pool must follow it).
+ *   A pool of num_pages pages; page p, kv-head h is the block starting at byte
+ *   (p*Hkv + h) * B_ph, B_ph = 2*P*d/4 + 2*(d/G)*P*4  (6144 bytes for d=128,
+ *   P=64, G=32).  Inside a block, for token slot t in [0,P) and channel c:
+ *     [K codes]  P*d/4 bytes, token-major:  byte t*(d/4) + c/4
+ *     [V codes]  P*d/4 bytes, quad-major:   byte P*d/4 + (c/4)*P + t
+ *     [K s,z]    (d/G)*P 4-byte entries, group-major: entry (c/G)*P + t
+ *     [V s,z]    same, after the K entries
+ *   A code byte holds the four channels 4j..4j+3 of one token; channel c sits
+ *   in bits 2*(c%4)..2*(c%4)+1.  An s,z entry is the binary16 scale followed by
+ *   the binary16 zero point, little-endian.  The stored row is
+ *   Q(x~)_c = s * (code_c - z).
+ */
+#ifndef OSCAR_H
+#define OSCAR_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  OSCAR_OK = 0,
+  OSCAR_ERR_INVALID_ARG = 1,         /* null pointer, negative size, bad ratio ... */
+  OSCAR_ERR_UNSUPPORTED = 2,         /* valid but unsupported shape               */
+  OSCAR_ERR_WORKSPACE_TOO_SMALL = 3, /* workspace_bytes below the required size   */
+  OSCAR_ERR_HIP = 4                  /* the HIP runtime reported an error         */
+} oscar_status;
+
+typedef enum { OSCAR_OUT_BF16 = 0, OSCAR_OUT_F32 = 1 } oscar_dtype;
+
+/* Geometry of one layer's page pool.  Host struct, read only. */
+typedef struct {
+  int32_t head_dim;     /* d, channels per head (128)                 */
+  int32_t num_kv_heads; /* Hkv >= 1                                   */
+  int32_t page_size;    /* P, token slots per page (64)               */
+  int32_t group_size;   /* G, channels per quantization group (32)    */
+  int64_t num_pages;    /* pages in the pool (>= 1)                   */
+} oscar_layout;
+
+/* Human-readable name of a status code (static storage). */
+const char *oscar_status_string(int status);
+
+/* Bytes of one page (all kv-heads): Hkv * B_ph.  0 if L is invalid. */
+size_t oscar_page_bytes(const oscar_layout *L);
+
+/* Bytes of the whole pool: num_pages * oscar_page_bytes(L). */
+size_t oscar_pool_bytes(const oscar_layout *L);
+
+/* Check a layout; OSCAR_OK if this build supports it. */
+int oscar_layout_check(const oscar_layout *L);
+
+/*
+ * oscar_kv_append -- the cache update (Sec. 4 "KV Cache Update"; App. "Scale
+ * Determination and Per-token Clipping Details"; Alg. 1 QuantizeAndWrite).
+ * For each new token i and kv-head h, and for X in {K, V}:
+ *   x~ = x R_X                      rotation, x~_j = sum_c x_c R_X[c][j]
+ *                                   (summed in fp64, rounded once to fp32)
+ *   per group g of G channels:
+ *     tau = clip_X * max|x~|        clipping threshold
+ *     y   = min(max(x~, -tau), tau)
+ *     a = min y, b = max y, s = fp16((b - a)/3), z = fp16(-a / s)
+ *     code = clamp(round_half_even(y / s + z), 0, 3)
+ *   (a group with fp16 scale 0 stores s = 1, z = fp16(-a), codes 0; a zero
+ *   point of 0 is stored as +0), packed into the slot per the page layout.
+ *   k_new, v_new : bf16 [n_tok, Hkv, d], row-major
+ *   slot_mapping : int64 [n_tok], slot = page_id * P + offset; slots must be
+ *                  distinct within one call
+ *   R_k, R_v     : fp32 [d, d], row-major, orthogonal
+ *   clip_k/_v    : ratios in (0, 1]; 1 disables clipping
+ * n_tok == 0 launches nothing.  Only the addressed slots are written.
+ */
+int oscar_kv_append(const oscar_layout *L, void *pages, const void *k_new, const void *v_new,
+                    const int64_t *slot_mapping, int32_t n_tok, const float *R_k,
+                    const float *R_v, float clip_k, float clip_v, void *stream);
+
+/*
+ * Workspace for decode: bytes needed by oscar_decode_attn (and its stages) for
+ * B sequences, Hq query heads and num_splits splits per sequence.
+ */
+size_t oscar_decode_workspace_bytes(const oscar_layout *L, int32_t B, int32_t Hq,
+                                    int32_t num_splits);
+
+/*
+ * A split count that fills the GPU for B sequences whose longest context is
+ * max_seq_len tokens (>= 1).  Every split covers at most
+ * ceil(max_pages_per_seq / num_splits) pages.
+ */
+int32_t oscar_default_num_splits(const oscar_layout *L, int32_t B, int32_t Hq,
+                                 int32_t max_seq_len);
+
+/*
+ * oscar_decode_attn -- one decode step of attention for B sequences over the
+ * INT2 cache (Alg. 1 DecodeStep; Sec. 4 "Decoding Attention Kernel").
+ * For sequence b and query head h (kv-head h / (Hq/Hkv)):
+ *   o = softmax(sm_scale * q K^T) V,  K^ = Q(K~) R_k^T,  V^ = Q(V~) R_v^T,
+ * over the cached tokens t < seq_lens[b], evaluated as
+ *   q~ = q R_k;  scores against Q(K~);  o~ = softmax-weighted sum of Q(V~);
+ *   o = o~ R_v^T,
+ * split along the sequence into num_splits parts merged with a log-sum-exp
+ * reduce.  No host synchronization, no allocation.
+ *   q            : bf16 [B, Hq, d]; Hq % Hkv == 0, Hq/Hkv <= 16
+ *   block_table  : int32 [B, max_pages_per_seq]; token t of sequence b is in
+ *                  page block_table[b][t / P], slot t % P
+ *   seq_lens     : int32 [B], tokens in cache, 1 <= seq_lens[b] <=
+ *                  max_pages_per_seq * P (the current token already appended)
+ *   sm_scale     : logit scale, 1/sqrt(d) for standard attention
+ *   num_splits   : >= 1, or 0 for oscar_default_num_splits(L, B, Hq,
+ *                  max_pages_per_seq * P)
+ *   workspace    : >= oscar_decode_workspace_bytes(L, B, Hq, num_splits) bytes,
+ *                  256-byte aligned, contents need no initialization
+ *   out          : [B, Hq, d] of out_dtype (bf16 is the round-to-nearest-even
+ *                  of the fp32 result)
+ */
+int oscar_decode_attn(const oscar_layout *L, const void *pages, const void *q, int32_t B,
+                      int32_t Hq, const int32_t *block_table, int32_t max_pages_per_seq,
+                      const int32_t *seq_lens, const float *R_k, const float *R_v,
+                      float sm_scale, int32_t num_splits, void *workspace,
+                      size_t workspace_bytes, void *out, oscar_dtype out_dtype, void *stream);
+
+/*
+ * The three stages of oscar_decode_attn, for callers that schedule or time
+ * them separately.  Called in this order on one stream with the same
+ * arguments they equal one oscar_decode_attn call.
+ *   prepare : q~ = q R_k scaled by sm_scale*log2(e), into the workspace.
+ *   split   : per (sequence, kv-head, split) partial softmax state over the
+ *             split's pages, into the workspace.
+ *   reduce  : log-sum-exp merge of the splits, o = o~ R_v^T, into out.
+ */
+int oscar_decode_prepare(const oscar_layout *L, const void *q, int32_t B, int32_t Hq,
+                         const float *R_k, float sm_scale, int32_t num_splits,
+                         void *workspace, size_t workspace_bytes, void *stream);
+int oscar_decode_split(const oscar_layout *L, const void *pages, int32_t B, int32_t Hq,
+                       const int32_t *block_table, int32_t max_pages_per_seq,
+                       const int32_t *seq_lens, int32_t num_splits, void *workspace,
+                       size_t workspace_bytes, void *stream);
+int oscar_decode_reduce(const oscar_layout *L, int32_t B, int32_t Hq, const float *R_v,
+                        int32_t num_splits, void *workspace, size_t workspace_bytes, void *out,
+                        oscar_dtype out_dtype, void *stream);
+
+/*
+ * bf16 paged-decode baseline (same paging, uncompressed cache), for comparing
+ * against the INT2 path on the same GPU.  A bf16 page-head block (page p,
+ * kv-head h) starts at element (p*Hkv + h) * 2*P*d and holds
+ * [K: P x d bf16, token-major][V: P x d bf16, token-major].
+ */
+size_t oscar_bf16_page_bytes(const oscar_layout *L);
+int oscar_bf16_kv_append(const oscar_layout *L, void *pages, const void *k_new,
+                         const void *v_new, const int64_t *slot_mapping, int32_t n_tok,
+                         void *stream);
+size_t oscar_bf16_decode_workspace_bytes(const oscar_layout *L, int32_t B, int32_t Hq,
+                                         int32_t num_splits);
+int oscar_bf16_decode_attn(const oscar_layout *L, const void *pages, const void *q, int32_t B,
+                           int32_t Hq, const int32_t *block_table, int32_t max_pages_per_seq,
+                           const int32_t *seq_lens, float sm_scale, int32_t num_splits,
+                           void *workspace, size_t workspace_bytes, void *out,
+                           oscar_dtype out_dtype, void *stream);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* OSCAR_H */

@@ -1,0 +1,269 @@
+"""Python binding of liboscar (INT2 KV-cache append + paged decode attention for
+OSCAR, arXiv 2605.17757, on MI355X / gfx950).
+
+Argument marshalling only: every function checks tensor dtypes, devices and
+shapes, then calls the C ABI of ``liboscar.so`` (declared in include/oscar.h)
+with raw device pointers and the current HIP stream.  All computation happens
+in the library's HIP kernels; there is no fallback of any kind.  If the shared
+library is missing, importing works but the first call raises OscarError.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+import torch
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "liboscar.so")
+
+OK, ERR_INVALID_ARG, ERR_UNSUPPORTED, ERR_WORKSPACE_TOO_SMALL, ERR_HIP = range(5)
+OUT_BF16, OUT_F32 = 0, 1
+
+HEAD_DIM, PAGE_SIZE, GROUP_SIZE = 128, 64, 32
+
+# Every symbol include/oscar.h declares.
+EXPORTS = (
+    "oscar_status_string", "oscar_page_bytes", "oscar_pool_bytes", "oscar_layout_check",
+    "oscar_kv_append", "oscar_decode_workspace_bytes", "oscar_default_num_splits",
+    "oscar_decode_attn", "oscar_decode_prepare", "oscar_decode_split", "oscar_decode_reduce",
+    "oscar_bf16_page_bytes", "oscar_bf16_kv_append", "oscar_bf16_decode_workspace_bytes",
+    "oscar_bf16_decode_attn",
+)
+
+
+class OscarError(RuntimeError):
+    def __init__(self, status: int, where: str):
+        self.status = status
+        super().__init__("%s failed: %s" % (where, status_string(status) if _lib else status))
+
+
+class Layout(ctypes.Structure):
+    """Mirror of ``oscar_layout``."""
+    _fields_ = [("head_dim", ctypes.c_int32), ("num_kv_heads", ctypes.c_int32),
+                ("page_size", ctypes.c_int32), ("group_size", ctypes.c_int32),
+                ("num_pages", ctypes.c_int64)]
+
+    def __init__(self, num_kv_heads: int, num_pages: int, head_dim: int = HEAD_DIM,
+                 page_size: int = PAGE_SIZE, group_size: int = GROUP_SIZE):
+        super().__init__(head_dim, num_kv_heads, page_size, group_size, num_pages)
+
+
+_lib = None
+
+
+def lib() -> ctypes.CDLL:
+    """The loaded liboscar.so (raises OscarError(-1) if it is not built)."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise OscarError(-1, "loading %s (not built: run python paper_2605_17757_amd/build.py)"
+                             % LIB_PATH)
+        L = ctypes.CDLL(LIB_PATH)
+        P, i32, i64, f32, sz = (ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64, ctypes.c_float,
+                                ctypes.c_size_t)
+        LP = ctypes.POINTER(Layout)
+        sigs = {
+            "oscar_status_string": (ctypes.c_char_p, [ctypes.c_int]),
+            "oscar_page_bytes": (sz, [LP]),
+            "oscar_pool_bytes": (sz, [LP]),
+            "oscar_layout_check": (ctypes.c_int, [LP]),
+            "oscar_kv_append": (ctypes.c_int, [LP, P, P, P, P, i32, P, P, f32, f32, P]),
+            "oscar_decode_workspace_bytes": (sz, [LP, i32, i32, i32]),
+            "oscar_default_num_splits": (i32, [LP, i32, i32, i32]),
+            "oscar_decode_attn": (ctypes.c_int, [LP, P, P, i32, i32, P, i32, P, P, P, f32, i32, P,
+                                                 sz, P, ctypes.c_int, P]),
+            "oscar_decode_prepare": (ctypes.c_int, [LP, P, i32, i32, P, f32, i32, P, sz, P]),
+            "oscar_decode_split": (ctypes.c_int, [LP, P, i32, i32, P, i32, P, i32, P, sz, P]),
+            "oscar_decode_reduce": (ctypes.c_int, [LP, i32, i32, P, i32, P, sz, P, ctypes.c_int,
+                                                   P]),
+            "oscar_bf16_page_bytes": (sz, [LP]),
+            "oscar_bf16_kv_append": (ctypes.c_int, [LP, P, P, P, P, i32, P]),
+            "oscar_bf16_decode_workspace_bytes": (sz, [LP, i32, i32, i32]),
+            "oscar_bf16_decode_attn": (ctypes.c_int, [LP, P, P, i32, i32, P, i32, P, f32, i32, P,
+                                                      sz, P, ctypes.c_int, P]),
+        }
+        for name, (res, args) in sigs.items():
+            fn = getattr(L, name)
+            fn.restype = res
+            fn.argtypes = args
+        _lib = L
+    return _lib
+
+
+def status_string(status: int) -> str:
+    return lib().oscar_status_string(int(status)).decode()
+
+
+def _check(status: int, where: str):
+    if status != OK:
+        raise OscarError(status, where)
+
+
+def _stream(stream):
+    if stream is None:
+        return ctypes.c_void_p(torch.cuda.current_stream().cuda_stream)
+    if isinstance(stream, torch.cuda.Stream):
+        return ctypes.c_void_p(stream.cuda_stream)
+    return ctypes.c_void_p(int(stream))
+
+
+def _ptr(t: torch.Tensor, dtype, name: str, numel: int | None = None):
+    if not isinstance(t, torch.Tensor):
+        raise TypeError("%s must be a torch.Tensor" % name)
+    if not t.is_cuda:
+        raise ValueError("%s must be a GPU tensor" % name)
+    if t.dtype != dtype:
+        raise TypeError("%s must be %s, got %s" % (name, dtype, t.dtype))
+    if not t.is_contiguous():
+        raise ValueError("%s must be contiguous" % name)
+    if numel is not None and t.numel() != numel:
+        raise ValueError("%s has %d elements, expected %d" % (name, t.numel(), numel))
+    return ctypes.c_void_p(t.data_ptr())
+
+
+# ---------------------------------------------------------------------------
+# sizes and helpers
+# ---------------------------------------------------------------------------
+
+def page_bytes(layout: Layout) -> int:
+    return int(lib().oscar_page_bytes(ctypes.byref(layout)))
+
+
+def pool_bytes(layout: Layout) -> int:
+    return int(lib().oscar_pool_bytes(ctypes.byref(layout)))
+
+
+def layout_check(layout: Layout) -> int:
+    return int(lib().oscar_layout_check(ctypes.byref(layout)))
+
+
+def decode_workspace_bytes(layout: Layout, B: int, Hq: int, num_splits: int) -> int:
+    return int(lib().oscar_decode_workspace_bytes(ctypes.byref(layout), B, Hq, num_splits))
+
+
+def default_num_splits(layout: Layout, B: int, Hq: int, max_seq_len: int) -> int:
+    return int(lib().oscar_default_num_splits(ctypes.byref(layout), B, Hq, max_seq_len))
+
+
+def alloc_pool(layout: Layout, device="cuda") -> torch.Tensor:
+    return torch.zeros(pool_bytes(layout), dtype=torch.uint8, device=device)
+
+
+def alloc_workspace(layout: Layout, B: int, Hq: int, num_splits: int, device="cuda"):
+    n = decode_workspace_bytes(layout, B, Hq, num_splits)
+    if n == 0:
+        raise OscarError(ERR_INVALID_ARG, "decode_workspace_bytes")
+    return torch.empty(n, dtype=torch.uint8, device=device)
+
+
+# ---------------------------------------------------------------------------
+# the hot path
+# ---------------------------------------------------------------------------
+
+def kv_append(layout: Layout, pages, k_new, v_new, slot_mapping, R_k, R_v, clip_k: float,
+              clip_v: float, stream=None) -> None:
+    """Rotate, clip, INT2-quantize and pack n_tok new K/V rows into ``pages``."""
+    n_tok = int(slot_mapping.numel())
+    d, hkv = layout.head_dim, layout.num_kv_heads
+    st = lib().oscar_kv_append(
+        ctypes.byref(layout), _ptr(pages, torch.uint8, "pages", pool_bytes(layout)),
+        _ptr(k_new, torch.bfloat16, "k_new", n_tok * hkv * d),
+        _ptr(v_new, torch.bfloat16, "v_new", n_tok * hkv * d),
+        _ptr(slot_mapping, torch.int64, "slot_mapping"), n_tok,
+        _ptr(R_k, torch.float32, "R_k", d * d), _ptr(R_v, torch.float32, "R_v", d * d),
+        float(clip_k), float(clip_v), _stream(stream))
+    _check(st, "oscar_kv_append")
+
+
+def _decode_args(layout, q, block_table, seq_lens):
+    if q.dim() != 3:
+        raise ValueError("q must be [B, Hq, d]")
+    B, Hq = int(q.shape[0]), int(q.shape[1])
+    if block_table.dim() != 2 or block_table.shape[0] != B:
+        raise ValueError("block_table must be [B, max_pages_per_seq]")
+    return B, Hq, int(block_table.shape[1])
+
+
+def decode_attn(layout: Layout, pages, q, block_table, seq_lens, R_k, R_v, sm_scale: float,
+                num_splits: int, workspace, out, stream=None) -> None:
+    """One decode step of attention over the INT2 cache into ``out`` ([B, Hq, d],
+    bf16 or fp32)."""
+    B, Hq, mp = _decode_args(layout, q, block_table, seq_lens)
+    d = layout.head_dim
+    out_dtype = OUT_F32 if out.dtype == torch.float32 else OUT_BF16
+    st = lib().oscar_decode_attn(
+        ctypes.byref(layout), _ptr(pages, torch.uint8, "pages", pool_bytes(layout)),
+        _ptr(q, torch.bfloat16, "q", B * Hq * d), B, Hq,
+        _ptr(block_table, torch.int32, "block_table", B * mp), mp,
+        _ptr(seq_lens, torch.int32, "seq_lens", B), _ptr(R_k, torch.float32, "R_k", d * d),
+        _ptr(R_v, torch.float32, "R_v", d * d), float(sm_scale), int(num_splits),
+        _ptr(workspace, torch.uint8, "workspace"), workspace.numel(),
+        _ptr(out, out.dtype, "out", B * Hq * d), out_dtype, _stream(stream))
+    _check(st, "oscar_decode_attn")
+
+
+def decode_prepare(layout: Layout, q, R_k, sm_scale: float, num_splits: int, workspace,
+                   stream=None) -> None:
+    B, Hq, d = int(q.shape[0]), int(q.shape[1]), layout.head_dim
+    st = lib().oscar_decode_prepare(
+        ctypes.byref(layout), _ptr(q, torch.bfloat16, "q", B * Hq * d), B, Hq,
+        _ptr(R_k, torch.float32, "R_k", d * d), float(sm_scale), int(num_splits),
+        _ptr(workspace, torch.uint8, "workspace"), workspace.numel(), _stream(stream))
+    _check(st, "oscar_decode_prepare")
+
+
+def decode_split(layout: Layout, pages, B: int, Hq: int, block_table, seq_lens,
+                 num_splits: int, workspace, stream=None) -> None:
+    mp = int(block_table.shape[1])
+    st = lib().oscar_decode_split(
+        ctypes.byref(layout), _ptr(pages, torch.uint8, "pages", pool_bytes(layout)), B, Hq,
+        _ptr(block_table, torch.int32, "block_table", B * mp), mp,
+        _ptr(seq_lens, torch.int32, "seq_lens", B), int(num_splits),
+        _ptr(workspace, torch.uint8, "workspace"), workspace.numel(), _stream(stream))
+    _check(st, "oscar_decode_split")
+
+
+def decode_reduce(layout: Layout, B: int, Hq: int, R_v, num_splits: int, workspace, out,
+                  stream=None) -> None:
+    d = layout.head_dim
+    out_dtype = OUT_F32 if out.dtype == torch.float32 else OUT_BF16
+    st = lib().oscar_decode_reduce(
+        ctypes.byref(layout), B, Hq, _ptr(R_v, torch.float32, "R_v", d * d), int(num_splits),
+        _ptr(workspace, torch.uint8, "workspace"), workspace.numel(),
+        _ptr(out, out.dtype, "out", B * Hq * d), out_dtype, _stream(stream))
+    _check(st, "oscar_decode_reduce")
+
+
+# ---------------------------------------------------------------------------
+# bf16 baseline
+# ---------------------------------------------------------------------------
+
+def bf16_pool_bytes(layout: Layout) -> int:
+    return int(lib().oscar_bf16_page_bytes(ctypes.byref(layout))) * int(layout.num_pages)
+
+
+def bf16_kv_append(layout: Layout, pages, k_new, v_new, slot_mapping, stream=None) -> None:
+    n_tok = int(slot_mapping.numel())
+    d, hkv = layout.head_dim, layout.num_kv_heads
+    st = lib().oscar_bf16_kv_append(
+        ctypes.byref(layout), _ptr(pages, torch.bfloat16, "pages", bf16_pool_bytes(layout) // 2),
+        _ptr(k_new, torch.bfloat16, "k_new", n_tok * hkv * d),
+        _ptr(v_new, torch.bfloat16, "v_new", n_tok * hkv * d),
+        _ptr(slot_mapping, torch.int64, "slot_mapping"), n_tok, _stream(stream))
+    _check(st, "oscar_bf16_kv_append")
+
+
+def bf16_decode_attn(layout: Layout, pages, q, block_table, seq_lens, sm_scale: float,
+                     num_splits: int, workspace, out, stream=None) -> None:
+    B, Hq, mp = _decode_args(layout, q, block_table, seq_lens)
+    d = layout.head_dim
+    out_dtype = OUT_F32 if out.dtype == torch.float32 else OUT_BF16
+    st = lib().oscar_bf16_decode_attn(
+        ctypes.byref(layout), _ptr(pages, torch.bfloat16, "pages", bf16_pool_bytes(layout) // 2),
+        _ptr(q, torch.bfloat16, "q", B * Hq * d), B, Hq,
+        _ptr(block_table, torch.int32, "block_table", B * mp), mp,
+        _ptr(seq_lens, torch.int32, "seq_lens", B), float(sm_scale), int(num_splits),
+        _ptr(workspace, torch.uint8, "workspace"), workspace.numel(),
+        _ptr(out, out.dtype, "out", B * Hq * d), out_dtype, _stream(stream))
+    _check(st, "oscar_bf16_decode_attn")

@@ -1,0 +1,196 @@
+// Cache update: rotate -> clip -> asymmetric INT2 per 32-channel group -> pack.
+// (Sec. 4 "KV Cache Update"; App. "Scale Determination and Per-token Clipping
+// Details"; Alg. 1 QuantizeAndWrite.)
+//
+// This file is compiled with -ffp-contract=off: every fp32 step below is one
+// IEEE operation (no fused multiply-add), and the rotation is an explicit fp64
+// fused multiply-add chain in ascending channel order.  Because each product of
+// a bf16 input and an fp32 matrix entry is exact in fp64, that chain equals
+// "sum in fp64, ascending, round once to fp32" bit for bit.
+//
+// Work decomposition: blockIdx.y selects K (0) or V (1); the block stages that
+// rotation matrix (64 KB fp32) in LDS.  Each wave takes four rows (token, head)
+// at a time; lane l computes output channels l and l+64 of the four rows, so
+// every matrix element read from LDS feeds four fp64 FMAs.  A 32-channel group
+// is then one half of the wave: channels 0-31 / 64-95 live in lanes 0-31,
+// channels 32-63 / 96-127 in lanes 32-63, and the group reductions are 5-step
+// xor shuffles inside the half wave.
+#include <hip/hip_fp16.h>
+
+#include "internal.h"
+
+namespace oscar {
+namespace {
+
+constexpr int kWaves = 4;
+constexpr int kRows = 4;  // rows per wave item
+
+__device__ inline float f16_bits_to_f32(uint16_t h) { return __half2float(__ushort_as_half(h)); }
+
+// binary16 with saturation to +-65504 (round to nearest even).
+__device__ inline uint16_t f16_sat_bits(float f) {
+  f = fminf(fmaxf(f, -65504.0f), 65504.0f);
+  return __half_as_ushort(__float2half_rn(f));
+}
+
+// A zero point of zero is stored as +0.  This is done on the binary16 bits: the
+// compiler may drop an "x + 0.0f" whose result only feeds fmaxf/fminf.
+__device__ inline uint16_t plus_zero(uint16_t h) { return (h & 0x7fffu) ? h : (uint16_t)0; }
+
+__device__ inline float half_wave_max(float x) {
+#pragma unroll
+  for (int m = 16; m >= 1; m >>= 1) x = fmaxf(x, __shfl_xor(x, m, 64));
+  return x;
+}
+__device__ inline float half_wave_min(float x) {
+#pragma unroll
+  for (int m = 16; m >= 1; m >>= 1) x = fminf(x, __shfl_xor(x, m, 64));
+  return x;
+}
+
+struct QOut {
+  uint32_t code;
+  uint16_t s16, z16;
+};
+
+// Clip and quantize one channel value x of a group spread over a half wave.
+__device__ inline QOut quantize(float x, float clip) {
+  QOut o;
+  const float m = half_wave_max(fabsf(x));
+  const float tau = __fmul_rn(clip, m);
+  const float y = fminf(fmaxf(x, -tau), tau);
+  const float a = half_wave_min(y);
+  const float b = half_wave_max(y);
+  const float s = __fdiv_rn(__fsub_rn(b, a), 3.0f);
+  uint16_t s16 = f16_sat_bits(s);
+  if ((s16 & 0x7fffu) == 0) {
+    o.s16 = 0x3c00u;  // 1.0
+    o.z16 = plus_zero(f16_sat_bits(-a));
+    o.code = 0;
+  } else {
+    const float sf = f16_bits_to_f32(s16);
+    const uint16_t z16 = plus_zero(f16_sat_bits(__fdiv_rn(-a, sf)));
+    const float zf = f16_bits_to_f32(z16);
+    float r = rintf(__fadd_rn(__fdiv_rn(y, sf), zf));
+    r = fminf(fmaxf(r, 0.0f), 3.0f);
+    o.s16 = s16;
+    o.z16 = z16;
+    o.code = (uint32_t)r;
+  }
+  return o;
+}
+
+// OR the 2-bit codes of lanes 4j..4j+3 into the byte of quad j (valid in lane 4j).
+__device__ inline uint32_t pack_quad(uint32_t code, int lane) {
+  uint32_t v = code << (2 * (lane & 3));
+  v |= __shfl_xor(v, 1, 64);
+  v |= __shfl_xor(v, 2, 64);
+  return v;
+}
+
+__global__ __launch_bounds__(256) void append_kernel(
+    uint8_t* __restrict__ pages, int Hkv, const uint16_t* __restrict__ k,
+    const uint16_t* __restrict__ v, const int64_t* __restrict__ slots, int n_rows,
+    const float* __restrict__ Rk, const float* __restrict__ Rv, float clip_k, float clip_v) {
+  __shared__ float Rs[kD * kD];
+  __shared__ double xs[kWaves][kD][kRows];
+
+  const int is_v = blockIdx.y;
+  const float* __restrict__ R = is_v ? Rv : Rk;
+  const uint16_t* __restrict__ X = is_v ? v : k;
+  const float clip = is_v ? clip_v : clip_k;
+
+  for (int i = threadIdx.x; i < kD * kD / 4; i += blockDim.x)
+    reinterpret_cast<float4*>(Rs)[i] = reinterpret_cast<const float4*>(R)[i];
+
+  const int w = threadIdx.x >> 6;
+  const int l = threadIdx.x & 63;
+  const int n_items = (n_rows + kRows - 1) / kRows;
+  const uint32_t sz_base = is_v ? kOffVSz : kOffKSz;
+
+  // The loop bound is uniform across the block so that __syncthreads is legal.
+  for (int base = blockIdx.x * kWaves; base < n_items; base += gridDim.x * kWaves) {
+    const int item = base + w;
+    __syncthreads();  // xs reuse; first pass also covers the R staging
+    for (int rr = 0; rr < kRows; ++rr) {
+      const int row = item * kRows + rr;
+      double x0 = 0.0, x1 = 0.0;
+      if (item < n_items && row < n_rows) {
+        const uint32_t pair = reinterpret_cast<const uint32_t*>(X + (size_t)row * kD)[l];
+        x0 = (double)__uint_as_float(pair << 16);
+        x1 = (double)__uint_as_float(pair & 0xffff0000u);
+      }
+      xs[w][2 * l][rr] = x0;
+      xs[w][2 * l + 1][rr] = x1;
+    }
+    __syncthreads();
+    if (item >= n_items) continue;
+
+    double acc0[kRows], acc1[kRows];
+#pragma unroll
+    for (int rr = 0; rr < kRows; ++rr) acc0[rr] = acc1[rr] = 0.0;
+#pragma unroll 4
+    for (int c = 0; c < kD; ++c) {
+      const double r0 = (double)Rs[c * kD + l];
+      const double r1 = (double)Rs[c * kD + l + 64];
+#pragma unroll
+      for (int rr = 0; rr < kRows; ++rr) {
+        const double xc = xs[w][c][rr];
+        acc0[rr] = __fma_rn(xc, r0, acc0[rr]);
+        acc1[rr] = __fma_rn(xc, r1, acc1[rr]);
+      }
+    }
+
+#pragma unroll
+    for (int rr = 0; rr < kRows; ++rr) {
+      const int row = item * kRows + rr;
+      const float xt0 = __double2float_rn(acc0[rr]);  // channel l
+      const float xt1 = __double2float_rn(acc1[rr]);  // channel l + 64
+      const QOut q0 = quantize(xt0, clip);
+      const QOut q1 = quantize(xt1, clip);
+      const uint32_t byte0 = pack_quad(q0.code, l);    // quad l/4
+      const uint32_t byte1 = pack_quad(q1.code, l);    // quad 16 + l/4
+      if (row >= n_rows) continue;                     // uniform across the wave
+      const int tok = row / Hkv;
+      const int h = row - tok * Hkv;
+      const int64_t slot = slots[tok];
+      const int64_t page = slot / kP;
+      const int t = (int)(slot - page * kP);
+      uint8_t* blk = pages + ((size_t)page * Hkv + h) * kBlockBytes;
+      if ((l & 3) == 0) {
+        const int j0 = l >> 2, j1 = 16 + (l >> 2);
+        if (is_v) {
+          blk[kOffVCodes + j0 * kP + t] = (uint8_t)byte0;
+          blk[kOffVCodes + j1 * kP + t] = (uint8_t)byte1;
+        } else {
+          blk[kOffKCodes + t * (kD / 4) + j0] = (uint8_t)byte0;
+          blk[kOffKCodes + t * (kD / 4) + j1] = (uint8_t)byte1;
+        }
+      }
+      if ((l & 31) == 0) {
+        const int g0 = l >> 5, g1 = 2 + (l >> 5);
+        *reinterpret_cast<uint32_t*>(blk + sz_base + (g0 * kP + t) * 4) =
+            (uint32_t)q0.s16 | ((uint32_t)q0.z16 << 16);
+        *reinterpret_cast<uint32_t*>(blk + sz_base + (g1 * kP + t) * 4) =
+            (uint32_t)q1.s16 | ((uint32_t)q1.z16 << 16);
+      }
+    }
+  }
+}
+
+}  // namespace
+
+hipError_t launch_append(void* pages, int64_t Hkv, const uint16_t* k, const uint16_t* v,
+                         const int64_t* slots, int n_tok, const float* Rk, const float* Rv,
+                         float clip_k, float clip_v, hipStream_t st) {
+  const int64_t n_rows = (int64_t)n_tok * Hkv;
+  const int64_t n_items = (n_rows + kRows - 1) / kRows;
+  int64_t blocks = (n_items + kWaves - 1) / kWaves;
+  if (blocks > 1024) blocks = 1024;
+  dim3 grid((unsigned)blocks, 2);
+  hipLaunchKernelGGL(append_kernel, grid, dim3(256), 0, st, static_cast<uint8_t*>(pages),
+                     (int)Hkv, k, v, slots, (int)n_rows, Rk, Rv, clip_k, clip_v);
+  return hipGetLastError();
+}
+
+}  // namespace oscar

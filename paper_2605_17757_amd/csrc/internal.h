@@ -1,0 +1,60 @@
+// Internal declarations shared by the liboscar host entry points and kernels.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+namespace oscar {
+
+// Supported geometry: head dim 128, 64 token slots per page, 32-channel groups.
+constexpr int kD = 128;
+constexpr int kP = 64;
+constexpr int kG = 32;
+constexpr int kNG = kD / kG;                       // groups per head
+constexpr int kCodeBytes = kP * kD / 4;            // one code region of a page-head block
+constexpr int kSzBytes = kNG * kP * 4;             // one (scale, zero) region
+constexpr int kBlockBytes = 2 * kCodeBytes + 2 * kSzBytes;   // 6144
+constexpr int kOffKCodes = 0;
+constexpr int kOffVCodes = kCodeBytes;             // 2048
+constexpr int kOffKSz = 2 * kCodeBytes;            // 4096
+constexpr int kOffVSz = 2 * kCodeBytes + kSzBytes; // 5120
+constexpr int kMaxGroupHeads = 16;                 // query heads per kv-head
+
+// Workspace carving for decode (byte offsets, 256-aligned).
+struct DecodeWs {
+  size_t qt_off, po_off, pml_off, total;
+};
+inline size_t align256(size_t x) { return (x + 255) & ~size_t(255); }
+inline DecodeWs decode_ws(int64_t B, int64_t Hq, int64_t S) {
+  DecodeWs w;
+  w.qt_off = 0;
+  w.po_off = align256(w.qt_off + (size_t)(B * Hq) * kD * sizeof(float));
+  w.pml_off = align256(w.po_off + (size_t)(B * Hq * S) * kD * sizeof(float));
+  w.total = align256(w.pml_off + (size_t)(B * Hq * S) * 2 * sizeof(float));
+  return w;
+}
+
+// Kernel launchers (each returns the hipError_t of its launch).
+hipError_t launch_append(void* pages, int64_t Hkv, const uint16_t* k, const uint16_t* v,
+                         const int64_t* slots, int n_tok, const float* Rk, const float* Rv,
+                         float clip_k, float clip_v, hipStream_t st);
+
+hipError_t launch_decode_prepare(const uint16_t* q, int B, int Hq, const float* Rk,
+                                 float qscale, float* qt, hipStream_t st);
+hipError_t launch_decode_split(const uint8_t* pages, int Hkv, int B, int Hq,
+                               const int32_t* block_table, int max_pages,
+                               const int32_t* seq_lens, int num_splits, const float* qt,
+                               float* part_o, float* part_ml, hipStream_t st);
+hipError_t launch_decode_reduce(int B, int Hq, int num_splits, const float* part_o,
+                                const float* part_ml, const float* Rv, void* out, int out_f32,
+                                hipStream_t st);
+
+hipError_t launch_bf16_append(void* pages, int64_t Hkv, const uint16_t* k, const uint16_t* v,
+                              const int64_t* slots, int n_tok, hipStream_t st);
+hipError_t launch_bf16_split(const uint16_t* pages, int Hkv, int B, int Hq,
+                             const int32_t* block_table, int max_pages,
+                             const int32_t* seq_lens, int num_splits, const float* qt,
+                             float* part_o, float* part_ml, hipStream_t st);
+
+}  // namespace oscar

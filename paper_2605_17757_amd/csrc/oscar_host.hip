@@ -1,0 +1,286 @@
+// liboscar C ABI: argument validation, workspace carving and kernel launches.
+// Every entry point validates all host arguments before launching anything.
+#include <math.h>
+
+#include <atomic>
+
+#include "../../include/oscar.h"
+#include "internal.h"
+
+using namespace oscar;
+
+namespace {
+
+constexpr float kLog2e = 1.4426950408889634f;
+
+int check_layout(const oscar_layout* L) {
+  if (!L) return OSCAR_ERR_INVALID_ARG;
+  if (L->head_dim <= 0 || L->num_kv_heads <= 0 || L->page_size <= 0 || L->group_size <= 0 ||
+      L->num_pages <= 0)
+    return OSCAR_ERR_INVALID_ARG;
+  if (L->head_dim % L->group_size != 0 || L->head_dim % 4 != 0) return OSCAR_ERR_INVALID_ARG;
+  if (L->head_dim != kD || L->page_size != kP || L->group_size != kG) return OSCAR_ERR_UNSUPPORTED;
+  if (L->num_kv_heads > 65535) return OSCAR_ERR_UNSUPPORTED;
+  return OSCAR_OK;
+}
+
+bool clip_ok(float c) { return isfinite(c) && c > 0.0f && c <= 1.0f; }
+
+int device_cus() {
+  static std::atomic<int> cached{0};
+  int v = cached.load(std::memory_order_relaxed);
+  if (v > 0) return v;
+  int dev = 0, cus = 0;
+  if (hipGetDevice(&dev) == hipSuccess &&
+      hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) == hipSuccess &&
+      cus > 0)
+    v = cus;
+  else
+    v = 256;
+  cached.store(v, std::memory_order_relaxed);
+  return v;
+}
+
+int hip_status(hipError_t e) { return e == hipSuccess ? OSCAR_OK : OSCAR_ERR_HIP; }
+
+int check_decode_common(const oscar_layout* L, int32_t B, int32_t Hq, int32_t num_splits) {
+  int st = check_layout(L);
+  if (st) return st;
+  if (B < 1 || Hq < 1 || num_splits < 1) return OSCAR_ERR_INVALID_ARG;
+  if (Hq % L->num_kv_heads != 0) return OSCAR_ERR_INVALID_ARG;
+  if (Hq / L->num_kv_heads > kMaxGroupHeads) return OSCAR_ERR_UNSUPPORTED;
+  if (B > 65535) return OSCAR_ERR_UNSUPPORTED;
+  return OSCAR_OK;
+}
+
+// Split count for num_splits == 0: >= 1, or -status for an invalid layout, or 0
+// for an invalid max_pages_per_seq.
+int32_t resolve_default_splits(const oscar_layout* L, int32_t B, int32_t Hq,
+                               int32_t max_pages_per_seq) {
+  const int ls = check_layout(L);
+  if (ls) return -ls;
+  if (max_pages_per_seq < 1) return 0;
+  int64_t max_len = (int64_t)max_pages_per_seq * L->page_size;
+  if (max_len > 0x7fffffffLL) max_len = 0x7fffffffLL;
+  return oscar_default_num_splits(L, B, Hq, (int32_t)max_len);
+}
+
+bool aligned(const void* p, size_t a) { return (reinterpret_cast<uintptr_t>(p) & (a - 1)) == 0; }
+
+}  // namespace
+
+extern "C" {
+
+const char* oscar_status_string(int status) {
+  switch (status) {
+    case OSCAR_OK: return "OSCAR_OK";
+    case OSCAR_ERR_INVALID_ARG: return "OSCAR_ERR_INVALID_ARG";
+    case OSCAR_ERR_UNSUPPORTED: return "OSCAR_ERR_UNSUPPORTED";
+    case OSCAR_ERR_WORKSPACE_TOO_SMALL: return "OSCAR_ERR_WORKSPACE_TOO_SMALL";
+    case OSCAR_ERR_HIP: return "OSCAR_ERR_HIP";
+    default: return "OSCAR_ERR_UNKNOWN";
+  }
+}
+
+int oscar_layout_check(const oscar_layout* L) { return check_layout(L); }
+
+size_t oscar_page_bytes(const oscar_layout* L) {
+  if (check_layout(L) == OSCAR_ERR_INVALID_ARG) return 0;
+  const size_t d = (size_t)L->head_dim, P = (size_t)L->page_size, G = (size_t)L->group_size;
+  return (size_t)L->num_kv_heads * (2 * P * (d / 4) + 2 * (d / G) * P * 4);
+}
+
+size_t oscar_pool_bytes(const oscar_layout* L) {
+  const size_t pb = oscar_page_bytes(L);
+  return pb ? pb * (size_t)L->num_pages : 0;
+}
+
+size_t oscar_decode_workspace_bytes(const oscar_layout* L, int32_t B, int32_t Hq,
+                                    int32_t num_splits) {
+  if (check_decode_common(L, B, Hq, num_splits) != OSCAR_OK) return 0;
+  return decode_ws(B, Hq, num_splits).total;
+}
+
+int32_t oscar_default_num_splits(const oscar_layout* L, int32_t B, int32_t Hq,
+                                 int32_t max_seq_len) {
+  if (check_layout(L) != OSCAR_OK || B < 1 || Hq < 1 || max_seq_len < 1) return 1;
+  const int64_t pages = (max_seq_len + L->page_size - 1) / L->page_size;
+  const int64_t target_blocks = 4LL * device_cus();
+  const int64_t pairs = (int64_t)B * L->num_kv_heads;
+  int64_t s = (target_blocks + pairs - 1) / pairs;
+  int64_t cap = pages / 4;  // keep at least one page per wave of a split
+  if (cap < 1) cap = 1;
+  if (s > cap) s = cap;
+  if (s < 1) s = 1;
+  return (int32_t)s;
+}
+
+int oscar_kv_append(const oscar_layout* L, void* pages, const void* k_new, const void* v_new,
+                    const int64_t* slot_mapping, int32_t n_tok, const float* R_k,
+                    const float* R_v, float clip_k, float clip_v, void* stream) {
+  int st = check_layout(L);
+  if (st) return st;
+  if (n_tok < 0 || !clip_ok(clip_k) || !clip_ok(clip_v)) return OSCAR_ERR_INVALID_ARG;
+  if (n_tok == 0) return OSCAR_OK;
+  if (!pages || !k_new || !v_new || !slot_mapping || !R_k || !R_v) return OSCAR_ERR_INVALID_ARG;
+  if (!aligned(k_new, 4) || !aligned(v_new, 4) || !aligned(R_k, 16) || !aligned(R_v, 16) ||
+      !aligned(pages, 16) || !aligned(slot_mapping, 8))
+    return OSCAR_ERR_INVALID_ARG;
+  if ((int64_t)n_tok * L->num_kv_heads > 0x7fffffffLL) return OSCAR_ERR_UNSUPPORTED;
+  return hip_status(launch_append(pages, L->num_kv_heads, static_cast<const uint16_t*>(k_new),
+                                  static_cast<const uint16_t*>(v_new), slot_mapping, n_tok, R_k,
+                                  R_v, clip_k, clip_v, static_cast<hipStream_t>(stream)));
+}
+
+int oscar_decode_prepare(const oscar_layout* L, const void* q, int32_t B, int32_t Hq,
+                         const float* R_k, float sm_scale, int32_t num_splits, void* workspace,
+                         size_t workspace_bytes, void* stream) {
+  int st = check_decode_common(L, B, Hq, num_splits);
+  if (st) return st;
+  if (!q || !R_k || !workspace || !isfinite(sm_scale)) return OSCAR_ERR_INVALID_ARG;
+  if (!aligned(workspace, 256) || !aligned(q, 4)) return OSCAR_ERR_INVALID_ARG;
+  const DecodeWs ws = decode_ws(B, Hq, num_splits);
+  if (workspace_bytes < ws.total) return OSCAR_ERR_WORKSPACE_TOO_SMALL;
+  float* qt = reinterpret_cast<float*>(static_cast<uint8_t*>(workspace) + ws.qt_off);
+  return hip_status(launch_decode_prepare(static_cast<const uint16_t*>(q), B, Hq, R_k,
+                                          sm_scale * kLog2e, qt,
+                                          static_cast<hipStream_t>(stream)));
+}
+
+int oscar_decode_split(const oscar_layout* L, const void* pages, int32_t B, int32_t Hq,
+                       const int32_t* block_table, int32_t max_pages_per_seq,
+                       const int32_t* seq_lens, int32_t num_splits, void* workspace,
+                       size_t workspace_bytes, void* stream) {
+  int st = check_decode_common(L, B, Hq, num_splits);
+  if (st) return st;
+  if (!pages || !block_table || !seq_lens || !workspace || max_pages_per_seq < 1)
+    return OSCAR_ERR_INVALID_ARG;
+  if (!aligned(workspace, 256) || !aligned(pages, 16)) return OSCAR_ERR_INVALID_ARG;
+  const DecodeWs ws = decode_ws(B, Hq, num_splits);
+  if (workspace_bytes < ws.total) return OSCAR_ERR_WORKSPACE_TOO_SMALL;
+  uint8_t* base = static_cast<uint8_t*>(workspace);
+  return hip_status(launch_decode_split(
+      static_cast<const uint8_t*>(pages), L->num_kv_heads, B, Hq, block_table, max_pages_per_seq,
+      seq_lens, num_splits, reinterpret_cast<const float*>(base + ws.qt_off),
+      reinterpret_cast<float*>(base + ws.po_off), reinterpret_cast<float*>(base + ws.pml_off),
+      static_cast<hipStream_t>(stream)));
+}
+
+int oscar_decode_reduce(const oscar_layout* L, int32_t B, int32_t Hq, const float* R_v,
+                        int32_t num_splits, void* workspace, size_t workspace_bytes, void* out,
+                        oscar_dtype out_dtype, void* stream) {
+  int st = check_decode_common(L, B, Hq, num_splits);
+  if (st) return st;
+  if (!R_v || !workspace || !out) return OSCAR_ERR_INVALID_ARG;
+  if (out_dtype != OSCAR_OUT_BF16 && out_dtype != OSCAR_OUT_F32) return OSCAR_ERR_INVALID_ARG;
+  if (!aligned(workspace, 256) || !aligned(out, out_dtype == OSCAR_OUT_F32 ? 4 : 2))
+    return OSCAR_ERR_INVALID_ARG;
+  const DecodeWs ws = decode_ws(B, Hq, num_splits);
+  if (workspace_bytes < ws.total) return OSCAR_ERR_WORKSPACE_TOO_SMALL;
+  uint8_t* base = static_cast<uint8_t*>(workspace);
+  return hip_status(launch_decode_reduce(B, Hq, num_splits,
+                                         reinterpret_cast<const float*>(base + ws.po_off),
+                                         reinterpret_cast<const float*>(base + ws.pml_off), R_v,
+                                         out, out_dtype == OSCAR_OUT_F32 ? 1 : 0,
+                                         static_cast<hipStream_t>(stream)));
+}
+
+int oscar_decode_attn(const oscar_layout* L, const void* pages, const void* q, int32_t B,
+                      int32_t Hq, const int32_t* block_table, int32_t max_pages_per_seq,
+                      const int32_t* seq_lens, const float* R_k, const float* R_v,
+                      float sm_scale, int32_t num_splits, void* workspace,
+                      size_t workspace_bytes, void* out, oscar_dtype out_dtype, void* stream) {
+  if (num_splits < 0) return OSCAR_ERR_INVALID_ARG;
+  if (num_splits == 0) {
+    num_splits = resolve_default_splits(L, B, Hq, max_pages_per_seq);
+    if (num_splits < 1) return num_splits == 0 ? OSCAR_ERR_INVALID_ARG : -num_splits;
+  }
+  // validate every argument of all three stages before launching any of them
+  int st = check_decode_common(L, B, Hq, num_splits);
+  if (st) return st;
+  if (!pages || !q || !block_table || !seq_lens || !R_k || !R_v || !workspace || !out ||
+      max_pages_per_seq < 1 || !isfinite(sm_scale))
+    return OSCAR_ERR_INVALID_ARG;
+  if (out_dtype != OSCAR_OUT_BF16 && out_dtype != OSCAR_OUT_F32) return OSCAR_ERR_INVALID_ARG;
+  if (!aligned(workspace, 256) || !aligned(pages, 16) || !aligned(q, 4) ||
+      !aligned(out, out_dtype == OSCAR_OUT_F32 ? 4 : 2))
+    return OSCAR_ERR_INVALID_ARG;
+  if (workspace_bytes < decode_ws(B, Hq, num_splits).total) return OSCAR_ERR_WORKSPACE_TOO_SMALL;
+  st = oscar_decode_prepare(L, q, B, Hq, R_k, sm_scale, num_splits, workspace, workspace_bytes,
+                            stream);
+  if (st) return st;
+  st = oscar_decode_split(L, pages, B, Hq, block_table, max_pages_per_seq, seq_lens, num_splits,
+                          workspace, workspace_bytes, stream);
+  if (st) return st;
+  return oscar_decode_reduce(L, B, Hq, R_v, num_splits, workspace, workspace_bytes, out,
+                             out_dtype, stream);
+}
+
+// ---------------------------------------------------------------------------
+// bf16 baseline
+// ---------------------------------------------------------------------------
+
+size_t oscar_bf16_page_bytes(const oscar_layout* L) {
+  if (check_layout(L) == OSCAR_ERR_INVALID_ARG) return 0;
+  return (size_t)L->num_kv_heads * 2 * (size_t)L->page_size * (size_t)L->head_dim * 2;
+}
+
+int oscar_bf16_kv_append(const oscar_layout* L, void* pages, const void* k_new,
+                         const void* v_new, const int64_t* slot_mapping, int32_t n_tok,
+                         void* stream) {
+  int st = check_layout(L);
+  if (st) return st;
+  if (n_tok < 0) return OSCAR_ERR_INVALID_ARG;
+  if (n_tok == 0) return OSCAR_OK;
+  if (!pages || !k_new || !v_new || !slot_mapping) return OSCAR_ERR_INVALID_ARG;
+  if (!aligned(pages, 16) || !aligned(k_new, 4) || !aligned(v_new, 4)) return OSCAR_ERR_INVALID_ARG;
+  return hip_status(launch_bf16_append(pages, L->num_kv_heads,
+                                       static_cast<const uint16_t*>(k_new),
+                                       static_cast<const uint16_t*>(v_new), slot_mapping, n_tok,
+                                       static_cast<hipStream_t>(stream)));
+}
+
+size_t oscar_bf16_decode_workspace_bytes(const oscar_layout* L, int32_t B, int32_t Hq,
+                                         int32_t num_splits) {
+  return oscar_decode_workspace_bytes(L, B, Hq, num_splits);
+}
+
+int oscar_bf16_decode_attn(const oscar_layout* L, const void* pages, const void* q, int32_t B,
+                           int32_t Hq, const int32_t* block_table, int32_t max_pages_per_seq,
+                           const int32_t* seq_lens, float sm_scale, int32_t num_splits,
+                           void* workspace, size_t workspace_bytes, void* out,
+                           oscar_dtype out_dtype, void* stream) {
+  if (num_splits < 0) return OSCAR_ERR_INVALID_ARG;
+  if (num_splits == 0) {
+    num_splits = resolve_default_splits(L, B, Hq, max_pages_per_seq);
+    if (num_splits < 1) return num_splits == 0 ? OSCAR_ERR_INVALID_ARG : -num_splits;
+  }
+  int st = check_decode_common(L, B, Hq, num_splits);
+  if (st) return st;
+  if (!pages || !q || !block_table || !seq_lens || !workspace || !out || max_pages_per_seq < 1 ||
+      !isfinite(sm_scale))
+    return OSCAR_ERR_INVALID_ARG;
+  if (out_dtype != OSCAR_OUT_BF16 && out_dtype != OSCAR_OUT_F32) return OSCAR_ERR_INVALID_ARG;
+  if (!aligned(workspace, 256) || !aligned(pages, 16) || !aligned(q, 4) ||
+      !aligned(out, out_dtype == OSCAR_OUT_F32 ? 4 : 2))
+    return OSCAR_ERR_INVALID_ARG;
+  const DecodeWs ws = decode_ws(B, Hq, num_splits);
+  if (workspace_bytes < ws.total) return OSCAR_ERR_WORKSPACE_TOO_SMALL;
+  uint8_t* base = static_cast<uint8_t*>(workspace);
+  float* qt = reinterpret_cast<float*>(base + ws.qt_off);
+  float* po = reinterpret_cast<float*>(base + ws.po_off);
+  float* pml = reinterpret_cast<float*>(base + ws.pml_off);
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  // q scaled by sm_scale*log2 e, no rotation (R = I); reduce with R = I
+  st = hip_status(launch_decode_prepare(static_cast<const uint16_t*>(q), B, Hq, nullptr,
+                                        sm_scale * kLog2e, qt, s));
+  if (st) return st;
+  st = hip_status(launch_bf16_split(static_cast<const uint16_t*>(pages), L->num_kv_heads, B, Hq,
+                                    block_table, max_pages_per_seq, seq_lens, num_splits, qt, po,
+                                    pml, s));
+  if (st) return st;
+  return hip_status(launch_decode_reduce(B, Hq, num_splits, po, pml, nullptr, out,
+                                         out_dtype == OSCAR_OUT_F32 ? 1 : 0, s));
+}
+
+}  // extern "C"

@@ -1,0 +1,132 @@
+"""Host-only checks of the C ABI: the library loads, exports every symbol that
+include/oscar.h declares, sizes its buffers as the layout definition says, and
+rejects every invalid argument with the documented status before launching
+anything (these calls never reach the GPU, so they run without one)."""
+import ctypes
+import os
+import re
+
+import pytest
+
+import oracle
+import paper_2605_17757_amd as ok
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "oscar.h")
+
+FAKE = ctypes.c_void_p(0x10000)     # never dereferenced: validation fails first
+
+
+def _declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(oscar_[a-z0-9_]+)\s*\(", text)))
+
+
+@pytest.fixture(scope="module")
+def L():
+    if not os.path.exists(ok.LIB_PATH):
+        pytest.fail("liboscar.so is not built (run python paper_2605_17757_amd/build.py)")
+    return ok.lib()
+
+
+def test_exports_every_declared_symbol(L):
+    declared = _declared_functions()
+    assert set(declared) == set(ok.EXPORTS)
+    for name in declared:
+        assert hasattr(L, name), name
+
+
+def test_status_strings(L):
+    assert ok.status_string(0) == "OSCAR_OK"
+    assert ok.status_string(3) == "OSCAR_ERR_WORKSPACE_TOO_SMALL"
+    assert ok.status_string(99) == "OSCAR_ERR_UNKNOWN"
+
+
+def test_sizes_follow_layout_definition(L):
+    for hkv in (1, 8):
+        lay = ok.Layout(num_kv_heads=hkv, num_pages=10)
+        # the oracle implements the same byte layout independently
+        assert ok.page_bytes(lay) == hkv * oracle.page_head_bytes(128, 64, 32) == hkv * 6144
+        assert ok.pool_bytes(lay) == 10 * hkv * 6144
+        assert ok.bf16_pool_bytes(lay) == 10 * hkv * 2 * 64 * 128 * 2
+    lay = ok.Layout(num_kv_heads=8, num_pages=10)
+    ws = ok.decode_workspace_bytes(lay, 64, 32, 8)
+    need = 64 * 32 * 128 * 4 + 64 * 32 * 8 * 128 * 4 + 64 * 32 * 8 * 2 * 4
+    assert need <= ws <= need + 3 * 256 and ws % 256 == 0
+
+
+def test_layout_validation(L):
+    assert ok.layout_check(ok.Layout(8, 10)) == ok.OK
+    assert ok.layout_check(ok.Layout(0, 10)) == ok.ERR_INVALID_ARG
+    assert ok.layout_check(ok.Layout(8, 0)) == ok.ERR_INVALID_ARG
+    assert ok.layout_check(ok.Layout(8, 10, head_dim=64)) == ok.ERR_UNSUPPORTED
+    assert ok.layout_check(ok.Layout(8, 10, page_size=16)) == ok.ERR_UNSUPPORTED
+    assert ok.layout_check(ok.Layout(8, 10, group_size=64)) == ok.ERR_UNSUPPORTED
+    assert ok.layout_check(ok.Layout(8, 10, group_size=48)) == ok.ERR_INVALID_ARG   # G does not divide d
+    assert L.oscar_layout_check(None) == ok.ERR_INVALID_ARG
+    assert ok.page_bytes(ok.Layout(0, 10)) == 0
+
+
+def _append(L, lay, n_tok=4, clip_k=0.9, clip_v=0.9, pages=FAKE, k=FAKE, slots=FAKE):
+    return L.oscar_kv_append(ctypes.byref(lay), pages, k, FAKE, slots, n_tok, FAKE, FAKE,
+                             clip_k, clip_v, None)
+
+
+def test_append_rejects_invalid_arguments(L):
+    lay = ok.Layout(8, 10)
+    assert _append(L, lay, clip_k=0.0) == ok.ERR_INVALID_ARG
+    assert _append(L, lay, clip_v=1.5) == ok.ERR_INVALID_ARG
+    assert _append(L, lay, clip_k=float("nan")) == ok.ERR_INVALID_ARG
+    assert _append(L, lay, n_tok=-1) == ok.ERR_INVALID_ARG
+    assert _append(L, lay, pages=None) == ok.ERR_INVALID_ARG
+    assert _append(L, lay, slots=None) == ok.ERR_INVALID_ARG
+    assert _append(L, lay, k=ctypes.c_void_p(0x10001)) == ok.ERR_INVALID_ARG     # misaligned
+    assert _append(L, ok.Layout(8, 10, head_dim=256)) == ok.ERR_UNSUPPORTED
+    # zero tokens: nothing to do, nothing launched
+    assert _append(L, lay, n_tok=0, pages=None) == ok.OK
+
+
+def _decode(L, lay, B=2, Hq=32, mp=4, S=2, ws_bytes=1 << 30, out_dtype=0, sm=0.088,
+            ws=FAKE, q=FAKE):
+    return L.oscar_decode_attn(ctypes.byref(lay), FAKE, q, B, Hq, FAKE, mp, FAKE, FAKE, FAKE,
+                               sm, S, ws, ws_bytes, FAKE, out_dtype, None)
+
+
+def test_decode_rejects_invalid_arguments(L):
+    lay = ok.Layout(8, 10)
+    assert _decode(L, lay, Hq=30) == ok.ERR_INVALID_ARG          # Hq % Hkv
+    assert _decode(L, lay, Hq=8 * 17) == ok.ERR_UNSUPPORTED      # > 16 heads per kv-head
+    assert _decode(L, lay, B=0) == ok.ERR_INVALID_ARG
+    assert _decode(L, lay, S=-1) == ok.ERR_INVALID_ARG
+    assert _decode(L, lay, mp=0) == ok.ERR_INVALID_ARG
+    assert _decode(L, lay, out_dtype=7) == ok.ERR_INVALID_ARG
+    assert _decode(L, lay, sm=float("inf")) == ok.ERR_INVALID_ARG
+    assert _decode(L, lay, q=None) == ok.ERR_INVALID_ARG
+    assert _decode(L, lay, ws=ctypes.c_void_p(0x10010)) == ok.ERR_INVALID_ARG   # not 256-aligned
+    need = ok.decode_workspace_bytes(lay, 2, 32, 2)
+    assert _decode(L, lay, ws_bytes=need - 1) == ok.ERR_WORKSPACE_TOO_SMALL
+    assert _decode(L, ok.Layout(8, 10, page_size=32)) == ok.ERR_UNSUPPORTED
+    # default split count on an invalid layout reports the layout error
+    assert _decode(L, ok.Layout(0, 10), S=0) == ok.ERR_INVALID_ARG
+    assert L.oscar_bf16_decode_attn(ctypes.byref(lay), FAKE, FAKE, 2, 30, FAKE, 4, FAKE, 0.088,
+                                    2, FAKE, 1 << 30, FAKE, 0, None) == ok.ERR_INVALID_ARG
+
+
+def test_stage_entry_points_validate(L):
+    lay = ok.Layout(8, 10)
+    need = ok.decode_workspace_bytes(lay, 2, 32, 2)
+    assert L.oscar_decode_prepare(ctypes.byref(lay), FAKE, 2, 32, FAKE, 0.088, 2, FAKE,
+                                  need - 1, None) == ok.ERR_WORKSPACE_TOO_SMALL
+    assert L.oscar_decode_split(ctypes.byref(lay), None, 2, 32, FAKE, 4, FAKE, 2, FAKE, need,
+                                None) == ok.ERR_INVALID_ARG
+    assert L.oscar_decode_reduce(ctypes.byref(lay), 2, 32, FAKE, 2, FAKE, need, FAKE, 5,
+                                 None) == ok.ERR_INVALID_ARG
+
+
+def test_default_num_splits_bounds(L):
+    lay = ok.Layout(8, 10)
+    assert ok.default_num_splits(lay, 64, 32, 32768) >= 1
+    # never more splits than a quarter of the pages of the longest sequence
+    assert ok.default_num_splits(lay, 1, 32, 256) == 1
+    assert ok.default_num_splits(lay, 1, 32, 8192) <= 8192 // 64 // 4

@@ -1,0 +1,215 @@
+"""GPU parity of liboscar against the CPU oracle (same seeded inputs, every
+output element compared).  Sizes are chosen so the oracle finishes in seconds
+while spanning many 64-token pages, several splits and ragged tails."""
+import math
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import paper_2605_17757_amd as ok
+import workloads as W
+from helpers import (DECODE_TOL, Case, bits, compare_pools, gpu_append, gpu_decode, log,
+                     make_case, max_abs, oracle_append, oracle_decode)
+
+pytestmark = pytest.mark.gpu
+
+
+def _run_full(case: Case, num_splits: int = 0, check_bf16: bool = True):
+    log("case", case.cfg.name, "B", case.cfg.B, "Hq", case.cfg.Hq, "Hkv", case.cfg.Hkv,
+        "lens", list(case.cfg.lens[:4]), "splits", num_splits)
+    pool = gpu_append(case)
+    ora = oracle_append(case)
+    nd, nt = compare_pools(pool.cpu().numpy(), ora, case)
+    log("  append: differing bytes", nd, "tolerated near-boundary rows", nt)
+    ref = oracle_decode(case, ora)
+    out = gpu_decode(case, pool, num_splits)
+    err = max_abs(out, ref)
+    log("  decode max|err| = %.3g" % err)
+    assert err <= DECODE_TOL
+    if check_bf16:
+        outb = gpu_decode(case, pool, num_splits, out_dtype=torch.bfloat16)
+        assert torch.equal(outb.cpu(), out.cpu().to(torch.bfloat16))
+    return pool, ora, out
+
+
+def test_config0_tiny():
+    _run_full(make_case(W.config(0)))
+
+
+def test_config1_qwen3_4b_shape():
+    _run_full(make_case(W.config(1)))
+
+
+def test_config2_qwen3_8b_batch1():
+    _run_full(make_case(W.config(2, batch=1)))
+
+
+def test_config3_shape_reduced_batch_and_length():
+    # Qwen3-32B heads (64/8, GQA 8) at batch 3 and 2k-4k tokens
+    cfg = W.config(3, batch=3)
+    cfg.lens = np.array([4096, 2049, 3007], np.int32)
+    _run_full(make_case(cfg))
+
+
+def test_config4_shape_student_t_many_splits():
+    # 96/8 heads (GQA 12), Student-t keys, distinct rotations, >= 64 splits
+    cfg = W.config(4, batch=2)
+    cfg.lens = np.array([8192, 5000], np.int32)
+    _run_full(make_case(cfg), num_splits=64)
+
+
+def test_composed_rotation_hadamard_bitreversal():
+    cfg = W.config(1)
+    cfg.lens = np.array([3000], np.int32)
+    _run_full(make_case(cfg, compose=True))
+
+
+@pytest.mark.parametrize("g", [1, 2, 3, 4, 8, 12, 16])
+def test_gqa_ratios_and_ragged_lengths(g):
+    Hkv = 2
+    lens = [1, 63, 64, 65, 129, 700]
+    cfg = W.custom("gqa%d" % g, len(lens), g * Hkv, Hkv, lens, seed_index=70 + g,
+                   k_outliers=(5, 90), v_outliers=(17,))
+    _run_full(make_case(cfg), num_splits=3)
+
+
+def test_split_count_invariance():
+    cfg = W.config(1)
+    cfg.lens = np.array([5000], np.int32)
+    case = make_case(cfg)
+    pool = gpu_append(case)
+    ref = oracle_decode(case, oracle_append(case))
+    outs = []
+    for S in (1, 2, 3, 7, 20, 64, 79, 256):
+        out = gpu_decode(case, pool, S)
+        err = max_abs(out, ref)
+        log("splits", S, "max|err| %.3g" % err)
+        assert err <= DECODE_TOL
+        outs.append(out.cpu())
+    for o in outs[1:]:
+        assert max_abs(o, outs[0].numpy()) <= 1e-5
+
+
+def test_page_shuffle_invariance():
+    cfg = W.custom("shuffle", 2, 8, 2, [900, 333], seed_index=81)
+    case = make_case(cfg)
+    pool = gpu_append(case)
+    out = gpu_decode(case, pool, 4)
+    # move every page to a new position and remap the block table
+    bph = ok.page_bytes(case.layout)
+    perm = np.random.default_rng(5).permutation(case.num_pages)
+    moved = torch.empty_like(pool)
+    pv = pool.view(case.num_pages, bph)
+    mv = moved.view(case.num_pages, bph)
+    mv[torch.from_numpy(perm).cuda()] = pv
+    out2 = gpu_decode(case, moved, 4, table=perm[case.table].astype(np.int32))
+    assert torch.equal(out.cpu(), out2.cpu())
+
+
+def test_decode_stages_equal_single_call():
+    cfg = W.custom("stages", 3, 16, 4, [300, 64, 1000], seed_index=82)
+    case = make_case(cfg)
+    pool = gpu_append(case)
+    lay = case.layout
+    S = 5
+    ws = ok.alloc_workspace(lay, cfg.B, cfg.Hq, S)
+    out_a = gpu_decode(case, pool, S)
+    out_b = torch.empty_like(out_a)
+    q = case.q.cuda()
+    bt = torch.from_numpy(case.table).cuda()
+    sl = torch.from_numpy(cfg.lens).cuda()
+    Rk = torch.from_numpy(case.Rk).cuda()
+    Rv = torch.from_numpy(case.Rv).cuda()
+    ok.decode_prepare(lay, q, Rk, cfg.sm_scale, S, ws)
+    ok.decode_split(lay, pool, cfg.B, cfg.Hq, bt, sl, S, ws)
+    ok.decode_reduce(lay, cfg.B, cfg.Hq, Rv, S, ws, out_b)
+    torch.cuda.synchronize()
+    assert torch.equal(out_a.cpu(), out_b.cpu())
+
+
+def test_append_fuzz_edge_rows():
+    rng = np.random.default_rng(11)
+    Hkv, num_pages = 3, 40
+    cfg = W.custom("fuzz", 1, 3, Hkv, [1], seed_index=83, clip_k=0.5, clip_v=1.0)
+    n_tok = 777
+    slots = rng.permutation(num_pages * 64)[:n_tok].astype(np.int64)
+    x = rng.standard_normal((2, n_tok, Hkv, 128)).astype(np.float32)
+    x[:, :50] = 0.0                                      # all-zero rows (degenerate groups)
+    x[:, 50:100] = 3.25                                  # constant rows
+    x[:, 100:150] *= 1e4                                 # large magnitudes
+    x[:, 150:200] *= 1e-6                                # tiny magnitudes
+    df = 3.0
+    x[:, 200:400] = rng.standard_t(df, size=(2, 200, Hkv, 128))
+    x[:, 400:420, :, :40] = 0.0                          # partly zero rows
+    k = torch.from_numpy(W.f32_to_bf16_bits(x[0]).view(np.int16)).view(torch.bfloat16)
+    v = torch.from_numpy(W.f32_to_bf16_bits(x[1]).view(np.int16)).view(torch.bfloat16)
+    for compose in (False, True):
+        Rk = W.rotation(901, compose=compose)
+        Rv = W.rotation(902, compose=compose)
+        case = Case(cfg, Rk, Rv, np.zeros((1, 1), np.int32), num_pages, None, k, v, slots)
+        pool = gpu_append(case)
+        ora = oracle_append(case)
+        nd, nt = compare_pools(pool.cpu().numpy(), ora, case)
+        log("fuzz compose=%s differing bytes %d tolerated rows %d" % (compose, nd, nt))
+
+
+def test_append_only_touches_addressed_slots():
+    cfg = W.custom("touch", 1, 4, 2, [1], seed_index=84)
+    Rk, Rv = W.rotation(5), W.rotation(6)
+    slots = np.array([3, 64 + 17, 5 * 64 + 63], np.int64)
+    rng = np.random.default_rng(2)
+    x = rng.standard_normal((2, 3, 2, 128)).astype(np.float32)
+    k = torch.from_numpy(W.f32_to_bf16_bits(x[0]).view(np.int16)).view(torch.bfloat16)
+    v = torch.from_numpy(W.f32_to_bf16_bits(x[1]).view(np.int16)).view(torch.bfloat16)
+    case = Case(cfg, Rk, Rv, np.zeros((1, 1), np.int32), 8, None, k, v, slots)
+    pool = torch.full((ok.pool_bytes(case.layout),), 0xA5, dtype=torch.uint8, device="cuda")
+    gpu_append(case, pool)
+    ora = np.full(ok.pool_bytes(case.layout), 0xA5, np.uint8)
+    oracle.kv_append(ora, d=128, Hkv=2, P=64, G=32, k=bits(k), v=bits(v), slot_mapping=slots,
+                     Rk=Rk, Rv=Rv, clip_k=cfg.clip_k, clip_v=cfg.clip_v)
+    assert np.array_equal(pool.cpu().numpy(), ora)
+
+
+def test_bf16_baseline_parity():
+    cfg = W.custom("bf16base", 3, 24, 2, [1, 1000, 2500], seed_index=85, k_outliers=(3,))
+    case = make_case(cfg)
+    lay = case.layout
+    pool = torch.zeros(ok.bf16_pool_bytes(lay) // 2, dtype=torch.bfloat16, device="cuda")
+    ok.bf16_kv_append(lay, pool, case.k.cuda(), case.v.cuda(),
+                      torch.from_numpy(case.slots).cuda())
+    ora = np.zeros(ok.bf16_pool_bytes(lay) // 2, np.uint16)
+    oracle.bf16_append(ora, d=128, Hkv=2, P=64, k=bits(case.k), v=bits(case.v),
+                       slot_mapping=case.slots)
+    assert np.array_equal(bits(pool), ora)
+    ref = oracle.bf16_decode(ora, d=128, Hkv=2, P=64, q=bits(case.q), block_table=case.table,
+                             seq_lens=cfg.lens, sm_scale=cfg.sm_scale)
+    for S in (1, 6):
+        ws = ok.alloc_workspace(lay, cfg.B, cfg.Hq, S)
+        out = torch.empty(cfg.B, cfg.Hq, 128, dtype=torch.float32, device="cuda")
+        ok.bf16_decode_attn(lay, pool, case.q.cuda(), torch.from_numpy(case.table).cuda(),
+                            torch.from_numpy(cfg.lens).cuda(), cfg.sm_scale, S, ws, out)
+        torch.cuda.synchronize()
+        err = max_abs(out, ref)
+        log("bf16 baseline splits", S, "max|err| %.3g" % err)
+        assert err <= DECODE_TOL
+
+
+def test_append_zero_point_sign_and_hand_rows():
+    # R = I and rows whose group minimum is exactly 0 (z = -0/s must be stored
+    # as +0), all-zero groups (degenerate), and exactly representable groups.
+    cfg = W.custom("zeros", 1, 2, 2, [1], seed_index=86, clip_k=1.0, clip_v=1.0)
+    eye = np.eye(128, dtype=np.float32)
+    rows = np.zeros((2, 4, 2, 128), np.float32)
+    rows[:, 0, :, :32] = np.tile([0, 1, 2, 3], 8)          # min exactly 0
+    rows[:, 1, :, 32:64] = np.tile([-1.5, -0.5, 0.5, 1.5], 8)
+    rows[:, 2, :, 64:96] = -np.tile([0, 1, 2, 3], 8)        # max exactly 0
+    rows[:, 3] = np.linspace(-2, 2, 128)
+    k = torch.from_numpy(W.f32_to_bf16_bits(rows[0]).view(np.int16)).view(torch.bfloat16)
+    v = torch.from_numpy(W.f32_to_bf16_bits(rows[1]).view(np.int16)).view(torch.bfloat16)
+    slots = np.array([0, 65, 130, 7], np.int64)
+    case = Case(cfg, eye, eye, np.zeros((1, 1), np.int32), 3, None, k, v, slots)
+    pool = gpu_append(case)
+    ora = oracle_append(case)
+    assert np.array_equal(pool.cpu().numpy(), ora)
