@@ -28,6 +28,8 @@ SOURCES = {
     "oscar_host.hip": [],
     "append.hip": ["-ffp-contract=off"],
     "decode.hip": [],
+    # keep MFMA accumulators in VGPRs: the kernel shifts and reads them with VALU ops
+    "decode_mfma.hip": ["-mllvm", "-amdgpu-mfma-vgpr-form=1"],
     "bf16_decode.hip": [],
 }
 

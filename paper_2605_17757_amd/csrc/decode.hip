@@ -11,6 +11,7 @@
 //   q~ . Q(k~) = sum_g s_g (sum_{c in g} q~_c code_c - z_g sum_{c in g} q~_c).
 // Scores are kept in log2 units (q~ carries log2 e) so the softmax uses exp2.
 #include <hip/hip_fp16.h>
+#include <stdlib.h>
 
 #include "internal.h"
 
@@ -364,6 +365,13 @@ hipError_t launch_decode_split(const uint8_t* pages, int Hkv, int B, int Hq,
                                const int32_t* block_table, int max_pages,
                                const int32_t* seq_lens, int num_splits, const float* qt,
                                float* part_o, float* part_ml, hipStream_t st) {
+  static const bool use_v0 = [] {
+    const char* e = getenv("OSCAR_SPLIT_KERNEL");
+    return e && e[0] == 'v' && e[1] == '0';
+  }();
+  if (!use_v0)
+    return launch_decode_split_mfma(pages, Hkv, B, Hq, block_table, max_pages, seq_lens,
+                                    num_splits, qt, part_o, part_ml, st);
   const int g = Hq / Hkv;
   if (g <= 4)
     return launch_split_nh<4>(pages, Hkv, B, Hq, block_table, max_pages, seq_lens, num_splits,

@@ -105,10 +105,13 @@ int32_t oscar_default_num_splits(const oscar_layout* L, int32_t B, int32_t Hq,
                                  int32_t max_seq_len) {
   if (check_layout(L) != OSCAR_OK || B < 1 || Hq < 1 || max_seq_len < 1) return 1;
   const int64_t pages = (max_seq_len + L->page_size - 1) / L->page_size;
-  const int64_t target_blocks = 4LL * device_cus();
-  const int64_t pairs = (int64_t)B * L->num_kv_heads;
-  int64_t s = (target_blocks + pairs - 1) / pairs;
-  int64_t cap = pages / 4;  // keep at least one page per wave of a split
+  // one wave per (split, kv-head, sequence, 4 query heads); aim for 8 waves per
+  // compute unit
+  const int64_t target_waves = 8LL * device_cus();
+  const int64_t chunks = (Hq % L->num_kv_heads == 0) ? (Hq / L->num_kv_heads + 3) / 4 : 1;
+  const int64_t pairs = (int64_t)B * L->num_kv_heads * chunks;
+  int64_t s = (target_waves + pairs - 1) / pairs;
+  int64_t cap = pages / 2;  // at least two pages per split
   if (cap < 1) cap = 1;
   if (s > cap) s = cap;
   if (s < 1) s = 1;

@@ -127,6 +127,6 @@ def test_stage_entry_points_validate(L):
 def test_default_num_splits_bounds(L):
     lay = ok.Layout(8, 10)
     assert ok.default_num_splits(lay, 64, 32, 32768) >= 1
-    # never more splits than a quarter of the pages of the longest sequence
-    assert ok.default_num_splits(lay, 1, 32, 256) == 1
-    assert ok.default_num_splits(lay, 1, 32, 8192) <= 8192 // 64 // 4
+    # never fewer than two pages per split
+    assert ok.default_num_splits(lay, 1, 32, 128) == 1
+    assert ok.default_num_splits(lay, 1, 32, 8192) <= 8192 // 64 // 2

