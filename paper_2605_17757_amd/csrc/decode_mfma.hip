@@ -110,15 +110,25 @@ __device__ inline float quad_max(float x) {
   x = fmaxf(x, __int_as_float(__builtin_amdgcn_update_dpp(0, v, 0x4E, 0xF, 0xF, false)));
   return x;
 }
-__device__ inline float rows_max(float x) {  // over lanes l, l^16, l^32, l^48
-  x = fmaxf(x, __shfl_xor(x, 16, 64));
-  return fmaxf(x, __shfl_xor(x, 32, 64));
+// Reductions over lanes l, l^16, l^32, l^48 with the gfx950 row-swap permutes
+// (VALU only, no LDS round trip): swapping a value with itself across the wave
+// halves / odd-even rows leaves x[l] and x[l^32] (then x[l^16]) in the two outputs.
+__device__ inline float rows_max(float x) {
+  uint32_t u = __float_as_uint(x);
+  auto a = __builtin_amdgcn_permlane32_swap(u, u, false, false);
+  x = fmaxf(__uint_as_float(a[0]), __uint_as_float(a[1]));
+  u = __float_as_uint(x);
+  auto b = __builtin_amdgcn_permlane16_swap(u, u, false, false);
+  return fmaxf(__uint_as_float(b[0]), __uint_as_float(b[1]));
 }
 __device__ inline float rows_sum(float x) {
-  x += __shfl_xor(x, 16, 64);
-  return x + __shfl_xor(x, 32, 64);
+  uint32_t u = __float_as_uint(x);
+  auto a = __builtin_amdgcn_permlane32_swap(u, u, false, false);
+  x = __uint_as_float(a[0]) + __uint_as_float(a[1]);
+  u = __float_as_uint(x);
+  auto b = __builtin_amdgcn_permlane16_swap(u, u, false, false);
+  return __uint_as_float(b[0]) + __uint_as_float(b[1]);
 }
-
 // Pack byte `sel` (0..3) of four words into one dword (bytes in order a, b, c, d).
 __device__ inline uint32_t pack4(uint32_t a, uint32_t b, uint32_t c, uint32_t d, uint32_t sel) {
   const uint32_t lo2 = 0x0c0c0400u + sel * 0x00000101u;  // [x.sel, y.sel, 0, 0]
