@@ -13,31 +13,34 @@
 // The integer parts are int8 matrix products:
 //   * q~ of a head is scaled to a 24-bit integer (q_int = rne(q~ * Q / max|q~|),
 //     Q = 8355000) and split into three signed int8 digits,
-//     q_int = 65536 d2 + 256 d1 + d0; the codes are int8 0..3.  Per 16-token tile
-//     the products codes x d_j go to separate accumulators, combined as
+//     q_int = 65536 d2 + 256 d1 + d0; the codes are int8 0..3.  The products of
+//     the codes with each digit go to separate accumulators, combined as
 //     ((a_2 << 8) + a_1) << 8 + a_0, exact in int32 (|.| <= 32 * 3 * Q < 2^31).
-//   * w of a head on one page is scaled to [0, Q] (scale p_max * max s_v of the
-//     page) and split the same way; the V codes are the other operand
-//     (|.| <= 64 * 3 * Q < 2^31).
+//   * w of a (head, group) row on one page is scaled to [0, Q] (scale: the page's
+//     p_max of the head times the largest V scale of the group) and split the
+//     same way; the V codes are the other operand (|.| <= 64 * 3 * Q < 2^31).
 // The products are exact, so the approximations are the 24-bit quantization of
-// q~ and of w (relative 2^-24 of the head's largest value) and fp32
-// accumulation.  (With 16-bit scaling the error reached 1.4e-3 on outputs of
-// magnitude ~30; 24 bits keeps it near 1e-5.)
+// q~ and of w (relative 2^-24 of the largest value) and fp32 accumulation.
+//
+// Data path.  Each page-head block (6144 B) is read with six coalesced 16-byte
+// loads per lane into registers (issued one page ahead) and stored to a per-wave
+// LDS copy, from which every lane reads the operands of its role.  In the LDS
+// copy every 8 16-byte chunks of the K-code region are followed by one chunk of
+// padding, which spreads the per-token reads of the score operands over the banks.
 //
 // Lane roles (l = lane, lo = l & 15, hi = l >> 4), MFMA 16x16x64 layout: A row =
 // lo, B column = lo, k-slots (hi, element), D (row 4*hi + i, column lo):
-//   score tile u (u = 0..3): MFMA row r <-> token 16*(r>>2) + 4u + (r&3);
-//     A operand lane l = K codes of token 16*(lo>>2) + 4u + (lo&3), dwords hi
-//     (instruction X=0, groups 0/1) and 4+hi (X=1, groups 2/3), expanded as
-//     M_j = (x >> 2j) & 0x03030303 (element 4j+b <-> channel 16w + 4b + j);
-//     B column lo = (head lo>>2, group lo&3), zero outside that group;
-//     D lane l holds (head lo>>2, group lo&3) for tokens 16*hi + 4u + i.
-//   after a sum over the 4 group lanes, lane l holds the scores of head lo>>2
-//   for its 16 tokens 16*hi + (0..15): exactly the k-slots of the P.V A operand
-//   row lo = (head, group) -- no data movement between softmax and P.V.
-//   P.V tile (set S, f): B column lo = channel 4*(16S + lo) + f, V codes of quad
-//     16S + lo, tokens 16*hi + (0..15) (quad-major V layout: one 16-byte load);
-//     D lane l, register 2S + (lo>>3) = (head hi, group of the column).
+//   scores, tile u (u = 0..3): A = q digits, row (head lo>>2, group lo&3), zero
+//     outside that group; B = K codes of token 4*lo + u (code dword hi for
+//     instruction X=0, 4+hi for X=1), expanded as M_j = (x >> 2j) & 0x03030303
+//     (element 4j+b <-> channel 16w + 4b + j);  D lane l, register i = (head hi,
+//     group i) of token 4*lo + u, so the sum over groups stays inside the lane.
+//   p (head hi, tokens 4*lo + u) goes through LDS to the P.V operand layout.
+//   P.V, tile (G, F) (G = 0..3, F = 0..1): A = w digits, row (head lo>>2, group
+//     lo&3), k = tokens 16*hi + (0..15); B column lo = channel
+//     32G + 4(lo&7) + 2F + (lo>>3) (all 16 columns in group G);  D lane l,
+//     register G = (head hi, group G) at that channel: the useful register index is
+//     the same in every lane.
 #include <hip/hip_fp16.h>
 
 #include "internal.h"
@@ -47,9 +50,17 @@ namespace {
 
 typedef int v4i __attribute__((ext_vector_type(4)));
 
-constexpr float kQMax = 8355000.0f;       // keeps the top digit of a 3-digit split in int8
+constexpr float kQMax = 8355000.0f;        // 3-digit split keeps the top digit in int8
 constexpr float kMagic = 8388608.0f;       // 2^23: x + 2^23 (0 <= x < 2^23) has x in its mantissa
+constexpr float kDigitBias = 32896.0f;     // 128 + 128 * 256 (offset of the two low digits)
 constexpr int kNDig = 3;                   // int8 digits per scaled value (most significant first)
+constexpr int kChunks = kBlockBytes / 16;  // 384 16-byte chunks per page-head block
+constexpr int kSlots = kChunks + 16;       // LDS copy: 16 padding chunks in the K-code region
+// byte offsets of the regions in the LDS copy
+constexpr int kLdsKCodes = 0;              // chunk c < 128 at slot c + (c >> 3)
+constexpr int kLdsVCodes = 144 * 16;       // chunk c >= 128 at slot c + 16
+constexpr int kLdsKSz = (256 + 16) * 16;
+constexpr int kLdsVSz = (320 + 16) * 16;
 
 __device__ inline v4i mfma(v4i a, v4i b, v4i c) {
   return __builtin_amdgcn_mfma_i32_16x16x64_i8(a, b, c, 0, 0, 0);
@@ -92,27 +103,32 @@ __device__ inline uint32_t max_u16x2(uint32_t a, uint32_t b) {
 }
 
 __device__ inline float h_lo(uint32_t w) { return __half2float(__ushort_as_half((uint16_t)(w & 0xffffu))); }
-__device__ inline float h_hi(uint32_t w) { return __half2float(__ushort_as_half((uint16_t)(w >> 16))); }
 __device__ inline uint32_t comp(uint4 v, int i) { return i == 0 ? v.x : i == 1 ? v.y : i == 2 ? v.z : v.w; }
+__device__ inline float compf(float4 v, int i) { return i == 0 ? v.x : i == 1 ? v.y : i == 2 ? v.z : v.w; }
 
-// sum over the 4 lanes of a quad (xor 1, xor 2) with DPP
-__device__ inline float quad_sum(float x) {
-  int v = __float_as_int(x);
-  x += __int_as_float(__builtin_amdgcn_update_dpp(0, v, 0xB1, 0xF, 0xF, false));  // [1,0,3,2]
-  v = __float_as_int(x);
-  x += __int_as_float(__builtin_amdgcn_update_dpp(0, v, 0x4E, 0xF, 0xF, false));  // [2,3,0,1]
+// Max / sum over the 16 lanes of a row (quad swaps, then row rotations by 4 and 8).
+__device__ inline float row16_max(float x) {
+  x = fmaxf(x, __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(x), 0xB1, 0xF, 0xF, false)));
+  x = fmaxf(x, __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(x), 0x4E, 0xF, 0xF, false)));
+  x = fmaxf(x, __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(x), 0x124, 0xF, 0xF, false)));
+  x = fmaxf(x, __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(x), 0x128, 0xF, 0xF, false)));
+  return x;
+}
+__device__ inline float row16_sum(float x) {
+  x += __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(x), 0xB1, 0xF, 0xF, false));
+  x += __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(x), 0x4E, 0xF, 0xF, false));
+  x += __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(x), 0x124, 0xF, 0xF, false));
+  x += __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(x), 0x128, 0xF, 0xF, false));
   return x;
 }
 __device__ inline float quad_max(float x) {
-  int v = __float_as_int(x);
-  x = fmaxf(x, __int_as_float(__builtin_amdgcn_update_dpp(0, v, 0xB1, 0xF, 0xF, false)));
-  v = __float_as_int(x);
-  x = fmaxf(x, __int_as_float(__builtin_amdgcn_update_dpp(0, v, 0x4E, 0xF, 0xF, false)));
+  x = fmaxf(x, __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(x), 0xB1, 0xF, 0xF, false)));
+  x = fmaxf(x, __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(x), 0x4E, 0xF, 0xF, false)));
   return x;
 }
-// Reductions over lanes l, l^16, l^32, l^48 with the gfx950 row-swap permutes
-// (VALU only, no LDS round trip): swapping a value with itself across the wave
-// halves / odd-even rows leaves x[l] and x[l^32] (then x[l^16]) in the two outputs.
+// Reductions over lanes l, l^16, l^32, l^48 with the gfx950 row-swap permutes:
+// swapping a value with itself across the wave halves / odd-even rows leaves
+// x[l] and x[l^32] (then x[l^16]) in the two outputs.
 __device__ inline float rows_max(float x) {
   uint32_t u = __float_as_uint(x);
   auto a = __builtin_amdgcn_permlane32_swap(u, u, false, false);
@@ -129,13 +145,6 @@ __device__ inline float rows_sum(float x) {
   auto b = __builtin_amdgcn_permlane16_swap(u, u, false, false);
   return __uint_as_float(b[0]) + __uint_as_float(b[1]);
 }
-// Pack byte `sel` (0..3) of four words into one dword (bytes in order a, b, c, d).
-__device__ inline uint32_t pack4(uint32_t a, uint32_t b, uint32_t c, uint32_t d, uint32_t sel) {
-  const uint32_t lo2 = 0x0c0c0400u + sel * 0x00000101u;  // [x.sel, y.sel, 0, 0]
-  const uint32_t ab = __builtin_amdgcn_perm(b, a, lo2);
-  const uint32_t cd = __builtin_amdgcn_perm(d, c, lo2);
-  return __builtin_amdgcn_perm(cd, ab, 0x05040100u);
-}
 
 // ((a << 8) + b) << 8 + c for signed digit sums, in unsigned arithmetic (the
 // intermediate values may be negative; the result fits in int32).
@@ -143,153 +152,176 @@ __device__ inline int combine3(int a, int b, int c) {
   return (int)((((uint32_t)a << 8) + (uint32_t)b) * 256u + (uint32_t)c);
 }
 
-struct PageBuf {
-  uint32_t kx0[4], kx1[4];  // K code dwords for the score A operands, per tile
-  uint4 ksz[4];             // K (s,z) of tokens 16*hi + 4u + (0..3), group lo&3
-  uint4 vq[2];              // V codes, quads lo and 16+lo, tokens 16*hi + (0..15)
-  uint4 vsz[4];             // V (s,z), same tokens and group as ksz
+// Per-wave LDS: the page copy and the exchanges between lane roles.
+struct WaveLds {
+  uint4 page[kSlots];   // page-head block, K-code region padded
+  float4 p[4][16];      // softmax weights of the page, [head][token / 4]
+  float2 hs[4];         // (alpha, p_max) per head
+  float ws[16];         // P.V scale per (head, group); at the end, sum w z per (head, group)
+  float qs[16];         // sum of q_int per (head, group)
+  float sq[4];          // q scale per head
 };
 
-__device__ inline void load_page(PageBuf& pb, const uint8_t* __restrict__ blk, int lo, int hi) {
-#pragma unroll
-  for (int u = 0; u < 4; ++u) {
-    const int tok = 16 * (lo >> 2) + 4 * u + (lo & 3);
-    pb.kx0[u] = *reinterpret_cast<const uint32_t*>(blk + kOffKCodes + tok * 32 + 4 * hi);
-    pb.kx1[u] = *reinterpret_cast<const uint32_t*>(blk + kOffKCodes + tok * 32 + 16 + 4 * hi);
-  }
-  const int G = lo & 3;
-#pragma unroll
-  for (int u = 0; u < 4; ++u) {
-    pb.ksz[u] = *reinterpret_cast<const uint4*>(blk + kOffKSz + (G * kP + 16 * hi + 4 * u) * 4);
-    pb.vsz[u] = *reinterpret_cast<const uint4*>(blk + kOffVSz + (G * kP + 16 * hi + 4 * u) * 4);
-  }
-  pb.vq[0] = *reinterpret_cast<const uint4*>(blk + kOffVCodes + lo * kP + 16 * hi);
-  pb.vq[1] = *reinterpret_cast<const uint4*>(blk + kOffVCodes + (16 + lo) * kP + 16 * hi);
+typedef uint32_t u4 __attribute__((ext_vector_type(4)));
+
+struct Stage {  // chunks 64 i + lane of the next page, i = 0..5
+  u4 v0, v1, v2, v3, v4, v5;
+};
+
+__device__ inline void stage_load(Stage& s, const uint8_t* __restrict__ blk, int l) {
+  const u4* src = reinterpret_cast<const u4*>(blk) + l;
+  s.v0 = src[0];
+  s.v1 = src[64];
+  s.v2 = src[128];
+  s.v3 = src[192];
+  s.v4 = src[256];
+  s.v5 = src[320];
+}
+__device__ inline void stage_store(uint4* page, const Stage& s, int l) {
+  u4* dst = reinterpret_cast<u4*>(page);
+  const int a = l + (l >> 3);  // K-code chunks 0..127: slot c + (c >> 3)
+  dst[a] = s.v0;
+  dst[72 + a] = s.v1;
+  dst[144 + l] = s.v2;  // chunks >= 128: slot c + 16
+  dst[208 + l] = s.v3;
+  dst[272 + l] = s.v4;
+  dst[336 + l] = s.v5;
 }
 
 struct WaveState {
-  v4i bq[2][kNDig];     // query operands [instruction X][digit, most significant first]
-  float sq;             // q scale of head lo>>2
-  float qs;             // sum of q_int over group lo&3 of head lo>>2
-  float m;              // running max (log2 units), head lo>>2
-  float lsum;           // partial sum of p over this lane's tokens, head lo>>2
-  float zacc;           // partial sum of w * z_v, (head lo>>2, group lo&3)
-  float of[8];          // unnormalized o~ of head hi at this lane's 8 channels
+  v4i bq[2][kNDig];     // query digits, A operand [instruction X][digit]
+  float qs[4];          // sum of q_int over group i of head hi
+  float sq;             // q scale of head hi
+  float m;              // running max (log2 units), head hi
+  float lsum;           // partial sum of p over this lane's tokens, head hi
+  float zacc;           // partial sum of w z_v, (head lo>>2, group lo&3)
+  float of[8];          // unnormalized o~ of head hi, tile (G, F) at of[2G + F]
 };
 
 // FULL: all 64 token slots of the page are in the sequence (every page but
 // possibly the sequence's last); otherwise slots >= ntok are masked.
 template <bool FULL>
-__device__ inline void compute_page(WaveState& st, const PageBuf& pb, int ntok, int lo, int hi) {
-  // ---- scores ----
-  // One accumulator per digit of q_int (independent MFMAs), combined as
-  // (a_2 << 16) + (a_1 << 8) + a_0 for the most to least significant digit.
-  float S[4][4];
+__device__ inline void compute_page(WaveState& st, WaveLds& L, int ntok, int lo, int hi) {
+  const char* pb = reinterpret_cast<const char*>(L.page);
+  // ---- scores of head hi for tokens 4*lo + u ----
+  const uint32_t* kc = reinterpret_cast<const uint32_t*>(pb + kLdsKCodes + 144 * lo + 4 * hi);
+  uint4 ksz[4];  // (s, z) of tokens 4*lo + (0..3), group i
+#pragma unroll
+  for (int i = 0; i < 4; ++i) ksz[i] = *reinterpret_cast<const uint4*>(pb + kLdsKSz + 256 * i + 16 * lo);
+  float S[4];
 #pragma unroll
   for (int u = 0; u < 4; ++u) {
-    const v4i a0 = expand2(pb.kx0[u]);
-    const v4i a1 = expand2(pb.kx1[u]);
+    const v4i b0 = expand2(kc[8 * u]);
+    const v4i b1 = expand2(kc[8 * u + 4]);
     v4i d[kNDig];
 #pragma unroll
     for (int dg = 0; dg < kNDig; ++dg) {
       const v4i z4 = {0, 0, 0, 0};
-      d[dg] = mfma(a1, st.bq[1][dg], mfma(a0, st.bq[0][dg], z4));
+      d[dg] = mfma(st.bq[1][dg], b1, mfma(st.bq[0][dg], b0, z4));
     }
+    float acc = 0.0f;
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
       const int t = combine3(d[0][i], d[1][i], d[2][i]);
-      const uint32_t sz = comp(pb.ksz[u], i);
+      const uint32_t sz = comp(ksz[i], u);
       // s * (acc - z * sum q_int) with s, z read from the packed binary16 pair
-      const float part = mix_lo(sz, mix_nhi(sz, st.qs, (float)t), 0.0f);
-      S[u][i] = quad_sum(part);
+      acc = mix_lo(sz, mix_nhi(sz, st.qs[i], (float)t), acc);
     }
+    S[u] = acc;
   }
-  // ---- online softmax (head lo>>2, tokens 16*hi + 4u + i) ----
-  const int tbase = 16 * hi;
-  auto valid = [&](int u, int i) { return FULL || tbase + 4 * u + i < ntok; };
+  // ---- online softmax, head hi ----
+  auto valid = [&](int u) { return FULL || 4 * lo + u < ntok; };
   float mx = -INFINITY;
 #pragma unroll
   for (int u = 0; u < 4; ++u)
-#pragma unroll
-    for (int i = 0; i < 4; ++i)
-      if (valid(u, i)) mx = fmaxf(mx, S[u][i]);
-  mx = rows_max(mx) * st.sq;  // sq > 0
+    if (valid(u)) mx = fmaxf(mx, S[u]);
+  mx = row16_max(mx) * st.sq;  // sq > 0; at least one valid token per page
   const float mn = fmaxf(st.m, mx);
   const float alpha = ex2(st.m - mn);  // m = -inf on the first page -> 0
   const float pmax = ex2(mx - mn);
+  float p[4];
   float ls = 0.0f;
 #pragma unroll
-  for (int u = 0; u < 4; ++u)
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      const float p = valid(u, i) ? ex2(fmaf(st.sq, S[u][i], -mn)) : 0.0f;
-      S[u][i] = p;
-      ls += p;
-    }
+  for (int u = 0; u < 4; ++u) {
+    p[u] = valid(u) ? ex2(fmaf(st.sq, S[u], -mn)) : 0.0f;
+    ls += p[u];
+  }
   st.lsum = fmaf(st.lsum, alpha, ls);
   st.m = mn;
-  // ---- P.V weights w = p * s_v, quantized per head to three int8 digits ----
-  // largest V scale of the page: scales are positive binary16, so their bit
-  // patterns order like their values (packed u16 max; the high halves are ignored)
+  L.p[hi][lo] = make_float4(p[0], p[1], p[2], p[3]);
+  L.hs[hi] = make_float2(alpha, pmax);  // every lane of the row writes the same value
+
+  // ---- P.V weights w = p * s_v of row (head lo>>2, group lo&3), tokens 16*hi + e ----
+  const int wh = lo >> 2, wg = lo & 3;
+  const float2 hsw = L.hs[wh];
+  float4 pw[4];
+  uint4 vz[4];
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    pw[j] = L.p[wh][4 * hi + j];
+    vz[j] = *reinterpret_cast<const uint4*>(pb + kLdsVSz + 256 * wg + 64 * hi + 16 * j);
+  }
+  uint32_t sz[16];
+#pragma unroll
+  for (int e = 0; e < 16; ++e) {
+    sz[e] = comp(vz[e >> 2], e & 3);
+    if (!FULL && 16 * hi + e >= ntok) sz[e] = 0u;  // (0, 0): w = 0, z = 0
+  }
+  // largest V scale of the group on this page: scales are positive binary16, so
+  // their bit patterns order like their values (packed u16 max; high halves ignored)
   uint32_t smax = 0;
 #pragma unroll
-  for (int u = 0; u < 4; ++u)
-#pragma unroll
-    for (int i = 0; i < 4; ++i)
-      smax = max_u16x2(smax, valid(u, i) ? comp(pb.vsz[u], i) : 0u);
-  const float svmax = rows_max(quad_max(h_lo(smax)));  // whole page, all groups
-  const float sig = pmax * svmax;  // >= every w of this head on this page
-  const float inv = sig > 0.0f ? kQMax / sig : 0.0f;
-  const float wscale = sig * (1.0f / kQMax);
+  for (int e = 0; e < 16; ++e) smax = max_u16x2(smax, sz[e]);
+  const float svmax = rows_max(h_lo(smax));
+  const float sig = hsw.y * svmax;  // >= every w of the row on this page
+  const float inv = sig > 0.0f ? kQMax * __builtin_amdgcn_rcpf(sig) : 0.0f;
+  L.ws[lo] = sig * (1.0f / kQMax);
   float zp = 0.0f;
-  uint32_t wd[kNDig][4];
-#pragma unroll
-  for (int u = 0; u < 4; ++u) {
-    uint32_t b0[4], b1[4], b2[4];
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      const uint32_t sz = valid(u, i) ? comp(pb.vsz[u], i) : 0u;  // (0, 0): w = 0, z = 0
-      const float w = mix_lo(sz, S[u][i], 0.0f);
-      // mantissa of f = rne(w * inv) = k in [0, Q]; signed digits of k:
-      // d0 = byte 0 of k, d1 = byte 1 of k + 128, d2 = byte 2 of k + 32896
-      const float f = fmaf(w, inv, kMagic);
-      b0[i] = __float_as_uint(f);
-      b1[i] = b0[i] + 128u;
-      b2[i] = b0[i] + 32896u;
-      zp = mix_hi(sz, w, zp);  // unquantized w: differs from the quantized by <= 2^-24 sig
-    }
-    wd[0][u] = pack4(b2[0], b2[1], b2[2], b2[3], 2);
-    wd[1][u] = pack4(b1[0], b1[1], b1[2], b1[3], 1);
-    wd[2][u] = pack4(b0[0], b0[1], b0[2], b0[3], 0);
-  }
   v4i aw[kNDig];
 #pragma unroll
-  for (int dg = 0; dg < kNDig; ++dg)
-    aw[dg] = v4i{(int)wd[dg][0], (int)wd[dg][1], (int)wd[dg][2], (int)wd[dg][3]};
-  st.zacc = fmaf(st.zacc, alpha, zp);
-  // ---- P.V on the matrix cores ----
-  // per-head factors of head hi for the accumulators of this lane
-  const float ascale = __shfl(alpha, 4 * hi, 64);
-  const float awsc = __shfl(wscale, 4 * hi, 64);
-  const bool upper = (lo >> 3) != 0;
+  for (int j = 0; j < 4; ++j) {
+    uint32_t f[4];
 #pragma unroll
-  for (int S_ = 0; S_ < 2; ++S_) {
-    const uint4 d = pb.vq[S_];
+    for (int b = 0; b < 4; ++b) {
+      const int e = 4 * j + b;
+      const float w = mix_lo(sz[e], compf(pw[j], b), 0.0f);
+      // mantissa of rne(w * inv) + 2^23 + 32896 = k + 32896, k in [0, Q]:
+      // k = 65536 d2 + 256 d1 + d0 with d0, d1 = (bytes 0, 1) ^ 0x80, d2 = byte 2
+      f[b] = __float_as_uint(fmaf(w, inv, kMagic + kDigitBias));
+      zp = mix_hi(sz[e], w, zp);  // unquantized w: differs from the quantized by <= 2^-24 sig
+    }
+    const uint32_t t01 = __builtin_amdgcn_perm(f[1], f[0], 0x05010400u) ^ 0x80808080u;  // [f0.0 f1.0 f0.1 f1.1]
+    const uint32_t t23 = __builtin_amdgcn_perm(f[3], f[2], 0x05010400u) ^ 0x80808080u;
+    const uint32_t h01 = __builtin_amdgcn_perm(f[1], f[0], 0x0c0c0602u);                // [f0.2 f1.2 0 0]
+    const uint32_t h23 = __builtin_amdgcn_perm(f[3], f[2], 0x0c0c0602u);
+    aw[2][j] = (int)__builtin_amdgcn_perm(t23, t01, 0x05040100u);
+    aw[1][j] = (int)__builtin_amdgcn_perm(t23, t01, 0x07060302u);
+    aw[0][j] = (int)__builtin_amdgcn_perm(h23, h01, 0x05040100u);
+  }
+  st.zacc = fmaf(st.zacc, hsw.x, zp);
+
+  // ---- P.V on the matrix cores: lane (channel column, head hi) ----
+  const float4 ws = *reinterpret_cast<const float4*>(&L.ws[4 * hi]);
+  const uint32_t sh = 2u * (uint32_t)(lo >> 3);
+  const char* vb = pb + kLdsVCodes + 64 * (lo & 7) + 16 * hi;
 #pragma unroll
-    for (int f = 0; f < 4; ++f) {
+  for (int G = 0; G < 4; ++G) {
+    const uint4 x = *reinterpret_cast<const uint4*>(vb + 512 * G);  // quad 8G + (lo&7)
+    const uint4 y = make_uint4(x.x >> sh, x.y >> sh, x.z >> sh, x.w >> sh);
+#pragma unroll
+    for (int F = 0; F < 2; ++F) {
       const uint32_t msk = 0x03030303u;
-      const v4i bv = {(int)((d.x >> (2 * f)) & msk), (int)((d.y >> (2 * f)) & msk),
-                      (int)((d.z >> (2 * f)) & msk), (int)((d.w >> (2 * f)) & msk)};
+      const v4i bv = {(int)((y.x >> (4 * F)) & msk), (int)((y.y >> (4 * F)) & msk),
+                      (int)((y.z >> (4 * F)) & msk), (int)((y.w >> (4 * F)) & msk)};
       int e[kNDig];
 #pragma unroll
       for (int dg = 0; dg < kNDig; ++dg) {
         const v4i z4 = {0, 0, 0, 0};
-        const v4i acc = mfma(aw[dg], bv, z4);
-        e[dg] = upper ? acc[2 * S_ + 1] : acc[2 * S_];  // row (head hi, group of column)
+        e[dg] = mfma(aw[dg], bv, z4)[G];  // row (head hi, group G)
       }
-      const int useful = combine3(e[0], e[1], e[2]);
-      float& o = st.of[S_ * 4 + f];
-      o = fmaf((float)useful, awsc, o * ascale);
+      const int t = combine3(e[0], e[1], e[2]);
+      float& o = st.of[2 * G + F];
+      o = fmaf((float)t, compf(ws, G), o * alpha);
     }
   }
 }
@@ -297,11 +329,12 @@ __device__ inline void compute_page(WaveState& st, const PageBuf& pb, int ntok, 
 // Grid: 1-D, ceil(S*Hkv*B / 8) * 8 * nch workgroups of one wave.  Workgroup id
 // -> (xcd = id % 8, slot = id / 8); chunk = slot % nch; item = (slot / nch) * 8
 // + xcd; item -> (split, kv-head, sequence).  Items beyond S*Hkv*B exit.
-__global__ __launch_bounds__(64) void split_mfma_kernel(
+__global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(4, 4))) void split_mfma_kernel(
     const uint8_t* __restrict__ pages, int Hkv, int Hq, const int32_t* __restrict__ block_table,
     int max_pages, const int32_t* __restrict__ seq_lens, int num_splits, int pages_per_split,
     int B, const float* __restrict__ qt, float* __restrict__ part_o,
     float* __restrict__ part_ml) {
+  __shared__ WaveLds L;
   const int g = Hq / Hkv;
   const int nch = (g + 3) >> 2;
   const int xcd = blockIdx.x & 7;
@@ -313,20 +346,24 @@ __global__ __launch_bounds__(64) void split_mfma_kernel(
   const int kvh = (int)((item / num_splits) % Hkv);
   const int b = (int)(item / ((int64_t)num_splits * Hkv));
   const int l = threadIdx.x, lo = l & 15, hi = l >> 4;
-  const int hq = lo >> 2, G = lo & 3;
   const int len = seq_lens[b];
   const int npg = (len + kP - 1) / kP;
   const int p0 = s * pages_per_split;
   const int p1 = min(npg, p0 + pages_per_split);
 
+  const int32_t* __restrict__ bt = block_table + (size_t)b * max_pages;
+  const uint8_t* __restrict__ base = pages + (size_t)kvh * kBlockBytes;
+  const size_t page_stride = (size_t)Hkv * kBlockBytes;
+
   WaveState st;
   // ---- query operands: q_int = rne(q~ * Q / max|q~|), three int8 digits ----
-  // Lane (head hq, group G, k-group hi) owns channels 32G + 16(hi&1) + 0..15 when
-  // (hi>>1) == (G&1), for instruction X = G>>1; it is zero otherwise.
+  // Lane (head lo>>2, group G = lo&3, k-group hi) owns channels 32G + 16(hi&1) +
+  // 0..15 when (hi>>1) == (G&1), for instruction X = G>>1; it is zero otherwise.
   {
+    const int G = lo & 3;
     const bool owns = (hi >> 1) == (G & 1);
     const int cbase = 32 * G + 16 * (hi & 1);
-    const int hloc = 4 * chunk + hq;
+    const int hloc = 4 * chunk + (lo >> 2);
     float qv[16];
     float amax = 0.0f;
 #pragma unroll
@@ -344,7 +381,7 @@ __global__ __launch_bounds__(64) void split_mfma_kernel(
     }
     amax = rows_max(quad_max(amax));  // all 128 channels of the head
     const float inv = amax > 0.0f ? kQMax / amax : 0.0f;
-    st.sq = amax > 0.0f ? amax * (1.0f / kQMax) : 1.0f;
+    const float sq = amax > 0.0f ? amax * (1.0f / kQMax) : 1.0f;
     int qi[16];
     int qsum = 0;
 #pragma unroll
@@ -384,7 +421,11 @@ __global__ __launch_bounds__(64) void split_mfma_kernel(
     // sum over the group's 32 channels (two owning lanes), exact in int
     qsum += __shfl_xor(qsum, 16, 64);
     qsum += __shfl_xor(qsum, 32, 64);
-    st.qs = (float)qsum;
+    L.qs[lo] = (float)qsum;  // lanes of equal lo write equal values
+    L.sq[lo >> 2] = sq;
+    const float4 q4 = *reinterpret_cast<const float4*>(&L.qs[4 * hi]);
+    st.qs[0] = q4.x; st.qs[1] = q4.y; st.qs[2] = q4.z; st.qs[3] = q4.w;
+    st.sq = L.sq[hi];
     st.m = -INFINITY;
     st.lsum = 0.0f;
     st.zacc = 0.0f;
@@ -392,51 +433,42 @@ __global__ __launch_bounds__(64) void split_mfma_kernel(
     for (int k = 0; k < 8; ++k) st.of[k] = 0.0f;
   }
 
-  const int32_t* __restrict__ bt = block_table + (size_t)b * max_pages;
-  const uint8_t* __restrict__ base = pages + (size_t)kvh * kBlockBytes;
-  const size_t page_stride = (size_t)Hkv * kBlockBytes;
+  Stage sg;
+  if (p0 < p1) stage_load(sg, base + (size_t)bt[p0] * page_stride, l);
   // pages [p0, pf) are full; page pf (if < p1) is the sequence's partial last page
-  const int pf = (p1 == npg && (len & (kP - 1)) != 0) ? p1 - 1 : p1;
-  PageBuf pa, pb;
-  if (p0 < p1) load_page(pa, base + (size_t)bt[p0] * page_stride, lo, hi);
-  int pg = p0;
-  for (; pg + 1 < pf; pg += 2) {
-    load_page(pb, base + (size_t)bt[pg + 1] * page_stride, lo, hi);
-    compute_page<true>(st, pa, kP, lo, hi);
-    if (pg + 2 < p1) load_page(pa, base + (size_t)bt[pg + 2] * page_stride, lo, hi);
-    compute_page<true>(st, pb, kP, lo, hi);
+  const int pf = (p0 < p1 && p1 == npg && (len & (kP - 1)) != 0) ? p1 - 1 : p1;
+  int nxt = (p0 < p1) ? bt[min(p0 + 1, p1 - 1)] : 0;
+  for (int pg = p0; pg < pf; ++pg) {
+    stage_store(L.page, sg, l);
+    stage_load(sg, base + (size_t)nxt * page_stride, l);  // page pg+1 (the last page again at the end)
+    nxt = bt[min(pg + 2, p1 - 1)];
+    compute_page<true>(st, L, kP, lo, hi);
   }
-  if (pg < pf) {  // one full page left; pa holds it
-    if (pg + 1 < p1) load_page(pb, base + (size_t)bt[pg + 1] * page_stride, lo, hi);
-    compute_page<true>(st, pa, kP, lo, hi);
-    ++pg;
-    if (pg < p1) compute_page<false>(st, pb, len - pg * kP, lo, hi);
-  } else if (pg < p1) {  // only the partial page left; pa holds it
-    compute_page<false>(st, pa, len - pg * kP, lo, hi);
+  if (pf < p1) {  // the partial last page; the stage holds it
+    stage_store(L.page, sg, l);
+    compute_page<false>(st, L, len - pf * kP, lo, hi);
   }
 
   // ---- write the split's partial state ----
-  const float ltot = rows_sum(st.lsum);            // head lo>>2
-  const float ztot = rows_sum(st.zacc);            // (head lo>>2, group lo&3)
-  const int hout = 4 * chunk + hi;                 // accumulator head of this lane
-  const float mh = __shfl(st.m, 4 * hi, 64);
-  const float lh = __shfl(ltot, 4 * hi, 64);
-  float zh2[2];
-#pragma unroll
-  for (int S_ = 0; S_ < 2; ++S_) zh2[S_] = __shfl(ztot, 4 * hi + 2 * S_ + (lo >> 3), 64);
-  if (hout >= g) return;  // padding head (every lane took part in the shuffles above)
+  const float ltot = row16_sum(st.lsum);  // head hi
+  const float ztot = rows_sum(st.zacc);   // (head lo>>2, group lo&3)
+  L.ws[lo] = ztot;                        // lanes of equal lo write equal values
+  const float4 zh = *reinterpret_cast<const float4*>(&L.ws[4 * hi]);
+  const int hout = 4 * chunk + hi;        // head of this lane's accumulators
+  if (hout >= g) return;                  // padding head
   const size_t row = ((size_t)b * Hq + kvh * g + hout) * num_splits + s;
+  const bool empty = st.m == -INFINITY;
 #pragma unroll
-  for (int S_ = 0; S_ < 2; ++S_) {
+  for (int G = 0; G < 4; ++G) {
 #pragma unroll
-    for (int f = 0; f < 4; ++f) {
-      const int ch = 4 * (16 * S_ + lo) + f;
-      part_o[row * kD + ch] = (mh == -INFINITY) ? 0.0f : st.of[S_ * 4 + f] - zh2[S_];
+    for (int F = 0; F < 2; ++F) {
+      const int ch = 32 * G + 4 * (lo & 7) + 2 * F + (lo >> 3);
+      part_o[row * kD + ch] = empty ? 0.0f : st.of[2 * G + F] - compf(zh, G);
     }
   }
   if (lo == 0) {
-    part_ml[row * 2] = mh;
-    part_ml[row * 2 + 1] = lh;
+    part_ml[row * 2] = st.m;
+    part_ml[row * 2 + 1] = ltot;
   }
 }
 
