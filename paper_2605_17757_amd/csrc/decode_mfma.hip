@@ -1,10 +1,9 @@
-// Split kernel of INT2 decode attention on the matrix cores (gfx950
-// v_mfma_i32_16x16x64_i8).  One wave per (split, kv-head, sequence, chunk of 4
-// query heads); the wave walks its pages (64 tokens each) and keeps the
-// online-softmax state of its 4 heads in registers.  Waves of the same (split,
-// kv-head, sequence) and different chunks get workgroup ids that are equal
-// modulo 8, so under round-robin dispatch over the 8 XCDs they share one XCD's
-// L2 for the page data they both read.
+// Split kernel of INT2 decode attention on the matrix cores (gfx950 int8 MFMA).
+// One wave per (split, kv-head, sequence, chunk of 4 query heads); the wave walks
+// its pages (64 tokens each) and keeps the online-softmax state of its 4 heads in
+// registers.  Waves of the same (split, kv-head, sequence) and different chunks
+// get workgroup ids that are equal modulo 8, so under round-robin dispatch over
+// the 8 XCDs they share one XCD's L2 for the page data they both read.
 //
 // Arithmetic (Sec. 2: K^ = Q(K R) R^T; Alg. 1 DecodeStep), per 32-channel group g
 // with Q(x~)_c = s_g (code_c - z_g):
@@ -13,9 +12,9 @@
 // The integer parts are int8 matrix products:
 //   * q~ of a head is scaled to a 24-bit integer (q_int = rne(q~ * Q / max|q~|),
 //     Q = 8355000) and split into three signed int8 digits,
-//     q_int = 65536 d2 + 256 d1 + d0; the codes are int8 0..3.  The products of
-//     the codes with each digit go to separate accumulators, combined as
-//     ((a_2 << 8) + a_1) << 8 + a_0, exact in int32 (|.| <= 32 * 3 * Q < 2^31).
+//     q_int = 65536 d_0 + 256 d_1 + d_2; the codes are int8 0..3.  The three
+//     digits are three rows of one MFMA, combined as ((a_0 << 8) + a_1) << 8 + a_2,
+//     exact in int32 (|.| <= 32 * 3 * Q < 2^31).
 //   * w of a (head, group) row on one page is scaled to [0, Q] (scale: the page's
 //     p_max of the head times the largest V scale of the group) and split the
 //     same way; the V codes are the other operand (|.| <= 64 * 3 * Q < 2^31).
@@ -28,19 +27,22 @@
 // copy every 8 16-byte chunks of the K-code region are followed by one chunk of
 // padding, which spreads the per-token reads of the score operands over the banks.
 //
-// Lane roles (l = lane, lo = l & 15, hi = l >> 4), MFMA 16x16x64 layout: A row =
-// lo, B column = lo, k-slots (hi, element), D (row 4*hi + i, column lo):
-//   scores, tile u (u = 0..3): A = q digits, row (head lo>>2, group lo&3), zero
-//     outside that group; B = K codes of token 4*lo + u (code dword hi for
-//     instruction X=0, 4+hi for X=1), expanded as M_j = (x >> 2j) & 0x03030303
-//     (element 4j+b <-> channel 16w + 4b + j);  D lane l, register i = (head hi,
-//     group i) of token 4*lo + u, so the sum over groups stays inside the lane.
-//   p (head hi, tokens 4*lo + u) goes through LDS to the P.V operand layout.
-//   P.V, tile (G, F) (G = 0..3, F = 0..1): A = w digits, row (head lo>>2, group
-//     lo&3), k = tokens 16*hi + (0..15); B column lo = channel
-//     32G + 4(lo&7) + 2F + (lo>>3) (all 16 columns in group G);  D lane l,
-//     register G = (head hi, group G) at that channel: the useful register index is
-//     the same in every lane.
+// Lane roles (l = lane, lo = l & 15, hi = l >> 4).  MFMA 16x16 layout: A row = lo,
+// B column = lo, k-slots (hi, element), D (row 4*hi + i, column lo).  MFMA rows
+// are (head lo>>2, digit lo&3); digit row 3 is padding whose output is never read.
+//   scores, token tile u (u = 0..3), group g: 16x16x32; A = digit of q~ of the head
+//     on 8 channels of g per k-group; B = K codes of token 4*lo + u on the same
+//     channels (element e of k-group hi <-> channel
+//     32g + 16(hi>>1) + 4(e&3) + 2(hi&1) + (e>>2)).  D lane l, register i = digit
+//     i of head hi for token 4*lo + u: digits combine inside the lane, and the
+//     sum over groups too.
+//   p (head hi, tokens 4*lo + u) goes through LDS to the weight layout: lane
+//     (head lo>>2, group lo&3) computes w for tokens 16*hi + (0..15) and stores
+//     its three digit operands to LDS, where the P.V layout reads them back.
+//   P.V, tile (G, F) (G = 0..3, F = 0..1): 16x16x64; A = digit of w of (head,
+//     group G), k = tokens 16*hi + (0..15); B column lo = channel
+//     32G + 4(lo&7) + 2F + (lo>>3) (all 16 columns in group G).  D lane l,
+//     register i = digit i of head hi at that channel.
 #include <hip/hip_fp16.h>
 
 #include "internal.h"
@@ -61,18 +63,18 @@ constexpr int kLdsKCodes = 0;              // chunk c < 128 at slot c + (c >> 3)
 constexpr int kLdsVCodes = 144 * 16;       // chunk c >= 128 at slot c + 16
 constexpr int kLdsKSz = (256 + 16) * 16;
 constexpr int kLdsVSz = (320 + 16) * 16;
+// Weight-digit operands of a page, stored over the page's K codes and K scales
+// (no longer needed once the scores are done): group G at kLdsW[G], 16 bytes per
+// (row 3*head + digit, k-group).
+__device__ inline int lds_w(int G) { return G < 3 ? 768 * G : kLdsKSz; }
 
-__device__ inline v4i mfma(v4i a, v4i b, v4i c) {
-  return __builtin_amdgcn_mfma_i32_16x16x64_i8(a, b, c, 0, 0, 0);
+__device__ inline v4i mfma64(v4i a, v4i b) {
+  const v4i z = {0, 0, 0, 0};
+  return __builtin_amdgcn_mfma_i32_16x16x64_i8(a, b, z, 0, 0, 0);
 }
-
-__device__ inline v4i expand2(uint32_t x) {  // four int8-dwords of 2-bit fields
-  v4i r;
-  r.x = (int)(x & 0x03030303u);
-  r.y = (int)((x >> 2) & 0x03030303u);
-  r.z = (int)((x >> 4) & 0x03030303u);
-  r.w = (int)((x >> 6) & 0x03030303u);
-  return r;
+__device__ inline v4i mfma32(long a, long b) {
+  const v4i z = {0, 0, 0, 0};
+  return __builtin_amdgcn_mfma_i32_16x16x32_i8(a, b, z, 0, 0, 0);
 }
 
 // raw v_exp_f32 (results below 2^-126 flush to 0: negligible softmax weights)
@@ -149,7 +151,9 @@ __device__ inline float rows_sum(float x) {
 // ((a << 8) + b) << 8 + c for signed digit sums, in unsigned arithmetic (the
 // intermediate values may be negative; the result fits in int32).
 __device__ inline int combine3(int a, int b, int c) {
-  return (int)((((uint32_t)a << 8) + (uint32_t)b) * 256u + (uint32_t)c);
+  uint32_t t = ((uint32_t)a << 8) + (uint32_t)b;
+  asm("" : "+v"(t));  // keeps two shift-adds (no re-association into 2 shifts + add3)
+  return (int)((t << 8) + (uint32_t)c);
 }
 
 // Per-wave LDS: the page copy and the exchanges between lane roles.
@@ -189,7 +193,7 @@ __device__ inline void stage_store(uint4* page, const Stage& s, int l) {
 }
 
 struct WaveState {
-  v4i bq[2][kNDig];     // query digits, A operand [instruction X][digit]
+  long aq[4];           // query digit operand per group (row: head lo>>2, digit lo&3)
   float qs[4];          // sum of q_int over group i of head hi
   float sq;             // q scale of head hi
   float m;              // running max (log2 units), head hi
@@ -202,30 +206,28 @@ struct WaveState {
 // possibly the sequence's last); otherwise slots >= ntok are masked.
 template <bool FULL>
 __device__ inline void compute_page(WaveState& st, WaveLds& L, int ntok, int lo, int hi) {
-  const char* pb = reinterpret_cast<const char*>(L.page);
+  char* pb = reinterpret_cast<char*>(L.page);
   // ---- scores of head hi for tokens 4*lo + u ----
-  const uint32_t* kc = reinterpret_cast<const uint32_t*>(pb + kLdsKCodes + 144 * lo + 4 * hi);
+  // code dword 2g + (hi>>1) of token 4*lo + u at byte 32u + 8g from the lane base
+  const uint32_t* kc = reinterpret_cast<const uint32_t*>(pb + kLdsKCodes + 144 * lo + 4 * (hi >> 1));
+  const uint32_t sh4 = 4u * (uint32_t)(hi & 1);
   uint4 ksz[4];  // (s, z) of tokens 4*lo + (0..3), group i
 #pragma unroll
   for (int i = 0; i < 4; ++i) ksz[i] = *reinterpret_cast<const uint4*>(pb + kLdsKSz + 256 * i + 16 * lo);
   float S[4];
 #pragma unroll
   for (int u = 0; u < 4; ++u) {
-    const v4i b0 = expand2(kc[8 * u]);
-    const v4i b1 = expand2(kc[8 * u + 4]);
-    v4i d[kNDig];
-#pragma unroll
-    for (int dg = 0; dg < kNDig; ++dg) {
-      const v4i z4 = {0, 0, 0, 0};
-      d[dg] = mfma(st.bq[1][dg], b1, mfma(st.bq[0][dg], b0, z4));
-    }
     float acc = 0.0f;
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      const int t = combine3(d[0][i], d[1][i], d[2][i]);
-      const uint32_t sz = comp(ksz[i], u);
+    for (int g = 0; g < 4; ++g) {
+      const uint32_t y = kc[8 * u + 2 * g] >> sh4;  // fields 2(hi&1), 2(hi&1)+1 of each byte
+      const uint32_t msk = 0x03030303u;
+      const long b = (long)((uint64_t)(y & msk) | ((uint64_t)((y >> 2) & msk) << 32));
+      const v4i d = mfma32(st.aq[g], b);
+      const int t = combine3(d[0], d[1], d[2]);
+      const uint32_t sz = comp(ksz[g], u);
       // s * (acc - z * sum q_int) with s, z read from the packed binary16 pair
-      acc = mix_lo(sz, mix_nhi(sz, st.qs[i], (float)t), acc);
+      acc = mix_lo(sz, mix_nhi(sz, st.qs[g], (float)t), acc);
     }
     S[u] = acc;
   }
@@ -251,7 +253,7 @@ __device__ inline void compute_page(WaveState& st, WaveLds& L, int ntok, int lo,
   L.p[hi][lo] = make_float4(p[0], p[1], p[2], p[3]);
   L.hs[hi] = make_float2(alpha, pmax);  // every lane of the row writes the same value
 
-  // ---- P.V weights w = p * s_v of row (head lo>>2, group lo&3), tokens 16*hi + e ----
+  // ---- P.V weights w = p * s_v of (head lo>>2, group lo&3), tokens 16*hi + e ----
   const int wh = lo >> 2, wg = lo & 3;
   const float2 hsw = L.hs[wh];
   float4 pw[4];
@@ -269,15 +271,18 @@ __device__ inline void compute_page(WaveState& st, WaveLds& L, int ntok, int lo,
   }
   // largest V scale of the group on this page: scales are positive binary16, so
   // their bit patterns order like their values (packed u16 max; high halves ignored)
-  uint32_t smax = 0;
+  uint32_t m8[8];
 #pragma unroll
-  for (int e = 0; e < 16; ++e) smax = max_u16x2(smax, sz[e]);
+  for (int e = 0; e < 8; ++e) m8[e] = max_u16x2(sz[e], sz[e + 8]);
+#pragma unroll
+  for (int e = 0; e < 4; ++e) m8[e] = max_u16x2(m8[e], m8[e + 4]);
+  const uint32_t smax = max_u16x2(max_u16x2(m8[0], m8[2]), max_u16x2(m8[1], m8[3]));
   const float svmax = rows_max(h_lo(smax));
   const float sig = hsw.y * svmax;  // >= every w of the row on this page
   const float inv = sig > 0.0f ? kQMax * __builtin_amdgcn_rcpf(sig) : 0.0f;
   L.ws[lo] = sig * (1.0f / kQMax);
   float zp = 0.0f;
-  v4i aw[kNDig];
+  uint32_t aw[kNDig][4];
 #pragma unroll
   for (int j = 0; j < 4; ++j) {
     uint32_t f[4];
@@ -286,7 +291,7 @@ __device__ inline void compute_page(WaveState& st, WaveLds& L, int ntok, int lo,
       const int e = 4 * j + b;
       const float w = mix_lo(sz[e], compf(pw[j], b), 0.0f);
       // mantissa of rne(w * inv) + 2^23 + 32896 = k + 32896, k in [0, Q]:
-      // k = 65536 d2 + 256 d1 + d0 with d0, d1 = (bytes 0, 1) ^ 0x80, d2 = byte 2
+      // k = 65536 d_0 + 256 d_1 + d_2 with d_2, d_1 = (bytes 0, 1) ^ 0x80, d_0 = byte 2
       f[b] = __float_as_uint(fmaf(w, inv, kMagic + kDigitBias));
       zp = mix_hi(sz[e], w, zp);  // unquantized w: differs from the quantized by <= 2^-24 sig
     }
@@ -294,18 +299,28 @@ __device__ inline void compute_page(WaveState& st, WaveLds& L, int ntok, int lo,
     const uint32_t t23 = __builtin_amdgcn_perm(f[3], f[2], 0x05010400u) ^ 0x80808080u;
     const uint32_t h01 = __builtin_amdgcn_perm(f[1], f[0], 0x0c0c0602u);                // [f0.2 f1.2 0 0]
     const uint32_t h23 = __builtin_amdgcn_perm(f[3], f[2], 0x0c0c0602u);
-    aw[2][j] = (int)__builtin_amdgcn_perm(t23, t01, 0x05040100u);
-    aw[1][j] = (int)__builtin_amdgcn_perm(t23, t01, 0x07060302u);
-    aw[0][j] = (int)__builtin_amdgcn_perm(h23, h01, 0x05040100u);
+    aw[2][j] = __builtin_amdgcn_perm(t23, t01, 0x05040100u);
+    aw[1][j] = __builtin_amdgcn_perm(t23, t01, 0x07060302u);
+    aw[0][j] = __builtin_amdgcn_perm(h23, h01, 0x05040100u);
   }
   st.zacc = fmaf(st.zacc, hsw.x, zp);
+  {  // digit operands to LDS: group wg, rows 3*wh + digit, k-group hi
+    char* wp = pb + lds_w(wg) + 16 * (4 * (3 * wh) + hi);
+#pragma unroll
+    for (int dg = 0; dg < kNDig; ++dg)
+      *reinterpret_cast<uint4*>(wp + 64 * dg) = make_uint4(aw[dg][0], aw[dg][1], aw[dg][2], aw[dg][3]);
+  }
 
   // ---- P.V on the matrix cores: lane (channel column, head hi) ----
   const float4 ws = *reinterpret_cast<const float4*>(&L.ws[4 * hi]);
   const uint32_t sh = 2u * (uint32_t)(lo >> 3);
   const char* vb = pb + kLdsVCodes + 64 * (lo & 7) + 16 * hi;
+  // A operand row (head lo>>2, digit lo&3); the padding digit row reads digit 2
+  const char* ab = pb + 16 * (4 * (3 * (lo >> 2) + min(lo & 3, 2)) + hi);
 #pragma unroll
   for (int G = 0; G < 4; ++G) {
+    const uint4 a4 = *reinterpret_cast<const uint4*>(ab + lds_w(G));
+    const v4i aop = {(int)a4.x, (int)a4.y, (int)a4.z, (int)a4.w};
     const uint4 x = *reinterpret_cast<const uint4*>(vb + 512 * G);  // quad 8G + (lo&7)
     const uint4 y = make_uint4(x.x >> sh, x.y >> sh, x.z >> sh, x.w >> sh);
 #pragma unroll
@@ -313,13 +328,8 @@ __device__ inline void compute_page(WaveState& st, WaveLds& L, int ntok, int lo,
       const uint32_t msk = 0x03030303u;
       const v4i bv = {(int)((y.x >> (4 * F)) & msk), (int)((y.y >> (4 * F)) & msk),
                       (int)((y.z >> (4 * F)) & msk), (int)((y.w >> (4 * F)) & msk)};
-      int e[kNDig];
-#pragma unroll
-      for (int dg = 0; dg < kNDig; ++dg) {
-        const v4i z4 = {0, 0, 0, 0};
-        e[dg] = mfma(aw[dg], bv, z4)[G];  // row (head hi, group G)
-      }
-      const int t = combine3(e[0], e[1], e[2]);
+      const v4i d = mfma64(aop, bv);
+      const int t = combine3(d[0], d[1], d[2]);
       float& o = st.of[2 * G + F];
       o = fmaf((float)t, compf(ws, G), o * alpha);
     }
@@ -335,8 +345,8 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(4, 4))) void
     int B, const float* __restrict__ qt, float* __restrict__ part_o,
     float* __restrict__ part_ml) {
   __shared__ WaveLds L;
-  const int g = Hq / Hkv;
-  const int nch = (g + 3) >> 2;
+  const int g_heads = Hq / Hkv;
+  const int nch = (g_heads + 3) >> 2;
   const int xcd = blockIdx.x & 7;
   const int slot = blockIdx.x >> 3;
   const int chunk = slot % nch;
@@ -357,72 +367,60 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(4, 4))) void
 
   WaveState st;
   // ---- query operands: q_int = rne(q~ * Q / max|q~|), three int8 digits ----
-  // Lane (head lo>>2, group G = lo&3, k-group hi) owns channels 32G + 16(hi&1) +
-  // 0..15 when (hi>>1) == (G&1), for instruction X = G>>1; it is zero otherwise.
+  // Lane (head lo>>2, digit lo&3, k-group hi) holds, for group g, element e of
+  // the k-group: channel 32g + 16(hi>>1) + 4(e&3) + 2(hi&1) + (e>>2).
   {
-    const int G = lo & 3;
-    const bool owns = (hi >> 1) == (G & 1);
-    const int cbase = 32 * G + 16 * (hi & 1);
-    const int hloc = 4 * chunk + (lo >> 2);
-    float qv[16];
+    const int h = lo >> 2, dsel = lo & 3;
+    const int hloc = 4 * chunk + h;
+    float qv[4][8];
     float amax = 0.0f;
 #pragma unroll
-    for (int e = 0; e < 16; ++e) qv[e] = 0.0f;
-    if (owns && hloc < g) {
-      const float4* src =
-          reinterpret_cast<const float4*>(qt + ((size_t)b * Hq + kvh * g + hloc) * kD + cbase);
+    for (int g = 0; g < 4; ++g)
 #pragma unroll
-      for (int v = 0; v < 4; ++v) {
-        const float4 x = src[v];
-        qv[4 * v] = x.x; qv[4 * v + 1] = x.y; qv[4 * v + 2] = x.z; qv[4 * v + 3] = x.w;
-      }
+      for (int e = 0; e < 8; ++e) qv[g][e] = 0.0f;
+    if (hloc < g_heads) {
+      const float* src = qt + ((size_t)b * Hq + kvh * g_heads + hloc) * kD + 16 * (hi >> 1) + 2 * (hi & 1);
 #pragma unroll
-      for (int e = 0; e < 16; ++e) amax = fmaxf(amax, fabsf(qv[e]));
+      for (int g = 0; g < 4; ++g)
+#pragma unroll
+        for (int bb = 0; bb < 4; ++bb) {
+          const float2 x = *reinterpret_cast<const float2*>(src + 32 * g + 4 * bb);
+          qv[g][bb] = x.x;
+          qv[g][4 + bb] = x.y;
+        }
+#pragma unroll
+      for (int g = 0; g < 4; ++g)
+#pragma unroll
+        for (int e = 0; e < 8; ++e) amax = fmaxf(amax, fabsf(qv[g][e]));
     }
-    amax = rows_max(quad_max(amax));  // all 128 channels of the head
+    amax = rows_max(amax);  // all 128 channels of the head (k-groups hi)
     const float inv = amax > 0.0f ? kQMax / amax : 0.0f;
     const float sq = amax > 0.0f ? amax * (1.0f / kQMax) : 1.0f;
-    int qi[16];
-    int qsum = 0;
+    float qsum[4];
 #pragma unroll
-    for (int e = 0; e < 16; ++e) {
-      qi[e] = (int)rintf(qv[e] * inv);
-      qsum += qi[e];
-    }
-    // element 4j + b of the operand <-> channel cbase + 4b + j;
-    // q = 65536 d2 + 256 d1 + d0 with d0 = q - 256 c1, c1 = (q + 128) >> 8, etc.
-    uint32_t dw[kNDig][4];
+    for (int g = 0; g < 4; ++g) {
+      int sum = 0;
+      uint32_t w[2] = {0u, 0u};
 #pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      uint32_t w2 = 0, w1 = 0, w0 = 0;
-#pragma unroll
-      for (int bb = 0; bb < 4; ++bb) {
-        const int v = qi[4 * bb + j];
+      for (int e = 0; e < 8; ++e) {
+        const int v = (int)rintf(qv[g][e] * inv);
+        sum += v;
+        // q = 65536 d_0 + 256 d_1 + d_2 with d_2 = q - 256 c1, c1 = (q + 128) >> 8, etc.
         const int c1 = (v + 128) >> 8;
-        const int d0 = v - 256 * c1;
-        const int d2 = (c1 + 128) >> 8;
-        const int d1 = c1 - 256 * d2;
-        w2 |= ((uint32_t)d2 & 0xffu) << (8 * bb);
-        w1 |= ((uint32_t)d1 & 0xffu) << (8 * bb);
-        w0 |= ((uint32_t)d0 & 0xffu) << (8 * bb);
+        const int d2 = v - 256 * c1;
+        const int d0 = (c1 + 128) >> 8;
+        const int d1 = c1 - 256 * d0;
+        const int dv = dsel == 0 ? d0 : dsel == 1 ? d1 : dsel == 2 ? d2 : 0;
+        w[e >> 2] |= ((uint32_t)dv & 0xffu) << (8 * (e & 3));
       }
-      dw[0][j] = w2;
-      dw[1][j] = w1;
-      dw[2][j] = w0;
+      st.aq[g] = (long)((uint64_t)w[0] | ((uint64_t)w[1] << 32));
+      // sum over the group's 32 channels (k-groups hi), exact in int
+      sum += __shfl_xor(sum, 16, 64);
+      sum += __shfl_xor(sum, 32, 64);
+      qsum[g] = (float)sum;
     }
-    const v4i zero = {0, 0, 0, 0};
-    const bool x1 = (G >> 1) != 0;
-#pragma unroll
-    for (int dg = 0; dg < kNDig; ++dg) {
-      const v4i v = {(int)dw[dg][0], (int)dw[dg][1], (int)dw[dg][2], (int)dw[dg][3]};
-      st.bq[0][dg] = x1 ? zero : v;
-      st.bq[1][dg] = x1 ? v : zero;
-    }
-    // sum over the group's 32 channels (two owning lanes), exact in int
-    qsum += __shfl_xor(qsum, 16, 64);
-    qsum += __shfl_xor(qsum, 32, 64);
-    L.qs[lo] = (float)qsum;  // lanes of equal lo write equal values
-    L.sq[lo >> 2] = sq;
+    L.qs[lo] = dsel == 0 ? qsum[0] : dsel == 1 ? qsum[1] : dsel == 2 ? qsum[2] : qsum[3];  // (head h, group dsel)
+    L.sq[h] = sq;  // lanes of equal h write equal values
     const float4 q4 = *reinterpret_cast<const float4*>(&L.qs[4 * hi]);
     st.qs[0] = q4.x; st.qs[1] = q4.y; st.qs[2] = q4.z; st.qs[3] = q4.w;
     st.sq = L.sq[hi];
@@ -433,15 +431,22 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(4, 4))) void
     for (int k = 0; k < 8; ++k) st.of[k] = 0.0f;
   }
 
+  // Block-table entries of the split, 64 pages at a time: lane i holds the entry
+  // of page cb + i (a vector load, so that waiting for it never waits on LDS).
+  int cb = p0;
+  int btv = (p0 + l < p1) ? bt[p0 + l] : 0;
   Stage sg;
-  if (p0 < p1) stage_load(sg, base + (size_t)bt[p0] * page_stride, l);
+  if (p0 < p1) stage_load(sg, base + (size_t)__builtin_amdgcn_readlane(btv, 0) * page_stride, l);
   // pages [p0, pf) are full; page pf (if < p1) is the sequence's partial last page
   const int pf = (p0 < p1 && p1 == npg && (len & (kP - 1)) != 0) ? p1 - 1 : p1;
-  int nxt = (p0 < p1) ? bt[min(p0 + 1, p1 - 1)] : 0;
   for (int pg = p0; pg < pf; ++pg) {
     stage_store(L.page, sg, l);
-    stage_load(sg, base + (size_t)nxt * page_stride, l);  // page pg+1 (the last page again at the end)
-    nxt = bt[min(pg + 2, p1 - 1)];
+    const int nx = min(pg + 1, p1 - 1);  // page pg+1 (the last page again at the end)
+    if (nx - cb >= 64) {                 // uniform: next 64 entries
+      cb += 64;
+      btv = (cb + l < p1) ? bt[cb + l] : 0;
+    }
+    stage_load(sg, base + (size_t)__builtin_amdgcn_readlane(btv, nx - cb) * page_stride, l);
     compute_page<true>(st, L, kP, lo, hi);
   }
   if (pf < p1) {  // the partial last page; the stage holds it
@@ -455,8 +460,8 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(4, 4))) void
   L.ws[lo] = ztot;                        // lanes of equal lo write equal values
   const float4 zh = *reinterpret_cast<const float4*>(&L.ws[4 * hi]);
   const int hout = 4 * chunk + hi;        // head of this lane's accumulators
-  if (hout >= g) return;                  // padding head
-  const size_t row = ((size_t)b * Hq + kvh * g + hout) * num_splits + s;
+  if (hout >= g_heads) return;            // padding head
+  const size_t row = ((size_t)b * Hq + kvh * g_heads + hout) * num_splits + s;
   const bool empty = st.m == -INFINITY;
 #pragma unroll
   for (int G = 0; G < 4; ++G) {
