@@ -11,8 +11,11 @@ batch 64, per-sequence context lengths uniform in [16384, 32768], page size 64,
 shuffled non-contiguous pages.
 
 Prints one JSON line.  `value` is the step's algorithmic HBM bytes divided by
-the step time (GB/s).  `roofline` is the split kernel (the dominant kernel),
-timed with HIP events on the library's stream inside the timed loop.
+the step time (GB/s): K eager steps bracketed by torch.cuda.synchronize(), wall
+clock.  `roofline` is the split kernel (the dominant kernel), timed with HIP
+events on the library's stream around K back-to-back launches; `kernels_us`
+breaks one step down with events between the stages (a separate pass, since
+those events add launch gaps).
 `cpu_baseline` is the CPU oracle timed on a bounded sample of the same
 workload.  `bf16_baseline` is the bf16 paged-decode kernel on the same
 sequences.
@@ -47,6 +50,9 @@ def parse():
     ap.add_argument("--num-splits", type=int, default=0, help="0 = library default")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-bf16-baseline", action="store_true")
+    ap.add_argument("--graph", action="store_true",
+                    help="also time HIP-graph replays of the step (reported under timing; "
+                         "slower than eager launches on ROCm 7.x, so never used for value)")
     ap.add_argument("--cpu-seconds", type=float, default=10.0,
                     help="target CPU time for the oracle baseline sample")
     return ap.parse_args()
@@ -131,17 +137,64 @@ def main():
     for _ in range(args.warmup):
         step()
     torch.cuda.synchronize()
+    ref_out = out.clone()
+
+    def timed(run_one):
+        """K steps bracketed by synchronize; HIP events around the whole region."""
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        w0 = time.perf_counter()
+        e0.record(stream)
+        for _ in range(args.steps):
+            run_one()
+        e1.record(stream)
+        torch.cuda.synchronize()
+        wall_us = (time.perf_counter() - w0) / args.steps * 1e6
+        return wall_us, e0.elapsed_time(e1) * 1e3 / args.steps
+
+    eager_wall_us, eager_ev_us = timed(step)
+
+    # Optional: the step captured once as a HIP graph and replayed; reported only
+    # when every replay reproduces the eager output bit for bit.
+    graph_note = "not timed (pass --graph)"
+    graph_wall_us = graph_ev_us = None
+    if args.graph:
+        try:
+            g = torch.cuda.CUDAGraph()
+            side = torch.cuda.Stream()
+            side.wait_stream(torch.cuda.current_stream())
+            with torch.cuda.stream(side):
+                step()  # warm the side stream
+            torch.cuda.current_stream().wait_stream(side)
+            torch.cuda.synchronize()
+            with torch.cuda.graph(g):
+                step()
+            torch.cuda.synchronize()
+            ok_replays = True
+            for _ in range(3):
+                out.zero_()
+                g.replay()
+                torch.cuda.synchronize()
+                ok_replays &= bool(torch.equal(out, ref_out))
+            if ok_replays:
+                graph_wall_us, graph_ev_us = timed(g.replay)
+                ok_replays = bool(torch.equal(out, ref_out))
+            graph_note = "timed" if ok_replays else "replay output differs from eager: not timed"
+            if not ok_replays:
+                graph_wall_us = graph_ev_us = None
+        except Exception as exc:  # capture unsupported: report and time eagerly
+            graph_note = "capture failed: %s" % (type(exc).__name__,)
+    us_step = eager_wall_us
+
+    # per-stage breakdown: a separate pass with events between the stages
     evs = [[torch.cuda.Event(enable_timing=True) for _ in range(5)] for _ in range(args.steps)]
     torch.cuda.synchronize()
-    w0 = time.perf_counter()
     for i in range(args.steps):
         step(evs[i])
     torch.cuda.synchronize()
-    wall = time.perf_counter() - w0
     seg = np.array([[evs[i][j].elapsed_time(evs[i][j + 1]) for j in range(4)]
                     for i in range(args.steps)]) * 1e3               # us
     step_us = np.array([evs[i][0].elapsed_time(evs[i][4]) for i in range(args.steps)]) * 1e3
-    us_step = wall / args.steps * 1e6
 
     # ---- algorithmic bytes ----
     pages_used = int(np.sum((lens + 63) // 64))
@@ -151,7 +204,15 @@ def main():
     qo_bytes = 2 * B * Hq * d * 2
     append_bytes = 2 * B * Hkv * d * 2 + B * Hkv * INT2_BYTES_PER_TOKEN_HEAD + B * 8 + 2 * d * d * 4
     step_bytes = split_bytes + qo_bytes + append_bytes + 2 * d * d * 4
-    split_us = float(np.mean(seg[:, 2]))
+    # the dominant kernel alone: K back-to-back launches between two events on its stream
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    e0.record(stream)
+    for _ in range(args.steps):
+        ok.decode_split(lay, pool, B, Hq, bt, sl, S, ws)
+    e1.record(stream)
+    torch.cuda.synchronize()
+    split_us = e0.elapsed_time(e1) * 1e3 / args.steps
     achieved = split_bytes / (split_us * 1e-6) / 1e9
 
     res = {
@@ -176,10 +237,18 @@ def main():
             "seq_len_mean": float(lens.mean()), "seq_len_min": int(lens.min()),
             "seq_len_max": int(lens.max()), "num_splits": S, "new_tokens_per_step": B,
         },
+        "timing": {
+            "us_per_step_eager_wall": round(eager_wall_us, 2),
+            "us_per_step_eager_events": round(eager_ev_us, 2),
+            "us_per_step_graph_wall": None if graph_wall_us is None else round(graph_wall_us, 2),
+            "us_per_step_graph_events": None if graph_ev_us is None else round(graph_ev_us, 2),
+            "graph_replay": graph_note,
+        },
         "kernels_us": {
             "kv_append": round(float(np.mean(seg[:, 0])), 2),
             "decode_prepare": round(float(np.mean(seg[:, 1])), 2),
-            "decode_split": round(split_us, 2),
+            "decode_split": round(float(np.mean(seg[:, 2])), 2),
+            "decode_split_back_to_back": round(split_us, 2),
             "decode_reduce": round(float(np.mean(seg[:, 3])), 2),
             "step_events_median": round(float(np.median(step_us)), 2),
             "step_events_p10": round(float(np.percentile(step_us, 10)), 2),

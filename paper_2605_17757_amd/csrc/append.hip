@@ -100,8 +100,14 @@ __global__ __launch_bounds__(256) void append_kernel(
   const uint16_t* __restrict__ X = is_v ? v : k;
   const float clip = is_v ? clip_v : clip_k;
 
-  for (int i = threadIdx.x; i < kD * kD / 4; i += blockDim.x)
-    reinterpret_cast<float4*>(Rs)[i] = reinterpret_cast<const float4*>(R)[i];
+  {  // 16 float4 per thread, all loads issued before the stores
+    float4 v[kD * kD / 4 / 256];
+#pragma unroll
+    for (int k = 0; k < kD * kD / 4 / 256; ++k)
+      v[k] = reinterpret_cast<const float4*>(R)[threadIdx.x + 256 * k];
+#pragma unroll
+    for (int k = 0; k < kD * kD / 4 / 256; ++k) reinterpret_cast<float4*>(Rs)[threadIdx.x + 256 * k] = v[k];
+  }
 
   const int w = threadIdx.x >> 6;
   const int l = threadIdx.x & 63;

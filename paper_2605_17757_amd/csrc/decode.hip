@@ -39,38 +39,64 @@ __device__ inline float wave_sum(float x) {
 }
 
 // ---------------------------------------------------------------------------
-// prepare: 16 query rows per block, R_k read once per block (coalesced in j).
+// prepare: 8 query rows per block.  R_k (64 KB) is copied to LDS once per block;
+// thread (channel j, row group) computes 4 rows of column j, reading R_k[c][j]
+// (consecutive j: no bank conflicts) and the rows' q[c..c+3] (broadcast).
 // ---------------------------------------------------------------------------
-constexpr int kPrepRows = 16;
+constexpr int kPrepRows = 8;
 
 __global__ __launch_bounds__(256) void prepare_kernel(const uint16_t* __restrict__ q, int rows,
                                                       const float* __restrict__ Rk, float qscale,
                                                       float* __restrict__ qt) {
-  __shared__ float qs[kD][kPrepRows];
+  __shared__ float4 Rs[kD * kD / 4];
+  __shared__ float4 qs[kPrepRows][kD / 4];
   const int r0 = blockIdx.x * kPrepRows;
-  for (int i = threadIdx.x; i < kPrepRows * kD; i += blockDim.x) {
-    const int r = i / kD, c = i % kD;
-    qs[c][r] = (r0 + r < rows) ? bf16_to_f32(q[(size_t)(r0 + r) * kD + c]) : 0.0f;
+  const int t = threadIdx.x;
+  if (Rk) {
+    // 16 float4 per thread, all loads issued before the stores (no per-load wait)
+    float4 v[kD * kD / 4 / 256];
+#pragma unroll
+    for (int k = 0; k < kD * kD / 4 / 256; ++k) v[k] = reinterpret_cast<const float4*>(Rk)[t + 256 * k];
+#pragma unroll
+    for (int k = 0; k < kD * kD / 4 / 256; ++k) Rs[t + 256 * k] = v[k];
+  }
+  {  // 8 rows x 128 bf16 = 256 threads x 4 values
+    const int r = t >> 5, c4 = t & 31;
+    float4 x = make_float4(0.0f, 0.0f, 0.0f, 0.0f);
+    if (r0 + r < rows) {
+      const uint2 w = reinterpret_cast<const uint2*>(q + (size_t)(r0 + r) * kD)[c4];
+      x = make_float4(bf16_to_f32((uint16_t)(w.x & 0xffffu)), bf16_to_f32((uint16_t)(w.x >> 16)),
+                      bf16_to_f32((uint16_t)(w.y & 0xffffu)), bf16_to_f32((uint16_t)(w.y >> 16)));
+    }
+    qs[r][c4] = x;
   }
   __syncthreads();
-  const int j = threadIdx.x & (kD - 1);
-  const int rh = (threadIdx.x >> 7) * 8;
-  float acc[8];
+  const int j = t & (kD - 1);
+  const int rg = (t >> 7) * 4;
+  float acc[4] = {0.0f, 0.0f, 0.0f, 0.0f};
   if (Rk) {
+    const float* R = reinterpret_cast<const float*>(Rs);
+#pragma unroll 4
+    for (int c4 = 0; c4 < kD / 4; ++c4) {
+      const float r_0 = R[(4 * c4 + 0) * kD + j], r_1 = R[(4 * c4 + 1) * kD + j];
+      const float r_2 = R[(4 * c4 + 2) * kD + j], r_3 = R[(4 * c4 + 3) * kD + j];
 #pragma unroll
-    for (int i = 0; i < 8; ++i) acc[i] = 0.0f;
-    for (int c = 0; c < kD; ++c) {
-      const float r = Rk[c * kD + j];
-#pragma unroll
-      for (int i = 0; i < 8; ++i) acc[i] = fmaf(qs[c][rh + i], r, acc[i]);
+      for (int i = 0; i < 4; ++i) {
+        const float4 x = qs[rg + i][c4];
+        acc[i] = fmaf(x.x, r_0, acc[i]);
+        acc[i] = fmaf(x.y, r_1, acc[i]);
+        acc[i] = fmaf(x.z, r_2, acc[i]);
+        acc[i] = fmaf(x.w, r_3, acc[i]);
+      }
     }
   } else {  // R = I (bf16 baseline)
+    const float* Q = reinterpret_cast<const float*>(qs);
 #pragma unroll
-    for (int i = 0; i < 8; ++i) acc[i] = qs[j][rh + i];
+    for (int i = 0; i < 4; ++i) acc[i] = Q[(rg + i) * kD + j];
   }
 #pragma unroll
-  for (int i = 0; i < 8; ++i)
-    if (r0 + rh + i < rows) qt[(size_t)(r0 + rh + i) * kD + j] = acc[i] * qscale;
+  for (int i = 0; i < 4; ++i)
+    if (r0 + rg + i < rows) qt[(size_t)(r0 + rg + i) * kD + j] = acc[i] * qscale;
 }
 
 // ---------------------------------------------------------------------------
@@ -266,73 +292,90 @@ __global__ __launch_bounds__(256) void split_kernel(
 }
 
 // ---------------------------------------------------------------------------
-// reduce: 16 (sequence, head) rows per block; merge splits, then o = o~ R_v^T
-// with R_v staged transposed in LDS (Rt[c][j] = R_v[j][c]).
+// reduce: 8 (sequence, head) rows per block.
+//   1. thread (row, 4 channels): M = max_s m_s, L = sum_s 2^(m_s - M) l_s over
+//      the row's splits (empty splits have m_s = -inf), then
+//      o~[c] = sum_s 2^(m_s - M) part_o[s][c] / L with independent loads over s;
+//   2. o = o~ R_v^T, R_v copied to LDS with rows padded to 132 floats (16-byte
+//      aligned rows; threads of consecutive j read different banks).
 // ---------------------------------------------------------------------------
-constexpr int kRedRows = 16;
+constexpr int kRedRows = 8;
+constexpr int kRvPitch4 = kD / 4 + 1;  // row pitch of the LDS copy in float4
 
 __global__ __launch_bounds__(256) void reduce_kernel(int rows, int num_splits,
                                                      const float* __restrict__ part_o,
                                                      const float* __restrict__ part_ml,
                                                      const float* __restrict__ Rv,
                                                      void* __restrict__ out, int out_f32) {
-  __shared__ float Rt[kD][kD + 1];
-  __shared__ float om[kRedRows][kD];
-  __shared__ float rowM[kRedRows], rowInvL[kRedRows];
+  __shared__ float4 Rs[kD * kRvPitch4];
+  __shared__ float4 om[kRedRows][kD / 4];
   const int r0 = blockIdx.x * kRedRows;
+  const int t = threadIdx.x;
   if (Rv) {
-    for (int i = threadIdx.x; i < kD * kD; i += blockDim.x) {
-      const int j = i / kD, c = i % kD;
-      Rt[c][j] = Rv[i];
+    float4 v[kD * kD / 4 / 256];  // 16 float4 per thread, loads issued before the stores
+#pragma unroll
+    for (int k = 0; k < kD * kD / 4 / 256; ++k) v[k] = reinterpret_cast<const float4*>(Rv)[t + 256 * k];
+#pragma unroll
+    for (int k = 0; k < kD * kD / 4 / 256; ++k) {
+      const int i = t + 256 * k;
+      Rs[(i >> 5) * kRvPitch4 + (i & 31)] = v[k];
     }
   }
-  if (threadIdx.x < kRedRows) {
-    const int r = r0 + threadIdx.x;
-    float M = -INFINITY, L = 0.0f;
+  {  // 8 rows x 32 float4 columns: one (row, float4) per thread
+    const int rr = t >> 5, c4 = t & 31, r = r0 + rr;
+    float4 o = make_float4(0.0f, 0.0f, 0.0f, 0.0f);
     if (r < rows) {
-      for (int s = 0; s < num_splits; ++s) M = fmaxf(M, part_ml[((size_t)r * num_splits + s) * 2]);
-      for (int s = 0; s < num_splits; ++s) {
-        const float ms = part_ml[((size_t)r * num_splits + s) * 2];
-        if (ms != -INFINITY) L += exp2f(ms - M) * part_ml[((size_t)r * num_splits + s) * 2 + 1];
+      const float2* ml = reinterpret_cast<const float2*>(part_ml + (size_t)r * num_splits * 2);
+      float M = -INFINITY;
+#pragma unroll 8
+      for (int s = 0; s < num_splits; ++s) M = fmaxf(M, ml[s].x);
+      if (M != -INFINITY) {
+        const float4* po = reinterpret_cast<const float4*>(part_o + (size_t)r * num_splits * kD) + c4;
+        float L = 0.0f;
+#pragma unroll 8
+        for (int s = 0; s < num_splits; ++s) {
+          const float2 m = ml[s];
+          const float4 x = po[(size_t)s * (kD / 4)];  // loaded unconditionally: no load->branch chain
+          const bool live = m.x != -INFINITY;         // an empty split contributes nothing
+          const float e = live ? exp2f(m.x - M) : 0.0f;
+          L = fmaf(e, live ? m.y : 0.0f, L);
+          o.x = fmaf(e, live ? x.x : 0.0f, o.x); o.y = fmaf(e, live ? x.y : 0.0f, o.y);
+          o.z = fmaf(e, live ? x.z : 0.0f, o.z); o.w = fmaf(e, live ? x.w : 0.0f, o.w);
+        }
+        const float il = L > 0.0f ? 1.0f / L : 0.0f;
+        o.x *= il; o.y *= il; o.z *= il; o.w *= il;
       }
     }
-    rowM[threadIdx.x] = M;
-    rowInvL[threadIdx.x] = (L > 0.0f) ? 1.0f / L : 0.0f;
+    om[rr][c4] = o;
   }
   __syncthreads();
-  for (int i = threadIdx.x; i < kRedRows * kD; i += blockDim.x) {
-    const int rr = i / kD, c = i % kD, r = r0 + rr;
-    float o = 0.0f;
-    if (r < rows) {
-      const float M = rowM[rr];
-      for (int s = 0; s < num_splits; ++s) {
-        const size_t idx = (size_t)r * num_splits + s;
-        const float ms = part_ml[idx * 2];
-        if (ms != -INFINITY) o += exp2f(ms - M) * part_o[idx * kD + c];
-      }
-      o *= rowInvL[rr];
-    }
-    om[rr][c] = o;
-  }
-  __syncthreads();
-  const int j = threadIdx.x & (kD - 1);
-  const int rh = (threadIdx.x >> 7) * 8;
-  float acc[8];
+  const int j = t & (kD - 1);
+  const int rg = (t >> 7) * 4;
+  float acc[4];
   if (Rv) {
 #pragma unroll
-    for (int i = 0; i < 8; ++i) acc[i] = 0.0f;
-    for (int c = 0; c < kD; ++c) {
-      const float rv = Rt[c][j];
+    for (int i = 0; i < 4; ++i) acc[i] = 0.0f;
+    const float4* Rj = Rs + j * kRvPitch4;
+#pragma unroll 4
+    for (int c4 = 0; c4 < kD / 4; ++c4) {
+      const float4 rv = Rj[c4];
 #pragma unroll
-      for (int i = 0; i < 8; ++i) acc[i] = fmaf(om[rh + i][c], rv, acc[i]);
+      for (int i = 0; i < 4; ++i) {
+        const float4 x = om[rg + i][c4];
+        acc[i] = fmaf(x.x, rv.x, acc[i]);
+        acc[i] = fmaf(x.y, rv.y, acc[i]);
+        acc[i] = fmaf(x.z, rv.z, acc[i]);
+        acc[i] = fmaf(x.w, rv.w, acc[i]);
+      }
     }
   } else {  // R = I (bf16 baseline)
+    const float* O = reinterpret_cast<const float*>(om);
 #pragma unroll
-    for (int i = 0; i < 8; ++i) acc[i] = om[rh + i][j];
+    for (int i = 0; i < 4; ++i) acc[i] = O[(rg + i) * kD + j];
   }
 #pragma unroll
-  for (int i = 0; i < 8; ++i) {
-    const int r = r0 + rh + i;
+  for (int i = 0; i < 4; ++i) {
+    const int r = r0 + rg + i;
     if (r >= rows) continue;
     if (out_f32) static_cast<float*>(out)[(size_t)r * kD + j] = acc[i];
     else static_cast<uint16_t*>(out)[(size_t)r * kD + j] = f32_to_bf16_rne(acc[i]);

@@ -105,9 +105,10 @@ int32_t oscar_default_num_splits(const oscar_layout* L, int32_t B, int32_t Hq,
                                  int32_t max_seq_len) {
   if (check_layout(L) != OSCAR_OK || B < 1 || Hq < 1 || max_seq_len < 1) return 1;
   const int64_t pages = (max_seq_len + L->page_size - 1) / L->page_size;
-  // one wave per (split, kv-head, sequence, 4 query heads); aim for 8 waves per
-  // compute unit
-  const int64_t target_waves = 8LL * device_cus();
+  // one wave per (split, kv-head, sequence, 4 query heads); aim for 16 waves per
+  // compute unit (about four rounds of resident waves), which also evens out
+  // sequences of different lengths
+  const int64_t target_waves = 16LL * device_cus();
   const int64_t chunks = (Hq % L->num_kv_heads == 0) ? (Hq / L->num_kv_heads + 3) / 4 : 1;
   const int64_t pairs = (int64_t)B * L->num_kv_heads * chunks;
   int64_t s = (target_waves + pairs - 1) / pairs;
