@@ -118,9 +118,12 @@ size_t oscar_decode_workspace_bytes(const oscar_layout *L, int32_t B, int32_t Hq
                                     int32_t num_splits);
 
 /*
- * A split count that fills the GPU for B sequences whose longest context is
- * max_seq_len tokens (>= 1).  Every split covers at most
- * ceil(max_pages_per_seq / num_splits) pages.
+ * A split count for B sequences whose longest context is max_seq_len tokens
+ * (>= 1).  oscar_decode_attn divides the pages of all sequences evenly among the
+ * GPU's resident waves (about 16 per compute unit, ranges of at least 4 pages);
+ * num_splits bounds the number of partial states of one (sequence, head) row,
+ * and the returned value allows the cut that an average sequence length of half
+ * the longest produces (>= 2 unless the longest sequence has < 4 pages).
  */
 int32_t oscar_default_num_splits(const oscar_layout *L, int32_t B, int32_t Hq,
                                  int32_t max_seq_len);
@@ -133,13 +136,20 @@ int32_t oscar_default_num_splits(const oscar_layout *L, int32_t B, int32_t Hq,
  * over the cached tokens t < seq_lens[b], evaluated as
  *   q~ = q R_k;  scores against Q(K~);  o~ = softmax-weighted sum of Q(V~);
  *   o = o~ R_v^T,
- * split along the sequence into num_splits parts merged with a log-sum-exp
- * reduce.  No host synchronization, no allocation.
+ * split along the sequences and merged with a log-sum-exp reduce: the pages of
+ * all (sequence, kv-head) pairs are laid end to end and cut into equal ranges,
+ * one per resident wave, each range at least ceil(max_pages_per_seq /
+ * (num_splits - 1)) pages so that a row gets at most num_splits partial states
+ * (num_splits == 1: one range per (sequence, kv-head)).  The result does not
+ * depend on the cut beyond fp32 rounding.  No host synchronization, no
+ * allocation.
  *   q            : bf16 [B, Hq, d]; Hq % Hkv == 0, Hq/Hkv <= 16
  *   block_table  : int32 [B, max_pages_per_seq]; token t of sequence b is in
  *                  page block_table[b][t / P], slot t % P
  *   seq_lens     : int32 [B], tokens in cache, 1 <= seq_lens[b] <=
- *                  max_pages_per_seq * P (the current token already appended)
+ *                  max_pages_per_seq * P (the current token already appended);
+ *                  values outside are clamped to [0, max_pages_per_seq * P],
+ *                  and a sequence of length 0 gives a zero output
  *   sm_scale     : logit scale, 1/sqrt(d) for standard attention
  *   num_splits   : >= 1, or 0 for oscar_default_num_splits(L, B, Hq,
  *                  max_pages_per_seq * P)
@@ -159,8 +169,8 @@ int oscar_decode_attn(const oscar_layout *L, const void *pages, const void *q, i
  * them separately.  Called in this order on one stream with the same
  * arguments they equal one oscar_decode_attn call.
  *   prepare : q~ = q R_k scaled by sm_scale*log2(e), into the workspace.
- *   split   : per (sequence, kv-head, split) partial softmax state over the
- *             split's pages, into the workspace.
+ *   split   : partial softmax states over page ranges (see above), into the
+ *             workspace.
  *   reduce  : log-sum-exp merge of the splits, o = o~ R_v^T, into out.
  */
 int oscar_decode_prepare(const oscar_layout *L, const void *q, int32_t B, int32_t Hq,

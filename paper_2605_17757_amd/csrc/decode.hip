@@ -414,7 +414,7 @@ hipError_t launch_decode_split(const uint8_t* pages, int Hkv, int B, int Hq,
   }();
   if (!use_v0)
     return launch_decode_split_mfma(pages, Hkv, B, Hq, block_table, max_pages, seq_lens,
-                                    num_splits, qt, part_o, part_ml, st);
+                                    num_splits, 16 * device_cus(), qt, part_o, part_ml, st);
   const int g = Hq / Hkv;
   if (g <= 4)
     return launch_split_nh<4>(pages, Hkv, B, Hq, block_table, max_pages, seq_lens, num_splits,

@@ -45,6 +45,8 @@
 //     register i = digit i of head hi at that channel.
 #include <hip/hip_fp16.h>
 
+#include <algorithm>
+
 #include "internal.h"
 
 namespace oscar {
@@ -336,31 +338,18 @@ __device__ inline void compute_page(WaveState& st, WaveLds& L, int ntok, int lo,
   }
 }
 
-// Grid: 1-D, ceil(S*Hkv*B / 8) * 8 * nch workgroups of one wave.  Workgroup id
-// -> (xcd = id % 8, slot = id / 8); chunk = slot % nch; item = (slot / nch) * 8
-// + xcd; item -> (split, kv-head, sequence).  Items beyond S*Hkv*B exit.
-__global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(4, 4))) void split_mfma_kernel(
-    const uint8_t* __restrict__ pages, int Hkv, int Hq, const int32_t* __restrict__ block_table,
-    int max_pages, const int32_t* __restrict__ seq_lens, int num_splits, int pages_per_split,
-    int B, const float* __restrict__ qt, float* __restrict__ part_o,
-    float* __restrict__ part_ml) {
-  __shared__ WaveLds L;
+// Pages [p0, p1) of sequence b, kv-head kvh, query-head chunk `chunk`: online
+// softmax over the pages and the partial state written to slot `piece` of the
+// (sequence, head) rows.  `last`: the piece ends the sequence, so the slots
+// after it are marked empty.
+__device__ __attribute__((always_inline)) inline void process_piece(WaveLds& L, const uint8_t* __restrict__ pages, int Hkv, int Hq,
+                                     const int32_t* __restrict__ block_table, int max_pages, int b,
+                                     int len, int kvh, int chunk, int p0, int p1, int piece,
+                                     bool last, int num_splits, const float* __restrict__ qt,
+                                     float* __restrict__ part_o, float* __restrict__ part_ml) {
   const int g_heads = Hq / Hkv;
-  const int nch = (g_heads + 3) >> 2;
-  const int xcd = blockIdx.x & 7;
-  const int slot = blockIdx.x >> 3;
-  const int chunk = slot % nch;
-  const int64_t item = (int64_t)(slot / nch) * 8 + xcd;
-  if (item >= (int64_t)num_splits * Hkv * B) return;
-  const int s = (int)(item % num_splits);
-  const int kvh = (int)((item / num_splits) % Hkv);
-  const int b = (int)(item / ((int64_t)num_splits * Hkv));
   const int l = threadIdx.x, lo = l & 15, hi = l >> 4;
-  const int len = seq_lens[b];
   const int npg = (len + kP - 1) / kP;
-  const int p0 = s * pages_per_split;
-  const int p1 = min(npg, p0 + pages_per_split);
-
   const int32_t* __restrict__ bt = block_table + (size_t)b * max_pages;
   const uint8_t* __restrict__ base = pages + (size_t)kvh * kBlockBytes;
   const size_t page_stride = (size_t)Hkv * kBlockBytes;
@@ -461,7 +450,12 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(4, 4))) void
   const float4 zh = *reinterpret_cast<const float4*>(&L.ws[4 * hi]);
   const int hout = 4 * chunk + hi;        // head of this lane's accumulators
   if (hout >= g_heads) return;            // padding head
-  const size_t row = ((size_t)b * Hq + kvh * g_heads + hout) * num_splits + s;
+  const size_t row = ((size_t)b * Hq + kvh * g_heads + hout) * num_splits + piece;
+  if (last && lo == 0)  // the segment's last piece: the remaining slots hold nothing
+    for (int s2 = piece + 1; s2 < num_splits; ++s2) {
+      part_ml[(row + s2 - piece) * 2] = -INFINITY;
+      part_ml[(row + s2 - piece) * 2 + 1] = 0.0f;
+    }
   const bool empty = st.m == -INFINITY;
 #pragma unroll
   for (int G = 0; G < 4; ++G) {
@@ -477,20 +471,132 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(4, 4))) void
   }
 }
 
+// Balanced split (one persistent wave per range of pages).  The (sequence,
+// kv-head) page lists are laid end to end, T pages in total; range r covers
+// pages [r*pw, (r+1)*pw) with pw = max(ceil(T / n_ranges), ceil(max_pages /
+// (S - 1)), kMinRange), so every wave reads the same number of pages and a
+// sequence is cut into at most S pieces (piece = r - first range of the
+// sequence).  With S = 1 each range is one whole (sequence, kv-head).
+// Grid: ceil(n_ranges / 8) * 8 * nch one-wave workgroups; workgroup id -> (xcd =
+// id % 8, slot = id / 8); chunk = slot % nch; range = (slot / nch) * 8 + xcd, so
+// the chunks of one range share an XCD (and its L2) under round-robin dispatch.
+constexpr int kMinRange = 4;
+
+__device__ inline int wave_sum_i(int x) {
+#pragma unroll
+  for (int m = 32; m >= 1; m >>= 1) x += __shfl_xor(x, m, 64);
+  return x;
+}
+
+__global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(4, 4))) void split_mfma_kernel(
+    const uint8_t* __restrict__ pages, int Hkv, int Hq, const int32_t* __restrict__ block_table,
+    int max_pages, const int32_t* __restrict__ seq_lens, int num_splits, int n_ranges, int B,
+    const float* __restrict__ qt, float* __restrict__ part_o, float* __restrict__ part_ml) {
+  __shared__ WaveLds L;
+  const int g_heads = Hq / Hkv;
+  const int nch = (g_heads + 3) >> 2;
+  const int xcd = blockIdx.x & 7;
+  const int slot = blockIdx.x >> 3;
+  const int chunk = slot % nch;
+  const int r = (slot / nch) * 8 + xcd;
+  if (r >= n_ranges) return;
+  const int l = threadIdx.x;
+  auto seq_len = [&](int bb) {  // lengths beyond the block table are clamped
+    return min(max(seq_lens[bb], 0), max_pages * kP);
+  };
+  if (num_splits == 1) {  // one range per (sequence, kv-head)
+    const int b = r / Hkv, kvh = r % Hkv;
+    const int len = seq_len(b);
+    process_piece(L, pages, Hkv, Hq, block_table, max_pages, b, len, kvh, chunk, 0,
+                  (len + kP - 1) / kP, 0, true, 1, qt, part_o, part_ml);
+    return;
+  }
+  // total pages over all (sequence, kv-head)
+  int64_t T = 0;
+  for (int b0 = 0; b0 < B; b0 += 64) {
+    const int bb = b0 + l;
+    T += __builtin_amdgcn_readfirstlane(wave_sum_i(bb < B ? (seq_len(bb) + kP - 1) / kP : 0));
+  }
+  T *= Hkv;
+  const int64_t pw = max(max((T + n_ranges - 1) / n_ranges,
+                             (int64_t)((max_pages + num_splits - 2) / (num_splits - 1))),
+                         (int64_t)kMinRange);
+  int64_t x = (int64_t)r * pw;
+  const int64_t xe = min(T, x + pw);
+  // a sequence with no pages gets empty slots from range b mod n_ranges (chunk 0
+  // covers all heads)
+  if (chunk == 0)
+    for (int bb = r; bb < B; bb += n_ranges)
+      if (seq_len(bb) == 0)
+        for (int i = l; i < Hq * num_splits; i += 64) {
+          const size_t row = (size_t)bb * Hq * num_splits + i;
+          part_ml[row * 2] = -INFINITY;
+          part_ml[row * 2 + 1] = 0.0f;
+        }
+  if (x >= xe) return;
+  // the sequence holding page x: pages before sequence b, scanned 64 sequences at a time
+  int b = 0, npg_b = 0;
+  int64_t before = 0;  // pages of sequences < b, times Hkv
+  for (int b0 = 0; b0 < B; b0 += 64) {
+    const int bb = b0 + l;
+    const int np = bb < B ? (seq_len(bb) + kP - 1) / kP : 0;
+    int incl = np;  // inclusive prefix sum over the lanes
+#pragma unroll
+    for (int off = 1; off < 64; off <<= 1) {
+      const int y = __shfl_up(incl, off, 64);
+      if (l >= off) incl += y;
+    }
+    const int64_t lo_x = before + (int64_t)(incl - np) * Hkv;
+    const int64_t hi_x = before + (int64_t)incl * Hkv;
+    const uint64_t hit = __ballot(bb < B && np > 0 && lo_x <= x && x < hi_x);
+    if (hit) {
+      const int lane = __ffsll((unsigned long long)hit) - 1;
+      b = b0 + lane;
+      npg_b = __builtin_amdgcn_readlane(np, lane);
+      before += (int64_t)__builtin_amdgcn_readlane(incl - np, lane) * Hkv;
+      break;
+    }
+    before += (int64_t)__builtin_amdgcn_readlane(incl, 63) * Hkv;
+  }
+  if (npg_b == 0) return;  // not reached: page x < T lies in some sequence
+  int kvh = (int)((x - before) / npg_b);
+  while (true) {
+    const int64_t seg = before + (int64_t)kvh * npg_b;  // first page of (b, kvh)
+    const int64_t end = min(xe, seg + npg_b);
+    const int piece = (int)(r - seg / pw);
+    process_piece(L, pages, Hkv, Hq, block_table, max_pages, b, seq_len(b), kvh, chunk,
+                  (int)(x - seg), (int)(end - seg), piece, end == seg + npg_b, num_splits, qt,
+                  part_o, part_ml);
+    x = end;
+    if (x >= xe) break;
+    if (++kvh == Hkv) {  // next sequence with pages
+      kvh = 0;
+      before += (int64_t)npg_b * Hkv;
+      do {
+        if (++b >= B) return;  // not reached: pages remain before xe <= T
+        npg_b = (seq_len(b) + kP - 1) / kP;
+      } while (npg_b == 0);
+    }
+  }
+}
+
 }  // namespace
 
 hipError_t launch_decode_split_mfma(const uint8_t* pages, int Hkv, int B, int Hq,
                                     const int32_t* block_table, int max_pages,
-                                    const int32_t* seq_lens, int num_splits, const float* qt,
-                                    float* part_o, float* part_ml, hipStream_t st) {
+                                    const int32_t* seq_lens, int num_splits, int resident_waves,
+                                    const float* qt, float* part_o, float* part_ml,
+                                    hipStream_t st) {
   const int g = Hq / Hkv;
   const int nch = (g + 3) / 4;
-  const int pps = (max_pages + num_splits - 1) / num_splits;
-  const int64_t items = (int64_t)num_splits * Hkv * B;
-  const int64_t blocks = (items + 7) / 8 * 8 * nch;
+  // one range per resident wave (each range runs nch waves, one per chunk of heads)
+  const int64_t ranges =
+      num_splits == 1 ? (int64_t)B * Hkv : std::max<int64_t>(1, resident_waves / nch);
+  const int64_t blocks = (ranges + 7) / 8 * 8 * nch;
   if (blocks > 0x7fffffffLL) return hipErrorInvalidConfiguration;
   hipLaunchKernelGGL(split_mfma_kernel, dim3((unsigned)blocks), dim3(64), 0, st, pages, Hkv, Hq,
-                     block_table, max_pages, seq_lens, num_splits, pps, B, qt, part_o, part_ml);
+                     block_table, max_pages, seq_lens, num_splits, (int)ranges, B, qt, part_o,
+                     part_ml);
   return hipGetLastError();
 }
 

@@ -46,10 +46,14 @@ hipError_t launch_decode_split(const uint8_t* pages, int Hkv, int B, int Hq,
                                const int32_t* block_table, int max_pages,
                                const int32_t* seq_lens, int num_splits, const float* qt,
                                float* part_o, float* part_ml, hipStream_t st);
+// Balanced split kernel: `resident_waves` waves share the pages equally; a
+// (sequence, head) row gets at most num_splits partial states.
 hipError_t launch_decode_split_mfma(const uint8_t* pages, int Hkv, int B, int Hq,
                                     const int32_t* block_table, int max_pages,
-                                    const int32_t* seq_lens, int num_splits, const float* qt,
-                                    float* part_o, float* part_ml, hipStream_t st);
+                                    const int32_t* seq_lens, int num_splits, int resident_waves,
+                                    const float* qt, float* part_o, float* part_ml,
+                                    hipStream_t st);
+int device_cus();  // compute units of the current device (cached)
 hipError_t launch_decode_reduce(int B, int Hq, int num_splits, const float* part_o,
                                 const float* part_ml, const float* Rv, void* out, int out_f32,
                                 hipStream_t st);

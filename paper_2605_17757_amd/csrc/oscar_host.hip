@@ -2,12 +2,32 @@
 // Every entry point validates all host arguments before launching anything.
 #include <math.h>
 
+#include <algorithm>
 #include <atomic>
 
 #include "../../include/oscar.h"
 #include "internal.h"
 
 using namespace oscar;
+
+namespace oscar {
+
+int device_cus() {
+  static std::atomic<int> cached{0};
+  int v = cached.load(std::memory_order_relaxed);
+  if (v > 0) return v;
+  int dev = 0, cus = 0;
+  if (hipGetDevice(&dev) == hipSuccess &&
+      hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) == hipSuccess &&
+      cus > 0)
+    v = cus;
+  else
+    v = 256;
+  cached.store(v, std::memory_order_relaxed);
+  return v;
+}
+
+}  // namespace oscar
 
 namespace {
 
@@ -25,21 +45,6 @@ int check_layout(const oscar_layout* L) {
 }
 
 bool clip_ok(float c) { return isfinite(c) && c > 0.0f && c <= 1.0f; }
-
-int device_cus() {
-  static std::atomic<int> cached{0};
-  int v = cached.load(std::memory_order_relaxed);
-  if (v > 0) return v;
-  int dev = 0, cus = 0;
-  if (hipGetDevice(&dev) == hipSuccess &&
-      hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) == hipSuccess &&
-      cus > 0)
-    v = cus;
-  else
-    v = 256;
-  cached.store(v, std::memory_order_relaxed);
-  return v;
-}
 
 int hip_status(hipError_t e) { return e == hipSuccess ? OSCAR_OK : OSCAR_ERR_HIP; }
 
@@ -105,17 +110,19 @@ int32_t oscar_default_num_splits(const oscar_layout* L, int32_t B, int32_t Hq,
                                  int32_t max_seq_len) {
   if (check_layout(L) != OSCAR_OK || B < 1 || Hq < 1 || max_seq_len < 1) return 1;
   const int64_t pages = (max_seq_len + L->page_size - 1) / L->page_size;
-  // one wave per (split, kv-head, sequence, 4 query heads); aim for 16 waves per
-  // compute unit (about four rounds of resident waves), which also evens out
-  // sequences of different lengths
-  const int64_t target_waves = 16LL * device_cus();
+  if (pages < 4) return 1;
+  // The split kernel gives each of its ~16 waves per CU an equal share of all
+  // pages (ranges of >= 4 pages); a (sequence, head) row is cut into at most
+  // num_splits pieces.  Assuming sequences average half the longest, the range
+  // is ~B * Hkv * pages / 2 / waves pages; allow one more piece than the longest
+  // sequence needs at that range.
   const int64_t chunks = (Hq % L->num_kv_heads == 0) ? (Hq / L->num_kv_heads + 3) / 4 : 1;
-  const int64_t pairs = (int64_t)B * L->num_kv_heads * chunks;
-  int64_t s = (target_waves + pairs - 1) / pairs;
-  int64_t cap = pages / 2;  // at least two pages per split
-  if (cap < 1) cap = 1;
-  if (s > cap) s = cap;
-  if (s < 1) s = 1;
+  const int64_t ranges = std::max<int64_t>(1, 16LL * device_cus() / chunks);
+  int64_t range = ((int64_t)B * L->num_kv_heads * pages / 2 + ranges - 1) / ranges;
+  if (range < 4) range = 4;
+  int64_t s = (pages + range - 1) / range + 1;
+  if (s > pages / 2) s = pages / 2;  // at least two pages per piece on average
+  if (s < 2) s = 2;
   return (int32_t)s;
 }
 
