@@ -9,12 +9,14 @@
 // "sum in fp64, ascending, round once to fp32" bit for bit.
 //
 // Work decomposition: blockIdx.y selects K (0) or V (1); the block stages that
-// rotation matrix (64 KB fp32) in LDS.  Each wave takes four rows (token, head)
-// at a time; lane l computes output channels l and l+64 of the four rows, so
-// every matrix element read from LDS feeds four fp64 FMAs.  A 32-channel group
-// is then one half of the wave: channels 0-31 / 64-95 live in lanes 0-31,
-// channels 32-63 / 96-127 in lanes 32-63, and the group reductions are 5-step
-// xor shuffles inside the half wave.
+// rotation matrix (64 KB fp32) in LDS once and its four waves then take RW rows
+// (token, head) at a time, grid-stride.  Lane l computes output channels l and
+// l+64 of the rows, so every matrix element read from LDS feeds RW fp64 FMAs per
+// channel.  A 32-channel group is one half of the wave: channels 0-31 / 64-95
+// live in lanes 0-31, channels 32-63 / 96-127 in lanes 32-63; the group max /
+// min are DPP steps inside each row of 16 lanes plus one row-pair swap.
+// RW = 1 for small appends (one decode step: many short waves), 4 for bulk
+// cache builds (fewer matrix reads per FMA).
 #include <hip/hip_fp16.h>
 
 #include "internal.h"
@@ -23,7 +25,6 @@ namespace oscar {
 namespace {
 
 constexpr int kWaves = 4;
-constexpr int kRows = 4;  // rows per wave item
 
 __device__ inline float f16_bits_to_f32(uint16_t h) { return __half2float(__ushort_as_half(h)); }
 
@@ -37,16 +38,21 @@ __device__ inline uint16_t f16_sat_bits(float f) {
 // compiler may drop an "x + 0.0f" whose result only feeds fmaxf/fminf.
 __device__ inline uint16_t plus_zero(uint16_t h) { return (h & 0x7fffu) ? h : (uint16_t)0; }
 
-__device__ inline float half_wave_max(float x) {
-#pragma unroll
-  for (int m = 16; m >= 1; m >>= 1) x = fmaxf(x, __shfl_xor(x, m, 64));
-  return x;
+// max / min over the 32 lanes of a half wave: quad swaps and row rotations by 4
+// and 8 (DPP) reduce each row of 16 lanes, the row-pair swap joins rows 2k, 2k+1.
+template <bool MAX>
+__device__ inline float half_wave_reduce(float x) {
+  auto op = [](float a, float b) { return MAX ? fmaxf(a, b) : fminf(a, b); };
+  x = op(x, __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(x), 0xB1, 0xF, 0xF, false)));
+  x = op(x, __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(x), 0x4E, 0xF, 0xF, false)));
+  x = op(x, __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(x), 0x124, 0xF, 0xF, false)));
+  x = op(x, __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(x), 0x128, 0xF, 0xF, false)));
+  const uint32_t u = __float_as_uint(x);
+  const auto sw = __builtin_amdgcn_permlane16_swap(u, u, false, false);
+  return op(__uint_as_float(sw[0]), __uint_as_float(sw[1]));
 }
-__device__ inline float half_wave_min(float x) {
-#pragma unroll
-  for (int m = 16; m >= 1; m >>= 1) x = fminf(x, __shfl_xor(x, m, 64));
-  return x;
-}
+__device__ inline float half_wave_max(float x) { return half_wave_reduce<true>(x); }
+__device__ inline float half_wave_min(float x) { return half_wave_reduce<false>(x); }
 
 struct QOut {
   uint32_t code;
@@ -83,17 +89,18 @@ __device__ inline QOut quantize(float x, float clip) {
 // OR the 2-bit codes of lanes 4j..4j+3 into the byte of quad j (valid in lane 4j).
 __device__ inline uint32_t pack_quad(uint32_t code, int lane) {
   uint32_t v = code << (2 * (lane & 3));
-  v |= __shfl_xor(v, 1, 64);
-  v |= __shfl_xor(v, 2, 64);
+  v |= (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0xB1, 0xF, 0xF, false);  // lane ^ 1
+  v |= (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x4E, 0xF, 0xF, false);  // lane ^ 2
   return v;
 }
 
+template <int RW>
 __global__ __launch_bounds__(256) void append_kernel(
     uint8_t* __restrict__ pages, int Hkv, const uint16_t* __restrict__ k,
     const uint16_t* __restrict__ v, const int64_t* __restrict__ slots, int n_rows,
     const float* __restrict__ Rk, const float* __restrict__ Rv, float clip_k, float clip_v) {
   __shared__ float Rs[kD * kD];
-  __shared__ double xs[kWaves][kD][kRows];
+  __shared__ double xs[kWaves][RW][kD];
 
   const int is_v = blockIdx.y;
   const float* __restrict__ R = is_v ? Rv : Rk;
@@ -101,55 +108,53 @@ __global__ __launch_bounds__(256) void append_kernel(
   const float clip = is_v ? clip_v : clip_k;
 
   {  // 16 float4 per thread, all loads issued before the stores
-    float4 v[kD * kD / 4 / 256];
+    float4 r4[kD * kD / 4 / 256];
 #pragma unroll
-    for (int k = 0; k < kD * kD / 4 / 256; ++k)
-      v[k] = reinterpret_cast<const float4*>(R)[threadIdx.x + 256 * k];
+    for (int i = 0; i < kD * kD / 4 / 256; ++i)
+      r4[i] = reinterpret_cast<const float4*>(R)[threadIdx.x + 256 * i];
 #pragma unroll
-    for (int k = 0; k < kD * kD / 4 / 256; ++k) reinterpret_cast<float4*>(Rs)[threadIdx.x + 256 * k] = v[k];
+    for (int i = 0; i < kD * kD / 4 / 256; ++i) reinterpret_cast<float4*>(Rs)[threadIdx.x + 256 * i] = r4[i];
   }
+  __syncthreads();
 
   const int w = threadIdx.x >> 6;
   const int l = threadIdx.x & 63;
-  const int n_items = (n_rows + kRows - 1) / kRows;
+  const int n_items = (n_rows + RW - 1) / RW;
   const uint32_t sz_base = is_v ? kOffVSz : kOffKSz;
 
-  // The loop bound is uniform across the block so that __syncthreads is legal.
-  for (int base = blockIdx.x * kWaves; base < n_items; base += gridDim.x * kWaves) {
-    const int item = base + w;
-    __syncthreads();  // xs reuse; first pass also covers the R staging
-    for (int rr = 0; rr < kRows; ++rr) {
-      const int row = item * kRows + rr;
+  // each wave owns xs[w]: no block-level synchronization inside the loop
+  for (int item = blockIdx.x * kWaves + w; item < n_items; item += gridDim.x * kWaves) {
+#pragma unroll
+    for (int rr = 0; rr < RW; ++rr) {
+      const int row = item * RW + rr;
       double x0 = 0.0, x1 = 0.0;
-      if (item < n_items && row < n_rows) {
+      if (row < n_rows) {
         const uint32_t pair = reinterpret_cast<const uint32_t*>(X + (size_t)row * kD)[l];
         x0 = (double)__uint_as_float(pair << 16);
         x1 = (double)__uint_as_float(pair & 0xffff0000u);
       }
-      xs[w][2 * l][rr] = x0;
-      xs[w][2 * l + 1][rr] = x1;
+      xs[w][rr][2 * l] = x0;
+      xs[w][rr][2 * l + 1] = x1;
     }
-    __syncthreads();
-    if (item >= n_items) continue;
 
-    double acc0[kRows], acc1[kRows];
+    double acc0[RW], acc1[RW];
 #pragma unroll
-    for (int rr = 0; rr < kRows; ++rr) acc0[rr] = acc1[rr] = 0.0;
+    for (int rr = 0; rr < RW; ++rr) acc0[rr] = acc1[rr] = 0.0;
 #pragma unroll 4
     for (int c = 0; c < kD; ++c) {
       const double r0 = (double)Rs[c * kD + l];
       const double r1 = (double)Rs[c * kD + l + 64];
 #pragma unroll
-      for (int rr = 0; rr < kRows; ++rr) {
-        const double xc = xs[w][c][rr];
+      for (int rr = 0; rr < RW; ++rr) {
+        const double xc = xs[w][rr][c];
         acc0[rr] = __fma_rn(xc, r0, acc0[rr]);
         acc1[rr] = __fma_rn(xc, r1, acc1[rr]);
       }
     }
 
 #pragma unroll
-    for (int rr = 0; rr < kRows; ++rr) {
-      const int row = item * kRows + rr;
+    for (int rr = 0; rr < RW; ++rr) {
+      const int row = item * RW + rr;
       const float xt0 = __double2float_rn(acc0[rr]);  // channel l
       const float xt1 = __double2float_rn(acc1[rr]);  // channel l + 64
       const QOut q0 = quantize(xt0, clip);
@@ -190,12 +195,16 @@ hipError_t launch_append(void* pages, int64_t Hkv, const uint16_t* k, const uint
                          const int64_t* slots, int n_tok, const float* Rk, const float* Rv,
                          float clip_k, float clip_v, hipStream_t st) {
   const int64_t n_rows = (int64_t)n_tok * Hkv;
-  const int64_t n_items = (n_rows + kRows - 1) / kRows;
-  int64_t blocks = (n_items + kWaves - 1) / kWaves;
-  if (blocks > 1024) blocks = 1024;
-  dim3 grid((unsigned)blocks, 2);
-  hipLaunchKernelGGL(append_kernel, grid, dim3(256), 0, st, static_cast<uint8_t*>(pages),
-                     (int)Hkv, k, v, slots, (int)n_rows, Rk, Rv, clip_k, clip_v);
+  auto launch = [&](auto kernel, int rw) {
+    const int64_t n_items = (n_rows + rw - 1) / rw;
+    int64_t blocks = (n_items + kWaves - 1) / kWaves;
+    if (blocks > 1024) blocks = 1024;
+    hipLaunchKernelGGL(kernel, dim3((unsigned)blocks, 2), dim3(256), 0, st,
+                       static_cast<uint8_t*>(pages), (int)Hkv, k, v, slots, (int)n_rows, Rk, Rv,
+                       clip_k, clip_v);
+  };
+  if (n_rows <= 4096) launch(append_kernel<1>, 1);
+  else launch(append_kernel<4>, 4);
   return hipGetLastError();
 }
 
