@@ -137,10 +137,10 @@ int32_t oscar_default_num_splits(const oscar_layout *L, int32_t B, int32_t Hq,
  *   q~ = q R_k;  scores against Q(K~);  o~ = softmax-weighted sum of Q(V~);
  *   o = o~ R_v^T,
  * split along the sequences and merged with a log-sum-exp reduce: the pages of
- * all (sequence, kv-head) pairs are laid end to end and cut into equal ranges,
- * one per resident wave, each range at least ceil(max_pages_per_seq /
- * (num_splits - 1)) pages so that a row gets at most num_splits partial states
- * (num_splits == 1: one range per (sequence, kv-head)).  The result does not
+ * all sequences are laid end to end and cut into equal ranges (one wave per
+ * range and kv-head, about 16 waves per compute unit in all), each range at
+ * least ceil(max_pages_per_seq / (num_splits - 1)) pages so that a row gets at
+ * most num_splits partial states (num_splits == 1: one range per sequence).  The result does not
  * depend on the cut beyond fp32 rounding.  No host synchronization, no
  * allocation.
  *   q            : bf16 [B, Hq, d]; Hq % Hkv == 0, Hq/Hkv <= 16

@@ -471,15 +471,18 @@ __device__ __attribute__((always_inline)) inline void process_piece(WaveLds& L, 
   }
 }
 
-// Balanced split (one persistent wave per range of pages).  The (sequence,
-// kv-head) page lists are laid end to end, T pages in total; range r covers
-// pages [r*pw, (r+1)*pw) with pw = max(ceil(T / n_ranges), ceil(max_pages /
-// (S - 1)), kMinRange), so every wave reads the same number of pages and a
-// sequence is cut into at most S pieces (piece = r - first range of the
-// sequence).  With S = 1 each range is one whole (sequence, kv-head).
-// Grid: ceil(n_ranges / 8) * 8 * nch one-wave workgroups; workgroup id -> (xcd =
-// id % 8, slot = id / 8); chunk = slot % nch; range = (slot / nch) * 8 + xcd, so
-// the chunks of one range share an XCD (and its L2) under round-robin dispatch.
+// Balanced split (persistent waves over equal page ranges).  The sequences'
+// pages are laid end to end, T pages in total; range r covers pages
+// [r*pw, (r+1)*pw) with pw = max(ceil(T / n_ranges), ceil(max_pages / (S - 1)),
+// kMinRange), so every wave reads the same number of pages and a sequence is cut
+// into at most S pieces (piece = r - first range of the sequence).  Each range
+// runs one wave per (kv-head, chunk of query heads): the waves of a range read
+// the blocks of the same pages at the same time (each page's Hkv blocks are
+// contiguous).  With S = 1 each range is one whole sequence.
+// Grid: ceil(n_ranges * Hkv / 8) * 8 * nch one-wave workgroups; workgroup id ->
+// (xcd = id % 8, slot = id / 8); chunk = slot % nch; u = (slot / nch) * 8 + xcd;
+// (range, kv-head) = (u / Hkv, u % Hkv): the chunks of one (range, kv-head)
+// share an XCD (and its L2) under round-robin dispatch.
 constexpr int kMinRange = 4;
 
 __device__ inline int wave_sum_i(int x) {
@@ -498,34 +501,33 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(4, 4))) void
   const int xcd = blockIdx.x & 7;
   const int slot = blockIdx.x >> 3;
   const int chunk = slot % nch;
-  const int r = (slot / nch) * 8 + xcd;
-  if (r >= n_ranges) return;
+  const int64_t u = (int64_t)(slot / nch) * 8 + xcd;
+  if (u >= (int64_t)n_ranges * Hkv) return;
+  const int r = (int)(u / Hkv), kvh = (int)(u % Hkv);
   const int l = threadIdx.x;
   auto seq_len = [&](int bb) {  // lengths beyond the block table are clamped
     return min(max(seq_lens[bb], 0), max_pages * kP);
   };
-  if (num_splits == 1) {  // one range per (sequence, kv-head)
-    const int b = r / Hkv, kvh = r % Hkv;
-    const int len = seq_len(b);
-    process_piece(L, pages, Hkv, Hq, block_table, max_pages, b, len, kvh, chunk, 0,
+  if (num_splits == 1) {  // one range per sequence
+    const int len = seq_len(r);
+    process_piece(L, pages, Hkv, Hq, block_table, max_pages, r, len, kvh, chunk, 0,
                   (len + kP - 1) / kP, 0, true, 1, qt, part_o, part_ml);
     return;
   }
-  // total pages over all (sequence, kv-head)
+  // total pages over all sequences
   int64_t T = 0;
   for (int b0 = 0; b0 < B; b0 += 64) {
     const int bb = b0 + l;
     T += __builtin_amdgcn_readfirstlane(wave_sum_i(bb < B ? (seq_len(bb) + kP - 1) / kP : 0));
   }
-  T *= Hkv;
   const int64_t pw = max(max((T + n_ranges - 1) / n_ranges,
                              (int64_t)((max_pages + num_splits - 2) / (num_splits - 1))),
                          (int64_t)kMinRange);
   int64_t x = (int64_t)r * pw;
   const int64_t xe = min(T, x + pw);
-  // a sequence with no pages gets empty slots from range b mod n_ranges (chunk 0
-  // covers all heads)
-  if (chunk == 0)
+  // a sequence with no pages gets empty slots from the (range b mod n_ranges,
+  // kv-head 0, chunk 0) wave, for all its heads
+  if (kvh == 0 && chunk == 0)
     for (int bb = r; bb < B; bb += n_ranges)
       if (seq_len(bb) == 0)
         for (int i = l; i < Hq * num_splits; i += 64) {
@@ -536,7 +538,7 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(4, 4))) void
   if (x >= xe) return;
   // the sequence holding page x: pages before sequence b, scanned 64 sequences at a time
   int b = 0, npg_b = 0;
-  int64_t before = 0;  // pages of sequences < b, times Hkv
+  int64_t before = 0;
   for (int b0 = 0; b0 < B; b0 += 64) {
     const int bb = b0 + l;
     const int np = bb < B ? (seq_len(bb) + kP - 1) / kP : 0;
@@ -546,37 +548,31 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(4, 4))) void
       const int y = __shfl_up(incl, off, 64);
       if (l >= off) incl += y;
     }
-    const int64_t lo_x = before + (int64_t)(incl - np) * Hkv;
-    const int64_t hi_x = before + (int64_t)incl * Hkv;
-    const uint64_t hit = __ballot(bb < B && np > 0 && lo_x <= x && x < hi_x);
+    const uint64_t hit =
+        __ballot(bb < B && np > 0 && before + (incl - np) <= x && x < before + incl);
     if (hit) {
       const int lane = __ffsll((unsigned long long)hit) - 1;
       b = b0 + lane;
       npg_b = __builtin_amdgcn_readlane(np, lane);
-      before += (int64_t)__builtin_amdgcn_readlane(incl - np, lane) * Hkv;
+      before += __builtin_amdgcn_readlane(incl - np, lane);
       break;
     }
-    before += (int64_t)__builtin_amdgcn_readlane(incl, 63) * Hkv;
+    before += __builtin_amdgcn_readlane(incl, 63);
   }
   if (npg_b == 0) return;  // not reached: page x < T lies in some sequence
-  int kvh = (int)((x - before) / npg_b);
   while (true) {
-    const int64_t seg = before + (int64_t)kvh * npg_b;  // first page of (b, kvh)
-    const int64_t end = min(xe, seg + npg_b);
-    const int piece = (int)(r - seg / pw);
+    const int64_t end = min(xe, before + npg_b);
+    const int piece = (int)(r - before / pw);
     process_piece(L, pages, Hkv, Hq, block_table, max_pages, b, seq_len(b), kvh, chunk,
-                  (int)(x - seg), (int)(end - seg), piece, end == seg + npg_b, num_splits, qt,
-                  part_o, part_ml);
+                  (int)(x - before), (int)(end - before), piece, end == before + npg_b,
+                  num_splits, qt, part_o, part_ml);
     x = end;
     if (x >= xe) break;
-    if (++kvh == Hkv) {  // next sequence with pages
-      kvh = 0;
-      before += (int64_t)npg_b * Hkv;
-      do {
-        if (++b >= B) return;  // not reached: pages remain before xe <= T
-        npg_b = (seq_len(b) + kP - 1) / kP;
-      } while (npg_b == 0);
-    }
+    before += npg_b;
+    do {  // next sequence with pages
+      if (++b >= B) return;  // not reached: pages remain before xe <= T
+      npg_b = (seq_len(b) + kP - 1) / kP;
+    } while (npg_b == 0);
   }
 }
 
@@ -590,9 +586,10 @@ hipError_t launch_decode_split_mfma(const uint8_t* pages, int Hkv, int B, int Hq
   const int g = Hq / Hkv;
   const int nch = (g + 3) / 4;
   // one range per resident wave (each range runs nch waves, one per chunk of heads)
+  // one range per resident wave group (each range runs Hkv * nch waves)
   const int64_t ranges =
-      num_splits == 1 ? (int64_t)B * Hkv : std::max<int64_t>(1, resident_waves / nch);
-  const int64_t blocks = (ranges + 7) / 8 * 8 * nch;
+      num_splits == 1 ? (int64_t)B : std::max<int64_t>(1, resident_waves / (nch * Hkv));
+  const int64_t blocks = (ranges * Hkv + 7) / 8 * 8 * nch;
   if (blocks > 0x7fffffffLL) return hipErrorInvalidConfiguration;
   hipLaunchKernelGGL(split_mfma_kernel, dim3((unsigned)blocks), dim3(64), 0, st, pages, Hkv, Hq,
                      block_table, max_pages, seq_lens, num_splits, (int)ranges, B, qt, part_o,

@@ -117,8 +117,8 @@ int32_t oscar_default_num_splits(const oscar_layout* L, int32_t B, int32_t Hq,
   // is ~B * Hkv * pages / 2 / waves pages; allow one more piece than the longest
   // sequence needs at that range.
   const int64_t chunks = (Hq % L->num_kv_heads == 0) ? (Hq / L->num_kv_heads + 3) / 4 : 1;
-  const int64_t ranges = std::max<int64_t>(1, 16LL * device_cus() / chunks);
-  int64_t range = ((int64_t)B * L->num_kv_heads * pages / 2 + ranges - 1) / ranges;
+  const int64_t ranges = std::max<int64_t>(1, 16LL * device_cus() / (chunks * L->num_kv_heads));
+  int64_t range = ((int64_t)B * pages / 2 + ranges - 1) / ranges;
   if (range < 4) range = 4;
   int64_t s = (pages + range - 1) / range + 1;
   if (s > pages / 2) s = pages / 2;  // at least two pages per piece on average
