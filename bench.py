@@ -1,11 +1,11 @@
 #!/usr/bin/env python3
 """Benchmark of the OSCAR INT2 decode path on one MI355X.
 
-One step = one decode step of one attention layer for B sequences:
-  kv_append of each sequence's newest token (rotate, clip, INT2, pack)
-  + decode prepare (q~ = q R_k) + split (paged split-K attention over the INT2
-  cache) + reduce (log-sum-exp merge, o = o~ R_v^T),
-all on one HIP stream with the inputs already resident in HBM.  The default
+One step = one decode step of one attention layer for B sequences
+(oscar_decode_step): kv_append of each sequence's newest token (rotate, clip,
+INT2, pack) and the query rotation q~ = q R_k in one launch, then split (paged
+split-K attention over the INT2 cache) and reduce (log-sum-exp merge,
+o = o~ R_v^T), all on one HIP stream with the inputs already resident in HBM.  The default
 workload is the Qwen3-8B-shaped layer: 32 query / 8 KV heads, head dim 128,
 batch 64, per-sequence context lengths uniform in [16384, 32768], page size 64,
 shuffled non-contiguous pages.
@@ -50,6 +50,8 @@ def parse():
     ap.add_argument("--num-splits", type=int, default=0, help="0 = library default")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-bf16-baseline", action="store_true")
+    ap.add_argument("--settle-ms", type=float, default=50.0,
+                    help="untimed steps run for this long before the warm-up steps")
     ap.add_argument("--graph", action="store_true",
                     help="also time HIP-graph replays of the step (reported under timing; "
                          "slower than eager launches on ROCm 7.x, so never used for value)")
@@ -123,7 +125,14 @@ def main():
 
     stream = torch.cuda.current_stream()
 
+    def step_fused():
+        """The timed step: oscar_decode_step (cache update + query rotation in one
+        launch, then split, then reduce)."""
+        ok.decode_step(lay, pool, new_k, new_v, new_slots_t, cfg.clip_k, cfg.clip_v, q, bt, sl,
+                       Rk, Rv, cfg.sm_scale, S, ws, out)
+
     def step(ev=None):
+        """The same step as four separate stage calls, for the per-stage breakdown."""
         if ev: ev[0].record(stream)
         ok.kv_append(lay, pool, new_k, new_v, new_slots_t, Rk, Rv, cfg.clip_k, cfg.clip_v)
         if ev: ev[1].record(stream)
@@ -138,6 +147,23 @@ def main():
         step()
     torch.cuda.synchronize()
     ref_out = out.clone()
+    for _ in range(args.warmup):
+        step_fused()
+    torch.cuda.synchronize()
+    if not torch.equal(out, ref_out):
+        raise SystemExit("oscar_decode_step output differs from the four stage calls")
+    # Settle: after any pause of the GPU (here the output check above) the next
+    # ~60 steps run 5-20% slower while it ramps back up, whatever ran before the
+    # pause; untimed blocks of steps run back to back for --settle-ms right
+    # before the timed region.
+    t_settle = time.perf_counter()
+    while (time.perf_counter() - t_settle) * 1e3 < args.settle_ms:
+        s0, s1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        s0.record(stream)
+        for _ in range(20):
+            step_fused()
+        s1.record(stream)
+        torch.cuda.synchronize()
 
     def timed(run_one):
         """K steps bracketed by synchronize; HIP events around the whole region."""
@@ -152,7 +178,7 @@ def main():
         wall_us = (time.perf_counter() - w0) / args.steps * 1e6
         return wall_us, e0.elapsed_time(e1) * 1e3 / args.steps
 
-    eager_wall_us, eager_ev_us = timed(step)
+    eager_wall_us, eager_ev_us = timed(step_fused)
 
     # Optional: the step captured once as a HIP graph and replayed; reported only
     # when every replay reproduces the eager output bit for bit.
@@ -164,11 +190,11 @@ def main():
             side = torch.cuda.Stream()
             side.wait_stream(torch.cuda.current_stream())
             with torch.cuda.stream(side):
-                step()  # warm the side stream
+                step_fused()  # warm the side stream
             torch.cuda.current_stream().wait_stream(side)
             torch.cuda.synchronize()
             with torch.cuda.graph(g):
-                step()
+                step_fused()
             torch.cuda.synchronize()
             ok_replays = True
             for _ in range(3):

@@ -165,6 +165,22 @@ int oscar_decode_attn(const oscar_layout *L, const void *pages, const void *q, i
                       size_t workspace_bytes, void *out, oscar_dtype out_dtype, void *stream);
 
 /*
+ * oscar_decode_step -- one serving decode step (Alg. 1 DecodeStep): write the
+ * n_new newest tokens' K/V into the cache (exactly oscar_kv_append), then
+ * decode attention over the cache including them (exactly oscar_decode_attn),
+ * in three launches instead of four: the cache update and the query rotation
+ * share one launch.  Arguments as in oscar_kv_append and oscar_decode_attn; n_new
+ * may be 0 (no update; k_new, v_new, slot_mapping may then be NULL).  Every
+ * argument is validated before anything is launched.
+ */
+int oscar_decode_step(const oscar_layout *L, void *pages, const void *k_new, const void *v_new,
+                      const int64_t *slot_mapping, int32_t n_new, float clip_k, float clip_v,
+                      const void *q, int32_t B, int32_t Hq, const int32_t *block_table,
+                      int32_t max_pages_per_seq, const int32_t *seq_lens, const float *R_k,
+                      const float *R_v, float sm_scale, int32_t num_splits, void *workspace,
+                      size_t workspace_bytes, void *out, oscar_dtype out_dtype, void *stream);
+
+/*
  * The three stages of oscar_decode_attn, for callers that schedule or time
  * them separately.  Called in this order on one stream with the same
  * arguments they equal one oscar_decode_attn call.

@@ -26,7 +26,8 @@ HEAD_DIM, PAGE_SIZE, GROUP_SIZE = 128, 64, 32
 EXPORTS = (
     "oscar_status_string", "oscar_page_bytes", "oscar_pool_bytes", "oscar_layout_check",
     "oscar_kv_append", "oscar_decode_workspace_bytes", "oscar_default_num_splits",
-    "oscar_decode_attn", "oscar_decode_prepare", "oscar_decode_split", "oscar_decode_reduce",
+    "oscar_decode_attn", "oscar_decode_step", "oscar_decode_prepare", "oscar_decode_split",
+    "oscar_decode_reduce",
     "oscar_bf16_page_bytes", "oscar_bf16_kv_append", "oscar_bf16_decode_workspace_bytes",
     "oscar_bf16_decode_attn",
 )
@@ -73,6 +74,9 @@ def lib() -> ctypes.CDLL:
             "oscar_default_num_splits": (i32, [LP, i32, i32, i32]),
             "oscar_decode_attn": (ctypes.c_int, [LP, P, P, i32, i32, P, i32, P, P, P, f32, i32, P,
                                                  sz, P, ctypes.c_int, P]),
+            "oscar_decode_step": (ctypes.c_int, [LP, P, P, P, P, i32, f32, f32, P, i32, i32, P,
+                                                 i32, P, P, P, f32, i32, P, sz, P, ctypes.c_int,
+                                                 P]),
             "oscar_decode_prepare": (ctypes.c_int, [LP, P, i32, i32, P, f32, i32, P, sz, P]),
             "oscar_decode_split": (ctypes.c_int, [LP, P, i32, i32, P, i32, P, i32, P, sz, P]),
             "oscar_decode_reduce": (ctypes.c_int, [LP, i32, i32, P, i32, P, sz, P, ctypes.c_int,
@@ -201,6 +205,29 @@ def decode_attn(layout: Layout, pages, q, block_table, seq_lens, R_k, R_v, sm_sc
         _ptr(workspace, torch.uint8, "workspace"), workspace.numel(),
         _ptr(out, out.dtype, "out", B * Hq * d), out_dtype, _stream(stream))
     _check(st, "oscar_decode_attn")
+
+
+def decode_step(layout: Layout, pages, k_new, v_new, slot_mapping, clip_k: float,
+                clip_v: float, q, block_table, seq_lens, R_k, R_v, sm_scale: float,
+                num_splits: int, workspace, out, stream=None) -> None:
+    """One serving decode step: append the new tokens' K/V (``slot_mapping`` may be
+    empty), then attention over the cache into ``out``."""
+    B, Hq, mp = _decode_args(layout, q, block_table, seq_lens)
+    d, hkv = layout.head_dim, layout.num_kv_heads
+    n_new = int(slot_mapping.numel())
+    out_dtype = OUT_F32 if out.dtype == torch.float32 else OUT_BF16
+    kp = _ptr(k_new, torch.bfloat16, "k_new", n_new * hkv * d) if n_new else None
+    vp = _ptr(v_new, torch.bfloat16, "v_new", n_new * hkv * d) if n_new else None
+    sp = _ptr(slot_mapping, torch.int64, "slot_mapping") if n_new else None
+    st = lib().oscar_decode_step(
+        ctypes.byref(layout), _ptr(pages, torch.uint8, "pages", pool_bytes(layout)), kp, vp, sp,
+        n_new, float(clip_k), float(clip_v), _ptr(q, torch.bfloat16, "q", B * Hq * d), B, Hq,
+        _ptr(block_table, torch.int32, "block_table", B * mp), mp,
+        _ptr(seq_lens, torch.int32, "seq_lens", B), _ptr(R_k, torch.float32, "R_k", d * d),
+        _ptr(R_v, torch.float32, "R_v", d * d), float(sm_scale), int(num_splits),
+        _ptr(workspace, torch.uint8, "workspace"), workspace.numel(),
+        _ptr(out, out.dtype, "out", B * Hq * d), out_dtype, _stream(stream))
+    _check(st, "oscar_decode_step")
 
 
 def decode_prepare(layout: Layout, q, R_k, sm_scale: float, num_splits: int, workspace,

@@ -94,15 +94,78 @@ __device__ inline uint32_t pack_quad(uint32_t code, int lane) {
   return v;
 }
 
-template <int RW>
-__global__ __launch_bounds__(256) void append_kernel(
-    uint8_t* __restrict__ pages, int Hkv, const uint16_t* __restrict__ k,
-    const uint16_t* __restrict__ v, const int64_t* __restrict__ slots, int n_rows,
-    const float* __restrict__ Rk, const float* __restrict__ Rv, float clip_k, float clip_v) {
-  __shared__ float Rs[kD * kD];
-  __shared__ double xs[kWaves][RW][kD];
+__device__ inline float bf16_to_f32(uint16_t h) { return __uint_as_float(((uint32_t)h) << 16); }
 
-  const int is_v = blockIdx.y;
+// ---------------------------------------------------------------------------
+// prepare: 8 query rows per block.  R_k (64 KB) is copied to LDS once per block;
+// thread (channel j, row group) computes 4 rows of column j, reading R_k[c][j]
+// (consecutive j: no bank conflicts) and the rows' q[c..c+3] (broadcast).
+// ---------------------------------------------------------------------------
+constexpr int kPrepRows = 8;
+
+__device__ inline void prepare_body(float* Rsf, float4 (*qs)[kD / 4], int bx,
+                                    const uint16_t* __restrict__ q, int rows,
+                                    const float* __restrict__ Rk, float qscale,
+                                    float* __restrict__ qt) {
+  float4* Rs = reinterpret_cast<float4*>(Rsf);
+  const int r0 = bx * kPrepRows;
+  const int t = threadIdx.x;
+  if (Rk) {
+    // 16 float4 per thread, all loads issued before the stores (no per-load wait)
+    float4 v[kD * kD / 4 / 256];
+#pragma unroll
+    for (int k = 0; k < kD * kD / 4 / 256; ++k) v[k] = reinterpret_cast<const float4*>(Rk)[t + 256 * k];
+#pragma unroll
+    for (int k = 0; k < kD * kD / 4 / 256; ++k) Rs[t + 256 * k] = v[k];
+  }
+  {  // 8 rows x 128 bf16 = 256 threads x 4 values
+    const int r = t >> 5, c4 = t & 31;
+    float4 x = make_float4(0.0f, 0.0f, 0.0f, 0.0f);
+    if (r0 + r < rows) {
+      const uint2 w = reinterpret_cast<const uint2*>(q + (size_t)(r0 + r) * kD)[c4];
+      x = make_float4(bf16_to_f32((uint16_t)(w.x & 0xffffu)), bf16_to_f32((uint16_t)(w.x >> 16)),
+                      bf16_to_f32((uint16_t)(w.y & 0xffffu)), bf16_to_f32((uint16_t)(w.y >> 16)));
+    }
+    qs[r][c4] = x;
+  }
+  __syncthreads();
+  const int j = t & (kD - 1);
+  const int rg = (t >> 7) * 4;
+  float acc[4] = {0.0f, 0.0f, 0.0f, 0.0f};
+  if (Rk) {
+    const float* R = reinterpret_cast<const float*>(Rs);
+#pragma unroll 4
+    for (int c4 = 0; c4 < kD / 4; ++c4) {
+      const float r_0 = R[(4 * c4 + 0) * kD + j], r_1 = R[(4 * c4 + 1) * kD + j];
+      const float r_2 = R[(4 * c4 + 2) * kD + j], r_3 = R[(4 * c4 + 3) * kD + j];
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const float4 x = qs[rg + i][c4];
+        acc[i] = fmaf(x.x, r_0, acc[i]);
+        acc[i] = fmaf(x.y, r_1, acc[i]);
+        acc[i] = fmaf(x.z, r_2, acc[i]);
+        acc[i] = fmaf(x.w, r_3, acc[i]);
+      }
+    }
+  } else {  // R = I (bf16 baseline)
+    const float* Q = reinterpret_cast<const float*>(qs);
+#pragma unroll
+    for (int i = 0; i < 4; ++i) acc[i] = Q[(rg + i) * kD + j];
+  }
+#pragma unroll
+  for (int i = 0; i < 4; ++i)
+    if (r0 + rg + i < rows) qt[(size_t)(r0 + rg + i) * kD + j] = acc[i] * qscale;
+}
+
+// Cache update by one block: is_v selects K or V, blocks bx of gx take rows
+// grid-stride.  Rs: 64 KB LDS for the matrix, xs: the waves' input rows.
+template <int RW>
+__device__ inline void append_body(float* Rs, double (*xs)[RW][kD], int is_v, int bx, int gx,
+                                   uint8_t* __restrict__ pages, int Hkv,
+                                   const uint16_t* __restrict__ k, const uint16_t* __restrict__ v,
+                                   const int64_t* __restrict__ slots, int n_rows,
+                                   const float* __restrict__ Rk, const float* __restrict__ Rv,
+                                   float clip_k, float clip_v) {
   const float* __restrict__ R = is_v ? Rv : Rk;
   const uint16_t* __restrict__ X = is_v ? v : k;
   const float clip = is_v ? clip_v : clip_k;
@@ -123,7 +186,7 @@ __global__ __launch_bounds__(256) void append_kernel(
   const uint32_t sz_base = is_v ? kOffVSz : kOffKSz;
 
   // each wave owns xs[w]: no block-level synchronization inside the loop
-  for (int item = blockIdx.x * kWaves + w; item < n_items; item += gridDim.x * kWaves) {
+  for (int item = bx * kWaves + w; item < n_items; item += gx * kWaves) {
 #pragma unroll
     for (int rr = 0; rr < RW; ++rr) {
       const int row = item * RW + rr;
@@ -189,22 +252,97 @@ __global__ __launch_bounds__(256) void append_kernel(
   }
 }
 
+template <int RW>
+__global__ __launch_bounds__(256) void append_kernel(
+    uint8_t* __restrict__ pages, int Hkv, const uint16_t* __restrict__ k,
+    const uint16_t* __restrict__ v, const int64_t* __restrict__ slots, int n_rows,
+    const float* __restrict__ Rk, const float* __restrict__ Rv, float clip_k, float clip_v) {
+  __shared__ float Rs[kD * kD];
+  __shared__ double xs[kWaves][RW][kD];
+  append_body<RW>(Rs, xs, blockIdx.y, blockIdx.x, gridDim.x, pages, Hkv, k, v, slots, n_rows, Rk,
+                  Rv, clip_k, clip_v);
+}
+
+__global__ __launch_bounds__(256) void prepare_kernel(const uint16_t* __restrict__ q, int rows,
+                                                      const float* __restrict__ Rk, float qscale,
+                                                      float* __restrict__ qt) {
+  __shared__ float Rs[kD * kD];
+  __shared__ float4 qs[kPrepRows][kD / 4];
+  prepare_body(Rs, qs, blockIdx.x, q, rows, Rk, qscale, qt);
+}
+
+// One launch for a decode step's prologue: blockIdx.y 0/1 = K/V cache update
+// (append_blocks blocks), 2 = query rotation (prep_blocks blocks).  The two are
+// independent; the split kernel that follows needs both.
+template <int RW>
+__global__ __launch_bounds__(256) void prologue_kernel(
+    uint8_t* __restrict__ pages, int Hkv, const uint16_t* __restrict__ k,
+    const uint16_t* __restrict__ v, const int64_t* __restrict__ slots, int n_rows,
+    const float* __restrict__ Rk, const float* __restrict__ Rv, float clip_k, float clip_v,
+    int append_blocks, const uint16_t* __restrict__ q, int q_rows, float qscale,
+    float* __restrict__ qt, int prep_blocks) {
+  __shared__ float Rs[kD * kD];
+  __shared__ double xs[kWaves][RW][kD];
+  __shared__ float4 qs[kPrepRows][kD / 4];
+  if (blockIdx.y < 2) {
+    if ((int)blockIdx.x < append_blocks)
+      append_body<RW>(Rs, xs, blockIdx.y, blockIdx.x, append_blocks, pages, Hkv, k, v, slots,
+                      n_rows, Rk, Rv, clip_k, clip_v);
+  } else if ((int)blockIdx.x < prep_blocks) {
+    prepare_body(Rs, qs, blockIdx.x, q, q_rows, Rk, qscale, qt);
+  }
+}
+
+}  // namespace
+
+namespace {
+int64_t append_blocks_for(int64_t n_rows, int rw) {
+  const int64_t n_items = (n_rows + rw - 1) / rw;
+  const int64_t blocks = (n_items + kWaves - 1) / kWaves;
+  return blocks > 1024 ? 1024 : blocks;
+}
 }  // namespace
 
 hipError_t launch_append(void* pages, int64_t Hkv, const uint16_t* k, const uint16_t* v,
                          const int64_t* slots, int n_tok, const float* Rk, const float* Rv,
                          float clip_k, float clip_v, hipStream_t st) {
   const int64_t n_rows = (int64_t)n_tok * Hkv;
-  auto launch = [&](auto kernel, int rw) {
-    const int64_t n_items = (n_rows + rw - 1) / rw;
-    int64_t blocks = (n_items + kWaves - 1) / kWaves;
-    if (blocks > 1024) blocks = 1024;
-    hipLaunchKernelGGL(kernel, dim3((unsigned)blocks, 2), dim3(256), 0, st,
-                       static_cast<uint8_t*>(pages), (int)Hkv, k, v, slots, (int)n_rows, Rk, Rv,
-                       clip_k, clip_v);
-  };
-  if (n_rows <= 4096) launch(append_kernel<1>, 1);
-  else launch(append_kernel<4>, 4);
+  const int rw = n_rows <= 4096 ? 1 : 4;
+  const dim3 grid((unsigned)append_blocks_for(n_rows, rw), 2);
+  if (rw == 1)
+    hipLaunchKernelGGL(append_kernel<1>, grid, dim3(256), 0, st, static_cast<uint8_t*>(pages),
+                       (int)Hkv, k, v, slots, (int)n_rows, Rk, Rv, clip_k, clip_v);
+  else
+    hipLaunchKernelGGL(append_kernel<4>, grid, dim3(256), 0, st, static_cast<uint8_t*>(pages),
+                       (int)Hkv, k, v, slots, (int)n_rows, Rk, Rv, clip_k, clip_v);
+  return hipGetLastError();
+}
+
+hipError_t launch_decode_prepare(const uint16_t* q, int B, int Hq, const float* Rk,
+                                 float qscale, float* qt, hipStream_t st) {
+  const int rows = B * Hq;
+  hipLaunchKernelGGL(prepare_kernel, dim3((rows + kPrepRows - 1) / kPrepRows), dim3(256), 0, st,
+                     q, rows, Rk, qscale, qt);
+  return hipGetLastError();
+}
+
+hipError_t launch_step_prologue(void* pages, int64_t Hkv, const uint16_t* k, const uint16_t* v,
+                                const int64_t* slots, int n_tok, const float* Rk,
+                                const float* Rv, float clip_k, float clip_v, const uint16_t* q,
+                                int B, int Hq, float qscale, float* qt, hipStream_t st) {
+  const int64_t n_rows = (int64_t)n_tok * Hkv;
+  const int rw = n_rows <= 4096 ? 1 : 4;
+  const int ab = n_rows > 0 ? (int)append_blocks_for(n_rows, rw) : 0;
+  const int pb = (B * Hq + kPrepRows - 1) / kPrepRows;
+  const dim3 grid((unsigned)(ab > pb ? ab : pb), 3);
+  if (rw == 1)
+    hipLaunchKernelGGL(prologue_kernel<1>, grid, dim3(256), 0, st, static_cast<uint8_t*>(pages),
+                       (int)Hkv, k, v, slots, (int)n_rows, Rk, Rv, clip_k, clip_v, ab, q, B * Hq,
+                       qscale, qt, pb);
+  else
+    hipLaunchKernelGGL(prologue_kernel<4>, grid, dim3(256), 0, st, static_cast<uint8_t*>(pages),
+                       (int)Hkv, k, v, slots, (int)n_rows, Rk, Rv, clip_k, clip_v, ab, q, B * Hq,
+                       qscale, qt, pb);
   return hipGetLastError();
 }
 

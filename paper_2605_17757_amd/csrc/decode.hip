@@ -1,6 +1,7 @@
 // Decode attention over the INT2 paged cache (Alg. 1 DecodeStep; Sec. 4
 // "Decoding Attention Kernel"), in three kernels:
 //   prepare : q~ = q R_k * (sm_scale * log2 e)                    [B*Hq, 128] fp32
+//             (in append.hip, where it can share a launch with the cache update)
 //   split   : per (split, kv-head, sequence) block, online softmax over the
 //             split's pages in the rotated basis, unnormalized o~ and (m, l)
 //   reduce  : log-sum-exp merge of the splits, o = o~ R_v^T, bf16/fp32 store
@@ -36,67 +37,6 @@ __device__ inline float wave_sum(float x) {
 #pragma unroll
   for (int m = 32; m >= 1; m >>= 1) x += __shfl_xor(x, m, 64);
   return x;
-}
-
-// ---------------------------------------------------------------------------
-// prepare: 8 query rows per block.  R_k (64 KB) is copied to LDS once per block;
-// thread (channel j, row group) computes 4 rows of column j, reading R_k[c][j]
-// (consecutive j: no bank conflicts) and the rows' q[c..c+3] (broadcast).
-// ---------------------------------------------------------------------------
-constexpr int kPrepRows = 8;
-
-__global__ __launch_bounds__(256) void prepare_kernel(const uint16_t* __restrict__ q, int rows,
-                                                      const float* __restrict__ Rk, float qscale,
-                                                      float* __restrict__ qt) {
-  __shared__ float4 Rs[kD * kD / 4];
-  __shared__ float4 qs[kPrepRows][kD / 4];
-  const int r0 = blockIdx.x * kPrepRows;
-  const int t = threadIdx.x;
-  if (Rk) {
-    // 16 float4 per thread, all loads issued before the stores (no per-load wait)
-    float4 v[kD * kD / 4 / 256];
-#pragma unroll
-    for (int k = 0; k < kD * kD / 4 / 256; ++k) v[k] = reinterpret_cast<const float4*>(Rk)[t + 256 * k];
-#pragma unroll
-    for (int k = 0; k < kD * kD / 4 / 256; ++k) Rs[t + 256 * k] = v[k];
-  }
-  {  // 8 rows x 128 bf16 = 256 threads x 4 values
-    const int r = t >> 5, c4 = t & 31;
-    float4 x = make_float4(0.0f, 0.0f, 0.0f, 0.0f);
-    if (r0 + r < rows) {
-      const uint2 w = reinterpret_cast<const uint2*>(q + (size_t)(r0 + r) * kD)[c4];
-      x = make_float4(bf16_to_f32((uint16_t)(w.x & 0xffffu)), bf16_to_f32((uint16_t)(w.x >> 16)),
-                      bf16_to_f32((uint16_t)(w.y & 0xffffu)), bf16_to_f32((uint16_t)(w.y >> 16)));
-    }
-    qs[r][c4] = x;
-  }
-  __syncthreads();
-  const int j = t & (kD - 1);
-  const int rg = (t >> 7) * 4;
-  float acc[4] = {0.0f, 0.0f, 0.0f, 0.0f};
-  if (Rk) {
-    const float* R = reinterpret_cast<const float*>(Rs);
-#pragma unroll 4
-    for (int c4 = 0; c4 < kD / 4; ++c4) {
-      const float r_0 = R[(4 * c4 + 0) * kD + j], r_1 = R[(4 * c4 + 1) * kD + j];
-      const float r_2 = R[(4 * c4 + 2) * kD + j], r_3 = R[(4 * c4 + 3) * kD + j];
-#pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        const float4 x = qs[rg + i][c4];
-        acc[i] = fmaf(x.x, r_0, acc[i]);
-        acc[i] = fmaf(x.y, r_1, acc[i]);
-        acc[i] = fmaf(x.z, r_2, acc[i]);
-        acc[i] = fmaf(x.w, r_3, acc[i]);
-      }
-    }
-  } else {  // R = I (bf16 baseline)
-    const float* Q = reinterpret_cast<const float*>(qs);
-#pragma unroll
-    for (int i = 0; i < 4; ++i) acc[i] = Q[(rg + i) * kD + j];
-  }
-#pragma unroll
-  for (int i = 0; i < 4; ++i)
-    if (r0 + rg + i < rows) qt[(size_t)(r0 + rg + i) * kD + j] = acc[i] * qscale;
 }
 
 // ---------------------------------------------------------------------------
@@ -294,8 +234,9 @@ __global__ __launch_bounds__(256) void split_kernel(
 // ---------------------------------------------------------------------------
 // reduce: 8 (sequence, head) rows per block.
 //   1. thread (row, 4 channels): M = max_s m_s, L = sum_s 2^(m_s - M) l_s over
-//      the row's splits (empty splits have m_s = -inf), then
-//      o~[c] = sum_s 2^(m_s - M) part_o[s][c] / L with independent loads over s;
+//      the row's splits (empty splits have m_s = -inf and only follow live
+//      ones), then o~[c] = sum_s 2^(m_s - M) part_o[s][c] / L over the live
+//      splits, with independent loads over s;
 //   2. o = o~ R_v^T, R_v copied to LDS with rows padded to 132 floats (16-byte
 //      aligned rows; threads of consecutive j read different banks).
 // ---------------------------------------------------------------------------
@@ -326,14 +267,21 @@ __global__ __launch_bounds__(256) void reduce_kernel(int rows, int num_splits,
     float4 o = make_float4(0.0f, 0.0f, 0.0f, 0.0f);
     if (r < rows) {
       const float2* ml = reinterpret_cast<const float2*>(part_ml + (size_t)r * num_splits * 2);
+      // live slots lead (empty ones only follow the end of a sequence): n_live
+      // is one past the last live slot
       float M = -INFINITY;
+      int n_live = 0;
 #pragma unroll 8
-      for (int s = 0; s < num_splits; ++s) M = fmaxf(M, ml[s].x);
+      for (int s = 0; s < num_splits; ++s) {
+        const float m = ml[s].x;
+        M = fmaxf(M, m);
+        n_live = (m != -INFINITY) ? s + 1 : n_live;
+      }
       if (M != -INFINITY) {
         const float4* po = reinterpret_cast<const float4*>(part_o + (size_t)r * num_splits * kD) + c4;
         float L = 0.0f;
 #pragma unroll 8
-        for (int s = 0; s < num_splits; ++s) {
+        for (int s = 0; s < n_live; ++s) {
           const float2 m = ml[s];
           const float4 x = po[(size_t)s * (kD / 4)];  // loaded unconditionally: no load->branch chain
           const bool live = m.x != -INFINITY;         // an empty split contributes nothing
@@ -395,14 +343,6 @@ hipError_t launch_split_nh(const uint8_t* pages, int Hkv, int B, int Hq, const i
 }
 
 }  // namespace
-
-hipError_t launch_decode_prepare(const uint16_t* q, int B, int Hq, const float* Rk,
-                                 float qscale, float* qt, hipStream_t st) {
-  const int rows = B * Hq;
-  hipLaunchKernelGGL(prepare_kernel, dim3((rows + kPrepRows - 1) / kPrepRows), dim3(256), 0, st,
-                     q, rows, Rk, qscale, qt);
-  return hipGetLastError();
-}
 
 hipError_t launch_decode_split(const uint8_t* pages, int Hkv, int B, int Hq,
                                const int32_t* block_table, int max_pages,

@@ -42,6 +42,11 @@ hipError_t launch_append(void* pages, int64_t Hkv, const uint16_t* k, const uint
 
 hipError_t launch_decode_prepare(const uint16_t* q, int B, int Hq, const float* Rk,
                                  float qscale, float* qt, hipStream_t st);
+// Cache update of n_tok tokens and query rotation in one launch (decode step prologue).
+hipError_t launch_step_prologue(void* pages, int64_t Hkv, const uint16_t* k, const uint16_t* v,
+                                const int64_t* slots, int n_tok, const float* Rk,
+                                const float* Rv, float clip_k, float clip_v, const uint16_t* q,
+                                int B, int Hq, float qscale, float* qt, hipStream_t st);
 hipError_t launch_decode_split(const uint8_t* pages, int Hkv, int B, int Hq,
                                const int32_t* block_table, int max_pages,
                                const int32_t* seq_lens, int num_splits, const float* qt,

@@ -227,6 +227,59 @@ int oscar_decode_attn(const oscar_layout* L, const void* pages, const void* q, i
                              out_dtype, stream);
 }
 
+int oscar_decode_step(const oscar_layout* L, void* pages, const void* k_new, const void* v_new,
+                      const int64_t* slot_mapping, int32_t n_new, float clip_k, float clip_v,
+                      const void* q, int32_t B, int32_t Hq, const int32_t* block_table,
+                      int32_t max_pages_per_seq, const int32_t* seq_lens, const float* R_k,
+                      const float* R_v, float sm_scale, int32_t num_splits, void* workspace,
+                      size_t workspace_bytes, void* out, oscar_dtype out_dtype, void* stream) {
+  // append arguments (as oscar_kv_append)
+  int st = check_layout(L);
+  if (st) return st;
+  if (n_new < 0 || !clip_ok(clip_k) || !clip_ok(clip_v)) return OSCAR_ERR_INVALID_ARG;
+  if (n_new > 0) {
+    if (!k_new || !v_new || !slot_mapping) return OSCAR_ERR_INVALID_ARG;
+    if (!aligned(k_new, 4) || !aligned(v_new, 4) || !aligned(slot_mapping, 8))
+      return OSCAR_ERR_INVALID_ARG;
+    if ((int64_t)n_new * L->num_kv_heads > 0x7fffffffLL) return OSCAR_ERR_UNSUPPORTED;
+  }
+  // decode arguments (as oscar_decode_attn)
+  if (num_splits < 0) return OSCAR_ERR_INVALID_ARG;
+  if (num_splits == 0) {
+    num_splits = resolve_default_splits(L, B, Hq, max_pages_per_seq);
+    if (num_splits < 1) return num_splits == 0 ? OSCAR_ERR_INVALID_ARG : -num_splits;
+  }
+  st = check_decode_common(L, B, Hq, num_splits);
+  if (st) return st;
+  if (!pages || !q || !block_table || !seq_lens || !R_k || !R_v || !workspace || !out ||
+      max_pages_per_seq < 1 || !isfinite(sm_scale))
+    return OSCAR_ERR_INVALID_ARG;
+  if (out_dtype != OSCAR_OUT_BF16 && out_dtype != OSCAR_OUT_F32) return OSCAR_ERR_INVALID_ARG;
+  if (!aligned(workspace, 256) || !aligned(pages, 16) || !aligned(q, 4) || !aligned(R_k, 16) ||
+      !aligned(R_v, 16) || !aligned(out, out_dtype == OSCAR_OUT_F32 ? 4 : 2))
+    return OSCAR_ERR_INVALID_ARG;
+  const DecodeWs ws = decode_ws(B, Hq, num_splits);
+  if (workspace_bytes < ws.total) return OSCAR_ERR_WORKSPACE_TOO_SMALL;
+  hipStream_t hs = static_cast<hipStream_t>(stream);
+  uint8_t* base = static_cast<uint8_t*>(workspace);
+  float* qt = reinterpret_cast<float*>(base + ws.qt_off);
+  st = hip_status(launch_step_prologue(pages, L->num_kv_heads,
+                                       static_cast<const uint16_t*>(k_new),
+                                       static_cast<const uint16_t*>(v_new), slot_mapping, n_new,
+                                       R_k, R_v, clip_k, clip_v, static_cast<const uint16_t*>(q),
+                                       B, Hq, sm_scale * kLog2e, qt, hs));
+  if (st) return st;
+  st = hip_status(launch_decode_split(
+      static_cast<const uint8_t*>(pages), L->num_kv_heads, B, Hq, block_table, max_pages_per_seq,
+      seq_lens, num_splits, qt, reinterpret_cast<float*>(base + ws.po_off),
+      reinterpret_cast<float*>(base + ws.pml_off), hs));
+  if (st) return st;
+  return hip_status(launch_decode_reduce(B, Hq, num_splits,
+                                         reinterpret_cast<const float*>(base + ws.po_off),
+                                         reinterpret_cast<const float*>(base + ws.pml_off), R_v,
+                                         out, out_dtype == OSCAR_OUT_F32 ? 1 : 0, hs));
+}
+
 // ---------------------------------------------------------------------------
 // bf16 baseline
 // ---------------------------------------------------------------------------

@@ -113,6 +113,25 @@ def test_decode_rejects_invalid_arguments(L):
                                     2, FAKE, 1 << 30, FAKE, 0, None) == ok.ERR_INVALID_ARG
 
 
+def _step(L, lay, n_new=4, clip_k=0.9, B=2, Hq=32, S=2, ws_bytes=1 << 30, k=FAKE, slots=FAKE):
+    return L.oscar_decode_step(ctypes.byref(lay), FAKE, k, FAKE, slots, n_new, clip_k, 0.9, FAKE,
+                               B, Hq, FAKE, 4, FAKE, FAKE, FAKE, 0.088, S, FAKE, ws_bytes, FAKE,
+                               0, None)
+
+
+def test_decode_step_validates_both_halves(L):
+    lay = ok.Layout(8, 10)
+    assert _step(L, lay, clip_k=2.0) == ok.ERR_INVALID_ARG          # append half
+    assert _step(L, lay, n_new=-1) == ok.ERR_INVALID_ARG
+    assert _step(L, lay, k=None) == ok.ERR_INVALID_ARG
+    assert _step(L, lay, slots=ctypes.c_void_p(0x10004)) == ok.ERR_INVALID_ARG  # misaligned
+    assert _step(L, lay, Hq=30) == ok.ERR_INVALID_ARG               # decode half
+    assert _step(L, lay, S=-1) == ok.ERR_INVALID_ARG
+    need = ok.decode_workspace_bytes(lay, 2, 32, 2)
+    assert _step(L, lay, ws_bytes=need - 1) == ok.ERR_WORKSPACE_TOO_SMALL
+    assert _step(L, ok.Layout(8, 10, head_dim=64)) == ok.ERR_UNSUPPORTED
+
+
 def test_stage_entry_points_validate(L):
     lay = ok.Layout(8, 10)
     need = ok.decode_workspace_bytes(lay, 2, 32, 2)

@@ -131,6 +131,50 @@ def test_decode_stages_equal_single_call():
     assert torch.equal(out_a.cpu(), out_b.cpu())
 
 
+def test_decode_step_equals_append_then_attn():
+    """oscar_decode_step (cache update and query rotation in one launch, then
+    split and reduce) writes the same page bytes and returns the same output,
+    bit for bit, as oscar_kv_append followed by oscar_decode_attn; with no new
+    token it equals oscar_decode_attn."""
+    cfg = W.custom("step", 3, 16, 4, [300, 64, 1000], seed_index=83)
+    case = make_case(cfg)
+    lay = case.layout
+    last = np.cumsum(cfg.lens) - 1                    # each sequence's newest token
+    prev = np.setdiff1d(np.arange(len(case.slots)), last)
+    Rk = torch.from_numpy(case.Rk).cuda()
+    Rv = torch.from_numpy(case.Rv).cuda()
+    pool = ok.alloc_pool(lay)
+    ok.kv_append(lay, pool, case.k[prev].cuda(), case.v[prev].cuda(),
+                 torch.from_numpy(case.slots[prev]).cuda(), Rk, Rv, cfg.clip_k, cfg.clip_v)
+    new_k, new_v = case.k[last].cuda(), case.v[last].cuda()
+    new_s = torch.from_numpy(case.slots[last]).cuda()
+    q = case.q.cuda()
+    bt = torch.from_numpy(case.table).cuda()
+    sl = torch.from_numpy(cfg.lens).cuda()
+    S = 6
+    pool_a, pool_b = pool.clone(), pool.clone()
+    out_a = torch.empty(cfg.B, cfg.Hq, 128, dtype=torch.float32, device="cuda")
+    out_b = torch.empty_like(out_a)
+    ws_a = ok.alloc_workspace(lay, cfg.B, cfg.Hq, S)
+    ws_b = ok.alloc_workspace(lay, cfg.B, cfg.Hq, S)
+    ok.kv_append(lay, pool_a, new_k, new_v, new_s, Rk, Rv, cfg.clip_k, cfg.clip_v)
+    ok.decode_attn(lay, pool_a, q, bt, sl, Rk, Rv, cfg.sm_scale, S, ws_a, out_a)
+    ok.decode_step(lay, pool_b, new_k, new_v, new_s, cfg.clip_k, cfg.clip_v, q, bt, sl, Rk, Rv,
+                   cfg.sm_scale, S, ws_b, out_b)
+    torch.cuda.synchronize()
+    assert torch.equal(pool_a, pool_b)
+    assert torch.equal(out_a, out_b)
+    ref = oracle_decode(case, oracle_append(case))
+    assert max_abs(out_b, ref) <= DECODE_TOL
+    # no new token: the step is the decode alone
+    out_c = torch.empty_like(out_a)
+    empty = torch.empty(0, dtype=torch.int64, device="cuda")
+    ok.decode_step(lay, pool_b, None, None, empty, cfg.clip_k, cfg.clip_v, q, bt, sl, Rk, Rv,
+                   cfg.sm_scale, S, ws_b, out_c)
+    torch.cuda.synchronize()
+    assert torch.equal(out_a, out_c)
+
+
 def test_append_fuzz_edge_rows():
     rng = np.random.default_rng(11)
     Hkv, num_pages = 3, 40
