@@ -283,7 +283,7 @@ def main():
         "roofline": {
             "kernel": "decode_split", "bound": "hbm", "achieved": round(achieved, 1),
             "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4),
-            "traffic": None, "bytes_per_launch": split_bytes,
+            "traffic": split_traffic(), "bytes_per_launch": split_bytes,
         },
         "bytes": {"int2_kv": kv_bytes, "block_table": table_bytes, "q_and_out": qo_bytes,
                   "append": append_bytes, "step_total": step_bytes,
@@ -335,6 +335,22 @@ def main():
         res["cpu_baseline"] = cpu_baseline(cfg, table, Rk_np, Rv_np, q, args.cpu_seconds)
 
     print(json.dumps(res), flush=True)
+
+
+def split_traffic():
+    """HBM bytes per split launch from the committed rocprofv3 FETCH_SIZE /
+    WRITE_SIZE passes (scaled by a 1 GiB copy's counters), or None when the
+    split kernel's source has changed since those counters were taken."""
+    import hashlib
+    rec_path = os.path.join(ROOT, "profiles", "split_mfma_kernel_traffic.json")
+    try:
+        rec = json.load(open(rec_path))
+        src = open(os.path.join(ROOT, rec["source"]), "rb").read()
+    except (OSError, ValueError, KeyError):
+        return None
+    if hashlib.sha256(src).hexdigest() != rec.get("source_sha256"):
+        return None
+    return int(rec["traffic_bytes_per_launch"])
 
 
 def cpu_baseline(cfg, table, Rk_np, Rv_np, q, seconds, max_seqs=4):
