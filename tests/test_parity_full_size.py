@@ -1,0 +1,110 @@
+"""Full-size parity on sampled outputs.
+
+The bench workload (config 2: 64 sequences of 16k-32k tokens, 32/8 heads) and
+configs 3 and 4 at their full shapes, in the launch configuration bench.py
+times: the cache holds tokens 0..len-2 of every sequence, then one
+oscar_decode_step appends each sequence's newest token and decodes the whole
+batch with the default split count.  The GPU runs the whole batch; the oracle
+appends and decodes only the sampled sequences (all query heads of each),
+which is all that their outputs and pages depend on.  Compared: every output
+element of the sampled sequences (2e-3 on fp32) and every byte of their pages
+(bit-exact, near-boundary rule of helpers.compare_pools)."""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import paper_2605_17757_amd as ok
+import workloads as W
+from helpers import DECODE_TOL, Case, bits, compare_pools, log, max_abs
+
+pytestmark = pytest.mark.gpu
+
+
+def _full_size(cfg: W.Config, sample_b):
+    B, Hq, Hkv, d = cfg.B, cfg.Hq, cfg.Hkv, cfg.d
+    lens = cfg.lens.astype(np.int64)
+    table, num_pages = W.block_table(cfg)
+    lay = ok.Layout(num_kv_heads=Hkv, num_pages=num_pages)
+    Rk_np, Rv_np = W.rotations(cfg)
+    Rk = torch.from_numpy(Rk_np).cuda()
+    Rv = torch.from_numpy(Rv_np).cuda()
+    log("full size", cfg.name, "B", B, "Hq", Hq, "Hkv", Hkv, "pages", num_pages,
+        "sampled", list(sample_b))
+
+    # The sampled sequences' rows are drawn once on the CPU and used by both sides;
+    # the other sequences (which the sampled outputs do not read) are drawn on the
+    # GPU, whose generator gives different numbers.
+    host_kv = {b: W.cache_kv(cfg, b) for b in sample_b}
+
+    # ---- GPU: the whole batch, as the bench runs it ----
+    pool = ok.alloc_pool(lay)
+    new_k = torch.empty(B, Hkv, d, dtype=torch.bfloat16, device="cuda")
+    new_v = torch.empty_like(new_k)
+    new_slots = np.zeros(B, np.int64)
+    for b in range(B):
+        if b in host_kv:
+            k, v = host_kv[b][0].cuda(), host_kv[b][1].cuda()
+        else:
+            k, v = W.cache_kv(cfg, b, device="cuda")
+        n = int(lens[b])
+        slots = W.slots_for(table, b, np.arange(n))
+        ok.kv_append(lay, pool, k[:n - 1], v[:n - 1], torch.from_numpy(slots[:n - 1]).cuda(),
+                     Rk, Rv, cfg.clip_k, cfg.clip_v)
+        new_k[b], new_v[b], new_slots[b] = k[n - 1], v[n - 1], slots[n - 1]
+        del k, v
+    S = ok.default_num_splits(lay, B, Hq, int(table.shape[1]) * 64)
+    S = max(S, cfg.min_splits)
+    ws = ok.alloc_workspace(lay, B, Hq, S)
+    q = W.queries(cfg)
+    out = torch.empty(B, Hq, d, dtype=torch.float32, device="cuda")
+    ok.decode_step(lay, pool, new_k, new_v, torch.from_numpy(new_slots).cuda(), cfg.clip_k,
+                   cfg.clip_v, q.cuda(), torch.from_numpy(table).cuda(),
+                   torch.from_numpy(cfg.lens).cuda(), Rk, Rv, cfg.sm_scale, S, ws, out)
+    torch.cuda.synchronize()
+    log("  gpu done, splits", S)
+
+    # ---- oracle: the sampled sequences only ----
+    ora = np.zeros(ok.pool_bytes(lay), np.uint8)
+    ks, vs, ss = [], [], []
+    for b in sample_b:
+        k, v = host_kv[b]
+        slots = W.slots_for(table, b, np.arange(int(lens[b])))
+        oracle.kv_append(ora, d=d, Hkv=Hkv, P=64, G=32, k=bits(k), v=bits(v), slot_mapping=slots,
+                         Rk=Rk_np, Rv=Rv_np, clip_k=cfg.clip_k, clip_v=cfg.clip_v)
+        ks.append(k)
+        vs.append(v)
+        ss.append(slots)
+    pairs = np.array([(b, h) for b in sample_b for h in range(Hq)], np.int32)
+    ref = oracle.decode(ora, d=d, Hkv=Hkv, P=64, G=32, q=bits(q), block_table=table,
+                        seq_lens=cfg.lens, Rk=Rk_np, Rv=Rv_np, sm_scale=cfg.sm_scale, pairs=pairs)
+    got = out[torch.as_tensor(np.asarray(sample_b))].reshape(-1, d)
+    err = max_abs(got, ref)
+    log("  decode max|err| over %d (seq, head) rows = %.3g" % (len(pairs), err))
+    assert err <= DECODE_TOL
+
+    # ---- page bytes of the sampled sequences ----
+    bph = ok.page_bytes(lay)
+    gpu_sel = np.zeros_like(ora)
+    pool_pages = pool.view(num_pages, bph)
+    for b in sample_b:
+        ids = table[b, :(int(lens[b]) + 63) // 64]
+        gpu_sel.reshape(num_pages, bph)[ids] = pool_pages[torch.from_numpy(ids).cuda()].cpu().numpy()
+    case = Case(cfg, Rk_np, Rv_np, table, num_pages, q, torch.cat(ks), torch.cat(vs),
+                np.concatenate(ss))
+    nd, nt = compare_pools(gpu_sel, ora, case)
+    log("  append: differing bytes", nd, "tolerated near-boundary rows", nt)
+
+
+def test_full_size_bench_workload_qwen3_8b_b64():
+    cfg = W.config(2, batch=64)
+    lens = cfg.lens
+    _full_size(cfg, sorted({0, int(np.argmax(lens)), int(np.argmin(lens))}))
+
+
+def test_full_size_qwen3_32b_b128_ctx32k():
+    _full_size(W.config(3), [0, 127])
+
+
+def test_full_size_longctx_b16_ctx128k():
+    _full_size(W.config(4), [5])
