@@ -47,43 +47,66 @@ __global__ __launch_bounds__(256) void reduce_kernel(int rows, int num_splits,
   __shared__ float4 om[kRedRows][kD / 4];
   const int r0 = blockIdx.x * kRedRows;
   const int t = threadIdx.x;
-  if (Rv) {
-    float4 v[kD * kD / 4 / 256];  // 16 float4 per thread, loads issued before the stores
-#pragma unroll
-    for (int k = 0; k < kD * kD / 4 / 256; ++k) v[k] = reinterpret_cast<const float4*>(Rv)[t + 256 * k];
-#pragma unroll
-    for (int k = 0; k < kD * kD / 4 / 256; ++k) {
-      const int i = t + 256 * k;
-      Rs[(i >> 5) * kRvPitch4 + (i & 31)] = v[k];
-    }
-  }
   {  // 8 rows x 32 float4 columns: one (row, float4) per thread
     const int rr = t >> 5, c4 = t & 31, r = r0 + rr;
     float4 o = make_float4(0.0f, 0.0f, 0.0f, 0.0f);
-    if (r < rows) {
-      const float2* ml = reinterpret_cast<const float2*>(part_ml + (size_t)r * num_splits * 2);
-      // live slots lead (empty ones only follow the end of a sequence): n_live
-      // is one past the last live slot
-      float M = -INFINITY;
-      int n_live = 0;
-#pragma unroll 8
-      for (int s = 0; s < num_splits; ++s) {
+    const float2* ml = reinterpret_cast<const float2*>(part_ml + (size_t)r * num_splits * 2);
+    // live slots lead (empty ones only follow the end of a sequence): n_live is
+    // one past the last live slot.  Slot s is read by thread s % 32 of the row;
+    // maximum and last live slot are then reduced over the row's 32 threads.
+    float M = -INFINITY;
+    int n_live = 0;
+    const float m0 = (r < rows && c4 < num_splits) ? ml[c4].x : -INFINITY;
+    // R_v (row-major 128 x 128) to LDS, 16 float4 per thread: loads issued here so
+    // that they overlap the slot loads
+    float4 v[kD * kD / 4 / 256];
+    if (Rv) {
+#pragma unroll
+      for (int k = 0; k < kD * kD / 4 / 256; ++k) v[k] = reinterpret_cast<const float4*>(Rv)[t + 256 * k];
+    }
+    if (Rv) {
+#pragma unroll
+      for (int k = 0; k < kD * kD / 4 / 256; ++k) {
+        const int i = t + 256 * k;
+        Rs[(i >> 5) * kRvPitch4 + (i & 31)] = v[k];
+      }
+    }
+    M = m0;
+    n_live = m0 != -INFINITY ? c4 + 1 : 0;
+    if (r < rows)
+      for (int s = c4 + 32; s < num_splits; s += 32) {
         const float m = ml[s].x;
         M = fmaxf(M, m);
         n_live = (m != -INFINITY) ? s + 1 : n_live;
       }
+#pragma unroll
+    for (int off = 16; off >= 1; off >>= 1) {
+      M = fmaxf(M, __shfl_xor(M, off, 32));
+      n_live = max(n_live, __shfl_xor(n_live, off, 32));
+    }
+    if (r < rows) {
       if (M != -INFINITY) {
         const float4* po = reinterpret_cast<const float4*>(part_o + (size_t)r * num_splits * kD) + c4;
         float L = 0.0f;
-#pragma unroll 8
-        for (int s = 0; s < n_live; ++s) {
-          const float2 m = ml[s];
-          const float4 x = po[(size_t)s * (kD / 4)];  // loaded unconditionally: no load->branch chain
-          const bool live = m.x != -INFINITY;         // an empty split contributes nothing
-          const float e = live ? exp2f(m.x - M) : 0.0f;
-          L = fmaf(e, live ? m.y : 0.0f, L);
-          o.x = fmaf(e, live ? x.x : 0.0f, o.x); o.y = fmaf(e, live ? x.y : 0.0f, o.y);
-          o.z = fmaf(e, live ? x.z : 0.0f, o.z); o.w = fmaf(e, live ? x.w : 0.0f, o.w);
+        // up to 16 slots per round, loads issued together (indices clamped to the
+        // live range, weights of the clamped repeats set to 0)
+        for (int s0 = 0; s0 < n_live; s0 += 16) {
+          float2 m[16];
+          float4 x[16];
+#pragma unroll
+          for (int k = 0; k < 16; ++k) {
+            const int s = min(s0 + k, n_live - 1);
+            m[k] = ml[s];
+            x[k] = po[(size_t)s * (kD / 4)];
+          }
+#pragma unroll
+          for (int k = 0; k < 16; ++k) {
+            const bool use = s0 + k < n_live && m[k].x != -INFINITY;  // empty slots add nothing
+            const float e = use ? exp2f(m[k].x - M) : 0.0f;
+            L = fmaf(e, use ? m[k].y : 0.0f, L);
+            o.x = fmaf(e, use ? x[k].x : 0.0f, o.x); o.y = fmaf(e, use ? x[k].y : 0.0f, o.y);
+            o.z = fmaf(e, use ? x[k].z : 0.0f, o.z); o.w = fmaf(e, use ? x[k].w : 0.0f, o.w);
+          }
         }
         const float il = L > 0.0f ? 1.0f / L : 0.0f;
         o.x *= il; o.y *= il; o.z *= il; o.w *= il;

@@ -1,9 +1,8 @@
 // Split kernel of INT2 decode attention on the matrix cores (gfx950 int8 MFMA).
-// One wave per (split, kv-head, sequence, chunk of 4 query heads); the wave walks
-// its pages (64 tokens each) and keeps the online-softmax state of its 4 heads in
-// registers.  Waves of the same (split, kv-head, sequence) and different chunks
-// get workgroup ids that are equal modulo 8, so under round-robin dispatch over
-// the 8 XCDs they share one XCD's L2 for the page data they both read.
+// Persistent waves: each wave owns one (page range, kv-head, chunk of 4 query
+// heads), walks the range's pages (64 tokens each) and keeps the online-softmax
+// state of its 4 heads in registers; a range that crosses sequence boundaries
+// writes one partial state per sequence piece (see split_mfma_kernel).
 //
 // Arithmetic (Sec. 2: K^ = Q(K R) R^T; Alg. 1 DecodeStep), per 32-channel group g
 // with Q(x~)_c = s_g (code_c - z_g):
@@ -15,11 +14,12 @@
 //     q_int = 65536 d_0 + 256 d_1 + d_2; the codes are int8 0..3.  The three
 //     digits are three rows of one MFMA, combined as ((a_0 << 8) + a_1) << 8 + a_2,
 //     exact in int32 (|.| <= 32 * 3 * Q < 2^31).
-//   * w of a (head, group) row on one page is scaled to [0, Q] (scale: the page's
-//     p_max of the head times the largest V scale of the group) and split the
-//     same way; the V codes are the other operand (|.| <= 64 * 3 * Q < 2^31).
-// The products are exact, so the approximations are the 24-bit quantization of
-// q~ and of w (relative 2^-24 of the largest value) and fp32 accumulation.
+//   * w of a (head, group) row on one page is scaled to [0, 2^21] (scale: the
+//     page's p_max of the head times the largest V scale of the group) and split
+//     the same way; the V codes are the other operand, taken as code or 4 x code
+//     (|.| <= 64 * 12 * 2^21 < 2^31).
+// The products are exact, so the approximations are the quantization of q~ (24
+// bits) and of w (21 bits), relative to the largest value, and fp32 accumulation.
 //
 // Data path.  Each page-head block (6144 B) is read with six coalesced 16-byte
 // loads per lane into registers (issued one page ahead) and stored to a per-wave
@@ -54,7 +54,8 @@ namespace {
 
 typedef int v4i __attribute__((ext_vector_type(4)));
 
-constexpr float kQMax = 8355000.0f;        // 3-digit split keeps the top digit in int8
+constexpr float kQMax = 8355000.0f;        // q~ scale: the 3-digit split keeps the top digit in int8
+constexpr float kWMax = 2097152.0f;        // w scale 2^21: 64 * 12 * 2^21 < 2^31 (P.V columns may be x4)
 constexpr float kMagic = 8388608.0f;       // 2^23: x + 2^23 (0 <= x < 2^23) has x in its mantissa
 constexpr float kDigitBias = 32896.0f;     // 128 + 128 * 256 (offset of the two low digits)
 constexpr int kNDig = 3;                   // int8 digits per scaled value (most significant first)
@@ -114,10 +115,11 @@ __device__ inline float mix_nhi(uint32_t h, float b, float c) {  // -hi(h) * b +
   return r;
 }
 
-typedef unsigned short us2 __attribute__((ext_vector_type(2)));
-__device__ inline uint32_t max_u16x2(uint32_t a, uint32_t b) {
-  const us2 r = __builtin_elementwise_max(__builtin_bit_cast(us2, a), __builtin_bit_cast(us2, b));
-  return __builtin_bit_cast(uint32_t, r);
+// unsigned maximum of the low halves of three words (high half of the result unused)
+__device__ inline uint32_t max3_lo16(uint32_t a, uint32_t b, uint32_t c) {
+  uint32_t r;
+  asm("v_max3_u16 %0, %1, %2, %3" : "=v"(r) : "v"(a), "v"(b), "v"(c));
+  return r;
 }
 
 __device__ inline float h_lo(uint32_t w) { return __half2float(__ushort_as_half((uint16_t)(w & 0xffffu))); }
@@ -256,6 +258,8 @@ __device__ inline void compute_page(WaveState& st, WaveLds& L, int ntok, int lo,
     if (valid(u)) mx = fmaxf(mx, S[u]);
   mx = row16_max(mx) * st.sq;  // sq > 0; at least one valid token per page
   const float mn = fmaxf(st.m, mx);
+  // the running maxima of the wave's heads change on few pages: when none does,
+  // alpha = 1 and the rescaling below is skipped (same results)
   const float alpha = ex2(st.m - mn);  // m = -inf on the first page -> 0
   const float pmax = ex2(mx - mn);
   float p[4];
@@ -287,17 +291,16 @@ __device__ inline void compute_page(WaveState& st, WaveLds& L, int ntok, int lo,
     if (!FULL && 16 * hi + e >= ntok) sz[e] = 0u;  // (0, 0): w = 0, z = 0
   }
   // largest V scale of the group on this page: scales are positive binary16, so
-  // their bit patterns order like their values (packed u16 max; high halves ignored)
-  uint32_t m8[8];
+  // their bit patterns order like their values (high halves, the zero points, ignored)
+  uint32_t m5[6];
 #pragma unroll
-  for (int e = 0; e < 8; ++e) m8[e] = max_u16x2(sz[e], sz[e + 8]);
-#pragma unroll
-  for (int e = 0; e < 4; ++e) m8[e] = max_u16x2(m8[e], m8[e + 4]);
-  const uint32_t smax = max_u16x2(max_u16x2(m8[0], m8[2]), max_u16x2(m8[1], m8[3]));
+  for (int e = 0; e < 5; ++e) m5[e] = max3_lo16(sz[3 * e], sz[3 * e + 1], sz[3 * e + 2]);
+  m5[5] = sz[15];
+  const uint32_t smax = max3_lo16(max3_lo16(m5[0], m5[1], m5[2]), max3_lo16(m5[3], m5[4], m5[5]), 0u);
   const float svmax = rows_max(h_lo(smax));
   const float sig = hsw.y * svmax;  // >= every w of the row on this page
-  const float inv = sig > 0.0f ? kQMax * __builtin_amdgcn_rcpf(sig) : 0.0f;
-  L.ws[lo] = sig * (1.0f / kQMax);
+  const float inv = sig > 0.0f ? kWMax * __builtin_amdgcn_rcpf(sig) : 0.0f;
+  L.ws[lo] = sig * (1.0f / kWMax);
   float zp = 0.0f;
   uint32_t aw[kNDig][4];
 #pragma unroll
@@ -307,10 +310,10 @@ __device__ inline void compute_page(WaveState& st, WaveLds& L, int ntok, int lo,
     for (int b = 0; b < 4; ++b) {
       const int e = 4 * j + b;
       const float w = mix_lo(sz[e], compf(pw[j], b), 0.0f);
-      // mantissa of rne(w * inv) + 2^23 + 32896 = k + 32896, k in [0, Q]:
+      // mantissa of rne(w * inv) + 2^23 + 32896 = k + 32896, k in [0, 2^21]:
       // k = 65536 d_0 + 256 d_1 + d_2 with d_2, d_1 = (bytes 0, 1) ^ 0x80, d_0 = byte 2
       f[b] = __float_as_uint(fmaf(w, inv, kMagic + kDigitBias));
-      zp = mix_hi(sz[e], w, zp);  // unquantized w: differs from the quantized by <= 2^-24 sig
+      zp = mix_hi(sz[e], w, zp);  // unquantized w: differs from the quantized by <= 2^-22 sig
     }
     const uint32_t t01 = __builtin_amdgcn_perm(f[1], f[0], 0x05010400u) ^ 0x80808080u;  // [f0.0 f1.0 f0.1 f1.1]
     const uint32_t t23 = __builtin_amdgcn_perm(f[3], f[2], 0x05010400u) ^ 0x80808080u;
@@ -330,7 +333,9 @@ __device__ inline void compute_page(WaveState& st, WaveLds& L, int ntok, int lo,
 
   // ---- P.V on the matrix cores: lane (channel column, head hi) ----
   const float4 ws = *reinterpret_cast<const float4*>(&L.ws[4 * hi]);
-  const uint32_t sh = 2u * (uint32_t)(lo >> 3);
+  // B operand: field 2F + (lo>>3) of each token's byte, taken in place by the mask
+  // mk = 3 << 2(lo>>3): columns lo >= 8 hold 4 x code (undone when the state is written)
+  const uint32_t mk = 0x03030303u << (2 * (lo >> 3));
   // V codes of quad 8G + (lo&7), tokens 16*hi + (0..15)
   const char* vb = pb + kLdsVCodes + 16 * (4 * (lo & 7) + (hi ^ (((lo >> 2) & 1) << 1)));
   // A operand row (head lo>>2, digit lo&3); the padding digit row reads digit 2
@@ -340,12 +345,10 @@ __device__ inline void compute_page(WaveState& st, WaveLds& L, int ntok, int lo,
     const uint4 a4 = *reinterpret_cast<const uint4*>(ab + 16 * w_base(G));
     const v4i aop = {(int)a4.x, (int)a4.y, (int)a4.z, (int)a4.w};
     const uint4 x = *reinterpret_cast<const uint4*>(vb + 512 * G);  // quad 8G + (lo&7)
-    const uint4 y = make_uint4(x.x >> sh, x.y >> sh, x.z >> sh, x.w >> sh);
 #pragma unroll
     for (int F = 0; F < 2; ++F) {
-      const uint32_t msk = 0x03030303u;
-      const v4i bv = {(int)((y.x >> (4 * F)) & msk), (int)((y.y >> (4 * F)) & msk),
-                      (int)((y.z >> (4 * F)) & msk), (int)((y.w >> (4 * F)) & msk)};
+      const v4i bv = {(int)((x.x >> (4 * F)) & mk), (int)((x.y >> (4 * F)) & mk),
+                      (int)((x.z >> (4 * F)) & mk), (int)((x.w >> (4 * F)) & mk)};
       const v4i d = mfma64(aop, bv);
       const int t = combine3(d[0], d[1], d[2]);
       float& o = st.of[2 * G + F];
@@ -473,12 +476,13 @@ __device__ __attribute__((always_inline)) inline void process_piece(WaveLds& L, 
       part_ml[(row + s2 - piece) * 2 + 1] = 0.0f;
     }
   const bool empty = st.m == -INFINITY;
+  const float cs = lo >= 8 ? 0.25f : 1.0f;  // P.V columns lo >= 8 accumulate 4 x code
 #pragma unroll
   for (int G = 0; G < 4; ++G) {
 #pragma unroll
     for (int F = 0; F < 2; ++F) {
       const int ch = 32 * G + 4 * (lo & 7) + 2 * F + (lo >> 3);
-      part_o[row * kD + ch] = empty ? 0.0f : st.of[2 * G + F] - compf(zh, G);
+      part_o[row * kD + ch] = empty ? 0.0f : fmaf(st.of[2 * G + F], cs, -compf(zh, G));
     }
   }
   if (lo == 0) {
