@@ -360,12 +360,14 @@ __device__ inline void compute_page(WaveState& st, WaveLds& L, int ntok, int lo,
 // Pages [p0, p1) of sequence b, kv-head kvh, query-head chunk `chunk`: online
 // softmax over the pages and the partial state written to slot `piece` of the
 // (sequence, head) rows.  `last`: the piece ends the sequence, so the slots
-// after it are marked empty.
+// after it are marked empty.  The wave has done `done0` of its `total` pages
+// before this piece (issue-priority bands).
 __device__ __attribute__((always_inline)) inline void process_piece(WaveLds& L, const uint8_t* __restrict__ pages, int Hkv, int Hq,
                                      const int32_t* __restrict__ block_table, int max_pages, int b,
                                      int len, int kvh, int chunk, int p0, int p1, int piece,
                                      bool last, int num_splits, const float* __restrict__ qt,
-                                     float* __restrict__ part_o, float* __restrict__ part_ml) {
+                                     float* __restrict__ part_o, float* __restrict__ part_ml,
+                                     int done0, int total) {
   const int g_heads = Hq / Hkv;
   const int l = threadIdx.x, lo = l & 15, hi = l >> 4;
   const int npg = (len + kP - 1) / kP;
@@ -447,15 +449,30 @@ __device__ __attribute__((always_inline)) inline void process_piece(WaveLds& L, 
   if (p0 < p1) stage_load(sg, base + (size_t)__builtin_amdgcn_readlane(btv, 0) * page_stride, l);
   // pages [p0, pf) are full; page pf (if < p1) is the sequence's partial last page
   const int pf = (p0 < p1 && p1 == npg && (len & (kP - 1)) != 0) ? p1 - 1 : p1;
-  for (int pg = p0; pg < pf; ++pg) {
-    stage_store(L.page, sg, l);
-    const int nx = min(pg + 1, p1 - 1);  // page pg+1 (the last page again at the end)
-    if (nx - cb >= 64) {                 // uniform: next 64 entries
-      cb += 64;
-      btv = (cb + l < p1) ? bt[cb + l] : 0;
+  // Full pages in four bands of the wave's whole page count (done0 pages of it
+  // before this piece, total in all): the wave lowers its issue priority at
+  // 25 %, 50 % and 75 % of its pages.  Waves sharing a SIMD otherwise issue in age
+  // order, and the youngest of them finished up to 1.7x later than the oldest
+  // with the same page count; waves that are behind now go first.
+  int pg = p0;
+  for (int band = 1; band <= 4; ++band) {
+    const int lim = (int)(((int64_t)(25 * band) * total + 99) / 100) - done0 + p0;  // band end
+    const int e = min(max(lim, pg), pf);
+    for (; pg < e; ++pg) {
+      stage_store(L.page, sg, l);
+      const int nx = min(pg + 1, p1 - 1);  // page pg+1 (the last page again at the end)
+      if (nx - cb >= 64) {                 // uniform: next 64 entries
+        cb += 64;
+        btv = (cb + l < p1) ? bt[cb + l] : 0;
+      }
+      stage_load(sg, base + (size_t)__builtin_amdgcn_readlane(btv, nx - cb) * page_stride, l);
+      compute_page<true>(st, L, kP, lo, hi);
     }
-    stage_load(sg, base + (size_t)__builtin_amdgcn_readlane(btv, nx - cb) * page_stride, l);
-    compute_page<true>(st, L, kP, lo, hi);
+    if (band < 4 && lim > p0 && lim <= pf) {  // the band ended inside this piece
+      if (band == 1) __builtin_amdgcn_s_setprio(2);
+      else if (band == 2) __builtin_amdgcn_s_setprio(1);
+      else __builtin_amdgcn_s_setprio(0);
+    }
   }
   if (pf < p1) {  // the partial last page; the stage holds it
     stage_store(L.page, sg, l);
@@ -531,7 +548,7 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(4, 4))) void
   if (num_splits == 1) {  // one range per sequence
     const int len = seq_len(r);
     process_piece(L, pages, Hkv, Hq, block_table, max_pages, r, len, kvh, chunk, 0,
-                  (len + kP - 1) / kP, 0, true, 1, qt, part_o, part_ml);
+                  (len + kP - 1) / kP, 0, true, 1, qt, part_o, part_ml, 0, 1 << 20);
     return;
   }
   // total pages over all sequences
@@ -580,12 +597,14 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(4, 4))) void
     before += __builtin_amdgcn_readlane(incl, 63);
   }
   if (npg_b == 0) return;  // not reached: page x < T lies in some sequence
+  const int64_t x0 = x;
+  __builtin_amdgcn_s_setprio(3);  // lowered in bands as the wave's pages are done
   while (true) {
     const int64_t end = min(xe, before + npg_b);
     const int piece = (int)(r - before / pw);
     process_piece(L, pages, Hkv, Hq, block_table, max_pages, b, seq_len(b), kvh, chunk,
                   (int)(x - before), (int)(end - before), piece, end == before + npg_b,
-                  num_splits, qt, part_o, part_ml);
+                  num_splits, qt, part_o, part_ml, (int)(x - x0), (int)(xe - x0));
     x = end;
     if (x >= xe) break;
     before += npg_b;
