@@ -241,6 +241,29 @@ def main():
     split_us = e0.elapsed_time(e1) * 1e3 / args.steps
     achieved = split_bytes / (split_us * 1e-6) / 1e9
 
+    # ---- the 64-token-per-sequence cache update (4096 tokens x 8 KV heads) ----
+    # into each sequence's spare slots len_b .. len_b + 63 (never read by the
+    # decode above, whose lengths stay len_b); rotation-bound: 2 * 128 * 128 FLOP
+    # per row (token, KV head, K or V), accumulated in fp64
+    n_new = 64
+    ak = torch.randn(B * n_new, Hkv, d, device=dev).to(torch.bfloat16)
+    av = torch.randn(B * n_new, Hkv, d, device=dev).to(torch.bfloat16)
+    aslots = torch.from_numpy(np.concatenate(
+        [W.slots_for(table, b, np.arange(int(lens[b]), int(lens[b]) + n_new)) for b in range(B)])).to(dev)
+    for _ in range(3):
+        ok.kv_append(lay, pool, ak, av, aslots, Rk, Rv, cfg.clip_k, cfg.clip_v)
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    e0.record(stream)
+    for _ in range(args.steps):
+        ok.kv_append(lay, pool, ak, av, aslots, Rk, Rv, cfg.clip_k, cfg.clip_v)
+    e1.record(stream)
+    torch.cuda.synchronize()
+    app_us = e0.elapsed_time(e1) * 1e3 / args.steps
+    app_rows = 2 * B * n_new * Hkv
+    app_flop = app_rows * 2 * d * d
+    del ak, av
+
     res = {
         "metric": METRIC,
         "value": round(step_bytes / (us_step * 1e-6) / 1e9, 1),
@@ -284,6 +307,13 @@ def main():
             "kernel": "decode_split", "bound": "hbm", "achieved": round(achieved, 1),
             "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4),
             "traffic": split_traffic(), "bytes_per_launch": split_bytes,
+        },
+        "append_64_tokens_per_seq": {
+            "tokens": B * n_new, "rows": app_rows, "us": round(app_us, 2),
+            "bound": "alu", "achieved_tflops_fp64": round(app_flop / (app_us * 1e-6) / 1e12, 2),
+            "peak_tflops_fp64": 78.6,
+            "frac": round(app_flop / (app_us * 1e-6) / 1e12 / 78.6, 4),
+            "bytes": 2 * B * n_new * Hkv * d * 2 + B * n_new * Hkv * INT2_BYTES_PER_TOKEN_HEAD,
         },
         "bytes": {"int2_kv": kv_bytes, "block_table": table_bytes, "q_and_out": qo_bytes,
                   "append": append_bytes, "step_total": step_bytes,

@@ -9,15 +9,16 @@
 // "sum in fp64, ascending, round once to fp32" bit for bit.
 //
 // Work decomposition: blockIdx.y selects K (0) or V (1); the block stages that
-// rotation matrix (64 KB fp32) in LDS once and its four waves then take RW rows
-// (token, head) at a time, grid-stride.  Lane l computes output channels l and
-// l+64 of the rows, so every matrix element read from LDS feeds RW fp64 FMAs per
-// channel.  A 32-channel group is one half of the wave: channels 0-31 / 64-95
-// live in lanes 0-31, channels 32-63 / 96-127 in lanes 32-63; the group max /
-// min are DPP steps inside each row of 16 lanes plus one row-pair swap.
-// RW = 1 for small appends (one decode step: many short waves), 4 for bulk
-// cache builds (fewer matrix reads per FMA).
+// rotation matrix (64 KB fp32) in LDS once and its waves then take rows (token,
+// head), grid-stride.  Lane l computes output channels l and l+64 of the rows.
+// A 32-channel group is one half of the wave: channels 0-31 / 64-95 live in lanes
+// 0-31, channels 32-63 / 96-127 in lanes 32-63; the group max / min are DPP steps
+// inside each row of 16 lanes plus one row-pair swap.  Small appends (a decode
+// step) run one row per wave on many short waves; large ones run the bulk kernel
+// below (8 rows per wave, persistent blocks).
 #include <hip/hip_fp16.h>
+
+#include <algorithm>
 
 #include "internal.h"
 
@@ -157,6 +158,45 @@ __device__ inline void prepare_body(float* Rsf, float4 (*qs)[kD / 4], int bx,
     if (r0 + rg + i < rows) qt[(size_t)(r0 + rg + i) * kD + j] = acc[i] * qscale;
 }
 
+// Clip, quantize, pack and write one rotated row (token, head) whose channels l
+// and l + 64 are in lane l.  Rows >= n_rows (wave-uniform) only take part in the
+// cross-lane steps.
+__device__ inline void store_row(uint8_t* __restrict__ pages, int Hkv,
+                                 const int64_t* __restrict__ slots, int n_rows, int row, int is_v,
+                                 float clip, double acc0, double acc1, int l) {
+  const float xt0 = __double2float_rn(acc0);  // channel l
+  const float xt1 = __double2float_rn(acc1);  // channel l + 64
+  const QOut q0 = quantize(xt0, clip);
+  const QOut q1 = quantize(xt1, clip);
+  const uint32_t byte0 = pack_quad(q0.code, l);  // quad l/4
+  const uint32_t byte1 = pack_quad(q1.code, l);  // quad 16 + l/4
+  if (row >= n_rows) return;                     // uniform across the wave
+  const int tok = row / Hkv;
+  const int h = row - tok * Hkv;
+  const int64_t slot = slots[tok];
+  const int64_t page = slot / kP;
+  const int t = (int)(slot - page * kP);
+  uint8_t* blk = pages + ((size_t)page * Hkv + h) * kBlockBytes;
+  if ((l & 3) == 0) {
+    const int j0 = l >> 2, j1 = 16 + (l >> 2);
+    if (is_v) {
+      blk[kOffVCodes + j0 * kP + t] = (uint8_t)byte0;
+      blk[kOffVCodes + j1 * kP + t] = (uint8_t)byte1;
+    } else {
+      blk[kOffKCodes + t * (kD / 4) + j0] = (uint8_t)byte0;
+      blk[kOffKCodes + t * (kD / 4) + j1] = (uint8_t)byte1;
+    }
+  }
+  if ((l & 31) == 0) {
+    const uint32_t sz_base = is_v ? kOffVSz : kOffKSz;
+    const int g0 = l >> 5, g1 = 2 + (l >> 5);
+    *reinterpret_cast<uint32_t*>(blk + sz_base + (g0 * kP + t) * 4) =
+        (uint32_t)q0.s16 | ((uint32_t)q0.z16 << 16);
+    *reinterpret_cast<uint32_t*>(blk + sz_base + (g1 * kP + t) * 4) =
+        (uint32_t)q1.s16 | ((uint32_t)q1.z16 << 16);
+  }
+}
+
 // Cache update by one block: is_v selects K or V, blocks bx of gx take rows
 // grid-stride.  Rs: 64 KB LDS for the matrix, xs: the waves' input rows.
 template <int RW>
@@ -183,7 +223,6 @@ __device__ inline void append_body(float* Rs, double (*xs)[RW][kD], int is_v, in
   const int w = threadIdx.x >> 6;
   const int l = threadIdx.x & 63;
   const int n_items = (n_rows + RW - 1) / RW;
-  const uint32_t sz_base = is_v ? kOffVSz : kOffKSz;
 
   // each wave owns xs[w]: no block-level synchronization inside the loop
   for (int item = bx * kWaves + w; item < n_items; item += gx * kWaves) {
@@ -216,39 +255,8 @@ __device__ inline void append_body(float* Rs, double (*xs)[RW][kD], int is_v, in
     }
 
 #pragma unroll
-    for (int rr = 0; rr < RW; ++rr) {
-      const int row = item * RW + rr;
-      const float xt0 = __double2float_rn(acc0[rr]);  // channel l
-      const float xt1 = __double2float_rn(acc1[rr]);  // channel l + 64
-      const QOut q0 = quantize(xt0, clip);
-      const QOut q1 = quantize(xt1, clip);
-      const uint32_t byte0 = pack_quad(q0.code, l);    // quad l/4
-      const uint32_t byte1 = pack_quad(q1.code, l);    // quad 16 + l/4
-      if (row >= n_rows) continue;                     // uniform across the wave
-      const int tok = row / Hkv;
-      const int h = row - tok * Hkv;
-      const int64_t slot = slots[tok];
-      const int64_t page = slot / kP;
-      const int t = (int)(slot - page * kP);
-      uint8_t* blk = pages + ((size_t)page * Hkv + h) * kBlockBytes;
-      if ((l & 3) == 0) {
-        const int j0 = l >> 2, j1 = 16 + (l >> 2);
-        if (is_v) {
-          blk[kOffVCodes + j0 * kP + t] = (uint8_t)byte0;
-          blk[kOffVCodes + j1 * kP + t] = (uint8_t)byte1;
-        } else {
-          blk[kOffKCodes + t * (kD / 4) + j0] = (uint8_t)byte0;
-          blk[kOffKCodes + t * (kD / 4) + j1] = (uint8_t)byte1;
-        }
-      }
-      if ((l & 31) == 0) {
-        const int g0 = l >> 5, g1 = 2 + (l >> 5);
-        *reinterpret_cast<uint32_t*>(blk + sz_base + (g0 * kP + t) * 4) =
-            (uint32_t)q0.s16 | ((uint32_t)q0.z16 << 16);
-        *reinterpret_cast<uint32_t*>(blk + sz_base + (g1 * kP + t) * 4) =
-            (uint32_t)q1.s16 | ((uint32_t)q1.z16 << 16);
-      }
-    }
+    for (int rr = 0; rr < RW; ++rr)
+      store_row(pages, Hkv, slots, n_rows, item * RW + rr, is_v, clip, acc0[rr], acc1[rr], l);
   }
 }
 
@@ -261,6 +269,120 @@ __global__ __launch_bounds__(256) void append_kernel(
   __shared__ double xs[kWaves][RW][kD];
   append_body<RW>(Rs, xs, blockIdx.y, blockIdx.x, gridDim.x, pages, Hkv, k, v, slots, n_rows, Rk,
                   Rv, clip_k, clip_v);
+}
+
+// ---------------------------------------------------------------------------
+// Bulk cache update (large appends): persistent blocks of 8 waves, one per CU;
+// blockIdx.y selects K or V.  A wave takes 8 rows at a time as 4 row pairs: the
+// two halves of the wave hold rows 2p and 2p + 1 of pair p, and lane l' = l & 31
+// of a half computes channels l' + 32 q (q = 0..3), so each group of 32 channels
+// is one half wave as in the small-append path.  The matrix is staged once per
+// block as Rq[c][l'] = R[c][l' + 32 q], q = 0..3; the rows are kept in LDS as
+// fp64 (channels 2i, 2i + 1 in one 16-byte read), and every lane runs its 16 fp64
+// chains (4 pairs x 4 channels) in ascending channel order.
+// ---------------------------------------------------------------------------
+constexpr int kBulkWaves = 8;
+constexpr int kBulkRows = 8;
+
+// store_row for the pair layout: lane l' of the half holds channels l' + 32 q.
+__device__ inline void store_row4(uint8_t* __restrict__ pages, int Hkv,
+                                  const int64_t* __restrict__ slots, int n_rows, int row,
+                                  int is_v, float clip, const double (&acc)[4], int lp) {
+  QOut qo[4];
+  uint32_t byte[4];
+#pragma unroll
+  for (int q = 0; q < 4; ++q) {
+    qo[q] = quantize(__double2float_rn(acc[q]), clip);  // group q of the row
+    byte[q] = pack_quad(qo[q].code, lp);                 // quad 8 q + l'/4
+  }
+  if (row >= n_rows) return;
+  const int tok = row / Hkv;
+  const int h = row - tok * Hkv;
+  const int64_t slot = slots[tok];
+  const int64_t page = slot / kP;
+  const int t = (int)(slot - page * kP);
+  uint8_t* blk = pages + ((size_t)page * Hkv + h) * kBlockBytes;
+  if ((lp & 3) == 0) {
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      const int j = 8 * q + (lp >> 2);
+      if (is_v) blk[kOffVCodes + j * kP + t] = (uint8_t)byte[q];
+      else blk[kOffKCodes + t * (kD / 4) + j] = (uint8_t)byte[q];
+    }
+  }
+  if (lp == 0) {
+    const uint32_t sz_base = is_v ? kOffVSz : kOffKSz;
+#pragma unroll
+    for (int q = 0; q < 4; ++q)
+      *reinterpret_cast<uint32_t*>(blk + sz_base + (q * kP + t) * 4) =
+          (uint32_t)qo[q].s16 | ((uint32_t)qo[q].z16 << 16);
+  }
+}
+
+__global__ __launch_bounds__(512) void append_bulk_kernel(
+    uint8_t* __restrict__ pages, int Hkv, const uint16_t* __restrict__ k,
+    const uint16_t* __restrict__ v, const int64_t* __restrict__ slots, int n_rows,
+    const float* __restrict__ Rk, const float* __restrict__ Rv, float clip_k, float clip_v) {
+  // xs first: its reads use the 16-bit LDS offset field
+  __shared__ double2 xs[kBulkWaves][kBulkRows][kD / 2];      // 64 KB
+  __shared__ float4 Rq[kD][kD / 4];                          // 64 KB
+  const int is_v = blockIdx.y;
+  const float* __restrict__ R = is_v ? Rv : Rk;
+  const uint16_t* __restrict__ X = is_v ? v : k;
+  const float clip = is_v ? clip_v : clip_k;
+  const int t = threadIdx.x;
+  {  // 8 float4 per thread, loads issued before the stores
+    float4 r4[kD * kD / 4 / 512];
+#pragma unroll
+    for (int i = 0; i < kD * kD / 4 / 512; ++i) r4[i] = reinterpret_cast<const float4*>(R)[t + 512 * i];
+    float* rq = reinterpret_cast<float*>(Rq);
+#pragma unroll
+    for (int i = 0; i < kD * kD / 4 / 512; ++i) {
+      const int f = t + 512 * i, c = f >> 5, j = 4 * (f & 31);  // R[c][j..j+3]
+      const int q = j >> 5, lp = j & 31;                          // channel j = lp + 32 q
+      rq[(c * 32 + lp + 0) * 4 + q] = r4[i].x;
+      rq[(c * 32 + lp + 1) * 4 + q] = r4[i].y;
+      rq[(c * 32 + lp + 2) * 4 + q] = r4[i].z;
+      rq[(c * 32 + lp + 3) * 4 + q] = r4[i].w;
+    }
+  }
+  __syncthreads();
+  const int w = t >> 6, l = t & 63, half = l >> 5, lp = l & 31;
+  const int n_items = (n_rows + kBulkRows - 1) / kBulkRows;
+  for (int item = blockIdx.x * kBulkWaves + w; item < n_items; item += gridDim.x * kBulkWaves) {
+#pragma unroll
+    for (int rr = 0; rr < kBulkRows; ++rr) {
+      const int row = item * kBulkRows + rr;
+      double2 x = make_double2(0.0, 0.0);
+      if (row < n_rows) {
+        const uint32_t pair = reinterpret_cast<const uint32_t*>(X + (size_t)row * kD)[l];
+        x = make_double2((double)__uint_as_float(pair << 16), (double)__uint_as_float(pair & 0xffff0000u));
+      }
+      xs[w][rr][l] = x;  // channels 2l, 2l + 1
+    }
+    double acc[kBulkRows / 2][4];
+#pragma unroll
+    for (int p = 0; p < kBulkRows / 2; ++p)
+#pragma unroll
+      for (int q = 0; q < 4; ++q) acc[p][q] = 0.0;
+#pragma unroll 2
+    for (int c2 = 0; c2 < kD / 2; ++c2) {
+      const float4 ra = Rq[2 * c2][lp], rb = Rq[2 * c2 + 1][lp];
+      const double a[4] = {ra.x, ra.y, ra.z, ra.w}, b[4] = {rb.x, rb.y, rb.z, rb.w};
+#pragma unroll
+      for (int p = 0; p < kBulkRows / 2; ++p) {
+        const double2 x = xs[w][2 * p + half][c2];  // channels 2 c2, 2 c2 + 1 of the row
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          acc[p][q] = __fma_rn(x.x, a[q], acc[p][q]);
+          acc[p][q] = __fma_rn(x.y, b[q], acc[p][q]);
+        }
+      }
+    }
+#pragma unroll
+    for (int p = 0; p < kBulkRows / 2; ++p)
+      store_row4(pages, Hkv, slots, n_rows, item * kBulkRows + 2 * p + half, is_v, clip, acc[p], lp);
+  }
 }
 
 __global__ __launch_bounds__(256) void prepare_kernel(const uint16_t* __restrict__ q, int rows,
@@ -307,14 +429,19 @@ hipError_t launch_append(void* pages, int64_t Hkv, const uint16_t* k, const uint
                          const int64_t* slots, int n_tok, const float* Rk, const float* Rv,
                          float clip_k, float clip_v, hipStream_t st) {
   const int64_t n_rows = (int64_t)n_tok * Hkv;
-  const int rw = n_rows <= 4096 ? 1 : 4;
-  const dim3 grid((unsigned)append_blocks_for(n_rows, rw), 2);
-  if (rw == 1)
+  if (n_rows <= 4096) {  // one decode step: many short waves
+    const dim3 grid((unsigned)append_blocks_for(n_rows, 1), 2);
     hipLaunchKernelGGL(append_kernel<1>, grid, dim3(256), 0, st, static_cast<uint8_t*>(pages),
                        (int)Hkv, k, v, slots, (int)n_rows, Rk, Rv, clip_k, clip_v);
-  else
-    hipLaunchKernelGGL(append_kernel<4>, grid, dim3(256), 0, st, static_cast<uint8_t*>(pages),
-                       (int)Hkv, k, v, slots, (int)n_rows, Rk, Rv, clip_k, clip_v);
+  } else {  // bulk: one persistent 8-wave block per CU, half of them per tensor
+    const int64_t items = (n_rows + kBulkRows - 1) / kBulkRows;
+    int64_t nb = (items + kBulkWaves - 1) / kBulkWaves;
+    const int64_t cap = std::max<int64_t>(1, device_cus() / 2);
+    if (nb > cap) nb = cap;
+    hipLaunchKernelGGL(append_bulk_kernel, dim3((unsigned)nb, 2), dim3(512), 0, st,
+                       static_cast<uint8_t*>(pages), (int)Hkv, k, v, slots, (int)n_rows, Rk, Rv,
+                       clip_k, clip_v);
+  }
   return hipGetLastError();
 }
 
