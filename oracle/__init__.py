@@ -14,6 +14,11 @@ What it computes (arXiv 2605.17757):
   * ``decode_brute``  -- the same in the original basis (dequantize, rotate back,
                          plain softmax attention); tiny inputs only.
   * ``bf16_decode``   -- plain fp64 attention over a bf16 paged cache.
+  * ``seg_write``, ``mixed_update``, ``decode_mixed`` -- the mixed-precision
+                         cache of Sec. 4 "KV Cache Layout": bf16 sink and recent
+                         window around the INT2 history, the per-step demotion of
+                         the oldest window token (Alg. 1 DecodeStep) and decode
+                         attention over all three segments.
 """
 from __future__ import annotations
 
@@ -75,6 +80,14 @@ def lib():
         L.oracle_f16_to_f32.argtypes = [ctypes.c_uint16]
         L.oracle_bf16_to_f32.restype = f32
         L.oracle_bf16_to_f32.argtypes = [ctypes.c_uint16]
+        L.oracle_seg_write.restype = i32
+        L.oracle_seg_write.argtypes = [i32, i32, i32, i32, i32, P, P, P, P, P, i32]
+        L.oracle_mixed_update.restype = i64
+        L.oracle_mixed_update.argtypes = [i32, i32, i32, i32, i64, P, P, i32, i32, i32, P, P, P,
+                                          i32, P, P, P, f32, f32]
+        L.oracle_decode_mixed.restype = i32
+        L.oracle_decode_mixed.argtypes = [i32, i32, i32, i32, i64, P, P, i32, i32, P, i32, i32, P,
+                                          i32, P, P, P, f64, P, i32, P]
         L.oracle_num_threads.restype = i32
         _lib = L
     return _lib
@@ -228,4 +241,67 @@ def bf16_decode(pages: np.ndarray, *, d: int, Hkv: int, P: int, q: np.ndarray,
                                   bt.shape[1], _ptr(sl), float(sm_scale), pp, n, _ptr(out))
     if rc:
         raise ValueError("oracle bf16_decode: bad page id, length or head")
+    return out
+
+
+def seg_elems(*, d: int, Hkv: int, B: int, S0: int, W: int) -> int:
+    """bf16 elements of the segment store: [B][Hkv][K, V][S0 + W][d]."""
+    return B * Hkv * 2 * (S0 + W) * d
+
+
+def seg_write(seg: np.ndarray, *, d: int, Hkv: int, B: int, S0: int, W: int, k: np.ndarray,
+              v: np.ndarray, seq_idx: np.ndarray, pos: np.ndarray) -> None:
+    """Copy bf16 rows (k, v: [n, Hkv, d] bits) of sequence seq_idx[i] at position
+    pos[i] into their sink / window slot of ``seg`` (uint16, modified in place)."""
+    assert seg.dtype == np.uint16 and seg.flags["C_CONTIGUOUS"]
+    si = _c(seq_idx, np.int32)
+    ps = _c(pos, np.int64)
+    rc = lib().oracle_seg_write(d, Hkv, S0, W, B, _ptr(seg), _ptr(_c(k, np.uint16)),
+                                _ptr(_c(v, np.uint16)), _ptr(si), _ptr(ps), si.shape[0])
+    if rc:
+        raise ValueError("oracle seg_write: bad sequence or a position without a bf16 slot")
+
+
+def mixed_update(pages: np.ndarray, seg: np.ndarray, *, d: int, Hkv: int, P: int, G: int,
+                 S0: int, W: int, k_new: np.ndarray, v_new: np.ndarray, block_table: np.ndarray,
+                 seq_lens: np.ndarray, Rk: np.ndarray, Rv: np.ndarray, clip_k: float,
+                 clip_v: float) -> int:
+    """One new token per sequence at position seq_lens[b] - 1 (k_new, v_new:
+    [B, Hkv, d] bf16 bits): sink, window with demotion of the oldest window token
+    into INT2, or INT2 directly when W = 0.  ``pages`` and ``seg`` change in place."""
+    bt = _c(block_table, np.int32)
+    sl = _c(seq_lens, np.int32)
+    B = sl.shape[0]
+    num_pages = pages.size // (Hkv * page_head_bytes(d, P, G))
+    rc = lib().oracle_mixed_update(d, Hkv, P, G, num_pages, _ptr(pages), _ptr(seg), S0, W, B,
+                                   _ptr(_c(k_new, np.uint16)), _ptr(_c(v_new, np.uint16)),
+                                   _ptr(bt), bt.shape[1], _ptr(sl), _ptr(_c(Rk, np.float32)),
+                                   _ptr(_c(Rv, np.float32)), float(clip_k), float(clip_v))
+    if rc < 0:
+        raise ValueError("oracle mixed_update: bad length or page")
+    return int(rc)
+
+
+def decode_mixed(pages: np.ndarray, seg: np.ndarray, *, d: int, Hkv: int, P: int, G: int,
+                 S0: int, W: int, q: np.ndarray, block_table: np.ndarray, seq_lens: np.ndarray,
+                 Rk: np.ndarray, Rv: np.ndarray, sm_scale: float, pairs=None) -> np.ndarray:
+    """fp64 decode attention over bf16 sink + INT2 history + bf16 window."""
+    q = _c(q, np.uint16)
+    B, Hq = q.shape[0], q.shape[1]
+    bt = _c(block_table, np.int32)
+    sl = _c(seq_lens, np.int32)
+    num_pages = pages.size // (Hkv * page_head_bytes(d, P, G))
+    if pairs is None:
+        out = np.zeros((B, Hq, d), np.float64)
+        pp, n = None, 0
+    else:
+        pr = _c(pairs, np.int32).reshape(-1, 2)
+        out = np.zeros((pr.shape[0], d), np.float64)
+        pp, n = _ptr(pr), pr.shape[0]
+    rc = lib().oracle_decode_mixed(d, Hkv, P, G, num_pages, _ptr(pages), _ptr(_c(seg, np.uint16)),
+                                   S0, W, _ptr(q), B, Hq, _ptr(bt), bt.shape[1], _ptr(sl),
+                                   _ptr(_c(Rk, np.float32)), _ptr(_c(Rv, np.float32)),
+                                   float(sm_scale), pp, n, _ptr(out))
+    if rc:
+        raise ValueError("oracle decode_mixed: bad page id, length or head")
     return out

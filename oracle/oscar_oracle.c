@@ -11,7 +11,10 @@
  *   - decode attention over the packed cache (Alg. 1 DecodeStep; Sec. 2
  *     attention definition), evaluated in fp64 in the rotated basis, plus a
  *     brute-force evaluation in the original basis;
- *   - plain fp64 attention over a bf16 paged cache (the bf16 baseline).
+ *   - plain fp64 attention over a bf16 paged cache (the bf16 baseline);
+ *   - the mixed-precision cache of Sec. 4 "KV Cache Layout": bf16 sink and
+ *     recent window around the INT2 history, the per-step demotion of the
+ *     oldest window token (Alg. 1 DecodeStep) and decode attention over it.
  *
  * Only the test suite, the package smoke check and the benchmark's CPU-baseline
  * leg may load this library.  It shares no code, header or table with the GPU
@@ -490,6 +493,189 @@ int oracle_bf16_append(int d, int Hkv, int P, int64_t num_pages, uint16_t *pages
     }
   }
   return 0;
+}
+
+/* ------------------------------------------------------------------------- */
+/* Mixed-precision cache: bf16 sink, INT2 history, bf16 recent window         */
+/* ------------------------------------------------------------------------- */
+/*
+ * Sec. 4 "KV Cache Layout": at decode length n the logical cache of a sequence
+ * is the bf16 sink [0, S0), the INT2 history [S0, n - W) and the bf16 recent
+ * window [n - W, n), with the bounds clamped: lo = min(S0, n), hi = max(lo, n - W);
+ * history tokens live in the paged INT2 pool at their own positions.
+ *
+ * bf16 segment store (a layout of this library, not of the paper): for each
+ * (sequence b, kv-head h) a block of 2*(S0+W) rows of d bf16 values, the K rows of
+ * all slots and then the V rows:
+ *   K(b, h, slot, c) at element (((b*Hkv + h)*2 + 0)*(S0+W) + slot)*d + c
+ *   V(b, h, slot, c) at element (((b*Hkv + h)*2 + 1)*(S0+W) + slot)*d + c
+ * A sink position p < S0 uses slot p; a position p >= S0 of the recent window
+ * uses slot S0 + (p - S0) mod W.
+ */
+static int64_t seg_slot(int S0, int W, int64_t p) {
+  if (p < 0) return -1;
+  if (p < S0) return p;
+  if (W <= 0) return -1;
+  return S0 + (p - S0) % W;
+}
+
+static size_t seg_row(int d, int Hkv, int S0, int W, int b, int h, int is_v, int64_t slot) {
+  return ((((size_t)b * Hkv + (size_t)h) * 2 + (size_t)is_v) * (size_t)(S0 + W) + (size_t)slot) *
+         (size_t)d;
+}
+
+/* Copy bf16 rows (token i: k/v[i][Hkv][d]) of sequence seq_idx[i] at position
+ * pos[i] into their sink or window slot.  Returns 0, or -1 on a bad index or a
+ * position that has no bf16 slot (p >= S0 with W = 0). */
+int oracle_seg_write(int d, int Hkv, int S0, int W, int B, uint16_t *seg, const uint16_t *k,
+                     const uint16_t *v, const int32_t *seq_idx, const int64_t *pos, int n_tok) {
+  for (int i = 0; i < n_tok; ++i) {
+    int b = seq_idx[i];
+    int64_t slot = seg_slot(S0, W, pos[i]);
+    if (b < 0 || b >= B || slot < 0) return -1;
+    for (int h = 0; h < Hkv; ++h) {
+      memcpy(seg + seg_row(d, Hkv, S0, W, b, h, 0, slot), k + ((size_t)i * Hkv + h) * d,
+             sizeof(uint16_t) * (size_t)d);
+      memcpy(seg + seg_row(d, Hkv, S0, W, b, h, 1, slot), v + ((size_t)i * Hkv + h) * d,
+             sizeof(uint16_t) * (size_t)d);
+    }
+  }
+  return 0;
+}
+
+/* The cache side of Alg. 1 DecodeStep for one new token per sequence, at
+ * position p = seq_lens[b] - 1 (k_new, v_new: bf16 [B][Hkv][d]):
+ *   p < S0          -> the token joins the bf16 sink;
+ *   p >= S0, W = 0  -> the token is quantized into the INT2 history at once;
+ *   otherwise       -> the token joins the recent window; if the window then
+ *                      holds more than W tokens (p - W >= S0), its oldest token,
+ *                      at position p - W, is quantized into the INT2 history
+ *                      (QuantizeAndWrite) before its slot is reused.
+ * Quantization is the cache update above (rotation from the bf16 row).
+ * Returns the number of saturated fp16 stores, or -1 on a bad length / page. */
+int64_t oracle_mixed_update(int d, int Hkv, int P, int G, int64_t num_pages, uint8_t *pages,
+                            uint16_t *seg, int S0, int W, int B, const uint16_t *k_new,
+                            const uint16_t *v_new, const int32_t *block_table, int max_pages,
+                            const int32_t *seq_lens, const float *Rk, const float *Rv,
+                            float clip_k, float clip_v) {
+  int64_t sat = 0;
+  uint16_t *ko = (uint16_t *)malloc(sizeof(uint16_t) * (size_t)Hkv * d);
+  uint16_t *vo = (uint16_t *)malloc(sizeof(uint16_t) * (size_t)Hkv * d);
+  int rc = 0;
+  for (int b = 0; b < B && !rc; ++b) {
+    int64_t p = (int64_t)seq_lens[b] - 1;
+    if (p < 0 || p >= (int64_t)max_pages * P) { rc = -1; break; }
+    const uint16_t *kn = k_new + (size_t)b * Hkv * d;
+    const uint16_t *vn = v_new + (size_t)b * Hkv * d;
+    int64_t quant_pos = -1;           /* position quantized into INT2 this step */
+    const uint16_t *qk = NULL, *qv = NULL;
+    if (p >= S0 && W == 0) {
+      quant_pos = p; qk = kn; qv = vn;
+    } else if (p >= S0 && p - W >= S0) {
+      int64_t slot = seg_slot(S0, W, p - W);
+      for (int h = 0; h < Hkv; ++h) {
+        memcpy(ko + (size_t)h * d, seg + seg_row(d, Hkv, S0, W, b, h, 0, slot), sizeof(uint16_t) * (size_t)d);
+        memcpy(vo + (size_t)h * d, seg + seg_row(d, Hkv, S0, W, b, h, 1, slot), sizeof(uint16_t) * (size_t)d);
+      }
+      quant_pos = p - W; qk = ko; qv = vo;
+    }
+    if (quant_pos >= 0) {
+      int32_t page = block_table[(size_t)b * max_pages + quant_pos / P];
+      int64_t slot = (int64_t)page * P + quant_pos % P;
+      int64_t r = oracle_kv_append(d, Hkv, P, G, num_pages, pages, qk, qv, &slot, 1, Rk, Rv,
+                                   clip_k, clip_v);
+      if (r < 0) { rc = -1; break; }
+      sat += r;
+    }
+    if (p < S0 || W > 0) {
+      int32_t bb = b;
+      if (oracle_seg_write(d, Hkv, S0, W, B, seg, kn, vn, &bb, &p, 1)) { rc = -1; break; }
+    }
+  }
+  free(ko); free(vo);
+  return rc ? -1 : sat;
+}
+
+/* Decode attention over the mixed cache (Alg. 1 DecodeStep: concatenate the bf16
+ * sink, the dequantized and back-rotated INT2 history and the bf16 recent window,
+ * then softmax(sm_scale * q K^T) V), fp64.  The history part is evaluated in the
+ * rotated basis as in oracle_decode; the bf16 parts in the original basis:
+ *   o = ( [sum_hist p_t Q(v~_t)] Rv^T + sum_bf16 p_t v_t ) / sum_t p_t.
+ * Output layout as oracle_decode.  Returns 0 or -1. */
+int oracle_decode_mixed(int d, int Hkv, int P, int G, int64_t num_pages, const uint8_t *pages,
+                        const uint16_t *seg, int S0, int W, const uint16_t *q, int B, int Hq,
+                        const int32_t *block_table, int max_pages, const int32_t *seq_lens,
+                        const float *Rk, const float *Rv, double sm_scale, const int32_t *pairs,
+                        int n_pairs, double *out) {
+  geo_t g = {d, Hkv, P, G};
+  if (Hq % Hkv || S0 < 0 || W < 0) return -1;
+  int group = Hq / Hkv;
+  int n = pairs ? n_pairs : B * Hq;
+  int bad = 0;
+#pragma omp parallel for reduction(+ : bad) schedule(dynamic, 1)
+  for (int i = 0; i < n; ++i) {
+    int b = pairs ? pairs[2 * i] : i / Hq;
+    int h = pairs ? pairs[2 * i + 1] : i % Hq;
+    int len = (b >= 0 && b < B) ? seq_lens[b] : 0;
+    if (h < 0 || h >= Hq || len < 1 || len > max_pages * P) { bad += 1; continue; }
+    int kvh = h / group;
+    int lo = len < S0 ? len : S0;
+    int hi = len - W > lo ? len - W : lo;
+    const uint16_t *qr = q + ((size_t)b * Hq + h) * d;
+    double *qd = (double *)malloc(sizeof(double) * (size_t)d);
+    double *qt = (double *)calloc((size_t)d, sizeof(double));
+    double *row = (double *)malloc(sizeof(double) * (size_t)d);
+    double *ot = (double *)calloc((size_t)d, sizeof(double));
+    double *op = (double *)calloc((size_t)d, sizeof(double));
+    double *score = (double *)malloc(sizeof(double) * (size_t)len);
+    for (int c = 0; c < d; ++c) qd[c] = (double)oracle_bf16_to_f32(qr[c]);
+    for (int j = 0; j < d; ++j) {
+      double acc = 0.0;
+      for (int c = 0; c < d; ++c) acc += qd[c] * (double)Rk[(size_t)c * d + j];
+      qt[j] = acc;
+    }
+    double m = -INFINITY;
+    int ok = 1;
+    for (int t = 0; t < len && ok; ++t) {
+      double acc = 0.0;
+      if (t < lo || t >= hi) {
+        const uint16_t *kr = seg + seg_row(d, Hkv, S0, W, b, kvh, 0, seg_slot(S0, W, t));
+        for (int c = 0; c < d; ++c) acc += qd[c] * (double)oracle_bf16_to_f32(kr[c]);
+      } else {
+        int32_t page = block_table[(size_t)b * max_pages + t / P];
+        if (page < 0 || page >= num_pages) { ok = 0; break; }
+        dequant_rotated(g, block_ptr(g, (uint8_t *)pages, page, kvh), 0, t % P, row);
+        for (int c = 0; c < d; ++c) acc += qt[c] * row[c];
+      }
+      score[t] = sm_scale * acc;
+      if (score[t] > m) m = score[t];
+    }
+    if (ok) {
+      double l = 0.0;
+      for (int t = 0; t < len; ++t) {
+        double pt = exp(score[t] - m);
+        l += pt;
+        if (t < lo || t >= hi) {
+          const uint16_t *vr = seg + seg_row(d, Hkv, S0, W, b, kvh, 1, seg_slot(S0, W, t));
+          for (int c = 0; c < d; ++c) op[c] += pt * (double)oracle_bf16_to_f32(vr[c]);
+        } else {
+          int32_t page = block_table[(size_t)b * max_pages + t / P];
+          dequant_rotated(g, block_ptr(g, (uint8_t *)pages, page, kvh), 1, t % P, row);
+          for (int c = 0; c < d; ++c) ot[c] += pt * row[c];
+        }
+      }
+      double *o = out + (size_t)i * d;
+      for (int j = 0; j < d; ++j) {
+        double acc = 0.0;
+        for (int c = 0; c < d; ++c) acc += ot[c] * (double)Rv[(size_t)j * d + c];
+        o[j] = (acc + op[j]) / l;
+      }
+    } else {
+      bad += 1;
+    }
+    free(qd); free(qt); free(row); free(ot); free(op); free(score);
+  }
+  return bad ? -1 : 0;
 }
 
 int oracle_num_threads(void) {
