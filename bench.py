@@ -18,7 +18,8 @@ breaks one step down with events between the stages (a separate pass, since
 those events add launch gaps).
 `cpu_baseline` is the CPU oracle timed on a bounded sample of the same
 workload.  `bf16_baseline` is the bf16 paged-decode kernel on the same
-sequences.
+sequences.  `mixed_cache_step` is oscar_decode_step_mixed on the same sequences
+with a bf16 sink of 64 and a bf16 window of 256 tokens around the INT2 history.
 """
 from __future__ import annotations
 
@@ -57,6 +58,10 @@ def parse():
                          "slower than eager launches on ROCm 7.x, so never used for value)")
     ap.add_argument("--cpu-seconds", type=float, default=10.0,
                     help="target CPU time for the oracle baseline sample")
+    ap.add_argument("--no-mixed", action="store_true",
+                    help="skip the mixed-precision cache step (bf16 sink + window)")
+    ap.add_argument("--sink", type=int, default=64, help="mixed cache: bf16 sink tokens S0")
+    ap.add_argument("--window", type=int, default=256, help="mixed cache: bf16 window tokens W")
     return ap.parse_args()
 
 
@@ -102,6 +107,11 @@ def main():
     new_k = torch.empty(B, Hkv, d, dtype=torch.bfloat16, device=dev)
     new_v = torch.empty_like(new_k)
     new_slots = np.zeros(B, np.int64)
+    # mixed cache: the same pool serves as its INT2 history (its history tokens are
+    # quantized from the same rows); the sink and window rows go to a segment store
+    S0m, Wm = args.sink, args.window
+    seg_store = None if args.no_mixed else ok.alloc_seg(lay, B, S0m, Wm)
+    pre = torch.from_numpy(cfg.lens - 1).to(dev)
     for b in range(B):
         k, v = W.cache_kv(cfg, b, device=dev)
         n = int(lens[b])
@@ -111,6 +121,13 @@ def main():
                      cfg.clip_v)
         if bf_pool is not None:
             ok.bf16_kv_append(lay, bf_pool, k, v, slots)
+        if seg_store is not None:  # sink and window tokens of the cache of length n - 1
+            lo = min(S0m, n - 1)
+            keep = torch.from_numpy(np.r_[0:lo, max(lo, n - 1 - Wm):n - 1].astype(np.int64)).to(dev)
+            if keep.numel():
+                ok.mixed_append(lay, pool, seg_store, S0m, Wm, k[keep], v[keep],
+                                torch.full((keep.numel(),), b, dtype=torch.int32, device=dev),
+                                keep, bt, pre, Rk, Rv, cfg.clip_k, cfg.clip_v)
         new_k[b] = k[n - 1]
         new_v[b] = v[n - 1]
         new_slots[b] = int(W.slots_for(table, b, [n - 1])[0])
@@ -319,6 +336,50 @@ def main():
                   "append": append_bytes, "step_total": step_bytes,
                   "bf16_kv_equivalent": int(lens.sum()) * Hkv * BF16_BYTES_PER_TOKEN_HEAD},
     }
+
+    # ---- the mixed-precision cache (bf16 sink S0 + INT2 history + bf16 window W) ----
+    # one oscar_decode_step_mixed per step: update (new token into the window,
+    # the window's oldest token demoted to INT2) + query rotation, INT2 split over
+    # the history, bf16 partial over sink and window, merge.  Run after the
+    # measurements above: its demotions rewrite pool slots they do not read.
+    if seg_store is not None:
+        mws = ok.alloc_mixed_workspace(lay, B, Hq, S)
+        mout = torch.empty_like(out)
+
+        def step_mixed():
+            ok.decode_step_mixed(lay, pool, seg_store, S0m, Wm, new_k, new_v, cfg.clip_k,
+                                 cfg.clip_v, q, bt, sl, Rk, Rv, cfg.sm_scale, S, mws, mout)
+
+        for _ in range(args.warmup):
+            step_mixed()
+        t_settle = time.perf_counter()
+        while (time.perf_counter() - t_settle) * 1e3 < args.settle_ms:
+            for _ in range(20):
+                step_mixed()
+            torch.cuda.synchronize()
+        m_wall_us, m_ev_us = timed(step_mixed)
+        lo_m = np.minimum(S0m, lens)
+        hi_m = np.maximum(lo_m, lens - Wm)
+        n_bf = lo_m + (lens - hi_m)
+        hist_pages = np.where(hi_m > lo_m, (hi_m + 63) // 64 - lo_m // 64, 0)
+        m_hist = int(np.sum(hi_m - lo_m)) * Hkv * INT2_BYTES_PER_TOKEN_HEAD
+        m_bf16 = int(np.sum(n_bf)) * Hkv * BF16_BYTES_PER_TOKEN_HEAD
+        n_dem = int(np.sum((lens - 1 - Wm >= S0m) & (Wm > 0)))
+        m_update = (2 * B * Hkv * d * 2          # new rows read
+                    + 2 * B * Hkv * d * 2        # new rows written to the window
+                    + 2 * n_dem * Hkv * d * 2    # demoted rows read
+                    + n_dem * Hkv * INT2_BYTES_PER_TOKEN_HEAD + 2 * d * d * 4)
+        m_bytes = (m_hist + m_bf16 + int(np.sum(hist_pages)) * 4 + B * 4 + qo_bytes + m_update
+                   + 2 * d * d * 4)
+        res["mixed_cache_step"] = {
+            "S0": S0m, "W": Wm, "us_per_step": round(m_wall_us, 2),
+            "us_per_step_events": round(m_ev_us, 2),
+            "GBps": round(m_bytes / (m_wall_us * 1e-6) / 1e9, 1),
+            "frac_of_peak": round(m_bytes / (m_wall_us * 1e-6) / 1e9 / HBM_PEAK_GBS, 4),
+            "bytes": {"int2_history": m_hist, "bf16_sink_window": m_bf16, "update": m_update,
+                      "step_total": m_bytes},
+        }
+        del mws, seg_store
 
     # ---- bf16 paged-decode baseline on the same sequences ----
     if bf_pool is not None:

@@ -201,6 +201,94 @@ int oscar_decode_reduce(const oscar_layout *L, int32_t B, int32_t Hq, const floa
                         oscar_dtype out_dtype, void *stream);
 
 /*
+ * Mixed-precision cache (Sec. 4 "KV Cache Layout"; Alg. 1 DecodeStep): the
+ * first S0 tokens of a sequence (attention sink) and its W most recent tokens
+ * stay in bf16; only the history between them is INT2.  At length n the cache
+ * of a sequence is
+ *   bf16 sink [0, lo), INT2 history [lo, hi), bf16 window [hi, n),
+ *   lo = min(S0, n), hi = max(lo, n - W)
+ * (S0 = W = 0: everything INT2, as oscar_kv_append / oscar_decode_attn).  The
+ * history lives in the paged pool at its own positions (block table as above);
+ * pool slots of sink and window positions are never written or read.  The bf16
+ * rows live in a segment store owned by the caller, an ABI like the page layout:
+ *   K(b, h, slot, c) at bf16 element (((b*Hkv + h)*2 + 0)*(S0+W) + slot)*d + c
+ *   V(b, h, slot, c) at bf16 element (((b*Hkv + h)*2 + 1)*(S0+W) + slot)*d + c
+ * position p < S0 uses slot p, a window position p >= S0 uses slot
+ * S0 + (p - S0) mod W.  S0 and W are arguments of every call and must stay the
+ * same for the life of a cache; 0 <= S0, 0 <= W, S0 + W <= 65536.
+ */
+
+/* Bytes of the segment store for B sequences: B * Hkv * 2 * (S0+W) * d * 2. */
+size_t oscar_seg_bytes(const oscar_layout *L, int32_t B, int32_t S0, int32_t W);
+
+/* Workspace of oscar_decode_attn_mixed / oscar_decode_step_mixed: rows of
+ * num_splits + 1 partial states (the INT2 pieces and one for the bf16 tokens). */
+size_t oscar_mixed_workspace_bytes(const oscar_layout *L, int32_t B, int32_t Hq,
+                                   int32_t num_splits);
+
+/*
+ * oscar_mixed_append -- build the mixed cache from a prompt: token i of sequence
+ * seq_idx[i] (int32, in [0, B)) at position pos[i] (int64) is written where a
+ * cache of length seq_lens[b] keeps it: positions in the history [lo, hi) are
+ * rotated, clipped and INT2-quantized into the pool exactly as by
+ * oscar_kv_append (slot block_table[b][p / P] * P + p % P); sink and window
+ * positions are copied into their segment slot; positions outside
+ * [0, seq_lens[b]) are skipped.  Tokens already in the cache are not moved: call
+ * it once with a sequence's whole prompt, then advance with
+ * oscar_decode_step_mixed.  Two tokens of one call must not share a slot (pool
+ * or segment).  k, v: bf16 [n_tok, Hkv, d]; other arguments as in
+ * oscar_kv_append and oscar_decode_attn.  n_tok == 0 launches nothing.
+ */
+int oscar_mixed_append(const oscar_layout *L, void *pages, void *seg, int32_t B, int32_t S0,
+                       int32_t W, const void *k, const void *v, const int32_t *seq_idx,
+                       const int64_t *pos, int32_t n_tok, const int32_t *block_table,
+                       int32_t max_pages_per_seq, const int32_t *seq_lens, const float *R_k,
+                       const float *R_v, float clip_k, float clip_v, void *stream);
+
+/*
+ * oscar_decode_attn_mixed -- decode attention over the mixed cache (Alg. 1
+ * DecodeStep): o = softmax(sm_scale * q K^T) V over all n = seq_lens[b] tokens,
+ * with bf16 K, V rows for the sink and window and K^ = Q(K~) R_k^T,
+ * V^ = Q(V~) R_v^T for the history.  The history is split and evaluated in the
+ * rotated basis as in oscar_decode_attn (num_splits pieces at most); the bf16
+ * tokens give one more partial state in the original basis; the merge computes
+ *   o = (sum_pieces e_s o~_s R_v^T + e_b o_b) / (sum_pieces e_s l_s + e_b l_b).
+ * Arguments as in oscar_decode_attn, plus seg (may be NULL when S0 = W = 0) and
+ * S0, W; workspace >= oscar_mixed_workspace_bytes(L, B, Hq, num_splits).
+ */
+int oscar_decode_attn_mixed(const oscar_layout *L, const void *pages, const void *seg,
+                            int32_t S0, int32_t W, const void *q, int32_t B, int32_t Hq,
+                            const int32_t *block_table, int32_t max_pages_per_seq,
+                            const int32_t *seq_lens, const float *R_k, const float *R_v,
+                            float sm_scale, int32_t num_splits, void *workspace,
+                            size_t workspace_bytes, void *out, oscar_dtype out_dtype,
+                            void *stream);
+
+/*
+ * oscar_decode_step_mixed -- one serving decode step over the mixed cache (Alg.
+ * 1 DecodeStep): every sequence b gains one token, k_new[b], v_new[b] (bf16
+ * [B, Hkv, d]), at position p = seq_lens[b] - 1 (seq_lens counts it):
+ *   p < S0          -> it joins the bf16 sink (slot p);
+ *   p >= S0, W = 0  -> it is INT2-quantized into the pool at position p;
+ *   otherwise       -> it joins the bf16 window; when p - W >= S0 the window's
+ *                      oldest token (position p - W, in the same segment slot)
+ *                      is first INT2-quantized into the pool at position p - W
+ *                      (QuantizeAndWrite of its bf16 row).
+ * Then decode attention over the updated cache, exactly oscar_decode_attn_mixed.
+ * Four launches: update + query rotation, INT2 split, bf16 partial, merge.  A
+ * sequence with seq_lens[b] = 0 gets no update and a zero output.  Arguments as
+ * in oscar_decode_attn_mixed and oscar_kv_append.
+ */
+int oscar_decode_step_mixed(const oscar_layout *L, void *pages, void *seg, int32_t S0,
+                            int32_t W, const void *k_new, const void *v_new, float clip_k,
+                            float clip_v, const void *q, int32_t B, int32_t Hq,
+                            const int32_t *block_table, int32_t max_pages_per_seq,
+                            const int32_t *seq_lens, const float *R_k, const float *R_v,
+                            float sm_scale, int32_t num_splits, void *workspace,
+                            size_t workspace_bytes, void *out, oscar_dtype out_dtype,
+                            void *stream);
+
+/*
  * bf16 paged-decode baseline (same paging, uncompressed cache), for comparing
  * against the INT2 path on the same GPU.  A bf16 page-head block (page p,
  * kv-head h) starts at element (p*Hkv + h) * 2*P*d and holds

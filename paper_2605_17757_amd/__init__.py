@@ -28,6 +28,8 @@ EXPORTS = (
     "oscar_kv_append", "oscar_decode_workspace_bytes", "oscar_default_num_splits",
     "oscar_decode_attn", "oscar_decode_step", "oscar_decode_prepare", "oscar_decode_split",
     "oscar_decode_reduce",
+    "oscar_seg_bytes", "oscar_mixed_workspace_bytes", "oscar_mixed_append",
+    "oscar_decode_attn_mixed", "oscar_decode_step_mixed",
     "oscar_bf16_page_bytes", "oscar_bf16_kv_append", "oscar_bf16_decode_workspace_bytes",
     "oscar_bf16_decode_attn",
 )
@@ -81,6 +83,16 @@ def lib() -> ctypes.CDLL:
             "oscar_decode_split": (ctypes.c_int, [LP, P, i32, i32, P, i32, P, i32, P, sz, P]),
             "oscar_decode_reduce": (ctypes.c_int, [LP, i32, i32, P, i32, P, sz, P, ctypes.c_int,
                                                    P]),
+            "oscar_seg_bytes": (sz, [LP, i32, i32, i32]),
+            "oscar_mixed_workspace_bytes": (sz, [LP, i32, i32, i32]),
+            "oscar_mixed_append": (ctypes.c_int, [LP, P, P, i32, i32, i32, P, P, P, P, i32, P,
+                                                  i32, P, P, P, f32, f32, P]),
+            "oscar_decode_attn_mixed": (ctypes.c_int, [LP, P, P, i32, i32, P, i32, i32, P, i32,
+                                                       P, P, P, f32, i32, P, sz, P, ctypes.c_int,
+                                                       P]),
+            "oscar_decode_step_mixed": (ctypes.c_int, [LP, P, P, i32, i32, P, P, f32, f32, P,
+                                                       i32, i32, P, i32, P, P, P, f32, i32, P, sz,
+                                                       P, ctypes.c_int, P]),
             "oscar_bf16_page_bytes": (sz, [LP]),
             "oscar_bf16_kv_append": (ctypes.c_int, [LP, P, P, P, P, i32, P]),
             "oscar_bf16_decode_workspace_bytes": (sz, [LP, i32, i32, i32]),
@@ -260,6 +272,95 @@ def decode_reduce(layout: Layout, B: int, Hq: int, R_v, num_splits: int, workspa
         _ptr(workspace, torch.uint8, "workspace"), workspace.numel(),
         _ptr(out, out.dtype, "out", B * Hq * d), out_dtype, _stream(stream))
     _check(st, "oscar_decode_reduce")
+
+
+# ---------------------------------------------------------------------------
+# mixed-precision cache (bf16 sink and recent window around the INT2 history)
+# ---------------------------------------------------------------------------
+
+def seg_bytes(layout: Layout, B: int, S0: int, W: int) -> int:
+    return int(lib().oscar_seg_bytes(ctypes.byref(layout), B, S0, W))
+
+
+def mixed_workspace_bytes(layout: Layout, B: int, Hq: int, num_splits: int) -> int:
+    return int(lib().oscar_mixed_workspace_bytes(ctypes.byref(layout), B, Hq, num_splits))
+
+
+def alloc_seg(layout: Layout, B: int, S0: int, W: int, device="cuda") -> torch.Tensor:
+    """Zeroed segment store, bf16 [B, Hkv, 2, S0 + W, d]."""
+    return torch.zeros(B, layout.num_kv_heads, 2, S0 + W, layout.head_dim, dtype=torch.bfloat16,
+                       device=device)
+
+
+def alloc_mixed_workspace(layout: Layout, B: int, Hq: int, num_splits: int, device="cuda"):
+    n = mixed_workspace_bytes(layout, B, Hq, num_splits)
+    if n == 0:
+        raise OscarError(ERR_INVALID_ARG, "mixed_workspace_bytes")
+    return torch.empty(n, dtype=torch.uint8, device=device)
+
+
+def _seg_ptr(layout, seg, B, S0, W):
+    if S0 + W == 0 and seg is None:
+        return None
+    return _ptr(seg, torch.bfloat16, "seg", seg_bytes(layout, B, S0, W) // 2)
+
+
+def mixed_append(layout: Layout, pages, seg, S0: int, W: int, k, v, seq_idx, pos, block_table,
+                 seq_lens, R_k, R_v, clip_k: float, clip_v: float, stream=None) -> None:
+    """Write prompt tokens (k, v: [n, Hkv, d]) of sequences ``seq_idx`` at positions
+    ``pos`` where a mixed cache of length ``seq_lens`` keeps them."""
+    n_tok = int(pos.numel())
+    d, hkv = layout.head_dim, layout.num_kv_heads
+    B, mp = int(block_table.shape[0]), int(block_table.shape[1])
+    st = lib().oscar_mixed_append(
+        ctypes.byref(layout), _ptr(pages, torch.uint8, "pages", pool_bytes(layout)),
+        _seg_ptr(layout, seg, B, S0, W), B, int(S0), int(W),
+        _ptr(k, torch.bfloat16, "k", n_tok * hkv * d), _ptr(v, torch.bfloat16, "v", n_tok * hkv * d),
+        _ptr(seq_idx, torch.int32, "seq_idx", n_tok), _ptr(pos, torch.int64, "pos", n_tok), n_tok,
+        _ptr(block_table, torch.int32, "block_table", B * mp), mp,
+        _ptr(seq_lens, torch.int32, "seq_lens", B), _ptr(R_k, torch.float32, "R_k", d * d),
+        _ptr(R_v, torch.float32, "R_v", d * d), float(clip_k), float(clip_v), _stream(stream))
+    _check(st, "oscar_mixed_append")
+
+
+def decode_attn_mixed(layout: Layout, pages, seg, S0: int, W: int, q, block_table, seq_lens, R_k,
+                      R_v, sm_scale: float, num_splits: int, workspace, out, stream=None) -> None:
+    """Decode attention over the mixed cache into ``out`` ([B, Hq, d], bf16 or fp32)."""
+    B, Hq, mp = _decode_args(layout, q, block_table, seq_lens)
+    d = layout.head_dim
+    out_dtype = OUT_F32 if out.dtype == torch.float32 else OUT_BF16
+    st = lib().oscar_decode_attn_mixed(
+        ctypes.byref(layout), _ptr(pages, torch.uint8, "pages", pool_bytes(layout)),
+        _seg_ptr(layout, seg, B, S0, W), int(S0), int(W),
+        _ptr(q, torch.bfloat16, "q", B * Hq * d), B, Hq,
+        _ptr(block_table, torch.int32, "block_table", B * mp), mp,
+        _ptr(seq_lens, torch.int32, "seq_lens", B), _ptr(R_k, torch.float32, "R_k", d * d),
+        _ptr(R_v, torch.float32, "R_v", d * d), float(sm_scale), int(num_splits),
+        _ptr(workspace, torch.uint8, "workspace"), workspace.numel(),
+        _ptr(out, out.dtype, "out", B * Hq * d), out_dtype, _stream(stream))
+    _check(st, "oscar_decode_attn_mixed")
+
+
+def decode_step_mixed(layout: Layout, pages, seg, S0: int, W: int, k_new, v_new, clip_k: float,
+                      clip_v: float, q, block_table, seq_lens, R_k, R_v, sm_scale: float,
+                      num_splits: int, workspace, out, stream=None) -> None:
+    """One decode step over the mixed cache: one new token per sequence (k_new,
+    v_new: [B, Hkv, d]) at position seq_lens[b] - 1, then attention into ``out``."""
+    B, Hq, mp = _decode_args(layout, q, block_table, seq_lens)
+    d, hkv = layout.head_dim, layout.num_kv_heads
+    out_dtype = OUT_F32 if out.dtype == torch.float32 else OUT_BF16
+    st = lib().oscar_decode_step_mixed(
+        ctypes.byref(layout), _ptr(pages, torch.uint8, "pages", pool_bytes(layout)),
+        _seg_ptr(layout, seg, B, S0, W), int(S0), int(W),
+        _ptr(k_new, torch.bfloat16, "k_new", B * hkv * d),
+        _ptr(v_new, torch.bfloat16, "v_new", B * hkv * d), float(clip_k), float(clip_v),
+        _ptr(q, torch.bfloat16, "q", B * Hq * d), B, Hq,
+        _ptr(block_table, torch.int32, "block_table", B * mp), mp,
+        _ptr(seq_lens, torch.int32, "seq_lens", B), _ptr(R_k, torch.float32, "R_k", d * d),
+        _ptr(R_v, torch.float32, "R_v", d * d), float(sm_scale), int(num_splits),
+        _ptr(workspace, torch.uint8, "workspace"), workspace.numel(),
+        _ptr(out, out.dtype, "out", B * Hq * d), out_dtype, _stream(stream))
+    _check(st, "oscar_decode_step_mixed")
 
 
 # ---------------------------------------------------------------------------

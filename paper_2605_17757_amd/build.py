@@ -31,6 +31,7 @@ SOURCES = {
     # keep MFMA accumulators in VGPRs: the kernel shifts and reads them with VALU ops
     "decode_mfma.hip": ["-mllvm", "-amdgpu-mfma-vgpr-form=1"],
     "bf16_decode.hip": [],
+    "mixed.hip": [],
 }
 
 

@@ -158,22 +158,136 @@ __device__ inline void prepare_body(float* Rsf, float4 (*qs)[kD / 4], int bx,
     if (r0 + rg + i < rows) qt[(size_t)(r0 + rg + i) * kD + j] = acc[i] * qscale;
 }
 
+// ---------------------------------------------------------------------------
+// Row routing.  A cache-update kernel takes rows (token, kv-head) = row; for each
+// row and tensor (is_v) a policy names
+//   src(row, is_v)  : the bf16 row to rotate and quantize (nullptr: none),
+//   slot(row)       : the pool slot that receives it (< 0: none),
+//   copy(row, is_v, l) : bf16 rows to copy into the mixed cache's segment store,
+//                     done by lane l for its 4 bytes after src has been read.
+// ---------------------------------------------------------------------------
+struct PlainRows {  // oscar_kv_append: token i -> slot_mapping[i]
+  const uint16_t* k;
+  const uint16_t* v;
+  const int64_t* slots;
+  int n_rows, Hkv;
+  __device__ const uint16_t* src(int row, int is_v) const {
+    return row < n_rows ? (is_v ? v : k) + (size_t)row * kD : nullptr;
+  }
+  __device__ int64_t slot(int row) const { return row < n_rows ? slots[row / Hkv] : -1; }
+  __device__ void copy(int, int, int) const {}
+};
+
+// Segment store of the mixed cache: [B][Hkv][K, V][S0 + W][d] bf16; position p
+// of a sequence has segment slot p (p < S0) or S0 + (p - S0) mod W (window).
+__device__ inline uint32_t* seg_row(uint16_t* seg, int Hkv, int S0, int W, int b, int h,
+                                    int is_v, int slot) {
+  return reinterpret_cast<uint32_t*>(
+      seg + ((((size_t)b * Hkv + h) * 2 + is_v) * (size_t)(S0 + W) + slot) * kD);
+}
+__device__ inline int seg_slot(int S0, int W, int p) { return p < S0 ? p : S0 + (p - S0) % W; }
+
+// oscar_mixed_append: token i of sequence seq_idx[i] at position pos[i] goes
+// where a cache of length seq_lens[b] keeps it: INT2 for the history [lo, hi)
+// (pool slot from the block table), bf16 segment slot otherwise; positions
+// outside [0, seq_lens[b]) are skipped.
+struct PrefillRows {
+  const uint16_t* k;
+  const uint16_t* v;
+  uint16_t* seg;
+  const int32_t* seq_idx;
+  const int64_t* pos;
+  const int32_t* seq_lens;
+  const int32_t* block_table;
+  int n_rows, Hkv, max_pages, S0, W;
+  // -1: skipped, 0: INT2, 1: bf16; b and p of the row's token
+  __device__ int route(int row, int& b, int& p) const {
+    if (row >= n_rows) return -1;
+    const int tok = row / Hkv;
+    b = seq_idx[tok];
+    const int64_t p64 = pos[tok];
+    const int len = min(max(seq_lens[b], 0), max_pages * kP);
+    if (p64 < 0 || p64 >= len) return -1;
+    p = (int)p64;
+    const int lo = min(S0, len), hi = max(lo, len - W);
+    return (p >= lo && p < hi) ? 0 : 1;
+  }
+  __device__ const uint16_t* src(int row, int is_v) const {
+    int b, p;
+    return route(row, b, p) == 0 ? (is_v ? v : k) + (size_t)row * kD : nullptr;
+  }
+  __device__ int64_t slot(int row) const {
+    int b, p;
+    if (route(row, b, p) != 0) return -1;
+    return (int64_t)block_table[(size_t)b * max_pages + p / kP] * kP + p % kP;
+  }
+  __device__ void copy(int row, int is_v, int l) const {
+    int b, p;
+    if (route(row, b, p) != 1) return;
+    const int h = row % Hkv;
+    seg_row(seg, Hkv, S0, W, b, h, is_v, seg_slot(S0, W, p))[l] =
+        reinterpret_cast<const uint32_t*>((is_v ? v : k) + (size_t)row * kD)[l];
+  }
+};
+
+// Decode step over the mixed cache: one new token per sequence b (row =
+// b * Hkv + h) at position p = seq_lens[b] - 1 (Alg. 1 DecodeStep):
+//   p < S0          -> bf16 sink slot p;
+//   p >= S0, W = 0  -> INT2 at position p;
+//   otherwise       -> bf16 window slot of p; when p - W >= S0 the token at
+//                      p - W, which holds that slot, is first quantized into
+//                      INT2 at position p - W (read before the slot is reused).
+struct StepRows {
+  const uint16_t* k;
+  const uint16_t* v;
+  uint16_t* seg;
+  const int32_t* seq_lens;
+  const int32_t* block_table;
+  int n_rows, Hkv, max_pages, S0, W;
+  __device__ int pos(int row) const {  // -1: no token
+    return row < n_rows ? min(max(seq_lens[row / Hkv], 0), max_pages * kP) - 1 : -1;
+  }
+  // position quantized into INT2 by this step, or -1
+  __device__ int qpos(int p) const {
+    if (p < S0) return -1;
+    if (W == 0) return p;
+    return p - W >= S0 ? p - W : -1;
+  }
+  __device__ const uint16_t* src(int row, int is_v) const {
+    const int p = pos(row), qp = qpos(p);
+    if (qp < 0) return nullptr;
+    if (qp == p) return (is_v ? v : k) + (size_t)row * kD;
+    const int b = row / Hkv, h = row % Hkv;
+    return reinterpret_cast<const uint16_t*>(seg_row(seg, Hkv, S0, W, b, h, is_v, seg_slot(S0, W, qp)));
+  }
+  __device__ int64_t slot(int row) const {
+    const int qp = qpos(pos(row));
+    if (qp < 0) return -1;
+    return (int64_t)block_table[(size_t)(row / Hkv) * max_pages + qp / kP] * kP + qp % kP;
+  }
+  __device__ void copy(int row, int is_v, int l) const {
+    const int p = pos(row);
+    if (p < 0 || (p >= S0 && W == 0)) return;
+    const int b = row / Hkv, h = row % Hkv;
+    // same lane and address as the read of a demoted row: ordered after it
+    seg_row(seg, Hkv, S0, W, b, h, is_v, seg_slot(S0, W, p))[l] =
+        reinterpret_cast<const uint32_t*>((is_v ? v : k) + (size_t)row * kD)[l];
+  }
+};
+
 // Clip, quantize, pack and write one rotated row (token, head) whose channels l
-// and l + 64 are in lane l.  Rows >= n_rows (wave-uniform) only take part in the
-// cross-lane steps.
-__device__ inline void store_row(uint8_t* __restrict__ pages, int Hkv,
-                                 const int64_t* __restrict__ slots, int n_rows, int row, int is_v,
-                                 float clip, double acc0, double acc1, int l) {
+// and l + 64 are in lane l, to pool slot `slot` (wave-uniform; < 0: the row only
+// takes part in the cross-lane steps).
+__device__ inline void store_row(uint8_t* __restrict__ pages, int Hkv, int64_t slot, int row,
+                                 int is_v, float clip, double acc0, double acc1, int l) {
   const float xt0 = __double2float_rn(acc0);  // channel l
   const float xt1 = __double2float_rn(acc1);  // channel l + 64
   const QOut q0 = quantize(xt0, clip);
   const QOut q1 = quantize(xt1, clip);
   const uint32_t byte0 = pack_quad(q0.code, l);  // quad l/4
   const uint32_t byte1 = pack_quad(q1.code, l);  // quad 16 + l/4
-  if (row >= n_rows) return;                     // uniform across the wave
-  const int tok = row / Hkv;
-  const int h = row - tok * Hkv;
-  const int64_t slot = slots[tok];
+  if (slot < 0) return;                          // uniform across the wave
+  const int h = row % Hkv;
   const int64_t page = slot / kP;
   const int t = (int)(slot - page * kP);
   uint8_t* blk = pages + ((size_t)page * Hkv + h) * kBlockBytes;
@@ -199,15 +313,12 @@ __device__ inline void store_row(uint8_t* __restrict__ pages, int Hkv,
 
 // Cache update by one block: is_v selects K or V, blocks bx of gx take rows
 // grid-stride.  Rs: 64 KB LDS for the matrix, xs: the waves' input rows.
-template <int RW>
+template <int RW, class Rows>
 __device__ inline void append_body(float* Rs, double (*xs)[RW][kD], int is_v, int bx, int gx,
-                                   uint8_t* __restrict__ pages, int Hkv,
-                                   const uint16_t* __restrict__ k, const uint16_t* __restrict__ v,
-                                   const int64_t* __restrict__ slots, int n_rows,
-                                   const float* __restrict__ Rk, const float* __restrict__ Rv,
-                                   float clip_k, float clip_v) {
+                                   uint8_t* __restrict__ pages, int Hkv, const Rows& rows,
+                                   int n_rows, const float* __restrict__ Rk,
+                                   const float* __restrict__ Rv, float clip_k, float clip_v) {
   const float* __restrict__ R = is_v ? Rv : Rk;
-  const uint16_t* __restrict__ X = is_v ? v : k;
   const float clip = is_v ? clip_v : clip_k;
 
   {  // 16 float4 per thread, all loads issued before the stores
@@ -230,13 +341,15 @@ __device__ inline void append_body(float* Rs, double (*xs)[RW][kD], int is_v, in
     for (int rr = 0; rr < RW; ++rr) {
       const int row = item * RW + rr;
       double x0 = 0.0, x1 = 0.0;
-      if (row < n_rows) {
-        const uint32_t pair = reinterpret_cast<const uint32_t*>(X + (size_t)row * kD)[l];
+      const uint16_t* src = rows.src(row, is_v);
+      if (src) {
+        const uint32_t pair = reinterpret_cast<const uint32_t*>(src)[l];
         x0 = (double)__uint_as_float(pair << 16);
         x1 = (double)__uint_as_float(pair & 0xffff0000u);
       }
       xs[w][rr][2 * l] = x0;
       xs[w][rr][2 * l + 1] = x1;
+      rows.copy(row, is_v, l);
     }
 
     double acc0[RW], acc1[RW];
@@ -255,20 +368,23 @@ __device__ inline void append_body(float* Rs, double (*xs)[RW][kD], int is_v, in
     }
 
 #pragma unroll
-    for (int rr = 0; rr < RW; ++rr)
-      store_row(pages, Hkv, slots, n_rows, item * RW + rr, is_v, clip, acc0[rr], acc1[rr], l);
+    for (int rr = 0; rr < RW; ++rr) {
+      const int row = item * RW + rr;
+      store_row(pages, Hkv, rows.slot(row), row, is_v, clip, acc0[rr], acc1[rr], l);
+    }
   }
 }
 
-template <int RW>
-__global__ __launch_bounds__(256) void append_kernel(
-    uint8_t* __restrict__ pages, int Hkv, const uint16_t* __restrict__ k,
-    const uint16_t* __restrict__ v, const int64_t* __restrict__ slots, int n_rows,
-    const float* __restrict__ Rk, const float* __restrict__ Rv, float clip_k, float clip_v) {
+template <int RW, class Rows>
+__global__ __launch_bounds__(256) void append_kernel(uint8_t* __restrict__ pages, int Hkv,
+                                                     Rows rows, int n_rows,
+                                                     const float* __restrict__ Rk,
+                                                     const float* __restrict__ Rv, float clip_k,
+                                                     float clip_v) {
   __shared__ float Rs[kD * kD];
   __shared__ double xs[kWaves][RW][kD];
-  append_body<RW>(Rs, xs, blockIdx.y, blockIdx.x, gridDim.x, pages, Hkv, k, v, slots, n_rows, Rk,
-                  Rv, clip_k, clip_v);
+  append_body<RW>(Rs, xs, blockIdx.y, blockIdx.x, gridDim.x, pages, Hkv, rows, n_rows, Rk, Rv,
+                  clip_k, clip_v);
 }
 
 // ---------------------------------------------------------------------------
@@ -284,9 +400,9 @@ __global__ __launch_bounds__(256) void append_kernel(
 constexpr int kBulkWaves = 8;
 constexpr int kBulkRows = 8;
 
-// store_row for the pair layout: lane l' of the half holds channels l' + 32 q.
-__device__ inline void store_row4(uint8_t* __restrict__ pages, int Hkv,
-                                  const int64_t* __restrict__ slots, int n_rows, int row,
+// store_row for the pair layout: lane l' of the half holds channels l' + 32 q;
+// slot is uniform across the half wave.
+__device__ inline void store_row4(uint8_t* __restrict__ pages, int Hkv, int64_t slot, int row,
                                   int is_v, float clip, const double (&acc)[4], int lp) {
   QOut qo[4];
   uint32_t byte[4];
@@ -295,10 +411,8 @@ __device__ inline void store_row4(uint8_t* __restrict__ pages, int Hkv,
     qo[q] = quantize(__double2float_rn(acc[q]), clip);  // group q of the row
     byte[q] = pack_quad(qo[q].code, lp);                 // quad 8 q + l'/4
   }
-  if (row >= n_rows) return;
-  const int tok = row / Hkv;
-  const int h = row - tok * Hkv;
-  const int64_t slot = slots[tok];
+  if (slot < 0) return;
+  const int h = row % Hkv;
   const int64_t page = slot / kP;
   const int t = (int)(slot - page * kP);
   uint8_t* blk = pages + ((size_t)page * Hkv + h) * kBlockBytes;
@@ -319,16 +433,15 @@ __device__ inline void store_row4(uint8_t* __restrict__ pages, int Hkv,
   }
 }
 
+template <class Rows>
 __global__ __launch_bounds__(512) void append_bulk_kernel(
-    uint8_t* __restrict__ pages, int Hkv, const uint16_t* __restrict__ k,
-    const uint16_t* __restrict__ v, const int64_t* __restrict__ slots, int n_rows,
-    const float* __restrict__ Rk, const float* __restrict__ Rv, float clip_k, float clip_v) {
+    uint8_t* __restrict__ pages, int Hkv, Rows rows, int n_rows, const float* __restrict__ Rk,
+    const float* __restrict__ Rv, float clip_k, float clip_v) {
   // xs first: its reads use the 16-bit LDS offset field
   __shared__ double2 xs[kBulkWaves][kBulkRows][kD / 2];      // 64 KB
   __shared__ float4 Rq[kD][kD / 4];                          // 64 KB
   const int is_v = blockIdx.y;
   const float* __restrict__ R = is_v ? Rv : Rk;
-  const uint16_t* __restrict__ X = is_v ? v : k;
   const float clip = is_v ? clip_v : clip_k;
   const int t = threadIdx.x;
   {  // 8 float4 per thread, loads issued before the stores
@@ -354,11 +467,13 @@ __global__ __launch_bounds__(512) void append_bulk_kernel(
     for (int rr = 0; rr < kBulkRows; ++rr) {
       const int row = item * kBulkRows + rr;
       double2 x = make_double2(0.0, 0.0);
-      if (row < n_rows) {
-        const uint32_t pair = reinterpret_cast<const uint32_t*>(X + (size_t)row * kD)[l];
+      const uint16_t* src = rows.src(row, is_v);
+      if (src) {
+        const uint32_t pair = reinterpret_cast<const uint32_t*>(src)[l];
         x = make_double2((double)__uint_as_float(pair << 16), (double)__uint_as_float(pair & 0xffff0000u));
       }
       xs[w][rr][l] = x;  // channels 2l, 2l + 1
+      rows.copy(row, is_v, l);
     }
     double acc[kBulkRows / 2][4];
 #pragma unroll
@@ -380,8 +495,10 @@ __global__ __launch_bounds__(512) void append_bulk_kernel(
       }
     }
 #pragma unroll
-    for (int p = 0; p < kBulkRows / 2; ++p)
-      store_row4(pages, Hkv, slots, n_rows, item * kBulkRows + 2 * p + half, is_v, clip, acc[p], lp);
+    for (int p = 0; p < kBulkRows / 2; ++p) {
+      const int row = item * kBulkRows + 2 * p + half;
+      store_row4(pages, Hkv, rows.slot(row), row, is_v, clip, acc[p], lp);
+    }
   }
 }
 
@@ -396,20 +513,19 @@ __global__ __launch_bounds__(256) void prepare_kernel(const uint16_t* __restrict
 // One launch for a decode step's prologue: blockIdx.y 0/1 = K/V cache update
 // (append_blocks blocks), 2 = query rotation (prep_blocks blocks).  The two are
 // independent; the split kernel that follows needs both.
-template <int RW>
+template <int RW, class Rows>
 __global__ __launch_bounds__(256) void prologue_kernel(
-    uint8_t* __restrict__ pages, int Hkv, const uint16_t* __restrict__ k,
-    const uint16_t* __restrict__ v, const int64_t* __restrict__ slots, int n_rows,
-    const float* __restrict__ Rk, const float* __restrict__ Rv, float clip_k, float clip_v,
-    int append_blocks, const uint16_t* __restrict__ q, int q_rows, float qscale,
-    float* __restrict__ qt, int prep_blocks) {
+    uint8_t* __restrict__ pages, int Hkv, Rows rows, int n_rows, const float* __restrict__ Rk,
+    const float* __restrict__ Rv, float clip_k, float clip_v, int append_blocks,
+    const uint16_t* __restrict__ q, int q_rows, float qscale, float* __restrict__ qt,
+    int prep_blocks) {
   __shared__ float Rs[kD * kD];
   __shared__ double xs[kWaves][RW][kD];
   __shared__ float4 qs[kPrepRows][kD / 4];
   if (blockIdx.y < 2) {
     if ((int)blockIdx.x < append_blocks)
-      append_body<RW>(Rs, xs, blockIdx.y, blockIdx.x, append_blocks, pages, Hkv, k, v, slots,
-                      n_rows, Rk, Rv, clip_k, clip_v);
+      append_body<RW>(Rs, xs, blockIdx.y, blockIdx.x, append_blocks, pages, Hkv, rows, n_rows,
+                      Rk, Rv, clip_k, clip_v);
   } else if ((int)blockIdx.x < prep_blocks) {
     prepare_body(Rs, qs, blockIdx.x, q, q_rows, Rk, qscale, qt);
   }
@@ -423,26 +539,64 @@ int64_t append_blocks_for(int64_t n_rows, int rw) {
   const int64_t blocks = (n_items + kWaves - 1) / kWaves;
   return blocks > 1024 ? 1024 : blocks;
 }
+
+template <class Rows>
+hipError_t launch_rows(void* pages, int64_t Hkv, const Rows& rows, int64_t n_rows, const float* Rk,
+                       const float* Rv, float clip_k, float clip_v, hipStream_t st) {
+  if (n_rows <= 4096) {  // one decode step: many short waves
+    const dim3 grid((unsigned)append_blocks_for(n_rows, 1), 2);
+    hipLaunchKernelGGL((append_kernel<1, Rows>), grid, dim3(256), 0, st, static_cast<uint8_t*>(pages),
+                       (int)Hkv, rows, (int)n_rows, Rk, Rv, clip_k, clip_v);
+  } else {  // bulk: one persistent 8-wave block per CU, half of them per tensor
+    const int64_t items = (n_rows + kBulkRows - 1) / kBulkRows;
+    int64_t nb = (items + kBulkWaves - 1) / kBulkWaves;
+    const int64_t cap = std::max<int64_t>(1, device_cus() / 2);
+    if (nb > cap) nb = cap;
+    hipLaunchKernelGGL(append_bulk_kernel<Rows>, dim3((unsigned)nb, 2), dim3(512), 0, st,
+                       static_cast<uint8_t*>(pages), (int)Hkv, rows, (int)n_rows, Rk, Rv, clip_k,
+                       clip_v);
+  }
+  return hipGetLastError();
+}
+
+template <class Rows>
+hipError_t launch_prologue(void* pages, int64_t Hkv, const Rows& rows, int64_t n_rows,
+                           const float* Rk, const float* Rv, float clip_k, float clip_v,
+                           const uint16_t* q, int B, int Hq, float qscale, float* qt,
+                           hipStream_t st) {
+  const int rw = n_rows <= 4096 ? 1 : 4;
+  const int ab = n_rows > 0 ? (int)append_blocks_for(n_rows, rw) : 0;
+  const int pb = (B * Hq + kPrepRows - 1) / kPrepRows;
+  const dim3 grid((unsigned)(ab > pb ? ab : pb), 3);
+  if (rw == 1)
+    hipLaunchKernelGGL((prologue_kernel<1, Rows>), grid, dim3(256), 0, st,
+                       static_cast<uint8_t*>(pages), (int)Hkv, rows, (int)n_rows, Rk, Rv, clip_k,
+                       clip_v, ab, q, B * Hq, qscale, qt, pb);
+  else
+    hipLaunchKernelGGL((prologue_kernel<4, Rows>), grid, dim3(256), 0, st,
+                       static_cast<uint8_t*>(pages), (int)Hkv, rows, (int)n_rows, Rk, Rv, clip_k,
+                       clip_v, ab, q, B * Hq, qscale, qt, pb);
+  return hipGetLastError();
+}
 }  // namespace
 
 hipError_t launch_append(void* pages, int64_t Hkv, const uint16_t* k, const uint16_t* v,
                          const int64_t* slots, int n_tok, const float* Rk, const float* Rv,
                          float clip_k, float clip_v, hipStream_t st) {
   const int64_t n_rows = (int64_t)n_tok * Hkv;
-  if (n_rows <= 4096) {  // one decode step: many short waves
-    const dim3 grid((unsigned)append_blocks_for(n_rows, 1), 2);
-    hipLaunchKernelGGL(append_kernel<1>, grid, dim3(256), 0, st, static_cast<uint8_t*>(pages),
-                       (int)Hkv, k, v, slots, (int)n_rows, Rk, Rv, clip_k, clip_v);
-  } else {  // bulk: one persistent 8-wave block per CU, half of them per tensor
-    const int64_t items = (n_rows + kBulkRows - 1) / kBulkRows;
-    int64_t nb = (items + kBulkWaves - 1) / kBulkWaves;
-    const int64_t cap = std::max<int64_t>(1, device_cus() / 2);
-    if (nb > cap) nb = cap;
-    hipLaunchKernelGGL(append_bulk_kernel, dim3((unsigned)nb, 2), dim3(512), 0, st,
-                       static_cast<uint8_t*>(pages), (int)Hkv, k, v, slots, (int)n_rows, Rk, Rv,
-                       clip_k, clip_v);
-  }
-  return hipGetLastError();
+  const PlainRows rows{k, v, slots, (int)n_rows, (int)Hkv};
+  return launch_rows(pages, Hkv, rows, n_rows, Rk, Rv, clip_k, clip_v, st);
+}
+
+hipError_t launch_mixed_append(void* pages, uint16_t* seg, int64_t Hkv, int S0, int W,
+                               const uint16_t* k, const uint16_t* v, const int32_t* seq_idx,
+                               const int64_t* pos, int n_tok, const int32_t* seq_lens,
+                               const int32_t* block_table, int max_pages, const float* Rk,
+                               const float* Rv, float clip_k, float clip_v, hipStream_t st) {
+  const int64_t n_rows = (int64_t)n_tok * Hkv;
+  const PrefillRows rows{k, v, seg, seq_idx, pos, seq_lens, block_table, (int)n_rows, (int)Hkv,
+                         max_pages, S0, W};
+  return launch_rows(pages, Hkv, rows, n_rows, Rk, Rv, clip_k, clip_v, st);
 }
 
 hipError_t launch_decode_prepare(const uint16_t* q, int B, int Hq, const float* Rk,
@@ -458,19 +612,21 @@ hipError_t launch_step_prologue(void* pages, int64_t Hkv, const uint16_t* k, con
                                 const float* Rv, float clip_k, float clip_v, const uint16_t* q,
                                 int B, int Hq, float qscale, float* qt, hipStream_t st) {
   const int64_t n_rows = (int64_t)n_tok * Hkv;
-  const int rw = n_rows <= 4096 ? 1 : 4;
-  const int ab = n_rows > 0 ? (int)append_blocks_for(n_rows, rw) : 0;
-  const int pb = (B * Hq + kPrepRows - 1) / kPrepRows;
-  const dim3 grid((unsigned)(ab > pb ? ab : pb), 3);
-  if (rw == 1)
-    hipLaunchKernelGGL(prologue_kernel<1>, grid, dim3(256), 0, st, static_cast<uint8_t*>(pages),
-                       (int)Hkv, k, v, slots, (int)n_rows, Rk, Rv, clip_k, clip_v, ab, q, B * Hq,
-                       qscale, qt, pb);
-  else
-    hipLaunchKernelGGL(prologue_kernel<4>, grid, dim3(256), 0, st, static_cast<uint8_t*>(pages),
-                       (int)Hkv, k, v, slots, (int)n_rows, Rk, Rv, clip_k, clip_v, ab, q, B * Hq,
-                       qscale, qt, pb);
-  return hipGetLastError();
+  const PlainRows rows{k, v, slots, (int)n_rows, (int)Hkv};
+  return launch_prologue(pages, Hkv, rows, n_rows, Rk, Rv, clip_k, clip_v, q, B, Hq, qscale, qt,
+                         st);
+}
+
+hipError_t launch_mixed_step_prologue(void* pages, uint16_t* seg, int64_t Hkv, int S0, int W,
+                                      const uint16_t* k, const uint16_t* v,
+                                      const int32_t* seq_lens, const int32_t* block_table,
+                                      int max_pages, const float* Rk, const float* Rv,
+                                      float clip_k, float clip_v, const uint16_t* q, int B,
+                                      int Hq, float qscale, float* qt, hipStream_t st) {
+  const int64_t n_rows = (int64_t)B * Hkv;
+  const StepRows rows{k, v, seg, seq_lens, block_table, (int)n_rows, (int)Hkv, max_pages, S0, W};
+  return launch_prologue(pages, Hkv, rows, n_rows, Rk, Rv, clip_k, clip_v, q, B, Hq, qscale, qt,
+                         st);
 }
 
 }  // namespace oscar

@@ -38,6 +38,9 @@ __device__ inline uint16_t f32_to_bf16_rne(float f) {
 constexpr int kRedRows = 8;
 constexpr int kRvPitch4 = kD / 4 + 1;  // row pitch of the LDS copy in float4
 
+// MIXED: a row has num_splits + 1 slots; the last holds the bf16 tokens' state
+// in the original basis, o = (sum_s e_s o~_s R_v^T + e_b o_b) / L.
+template <bool MIXED>
 __global__ __launch_bounds__(256) void reduce_kernel(int rows, int num_splits,
                                                      const float* __restrict__ part_o,
                                                      const float* __restrict__ part_ml,
@@ -45,18 +48,22 @@ __global__ __launch_bounds__(256) void reduce_kernel(int rows, int num_splits,
                                                      void* __restrict__ out, int out_f32) {
   __shared__ float4 Rs[kD * kRvPitch4];
   __shared__ float4 om[kRedRows][kD / 4];
+  __shared__ float eb_il[kRedRows];  // MIXED: e_b / L per row
+  const int stride = MIXED ? num_splits + 1 : num_splits;
   const int r0 = blockIdx.x * kRedRows;
   const int t = threadIdx.x;
   {  // 8 rows x 32 float4 columns: one (row, float4) per thread
     const int rr = t >> 5, c4 = t & 31, r = r0 + rr;
     float4 o = make_float4(0.0f, 0.0f, 0.0f, 0.0f);
-    const float2* ml = reinterpret_cast<const float2*>(part_ml + (size_t)r * num_splits * 2);
+    const float2* ml = reinterpret_cast<const float2*>(part_ml + (size_t)r * stride * 2);
     // live slots lead (empty ones only follow the end of a sequence): n_live is
     // one past the last live slot.  Slot s is read by thread s % 32 of the row;
     // maximum and last live slot are then reduced over the row's 32 threads.
     float M = -INFINITY;
     int n_live = 0;
     const float m0 = (r < rows && c4 < num_splits) ? ml[c4].x : -INFINITY;
+    float2 mb = make_float2(-INFINITY, 0.0f);
+    if (MIXED && r < rows) mb = ml[num_splits];
     // R_v (row-major 128 x 128) to LDS, 16 float4 per thread: loads issued here so
     // that they overlap the slot loads
     float4 v[kD * kD / 4 / 256];
@@ -84,9 +91,11 @@ __global__ __launch_bounds__(256) void reduce_kernel(int rows, int num_splits,
       M = fmaxf(M, __shfl_xor(M, off, 32));
       n_live = max(n_live, __shfl_xor(n_live, off, 32));
     }
+    if (MIXED) M = fmaxf(M, mb.x);
+    float ebl = 0.0f;
     if (r < rows) {
       if (M != -INFINITY) {
-        const float4* po = reinterpret_cast<const float4*>(part_o + (size_t)r * num_splits * kD) + c4;
+        const float4* po = reinterpret_cast<const float4*>(part_o + (size_t)r * stride * kD) + c4;
         float L = 0.0f;
         // up to 16 slots per round, loads issued together (indices clamped to the
         // live range, weights of the clamped repeats set to 0)
@@ -108,11 +117,18 @@ __global__ __launch_bounds__(256) void reduce_kernel(int rows, int num_splits,
             o.z = fmaf(e, use ? x[k].z : 0.0f, o.z); o.w = fmaf(e, use ? x[k].w : 0.0f, o.w);
           }
         }
+        float eb = 0.0f;
+        if (MIXED && mb.x != -INFINITY) {
+          eb = exp2f(mb.x - M);
+          L = fmaf(eb, mb.y, L);
+        }
         const float il = L > 0.0f ? 1.0f / L : 0.0f;
         o.x *= il; o.y *= il; o.z *= il; o.w *= il;
+        ebl = eb * il;
       }
     }
     om[rr][c4] = o;
+    if (MIXED && c4 == 0) eb_il[rr] = ebl;
   }
   __syncthreads();
   const int j = t & (kD - 1);
@@ -139,6 +155,15 @@ __global__ __launch_bounds__(256) void reduce_kernel(int rows, int num_splits,
 #pragma unroll
     for (int i = 0; i < 4; ++i) acc[i] = O[(rg + i) * kD + j];
   }
+  if (MIXED) {  // the bf16 tokens' part, already in the original basis
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int r = r0 + rg + i;
+      const float e = eb_il[rg + i];
+      if (r < rows && e != 0.0f)
+        acc[i] = fmaf(e, part_o[((size_t)r * stride + num_splits) * kD + j], acc[i]);
+    }
+  }
 #pragma unroll
   for (int i = 0; i < 4; ++i) {
     const int r = r0 + rg + i;
@@ -153,18 +178,24 @@ __global__ __launch_bounds__(256) void reduce_kernel(int rows, int num_splits,
 hipError_t launch_decode_split(const uint8_t* pages, int Hkv, int B, int Hq,
                                const int32_t* block_table, int max_pages,
                                const int32_t* seq_lens, int num_splits, const float* qt,
-                               float* part_o, float* part_ml, hipStream_t st) {
+                               float* part_o, float* part_ml, hipStream_t st,
+                               const MixedSpec* mixed) {
   // one resident wave per SIMD slot: 4 waves per SIMD, 4 SIMDs per CU
   return launch_decode_split_mfma(pages, Hkv, B, Hq, block_table, max_pages, seq_lens,
-                                  num_splits, 16 * device_cus(), qt, part_o, part_ml, st);
+                                  num_splits, 16 * device_cus(), qt, part_o, part_ml, st, mixed);
 }
 
 hipError_t launch_decode_reduce(int B, int Hq, int num_splits, const float* part_o,
                                 const float* part_ml, const float* Rv, void* out, int out_f32,
-                                hipStream_t st) {
+                                hipStream_t st, const MixedSpec* mixed) {
   const int rows = B * Hq;
-  hipLaunchKernelGGL(reduce_kernel, dim3((rows + kRedRows - 1) / kRedRows), dim3(256), 0, st,
-                     rows, num_splits, part_o, part_ml, Rv, out, out_f32);
+  const dim3 grid((rows + kRedRows - 1) / kRedRows);
+  if (mixed)
+    hipLaunchKernelGGL(reduce_kernel<true>, grid, dim3(256), 0, st, rows, num_splits, part_o,
+                       part_ml, Rv, out, out_f32);
+  else
+    hipLaunchKernelGGL(reduce_kernel<false>, grid, dim3(256), 0, st, rows, num_splits, part_o,
+                       part_ml, Rv, out, out_f32);
   return hipGetLastError();
 }
 

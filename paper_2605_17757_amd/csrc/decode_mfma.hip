@@ -221,10 +221,10 @@ struct WaveState {
   float of[8];          // unnormalized o~ of head hi, tile (G, F) at of[2G + F]
 };
 
-// FULL: all 64 token slots of the page are in the sequence (every page but
-// possibly the sequence's last); otherwise slots >= ntok are masked.
+// FULL: all 64 token slots of the page are read; otherwise only slots in
+// [t0, t1) (the partial first or last page of a token range).
 template <bool FULL>
-__device__ inline void compute_page(WaveState& st, WaveLds& L, int ntok, int lo, int hi) {
+__device__ inline void compute_page(WaveState& st, WaveLds& L, int t0, int t1, int lo, int hi) {
   char* pb = reinterpret_cast<char*>(L.page);
   // ---- scores of head hi for tokens 4*lo + u ----
   // code dword 2g + (hi>>1) of token 4*lo + u at byte 32u + 8g from the lane base
@@ -251,7 +251,7 @@ __device__ inline void compute_page(WaveState& st, WaveLds& L, int ntok, int lo,
     S[u] = acc;
   }
   // ---- online softmax, head hi ----
-  auto valid = [&](int u) { return FULL || 4 * lo + u < ntok; };
+  auto valid = [&](int u) { return FULL || (4 * lo + u >= t0 && 4 * lo + u < t1); };
   float mx = -INFINITY;
 #pragma unroll
   for (int u = 0; u < 4; ++u)
@@ -288,7 +288,7 @@ __device__ inline void compute_page(WaveState& st, WaveLds& L, int ntok, int lo,
 #pragma unroll
   for (int e = 0; e < 16; ++e) {
     sz[e] = comp(vz[e >> 2], e & 3);
-    if (!FULL && 16 * hi + e >= ntok) sz[e] = 0u;  // (0, 0): w = 0, z = 0
+    if (!FULL && (16 * hi + e < t0 || 16 * hi + e >= t1)) sz[e] = 0u;  // (0, 0): w = 0, z = 0
   }
   // largest V scale of the group on this page: scales are positive binary16, so
   // their bit patterns order like their values (high halves, the zero points, ignored)
@@ -357,21 +357,41 @@ __device__ inline void compute_page(WaveState& st, WaveLds& L, int ntok, int lo,
   }
 }
 
-// Pages [p0, p1) of sequence b, kv-head kvh, query-head chunk `chunk`: online
-// softmax over the pages and the partial state written to slot `piece` of the
-// (sequence, head) rows.  `last`: the piece ends the sequence, so the slots
-// after it are marked empty.  The wave has done `done0` of its `total` pages
-// before this piece (issue-priority bands).
+// The INT2 token range of a sequence in page terms: pages [first, first + npg)
+// of its block-table row; token slots [t0, 64) of the range's first page and
+// [0, t1) of its last page are in the range (t0 = 0, t1 = 64 when aligned).
+struct TokRange {
+  int first, npg, t0, t1;
+};
+// Tokens [lo, hi) of a sequence.
+__device__ inline TokRange tok_range(int lo, int hi) {
+  TokRange r;
+  r.first = lo / kP;
+  r.npg = hi > lo ? (hi + kP - 1) / kP - r.first : 0;
+  r.t0 = lo - r.first * kP;
+  r.t1 = hi - (r.first + r.npg - 1) * kP;
+  return r;
+}
+
+// Pages [p0, p1) of the token range R of sequence b (page indices relative to
+// R.first), kv-head kvh, query-head chunk `chunk`: online softmax over the pages
+// and the partial state written to slot `piece` of the (sequence, head) rows,
+// whose slots are row_stride apart.  `last`: the piece ends the range, so slots
+// piece + 1 .. num_splits - 1 are marked empty.  The wave has done `done0` of its
+// `total` pages before this piece (issue-priority bands).  Without MIXED the
+// range starts at token 0 (R.t0 = 0).
+template <bool MIXED>
 __device__ __attribute__((always_inline)) inline void process_piece(WaveLds& L, const uint8_t* __restrict__ pages, int Hkv, int Hq,
                                      const int32_t* __restrict__ block_table, int max_pages, int b,
-                                     int len, int kvh, int chunk, int p0, int p1, int piece,
-                                     bool last, int num_splits, const float* __restrict__ qt,
+                                     TokRange R, int kvh, int chunk, int p0, int p1, int piece,
+                                     bool last, int num_splits, int row_stride,
+                                     const float* __restrict__ qt,
                                      float* __restrict__ part_o, float* __restrict__ part_ml,
                                      int done0, int total) {
   const int g_heads = Hq / Hkv;
   const int l = threadIdx.x, lo = l & 15, hi = l >> 4;
-  const int npg = (len + kP - 1) / kP;
-  const int32_t* __restrict__ bt = block_table + (size_t)b * max_pages;
+  const int npg = R.npg;
+  const int32_t* __restrict__ bt = block_table + (size_t)b * max_pages + (MIXED ? R.first : 0);
   const uint8_t* __restrict__ base = pages + (size_t)kvh * kBlockBytes;
   const size_t page_stride = (size_t)Hkv * kBlockBytes;
 
@@ -447,14 +467,21 @@ __device__ __attribute__((always_inline)) inline void process_piece(WaveLds& L, 
   int btv = (p0 + l < p1) ? bt[p0 + l] : 0;
   Stage sg;
   if (p0 < p1) stage_load(sg, base + (size_t)__builtin_amdgcn_readlane(btv, 0) * page_stride, l);
-  // pages [p0, pf) are full; page pf (if < p1) is the sequence's partial last page
-  const int pf = (p0 < p1 && p1 == npg && (len & (kP - 1)) != 0) ? p1 - 1 : p1;
+  // pages [p0, pf) are full; page pf (if < p1) is the range's partial last page
+  int pf = (p0 < p1 && p1 == npg && R.t1 != kP) ? p1 - 1 : p1;
+  int pg = p0;
+  if (MIXED && p0 == 0 && p0 < p1 && R.t0 != 0) {  // the range's partial first page
+    stage_store(L.page, sg, l);
+    stage_load(sg, base + (size_t)__builtin_amdgcn_readlane(btv, min(1, p1 - 1)) * page_stride, l);
+    compute_page<false>(st, L, R.t0, npg == 1 ? R.t1 : kP, lo, hi);
+    pg = 1;
+    pf = max(pf, 1);  // a one-page range is done
+  }
   // Full pages in four bands of the wave's whole page count (done0 pages of it
   // before this piece, total in all): the wave lowers its issue priority at
   // 25 %, 50 % and 75 % of its pages.  Waves sharing a SIMD otherwise issue in age
   // order, and the youngest of them finished up to 1.7x later than the oldest
   // with the same page count; waves that are behind now go first.
-  int pg = p0;
   for (int band = 1; band <= 4; ++band) {
     const int lim = (int)(((int64_t)(25 * band) * total + 99) / 100) - done0 + p0;  // band end
     const int e = min(max(lim, pg), pf);
@@ -466,7 +493,7 @@ __device__ __attribute__((always_inline)) inline void process_piece(WaveLds& L, 
         btv = (cb + l < p1) ? bt[cb + l] : 0;
       }
       stage_load(sg, base + (size_t)__builtin_amdgcn_readlane(btv, nx - cb) * page_stride, l);
-      compute_page<true>(st, L, kP, lo, hi);
+      compute_page<true>(st, L, 0, kP, lo, hi);
     }
     if (band < 4 && lim > p0 && lim <= pf) {  // the band ended inside this piece
       if (band == 1) __builtin_amdgcn_s_setprio(2);
@@ -476,7 +503,7 @@ __device__ __attribute__((always_inline)) inline void process_piece(WaveLds& L, 
   }
   if (pf < p1) {  // the partial last page; the stage holds it
     stage_store(L.page, sg, l);
-    compute_page<false>(st, L, len - pf * kP, lo, hi);
+    compute_page<false>(st, L, 0, R.t1, lo, hi);
   }
 
   // ---- write the split's partial state ----
@@ -486,8 +513,8 @@ __device__ __attribute__((always_inline)) inline void process_piece(WaveLds& L, 
   const float4 zh = *reinterpret_cast<const float4*>(&L.ws[4 * hi]);
   const int hout = 4 * chunk + hi;        // head of this lane's accumulators
   if (hout >= g_heads) return;            // padding head
-  const size_t row = ((size_t)b * Hq + kvh * g_heads + hout) * num_splits + piece;
-  if (last && lo == 0)  // the segment's last piece: the remaining slots hold nothing
+  const size_t row = ((size_t)b * Hq + kvh * g_heads + hout) * (MIXED ? row_stride : num_splits) + piece;
+  if (last && lo == 0)  // the range's last piece: the remaining slots hold nothing
     for (int s2 = piece + 1; s2 < num_splits; ++s2) {
       part_ml[(row + s2 - piece) * 2] = -INFINITY;
       part_ml[(row + s2 - piece) * 2 + 1] = 0.0f;
@@ -515,7 +542,9 @@ __device__ __attribute__((always_inline)) inline void process_piece(WaveLds& L, 
 // into at most S pieces (piece = r - first range of the sequence).  Each range
 // runs one wave per (kv-head, chunk of query heads): the waves of a range read
 // the blocks of the same pages at the same time (each page's Hkv blocks are
-// contiguous).  With S = 1 each range is one whole sequence.
+// contiguous).  With S = 1 each range is one whole sequence.  With MIXED a
+// sequence's pages are those of its INT2 history only, and a row's slots are
+// row_stride apart (the slots after the S history slots belong to other kernels).
 // Grid: ceil(n_ranges * Hkv / 8) * 8 * nch one-wave workgroups; workgroup id ->
 // (xcd = id % 8, slot = id / 8); chunk = slot % nch; u = (slot / nch) * 8 + xcd;
 // (range, kv-head) = (u / Hkv, u % Hkv): the chunks of one (range, kv-head)
@@ -528,10 +557,12 @@ __device__ inline int wave_sum_i(int x) {
   return x;
 }
 
+template <bool MIXED>
 __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(4, 4))) void split_mfma_kernel(
     const uint8_t* __restrict__ pages, int Hkv, int Hq, const int32_t* __restrict__ block_table,
     int max_pages, const int32_t* __restrict__ seq_lens, int num_splits, int n_ranges, int B,
-    const float* __restrict__ qt, float* __restrict__ part_o, float* __restrict__ part_ml) {
+    const float* __restrict__ qt, float* __restrict__ part_o, float* __restrict__ part_ml,
+    int S0, int W, int row_stride) {
   __shared__ WaveLds L;
   const int g_heads = Hq / Hkv;
   const int nch = (g_heads + 3) >> 2;
@@ -542,20 +573,27 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(4, 4))) void
   if (u >= (int64_t)n_ranges * Hkv) return;
   const int r = (int)(u / Hkv), kvh = (int)(u % Hkv);
   const int l = threadIdx.x;
-  auto seq_len = [&](int bb) {  // lengths beyond the block table are clamped
-    return min(max(seq_lens[bb], 0), max_pages * kP);
+  const int stride = MIXED ? row_stride : num_splits;
+  // The INT2 tokens of sequence bb: all of them, or with MIXED the history
+  // [lo, hi), lo = min(S0, n), hi = max(lo, n - W) (the bf16 sink and recent
+  // window are handled elsewhere).  Lengths beyond the block table are clamped.
+  auto range_of = [&](int bb) {
+    const int len = min(max(seq_lens[bb], 0), max_pages * kP);
+    if (!MIXED) return tok_range(0, len);
+    const int lo = min(S0, len);
+    return tok_range(lo, max(lo, len - W));
   };
   if (num_splits == 1) {  // one range per sequence
-    const int len = seq_len(r);
-    process_piece(L, pages, Hkv, Hq, block_table, max_pages, r, len, kvh, chunk, 0,
-                  (len + kP - 1) / kP, 0, true, 1, qt, part_o, part_ml, 0, 1 << 20);
+    const TokRange R = range_of(r);
+    process_piece<MIXED>(L, pages, Hkv, Hq, block_table, max_pages, r, R, kvh, chunk, 0, R.npg,
+                         0, true, 1, stride, qt, part_o, part_ml, 0, 1 << 20);
     return;
   }
   // total pages over all sequences
   int64_t T = 0;
   for (int b0 = 0; b0 < B; b0 += 64) {
     const int bb = b0 + l;
-    T += __builtin_amdgcn_readfirstlane(wave_sum_i(bb < B ? (seq_len(bb) + kP - 1) / kP : 0));
+    T += __builtin_amdgcn_readfirstlane(wave_sum_i(bb < B ? range_of(bb).npg : 0));
   }
   const int64_t pw = max(max((T + n_ranges - 1) / n_ranges,
                              (int64_t)((max_pages + num_splits - 2) / (num_splits - 1))),
@@ -566,9 +604,9 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(4, 4))) void
   // kv-head 0, chunk 0) wave, for all its heads
   if (kvh == 0 && chunk == 0)
     for (int bb = r; bb < B; bb += n_ranges)
-      if (seq_len(bb) == 0)
+      if (range_of(bb).npg == 0)
         for (int i = l; i < Hq * num_splits; i += 64) {
-          const size_t row = (size_t)bb * Hq * num_splits + i;
+          const size_t row = ((size_t)bb * Hq + i / num_splits) * stride + i % num_splits;
           part_ml[row * 2] = -INFINITY;
           part_ml[row * 2 + 1] = 0.0f;
         }
@@ -578,7 +616,7 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(4, 4))) void
   int64_t before = 0;
   for (int b0 = 0; b0 < B; b0 += 64) {
     const int bb = b0 + l;
-    const int np = bb < B ? (seq_len(bb) + kP - 1) / kP : 0;
+    const int np = bb < B ? range_of(bb).npg : 0;
     int incl = np;  // inclusive prefix sum over the lanes
 #pragma unroll
     for (int off = 1; off < 64; off <<= 1) {
@@ -602,15 +640,15 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(4, 4))) void
   while (true) {
     const int64_t end = min(xe, before + npg_b);
     const int piece = (int)(r - before / pw);
-    process_piece(L, pages, Hkv, Hq, block_table, max_pages, b, seq_len(b), kvh, chunk,
-                  (int)(x - before), (int)(end - before), piece, end == before + npg_b,
-                  num_splits, qt, part_o, part_ml, (int)(x - x0), (int)(xe - x0));
+    process_piece<MIXED>(L, pages, Hkv, Hq, block_table, max_pages, b, range_of(b), kvh, chunk,
+                         (int)(x - before), (int)(end - before), piece, end == before + npg_b,
+                         num_splits, stride, qt, part_o, part_ml, (int)(x - x0), (int)(xe - x0));
     x = end;
     if (x >= xe) break;
     before += npg_b;
     do {  // next sequence with pages
       if (++b >= B) return;  // not reached: pages remain before xe <= T
-      npg_b = (seq_len(b) + kP - 1) / kP;
+      npg_b = range_of(b).npg;
     } while (npg_b == 0);
   }
 }
@@ -621,18 +659,22 @@ hipError_t launch_decode_split_mfma(const uint8_t* pages, int Hkv, int B, int Hq
                                     const int32_t* block_table, int max_pages,
                                     const int32_t* seq_lens, int num_splits, int resident_waves,
                                     const float* qt, float* part_o, float* part_ml,
-                                    hipStream_t st) {
+                                    hipStream_t st, const MixedSpec* mixed) {
   const int g = Hq / Hkv;
   const int nch = (g + 3) / 4;
-  // one range per resident wave (each range runs nch waves, one per chunk of heads)
   // one range per resident wave group (each range runs Hkv * nch waves)
   const int64_t ranges =
       num_splits == 1 ? (int64_t)B : std::max<int64_t>(1, resident_waves / (nch * Hkv));
   const int64_t blocks = (ranges * Hkv + 7) / 8 * 8 * nch;
   if (blocks > 0x7fffffffLL) return hipErrorInvalidConfiguration;
-  hipLaunchKernelGGL(split_mfma_kernel, dim3((unsigned)blocks), dim3(64), 0, st, pages, Hkv, Hq,
-                     block_table, max_pages, seq_lens, num_splits, (int)ranges, B, qt, part_o,
-                     part_ml);
+  if (mixed)
+    hipLaunchKernelGGL(split_mfma_kernel<true>, dim3((unsigned)blocks), dim3(64), 0, st, pages,
+                       Hkv, Hq, block_table, max_pages, seq_lens, num_splits, (int)ranges, B, qt,
+                       part_o, part_ml, mixed->S0, mixed->W, mixed->row_stride);
+  else
+    hipLaunchKernelGGL(split_mfma_kernel<false>, dim3((unsigned)blocks), dim3(64), 0, st, pages,
+                       Hkv, Hq, block_table, max_pages, seq_lens, num_splits, (int)ranges, B, qt,
+                       part_o, part_ml, 0, 0, num_splits);
   return hipGetLastError();
 }
 

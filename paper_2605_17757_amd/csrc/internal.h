@@ -35,6 +35,13 @@ inline DecodeWs decode_ws(int64_t B, int64_t Hq, int64_t S) {
   return w;
 }
 
+// Mixed-precision cache (bf16 sink [0, S0), INT2 history, bf16 window of W):
+// the decode rows have row_stride = num_splits + 1 partial-state slots, the last
+// one for the bf16 tokens.
+struct MixedSpec {
+  int S0, W, row_stride;
+};
+
 // Kernel launchers (each returns the hipError_t of its launch).
 hipError_t launch_append(void* pages, int64_t Hkv, const uint16_t* k, const uint16_t* v,
                          const int64_t* slots, int n_tok, const float* Rk, const float* Rv,
@@ -47,21 +54,46 @@ hipError_t launch_step_prologue(void* pages, int64_t Hkv, const uint16_t* k, con
                                 const int64_t* slots, int n_tok, const float* Rk,
                                 const float* Rv, float clip_k, float clip_v, const uint16_t* q,
                                 int B, int Hq, float qscale, float* qt, hipStream_t st);
+// Mixed cache: prompt tokens routed to INT2 or the bf16 segment store by their
+// position in a cache of length seq_lens[b].
+hipError_t launch_mixed_append(void* pages, uint16_t* seg, int64_t Hkv, int S0, int W,
+                               const uint16_t* k, const uint16_t* v, const int32_t* seq_idx,
+                               const int64_t* pos, int n_tok, const int32_t* seq_lens,
+                               const int32_t* block_table, int max_pages, const float* Rk,
+                               const float* Rv, float clip_k, float clip_v, hipStream_t st);
+// Mixed cache decode-step prologue: one new token per sequence (sink, window with
+// demotion of the oldest window token, or INT2) and the query rotation.
+hipError_t launch_mixed_step_prologue(void* pages, uint16_t* seg, int64_t Hkv, int S0, int W,
+                                      const uint16_t* k, const uint16_t* v,
+                                      const int32_t* seq_lens, const int32_t* block_table,
+                                      int max_pages, const float* Rk, const float* Rv,
+                                      float clip_k, float clip_v, const uint16_t* q, int B,
+                                      int Hq, float qscale, float* qt, hipStream_t st);
+// Partial softmax state of the bf16 tokens (sink and window) of every (sequence,
+// head) row, in the original basis, into slot num_splits of rows of num_splits + 1.
+hipError_t launch_seg_partial(const uint16_t* seg, int Hkv, int S0, int W, int B, int Hq,
+                              const int32_t* seq_lens, int max_pages, const uint16_t* q,
+                              float qscale, int num_splits, float* part_o, float* part_ml,
+                              hipStream_t st);
+// mixed == nullptr: every token of a sequence is INT2 (rows of num_splits slots).
 hipError_t launch_decode_split(const uint8_t* pages, int Hkv, int B, int Hq,
                                const int32_t* block_table, int max_pages,
                                const int32_t* seq_lens, int num_splits, const float* qt,
-                               float* part_o, float* part_ml, hipStream_t st);
+                               float* part_o, float* part_ml, hipStream_t st,
+                               const MixedSpec* mixed = nullptr);
 // Balanced split kernel: `resident_waves` waves share the pages equally; a
 // (sequence, head) row gets at most num_splits partial states.
 hipError_t launch_decode_split_mfma(const uint8_t* pages, int Hkv, int B, int Hq,
                                     const int32_t* block_table, int max_pages,
                                     const int32_t* seq_lens, int num_splits, int resident_waves,
                                     const float* qt, float* part_o, float* part_ml,
-                                    hipStream_t st);
+                                    hipStream_t st, const MixedSpec* mixed);
 int device_cus();  // compute units of the current device (cached)
+// mixed != nullptr: rows of num_splits + 1 slots, the last one in the original
+// basis (added after the back-rotation).
 hipError_t launch_decode_reduce(int B, int Hq, int num_splits, const float* part_o,
                                 const float* part_ml, const float* Rv, void* out, int out_f32,
-                                hipStream_t st);
+                                hipStream_t st, const MixedSpec* mixed = nullptr);
 
 hipError_t launch_bf16_append(void* pages, int64_t Hkv, const uint16_t* k, const uint16_t* v,
                               const int64_t* slots, int n_tok, hipStream_t st);

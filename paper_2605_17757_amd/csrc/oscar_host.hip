@@ -72,6 +72,14 @@ int32_t resolve_default_splits(const oscar_layout* L, int32_t B, int32_t Hq,
 
 bool aligned(const void* p, size_t a) { return (reinterpret_cast<uintptr_t>(p) & (a - 1)) == 0; }
 
+// Mixed cache: sink and window sizes (and B, for the segment store size).
+bool seg_ok(int32_t B, int32_t S0, int32_t W) {
+  return B >= 1 && B <= 65535 && S0 >= 0 && W >= 0 && (int64_t)S0 + W <= 65536;
+}
+size_t seg_bytes(const oscar_layout* L, int32_t B, int32_t S0, int32_t W) {
+  return (size_t)B * (size_t)L->num_kv_heads * 2 * (size_t)(S0 + W) * (size_t)L->head_dim * 2;
+}
+
 }  // namespace
 
 extern "C" {
@@ -278,6 +286,155 @@ int oscar_decode_step(const oscar_layout* L, void* pages, const void* k_new, con
                                          reinterpret_cast<const float*>(base + ws.po_off),
                                          reinterpret_cast<const float*>(base + ws.pml_off), R_v,
                                          out, out_dtype == OSCAR_OUT_F32 ? 1 : 0, hs));
+}
+
+// ---------------------------------------------------------------------------
+// mixed-precision cache
+// ---------------------------------------------------------------------------
+
+size_t oscar_seg_bytes(const oscar_layout* L, int32_t B, int32_t S0, int32_t W) {
+  if (check_layout(L) != OSCAR_OK || !seg_ok(B, S0, W)) return 0;
+  return seg_bytes(L, B, S0, W);
+}
+
+size_t oscar_mixed_workspace_bytes(const oscar_layout* L, int32_t B, int32_t Hq,
+                                   int32_t num_splits) {
+  if (check_decode_common(L, B, Hq, num_splits) != OSCAR_OK) return 0;
+  return decode_ws(B, Hq, (int64_t)num_splits + 1).total;
+}
+
+int oscar_mixed_append(const oscar_layout* L, void* pages, void* seg, int32_t B, int32_t S0,
+                       int32_t W, const void* k, const void* v, const int32_t* seq_idx,
+                       const int64_t* pos, int32_t n_tok, const int32_t* block_table,
+                       int32_t max_pages_per_seq, const int32_t* seq_lens, const float* R_k,
+                       const float* R_v, float clip_k, float clip_v, void* stream) {
+  int st = check_layout(L);
+  if (st) return st;
+  if (n_tok < 0 || B < 1 || !seg_ok(B, S0, W) || !clip_ok(clip_k) || !clip_ok(clip_v) ||
+      max_pages_per_seq < 1)
+    return OSCAR_ERR_INVALID_ARG;
+  if (n_tok == 0) return OSCAR_OK;
+  if (!pages || !k || !v || !seq_idx || !pos || !block_table || !seq_lens || !R_k || !R_v ||
+      (S0 + W > 0 && !seg))
+    return OSCAR_ERR_INVALID_ARG;
+  if (!aligned(k, 4) || !aligned(v, 4) || !aligned(R_k, 16) || !aligned(R_v, 16) ||
+      !aligned(pages, 16) || !aligned(pos, 8) || !aligned(seg, 16))
+    return OSCAR_ERR_INVALID_ARG;
+  if ((int64_t)n_tok * L->num_kv_heads > 0x7fffffffLL ||
+      (int64_t)max_pages_per_seq * L->page_size > 0x7fffffffLL)
+    return OSCAR_ERR_UNSUPPORTED;
+  return hip_status(launch_mixed_append(
+      pages, static_cast<uint16_t*>(seg), L->num_kv_heads, S0, W, static_cast<const uint16_t*>(k),
+      static_cast<const uint16_t*>(v), seq_idx, pos, n_tok, seq_lens, block_table,
+      max_pages_per_seq, R_k, R_v, clip_k, clip_v, static_cast<hipStream_t>(stream)));
+}
+
+namespace {
+
+// Validation shared by the two mixed decode entry points; resolves num_splits.
+int check_mixed_decode(const oscar_layout* L, const void* pages, const void* seg, int32_t S0,
+                       int32_t W, const void* q, int32_t B, int32_t Hq,
+                       const int32_t* block_table, int32_t max_pages_per_seq,
+                       const int32_t* seq_lens, const float* R_k, const float* R_v,
+                       float sm_scale, int32_t* num_splits, void* workspace,
+                       size_t workspace_bytes, void* out, oscar_dtype out_dtype) {
+  if (*num_splits < 0) return OSCAR_ERR_INVALID_ARG;
+  if (*num_splits == 0) {
+    const int32_t s = resolve_default_splits(L, B, Hq, max_pages_per_seq);
+    if (s < 1) return s == 0 ? OSCAR_ERR_INVALID_ARG : -s;
+    *num_splits = s;
+  }
+  int st = check_decode_common(L, B, Hq, *num_splits);
+  if (st) return st;
+  if (*num_splits > 0x3fffffff || !seg_ok(B, S0, W)) return OSCAR_ERR_INVALID_ARG;
+  if (!pages || !q || !block_table || !seq_lens || !R_k || !R_v || !workspace || !out ||
+      max_pages_per_seq < 1 || !isfinite(sm_scale) || (S0 + W > 0 && !seg))
+    return OSCAR_ERR_INVALID_ARG;
+  if ((int64_t)max_pages_per_seq * L->page_size > 0x7fffffffLL) return OSCAR_ERR_UNSUPPORTED;
+  if (out_dtype != OSCAR_OUT_BF16 && out_dtype != OSCAR_OUT_F32) return OSCAR_ERR_INVALID_ARG;
+  if (!aligned(workspace, 256) || !aligned(pages, 16) || !aligned(q, 4) || !aligned(R_k, 16) ||
+      !aligned(R_v, 16) || !aligned(seg, 16) ||
+      !aligned(out, out_dtype == OSCAR_OUT_F32 ? 4 : 2))
+    return OSCAR_ERR_INVALID_ARG;
+  if (workspace_bytes < decode_ws(B, Hq, (int64_t)*num_splits + 1).total)
+    return OSCAR_ERR_WORKSPACE_TOO_SMALL;
+  return OSCAR_OK;
+}
+
+// split (history), bf16 partial and merge of a mixed decode; qt already in the workspace
+int launch_mixed_rest(const oscar_layout* L, const void* pages, const void* seg, int32_t S0,
+                      int32_t W, const void* q, int32_t B, int32_t Hq, const int32_t* block_table,
+                      int32_t max_pages_per_seq, const int32_t* seq_lens, const float* R_v,
+                      float sm_scale, int32_t num_splits, void* workspace, void* out,
+                      oscar_dtype out_dtype, hipStream_t hs) {
+  const DecodeWs ws = decode_ws(B, Hq, (int64_t)num_splits + 1);
+  uint8_t* base = static_cast<uint8_t*>(workspace);
+  float* po = reinterpret_cast<float*>(base + ws.po_off);
+  float* pml = reinterpret_cast<float*>(base + ws.pml_off);
+  const MixedSpec mx{S0, W, num_splits + 1};
+  int st = hip_status(launch_decode_split(static_cast<const uint8_t*>(pages), L->num_kv_heads, B,
+                                          Hq, block_table, max_pages_per_seq, seq_lens,
+                                          num_splits, reinterpret_cast<const float*>(base + ws.qt_off),
+                                          po, pml, hs, &mx));
+  if (st) return st;
+  st = hip_status(launch_seg_partial(static_cast<const uint16_t*>(seg), L->num_kv_heads, S0, W, B,
+                                     Hq, seq_lens, max_pages_per_seq,
+                                     static_cast<const uint16_t*>(q), sm_scale * kLog2e,
+                                     num_splits, po, pml, hs));
+  if (st) return st;
+  return hip_status(launch_decode_reduce(B, Hq, num_splits, po, pml, R_v, out,
+                                         out_dtype == OSCAR_OUT_F32 ? 1 : 0, hs, &mx));
+}
+
+}  // namespace
+
+int oscar_decode_attn_mixed(const oscar_layout* L, const void* pages, const void* seg,
+                            int32_t S0, int32_t W, const void* q, int32_t B, int32_t Hq,
+                            const int32_t* block_table, int32_t max_pages_per_seq,
+                            const int32_t* seq_lens, const float* R_k, const float* R_v,
+                            float sm_scale, int32_t num_splits, void* workspace,
+                            size_t workspace_bytes, void* out, oscar_dtype out_dtype,
+                            void* stream) {
+  int st = check_mixed_decode(L, pages, seg, S0, W, q, B, Hq, block_table, max_pages_per_seq,
+                              seq_lens, R_k, R_v, sm_scale, &num_splits, workspace,
+                              workspace_bytes, out, out_dtype);
+  if (st) return st;
+  hipStream_t hs = static_cast<hipStream_t>(stream);
+  const DecodeWs ws = decode_ws(B, Hq, (int64_t)num_splits + 1);
+  float* qt = reinterpret_cast<float*>(static_cast<uint8_t*>(workspace) + ws.qt_off);
+  st = hip_status(launch_decode_prepare(static_cast<const uint16_t*>(q), B, Hq, R_k,
+                                        sm_scale * kLog2e, qt, hs));
+  if (st) return st;
+  return launch_mixed_rest(L, pages, seg, S0, W, q, B, Hq, block_table, max_pages_per_seq,
+                           seq_lens, R_v, sm_scale, num_splits, workspace, out, out_dtype, hs);
+}
+
+int oscar_decode_step_mixed(const oscar_layout* L, void* pages, void* seg, int32_t S0,
+                            int32_t W, const void* k_new, const void* v_new, float clip_k,
+                            float clip_v, const void* q, int32_t B, int32_t Hq,
+                            const int32_t* block_table, int32_t max_pages_per_seq,
+                            const int32_t* seq_lens, const float* R_k, const float* R_v,
+                            float sm_scale, int32_t num_splits, void* workspace,
+                            size_t workspace_bytes, void* out, oscar_dtype out_dtype,
+                            void* stream) {
+  int st = check_mixed_decode(L, pages, seg, S0, W, q, B, Hq, block_table, max_pages_per_seq,
+                              seq_lens, R_k, R_v, sm_scale, &num_splits, workspace,
+                              workspace_bytes, out, out_dtype);
+  if (st) return st;
+  if (!k_new || !v_new || !clip_ok(clip_k) || !clip_ok(clip_v)) return OSCAR_ERR_INVALID_ARG;
+  if (!aligned(k_new, 4) || !aligned(v_new, 4)) return OSCAR_ERR_INVALID_ARG;
+  if ((int64_t)B * L->num_kv_heads > 0x7fffffffLL) return OSCAR_ERR_UNSUPPORTED;
+  hipStream_t hs = static_cast<hipStream_t>(stream);
+  const DecodeWs ws = decode_ws(B, Hq, (int64_t)num_splits + 1);
+  float* qt = reinterpret_cast<float*>(static_cast<uint8_t*>(workspace) + ws.qt_off);
+  st = hip_status(launch_mixed_step_prologue(
+      pages, static_cast<uint16_t*>(seg), L->num_kv_heads, S0, W,
+      static_cast<const uint16_t*>(k_new), static_cast<const uint16_t*>(v_new), seq_lens,
+      block_table, max_pages_per_seq, R_k, R_v, clip_k, clip_v, static_cast<const uint16_t*>(q),
+      B, Hq, sm_scale * kLog2e, qt, hs));
+  if (st) return st;
+  return launch_mixed_rest(L, pages, seg, S0, W, q, B, Hq, block_table, max_pages_per_seq,
+                           seq_lens, R_v, sm_scale, num_splits, workspace, out, out_dtype, hs);
 }
 
 // ---------------------------------------------------------------------------

@@ -149,3 +149,67 @@ def test_default_num_splits_bounds(L):
     # never fewer than two pages per split
     assert ok.default_num_splits(lay, 1, 32, 128) == 1
     assert ok.default_num_splits(lay, 1, 32, 8192) <= 8192 // 64 // 2
+
+
+def test_mixed_sizes(L):
+    lay = ok.Layout(8, 10)
+    for B, S0, W_ in ((64, 64, 256), (3, 20, 100), (1, 0, 0), (2, 0, 64)):
+        # the oracle sizes the same segment store independently
+        assert ok.seg_bytes(lay, B, S0, W_) == 2 * oracle.seg_elems(d=128, Hkv=8, B=B, S0=S0, W=W_)
+    assert ok.seg_bytes(lay, 64, 64, 256) == 64 * 8 * 2 * 320 * 128 * 2
+    assert ok.seg_bytes(lay, 1, -1, 4) == 0
+    assert ok.seg_bytes(lay, 1, 4, -1) == 0
+    assert ok.seg_bytes(lay, 1, 60000, 6000) == 0      # S0 + W > 65536
+    assert ok.seg_bytes(lay, 0, 4, 4) == 0
+    # rows of num_splits + 1 partial states
+    assert ok.mixed_workspace_bytes(lay, 64, 32, 8) == ok.decode_workspace_bytes(lay, 64, 32, 9)
+    assert ok.mixed_workspace_bytes(lay, 64, 30, 8) == 0
+
+
+def _mixed_append(L, lay, n_tok=4, S0=64, W_=256, seg=FAKE, B=2, clip=0.9, pos=FAKE, mp=4):
+    return L.oscar_mixed_append(ctypes.byref(lay), FAKE, seg, B, S0, W_, FAKE, FAKE, FAKE, pos,
+                                n_tok, FAKE, mp, FAKE, FAKE, FAKE, clip, 0.9, None)
+
+
+def test_mixed_append_rejects_invalid_arguments(L):
+    lay = ok.Layout(8, 10)
+    assert _mixed_append(L, lay, S0=-1) == ok.ERR_INVALID_ARG
+    assert _mixed_append(L, lay, W_=-5) == ok.ERR_INVALID_ARG
+    assert _mixed_append(L, lay, S0=65536, W_=1) == ok.ERR_INVALID_ARG
+    assert _mixed_append(L, lay, seg=None) == ok.ERR_INVALID_ARG         # segments need a store
+    assert _mixed_append(L, lay, seg=ctypes.c_void_p(0x10008)) == ok.ERR_INVALID_ARG
+    assert _mixed_append(L, lay, pos=ctypes.c_void_p(0x10004)) == ok.ERR_INVALID_ARG
+    assert _mixed_append(L, lay, B=0) == ok.ERR_INVALID_ARG
+    assert _mixed_append(L, lay, clip=0.0) == ok.ERR_INVALID_ARG
+    assert _mixed_append(L, lay, mp=0) == ok.ERR_INVALID_ARG
+    assert _mixed_append(L, lay, n_tok=-1) == ok.ERR_INVALID_ARG
+    assert _mixed_append(L, ok.Layout(8, 10, head_dim=64)) == ok.ERR_UNSUPPORTED
+    assert _mixed_append(L, lay, n_tok=0) == ok.OK                         # nothing launched
+
+
+def _mixed_decode(L, lay, step=False, S0=64, W_=256, seg=FAKE, B=2, Hq=32, S=2,
+                  ws_bytes=1 << 30, k=FAKE, clip=0.9):
+    if step:
+        return L.oscar_decode_step_mixed(ctypes.byref(lay), FAKE, seg, S0, W_, k, FAKE, clip, 0.9,
+                                         FAKE, B, Hq, FAKE, 4, FAKE, FAKE, FAKE, 0.088, S, FAKE,
+                                         ws_bytes, FAKE, 0, None)
+    return L.oscar_decode_attn_mixed(ctypes.byref(lay), FAKE, seg, S0, W_, FAKE, B, Hq, FAKE, 4,
+                                     FAKE, FAKE, FAKE, 0.088, S, FAKE, ws_bytes, FAKE, 0, None)
+
+
+@pytest.mark.parametrize("step", [False, True])
+def test_mixed_decode_rejects_invalid_arguments(L, step):
+    lay = ok.Layout(8, 10)
+    assert _mixed_decode(L, lay, step, S0=-1) == ok.ERR_INVALID_ARG
+    assert _mixed_decode(L, lay, step, seg=None) == ok.ERR_INVALID_ARG
+    assert _mixed_decode(L, lay, step, Hq=30) == ok.ERR_INVALID_ARG
+    assert _mixed_decode(L, lay, step, Hq=8 * 17) == ok.ERR_UNSUPPORTED
+    assert _mixed_decode(L, lay, step, S=-1) == ok.ERR_INVALID_ARG
+    # the plain workspace (num_splits slots a row) is one slot short
+    plain = ok.decode_workspace_bytes(lay, 2, 32, 2)
+    assert _mixed_decode(L, lay, step, ws_bytes=plain) == ok.ERR_WORKSPACE_TOO_SMALL
+    need = ok.mixed_workspace_bytes(lay, 2, 32, 2)
+    assert _mixed_decode(L, lay, step, ws_bytes=need - 1) == ok.ERR_WORKSPACE_TOO_SMALL
+    if step:
+        assert _mixed_decode(L, lay, step, k=None) == ok.ERR_INVALID_ARG
+        assert _mixed_decode(L, lay, step, clip=1.5) == ok.ERR_INVALID_ARG
