@@ -19,6 +19,12 @@ What it computes (arXiv 2605.17757):
                          window around the INT2 history, the per-step demotion of
                          the oldest window token (Alg. 1 DecodeStep) and decode
                          attention over all three segments.
+
+Quantizer variants (keyword arguments, defaults = the hot path's format):
+``meta`` 0/1 stores scale and zero as binary16 / bfloat16; ``clip`` 0/1 takes the
+clip threshold as ratio x group absmax / the token's ratio-quantile of |x~| (App.
+"Scale Determination and Per-token Clipping Details"); ``G`` any divisor of d; a
+rotation of ``None`` is the identity.
 """
 from __future__ import annotations
 
@@ -59,16 +65,19 @@ def lib():
         L.oracle_page_head_bytes.argtypes = [i32, i32, i32]
         L.oracle_rotate_row.argtypes = [P, P, i32, P]
         L.oracle_quantize_row.restype = i32
-        L.oracle_quantize_row.argtypes = [P, i32, i32, f32, P, P, P]
+        L.oracle_quantize_row.argtypes = [P, i32, i32, f32, i32, i32, P, P, P]
+        L.oracle_token_quantile.restype = f32
+        L.oracle_token_quantile.argtypes = [P, i32, f32]
         L.oracle_kv_append.restype = i64
-        L.oracle_kv_append.argtypes = [i32, i32, i32, i32, i64, P, P, P, P, i32, P, P, f32, f32]
+        L.oracle_kv_append.argtypes = [i32, i32, i32, i32, i32, i32, i64, P, P, P, P, i32, P, P,
+                                       f32, f32]
         L.oracle_read_token.argtypes = [i32, i32, i32, i32, P, i64, i32, i32, i32, P, P, P]
         L.oracle_decode.restype = i32
-        L.oracle_decode.argtypes = [i32, i32, i32, i32, i64, P, P, i32, i32, P, i32, P, P, P,
-                                    f64, P, i32, P]
+        L.oracle_decode.argtypes = [i32, i32, i32, i32, i32, i64, P, P, i32, i32, P, i32, P, P,
+                                    P, f64, P, i32, P]
         L.oracle_decode_brute.restype = i32
-        L.oracle_decode_brute.argtypes = [i32, i32, i32, i32, i64, P, P, i32, i32, P, i32, P,
-                                          P, P, f64, P]
+        L.oracle_decode_brute.argtypes = [i32, i32, i32, i32, i32, i64, P, P, i32, i32, P, i32,
+                                          P, P, P, f64, P]
         L.oracle_bf16_decode.restype = i32
         L.oracle_bf16_decode.argtypes = [i32, i32, i32, i64, P, P, i32, i32, P, i32, P, f64,
                                          P, i32, P]
@@ -80,14 +89,16 @@ def lib():
         L.oracle_f16_to_f32.argtypes = [ctypes.c_uint16]
         L.oracle_bf16_to_f32.restype = f32
         L.oracle_bf16_to_f32.argtypes = [ctypes.c_uint16]
+        L.oracle_f32_to_bf16_rne.restype = ctypes.c_uint16
+        L.oracle_f32_to_bf16_rne.argtypes = [f32]
         L.oracle_seg_write.restype = i32
         L.oracle_seg_write.argtypes = [i32, i32, i32, i32, i32, P, P, P, P, P, i32]
         L.oracle_mixed_update.restype = i64
-        L.oracle_mixed_update.argtypes = [i32, i32, i32, i32, i64, P, P, i32, i32, i32, P, P, P,
-                                          i32, P, P, P, f32, f32]
+        L.oracle_mixed_update.argtypes = [i32, i32, i32, i32, i32, i32, i64, P, P, i32, i32, i32,
+                                          P, P, P, i32, P, P, P, f32, f32]
         L.oracle_decode_mixed.restype = i32
-        L.oracle_decode_mixed.argtypes = [i32, i32, i32, i32, i64, P, P, i32, i32, P, i32, i32, P,
-                                          i32, P, P, P, f64, P, i32, P]
+        L.oracle_decode_mixed.argtypes = [i32, i32, i32, i32, i32, i64, P, P, i32, i32, P, i32,
+                                          i32, P, i32, P, P, P, f64, P, i32, P]
         L.oracle_num_threads.restype = i32
         _lib = L
     return _lib
@@ -100,6 +111,14 @@ def _ptr(a: np.ndarray):
 
 def _c(a, dtype):
     return np.ascontiguousarray(a, dtype=dtype)
+
+
+def _rot(R):
+    """fp32 rotation matrix pointer, or NULL (identity) for None."""
+    if R is None:
+        return None, None
+    a = _c(R, np.float32)
+    return a, _ptr(a)
 
 
 def num_threads() -> int:
@@ -118,32 +137,48 @@ def f16_bits_to_f32(h: int) -> float:
     return float(lib().oracle_f16_to_f32(int(h)))
 
 
-def rotate_row(x: np.ndarray, R: np.ndarray) -> np.ndarray:
-    """x~ = x R (fp64 accumulation, one rounding to fp32)."""
+def f32_to_bf16_bits(x: float) -> int:
+    return int(lib().oracle_f32_to_bf16_rne(float(x)))
+
+
+def bf16_bits_to_f32(h: int) -> float:
+    return float(lib().oracle_bf16_to_f32(int(h)))
+
+
+def token_quantile(xt: np.ndarray, rho: float) -> float:
+    """The per-token clip threshold: rho-quantile of |x~| over the row (linear
+    interpolation of order statistics, fp32 steps)."""
+    xt = _c(xt, np.float32)
+    return float(lib().oracle_token_quantile(_ptr(xt), xt.shape[0], float(rho)))
+
+
+def rotate_row(x: np.ndarray, R) -> np.ndarray:
+    """x~ = x R (fp64 accumulation, one rounding to fp32); R None = identity."""
     x = _c(x, np.float32)
-    R = _c(R, np.float32)
+    Ra, Rp = _rot(R)
     d = x.shape[0]
     out = np.empty(d, np.float32)
-    lib().oracle_rotate_row(_ptr(x), _ptr(R), d, _ptr(out))
+    lib().oracle_rotate_row(_ptr(x), Rp, d, _ptr(out))
     return out
 
 
-def quantize_row(xt: np.ndarray, G: int, rho: float):
+def quantize_row(xt: np.ndarray, G: int, rho: float, *, meta: int = 0, clip: int = 0):
     """Clip + asymmetric INT2 of one rotated row -> (codes[d], s16[d/G], z16[d/G], n_sat)."""
     xt = _c(xt, np.float32)
     d = xt.shape[0]
     codes = np.zeros(d, np.uint8)
     s16 = np.zeros(d // G, np.uint16)
     z16 = np.zeros(d // G, np.uint16)
-    sat = lib().oracle_quantize_row(_ptr(xt), d, G, float(rho), _ptr(codes), _ptr(s16), _ptr(z16))
+    sat = lib().oracle_quantize_row(_ptr(xt), d, G, float(rho), int(meta), int(clip),
+                                    _ptr(codes), _ptr(s16), _ptr(z16))
     return codes, s16, z16, int(sat)
 
 
 def kv_append(pages: np.ndarray, *, d: int, Hkv: int, P: int, G: int, k: np.ndarray,
-              v: np.ndarray, slot_mapping: np.ndarray, Rk: np.ndarray, Rv: np.ndarray,
-              clip_k: float, clip_v: float) -> int:
+              v: np.ndarray, slot_mapping: np.ndarray, Rk, Rv, clip_k: float, clip_v: float,
+              meta: int = 0, clip: int = 0) -> int:
     """Quantize rows into ``pages`` (uint8, modified in place).  Returns the
-    number of saturated fp16 stores."""
+    number of saturated metadata stores."""
     assert pages.dtype == np.uint8 and pages.flags["C_CONTIGUOUS"]
     k = _c(k, np.uint16)
     v = _c(v, np.uint16)
@@ -151,9 +186,11 @@ def kv_append(pages: np.ndarray, *, d: int, Hkv: int, P: int, G: int, k: np.ndar
     n_tok = slots.shape[0]
     assert k.size == n_tok * Hkv * d and v.size == n_tok * Hkv * d
     num_pages = pages.size // (Hkv * page_head_bytes(d, P, G))
-    rc = lib().oracle_kv_append(d, Hkv, P, G, num_pages, _ptr(pages), _ptr(k), _ptr(v),
-                                _ptr(slots), n_tok, _ptr(_c(Rk, np.float32)),
-                                _ptr(_c(Rv, np.float32)), float(clip_k), float(clip_v))
+    Rka, Rkp = _rot(Rk)
+    Rva, Rvp = _rot(Rv)
+    rc = lib().oracle_kv_append(d, Hkv, P, G, int(meta), int(clip), num_pages, _ptr(pages),
+                                _ptr(k), _ptr(v), _ptr(slots), n_tok, Rkp, Rvp, float(clip_k),
+                                float(clip_v))
     if rc < 0:
         raise ValueError("oracle kv_append: slot outside the page pool")
     return int(rc)
@@ -170,8 +207,8 @@ def read_token(pages: np.ndarray, *, d: int, Hkv: int, P: int, G: int, page: int
 
 
 def decode(pages: np.ndarray, *, d: int, Hkv: int, P: int, G: int, q: np.ndarray,
-           block_table: np.ndarray, seq_lens: np.ndarray, Rk: np.ndarray, Rv: np.ndarray,
-           sm_scale: float, pairs=None) -> np.ndarray:
+           block_table: np.ndarray, seq_lens: np.ndarray, Rk, Rv, sm_scale: float, pairs=None,
+           meta: int = 0) -> np.ndarray:
     """fp64 decode attention.  q: bf16 bits [B, Hq, d].  Returns [B, Hq, d], or
     [n_pairs, d] when ``pairs`` (an [n, 2] array of (b, h)) is given."""
     q = _c(q, np.uint16)
@@ -186,26 +223,30 @@ def decode(pages: np.ndarray, *, d: int, Hkv: int, P: int, G: int, q: np.ndarray
         pr = _c(pairs, np.int32).reshape(-1, 2)
         out = np.zeros((pr.shape[0], d), np.float64)
         pp, n = _ptr(pr), pr.shape[0]
-    rc = lib().oracle_decode(d, Hkv, P, G, num_pages, _ptr(pages), _ptr(q), B, Hq, _ptr(bt),
-                             bt.shape[1], _ptr(sl), _ptr(_c(Rk, np.float32)),
-                             _ptr(_c(Rv, np.float32)), float(sm_scale), pp, n, _ptr(out))
+    Rka, Rkp = _rot(Rk)
+    Rva, Rvp = _rot(Rv)
+    rc = lib().oracle_decode(d, Hkv, P, G, int(meta), num_pages, _ptr(pages), _ptr(q), B, Hq,
+                             _ptr(bt), bt.shape[1], _ptr(sl), Rkp, Rvp, float(sm_scale), pp, n,
+                             _ptr(out))
     if rc:
         raise ValueError("oracle decode: bad page id, length or head")
     return out
 
 
 def decode_brute(pages: np.ndarray, *, d: int, Hkv: int, P: int, G: int, q: np.ndarray,
-                 block_table: np.ndarray, seq_lens: np.ndarray, Rk: np.ndarray,
-                 Rv: np.ndarray, sm_scale: float) -> np.ndarray:
+                 block_table: np.ndarray, seq_lens: np.ndarray, Rk, Rv, sm_scale: float,
+                 meta: int = 0) -> np.ndarray:
     q = _c(q, np.uint16)
     B, Hq = q.shape[0], q.shape[1]
     bt = _c(block_table, np.int32)
     sl = _c(seq_lens, np.int32)
     num_pages = pages.size // (Hkv * page_head_bytes(d, P, G))
     out = np.zeros((B, Hq, d), np.float64)
-    rc = lib().oracle_decode_brute(d, Hkv, P, G, num_pages, _ptr(pages), _ptr(q), B, Hq,
-                                   _ptr(bt), bt.shape[1], _ptr(sl), _ptr(_c(Rk, np.float32)),
-                                   _ptr(_c(Rv, np.float32)), float(sm_scale), _ptr(out))
+    Rka, Rkp = _rot(Rk)
+    Rva, Rvp = _rot(Rv)
+    rc = lib().oracle_decode_brute(d, Hkv, P, G, int(meta), num_pages, _ptr(pages), _ptr(q), B,
+                                   Hq, _ptr(bt), bt.shape[1], _ptr(sl), Rkp, Rvp, float(sm_scale),
+                                   _ptr(out))
     if rc:
         raise ValueError("oracle decode_brute: bad page id or length")
     return out
@@ -264,8 +305,8 @@ def seg_write(seg: np.ndarray, *, d: int, Hkv: int, B: int, S0: int, W: int, k: 
 
 def mixed_update(pages: np.ndarray, seg: np.ndarray, *, d: int, Hkv: int, P: int, G: int,
                  S0: int, W: int, k_new: np.ndarray, v_new: np.ndarray, block_table: np.ndarray,
-                 seq_lens: np.ndarray, Rk: np.ndarray, Rv: np.ndarray, clip_k: float,
-                 clip_v: float) -> int:
+                 seq_lens: np.ndarray, Rk, Rv, clip_k: float, clip_v: float, meta: int = 0,
+                 clip: int = 0) -> int:
     """One new token per sequence at position seq_lens[b] - 1 (k_new, v_new:
     [B, Hkv, d] bf16 bits): sink, window with demotion of the oldest window token
     into INT2, or INT2 directly when W = 0.  ``pages`` and ``seg`` change in place."""
@@ -273,10 +314,12 @@ def mixed_update(pages: np.ndarray, seg: np.ndarray, *, d: int, Hkv: int, P: int
     sl = _c(seq_lens, np.int32)
     B = sl.shape[0]
     num_pages = pages.size // (Hkv * page_head_bytes(d, P, G))
-    rc = lib().oracle_mixed_update(d, Hkv, P, G, num_pages, _ptr(pages), _ptr(seg), S0, W, B,
-                                   _ptr(_c(k_new, np.uint16)), _ptr(_c(v_new, np.uint16)),
-                                   _ptr(bt), bt.shape[1], _ptr(sl), _ptr(_c(Rk, np.float32)),
-                                   _ptr(_c(Rv, np.float32)), float(clip_k), float(clip_v))
+    Rka, Rkp = _rot(Rk)
+    Rva, Rvp = _rot(Rv)
+    rc = lib().oracle_mixed_update(d, Hkv, P, G, int(meta), int(clip), num_pages, _ptr(pages),
+                                   _ptr(seg), S0, W, B, _ptr(_c(k_new, np.uint16)),
+                                   _ptr(_c(v_new, np.uint16)), _ptr(bt), bt.shape[1], _ptr(sl),
+                                   Rkp, Rvp, float(clip_k), float(clip_v))
     if rc < 0:
         raise ValueError("oracle mixed_update: bad length or page")
     return int(rc)
@@ -284,7 +327,7 @@ def mixed_update(pages: np.ndarray, seg: np.ndarray, *, d: int, Hkv: int, P: int
 
 def decode_mixed(pages: np.ndarray, seg: np.ndarray, *, d: int, Hkv: int, P: int, G: int,
                  S0: int, W: int, q: np.ndarray, block_table: np.ndarray, seq_lens: np.ndarray,
-                 Rk: np.ndarray, Rv: np.ndarray, sm_scale: float, pairs=None) -> np.ndarray:
+                 Rk, Rv, sm_scale: float, pairs=None, meta: int = 0) -> np.ndarray:
     """fp64 decode attention over bf16 sink + INT2 history + bf16 window."""
     q = _c(q, np.uint16)
     B, Hq = q.shape[0], q.shape[1]
@@ -298,10 +341,12 @@ def decode_mixed(pages: np.ndarray, seg: np.ndarray, *, d: int, Hkv: int, P: int
         pr = _c(pairs, np.int32).reshape(-1, 2)
         out = np.zeros((pr.shape[0], d), np.float64)
         pp, n = _ptr(pr), pr.shape[0]
-    rc = lib().oracle_decode_mixed(d, Hkv, P, G, num_pages, _ptr(pages), _ptr(_c(seg, np.uint16)),
-                                   S0, W, _ptr(q), B, Hq, _ptr(bt), bt.shape[1], _ptr(sl),
-                                   _ptr(_c(Rk, np.float32)), _ptr(_c(Rv, np.float32)),
-                                   float(sm_scale), pp, n, _ptr(out))
+    Rka, Rkp = _rot(Rk)
+    Rva, Rvp = _rot(Rv)
+    rc = lib().oracle_decode_mixed(d, Hkv, P, G, int(meta), num_pages, _ptr(pages),
+                                   _ptr(_c(seg, np.uint16)), S0, W, _ptr(q), B, Hq, _ptr(bt),
+                                   bt.shape[1], _ptr(sl), Rkp, Rvp, float(sm_scale), pp, n,
+                                   _ptr(out))
     if rc:
         raise ValueError("oracle decode_mixed: bad page id, length or head")
     return out

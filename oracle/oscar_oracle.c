@@ -14,7 +14,11 @@
  *   - plain fp64 attention over a bf16 paged cache (the bf16 baseline);
  *   - the mixed-precision cache of Sec. 4 "KV Cache Layout": bf16 sink and
  *     recent window around the INT2 history, the per-step demotion of the
- *     oldest window token (Alg. 1 DecodeStep) and decode attention over it.
+ *     oldest window token (Alg. 1 DecodeStep) and decode attention over it;
+ *   - quantizer variants: the per-token quantile clip of App. "Scale
+ *     Determination and Per-token Clipping Details", bfloat16 scale/zero
+ *     metadata, any group size dividing d, and an identity rotation (a NULL
+ *     matrix: R_V absorbed into the projection weights, Sec. 4 "KV Cache Update").
  *
  * Only the test suite, the package smoke check and the benchmark's CPU-baseline
  * leg may load this library.  It shares no code, header or table with the GPU
@@ -91,12 +95,57 @@ uint16_t oracle_f32_to_f16_rne(float f) {
   return (uint16_t)(sign | (uint16_t)(ebias << 10) | man);
 }
 
+/* binary32 -> bfloat16, round to nearest, ties to even: bfloat16 keeps the
+ * binary32 exponent range and 8 significant bits, so the grid quantum at
+ * magnitude a is 2^(floor(log2 a) - 7) for normal a and 2^-133 below 2^-126.
+ * Values that round beyond the largest finite bfloat16 become infinity. */
+uint16_t oracle_f32_to_bf16_rne(float f) {
+  uint32_t u = bits_from_f32(f);
+  uint16_t sign = (uint16_t)((u >> 16) & 0x8000u);
+  double a = fabs((double)f);
+  if (isnan(f)) return (uint16_t)(sign | 0x7fc0u);
+  if (isinf(f)) return (uint16_t)(sign | 0x7f80u);
+  if (a == 0.0) return sign;
+  int e;
+  frexp(a, &e);                                /* a = m * 2^e, m in [0.5,1) */
+  int q_exp = (a < ldexp(1.0, -126)) ? -133 : (e - 1) - 7;
+  double q = ldexp(1.0, q_exp);
+  double n = a / q;                            /* exact */
+  double fl = floor(n);
+  double r = n - fl;
+  double k = fl;
+  if (r > 0.5 || (r == 0.5 && fmod(fl, 2.0) != 0.0)) k = fl + 1.0;
+  double res = k * q;                          /* exact in double */
+  double maxf = ldexp(255.0, 127 - 7);         /* (2 - 2^-7) * 2^127 */
+  if (res > maxf) return (uint16_t)(sign | 0x7f80u);
+  if (res == 0.0) return sign;
+  /* res is on the bfloat16 grid, hence exactly a binary32 value whose low 16
+   * bits are zero. */
+  return (uint16_t)(sign | (uint16_t)(bits_from_f32((float)res) >> 16));
+}
+
 /* Saturating binary16 conversion used for stored scale and zero: finite values
  * beyond +-65504 are clamped to +-65504 first, then rounded. */
 static uint16_t f16_sat(float f) {
   if (f > 65504.0f) f = 65504.0f;
   if (f < -65504.0f) f = -65504.0f;
   return oracle_f32_to_f16_rne(f);
+}
+
+/* Saturating bfloat16 conversion for stored scale and zero (a finite value
+ * that would round to infinity is stored as the largest finite bfloat16). */
+static uint16_t bf16_sat(float f) {
+  uint16_t h = oracle_f32_to_bf16_rne(f);
+  if ((h & 0x7fffu) == 0x7f80u) h = (uint16_t)((h & 0x8000u) | 0x7f7fu);
+  return h;
+}
+
+/* Stored metadata formats: 0 = binary16, 1 = bfloat16. */
+static uint16_t meta_store(int meta, float f) { return meta ? bf16_sat(f) : f16_sat(f); }
+static float meta_load(int meta, uint16_t h) { return meta ? oracle_bf16_to_f32(h) : oracle_f16_to_f32(h); }
+static int meta_saturates(int meta, float f) {
+  if (!meta) return fabsf(f) > 65504.0f;
+  return (oracle_f32_to_bf16_rne(f) & 0x7fffu) == 0x7f80u;
 }
 
 /* ------------------------------------------------------------------------- */
@@ -111,14 +160,14 @@ static uint16_t f16_sat(float f) {
  *   [K s,z]    (d/G)*P entries of 4 bytes, group-major: entry g*P + t
  *   [V s,z]    same
  * A code byte holds channels 4j..4j+3 of one token, channel c in bits 2*(c%4)
- * (least significant first).  An s,z entry is two little-endian binary16
- * values: scale, then zero.
+ * (least significant first).  An s,z entry is two little-endian 16-bit values
+ * (binary16 or bfloat16 by the metadata format): scale, then zero.
  */
 size_t oracle_page_head_bytes(int d, int P, int G) {
   return (size_t)2 * P * (d / 4) + (size_t)2 * (d / G) * P * 4;
 }
 
-typedef struct { int d, Hkv, P, G; } geo_t;
+typedef struct { int d, Hkv, P, G, meta; } geo_t;
 
 static size_t kcode_off(geo_t g, int t, int c) { return (size_t)t * (g.d / 4) + (size_t)(c / 4); }
 static size_t vcode_off(geo_t g, int t, int c) {
@@ -159,8 +208,12 @@ static void get_sz(geo_t g, const uint8_t *blk, int is_v, int grp, int t, uint16
 /* Rotation x~ = x R in row-vector convention (Sec. 2; App. scale determination):
  * x~_j = sum_c x_c R[c][j].  Products of a bf16-exact input and an fp32 matrix
  * entry are exact in fp64; they are summed in fp64 in ascending c and the sum is
- * rounded once to fp32. */
+ * rounded once to fp32.  R == NULL is the identity (x~ = x). */
 void oracle_rotate_row(const float *x, const float *R, int d, float *out) {
+  if (!R) {
+    for (int j = 0; j < d; ++j) out[j] = x[j];
+    return;
+  }
   for (int j = 0; j < d; ++j) {
     double acc = 0.0;
     for (int c = 0; c < d; ++c) acc = acc + (double)x[c] * (double)R[(size_t)c * d + j];
@@ -168,23 +221,63 @@ void oracle_rotate_row(const float *x, const float *R, int d, float *out) {
   }
 }
 
+/* Token-wise percentile clip threshold (App. "Scale Determination and Per-token
+ * Clipping Details"): tau = quantile_rho of {|x~_c|, c < d}, read as the linear
+ * interpolation between order statistics at position rho (d - 1) of the sorted
+ * values a_0 <= ... <= a_{d-1}, in fp32 operations:
+ *   pos = rho * (d - 1), k = floor(pos), f = pos - k,
+ *   tau = a_k + f * (a_{k+1} - a_k)   (tau = a_k when k = d - 1). */
+float oracle_token_quantile(const float *xt, int d, float rho) {
+  float *a = (float *)malloc(sizeof(float) * (size_t)d);
+  for (int c = 0; c < d; ++c) a[c] = fabsf(xt[c]);
+  for (int i = 1; i < d; ++i) {                   /* insertion sort, ascending */
+    float v = a[i];
+    int j = i - 1;
+    while (j >= 0 && a[j] > v) { a[j + 1] = a[j]; --j; }
+    a[j + 1] = v;
+  }
+  float pos = rho * (float)(d - 1);
+  int k = (int)floorf(pos);
+  if (k > d - 1) k = d - 1;
+  float tau;
+  if (k >= d - 1) {
+    tau = a[d - 1];
+  } else {
+    float f = pos - (float)k;
+    float diff = a[k + 1] - a[k];
+    float prod = f * diff;
+    tau = a[k] + prod;
+  }
+  free(a);
+  return tau;
+}
+
 /* Clip and quantize one rotated row (App. scale determination, per token and
  * per group of G channels):
- *   tau = rho * max|x~| over the group, y = clip(x~, -tau, tau)
- *   a = min y, b = max y, s = (b - a)/3, z = -a/s
+ *   clip = 0: tau = rho * max|x~| over the group;
+ *   clip = 1: tau = the token's rho-quantile of |x~| over all d channels
+ *             (oracle_token_quantile), the same for every group;
+ *   y = clip(x~, -tau, tau), a = min y, b = max y, s = (b - a)/3, z = -a/s,
  *   code = clip(round(y/s + z), 0, 3)
- * s and z are stored as binary16 and the codes are computed with the stored
- * values, so that dequantizing a code and quantizing it again returns it.
- * A group whose stored scale would be zero gets s = 1, z = -a, codes 0.
- * A zero point of zero is stored as +0.  Returns the number of saturated binary16 stores. */
-int oracle_quantize_row(const float *xt, int d, int G, float rho,
+ * s and z are stored in the metadata format (meta 0: binary16, 1: bfloat16) and
+ * the codes are computed with the stored values, so that dequantizing a code and
+ * quantizing it again returns it.  A group whose stored scale would be zero gets
+ * s = 1, z = -a, codes 0.  A zero point of zero is stored as +0.  Returns the
+ * number of saturated metadata stores. */
+int oracle_quantize_row(const float *xt, int d, int G, float rho, int meta, int clip,
                         uint8_t *codes, uint16_t *s_out, uint16_t *z_out) {
   int sat = 0;
+  const float tau_tok = clip ? oracle_token_quantile(xt, d, rho) : 0.0f;
   for (int grp = 0; grp < d / G; ++grp) {
     const float *x = xt + grp * G;
-    float m = 0.0f;
-    for (int c = 0; c < G; ++c) { float ax = fabsf(x[c]); if (ax > m) m = ax; }
-    float tau = rho * m;
+    float tau;
+    if (clip) {
+      tau = tau_tok;
+    } else {
+      float m = 0.0f;
+      for (int c = 0; c < G; ++c) { float ax = fabsf(x[c]); if (ax > m) m = ax; }
+      tau = rho * m;
+    }
     float a = 0.0f, b = 0.0f;
     for (int c = 0; c < G; ++c) {
       float y = fminf(fmaxf(x[c], -tau), tau);
@@ -192,22 +285,22 @@ int oracle_quantize_row(const float *xt, int d, int G, float rho,
       if (c == 0 || y > b) b = y;
     }
     float s = (b - a) / 3.0f;
-    if (fabsf(s) > 65504.0f) ++sat;
-    uint16_t s16 = f16_sat(s);
+    sat += meta_saturates(meta, s);
+    uint16_t s16 = meta_store(meta, s);
     uint16_t z16;
     if ((s16 & 0x7fffu) == 0) {
-      s16 = 0x3c00u;                                  /* 1.0 */
+      s16 = meta ? 0x3f80u : 0x3c00u;                 /* 1.0 */
       float na = -a + 0.0f;                           /* +0, never -0 */
-      if (fabsf(na) > 65504.0f) ++sat;
-      z16 = f16_sat(na);
+      sat += meta_saturates(meta, na);
+      z16 = meta_store(meta, na);
       for (int c = 0; c < G; ++c) codes[grp * G + c] = 0;
     } else {
-      float sf = oracle_f16_to_f32(s16);
+      float sf = meta_load(meta, s16);
       float z = -a / sf;
       z = z + 0.0f;                                   /* +0, never -0 */
-      if (fabsf(z) > 65504.0f) ++sat;
-      z16 = f16_sat(z);
-      float zf = oracle_f16_to_f32(z16);
+      sat += meta_saturates(meta, z);
+      z16 = meta_store(meta, z);
+      float zf = meta_load(meta, z16);
       for (int c = 0; c < G; ++c) {
         float y = fminf(fmaxf(x[c], -tau), tau);
         float u = y / sf;
@@ -226,12 +319,14 @@ int oracle_quantize_row(const float *xt, int d, int G, float rho,
 
 /* Quantize n_tok new rows into the paged cache (Alg. 1 QuantizeAndWrite; the
  * fused cache-write of Sec. 4).  k, v: bf16 [n_tok, Hkv, d]; slot_mapping[i] =
- * page*P + offset.  Rk, Rv: fp32 [d, d] row-major.  Returns the number of
- * saturated binary16 stores, or -1 on a slot outside the pool. */
-int64_t oracle_kv_append(int d, int Hkv, int P, int G, int64_t num_pages, uint8_t *pages,
-                         const uint16_t *k, const uint16_t *v, const int64_t *slot_mapping,
-                         int n_tok, const float *Rk, const float *Rv, float clip_k, float clip_v) {
-  geo_t g = {d, Hkv, P, G};
+ * page*P + offset.  Rk, Rv: fp32 [d, d] row-major, or NULL for the identity.
+ * meta, clip: metadata format and clip rule of oracle_quantize_row.  Returns the
+ * number of saturated metadata stores, or -1 on a slot outside the pool. */
+int64_t oracle_kv_append(int d, int Hkv, int P, int G, int meta, int clip, int64_t num_pages,
+                         uint8_t *pages, const uint16_t *k, const uint16_t *v,
+                         const int64_t *slot_mapping, int n_tok, const float *Rk,
+                         const float *Rv, float clip_k, float clip_v) {
+  geo_t g = {d, Hkv, P, G, meta};
   int64_t sat = 0, bad = 0;
 #pragma omp parallel for reduction(+ : sat, bad) schedule(static)
   for (int i = 0; i < n_tok; ++i) {
@@ -250,7 +345,7 @@ int64_t oracle_kv_append(int d, int Hkv, int P, int G, int64_t num_pages, uint8_
         const uint16_t *src = (is_v ? v : k) + ((size_t)i * Hkv + (size_t)h) * d;
         for (int c = 0; c < d; ++c) x[c] = oracle_bf16_to_f32(src[c]);
         oracle_rotate_row(x, is_v ? Rv : Rk, d, xt);
-        sat += oracle_quantize_row(xt, d, G, is_v ? clip_v : clip_k, codes, s16, z16);
+        sat += oracle_quantize_row(xt, d, G, is_v ? clip_v : clip_k, meta, clip, codes, s16, z16);
         for (int c = 0; c < d; ++c) put_code(g, blk, is_v, t, c, codes[c]);
         for (int grp = 0; grp < d / G; ++grp) put_sz(g, blk, is_v, grp, t, s16[grp], z16[grp]);
       }
@@ -263,7 +358,7 @@ int64_t oracle_kv_append(int d, int Hkv, int P, int G, int64_t num_pages, uint8_
 /* Read one token's codes and stored s,z back out of the cache (for tests). */
 void oracle_read_token(int d, int Hkv, int P, int G, const uint8_t *pages, int64_t page, int h,
                        int t, int is_v, uint8_t *codes, uint16_t *s16, uint16_t *z16) {
-  geo_t g = {d, Hkv, P, G};
+  geo_t g = {d, Hkv, P, G, 0};
   const uint8_t *blk = block_ptr(g, (uint8_t *)pages, page, h);
   for (int c = 0; c < d; ++c) codes[c] = (uint8_t)get_code(g, blk, is_v, t, c);
   for (int grp = 0; grp < d / G; ++grp) get_sz(g, blk, is_v, grp, t, &s16[grp], &z16[grp]);
@@ -275,7 +370,7 @@ static void dequant_rotated(geo_t g, const uint8_t *blk, int is_v, int t, double
   for (int grp = 0; grp < g.d / g.G; ++grp) {
     uint16_t s16, z16;
     get_sz(g, blk, is_v, grp, t, &s16, &z16);
-    double s = (double)oracle_f16_to_f32(s16), z = (double)oracle_f16_to_f32(z16);
+    double s = (double)meta_load(g.meta, s16), z = (double)meta_load(g.meta, z16);
     for (int c = grp * g.G; c < (grp + 1) * g.G; ++c)
       out[c] = s * ((double)get_code(g, blk, is_v, t, c) - z);
   }
@@ -311,7 +406,9 @@ static int decode_pair(geo_t g, const uint8_t *pages, int64_t num_pages, const u
   const uint16_t *qr = q + ((size_t)b * Hq + (size_t)h) * d;
   for (int j = 0; j < d; ++j) {
     double acc = 0.0;
-    for (int c = 0; c < d; ++c) acc += (double)oracle_bf16_to_f32(qr[c]) * (double)Rk[(size_t)c * d + j];
+    if (!Rk) acc = (double)oracle_bf16_to_f32(qr[j]);     /* identity rotation */
+    else
+      for (int c = 0; c < d; ++c) acc += (double)oracle_bf16_to_f32(qr[c]) * (double)Rk[(size_t)c * d + j];
     qt[j] = acc;
   }
   double m = -INFINITY;
@@ -332,10 +429,12 @@ static int decode_pair(geo_t g, const uint8_t *pages, int64_t num_pages, const u
     dequant_rotated(g, block_ptr(g, (uint8_t *)pages, page, kvh), 1, t % g.P, row);
     for (int c = 0; c < d; ++c) ot[c] += p * row[c];
   }
-  /* o = (ot / l) Rv^T, i.e. o_j = sum_c ot_c Rv[j][c] / l */
+  /* o = (ot / l) Rv^T, i.e. o_j = sum_c ot_c Rv[j][c] / l (Rv NULL: identity) */
   for (int j = 0; j < d; ++j) {
     double acc = 0.0;
-    for (int c = 0; c < d; ++c) acc += ot[c] * (double)Rv[(size_t)j * d + c];
+    if (!Rv) acc = ot[j];
+    else
+      for (int c = 0; c < d; ++c) acc += ot[c] * (double)Rv[(size_t)j * d + c];
     o[j] = acc / l;
   }
 done:
@@ -343,11 +442,12 @@ done:
   return rc;
 }
 
-int oracle_decode(int d, int Hkv, int P, int G, int64_t num_pages, const uint8_t *pages,
-                  const uint16_t *q, int B, int Hq, const int32_t *block_table, int max_pages,
-                  const int32_t *seq_lens, const float *Rk, const float *Rv, double sm_scale,
-                  const int32_t *pairs, int n_pairs, double *out) {
-  geo_t g = {d, Hkv, P, G};
+int oracle_decode(int d, int Hkv, int P, int G, int meta, int64_t num_pages,
+                  const uint8_t *pages, const uint16_t *q, int B, int Hq,
+                  const int32_t *block_table, int max_pages, const int32_t *seq_lens,
+                  const float *Rk, const float *Rv, double sm_scale, const int32_t *pairs,
+                  int n_pairs, double *out) {
+  geo_t g = {d, Hkv, P, G, meta};
   if (Hq % Hkv) return -1;
   int n = pairs ? n_pairs : B * Hq;
   int bad = 0;
@@ -366,11 +466,11 @@ int oracle_decode(int d, int Hkv, int P, int G, int64_t num_pages, const uint8_t
 /* Brute force in the original basis, following Alg. 1 DecodeStep literally:
  * dequantize the history, rotate it back (k^ = Q(k~) Rk^T, v^ = Q(v~) Rv^T),
  * then o = softmax(sm_scale * q k^T) v^.  O(len * d^2) per pair: tiny inputs. */
-int oracle_decode_brute(int d, int Hkv, int P, int G, int64_t num_pages, const uint8_t *pages,
-                        const uint16_t *q, int B, int Hq, const int32_t *block_table,
-                        int max_pages, const int32_t *seq_lens, const float *Rk,
-                        const float *Rv, double sm_scale, double *out) {
-  geo_t g = {d, Hkv, P, G};
+int oracle_decode_brute(int d, int Hkv, int P, int G, int meta, int64_t num_pages,
+                        const uint8_t *pages, const uint16_t *q, int B, int Hq,
+                        const int32_t *block_table, int max_pages, const int32_t *seq_lens,
+                        const float *Rk, const float *Rv, double sm_scale, double *out) {
+  geo_t g = {d, Hkv, P, G, meta};
   if (Hq % Hkv) return -1;
   int group = Hq / Hkv;
   double *rot = (double *)malloc(sizeof(double) * (size_t)d);
@@ -392,13 +492,17 @@ int oracle_decode_brute(int d, int Hkv, int P, int G, int64_t num_pages, const u
         dequant_rotated(g, blk, 0, t % P, rot);
         for (int j = 0; j < d; ++j) {          /* k^_j = sum_c Q(k~)_c Rk[j][c] */
           double acc = 0.0;
-          for (int c = 0; c < d; ++c) acc += rot[c] * (double)Rk[(size_t)j * d + c];
+          if (!Rk) acc = rot[j];
+          else
+            for (int c = 0; c < d; ++c) acc += rot[c] * (double)Rk[(size_t)j * d + c];
           khat[j] = acc;
         }
         dequant_rotated(g, blk, 1, t % P, rot);
         for (int j = 0; j < d; ++j) {
           double acc = 0.0;
-          for (int c = 0; c < d; ++c) acc += rot[c] * (double)Rv[(size_t)j * d + c];
+          if (!Rv) acc = rot[j];
+          else
+            for (int c = 0; c < d; ++c) acc += rot[c] * (double)Rv[(size_t)j * d + c];
           vhat[(size_t)t * d + j] = acc;
         }
         double s = 0.0;
@@ -553,7 +657,8 @@ int oracle_seg_write(int d, int Hkv, int S0, int W, int B, uint16_t *seg, const 
  *                      (QuantizeAndWrite) before its slot is reused.
  * Quantization is the cache update above (rotation from the bf16 row).
  * Returns the number of saturated fp16 stores, or -1 on a bad length / page. */
-int64_t oracle_mixed_update(int d, int Hkv, int P, int G, int64_t num_pages, uint8_t *pages,
+int64_t oracle_mixed_update(int d, int Hkv, int P, int G, int meta, int clip, int64_t num_pages,
+                            uint8_t *pages,
                             uint16_t *seg, int S0, int W, int B, const uint16_t *k_new,
                             const uint16_t *v_new, const int32_t *block_table, int max_pages,
                             const int32_t *seq_lens, const float *Rk, const float *Rv,
@@ -582,7 +687,7 @@ int64_t oracle_mixed_update(int d, int Hkv, int P, int G, int64_t num_pages, uin
     if (quant_pos >= 0) {
       int32_t page = block_table[(size_t)b * max_pages + quant_pos / P];
       int64_t slot = (int64_t)page * P + quant_pos % P;
-      int64_t r = oracle_kv_append(d, Hkv, P, G, num_pages, pages, qk, qv, &slot, 1, Rk, Rv,
+      int64_t r = oracle_kv_append(d, Hkv, P, G, meta, clip, num_pages, pages, qk, qv, &slot, 1, Rk, Rv,
                                    clip_k, clip_v);
       if (r < 0) { rc = -1; break; }
       sat += r;
@@ -602,12 +707,13 @@ int64_t oracle_mixed_update(int d, int Hkv, int P, int G, int64_t num_pages, uin
  * rotated basis as in oracle_decode; the bf16 parts in the original basis:
  *   o = ( [sum_hist p_t Q(v~_t)] Rv^T + sum_bf16 p_t v_t ) / sum_t p_t.
  * Output layout as oracle_decode.  Returns 0 or -1. */
-int oracle_decode_mixed(int d, int Hkv, int P, int G, int64_t num_pages, const uint8_t *pages,
+int oracle_decode_mixed(int d, int Hkv, int P, int G, int meta, int64_t num_pages,
+                        const uint8_t *pages,
                         const uint16_t *seg, int S0, int W, const uint16_t *q, int B, int Hq,
                         const int32_t *block_table, int max_pages, const int32_t *seq_lens,
                         const float *Rk, const float *Rv, double sm_scale, const int32_t *pairs,
                         int n_pairs, double *out) {
-  geo_t g = {d, Hkv, P, G};
+  geo_t g = {d, Hkv, P, G, meta};
   if (Hq % Hkv || S0 < 0 || W < 0) return -1;
   int group = Hq / Hkv;
   int n = pairs ? n_pairs : B * Hq;
@@ -631,7 +737,9 @@ int oracle_decode_mixed(int d, int Hkv, int P, int G, int64_t num_pages, const u
     for (int c = 0; c < d; ++c) qd[c] = (double)oracle_bf16_to_f32(qr[c]);
     for (int j = 0; j < d; ++j) {
       double acc = 0.0;
-      for (int c = 0; c < d; ++c) acc += qd[c] * (double)Rk[(size_t)c * d + j];
+      if (!Rk) acc = qd[j];
+      else
+        for (int c = 0; c < d; ++c) acc += qd[c] * (double)Rk[(size_t)c * d + j];
       qt[j] = acc;
     }
     double m = -INFINITY;
@@ -667,7 +775,9 @@ int oracle_decode_mixed(int d, int Hkv, int P, int G, int64_t num_pages, const u
       double *o = out + (size_t)i * d;
       for (int j = 0; j < d; ++j) {
         double acc = 0.0;
-        for (int c = 0; c < d; ++c) acc += ot[c] * (double)Rv[(size_t)j * d + c];
+        if (!Rv) acc = ot[j];
+        else
+          for (int c = 0; c < d; ++c) acc += ot[c] * (double)Rv[(size_t)j * d + c];
         o[j] = (acc + op[j]) / l;
       }
     } else {

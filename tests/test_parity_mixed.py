@@ -241,7 +241,8 @@ def test_mixed_many_steps_demote_in_order():
 
 
 def test_mixed_no_history_window_covers_everything():
-    """W larger than every sequence: no INT2 page is read (all splits empty)."""
+    """W larger than every sequence: no INT2 page is read (all splits empty), and the
+    result is the bf16 baseline's."""
     S0, W_ = 64, 1024
     lens = np.array([1, 64, 65, 700, 1088], np.int32)
     cfg = _mixed_cfg("mixed_nohist", lens, seed_index=202)
@@ -254,6 +255,21 @@ def test_mixed_no_history_window_covers_everything():
     err = max_abs(out, m.oracle_decode(ora_pages, ora_seg, lens))
     log("  max|err| = %.3g" % err)
     assert err <= DECODE_TOL
+    # every token bf16: the same attention as the bf16 paged-decode baseline over the
+    # same rows (two fp32 evaluations in different orders)
+    bf_pool = torch.zeros(ok.bf16_pool_bytes(m.lay) // 2, dtype=torch.bfloat16, device="cuda")
+    for b in range(cfg.B):
+        n = int(lens[b])
+        ok.bf16_kv_append(m.lay, bf_pool, m.kv[b][0][:n].cuda(), m.kv[b][1][:n].cuda(),
+                          torch.from_numpy(W.slots_for(m.table, b, np.arange(n))).cuda())
+    ws = ok.alloc_workspace(m.lay, cfg.B, cfg.Hq, 4)
+    bout = torch.empty_like(out)
+    ok.bf16_decode_attn(m.lay, bf_pool, m.q.cuda(), m.table_d, torch.from_numpy(lens).cuda(),
+                        cfg.sm_scale, 4, ws, bout)
+    torch.cuda.synchronize()
+    d = float((out - bout).abs().max())
+    log("  vs bf16 baseline max|diff| = %.3g" % d)
+    assert d <= 1e-4
 
 
 def test_mixed_zero_segments_equal_int2_path_bitwise():
