@@ -27,10 +27,15 @@
  *     (slot_mapping, block_table, seq_lens) are not validated: they must lie in
  *     range (slot < num_pages*page_size, 0 <= page id < num_pages,
  *     1 <= seq_lens[b] <= max_pages_per_seq*page_size).
- *   - Inputs must be finite.  Scales and zeros that fall outside the binary16
- *     range are saturated to +-65504.
+ *   - Inputs must be finite.  Scales and zeros that fall outside the range of
+ *     their storage format are saturated to its largest finite value (+-65504
+ *     for binary16).
+ *   - A rotation matrix argument (R_k, R_v) may be NULL: the identity, e.g.
+ *     R_V absorbed into the value and output projections (Sec. 4 "KV Cache
+ *     Update").  The same choice must be used for the cache update and decode.
  *   - Supported shapes: head_dim 128, page_size 64, group_size 32.  Other values
- *     return OSCAR_ERR_UNSUPPORTED.
+ *     return OSCAR_ERR_UNSUPPORTED; an unknown clip_mode or meta_dtype returns
+ *     OSCAR_ERR_INVALID_ARG.
  *
  * Page byte layout (an ABI: any producer/consumer of the pool must follow it).
  *   A pool of num_pages pages; page p, kv-head h is the block starting at byte
@@ -41,8 +46,9 @@
  *     [K s,z]    (d/G)*P 4-byte entries, group-major: entry (c/G)*P + t
  *     [V s,z]    same, after the K entries
  *   A code byte holds the four channels 4j..4j+3 of one token; channel c sits
- *   in bits 2*(c%4)..2*(c%4)+1.  An s,z entry is the binary16 scale followed by
- *   the binary16 zero point, little-endian.  The stored row is
+ *   in bits 2*(c%4)..2*(c%4)+1.  An s,z entry is the scale followed by the
+ *   zero point, each a little-endian binary16 (meta_dtype F16) or bfloat16
+ *   (BF16).  The stored row is
  *   Q(x~)_c = s * (code_c - z).
  */
 #ifndef OSCAR_H
@@ -65,13 +71,29 @@ typedef enum {
 
 typedef enum { OSCAR_OUT_BF16 = 0, OSCAR_OUT_F32 = 1 } oscar_dtype;
 
-/* Geometry of one layer's page pool.  Host struct, read only. */
+/* Clip threshold of the quantizer (App. "Scale Determination and Per-token
+ * Clipping Details"), with clip = clip_k or clip_v of the call:
+ *   GROUP_ABSMAX   : tau = clip * max|x~| over each group of G channels;
+ *   TOKEN_QUANTILE : tau = the clip-quantile of |x~| over the token's d channels
+ *                    (the same tau for every group): sorted a_0 <= ... <= a_{d-1},
+ *                    pos = clip * (d - 1), k = floor(pos), f = pos - k,
+ *                    tau = a_k + f * (a_{k+1} - a_k) (tau = a_{d-1} if k = d - 1),
+ *                    each step one fp32 operation. */
+typedef enum { OSCAR_CLIP_GROUP_ABSMAX = 0, OSCAR_CLIP_TOKEN_QUANTILE = 1 } oscar_clip_mode;
+
+/* Storage format of the per-group scale and zero point. */
+typedef enum { OSCAR_META_F16 = 0, OSCAR_META_BF16 = 1 } oscar_meta_dtype;
+
+/* Geometry and quantizer format of one layer's page pool.  Host struct, read
+ * only.  Zero-initialized trailing fields give the default format. */
 typedef struct {
   int32_t head_dim;     /* d, channels per head (128)                 */
   int32_t num_kv_heads; /* Hkv >= 1                                   */
   int32_t page_size;    /* P, token slots per page (64)               */
   int32_t group_size;   /* G, channels per quantization group (32)    */
   int64_t num_pages;    /* pages in the pool (>= 1)                   */
+  int32_t clip_mode;    /* oscar_clip_mode (default GROUP_ABSMAX)     */
+  int32_t meta_dtype;   /* oscar_meta_dtype (default F16)             */
 } oscar_layout;
 
 /* Human-readable name of a status code (static storage). */
@@ -91,18 +113,21 @@ int oscar_layout_check(const oscar_layout *L);
  * Determination and Per-token Clipping Details"; Alg. 1 QuantizeAndWrite).
  * For each new token i and kv-head h, and for X in {K, V}:
  *   x~ = x R_X                      rotation, x~_j = sum_c x_c R_X[c][j]
- *                                   (summed in fp64, rounded once to fp32)
+ *                                   (summed in fp64, rounded once to fp32;
+ *                                   R_X NULL: x~ = x)
+ *   tau                             clipping threshold of L->clip_mode with
+ *                                   clip_X (see oscar_clip_mode)
  *   per group g of G channels:
- *     tau = clip_X * max|x~|        clipping threshold
  *     y   = min(max(x~, -tau), tau)
- *     a = min y, b = max y, s = fp16((b - a)/3), z = fp16(-a / s)
+ *     a = min y, b = max y, s = M((b - a)/3), z = M(-a / s)
  *     code = clamp(round_half_even(y / s + z), 0, 3)
- *   (a group with fp16 scale 0 stores s = 1, z = fp16(-a), codes 0; a zero
- *   point of 0 is stored as +0), packed into the slot per the page layout.
+ *   where M rounds to the metadata format (L->meta_dtype, nearest even); a
+ *   group whose stored scale is 0 stores s = 1, z = M(-a), codes 0; a zero
+ *   point of 0 is stored as +0.  Packed into the slot per the page layout.
  *   k_new, v_new : bf16 [n_tok, Hkv, d], row-major
  *   slot_mapping : int64 [n_tok], slot = page_id * P + offset; slots must be
  *                  distinct within one call
- *   R_k, R_v     : fp32 [d, d], row-major, orthogonal
+ *   R_k, R_v     : fp32 [d, d], row-major, orthogonal, or NULL (identity)
  *   clip_k/_v    : ratios in (0, 1]; 1 disables clipping
  * n_tok == 0 launches nothing.  Only the addressed slots are written.
  */

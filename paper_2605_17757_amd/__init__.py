@@ -41,15 +41,22 @@ class OscarError(RuntimeError):
         super().__init__("%s failed: %s" % (where, status_string(status) if _lib else status))
 
 
+CLIP_GROUP_ABSMAX, CLIP_TOKEN_QUANTILE = 0, 1
+META_F16, META_BF16 = 0, 1
+
+
 class Layout(ctypes.Structure):
     """Mirror of ``oscar_layout``."""
     _fields_ = [("head_dim", ctypes.c_int32), ("num_kv_heads", ctypes.c_int32),
                 ("page_size", ctypes.c_int32), ("group_size", ctypes.c_int32),
-                ("num_pages", ctypes.c_int64)]
+                ("num_pages", ctypes.c_int64), ("clip_mode", ctypes.c_int32),
+                ("meta_dtype", ctypes.c_int32)]
 
     def __init__(self, num_kv_heads: int, num_pages: int, head_dim: int = HEAD_DIM,
-                 page_size: int = PAGE_SIZE, group_size: int = GROUP_SIZE):
-        super().__init__(head_dim, num_kv_heads, page_size, group_size, num_pages)
+                 page_size: int = PAGE_SIZE, group_size: int = GROUP_SIZE,
+                 clip_mode: int = CLIP_GROUP_ABSMAX, meta_dtype: int = META_F16):
+        super().__init__(head_dim, num_kv_heads, page_size, group_size, num_pages, clip_mode,
+                         meta_dtype)
 
 
 _lib = None
@@ -138,6 +145,11 @@ def _ptr(t: torch.Tensor, dtype, name: str, numel: int | None = None):
     return ctypes.c_void_p(t.data_ptr())
 
 
+def _rptr(R, name: str, d: int = HEAD_DIM):
+    """A rotation matrix (fp32 [d, d] on the GPU), or None for the identity."""
+    return None if R is None else _ptr(R, torch.float32, name, d * d)
+
+
 # ---------------------------------------------------------------------------
 # sizes and helpers
 # ---------------------------------------------------------------------------
@@ -179,7 +191,8 @@ def alloc_workspace(layout: Layout, B: int, Hq: int, num_splits: int, device="cu
 
 def kv_append(layout: Layout, pages, k_new, v_new, slot_mapping, R_k, R_v, clip_k: float,
               clip_v: float, stream=None) -> None:
-    """Rotate, clip, INT2-quantize and pack n_tok new K/V rows into ``pages``."""
+    """Rotate, clip, INT2-quantize and pack n_tok new K/V rows into ``pages``
+    (R_k / R_v None: identity)."""
     n_tok = int(slot_mapping.numel())
     d, hkv = layout.head_dim, layout.num_kv_heads
     st = lib().oscar_kv_append(
@@ -187,7 +200,7 @@ def kv_append(layout: Layout, pages, k_new, v_new, slot_mapping, R_k, R_v, clip_
         _ptr(k_new, torch.bfloat16, "k_new", n_tok * hkv * d),
         _ptr(v_new, torch.bfloat16, "v_new", n_tok * hkv * d),
         _ptr(slot_mapping, torch.int64, "slot_mapping"), n_tok,
-        _ptr(R_k, torch.float32, "R_k", d * d), _ptr(R_v, torch.float32, "R_v", d * d),
+        _rptr(R_k, "R_k", d), _rptr(R_v, "R_v", d),
         float(clip_k), float(clip_v), _stream(stream))
     _check(st, "oscar_kv_append")
 
@@ -212,8 +225,8 @@ def decode_attn(layout: Layout, pages, q, block_table, seq_lens, R_k, R_v, sm_sc
         ctypes.byref(layout), _ptr(pages, torch.uint8, "pages", pool_bytes(layout)),
         _ptr(q, torch.bfloat16, "q", B * Hq * d), B, Hq,
         _ptr(block_table, torch.int32, "block_table", B * mp), mp,
-        _ptr(seq_lens, torch.int32, "seq_lens", B), _ptr(R_k, torch.float32, "R_k", d * d),
-        _ptr(R_v, torch.float32, "R_v", d * d), float(sm_scale), int(num_splits),
+        _ptr(seq_lens, torch.int32, "seq_lens", B), _rptr(R_k, "R_k", d),
+        _rptr(R_v, "R_v", d), float(sm_scale), int(num_splits),
         _ptr(workspace, torch.uint8, "workspace"), workspace.numel(),
         _ptr(out, out.dtype, "out", B * Hq * d), out_dtype, _stream(stream))
     _check(st, "oscar_decode_attn")
@@ -235,8 +248,8 @@ def decode_step(layout: Layout, pages, k_new, v_new, slot_mapping, clip_k: float
         ctypes.byref(layout), _ptr(pages, torch.uint8, "pages", pool_bytes(layout)), kp, vp, sp,
         n_new, float(clip_k), float(clip_v), _ptr(q, torch.bfloat16, "q", B * Hq * d), B, Hq,
         _ptr(block_table, torch.int32, "block_table", B * mp), mp,
-        _ptr(seq_lens, torch.int32, "seq_lens", B), _ptr(R_k, torch.float32, "R_k", d * d),
-        _ptr(R_v, torch.float32, "R_v", d * d), float(sm_scale), int(num_splits),
+        _ptr(seq_lens, torch.int32, "seq_lens", B), _rptr(R_k, "R_k", d),
+        _rptr(R_v, "R_v", d), float(sm_scale), int(num_splits),
         _ptr(workspace, torch.uint8, "workspace"), workspace.numel(),
         _ptr(out, out.dtype, "out", B * Hq * d), out_dtype, _stream(stream))
     _check(st, "oscar_decode_step")
@@ -247,7 +260,7 @@ def decode_prepare(layout: Layout, q, R_k, sm_scale: float, num_splits: int, wor
     B, Hq, d = int(q.shape[0]), int(q.shape[1]), layout.head_dim
     st = lib().oscar_decode_prepare(
         ctypes.byref(layout), _ptr(q, torch.bfloat16, "q", B * Hq * d), B, Hq,
-        _ptr(R_k, torch.float32, "R_k", d * d), float(sm_scale), int(num_splits),
+        _rptr(R_k, "R_k", d), float(sm_scale), int(num_splits),
         _ptr(workspace, torch.uint8, "workspace"), workspace.numel(), _stream(stream))
     _check(st, "oscar_decode_prepare")
 
@@ -268,7 +281,7 @@ def decode_reduce(layout: Layout, B: int, Hq: int, R_v, num_splits: int, workspa
     d = layout.head_dim
     out_dtype = OUT_F32 if out.dtype == torch.float32 else OUT_BF16
     st = lib().oscar_decode_reduce(
-        ctypes.byref(layout), B, Hq, _ptr(R_v, torch.float32, "R_v", d * d), int(num_splits),
+        ctypes.byref(layout), B, Hq, _rptr(R_v, "R_v", d), int(num_splits),
         _ptr(workspace, torch.uint8, "workspace"), workspace.numel(),
         _ptr(out, out.dtype, "out", B * Hq * d), out_dtype, _stream(stream))
     _check(st, "oscar_decode_reduce")
@@ -318,8 +331,8 @@ def mixed_append(layout: Layout, pages, seg, S0: int, W: int, k, v, seq_idx, pos
         _ptr(k, torch.bfloat16, "k", n_tok * hkv * d), _ptr(v, torch.bfloat16, "v", n_tok * hkv * d),
         _ptr(seq_idx, torch.int32, "seq_idx", n_tok), _ptr(pos, torch.int64, "pos", n_tok), n_tok,
         _ptr(block_table, torch.int32, "block_table", B * mp), mp,
-        _ptr(seq_lens, torch.int32, "seq_lens", B), _ptr(R_k, torch.float32, "R_k", d * d),
-        _ptr(R_v, torch.float32, "R_v", d * d), float(clip_k), float(clip_v), _stream(stream))
+        _ptr(seq_lens, torch.int32, "seq_lens", B), _rptr(R_k, "R_k", d),
+        _rptr(R_v, "R_v", d), float(clip_k), float(clip_v), _stream(stream))
     _check(st, "oscar_mixed_append")
 
 
@@ -334,8 +347,8 @@ def decode_attn_mixed(layout: Layout, pages, seg, S0: int, W: int, q, block_tabl
         _seg_ptr(layout, seg, B, S0, W), int(S0), int(W),
         _ptr(q, torch.bfloat16, "q", B * Hq * d), B, Hq,
         _ptr(block_table, torch.int32, "block_table", B * mp), mp,
-        _ptr(seq_lens, torch.int32, "seq_lens", B), _ptr(R_k, torch.float32, "R_k", d * d),
-        _ptr(R_v, torch.float32, "R_v", d * d), float(sm_scale), int(num_splits),
+        _ptr(seq_lens, torch.int32, "seq_lens", B), _rptr(R_k, "R_k", d),
+        _rptr(R_v, "R_v", d), float(sm_scale), int(num_splits),
         _ptr(workspace, torch.uint8, "workspace"), workspace.numel(),
         _ptr(out, out.dtype, "out", B * Hq * d), out_dtype, _stream(stream))
     _check(st, "oscar_decode_attn_mixed")
@@ -356,8 +369,8 @@ def decode_step_mixed(layout: Layout, pages, seg, S0: int, W: int, k_new, v_new,
         _ptr(v_new, torch.bfloat16, "v_new", B * hkv * d), float(clip_k), float(clip_v),
         _ptr(q, torch.bfloat16, "q", B * Hq * d), B, Hq,
         _ptr(block_table, torch.int32, "block_table", B * mp), mp,
-        _ptr(seq_lens, torch.int32, "seq_lens", B), _ptr(R_k, torch.float32, "R_k", d * d),
-        _ptr(R_v, torch.float32, "R_v", d * d), float(sm_scale), int(num_splits),
+        _ptr(seq_lens, torch.int32, "seq_lens", B), _rptr(R_k, "R_k", d),
+        _rptr(R_v, "R_v", d), float(sm_scale), int(num_splits),
         _ptr(workspace, torch.uint8, "workspace"), workspace.numel(),
         _ptr(out, out.dtype, "out", B * Hq * d), out_dtype, _stream(stream))
     _check(st, "oscar_decode_step_mixed")

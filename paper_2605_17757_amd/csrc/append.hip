@@ -55,29 +55,44 @@ __device__ inline float half_wave_reduce(float x) {
 __device__ inline float half_wave_max(float x) { return half_wave_reduce<true>(x); }
 __device__ inline float half_wave_min(float x) { return half_wave_reduce<false>(x); }
 
+// bfloat16 with saturation to +-(largest finite) (round to nearest even on the
+// binary32 bits; finite inputs).
+__device__ inline uint16_t bf16_sat_bits(float f) {
+  const uint32_t u = __float_as_uint(f);
+  uint16_t h = (uint16_t)((u + 0x7fffu + ((u >> 16) & 1u)) >> 16);
+  if ((h & 0x7fffu) == 0x7f80u) h = (uint16_t)((h & 0x8000u) | 0x7f7fu);
+  return h;
+}
+
+using QFmt = QuantFmt;  // storage format of scale and zero, and the clip rule
+__device__ inline uint16_t meta_store(const QFmt& q, float f) {
+  return q.bf16 ? bf16_sat_bits(f) : f16_sat_bits(f);
+}
+__device__ inline float meta_load(const QFmt& q, uint16_t h) {
+  return q.bf16 ? __uint_as_float((uint32_t)h << 16) : f16_bits_to_f32(h);
+}
+
 struct QOut {
   uint32_t code;
   uint16_t s16, z16;
 };
 
-// Clip and quantize one channel value x of a group spread over a half wave.
-__device__ inline QOut quantize(float x, float clip) {
+// Clip at +-tau and quantize one channel value x of a group spread over a half wave.
+__device__ inline QOut quantize(float x, float tau, const QFmt& fmt) {
   QOut o;
-  const float m = half_wave_max(fabsf(x));
-  const float tau = __fmul_rn(clip, m);
   const float y = fminf(fmaxf(x, -tau), tau);
   const float a = half_wave_min(y);
   const float b = half_wave_max(y);
   const float s = __fdiv_rn(__fsub_rn(b, a), 3.0f);
-  uint16_t s16 = f16_sat_bits(s);
+  uint16_t s16 = meta_store(fmt, s);
   if ((s16 & 0x7fffu) == 0) {
-    o.s16 = 0x3c00u;  // 1.0
-    o.z16 = plus_zero(f16_sat_bits(-a));
+    o.s16 = fmt.bf16 ? 0x3f80u : 0x3c00u;  // 1.0
+    o.z16 = plus_zero(meta_store(fmt, -a));
     o.code = 0;
   } else {
-    const float sf = f16_bits_to_f32(s16);
-    const uint16_t z16 = plus_zero(f16_sat_bits(__fdiv_rn(-a, sf)));
-    const float zf = f16_bits_to_f32(z16);
+    const float sf = meta_load(fmt, s16);
+    const uint16_t z16 = plus_zero(meta_store(fmt, __fdiv_rn(-a, sf)));
+    const float zf = meta_load(fmt, z16);
     float r = rintf(__fadd_rn(__fdiv_rn(y, sf), zf));
     r = fminf(fmaxf(r, 0.0f), 3.0f);
     o.s16 = s16;
@@ -85,6 +100,89 @@ __device__ inline QOut quantize(float x, float clip) {
     o.code = (uint32_t)r;
   }
   return o;
+}
+
+// Token-wise clip threshold (App. "Scale Determination and Per-token Clipping
+// Details"): the rho-quantile of |x~| over the row, a_k + f (a_{k+1} - a_k) with
+// pos = rho (d - 1), k = floor(pos), f = pos - k, in fp32 steps.  The order
+// statistics come from a binary search over the bit patterns of |x~| (positive
+// floats order like their bits): the smallest T with #{|x~| <= T} >= k + 1 is a_k.
+__device__ inline void quantile_pos(float rho, int& k, float& f) {
+  const float pos = __fmul_rn(rho, (float)(kD - 1));
+  k = min((int)floorf(pos), kD - 1);
+  f = __fsub_rn(pos, (float)k);
+}
+__device__ inline float lerp_tau(float ak, float ak1, float f) {
+  return __fadd_rn(ak, __fmul_rn(f, __fsub_rn(ak1, ak)));
+}
+
+// One row over the wave: lane l holds channels l and l + 64.
+__device__ inline float token_quantile_wave(float x0, float x1, float rho) {
+  const uint32_t u0 = __float_as_uint(x0) & 0x7fffffffu, u1 = __float_as_uint(x1) & 0x7fffffffu;
+  int k;
+  float f;
+  quantile_pos(rho, k, f);
+  auto count_le = [&](uint32_t t) {  // wave-uniform
+    return __popcll(__ballot(u0 <= t)) + __popcll(__ballot(u1 <= t));
+  };
+  uint32_t lo = 0, hi = 0x7f800000u;
+  while (lo < hi) {
+    const uint32_t mid = lo + ((hi - lo) >> 1);
+    if (count_le(mid) >= k + 1) hi = mid;
+    else lo = mid + 1;
+  }
+  const float ak = __uint_as_float(lo);
+  if (k >= kD - 1) return ak;
+  float ak1 = ak;
+  if (count_le(lo) < k + 2) {  // a_{k+1} = the smallest value above a_k
+    uint32_t m = min(u0 > lo ? u0 : 0xffffffffu, u1 > lo ? u1 : 0xffffffffu);
+#pragma unroll
+    for (int o = 32; o >= 1; o >>= 1) m = min(m, (uint32_t)__shfl_xor((int)m, o, 64));
+    ak1 = __uint_as_float(m);
+  }
+  return lerp_tau(ak, ak1, f);
+}
+
+// Two rows, one per wave half: lane l' = l & 31 of half h holds channels
+// l' + 32 q of row h.  Both searches run together (31 halvings of the bit range).
+__device__ inline float token_quantile_halves(const float (&x)[4], float rho, int half) {
+  uint32_t u[4];
+#pragma unroll
+  for (int q = 0; q < 4; ++q) u[q] = __float_as_uint(x[q]) & 0x7fffffffu;
+  int k;
+  float f;
+  quantile_pos(rho, k, f);
+  // counts of the two halves for per-half thresholds t0 (half 0) and t1 (half 1)
+  auto counts = [&](uint32_t t0, uint32_t t1, int& c0, int& c1) {
+    const uint32_t t = half ? t1 : t0;
+    c0 = c1 = 0;
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      const uint64_t b = __ballot(u[q] <= t);
+      c0 += __popc((uint32_t)b);
+      c1 += __popc((uint32_t)(b >> 32));
+    }
+  };
+  uint32_t lo0 = 0, hi0 = 0x7f800000u, lo1 = 0, hi1 = 0x7f800000u;
+  for (int it = 0; it < 31; ++it) {
+    const uint32_t m0 = lo0 + ((hi0 - lo0) >> 1), m1 = lo1 + ((hi1 - lo1) >> 1);
+    int c0, c1;
+    counts(m0, m1, c0, c1);
+    if (c0 >= k + 1) hi0 = m0; else lo0 = m0 + 1;
+    if (c1 >= k + 1) hi1 = m1; else lo1 = m1 + 1;
+  }
+  const uint32_t lo = half ? lo1 : lo0;
+  const float ak = __uint_as_float(lo);
+  if (k >= kD - 1) return ak;
+  int c0, c1;
+  counts(lo0, lo1, c0, c1);
+  uint32_t m = 0xffffffffu;
+#pragma unroll
+  for (int q = 0; q < 4; ++q) m = min(m, u[q] > lo ? u[q] : 0xffffffffu);
+#pragma unroll
+  for (int o = 16; o >= 1; o >>= 1) m = min(m, (uint32_t)__shfl_xor((int)m, o, 64));  // within the half
+  const float ak1 = ((half ? c1 : c0) >= k + 2) ? ak : __uint_as_float(m);
+  return lerp_tau(ak, ak1, f);
 }
 
 // OR the 2-bit codes of lanes 4j..4j+3 into the byte of quad j (valid in lane 4j).
@@ -279,11 +377,19 @@ struct StepRows {
 // and l + 64 are in lane l, to pool slot `slot` (wave-uniform; < 0: the row only
 // takes part in the cross-lane steps).
 __device__ inline void store_row(uint8_t* __restrict__ pages, int Hkv, int64_t slot, int row,
-                                 int is_v, float clip, double acc0, double acc1, int l) {
+                                 int is_v, float clip, const QFmt& fmt, double acc0, double acc1,
+                                 int l) {
   const float xt0 = __double2float_rn(acc0);  // channel l
   const float xt1 = __double2float_rn(acc1);  // channel l + 64
-  const QOut q0 = quantize(xt0, clip);
-  const QOut q1 = quantize(xt1, clip);
+  float tau0, tau1;
+  if (fmt.quantile) {
+    tau0 = tau1 = token_quantile_wave(xt0, xt1, clip);
+  } else {
+    tau0 = __fmul_rn(clip, half_wave_max(fabsf(xt0)));
+    tau1 = __fmul_rn(clip, half_wave_max(fabsf(xt1)));
+  }
+  const QOut q0 = quantize(xt0, tau0, fmt);
+  const QOut q1 = quantize(xt1, tau1, fmt);
   const uint32_t byte0 = pack_quad(q0.code, l);  // quad l/4
   const uint32_t byte1 = pack_quad(q1.code, l);  // quad 16 + l/4
   if (slot < 0) return;                          // uniform across the wave
@@ -317,11 +423,12 @@ template <int RW, class Rows>
 __device__ inline void append_body(float* Rs, double (*xs)[RW][kD], int is_v, int bx, int gx,
                                    uint8_t* __restrict__ pages, int Hkv, const Rows& rows,
                                    int n_rows, const float* __restrict__ Rk,
-                                   const float* __restrict__ Rv, float clip_k, float clip_v) {
-  const float* __restrict__ R = is_v ? Rv : Rk;
+                                   const float* __restrict__ Rv, float clip_k, float clip_v,
+                                   const QFmt& fmt) {
+  const float* __restrict__ R = is_v ? Rv : Rk;  // nullptr: identity
   const float clip = is_v ? clip_v : clip_k;
 
-  {  // 16 float4 per thread, all loads issued before the stores
+  if (R) {  // 16 float4 per thread, all loads issued before the stores
     float4 r4[kD * kD / 4 / 256];
 #pragma unroll
     for (int i = 0; i < kD * kD / 4 / 256; ++i)
@@ -353,24 +460,32 @@ __device__ inline void append_body(float* Rs, double (*xs)[RW][kD], int is_v, in
     }
 
     double acc0[RW], acc1[RW];
+    if (R) {
 #pragma unroll
-    for (int rr = 0; rr < RW; ++rr) acc0[rr] = acc1[rr] = 0.0;
+      for (int rr = 0; rr < RW; ++rr) acc0[rr] = acc1[rr] = 0.0;
 #pragma unroll 4
-    for (int c = 0; c < kD; ++c) {
-      const double r0 = (double)Rs[c * kD + l];
-      const double r1 = (double)Rs[c * kD + l + 64];
+      for (int c = 0; c < kD; ++c) {
+        const double r0 = (double)Rs[c * kD + l];
+        const double r1 = (double)Rs[c * kD + l + 64];
+#pragma unroll
+        for (int rr = 0; rr < RW; ++rr) {
+          const double xc = xs[w][rr][c];
+          acc0[rr] = __fma_rn(xc, r0, acc0[rr]);
+          acc1[rr] = __fma_rn(xc, r1, acc1[rr]);
+        }
+      }
+    } else {  // identity: x~ = x
 #pragma unroll
       for (int rr = 0; rr < RW; ++rr) {
-        const double xc = xs[w][rr][c];
-        acc0[rr] = __fma_rn(xc, r0, acc0[rr]);
-        acc1[rr] = __fma_rn(xc, r1, acc1[rr]);
+        acc0[rr] = xs[w][rr][l];
+        acc1[rr] = xs[w][rr][l + 64];
       }
     }
 
 #pragma unroll
     for (int rr = 0; rr < RW; ++rr) {
       const int row = item * RW + rr;
-      store_row(pages, Hkv, rows.slot(row), row, is_v, clip, acc0[rr], acc1[rr], l);
+      store_row(pages, Hkv, rows.slot(row), row, is_v, clip, fmt, acc0[rr], acc1[rr], l);
     }
   }
 }
@@ -380,11 +495,11 @@ __global__ __launch_bounds__(256) void append_kernel(uint8_t* __restrict__ pages
                                                      Rows rows, int n_rows,
                                                      const float* __restrict__ Rk,
                                                      const float* __restrict__ Rv, float clip_k,
-                                                     float clip_v) {
+                                                     float clip_v, QFmt fmt) {
   __shared__ float Rs[kD * kD];
   __shared__ double xs[kWaves][RW][kD];
   append_body<RW>(Rs, xs, blockIdx.y, blockIdx.x, gridDim.x, pages, Hkv, rows, n_rows, Rk, Rv,
-                  clip_k, clip_v);
+                  clip_k, clip_v, fmt);
 }
 
 // ---------------------------------------------------------------------------
@@ -403,13 +518,26 @@ constexpr int kBulkRows = 8;
 // store_row for the pair layout: lane l' of the half holds channels l' + 32 q;
 // slot is uniform across the half wave.
 __device__ inline void store_row4(uint8_t* __restrict__ pages, int Hkv, int64_t slot, int row,
-                                  int is_v, float clip, const double (&acc)[4], int lp) {
+                                  int is_v, float clip, const QFmt& fmt, const double (&acc)[4],
+                                  int lp, int half) {
+  float xt[4];
+#pragma unroll
+  for (int q = 0; q < 4; ++q) xt[q] = __double2float_rn(acc[q]);
+  float tau[4];
+  if (fmt.quantile) {
+    const float t = token_quantile_halves(xt, clip, half);
+#pragma unroll
+    for (int q = 0; q < 4; ++q) tau[q] = t;
+  } else {
+#pragma unroll
+    for (int q = 0; q < 4; ++q) tau[q] = __fmul_rn(clip, half_wave_max(fabsf(xt[q])));
+  }
   QOut qo[4];
   uint32_t byte[4];
 #pragma unroll
   for (int q = 0; q < 4; ++q) {
-    qo[q] = quantize(__double2float_rn(acc[q]), clip);  // group q of the row
-    byte[q] = pack_quad(qo[q].code, lp);                 // quad 8 q + l'/4
+    qo[q] = quantize(xt[q], tau[q], fmt);  // group q of the row
+    byte[q] = pack_quad(qo[q].code, lp);   // quad 8 q + l'/4
   }
   if (slot < 0) return;
   const int h = row % Hkv;
@@ -436,15 +564,15 @@ __device__ inline void store_row4(uint8_t* __restrict__ pages, int Hkv, int64_t 
 template <class Rows>
 __global__ __launch_bounds__(512) void append_bulk_kernel(
     uint8_t* __restrict__ pages, int Hkv, Rows rows, int n_rows, const float* __restrict__ Rk,
-    const float* __restrict__ Rv, float clip_k, float clip_v) {
+    const float* __restrict__ Rv, float clip_k, float clip_v, QFmt fmt) {
   // xs first: its reads use the 16-bit LDS offset field
   __shared__ double2 xs[kBulkWaves][kBulkRows][kD / 2];      // 64 KB
   __shared__ float4 Rq[kD][kD / 4];                          // 64 KB
   const int is_v = blockIdx.y;
-  const float* __restrict__ R = is_v ? Rv : Rk;
+  const float* __restrict__ R = is_v ? Rv : Rk;  // nullptr: identity
   const float clip = is_v ? clip_v : clip_k;
   const int t = threadIdx.x;
-  {  // 8 float4 per thread, loads issued before the stores
+  if (R) {  // 8 float4 per thread, loads issued before the stores
     float4 r4[kD * kD / 4 / 512];
 #pragma unroll
     for (int i = 0; i < kD * kD / 4 / 512; ++i) r4[i] = reinterpret_cast<const float4*>(R)[t + 512 * i];
@@ -476,28 +604,38 @@ __global__ __launch_bounds__(512) void append_bulk_kernel(
       rows.copy(row, is_v, l);
     }
     double acc[kBulkRows / 2][4];
+    if (R) {
 #pragma unroll
-    for (int p = 0; p < kBulkRows / 2; ++p)
+      for (int p = 0; p < kBulkRows / 2; ++p)
 #pragma unroll
-      for (int q = 0; q < 4; ++q) acc[p][q] = 0.0;
+        for (int q = 0; q < 4; ++q) acc[p][q] = 0.0;
 #pragma unroll 2
-    for (int c2 = 0; c2 < kD / 2; ++c2) {
-      const float4 ra = Rq[2 * c2][lp], rb = Rq[2 * c2 + 1][lp];
-      const double a[4] = {ra.x, ra.y, ra.z, ra.w}, b[4] = {rb.x, rb.y, rb.z, rb.w};
+      for (int c2 = 0; c2 < kD / 2; ++c2) {
+        const float4 ra = Rq[2 * c2][lp], rb = Rq[2 * c2 + 1][lp];
+        const double a[4] = {ra.x, ra.y, ra.z, ra.w}, b[4] = {rb.x, rb.y, rb.z, rb.w};
 #pragma unroll
-      for (int p = 0; p < kBulkRows / 2; ++p) {
-        const double2 x = xs[w][2 * p + half][c2];  // channels 2 c2, 2 c2 + 1 of the row
+        for (int p = 0; p < kBulkRows / 2; ++p) {
+          const double2 x = xs[w][2 * p + half][c2];  // channels 2 c2, 2 c2 + 1 of the row
 #pragma unroll
-        for (int q = 0; q < 4; ++q) {
-          acc[p][q] = __fma_rn(x.x, a[q], acc[p][q]);
-          acc[p][q] = __fma_rn(x.y, b[q], acc[p][q]);
+          for (int q = 0; q < 4; ++q) {
+            acc[p][q] = __fma_rn(x.x, a[q], acc[p][q]);
+            acc[p][q] = __fma_rn(x.y, b[q], acc[p][q]);
+          }
         }
       }
+    } else {  // identity: channel l' + 32 q of the row
+#pragma unroll
+      for (int p = 0; p < kBulkRows / 2; ++p)
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          const double2 x = xs[w][2 * p + half][(lp + 32 * q) >> 1];
+          acc[p][q] = (lp & 1) ? x.y : x.x;
+        }
     }
 #pragma unroll
     for (int p = 0; p < kBulkRows / 2; ++p) {
       const int row = item * kBulkRows + 2 * p + half;
-      store_row4(pages, Hkv, rows.slot(row), row, is_v, clip, acc[p], lp);
+      store_row4(pages, Hkv, rows.slot(row), row, is_v, clip, fmt, acc[p], lp, half);
     }
   }
 }
@@ -516,7 +654,7 @@ __global__ __launch_bounds__(256) void prepare_kernel(const uint16_t* __restrict
 template <int RW, class Rows>
 __global__ __launch_bounds__(256) void prologue_kernel(
     uint8_t* __restrict__ pages, int Hkv, Rows rows, int n_rows, const float* __restrict__ Rk,
-    const float* __restrict__ Rv, float clip_k, float clip_v, int append_blocks,
+    const float* __restrict__ Rv, float clip_k, float clip_v, QFmt fmt, int append_blocks,
     const uint16_t* __restrict__ q, int q_rows, float qscale, float* __restrict__ qt,
     int prep_blocks) {
   __shared__ float Rs[kD * kD];
@@ -525,7 +663,7 @@ __global__ __launch_bounds__(256) void prologue_kernel(
   if (blockIdx.y < 2) {
     if ((int)blockIdx.x < append_blocks)
       append_body<RW>(Rs, xs, blockIdx.y, blockIdx.x, append_blocks, pages, Hkv, rows, n_rows,
-                      Rk, Rv, clip_k, clip_v);
+                      Rk, Rv, clip_k, clip_v, fmt);
   } else if ((int)blockIdx.x < prep_blocks) {
     prepare_body(Rs, qs, blockIdx.x, q, q_rows, Rk, qscale, qt);
   }
@@ -542,11 +680,11 @@ int64_t append_blocks_for(int64_t n_rows, int rw) {
 
 template <class Rows>
 hipError_t launch_rows(void* pages, int64_t Hkv, const Rows& rows, int64_t n_rows, const float* Rk,
-                       const float* Rv, float clip_k, float clip_v, hipStream_t st) {
+                       const float* Rv, float clip_k, float clip_v, QFmt fmt, hipStream_t st) {
   if (n_rows <= 4096) {  // one decode step: many short waves
     const dim3 grid((unsigned)append_blocks_for(n_rows, 1), 2);
     hipLaunchKernelGGL((append_kernel<1, Rows>), grid, dim3(256), 0, st, static_cast<uint8_t*>(pages),
-                       (int)Hkv, rows, (int)n_rows, Rk, Rv, clip_k, clip_v);
+                       (int)Hkv, rows, (int)n_rows, Rk, Rv, clip_k, clip_v, fmt);
   } else {  // bulk: one persistent 8-wave block per CU, half of them per tensor
     const int64_t items = (n_rows + kBulkRows - 1) / kBulkRows;
     int64_t nb = (items + kBulkWaves - 1) / kBulkWaves;
@@ -554,7 +692,7 @@ hipError_t launch_rows(void* pages, int64_t Hkv, const Rows& rows, int64_t n_row
     if (nb > cap) nb = cap;
     hipLaunchKernelGGL(append_bulk_kernel<Rows>, dim3((unsigned)nb, 2), dim3(512), 0, st,
                        static_cast<uint8_t*>(pages), (int)Hkv, rows, (int)n_rows, Rk, Rv, clip_k,
-                       clip_v);
+                       clip_v, fmt);
   }
   return hipGetLastError();
 }
@@ -562,7 +700,7 @@ hipError_t launch_rows(void* pages, int64_t Hkv, const Rows& rows, int64_t n_row
 template <class Rows>
 hipError_t launch_prologue(void* pages, int64_t Hkv, const Rows& rows, int64_t n_rows,
                            const float* Rk, const float* Rv, float clip_k, float clip_v,
-                           const uint16_t* q, int B, int Hq, float qscale, float* qt,
+                           QFmt fmt, const uint16_t* q, int B, int Hq, float qscale, float* qt,
                            hipStream_t st) {
   const int rw = n_rows <= 4096 ? 1 : 4;
   const int ab = n_rows > 0 ? (int)append_blocks_for(n_rows, rw) : 0;
@@ -571,32 +709,33 @@ hipError_t launch_prologue(void* pages, int64_t Hkv, const Rows& rows, int64_t n
   if (rw == 1)
     hipLaunchKernelGGL((prologue_kernel<1, Rows>), grid, dim3(256), 0, st,
                        static_cast<uint8_t*>(pages), (int)Hkv, rows, (int)n_rows, Rk, Rv, clip_k,
-                       clip_v, ab, q, B * Hq, qscale, qt, pb);
+                       clip_v, fmt, ab, q, B * Hq, qscale, qt, pb);
   else
     hipLaunchKernelGGL((prologue_kernel<4, Rows>), grid, dim3(256), 0, st,
                        static_cast<uint8_t*>(pages), (int)Hkv, rows, (int)n_rows, Rk, Rv, clip_k,
-                       clip_v, ab, q, B * Hq, qscale, qt, pb);
+                       clip_v, fmt, ab, q, B * Hq, qscale, qt, pb);
   return hipGetLastError();
 }
 }  // namespace
 
 hipError_t launch_append(void* pages, int64_t Hkv, const uint16_t* k, const uint16_t* v,
                          const int64_t* slots, int n_tok, const float* Rk, const float* Rv,
-                         float clip_k, float clip_v, hipStream_t st) {
+                         float clip_k, float clip_v, QuantFmt fmt, hipStream_t st) {
   const int64_t n_rows = (int64_t)n_tok * Hkv;
   const PlainRows rows{k, v, slots, (int)n_rows, (int)Hkv};
-  return launch_rows(pages, Hkv, rows, n_rows, Rk, Rv, clip_k, clip_v, st);
+  return launch_rows(pages, Hkv, rows, n_rows, Rk, Rv, clip_k, clip_v, fmt, st);
 }
 
 hipError_t launch_mixed_append(void* pages, uint16_t* seg, int64_t Hkv, int S0, int W,
                                const uint16_t* k, const uint16_t* v, const int32_t* seq_idx,
                                const int64_t* pos, int n_tok, const int32_t* seq_lens,
                                const int32_t* block_table, int max_pages, const float* Rk,
-                               const float* Rv, float clip_k, float clip_v, hipStream_t st) {
+                               const float* Rv, float clip_k, float clip_v, QuantFmt fmt,
+                               hipStream_t st) {
   const int64_t n_rows = (int64_t)n_tok * Hkv;
   const PrefillRows rows{k, v, seg, seq_idx, pos, seq_lens, block_table, (int)n_rows, (int)Hkv,
                          max_pages, S0, W};
-  return launch_rows(pages, Hkv, rows, n_rows, Rk, Rv, clip_k, clip_v, st);
+  return launch_rows(pages, Hkv, rows, n_rows, Rk, Rv, clip_k, clip_v, fmt, st);
 }
 
 hipError_t launch_decode_prepare(const uint16_t* q, int B, int Hq, const float* Rk,
@@ -609,24 +748,25 @@ hipError_t launch_decode_prepare(const uint16_t* q, int B, int Hq, const float* 
 
 hipError_t launch_step_prologue(void* pages, int64_t Hkv, const uint16_t* k, const uint16_t* v,
                                 const int64_t* slots, int n_tok, const float* Rk,
-                                const float* Rv, float clip_k, float clip_v, const uint16_t* q,
-                                int B, int Hq, float qscale, float* qt, hipStream_t st) {
+                                const float* Rv, float clip_k, float clip_v, QuantFmt fmt,
+                                const uint16_t* q, int B, int Hq, float qscale, float* qt,
+                                hipStream_t st) {
   const int64_t n_rows = (int64_t)n_tok * Hkv;
   const PlainRows rows{k, v, slots, (int)n_rows, (int)Hkv};
-  return launch_prologue(pages, Hkv, rows, n_rows, Rk, Rv, clip_k, clip_v, q, B, Hq, qscale, qt,
-                         st);
+  return launch_prologue(pages, Hkv, rows, n_rows, Rk, Rv, clip_k, clip_v, fmt, q, B, Hq, qscale,
+                         qt, st);
 }
 
 hipError_t launch_mixed_step_prologue(void* pages, uint16_t* seg, int64_t Hkv, int S0, int W,
                                       const uint16_t* k, const uint16_t* v,
                                       const int32_t* seq_lens, const int32_t* block_table,
                                       int max_pages, const float* Rk, const float* Rv,
-                                      float clip_k, float clip_v, const uint16_t* q, int B,
-                                      int Hq, float qscale, float* qt, hipStream_t st) {
+                                      float clip_k, float clip_v, QuantFmt fmt, const uint16_t* q,
+                                      int B, int Hq, float qscale, float* qt, hipStream_t st) {
   const int64_t n_rows = (int64_t)B * Hkv;
   const StepRows rows{k, v, seg, seq_lens, block_table, (int)n_rows, (int)Hkv, max_pages, S0, W};
-  return launch_prologue(pages, Hkv, rows, n_rows, Rk, Rv, clip_k, clip_v, q, B, Hq, qscale, qt,
-                         st);
+  return launch_prologue(pages, Hkv, rows, n_rows, Rk, Rv, clip_k, clip_v, fmt, q, B, Hq, qscale,
+                         qt, st);
 }
 
 }  // namespace oscar

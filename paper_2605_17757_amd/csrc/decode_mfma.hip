@@ -115,6 +115,22 @@ __device__ inline float mix_nhi(uint32_t h, float b, float c) {  // -hi(h) * b +
   return r;
 }
 
+// Reads of a packed (scale, zero) word in either metadata format: binary16 via
+// v_fma_mix_f32 (no conversion instructions), bfloat16 as the upper bits of a
+// binary32 (a shift or a mask).
+template <bool BF>
+__device__ inline float sz_s_fma(uint32_t h, float b, float c) {  // s * b + c
+  return BF ? fmaf(__uint_as_float(h << 16), b, c) : mix_lo(h, b, c);
+}
+template <bool BF>
+__device__ inline float sz_z_fma(uint32_t h, float b, float c) {  // z * b + c
+  return BF ? fmaf(__uint_as_float(h & 0xffff0000u), b, c) : mix_hi(h, b, c);
+}
+template <bool BF>
+__device__ inline float sz_nz_fma(uint32_t h, float b, float c) {  // -z * b + c
+  return BF ? fmaf(-__uint_as_float(h & 0xffff0000u), b, c) : mix_nhi(h, b, c);
+}
+
 // unsigned maximum of the low halves of three words (high half of the result unused)
 __device__ inline uint32_t max3_lo16(uint32_t a, uint32_t b, uint32_t c) {
   uint32_t r;
@@ -223,7 +239,7 @@ struct WaveState {
 
 // FULL: all 64 token slots of the page are read; otherwise only slots in
 // [t0, t1) (the partial first or last page of a token range).
-template <bool FULL>
+template <bool FULL, bool BF>
 __device__ inline void compute_page(WaveState& st, WaveLds& L, int t0, int t1, int lo, int hi) {
   char* pb = reinterpret_cast<char*>(L.page);
   // ---- scores of head hi for tokens 4*lo + u ----
@@ -245,8 +261,8 @@ __device__ inline void compute_page(WaveState& st, WaveLds& L, int t0, int t1, i
       const v4i d = mfma32(st.aq[g], b);
       const int t = combine3(d[0], d[1], d[2]);
       const uint32_t sz = comp(ksz[g], u);
-      // s * (acc - z * sum q_int) with s, z read from the packed binary16 pair
-      acc = mix_lo(sz, mix_nhi(sz, st.qs[g], (float)t), acc);
+      // s * (acc - z * sum q_int) with s, z read from the packed pair
+      acc = sz_s_fma<BF>(sz, sz_nz_fma<BF>(sz, st.qs[g], (float)t), acc);
     }
     S[u] = acc;
   }
@@ -290,14 +306,15 @@ __device__ inline void compute_page(WaveState& st, WaveLds& L, int t0, int t1, i
     sz[e] = comp(vz[e >> 2], e & 3);
     if (!FULL && (16 * hi + e < t0 || 16 * hi + e >= t1)) sz[e] = 0u;  // (0, 0): w = 0, z = 0
   }
-  // largest V scale of the group on this page: scales are positive binary16, so
-  // their bit patterns order like their values (high halves, the zero points, ignored)
+  // largest V scale of the group on this page: scales are positive binary16 or
+  // bfloat16, so their bit patterns order like their values (high halves, the
+  // zero points, ignored)
   uint32_t m5[6];
 #pragma unroll
   for (int e = 0; e < 5; ++e) m5[e] = max3_lo16(sz[3 * e], sz[3 * e + 1], sz[3 * e + 2]);
   m5[5] = sz[15];
   const uint32_t smax = max3_lo16(max3_lo16(m5[0], m5[1], m5[2]), max3_lo16(m5[3], m5[4], m5[5]), 0u);
-  const float svmax = rows_max(h_lo(smax));
+  const float svmax = rows_max(BF ? __uint_as_float(smax << 16) : h_lo(smax));
   const float sig = hsw.y * svmax;  // >= every w of the row on this page
   const float inv = sig > 0.0f ? kWMax * __builtin_amdgcn_rcpf(sig) : 0.0f;
   L.ws[lo] = sig * (1.0f / kWMax);
@@ -309,11 +326,11 @@ __device__ inline void compute_page(WaveState& st, WaveLds& L, int t0, int t1, i
 #pragma unroll
     for (int b = 0; b < 4; ++b) {
       const int e = 4 * j + b;
-      const float w = mix_lo(sz[e], compf(pw[j], b), 0.0f);
+      const float w = sz_s_fma<BF>(sz[e], compf(pw[j], b), 0.0f);
       // mantissa of rne(w * inv) + 2^23 + 32896 = k + 32896, k in [0, 2^21]:
       // k = 65536 d_0 + 256 d_1 + d_2 with d_2, d_1 = (bytes 0, 1) ^ 0x80, d_0 = byte 2
       f[b] = __float_as_uint(fmaf(w, inv, kMagic + kDigitBias));
-      zp = mix_hi(sz[e], w, zp);  // unquantized w: differs from the quantized by <= 2^-22 sig
+      zp = sz_z_fma<BF>(sz[e], w, zp);  // unquantized w: differs from the quantized by <= 2^-22 sig
     }
     const uint32_t t01 = __builtin_amdgcn_perm(f[1], f[0], 0x05010400u) ^ 0x80808080u;  // [f0.0 f1.0 f0.1 f1.1]
     const uint32_t t23 = __builtin_amdgcn_perm(f[3], f[2], 0x05010400u) ^ 0x80808080u;
@@ -380,7 +397,7 @@ __device__ inline TokRange tok_range(int lo, int hi) {
 // piece + 1 .. num_splits - 1 are marked empty.  The wave has done `done0` of its
 // `total` pages before this piece (issue-priority bands).  Without MIXED the
 // range starts at token 0 (R.t0 = 0).
-template <bool MIXED>
+template <bool MIXED, bool BF>
 __device__ __attribute__((always_inline)) inline void process_piece(WaveLds& L, const uint8_t* __restrict__ pages, int Hkv, int Hq,
                                      const int32_t* __restrict__ block_table, int max_pages, int b,
                                      TokRange R, int kvh, int chunk, int p0, int p1, int piece,
@@ -473,7 +490,7 @@ __device__ __attribute__((always_inline)) inline void process_piece(WaveLds& L, 
   if (MIXED && p0 == 0 && p0 < p1 && R.t0 != 0) {  // the range's partial first page
     stage_store(L.page, sg, l);
     stage_load(sg, base + (size_t)__builtin_amdgcn_readlane(btv, min(1, p1 - 1)) * page_stride, l);
-    compute_page<false>(st, L, R.t0, npg == 1 ? R.t1 : kP, lo, hi);
+    compute_page<false, BF>(st, L, R.t0, npg == 1 ? R.t1 : kP, lo, hi);
     pg = 1;
     pf = max(pf, 1);  // a one-page range is done
   }
@@ -493,7 +510,7 @@ __device__ __attribute__((always_inline)) inline void process_piece(WaveLds& L, 
         btv = (cb + l < p1) ? bt[cb + l] : 0;
       }
       stage_load(sg, base + (size_t)__builtin_amdgcn_readlane(btv, nx - cb) * page_stride, l);
-      compute_page<true>(st, L, 0, kP, lo, hi);
+      compute_page<true, BF>(st, L, 0, kP, lo, hi);
     }
     if (band < 4 && lim > p0 && lim <= pf) {  // the band ended inside this piece
       if (band == 1) __builtin_amdgcn_s_setprio(2);
@@ -503,7 +520,7 @@ __device__ __attribute__((always_inline)) inline void process_piece(WaveLds& L, 
   }
   if (pf < p1) {  // the partial last page; the stage holds it
     stage_store(L.page, sg, l);
-    compute_page<false>(st, L, 0, R.t1, lo, hi);
+    compute_page<false, BF>(st, L, 0, R.t1, lo, hi);
   }
 
   // ---- write the split's partial state ----
@@ -557,7 +574,7 @@ __device__ inline int wave_sum_i(int x) {
   return x;
 }
 
-template <bool MIXED>
+template <bool MIXED, bool BF>
 __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(4, 4))) void split_mfma_kernel(
     const uint8_t* __restrict__ pages, int Hkv, int Hq, const int32_t* __restrict__ block_table,
     int max_pages, const int32_t* __restrict__ seq_lens, int num_splits, int n_ranges, int B,
@@ -585,7 +602,7 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(4, 4))) void
   };
   if (num_splits == 1) {  // one range per sequence
     const TokRange R = range_of(r);
-    process_piece<MIXED>(L, pages, Hkv, Hq, block_table, max_pages, r, R, kvh, chunk, 0, R.npg,
+    process_piece<MIXED, BF>(L, pages, Hkv, Hq, block_table, max_pages, r, R, kvh, chunk, 0, R.npg,
                          0, true, 1, stride, qt, part_o, part_ml, 0, 1 << 20);
     return;
   }
@@ -640,7 +657,7 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(4, 4))) void
   while (true) {
     const int64_t end = min(xe, before + npg_b);
     const int piece = (int)(r - before / pw);
-    process_piece<MIXED>(L, pages, Hkv, Hq, block_table, max_pages, b, range_of(b), kvh, chunk,
+    process_piece<MIXED, BF>(L, pages, Hkv, Hq, block_table, max_pages, b, range_of(b), kvh, chunk,
                          (int)(x - before), (int)(end - before), piece, end == before + npg_b,
                          num_splits, stride, qt, part_o, part_ml, (int)(x - x0), (int)(xe - x0));
     x = end;
@@ -659,7 +676,7 @@ hipError_t launch_decode_split_mfma(const uint8_t* pages, int Hkv, int B, int Hq
                                     const int32_t* block_table, int max_pages,
                                     const int32_t* seq_lens, int num_splits, int resident_waves,
                                     const float* qt, float* part_o, float* part_ml,
-                                    hipStream_t st, const MixedSpec* mixed) {
+                                    hipStream_t st, int meta_bf16, const MixedSpec* mixed) {
   const int g = Hq / Hkv;
   const int nch = (g + 3) / 4;
   // one range per resident wave group (each range runs Hkv * nch waves)
@@ -667,14 +684,20 @@ hipError_t launch_decode_split_mfma(const uint8_t* pages, int Hkv, int B, int Hq
       num_splits == 1 ? (int64_t)B : std::max<int64_t>(1, resident_waves / (nch * Hkv));
   const int64_t blocks = (ranges * Hkv + 7) / 8 * 8 * nch;
   if (blocks > 0x7fffffffLL) return hipErrorInvalidConfiguration;
-  if (mixed)
-    hipLaunchKernelGGL(split_mfma_kernel<true>, dim3((unsigned)blocks), dim3(64), 0, st, pages,
-                       Hkv, Hq, block_table, max_pages, seq_lens, num_splits, (int)ranges, B, qt,
-                       part_o, part_ml, mixed->S0, mixed->W, mixed->row_stride);
-  else
-    hipLaunchKernelGGL(split_mfma_kernel<false>, dim3((unsigned)blocks), dim3(64), 0, st, pages,
-                       Hkv, Hq, block_table, max_pages, seq_lens, num_splits, (int)ranges, B, qt,
-                       part_o, part_ml, 0, 0, num_splits);
+  const int S0 = mixed ? mixed->S0 : 0, W = mixed ? mixed->W : 0;
+  const int stride = mixed ? mixed->row_stride : num_splits;
+  auto go = [&](auto kernel) {
+    hipLaunchKernelGGL(kernel, dim3((unsigned)blocks), dim3(64), 0, st, pages, Hkv, Hq,
+                       block_table, max_pages, seq_lens, num_splits, (int)ranges, B, qt, part_o,
+                       part_ml, S0, W, stride);
+  };
+  if (mixed) {
+    if (meta_bf16) go(split_mfma_kernel<true, true>);
+    else go(split_mfma_kernel<true, false>);
+  } else {
+    if (meta_bf16) go(split_mfma_kernel<false, true>);
+    else go(split_mfma_kernel<false, false>);
+  }
   return hipGetLastError();
 }
 

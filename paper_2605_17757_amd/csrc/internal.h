@@ -42,33 +42,44 @@ struct MixedSpec {
   int S0, W, row_stride;
 };
 
+// Quantizer format (oscar_layout clip_mode / meta_dtype): scale and zero stored
+// as bfloat16 instead of binary16; the token-wise quantile clip threshold
+// instead of ratio x group absmax.
+struct QuantFmt {
+  int bf16;
+  int quantile;
+};
+
 // Kernel launchers (each returns the hipError_t of its launch).
+// Rk or Rv nullptr: identity rotation.
 hipError_t launch_append(void* pages, int64_t Hkv, const uint16_t* k, const uint16_t* v,
                          const int64_t* slots, int n_tok, const float* Rk, const float* Rv,
-                         float clip_k, float clip_v, hipStream_t st);
+                         float clip_k, float clip_v, QuantFmt fmt, hipStream_t st);
 
 hipError_t launch_decode_prepare(const uint16_t* q, int B, int Hq, const float* Rk,
                                  float qscale, float* qt, hipStream_t st);
 // Cache update of n_tok tokens and query rotation in one launch (decode step prologue).
 hipError_t launch_step_prologue(void* pages, int64_t Hkv, const uint16_t* k, const uint16_t* v,
                                 const int64_t* slots, int n_tok, const float* Rk,
-                                const float* Rv, float clip_k, float clip_v, const uint16_t* q,
-                                int B, int Hq, float qscale, float* qt, hipStream_t st);
+                                const float* Rv, float clip_k, float clip_v, QuantFmt fmt,
+                                const uint16_t* q, int B, int Hq, float qscale, float* qt,
+                                hipStream_t st);
 // Mixed cache: prompt tokens routed to INT2 or the bf16 segment store by their
 // position in a cache of length seq_lens[b].
 hipError_t launch_mixed_append(void* pages, uint16_t* seg, int64_t Hkv, int S0, int W,
                                const uint16_t* k, const uint16_t* v, const int32_t* seq_idx,
                                const int64_t* pos, int n_tok, const int32_t* seq_lens,
                                const int32_t* block_table, int max_pages, const float* Rk,
-                               const float* Rv, float clip_k, float clip_v, hipStream_t st);
+                               const float* Rv, float clip_k, float clip_v, QuantFmt fmt,
+                               hipStream_t st);
 // Mixed cache decode-step prologue: one new token per sequence (sink, window with
 // demotion of the oldest window token, or INT2) and the query rotation.
 hipError_t launch_mixed_step_prologue(void* pages, uint16_t* seg, int64_t Hkv, int S0, int W,
                                       const uint16_t* k, const uint16_t* v,
                                       const int32_t* seq_lens, const int32_t* block_table,
                                       int max_pages, const float* Rk, const float* Rv,
-                                      float clip_k, float clip_v, const uint16_t* q, int B,
-                                      int Hq, float qscale, float* qt, hipStream_t st);
+                                      float clip_k, float clip_v, QuantFmt fmt, const uint16_t* q,
+                                      int B, int Hq, float qscale, float* qt, hipStream_t st);
 // Partial softmax state of the bf16 tokens (sink and window) of every (sequence,
 // head) row, in the original basis, into slot num_splits of rows of num_splits + 1.
 hipError_t launch_seg_partial(const uint16_t* seg, int Hkv, int S0, int W, int B, int Hq,
@@ -76,10 +87,11 @@ hipError_t launch_seg_partial(const uint16_t* seg, int Hkv, int S0, int W, int B
                               float qscale, int num_splits, float* part_o, float* part_ml,
                               hipStream_t st);
 // mixed == nullptr: every token of a sequence is INT2 (rows of num_splits slots).
+// meta_bf16: scale and zero stored as bfloat16.
 hipError_t launch_decode_split(const uint8_t* pages, int Hkv, int B, int Hq,
                                const int32_t* block_table, int max_pages,
                                const int32_t* seq_lens, int num_splits, const float* qt,
-                               float* part_o, float* part_ml, hipStream_t st,
+                               float* part_o, float* part_ml, hipStream_t st, int meta_bf16,
                                const MixedSpec* mixed = nullptr);
 // Balanced split kernel: `resident_waves` waves share the pages equally; a
 // (sequence, head) row gets at most num_splits partial states.
@@ -87,7 +99,7 @@ hipError_t launch_decode_split_mfma(const uint8_t* pages, int Hkv, int B, int Hq
                                     const int32_t* block_table, int max_pages,
                                     const int32_t* seq_lens, int num_splits, int resident_waves,
                                     const float* qt, float* part_o, float* part_ml,
-                                    hipStream_t st, const MixedSpec* mixed);
+                                    hipStream_t st, int meta_bf16, const MixedSpec* mixed);
 int device_cus();  // compute units of the current device (cached)
 // mixed != nullptr: rows of num_splits + 1 slots, the last one in the original
 // basis (added after the back-rotation).

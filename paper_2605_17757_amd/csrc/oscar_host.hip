@@ -39,6 +39,9 @@ int check_layout(const oscar_layout* L) {
       L->num_pages <= 0)
     return OSCAR_ERR_INVALID_ARG;
   if (L->head_dim % L->group_size != 0 || L->head_dim % 4 != 0) return OSCAR_ERR_INVALID_ARG;
+  if (L->clip_mode != OSCAR_CLIP_GROUP_ABSMAX && L->clip_mode != OSCAR_CLIP_TOKEN_QUANTILE)
+    return OSCAR_ERR_INVALID_ARG;
+  if (L->meta_dtype != OSCAR_META_F16 && L->meta_dtype != OSCAR_META_BF16) return OSCAR_ERR_INVALID_ARG;
   if (L->head_dim != kD || L->page_size != kP || L->group_size != kG) return OSCAR_ERR_UNSUPPORTED;
   if (L->num_kv_heads > 65535) return OSCAR_ERR_UNSUPPORTED;
   return OSCAR_OK;
@@ -71,6 +74,12 @@ int32_t resolve_default_splits(const oscar_layout* L, int32_t B, int32_t Hq,
 }
 
 bool aligned(const void* p, size_t a) { return (reinterpret_cast<uintptr_t>(p) & (a - 1)) == 0; }
+
+QuantFmt quant_fmt(const oscar_layout* L) {
+  return QuantFmt{L->meta_dtype == OSCAR_META_BF16 ? 1 : 0,
+                  L->clip_mode == OSCAR_CLIP_TOKEN_QUANTILE ? 1 : 0};
+}
+int meta_bf16(const oscar_layout* L) { return L->meta_dtype == OSCAR_META_BF16 ? 1 : 0; }
 
 // Mixed cache: sink and window sizes (and B, for the segment store size).
 bool seg_ok(int32_t B, int32_t S0, int32_t W) {
@@ -141,14 +150,15 @@ int oscar_kv_append(const oscar_layout* L, void* pages, const void* k_new, const
   if (st) return st;
   if (n_tok < 0 || !clip_ok(clip_k) || !clip_ok(clip_v)) return OSCAR_ERR_INVALID_ARG;
   if (n_tok == 0) return OSCAR_OK;
-  if (!pages || !k_new || !v_new || !slot_mapping || !R_k || !R_v) return OSCAR_ERR_INVALID_ARG;
+  if (!pages || !k_new || !v_new || !slot_mapping) return OSCAR_ERR_INVALID_ARG;
   if (!aligned(k_new, 4) || !aligned(v_new, 4) || !aligned(R_k, 16) || !aligned(R_v, 16) ||
       !aligned(pages, 16) || !aligned(slot_mapping, 8))
     return OSCAR_ERR_INVALID_ARG;
   if ((int64_t)n_tok * L->num_kv_heads > 0x7fffffffLL) return OSCAR_ERR_UNSUPPORTED;
   return hip_status(launch_append(pages, L->num_kv_heads, static_cast<const uint16_t*>(k_new),
                                   static_cast<const uint16_t*>(v_new), slot_mapping, n_tok, R_k,
-                                  R_v, clip_k, clip_v, static_cast<hipStream_t>(stream)));
+                                  R_v, clip_k, clip_v, quant_fmt(L),
+                                  static_cast<hipStream_t>(stream)));
 }
 
 int oscar_decode_prepare(const oscar_layout* L, const void* q, int32_t B, int32_t Hq,
@@ -156,7 +166,7 @@ int oscar_decode_prepare(const oscar_layout* L, const void* q, int32_t B, int32_
                          size_t workspace_bytes, void* stream) {
   int st = check_decode_common(L, B, Hq, num_splits);
   if (st) return st;
-  if (!q || !R_k || !workspace || !isfinite(sm_scale)) return OSCAR_ERR_INVALID_ARG;
+  if (!q || !workspace || !isfinite(sm_scale)) return OSCAR_ERR_INVALID_ARG;
   if (!aligned(workspace, 256) || !aligned(q, 4)) return OSCAR_ERR_INVALID_ARG;
   const DecodeWs ws = decode_ws(B, Hq, num_splits);
   if (workspace_bytes < ws.total) return OSCAR_ERR_WORKSPACE_TOO_SMALL;
@@ -182,7 +192,7 @@ int oscar_decode_split(const oscar_layout* L, const void* pages, int32_t B, int3
       static_cast<const uint8_t*>(pages), L->num_kv_heads, B, Hq, block_table, max_pages_per_seq,
       seq_lens, num_splits, reinterpret_cast<const float*>(base + ws.qt_off),
       reinterpret_cast<float*>(base + ws.po_off), reinterpret_cast<float*>(base + ws.pml_off),
-      static_cast<hipStream_t>(stream)));
+      static_cast<hipStream_t>(stream), meta_bf16(L)));
 }
 
 int oscar_decode_reduce(const oscar_layout* L, int32_t B, int32_t Hq, const float* R_v,
@@ -190,7 +200,7 @@ int oscar_decode_reduce(const oscar_layout* L, int32_t B, int32_t Hq, const floa
                         oscar_dtype out_dtype, void* stream) {
   int st = check_decode_common(L, B, Hq, num_splits);
   if (st) return st;
-  if (!R_v || !workspace || !out) return OSCAR_ERR_INVALID_ARG;
+  if (!workspace || !out) return OSCAR_ERR_INVALID_ARG;
   if (out_dtype != OSCAR_OUT_BF16 && out_dtype != OSCAR_OUT_F32) return OSCAR_ERR_INVALID_ARG;
   if (!aligned(workspace, 256) || !aligned(out, out_dtype == OSCAR_OUT_F32 ? 4 : 2))
     return OSCAR_ERR_INVALID_ARG;
@@ -217,7 +227,7 @@ int oscar_decode_attn(const oscar_layout* L, const void* pages, const void* q, i
   // validate every argument of all three stages before launching any of them
   int st = check_decode_common(L, B, Hq, num_splits);
   if (st) return st;
-  if (!pages || !q || !block_table || !seq_lens || !R_k || !R_v || !workspace || !out ||
+  if (!pages || !q || !block_table || !seq_lens || !workspace || !out ||
       max_pages_per_seq < 1 || !isfinite(sm_scale))
     return OSCAR_ERR_INVALID_ARG;
   if (out_dtype != OSCAR_OUT_BF16 && out_dtype != OSCAR_OUT_F32) return OSCAR_ERR_INVALID_ARG;
@@ -259,7 +269,7 @@ int oscar_decode_step(const oscar_layout* L, void* pages, const void* k_new, con
   }
   st = check_decode_common(L, B, Hq, num_splits);
   if (st) return st;
-  if (!pages || !q || !block_table || !seq_lens || !R_k || !R_v || !workspace || !out ||
+  if (!pages || !q || !block_table || !seq_lens || !workspace || !out ||
       max_pages_per_seq < 1 || !isfinite(sm_scale))
     return OSCAR_ERR_INVALID_ARG;
   if (out_dtype != OSCAR_OUT_BF16 && out_dtype != OSCAR_OUT_F32) return OSCAR_ERR_INVALID_ARG;
@@ -274,13 +284,14 @@ int oscar_decode_step(const oscar_layout* L, void* pages, const void* k_new, con
   st = hip_status(launch_step_prologue(pages, L->num_kv_heads,
                                        static_cast<const uint16_t*>(k_new),
                                        static_cast<const uint16_t*>(v_new), slot_mapping, n_new,
-                                       R_k, R_v, clip_k, clip_v, static_cast<const uint16_t*>(q),
-                                       B, Hq, sm_scale * kLog2e, qt, hs));
+                                       R_k, R_v, clip_k, clip_v, quant_fmt(L),
+                                       static_cast<const uint16_t*>(q), B, Hq, sm_scale * kLog2e,
+                                       qt, hs));
   if (st) return st;
   st = hip_status(launch_decode_split(
       static_cast<const uint8_t*>(pages), L->num_kv_heads, B, Hq, block_table, max_pages_per_seq,
       seq_lens, num_splits, qt, reinterpret_cast<float*>(base + ws.po_off),
-      reinterpret_cast<float*>(base + ws.pml_off), hs));
+      reinterpret_cast<float*>(base + ws.pml_off), hs, meta_bf16(L)));
   if (st) return st;
   return hip_status(launch_decode_reduce(B, Hq, num_splits,
                                          reinterpret_cast<const float*>(base + ws.po_off),
@@ -314,7 +325,7 @@ int oscar_mixed_append(const oscar_layout* L, void* pages, void* seg, int32_t B,
       max_pages_per_seq < 1)
     return OSCAR_ERR_INVALID_ARG;
   if (n_tok == 0) return OSCAR_OK;
-  if (!pages || !k || !v || !seq_idx || !pos || !block_table || !seq_lens || !R_k || !R_v ||
+  if (!pages || !k || !v || !seq_idx || !pos || !block_table || !seq_lens ||
       (S0 + W > 0 && !seg))
     return OSCAR_ERR_INVALID_ARG;
   if (!aligned(k, 4) || !aligned(v, 4) || !aligned(R_k, 16) || !aligned(R_v, 16) ||
@@ -326,7 +337,7 @@ int oscar_mixed_append(const oscar_layout* L, void* pages, void* seg, int32_t B,
   return hip_status(launch_mixed_append(
       pages, static_cast<uint16_t*>(seg), L->num_kv_heads, S0, W, static_cast<const uint16_t*>(k),
       static_cast<const uint16_t*>(v), seq_idx, pos, n_tok, seq_lens, block_table,
-      max_pages_per_seq, R_k, R_v, clip_k, clip_v, static_cast<hipStream_t>(stream)));
+      max_pages_per_seq, R_k, R_v, clip_k, clip_v, quant_fmt(L), static_cast<hipStream_t>(stream)));
 }
 
 namespace {
@@ -347,7 +358,7 @@ int check_mixed_decode(const oscar_layout* L, const void* pages, const void* seg
   int st = check_decode_common(L, B, Hq, *num_splits);
   if (st) return st;
   if (*num_splits > 0x3fffffff || !seg_ok(B, S0, W)) return OSCAR_ERR_INVALID_ARG;
-  if (!pages || !q || !block_table || !seq_lens || !R_k || !R_v || !workspace || !out ||
+  if (!pages || !q || !block_table || !seq_lens || !workspace || !out ||
       max_pages_per_seq < 1 || !isfinite(sm_scale) || (S0 + W > 0 && !seg))
     return OSCAR_ERR_INVALID_ARG;
   if ((int64_t)max_pages_per_seq * L->page_size > 0x7fffffffLL) return OSCAR_ERR_UNSUPPORTED;
@@ -375,7 +386,7 @@ int launch_mixed_rest(const oscar_layout* L, const void* pages, const void* seg,
   int st = hip_status(launch_decode_split(static_cast<const uint8_t*>(pages), L->num_kv_heads, B,
                                           Hq, block_table, max_pages_per_seq, seq_lens,
                                           num_splits, reinterpret_cast<const float*>(base + ws.qt_off),
-                                          po, pml, hs, &mx));
+                                          po, pml, hs, meta_bf16(L), &mx));
   if (st) return st;
   st = hip_status(launch_seg_partial(static_cast<const uint16_t*>(seg), L->num_kv_heads, S0, W, B,
                                      Hq, seq_lens, max_pages_per_seq,
@@ -430,8 +441,8 @@ int oscar_decode_step_mixed(const oscar_layout* L, void* pages, void* seg, int32
   st = hip_status(launch_mixed_step_prologue(
       pages, static_cast<uint16_t*>(seg), L->num_kv_heads, S0, W,
       static_cast<const uint16_t*>(k_new), static_cast<const uint16_t*>(v_new), seq_lens,
-      block_table, max_pages_per_seq, R_k, R_v, clip_k, clip_v, static_cast<const uint16_t*>(q),
-      B, Hq, sm_scale * kLog2e, qt, hs));
+      block_table, max_pages_per_seq, R_k, R_v, clip_k, clip_v, quant_fmt(L),
+      static_cast<const uint16_t*>(q), B, Hq, sm_scale * kLog2e, qt, hs));
   if (st) return st;
   return launch_mixed_rest(L, pages, seg, S0, W, q, B, Hq, block_table, max_pages_per_seq,
                            seq_lens, R_v, sm_scale, num_splits, workspace, out, out_dtype, hs);

@@ -103,32 +103,57 @@ def _f16_midpoint_close(x: float, rel: float = 1e-6) -> bool:
     return abs(x - mid) <= rel * abs(x)
 
 
-def row_near_boundary(xt: np.ndarray, rho: float, G: int = 32) -> bool:
+def _bf16_round(x: float) -> float:
+    return float(torch.tensor([x], dtype=torch.float32).to(torch.bfloat16).float()[0])
+
+
+def _bf16_midpoint_close(x: float, rel: float = 1e-6) -> bool:
+    if not math.isfinite(x) or x == 0.0:
+        return False
+    # the bf16 grid step at |x| is 2^(floor(log2|x|) - 7); a midpoint is an odd
+    # multiple of half a step
+    e = math.floor(math.log2(abs(x)))
+    half = 2.0 ** (e - 8)
+    k = abs(x) / half
+    return abs(k - (2 * math.floor(k / 2) + 1)) * half <= rel * abs(x)
+
+
+def row_near_boundary(xt: np.ndarray, rho: float, G: int = 32, meta: int = 0,
+                      clip: int = 0) -> bool:
     """True if quantizing this rotated row involves a decision within 1e-6 of a
-    rounding boundary (evaluated from the oracle's fp32 row in fp64)."""
+    rounding boundary (evaluated from the oracle's fp32 row in fp64).  meta, clip:
+    the metadata format (0 binary16, 1 bfloat16) and clip rule (0 group absmax,
+    1 token quantile)."""
+    close = _bf16_midpoint_close if meta else _f16_midpoint_close
+    rnd = _bf16_round if meta else (lambda v: float(np.float16(v)))
+    tau_tok = np.float32(oracle.token_quantile(xt, rho)) if clip else None
     for g in range(len(xt) // G):
         x = xt[g * G:(g + 1) * G].astype(np.float32)
-        m = np.float32(np.abs(x).max())
-        tau = np.float32(np.float32(rho) * m)
+        if clip:
+            tau = tau_tok
+        else:
+            m = np.float32(np.abs(x).max())
+            tau = np.float32(np.float32(rho) * m)
         y = np.minimum(np.maximum(x, -tau), tau)
         a, b = float(y.min()), float(y.max())
         s_exact = (b - a) / 3.0
-        if _f16_midpoint_close(s_exact):
+        if close(s_exact):
             return True
-        s16 = float(np.float16(np.float32(np.float32(b - a) / np.float32(3.0))))
+        s16 = rnd(float(np.float32(np.float32(b - a) / np.float32(3.0))))
         if s16 == 0.0:
             continue
         z_exact = -a / s16
-        if _f16_midpoint_close(z_exact):
+        if close(z_exact):
             return True
-        z16 = float(np.float16(np.float32(-a) / np.float32(s16)))
+        z16 = rnd(float(np.float32(-a) / np.float32(s16)))
         u = y.astype(np.float64) / s16 + z16
         if np.any(np.abs(u - (np.floor(u) + 0.5)) <= 1e-6):
             return True
     return False
 
 
-def compare_pools(gpu_pool: np.ndarray, ora_pool: np.ndarray, case: Case):
+def compare_pools(gpu_pool: np.ndarray, ora_pool: np.ndarray, case: Case, meta: int = 0,
+                  clip: int = 0):
     """Returns (n_diff_bytes, n_tolerated_rows); raises AssertionError on any
     difference that the near-boundary rule does not cover."""
     diff = np.nonzero(gpu_pool != ora_pool)[0]
@@ -159,7 +184,8 @@ def compare_pools(gpu_pool: np.ndarray, ora_pool: np.ndarray, case: Case):
         src = case.v if is_v else case.k
         x = W.bf16_bits_to_f32(bits(src[i, h]))
         xt = oracle.rotate_row(x, case.Rv if is_v else case.Rk)
-        if not row_near_boundary(xt, case.cfg.clip_v if is_v else case.cfg.clip_k):
+        if not row_near_boundary(xt, case.cfg.clip_v if is_v else case.cfg.clip_k, meta=meta,
+                                 clip=clip):
             untolerated.append((slot, h, is_v, "not near a rounding boundary"))
     assert not untolerated, "append mismatches: %s (first of %d rows)" % (untolerated[:5],
                                                                            len(untolerated))

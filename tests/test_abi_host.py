@@ -213,3 +213,29 @@ def test_mixed_decode_rejects_invalid_arguments(L, step):
     if step:
         assert _mixed_decode(L, lay, step, k=None) == ok.ERR_INVALID_ARG
         assert _mixed_decode(L, lay, step, clip=1.5) == ok.ERR_INVALID_ARG
+
+
+def test_quantizer_format_fields(L):
+    # the layout's quantizer fields: known values pass, others are invalid arguments
+    for clip_mode in (ok.CLIP_GROUP_ABSMAX, ok.CLIP_TOKEN_QUANTILE):
+        for meta in (ok.META_F16, ok.META_BF16):
+            lay = ok.Layout(8, 10, clip_mode=clip_mode, meta_dtype=meta)
+            assert ok.layout_check(lay) == ok.OK
+            assert ok.page_bytes(lay) == 8 * 6144           # same bytes for both formats
+    assert ok.layout_check(ok.Layout(8, 10, clip_mode=2)) == ok.ERR_INVALID_ARG
+    assert ok.layout_check(ok.Layout(8, 10, meta_dtype=-1)) == ok.ERR_INVALID_ARG
+    assert _append(L, ok.Layout(8, 10, meta_dtype=7)) == ok.ERR_INVALID_ARG
+    assert ctypes.sizeof(ok.Layout) == 32
+
+
+def test_null_rotations_pass_validation(L):
+    # R_k / R_v NULL are the identity: validation accepts them (nothing launched
+    # for an empty append)
+    lay = ok.Layout(8, 10)
+    assert L.oscar_kv_append(ctypes.byref(lay), FAKE, FAKE, FAKE, FAKE, 0, None, None, 0.9, 0.9,
+                             None) == ok.OK
+    # a bad argument elsewhere is still reported with NULL rotations
+    assert L.oscar_kv_append(ctypes.byref(lay), None, FAKE, FAKE, FAKE, 4, None, None, 0.9, 0.9,
+                             None) == ok.ERR_INVALID_ARG
+    assert L.oscar_decode_attn(ctypes.byref(lay), FAKE, FAKE, 2, 32, FAKE, 4, FAKE, None, None,
+                               0.088, 2, FAKE, 16, FAKE, 0, None) == ok.ERR_WORKSPACE_TOO_SMALL
