@@ -20,6 +20,8 @@ those events add launch gaps).
 workload.  `bf16_baseline` is the bf16 paged-decode kernel on the same
 sequences.  `mixed_cache_step` is oscar_decode_step_mixed on the same sequences
 with a bf16 sink of 64 and a bf16 window of 256 tokens around the INT2 history.
+`variants` times the same step with the cache in other quantizer formats: the
+paper's stated one (bf16 scale/zero, per-token quantile clip) and identity R_V.
 """
 from __future__ import annotations
 
@@ -58,6 +60,8 @@ def parse():
                          "slower than eager launches on ROCm 7.x, so never used for value)")
     ap.add_argument("--cpu-seconds", type=float, default=10.0,
                     help="target CPU time for the oracle baseline sample")
+    ap.add_argument("--no-variants", action="store_true",
+                    help="skip the quantizer-variant steps (paper format, identity R_V)")
     ap.add_argument("--no-mixed", action="store_true",
                     help="skip the mixed-precision cache step (bf16 sink + window)")
     ap.add_argument("--sink", type=int, default=64, help="mixed cache: bf16 sink tokens S0")
@@ -380,6 +384,54 @@ def main():
                       "step_total": m_bytes},
         }
         del mws, seg_store
+
+    # ---- quantizer variants on the same sequences: a cache of tokens 0..n-2 in the
+    # variant's format, then the same timed oscar_decode_step ----
+    if not args.no_variants:
+        del pool  # the INT2 pool of the main step is no longer needed
+        torch.cuda.empty_cache()
+        res["variants"] = {}
+        for vname, (clip_mode, meta, use_rv) in {
+                "paper_format": (ok.CLIP_TOKEN_QUANTILE, ok.META_BF16, True),
+                "identity_v": (ok.CLIP_GROUP_ABSMAX, ok.META_F16, False)}.items():
+            vlay = ok.Layout(num_kv_heads=Hkv, num_pages=num_pages, clip_mode=clip_mode,
+                             meta_dtype=meta)
+            vRv = Rv if use_rv else None
+            vpool = ok.alloc_pool(vlay)
+            t0 = time.time()
+            for b in range(B):
+                k, v = W.cache_kv(cfg, b, device=dev)
+                n = int(lens[b])
+                slots = torch.from_numpy(W.slots_for(table, b, np.arange(n - 1))).to(dev)
+                ok.kv_append(vlay, vpool, k[:n - 1], v[:n - 1], slots, Rk, vRv, cfg.clip_k,
+                             cfg.clip_v)
+                del k, v
+            torch.cuda.synchronize()
+            build_s = time.time() - t0
+
+            def step_v():
+                ok.decode_step(vlay, vpool, new_k, new_v, new_slots_t, cfg.clip_k, cfg.clip_v, q,
+                               bt, sl, Rk, vRv, cfg.sm_scale, S, ws, out)
+
+            for _ in range(args.warmup):
+                step_v()
+            t_settle = time.perf_counter()
+            while (time.perf_counter() - t_settle) * 1e3 < args.settle_ms:
+                for _ in range(20):
+                    step_v()
+                torch.cuda.synchronize()
+            v_wall_us, v_ev_us = timed(step_v)
+            vbytes = step_bytes - (0 if use_rv else 2 * d * d * 4)  # no R_v reads (append, reduce)
+            res["variants"][vname] = {
+                "clip_mode": "token_quantile" if clip_mode else "group_absmax",
+                "meta_dtype": "bf16" if meta else "f16", "R_v": "given" if use_rv else "identity",
+                "us_per_step": round(v_wall_us, 2), "us_per_step_events": round(v_ev_us, 2),
+                "GBps": round(vbytes / (v_wall_us * 1e-6) / 1e9, 1),
+                "frac_of_peak": round(vbytes / (v_wall_us * 1e-6) / 1e9 / HBM_PEAK_GBS, 4),
+                "cache_build_s": round(build_s, 2),
+            }
+            del vpool
+            torch.cuda.empty_cache()
 
     # ---- bf16 paged-decode baseline on the same sequences ----
     if bf_pool is not None:
