@@ -21,7 +21,8 @@ workload.  `bf16_baseline` is the bf16 paged-decode kernel on the same
 sequences.  `mixed_cache_step` is oscar_decode_step_mixed on the same sequences
 with a bf16 sink of 64 and a bf16 window of 256 tokens around the INT2 history.
 `variants` times the same step with the cache in other quantizer formats: the
-paper's stated one (bf16 scale/zero, per-token quantile clip) and identity R_V.
+paper's stated one (128-channel groups, bf16 scale/zero, per-token quantile clip)
+and identity R_V.
 """
 from __future__ import annotations
 
@@ -391,11 +392,11 @@ def main():
         del pool  # the INT2 pool of the main step is no longer needed
         torch.cuda.empty_cache()
         res["variants"] = {}
-        for vname, (clip_mode, meta, use_rv) in {
-                "paper_format": (ok.CLIP_TOKEN_QUANTILE, ok.META_BF16, True),
-                "identity_v": (ok.CLIP_GROUP_ABSMAX, ok.META_F16, False)}.items():
-            vlay = ok.Layout(num_kv_heads=Hkv, num_pages=num_pages, clip_mode=clip_mode,
-                             meta_dtype=meta)
+        for vname, (clip_mode, meta, use_rv, G) in {
+                "paper_format": (ok.CLIP_TOKEN_QUANTILE, ok.META_BF16, True, 128),
+                "identity_v": (ok.CLIP_GROUP_ABSMAX, ok.META_F16, False, 32)}.items():
+            vlay = ok.Layout(num_kv_heads=Hkv, num_pages=num_pages, group_size=G,
+                             clip_mode=clip_mode, meta_dtype=meta)
             vRv = Rv if use_rv else None
             vpool = ok.alloc_pool(vlay)
             t0 = time.time()
@@ -421,10 +422,16 @@ def main():
                     step_v()
                 torch.cuda.synchronize()
             v_wall_us, v_ev_us = timed(step_v)
-            vbytes = step_bytes - (0 if use_rv else 2 * d * d * 4)  # no R_v reads (append, reduce)
+            # per token-head: 64 B of codes + 2 (128 / G) (s, z) entries of 4 B; no R_v
+            # reads (update, reduce) without R_v
+            tok_b = 64 + 2 * (d // G) * 4
+            vbytes = (step_bytes - kv_bytes + int(lens.sum()) * Hkv * tok_b
+                      - B * Hkv * (INT2_BYTES_PER_TOKEN_HEAD - tok_b)
+                      - (0 if use_rv else 2 * d * d * 4))
             res["variants"][vname] = {
                 "clip_mode": "token_quantile" if clip_mode else "group_absmax",
                 "meta_dtype": "bf16" if meta else "f16", "R_v": "given" if use_rv else "identity",
+                "group_size": G, "bytes_per_token_head": tok_b, "step_bytes": vbytes,
                 "us_per_step": round(v_wall_us, 2), "us_per_step_events": round(v_ev_us, 2),
                 "GBps": round(vbytes / (v_wall_us * 1e-6) / 1e9, 1),
                 "frac_of_peak": round(vbytes / (v_wall_us * 1e-6) / 1e9 / HBM_PEAK_GBS, 4),

@@ -33,7 +33,7 @@
  *   - A rotation matrix argument (R_k, R_v) may be NULL: the identity, e.g.
  *     R_V absorbed into the value and output projections (Sec. 4 "KV Cache
  *     Update").  The same choice must be used for the cache update and decode.
- *   - Supported shapes: head_dim 128, page_size 64, group_size 32.  Other values
+ *   - Supported shapes: head_dim 128, page_size 64, group_size 32, 64 or 128.  Other values
  *     return OSCAR_ERR_UNSUPPORTED; an unknown clip_mode or meta_dtype returns
  *     OSCAR_ERR_INVALID_ARG.
  *

@@ -77,12 +77,9 @@ struct QOut {
   uint16_t s16, z16;
 };
 
-// Clip at +-tau and quantize one channel value x of a group spread over a half wave.
-__device__ inline QOut quantize(float x, float tau, const QFmt& fmt) {
+// Quantize one clipped channel value y of a group with minimum a and maximum b.
+__device__ inline QOut quantize(float y, float a, float b, const QFmt& fmt) {
   QOut o;
-  const float y = fminf(fmaxf(x, -tau), tau);
-  const float a = half_wave_min(y);
-  const float b = half_wave_max(y);
   const float s = __fdiv_rn(__fsub_rn(b, a), 3.0f);
   uint16_t s16 = meta_store(fmt, s);
   if ((s16 & 0x7fffu) == 0) {
@@ -376,6 +373,37 @@ struct StepRows {
 // Clip, quantize, pack and write one rotated row (token, head) whose channels l
 // and l + 64 are in lane l, to pool slot `slot` (wave-uniform; < 0: the row only
 // takes part in the cross-lane steps).
+// Group reductions of the one-row-per-wave layout (lane l: channels l, l + 64):
+// with 32-channel groups each value's group is a wave half, with 64 its whole
+// wave, with 128 both values over the wave.
+__device__ inline float wave_max(float x) {
+  x = half_wave_max(x);
+  const uint32_t u = __float_as_uint(x);
+  const auto sw = __builtin_amdgcn_permlane32_swap(u, u, false, false);
+  return fmaxf(__uint_as_float(sw[0]), __uint_as_float(sw[1]));
+}
+__device__ inline float wave_min(float x) {
+  x = half_wave_min(x);
+  const uint32_t u = __float_as_uint(x);
+  const auto sw = __builtin_amdgcn_permlane32_swap(u, u, false, false);
+  return fminf(__uint_as_float(sw[0]), __uint_as_float(sw[1]));
+}
+template <bool MAX>
+__device__ inline void group_reduce2(float v0, float v1, int ng, float& r0, float& r1) {
+  auto op = [](float a, float b) { return MAX ? fmaxf(a, b) : fminf(a, b); };
+  auto half = [](float x) { return MAX ? half_wave_max(x) : half_wave_min(x); };
+  auto wave = [](float x) { return MAX ? wave_max(x) : wave_min(x); };
+  if (ng == 4) {
+    r0 = half(v0);
+    r1 = half(v1);
+  } else if (ng == 2) {
+    r0 = wave(v0);
+    r1 = wave(v1);
+  } else {
+    r0 = r1 = wave(op(v0, v1));
+  }
+}
+
 __device__ inline void store_row(uint8_t* __restrict__ pages, int Hkv, int64_t slot, int row,
                                  int is_v, float clip, const QFmt& fmt, double acc0, double acc1,
                                  int l) {
@@ -385,18 +413,23 @@ __device__ inline void store_row(uint8_t* __restrict__ pages, int Hkv, int64_t s
   if (fmt.quantile) {
     tau0 = tau1 = token_quantile_wave(xt0, xt1, clip);
   } else {
-    tau0 = __fmul_rn(clip, half_wave_max(fabsf(xt0)));
-    tau1 = __fmul_rn(clip, half_wave_max(fabsf(xt1)));
+    group_reduce2<true>(fabsf(xt0), fabsf(xt1), fmt.ng, tau0, tau1);
+    tau0 = __fmul_rn(clip, tau0);
+    tau1 = __fmul_rn(clip, tau1);
   }
-  const QOut q0 = quantize(xt0, tau0, fmt);
-  const QOut q1 = quantize(xt1, tau1, fmt);
+  const float y0 = fminf(fmaxf(xt0, -tau0), tau0), y1 = fminf(fmaxf(xt1, -tau1), tau1);
+  float a0, a1, b0, b1;
+  group_reduce2<false>(y0, y1, fmt.ng, a0, a1);
+  group_reduce2<true>(y0, y1, fmt.ng, b0, b1);
+  const QOut q0 = quantize(y0, a0, b0, fmt);
+  const QOut q1 = quantize(y1, a1, b1, fmt);
   const uint32_t byte0 = pack_quad(q0.code, l);  // quad l/4
   const uint32_t byte1 = pack_quad(q1.code, l);  // quad 16 + l/4
   if (slot < 0) return;                          // uniform across the wave
   const int h = row % Hkv;
   const int64_t page = slot / kP;
   const int t = (int)(slot - page * kP);
-  uint8_t* blk = pages + ((size_t)page * Hkv + h) * kBlockBytes;
+  uint8_t* blk = pages + ((size_t)page * Hkv + h) * block_bytes(fmt.ng);
   if ((l & 3) == 0) {
     const int j0 = l >> 2, j1 = 16 + (l >> 2);
     if (is_v) {
@@ -407,13 +440,18 @@ __device__ inline void store_row(uint8_t* __restrict__ pages, int Hkv, int64_t s
       blk[kOffKCodes + t * (kD / 4) + j1] = (uint8_t)byte1;
     }
   }
-  if ((l & 31) == 0) {
-    const uint32_t sz_base = is_v ? kOffVSz : kOffKSz;
-    const int g0 = l >> 5, g1 = 2 + (l >> 5);
+  // (s, z) of the groups: value 0 of lane l is in group l / 32 (G = 32) or 0,
+  // value 1 in group 2 + l / 32 (G = 32), 1 (G = 64) or 0 (G = 128)
+  const uint32_t sz_base = is_v ? off_vsz(fmt.ng) : kOffKSz;
+  const bool lead = fmt.ng == 4 ? (l & 31) == 0 : l == 0;
+  if (lead) {
+    const int g0 = fmt.ng == 4 ? l >> 5 : 0;
+    const int g1 = fmt.ng == 4 ? 2 + (l >> 5) : fmt.ng == 2 ? 1 : -1;
     *reinterpret_cast<uint32_t*>(blk + sz_base + (g0 * kP + t) * 4) =
         (uint32_t)q0.s16 | ((uint32_t)q0.z16 << 16);
-    *reinterpret_cast<uint32_t*>(blk + sz_base + (g1 * kP + t) * 4) =
-        (uint32_t)q1.s16 | ((uint32_t)q1.z16 << 16);
+    if (g1 >= 0)
+      *reinterpret_cast<uint32_t*>(blk + sz_base + (g1 * kP + t) * 4) =
+          (uint32_t)q1.s16 | ((uint32_t)q1.z16 << 16);
   }
 }
 
@@ -523,27 +561,53 @@ __device__ inline void store_row4(uint8_t* __restrict__ pages, int Hkv, int64_t 
   float xt[4];
 #pragma unroll
   for (int q = 0; q < 4; ++q) xt[q] = __double2float_rn(acc[q]);
+  // group reductions of the two-rows-per-wave layout (lane l' of a half: channels
+  // l' + 32 q of its row): values q of one group over the half
+  auto reduce4 = [&](auto op, auto half_red, const float (&v)[4], float (&r)[4]) {
+    if (fmt.ng == 4) {
+#pragma unroll
+      for (int q = 0; q < 4; ++q) r[q] = half_red(v[q]);
+    } else if (fmt.ng == 2) {
+      r[0] = r[1] = half_red(op(v[0], v[1]));
+      r[2] = r[3] = half_red(op(v[2], v[3]));
+    } else {
+      r[0] = r[1] = r[2] = r[3] = half_red(op(op(v[0], v[1]), op(v[2], v[3])));
+    }
+  };
+  auto fmax_ = [](float a, float b) { return fmaxf(a, b); };
+  auto fmin_ = [](float a, float b) { return fminf(a, b); };
+  auto hmax = [](float x) { return half_wave_max(x); };
+  auto hmin = [](float x) { return half_wave_min(x); };
   float tau[4];
   if (fmt.quantile) {
     const float t = token_quantile_halves(xt, clip, half);
 #pragma unroll
     for (int q = 0; q < 4; ++q) tau[q] = t;
   } else {
+    float ax[4];
 #pragma unroll
-    for (int q = 0; q < 4; ++q) tau[q] = __fmul_rn(clip, half_wave_max(fabsf(xt[q])));
+    for (int q = 0; q < 4; ++q) ax[q] = fabsf(xt[q]);
+    reduce4(fmax_, hmax, ax, tau);
+#pragma unroll
+    for (int q = 0; q < 4; ++q) tau[q] = __fmul_rn(clip, tau[q]);
   }
+  float y[4], ga[4], gb[4];
+#pragma unroll
+  for (int q = 0; q < 4; ++q) y[q] = fminf(fmaxf(xt[q], -tau[q]), tau[q]);
+  reduce4(fmin_, hmin, y, ga);
+  reduce4(fmax_, hmax, y, gb);
   QOut qo[4];
   uint32_t byte[4];
 #pragma unroll
   for (int q = 0; q < 4; ++q) {
-    qo[q] = quantize(xt[q], tau[q], fmt);  // group q of the row
-    byte[q] = pack_quad(qo[q].code, lp);   // quad 8 q + l'/4
+    qo[q] = quantize(y[q], ga[q], gb[q], fmt);  // 32-channel slice q of the row
+    byte[q] = pack_quad(qo[q].code, lp);         // quad 8 q + l'/4
   }
   if (slot < 0) return;
   const int h = row % Hkv;
   const int64_t page = slot / kP;
   const int t = (int)(slot - page * kP);
-  uint8_t* blk = pages + ((size_t)page * Hkv + h) * kBlockBytes;
+  uint8_t* blk = pages + ((size_t)page * Hkv + h) * block_bytes(fmt.ng);
   if ((lp & 3) == 0) {
 #pragma unroll
     for (int q = 0; q < 4; ++q) {
@@ -552,12 +616,15 @@ __device__ inline void store_row4(uint8_t* __restrict__ pages, int Hkv, int64_t 
       else blk[kOffKCodes + t * (kD / 4) + j] = (uint8_t)byte[q];
     }
   }
-  if (lp == 0) {
-    const uint32_t sz_base = is_v ? kOffVSz : kOffKSz;
+  if (lp == 0) {  // group g holds the slices q = g (4 / ng) .. (g + 1) (4 / ng) - 1
+    const uint32_t sz_base = is_v ? off_vsz(fmt.ng) : kOffKSz;
 #pragma unroll
-    for (int q = 0; q < 4; ++q)
-      *reinterpret_cast<uint32_t*>(blk + sz_base + (q * kP + t) * 4) =
+    for (int g = 0; g < 4; ++g) {
+      if (g >= fmt.ng) break;
+      const int q = g * (4 / fmt.ng);
+      *reinterpret_cast<uint32_t*>(blk + sz_base + (g * kP + t) * 4) =
           (uint32_t)qo[q].s16 | ((uint32_t)qo[q].z16 << 16);
+    }
   }
 }
 

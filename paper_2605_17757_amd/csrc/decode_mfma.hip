@@ -46,6 +46,7 @@
 #include <hip/hip_fp16.h>
 
 #include <algorithm>
+#include <type_traits>
 
 #include "internal.h"
 
@@ -196,7 +197,7 @@ struct WaveLds {
   float4 p[4][17];      // softmax weights of the page, [head][token / 4] (pitch 17)
   float2 hs[4];         // (alpha, p_max) per head
   float ws[16];         // P.V scale per (head, group); at the end, sum w z per (head, group)
-  float qs[16];         // sum of q_int per (head, group)
+  int qs[16];           // sum of q_int per (head, 32-channel slice)
   float sq[4];          // q scale per head
 };
 
@@ -206,15 +207,20 @@ struct Stage {  // chunks 64 i + lane of the next page, i = 0..5
   u4 v0, v1, v2, v3, v4, v5;
 };
 
+// A page-head block has 256 + 32 NG chunks of 16 bytes (NG groups per head): the
+// codes, then 16 NG chunks of K (s, z) and 16 NG of V (s, z).  Chunks past the
+// block are not loaded.
+template <int NG>
 __device__ inline void stage_load(Stage& s, const uint8_t* __restrict__ blk, int l) {
   const u4* src = reinterpret_cast<const u4*>(blk) + l;
   s.v0 = src[0];
   s.v1 = src[64];
   s.v2 = src[128];
   s.v3 = src[192];
-  s.v4 = src[256];
-  s.v5 = src[320];
+  if (NG >= 2 || l < 32) s.v4 = src[256];
+  if (NG == 4) s.v5 = src[320];
 }
+template <int NG>
 __device__ inline void stage_store(uint4* page, const Stage& s, int l) {
   u4* dst = reinterpret_cast<u4*>(page);
   const int a = l + (l >> 3);                  // K codes
@@ -223,8 +229,15 @@ __device__ inline void stage_store(uint4* page, const Stage& s, int l) {
   dst[72 + a] = s.v1;
   dst[kSlotVCodes + v] = s.v2;
   dst[kSlotVCodes + 64 + v] = s.v3;
-  dst[kSlotKSz + l] = s.v4;
-  dst[kSlotVSz + l + (l >> 4)] = s.v5;
+  if (NG == 4) {
+    dst[kSlotKSz + l] = s.v4;
+    dst[kSlotVSz + l + (l >> 4)] = s.v5;
+  } else if (NG == 2) {  // chunk 256 + l: K (s, z) for l < 32, V (s, z) chunk l - 32 after
+    const int c = l - 32;
+    dst[l < 32 ? kSlotKSz + l : kSlotVSz + c + (c >> 4)] = s.v4;
+  } else if (l < 32) {   // chunk 256 + l: K (s, z) for l < 16, V (s, z) chunk l - 16
+    dst[l < 16 ? kSlotKSz + l : kSlotVSz + l - 16] = s.v4;
+  }
 }
 
 struct WaveState {
@@ -239,20 +252,23 @@ struct WaveState {
 
 // FULL: all 64 token slots of the page are read; otherwise only slots in
 // [t0, t1) (the partial first or last page of a token range).
-template <bool FULL, bool BF>
+// NG groups of 128 / NG channels per head: a group spans 4 / NG of the 32-channel
+// slices that the MFMA tiles use, which share its (s, z) and its P.V weights.
+template <bool FULL, bool BF, int NG>
 __device__ inline void compute_page(WaveState& st, WaveLds& L, int t0, int t1, int lo, int hi) {
   char* pb = reinterpret_cast<char*>(L.page);
   // ---- scores of head hi for tokens 4*lo + u ----
   // code dword 2g + (hi>>1) of token 4*lo + u at byte 32u + 8g from the lane base
   const uint32_t* kc = reinterpret_cast<const uint32_t*>(pb + kLdsKCodes + 144 * lo + 4 * (hi >> 1));
   const uint32_t sh4 = 4u * (uint32_t)(hi & 1);
-  uint4 ksz[4];  // (s, z) of tokens 4*lo + (0..3), group i
+  uint4 ksz[NG];  // (s, z) of tokens 4*lo + (0..3), group i
 #pragma unroll
-  for (int i = 0; i < 4; ++i) ksz[i] = *reinterpret_cast<const uint4*>(pb + kLdsKSz + 256 * i + 16 * lo);
+  for (int i = 0; i < NG; ++i) ksz[i] = *reinterpret_cast<const uint4*>(pb + kLdsKSz + 256 * i + 16 * lo);
   float S[4];
 #pragma unroll
   for (int u = 0; u < 4; ++u) {
     float acc = 0.0f;
+    int tg[4];
 #pragma unroll
     for (int g = 0; g < 4; ++g) {
       const uint32_t y = kc[8 * u + 2 * g] >> sh4;  // fields 2(hi&1), 2(hi&1)+1 of each byte
@@ -260,9 +276,24 @@ __device__ inline void compute_page(WaveState& st, WaveLds& L, int t0, int t1, i
       const long b = (long)((uint64_t)(y & msk) | ((uint64_t)((y >> 2) & msk) << 32));
       const v4i d = mfma32(st.aq[g], b);
       const int t = combine3(d[0], d[1], d[2]);
-      const uint32_t sz = comp(ksz[g], u);
-      // s * (acc - z * sum q_int) with s, z read from the packed pair
-      acc = sz_s_fma<BF>(sz, sz_nz_fma<BF>(sz, st.qs[g], (float)t), acc);
+      if (NG == 4) {
+        const uint32_t sz = comp(ksz[g], u);
+        // s * (acc - z * sum q_int) with s, z read from the packed pair
+        acc = sz_s_fma<BF>(sz, sz_nz_fma<BF>(sz, st.qs[g], (float)t), acc);
+      } else {
+        tg[g] = t;
+      }
+    }
+    if (NG == 2) {  // slices of a group added in int32 (|sum| < 2^31)
+#pragma unroll
+      for (int j = 0; j < 2; ++j) {
+        const uint32_t sz = comp(ksz[j], u);
+        acc = sz_s_fma<BF>(sz, sz_nz_fma<BF>(sz, st.qs[j], (float)(tg[2 * j] + tg[2 * j + 1])), acc);
+      }
+    } else if (NG == 1) {  // four slices: two int32 pair sums, added in fp32
+      const uint32_t sz = comp(ksz[0], u);
+      const float T = (float)(tg[0] + tg[1]) + (float)(tg[2] + tg[3]);
+      acc = sz_s_fma<BF>(sz, sz_nz_fma<BF>(sz, st.qs[0], T), 0.0f);
     }
     S[u] = acc;
   }
@@ -305,6 +336,7 @@ __device__ inline void compute_page(WaveState& st, WaveLds& L, int t0, int t1, i
   for (int e = 0; e < 16; ++e) {
     sz[e] = comp(vz[e >> 2], e & 3);
     if (!FULL && (16 * hi + e < t0 || 16 * hi + e >= t1)) sz[e] = 0u;  // (0, 0): w = 0, z = 0
+    if (NG < 4 && wg >= NG) sz[e] = 0u;  // no such group: lanes idle
   }
   // largest V scale of the group on this page: scales are positive binary16 or
   // bfloat16, so their bit patterns order like their values (high halves, the
@@ -341,7 +373,7 @@ __device__ inline void compute_page(WaveState& st, WaveLds& L, int t0, int t1, i
     aw[0][j] = __builtin_amdgcn_perm(h23, h01, 0x05040100u);
   }
   st.zacc = fmaf(st.zacc, hsw.x, zp);
-  {  // digit operands to LDS: group wg, rows 3*wh + digit, k-group hi
+  if (NG == 4 || wg < NG) {  // digit operands to LDS: group wg, rows 3*wh + digit, k-group hi
     char* wp = pb + 16 * (w_base(wg) + w_slot(wh, hi));
 #pragma unroll
     for (int dg = 0; dg < kNDig; ++dg)
@@ -359,7 +391,7 @@ __device__ inline void compute_page(WaveState& st, WaveLds& L, int t0, int t1, i
   const char* ab = pb + 16 * (w_slot(lo >> 2, hi) + min(lo & 3, 2));
 #pragma unroll
   for (int G = 0; G < 4; ++G) {
-    const uint4 a4 = *reinterpret_cast<const uint4*>(ab + 16 * w_base(G));
+    const uint4 a4 = *reinterpret_cast<const uint4*>(ab + 16 * w_base(G * NG / 4));  // its group's digits
     const v4i aop = {(int)a4.x, (int)a4.y, (int)a4.z, (int)a4.w};
     const uint4 x = *reinterpret_cast<const uint4*>(vb + 512 * G);  // quad 8G + (lo&7)
 #pragma unroll
@@ -369,7 +401,7 @@ __device__ inline void compute_page(WaveState& st, WaveLds& L, int t0, int t1, i
       const v4i d = mfma64(aop, bv);
       const int t = combine3(d[0], d[1], d[2]);
       float& o = st.of[2 * G + F];
-      o = fmaf((float)t, compf(ws, G), o * alpha);
+      o = fmaf((float)t, compf(ws, G * NG / 4), o * alpha);
     }
   }
 }
@@ -397,7 +429,7 @@ __device__ inline TokRange tok_range(int lo, int hi) {
 // piece + 1 .. num_splits - 1 are marked empty.  The wave has done `done0` of its
 // `total` pages before this piece (issue-priority bands).  Without MIXED the
 // range starts at token 0 (R.t0 = 0).
-template <bool MIXED, bool BF>
+template <bool MIXED, bool BF, int NG>
 __device__ __attribute__((always_inline)) inline void process_piece(WaveLds& L, const uint8_t* __restrict__ pages, int Hkv, int Hq,
                                      const int32_t* __restrict__ block_table, int max_pages, int b,
                                      TokRange R, int kvh, int chunk, int p0, int p1, int piece,
@@ -409,8 +441,8 @@ __device__ __attribute__((always_inline)) inline void process_piece(WaveLds& L, 
   const int l = threadIdx.x, lo = l & 15, hi = l >> 4;
   const int npg = R.npg;
   const int32_t* __restrict__ bt = block_table + (size_t)b * max_pages + (MIXED ? R.first : 0);
-  const uint8_t* __restrict__ base = pages + (size_t)kvh * kBlockBytes;
-  const size_t page_stride = (size_t)Hkv * kBlockBytes;
+  const uint8_t* __restrict__ base = pages + (size_t)kvh * block_bytes(NG);
+  const size_t page_stride = (size_t)Hkv * block_bytes(NG);
 
   WaveState st;
   // ---- query operands: q_int = rne(q~ * Q / max|q~|), three int8 digits ----
@@ -443,7 +475,7 @@ __device__ __attribute__((always_inline)) inline void process_piece(WaveLds& L, 
     amax = rows_max(amax);  // all 128 channels of the head (k-groups hi)
     const float inv = amax > 0.0f ? kQMax / amax : 0.0f;
     const float sq = amax > 0.0f ? amax * (1.0f / kQMax) : 1.0f;
-    float qsum[4];
+    int qsum[4];
 #pragma unroll
     for (int g = 0; g < 4; ++g) {
       int sum = 0;
@@ -464,12 +496,20 @@ __device__ __attribute__((always_inline)) inline void process_piece(WaveLds& L, 
       // sum over the group's 32 channels (k-groups hi), exact in int
       sum += __shfl_xor(sum, 16, 64);
       sum += __shfl_xor(sum, 32, 64);
-      qsum[g] = (float)sum;
+      qsum[g] = sum;
     }
     L.qs[lo] = dsel == 0 ? qsum[0] : dsel == 1 ? qsum[1] : dsel == 2 ? qsum[2] : qsum[3];  // (head h, group dsel)
     L.sq[h] = sq;  // lanes of equal h write equal values
-    const float4 q4 = *reinterpret_cast<const float4*>(&L.qs[4 * hi]);
-    st.qs[0] = q4.x; st.qs[1] = q4.y; st.qs[2] = q4.z; st.qs[3] = q4.w;
+    const int4 q4 = *reinterpret_cast<const int4*>(&L.qs[4 * hi]);
+    if (NG == 4) {
+      st.qs[0] = (float)q4.x; st.qs[1] = (float)q4.y; st.qs[2] = (float)q4.z; st.qs[3] = (float)q4.w;
+    } else if (NG == 2) {  // sums over the group's slices, in int32 (|sum| < 2^31)
+      st.qs[0] = (float)(q4.x + q4.y); st.qs[1] = (float)(q4.z + q4.w);
+      st.qs[2] = st.qs[3] = 0.0f;
+    } else {
+      st.qs[0] = (float)(q4.x + q4.y + q4.z + q4.w);
+      st.qs[1] = st.qs[2] = st.qs[3] = 0.0f;
+    }
     st.sq = L.sq[hi];
     st.m = -INFINITY;
     st.lsum = 0.0f;
@@ -483,14 +523,14 @@ __device__ __attribute__((always_inline)) inline void process_piece(WaveLds& L, 
   int cb = p0;
   int btv = (p0 + l < p1) ? bt[p0 + l] : 0;
   Stage sg;
-  if (p0 < p1) stage_load(sg, base + (size_t)__builtin_amdgcn_readlane(btv, 0) * page_stride, l);
+  if (p0 < p1) stage_load<NG>(sg, base + (size_t)__builtin_amdgcn_readlane(btv, 0) * page_stride, l);
   // pages [p0, pf) are full; page pf (if < p1) is the range's partial last page
   int pf = (p0 < p1 && p1 == npg && R.t1 != kP) ? p1 - 1 : p1;
   int pg = p0;
   if (MIXED && p0 == 0 && p0 < p1 && R.t0 != 0) {  // the range's partial first page
-    stage_store(L.page, sg, l);
-    stage_load(sg, base + (size_t)__builtin_amdgcn_readlane(btv, min(1, p1 - 1)) * page_stride, l);
-    compute_page<false, BF>(st, L, R.t0, npg == 1 ? R.t1 : kP, lo, hi);
+    stage_store<NG>(L.page, sg, l);
+    stage_load<NG>(sg, base + (size_t)__builtin_amdgcn_readlane(btv, min(1, p1 - 1)) * page_stride, l);
+    compute_page<false, BF, NG>(st, L, R.t0, npg == 1 ? R.t1 : kP, lo, hi);
     pg = 1;
     pf = max(pf, 1);  // a one-page range is done
   }
@@ -503,14 +543,14 @@ __device__ __attribute__((always_inline)) inline void process_piece(WaveLds& L, 
     const int lim = (int)(((int64_t)(25 * band) * total + 99) / 100) - done0 + p0;  // band end
     const int e = min(max(lim, pg), pf);
     for (; pg < e; ++pg) {
-      stage_store(L.page, sg, l);
+      stage_store<NG>(L.page, sg, l);
       const int nx = min(pg + 1, p1 - 1);  // page pg+1 (the last page again at the end)
       if (nx - cb >= 64) {                 // uniform: next 64 entries
         cb += 64;
         btv = (cb + l < p1) ? bt[cb + l] : 0;
       }
-      stage_load(sg, base + (size_t)__builtin_amdgcn_readlane(btv, nx - cb) * page_stride, l);
-      compute_page<true, BF>(st, L, 0, kP, lo, hi);
+      stage_load<NG>(sg, base + (size_t)__builtin_amdgcn_readlane(btv, nx - cb) * page_stride, l);
+      compute_page<true, BF, NG>(st, L, 0, kP, lo, hi);
     }
     if (band < 4 && lim > p0 && lim <= pf) {  // the band ended inside this piece
       if (band == 1) __builtin_amdgcn_s_setprio(2);
@@ -519,8 +559,8 @@ __device__ __attribute__((always_inline)) inline void process_piece(WaveLds& L, 
     }
   }
   if (pf < p1) {  // the partial last page; the stage holds it
-    stage_store(L.page, sg, l);
-    compute_page<false, BF>(st, L, 0, R.t1, lo, hi);
+    stage_store<NG>(L.page, sg, l);
+    compute_page<false, BF, NG>(st, L, 0, R.t1, lo, hi);
   }
 
   // ---- write the split's partial state ----
@@ -543,7 +583,7 @@ __device__ __attribute__((always_inline)) inline void process_piece(WaveLds& L, 
 #pragma unroll
     for (int F = 0; F < 2; ++F) {
       const int ch = 32 * G + 4 * (lo & 7) + 2 * F + (lo >> 3);
-      part_o[row * kD + ch] = empty ? 0.0f : fmaf(st.of[2 * G + F], cs, -compf(zh, G));
+      part_o[row * kD + ch] = empty ? 0.0f : fmaf(st.of[2 * G + F], cs, -compf(zh, G * NG / 4));
     }
   }
   if (lo == 0) {
@@ -574,7 +614,7 @@ __device__ inline int wave_sum_i(int x) {
   return x;
 }
 
-template <bool MIXED, bool BF>
+template <bool MIXED, bool BF, int NG>
 __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(4, 4))) void split_mfma_kernel(
     const uint8_t* __restrict__ pages, int Hkv, int Hq, const int32_t* __restrict__ block_table,
     int max_pages, const int32_t* __restrict__ seq_lens, int num_splits, int n_ranges, int B,
@@ -602,7 +642,7 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(4, 4))) void
   };
   if (num_splits == 1) {  // one range per sequence
     const TokRange R = range_of(r);
-    process_piece<MIXED, BF>(L, pages, Hkv, Hq, block_table, max_pages, r, R, kvh, chunk, 0, R.npg,
+    process_piece<MIXED, BF, NG>(L, pages, Hkv, Hq, block_table, max_pages, r, R, kvh, chunk, 0, R.npg,
                          0, true, 1, stride, qt, part_o, part_ml, 0, 1 << 20);
     return;
   }
@@ -657,7 +697,7 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(4, 4))) void
   while (true) {
     const int64_t end = min(xe, before + npg_b);
     const int piece = (int)(r - before / pw);
-    process_piece<MIXED, BF>(L, pages, Hkv, Hq, block_table, max_pages, b, range_of(b), kvh, chunk,
+    process_piece<MIXED, BF, NG>(L, pages, Hkv, Hq, block_table, max_pages, b, range_of(b), kvh, chunk,
                          (int)(x - before), (int)(end - before), piece, end == before + npg_b,
                          num_splits, stride, qt, part_o, part_ml, (int)(x - x0), (int)(xe - x0));
     x = end;
@@ -676,7 +716,8 @@ hipError_t launch_decode_split_mfma(const uint8_t* pages, int Hkv, int B, int Hq
                                     const int32_t* block_table, int max_pages,
                                     const int32_t* seq_lens, int num_splits, int resident_waves,
                                     const float* qt, float* part_o, float* part_ml,
-                                    hipStream_t st, int meta_bf16, const MixedSpec* mixed) {
+                                    hipStream_t st, int meta_bf16, int ng,
+                                    const MixedSpec* mixed) {
   const int g = Hq / Hkv;
   const int nch = (g + 3) / 4;
   // one range per resident wave group (each range runs Hkv * nch waves)
@@ -691,12 +732,20 @@ hipError_t launch_decode_split_mfma(const uint8_t* pages, int Hkv, int B, int Hq
                        block_table, max_pages, seq_lens, num_splits, (int)ranges, B, qt, part_o,
                        part_ml, S0, W, stride);
   };
+  auto by_ng = [&](auto mixed_c, auto bf_c) {
+    constexpr bool M = decltype(mixed_c)::value, BFV = decltype(bf_c)::value;
+    if (ng == 4) go(split_mfma_kernel<M, BFV, 4>);
+    else if (ng == 2) go(split_mfma_kernel<M, BFV, 2>);
+    else go(split_mfma_kernel<M, BFV, 1>);
+  };
+  using T = std::true_type;
+  using F = std::false_type;
   if (mixed) {
-    if (meta_bf16) go(split_mfma_kernel<true, true>);
-    else go(split_mfma_kernel<true, false>);
+    if (meta_bf16) by_ng(T{}, T{});
+    else by_ng(T{}, F{});
   } else {
-    if (meta_bf16) go(split_mfma_kernel<false, true>);
-    else go(split_mfma_kernel<false, false>);
+    if (meta_bf16) by_ng(F{}, T{});
+    else by_ng(F{}, F{});
   }
   return hipGetLastError();
 }

@@ -7,18 +7,19 @@
 
 namespace oscar {
 
-// Supported geometry: head dim 128, 64 token slots per page, 32-channel groups.
+// Supported geometry: head dim 128, 64 token slots per page, groups of 32, 64 or
+// 128 channels (ng = 128 / G = 4, 2 or 1 groups per head).
 constexpr int kD = 128;
 constexpr int kP = 64;
-constexpr int kG = 32;
-constexpr int kNG = kD / kG;                       // groups per head
+constexpr int kG = 32;                             // the default group size
 constexpr int kCodeBytes = kP * kD / 4;            // one code region of a page-head block
-constexpr int kSzBytes = kNG * kP * 4;             // one (scale, zero) region
-constexpr int kBlockBytes = 2 * kCodeBytes + 2 * kSzBytes;   // 6144
 constexpr int kOffKCodes = 0;
 constexpr int kOffVCodes = kCodeBytes;             // 2048
 constexpr int kOffKSz = 2 * kCodeBytes;            // 4096
-constexpr int kOffVSz = 2 * kCodeBytes + kSzBytes; // 5120
+// one (scale, zero) region, the V one's offset and the block size for ng groups
+__host__ __device__ constexpr int sz_bytes(int ng) { return ng * kP * 4; }
+__host__ __device__ constexpr int off_vsz(int ng) { return kOffKSz + sz_bytes(ng); }
+__host__ __device__ constexpr int block_bytes(int ng) { return 2 * kCodeBytes + 2 * sz_bytes(ng); }
 constexpr int kMaxGroupHeads = 16;                 // query heads per kv-head
 
 // Workspace carving for decode (byte offsets, 256-aligned).
@@ -48,6 +49,7 @@ struct MixedSpec {
 struct QuantFmt {
   int bf16;
   int quantile;
+  int ng;  // groups per head (128 / G)
 };
 
 // Kernel launchers (each returns the hipError_t of its launch).
@@ -87,19 +89,20 @@ hipError_t launch_seg_partial(const uint16_t* seg, int Hkv, int S0, int W, int B
                               float qscale, int num_splits, float* part_o, float* part_ml,
                               hipStream_t st);
 // mixed == nullptr: every token of a sequence is INT2 (rows of num_splits slots).
-// meta_bf16: scale and zero stored as bfloat16.
+// meta_bf16: scale and zero stored as bfloat16; ng: groups per head.
 hipError_t launch_decode_split(const uint8_t* pages, int Hkv, int B, int Hq,
                                const int32_t* block_table, int max_pages,
                                const int32_t* seq_lens, int num_splits, const float* qt,
                                float* part_o, float* part_ml, hipStream_t st, int meta_bf16,
-                               const MixedSpec* mixed = nullptr);
+                               int ng, const MixedSpec* mixed = nullptr);
 // Balanced split kernel: `resident_waves` waves share the pages equally; a
 // (sequence, head) row gets at most num_splits partial states.
 hipError_t launch_decode_split_mfma(const uint8_t* pages, int Hkv, int B, int Hq,
                                     const int32_t* block_table, int max_pages,
                                     const int32_t* seq_lens, int num_splits, int resident_waves,
                                     const float* qt, float* part_o, float* part_ml,
-                                    hipStream_t st, int meta_bf16, const MixedSpec* mixed);
+                                    hipStream_t st, int meta_bf16, int ng,
+                                    const MixedSpec* mixed);
 int device_cus();  // compute units of the current device (cached)
 // mixed != nullptr: rows of num_splits + 1 slots, the last one in the original
 // basis (added after the back-rotation).

@@ -42,7 +42,9 @@ int check_layout(const oscar_layout* L) {
   if (L->clip_mode != OSCAR_CLIP_GROUP_ABSMAX && L->clip_mode != OSCAR_CLIP_TOKEN_QUANTILE)
     return OSCAR_ERR_INVALID_ARG;
   if (L->meta_dtype != OSCAR_META_F16 && L->meta_dtype != OSCAR_META_BF16) return OSCAR_ERR_INVALID_ARG;
-  if (L->head_dim != kD || L->page_size != kP || L->group_size != kG) return OSCAR_ERR_UNSUPPORTED;
+  if (L->head_dim != kD || L->page_size != kP ||
+      (L->group_size != 32 && L->group_size != 64 && L->group_size != 128))
+    return OSCAR_ERR_UNSUPPORTED;
   if (L->num_kv_heads > 65535) return OSCAR_ERR_UNSUPPORTED;
   return OSCAR_OK;
 }
@@ -77,9 +79,10 @@ bool aligned(const void* p, size_t a) { return (reinterpret_cast<uintptr_t>(p) &
 
 QuantFmt quant_fmt(const oscar_layout* L) {
   return QuantFmt{L->meta_dtype == OSCAR_META_BF16 ? 1 : 0,
-                  L->clip_mode == OSCAR_CLIP_TOKEN_QUANTILE ? 1 : 0};
+                  L->clip_mode == OSCAR_CLIP_TOKEN_QUANTILE ? 1 : 0, kD / L->group_size};
 }
 int meta_bf16(const oscar_layout* L) { return L->meta_dtype == OSCAR_META_BF16 ? 1 : 0; }
+int groups(const oscar_layout* L) { return kD / L->group_size; }
 
 // Mixed cache: sink and window sizes (and B, for the segment store size).
 bool seg_ok(int32_t B, int32_t S0, int32_t W) {
@@ -192,7 +195,7 @@ int oscar_decode_split(const oscar_layout* L, const void* pages, int32_t B, int3
       static_cast<const uint8_t*>(pages), L->num_kv_heads, B, Hq, block_table, max_pages_per_seq,
       seq_lens, num_splits, reinterpret_cast<const float*>(base + ws.qt_off),
       reinterpret_cast<float*>(base + ws.po_off), reinterpret_cast<float*>(base + ws.pml_off),
-      static_cast<hipStream_t>(stream), meta_bf16(L)));
+      static_cast<hipStream_t>(stream), meta_bf16(L), groups(L)));
 }
 
 int oscar_decode_reduce(const oscar_layout* L, int32_t B, int32_t Hq, const float* R_v,
@@ -291,7 +294,7 @@ int oscar_decode_step(const oscar_layout* L, void* pages, const void* k_new, con
   st = hip_status(launch_decode_split(
       static_cast<const uint8_t*>(pages), L->num_kv_heads, B, Hq, block_table, max_pages_per_seq,
       seq_lens, num_splits, qt, reinterpret_cast<float*>(base + ws.po_off),
-      reinterpret_cast<float*>(base + ws.pml_off), hs, meta_bf16(L)));
+      reinterpret_cast<float*>(base + ws.pml_off), hs, meta_bf16(L), groups(L)));
   if (st) return st;
   return hip_status(launch_decode_reduce(B, Hq, num_splits,
                                          reinterpret_cast<const float*>(base + ws.po_off),
@@ -386,7 +389,7 @@ int launch_mixed_rest(const oscar_layout* L, const void* pages, const void* seg,
   int st = hip_status(launch_decode_split(static_cast<const uint8_t*>(pages), L->num_kv_heads, B,
                                           Hq, block_table, max_pages_per_seq, seq_lens,
                                           num_splits, reinterpret_cast<const float*>(base + ws.qt_off),
-                                          po, pml, hs, meta_bf16(L), &mx));
+                                          po, pml, hs, meta_bf16(L), groups(L), &mx));
   if (st) return st;
   st = hip_status(launch_seg_partial(static_cast<const uint16_t*>(seg), L->num_kv_heads, S0, W, B,
                                      Hq, seq_lens, max_pages_per_seq,

@@ -153,14 +153,15 @@ def row_near_boundary(xt: np.ndarray, rho: float, G: int = 32, meta: int = 0,
 
 
 def compare_pools(gpu_pool: np.ndarray, ora_pool: np.ndarray, case: Case, meta: int = 0,
-                  clip: int = 0):
+                  clip: int = 0, G: int = 32):
     """Returns (n_diff_bytes, n_tolerated_rows); raises AssertionError on any
     difference that the near-boundary rule does not cover."""
     diff = np.nonzero(gpu_pool != ora_pool)[0]
     if diff.size == 0:
         return 0, 0
     hkv = case.cfg.Hkv
-    bph = 6144
+    szb = (128 // G) * 64 * 4                      # one (s, z) region
+    bph = 4096 + 2 * szb
     slot_to_tok = {int(s): i for i, s in enumerate(case.slots)}
     bad_rows = set()
     for off in diff:
@@ -170,10 +171,10 @@ def compare_pools(gpu_pool: np.ndarray, ora_pool: np.ndarray, case: Case, meta: 
             t, is_v = inner // 32, 0
         elif inner < 4096:
             t, is_v = (inner - 2048) % 64, 1
-        elif inner < 5120:
+        elif inner < 4096 + szb:
             t, is_v = ((inner - 4096) // 4) % 64, 0
         else:
-            t, is_v = ((inner - 5120) // 4) % 64, 1
+            t, is_v = ((inner - 4096 - szb) // 4) % 64, 1
         bad_rows.add((page * 64 + t, h, is_v))
     untolerated = []
     for slot, h, is_v in sorted(bad_rows):
@@ -184,8 +185,8 @@ def compare_pools(gpu_pool: np.ndarray, ora_pool: np.ndarray, case: Case, meta: 
         src = case.v if is_v else case.k
         x = W.bf16_bits_to_f32(bits(src[i, h]))
         xt = oracle.rotate_row(x, case.Rv if is_v else case.Rk)
-        if not row_near_boundary(xt, case.cfg.clip_v if is_v else case.cfg.clip_k, meta=meta,
-                                 clip=clip):
+        if not row_near_boundary(xt, case.cfg.clip_v if is_v else case.cfg.clip_k, G=G,
+                                 meta=meta, clip=clip):
             untolerated.append((slot, h, is_v, "not near a rounding boundary"))
     assert not untolerated, "append mismatches: %s (first of %d rows)" % (untolerated[:5],
                                                                            len(untolerated))

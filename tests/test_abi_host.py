@@ -62,7 +62,13 @@ def test_layout_validation(L):
     assert ok.layout_check(ok.Layout(8, 0)) == ok.ERR_INVALID_ARG
     assert ok.layout_check(ok.Layout(8, 10, head_dim=64)) == ok.ERR_UNSUPPORTED
     assert ok.layout_check(ok.Layout(8, 10, page_size=16)) == ok.ERR_UNSUPPORTED
-    assert ok.layout_check(ok.Layout(8, 10, group_size=64)) == ok.ERR_UNSUPPORTED
+    assert ok.layout_check(ok.Layout(8, 10, group_size=64)) == ok.OK
+    assert ok.layout_check(ok.Layout(8, 10, group_size=128)) == ok.OK
+    assert ok.layout_check(ok.Layout(8, 10, group_size=16)) == ok.ERR_UNSUPPORTED
+    # block sizes follow the layout definition for every group size
+    for G in (32, 64, 128):
+        lay = ok.Layout(8, 10, group_size=G)
+        assert ok.page_bytes(lay) == 8 * oracle.page_head_bytes(128, 64, G) == 8 * (4096 + 2 * (128 // G) * 256)
     assert ok.layout_check(ok.Layout(8, 10, group_size=48)) == ok.ERR_INVALID_ARG   # G does not divide d
     assert L.oscar_layout_check(None) == ok.ERR_INVALID_ARG
     assert ok.page_bytes(ok.Layout(0, 10)) == 0

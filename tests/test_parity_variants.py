@@ -1,8 +1,9 @@
 """GPU parity of the quantizer variants (App. "Scale Determination and Per-token
 Clipping Details"; Sec. 4 "KV Cache Update") against the oracle, through the C
-ABI: bfloat16 scale/zero metadata, the per-token quantile clip threshold, the
-two together (the format the paper states), and identity rotations (R_V absorbed
-into the projection weights; no rotation at all).  Page bytes bit-exact (with
+ABI: bfloat16 scale/zero metadata, the per-token quantile clip threshold, groups
+of 64 and 128 channels, all three together (the format the paper states: G = 128,
+bf16 scale/zero, quantile clip), and identity rotations (R_V absorbed into the
+projection weights; no rotation at all).  Page bytes bit-exact (with
 the near-boundary rule of helpers.compare_pools, applied in the variant's own
 arithmetic); decode within 2e-3 on the fp32 output."""
 import numpy as np
@@ -16,28 +17,32 @@ from helpers import DECODE_TOL, Case, bits, compare_pools, log, max_abs
 
 pytestmark = pytest.mark.gpu
 
-D, P, G = 128, 64, 32
+D, P = 128, 64
 
-# name -> (meta_dtype, clip_mode, rotate K, rotate V)
+# name -> (meta_dtype, clip_mode, rotate K, rotate V, group size).  The paper's
+# stated format: groups of 128 channels, bf16 scale/zero, per-token quantile clip.
 VARIANTS = {
-    "bf16_meta": (1, 0, True, True),
-    "token_quantile": (0, 1, True, True),
-    "paper_format": (1, 1, True, True),
-    "identity_v": (0, 0, True, False),
-    "identity_kv_paper_format": (1, 1, False, False),
+    "bf16_meta": (1, 0, True, True, 32),
+    "token_quantile": (0, 1, True, True, 32),
+    "g64": (0, 0, True, True, 64),
+    "g128": (0, 0, True, True, 128),
+    "paper_format": (1, 1, True, True, 128),
+    "paper_format_g64": (1, 1, True, True, 64),
+    "identity_v": (0, 0, True, False, 32),
+    "identity_kv_paper_format": (1, 1, False, False, 128),
 }
 
 
 class VCase:
     def __init__(self, cfg: W.Config, variant: str):
         self.cfg = cfg
-        self.meta, self.clip, rk, rv = VARIANTS[variant]
+        self.meta, self.clip, rk, rv, self.G = VARIANTS[variant]
         Rk, Rv = W.rotations(cfg)
         self.Rk = Rk if rk else None
         self.Rv = Rv if rv else None
         self.table, self.num_pages = W.block_table(cfg)
-        self.lay = ok.Layout(num_kv_heads=cfg.Hkv, num_pages=self.num_pages, clip_mode=self.clip,
-                             meta_dtype=self.meta)
+        self.lay = ok.Layout(num_kv_heads=cfg.Hkv, num_pages=self.num_pages, group_size=self.G,
+                             clip_mode=self.clip, meta_dtype=self.meta)
         self.kv = [W.cache_kv(cfg, b) for b in range(cfg.B)]
         self.q = W.queries(cfg)
         self.Rk_d = None if self.Rk is None else torch.from_numpy(self.Rk).cuda()
@@ -66,13 +71,13 @@ class VCase:
     def oracle_append(self, upto):
         c = self.case(upto)
         pool = np.zeros(ok.pool_bytes(self.lay), np.uint8)
-        oracle.kv_append(pool, d=D, Hkv=self.cfg.Hkv, P=P, G=G, k=bits(c.k), v=bits(c.v),
+        oracle.kv_append(pool, d=D, Hkv=self.cfg.Hkv, P=P, G=self.G, k=bits(c.k), v=bits(c.v),
                          slot_mapping=c.slots, Rk=self.Rk, Rv=self.Rv, clip_k=self.cfg.clip_k,
                          clip_v=self.cfg.clip_v, meta=self.meta, clip=self.clip)
         return pool
 
     def oracle_decode(self, pool, lens):
-        return oracle.decode(pool, d=D, Hkv=self.cfg.Hkv, P=P, G=G, q=bits(self.q),
+        return oracle.decode(pool, d=D, Hkv=self.cfg.Hkv, P=P, G=self.G, q=bits(self.q),
                              block_table=self.table, seq_lens=np.asarray(lens, np.int32),
                              Rk=self.Rk, Rv=self.Rv, sm_scale=self.cfg.sm_scale, meta=self.meta)
 
@@ -88,7 +93,7 @@ class VCase:
 
     def compare(self, gpu_pool, ora_pool, upto):
         nd, nt = compare_pools(gpu_pool.cpu().numpy(), ora_pool, self.case(upto), meta=self.meta,
-                               clip=self.clip)
+                               clip=self.clip, G=self.G)
         log("  pool: differing bytes", nd, "tolerated near-boundary rows", nt)
 
 
@@ -116,7 +121,8 @@ def test_variant_append_and_decode_small(variant):
     assert torch.equal(outb.cpu(), vc.gpu_decode(pool, lens, 3).cpu().to(torch.bfloat16))
 
 
-@pytest.mark.parametrize("variant", ["token_quantile", "paper_format", "identity_kv_paper_format"])
+@pytest.mark.parametrize("variant", ["token_quantile", "g64", "paper_format",
+                                     "identity_kv_paper_format"])
 def test_variant_bulk_append_qwen3_4b_shape(variant):
     """8192 tokens x 8 KV heads: the bulk cache update (two rows per wave, the
     quantile searched per wave half)."""
@@ -131,7 +137,7 @@ def test_variant_bulk_append_qwen3_4b_shape(variant):
     assert err <= DECODE_TOL
 
 
-@pytest.mark.parametrize("variant", ["paper_format", "identity_v"])
+@pytest.mark.parametrize("variant", ["paper_format", "g64", "identity_v"])
 def test_variant_decode_step(variant):
     """oscar_decode_step (cache update of the newest token + decode) in the variant
     format equals the oracle's append of every token + decode."""
@@ -158,7 +164,8 @@ def test_variant_decode_step(variant):
 
 def test_variant_mixed_cache_paper_format():
     """The mixed-precision cache in the paper's format: bf16 sink 64 and window 256
-    around an INT2 history with bf16 metadata and the per-token quantile clip;
+    around an INT2 history with 128-channel groups, bf16 metadata and the
+    per-token quantile clip;
     prompt by oscar_mixed_append, newest token by oscar_decode_step_mixed (with
     demotion), against the oracle's one-token-per-step loop."""
     S0, W_ = 64, 256
@@ -191,7 +198,7 @@ def test_variant_mixed_cache_paper_format():
     for b in range(cfg.B):
         kb, vb = bits(vc.kv[b][0]), bits(vc.kv[b][1])
         for n in range(1, int(lens[b]) + 1):
-            oracle.mixed_update(ora, oseg[b * chunk:(b + 1) * chunk], d=D, Hkv=cfg.Hkv, P=P, G=G,
+            oracle.mixed_update(ora, oseg[b * chunk:(b + 1) * chunk], d=D, Hkv=cfg.Hkv, P=P, G=vc.G,
                                 S0=S0, W=W_, k_new=kb[n - 1:n], v_new=vb[n - 1:n],
                                 block_table=vc.table[b:b + 1], seq_lens=np.array([n], np.int32),
                                 Rk=vc.Rk, Rv=vc.Rv, clip_k=cfg.clip_k, clip_v=cfg.clip_v,
@@ -202,11 +209,11 @@ def test_variant_mixed_cache_paper_format():
     sl = np.concatenate([W.slots_for(vc.table, b, np.arange(lo, hi)) for b, (lo, hi) in enumerate(hist)])
     nd, nt = compare_pools(pool.cpu().numpy(), ora,
                            Case(cfg, vc.Rk, vc.Rv, vc.table, vc.num_pages, vc.q, ks, vs, sl),
-                           meta=vc.meta, clip=vc.clip)
+                           meta=vc.meta, clip=vc.clip, G=vc.G)
     log("  pool: differing bytes", nd, "tolerated", nt)
     gseg = seg.cpu().contiguous().view(torch.int16).numpy().view(np.uint16).reshape(-1)
     assert np.array_equal(gseg, oseg)
-    ref = oracle.decode_mixed(ora, oseg, d=D, Hkv=cfg.Hkv, P=P, G=G, S0=S0, W=W_, q=bits(vc.q),
+    ref = oracle.decode_mixed(ora, oseg, d=D, Hkv=cfg.Hkv, P=P, G=vc.G, S0=S0, W=W_, q=bits(vc.q),
                               block_table=vc.table, seq_lens=lens, Rk=vc.Rk, Rv=vc.Rv,
                               sm_scale=cfg.sm_scale, meta=vc.meta)
     err = max_abs(out, ref)
@@ -219,11 +226,12 @@ def test_variant_full_size_bench_workload_paper_format():
     format, as bench.py runs it (cache of tokens 0..n-2, one oscar_decode_step),
     sampled sequences against the oracle."""
     cfg = W.config(2, batch=64)
-    meta, clip = 1, 1
+    meta, clip, G = 1, 1, 128
     B, Hq, Hkv = cfg.B, cfg.Hq, cfg.Hkv
     lens = cfg.lens.astype(np.int64)
     table, num_pages = W.block_table(cfg)
-    lay = ok.Layout(num_kv_heads=Hkv, num_pages=num_pages, clip_mode=clip, meta_dtype=meta)
+    lay = ok.Layout(num_kv_heads=Hkv, num_pages=num_pages, group_size=G, clip_mode=clip,
+                    meta_dtype=meta)
     Rk_np, Rv_np = W.rotations(cfg)
     Rk, Rv = torch.from_numpy(Rk_np).cuda(), torch.from_numpy(Rv_np).cuda()
     sample = sorted({0, int(np.argmax(lens)), int(np.argmin(lens))})
@@ -278,5 +286,5 @@ def test_variant_full_size_bench_workload_paper_format():
         gpu_sel.reshape(num_pages, bph)[ids] = pool_pages[torch.from_numpy(ids).cuda()].cpu().numpy()
     nd, nt = compare_pools(gpu_sel, ora, Case(cfg, Rk_np, Rv_np, table, num_pages, q,
                                               torch.cat(ks), torch.cat(vs), np.concatenate(ss)),
-                           meta=meta, clip=clip)
+                           meta=meta, clip=clip, G=G)
     log("  pool: differing bytes", nd, "tolerated", nt)
