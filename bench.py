@@ -61,6 +61,8 @@ def parse():
                          "slower than eager launches on ROCm 7.x, so never used for value)")
     ap.add_argument("--cpu-seconds", type=float, default=10.0,
                     help="target CPU time for the oracle baseline sample")
+    ap.add_argument("--no-prefill", action="store_true",
+                    help="skip the prefill-scale cache write (one 131072-token prompt)")
     ap.add_argument("--no-variants", action="store_true",
                     help="skip the quantizer-variant steps (paper format, identity R_V)")
     ap.add_argument("--no-mixed", action="store_true",
@@ -286,6 +288,47 @@ def main():
     app_flop = app_rows * 2 * d * d
     del ak, av
 
+    # ---- prefill-scale cache write: one 131072-token prompt x 8 KV heads routed by
+    # oscar_mixed_append (bf16 sink 64 + window 256, the rest INT2), into a pool of
+    # its own; rotation-bound like the 64-token update ----
+    pf = None
+    if not args.no_prefill:
+        pf_tok = 131072
+        pf_pages = (pf_tok + 63) // 64
+        pf_lay = ok.Layout(num_kv_heads=Hkv, num_pages=pf_pages)
+        pf_pool = ok.alloc_pool(pf_lay)
+        pf_seg = ok.alloc_seg(pf_lay, 1, S0m, Wm)
+        pk = torch.randn(pf_tok, Hkv, d, device=dev).to(torch.bfloat16)
+        pv = torch.randn(pf_tok, Hkv, d, device=dev).to(torch.bfloat16)
+        pidx = torch.zeros(pf_tok, dtype=torch.int32, device=dev)
+        ppos = torch.arange(pf_tok, dtype=torch.int64, device=dev)
+        pbt = torch.arange(pf_pages, dtype=torch.int32, device=dev).view(1, pf_pages)
+        plen = torch.tensor([pf_tok], dtype=torch.int32, device=dev)
+
+        def prefill():
+            ok.mixed_append(pf_lay, pf_pool, pf_seg, S0m, Wm, pk, pv, pidx, ppos, pbt, plen, Rk,
+                            Rv, cfg.clip_k, cfg.clip_v)
+
+        prefill()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        n_pf = 5
+        e0.record(stream)
+        for _ in range(n_pf):
+            prefill()
+        e1.record(stream)
+        torch.cuda.synchronize()
+        pf_us = e0.elapsed_time(e1) * 1e3 / n_pf
+        pf_rows = 2 * (pf_tok - S0m - Wm) * Hkv                   # quantized rows (K and V)
+        pf_flop = pf_rows * 2 * d * d                              # their rotations
+        pf = {"tokens": pf_tok, "kv_heads": Hkv, "S0": S0m, "W": Wm, "us": round(pf_us, 1),
+              "tokens_per_s": round(pf_tok / (pf_us * 1e-6), 1), "bound": "alu",
+              "achieved_tflops_fp64": round(pf_flop / (pf_us * 1e-6) / 1e12, 2),
+              "peak_tflops_fp64": 78.6,
+              "frac": round(pf_flop / (pf_us * 1e-6) / 1e12 / 78.6, 4),
+              "int2_rows": pf_rows}
+        del pf_pool, pf_seg, pk, pv
+
     res = {
         "metric": METRIC,
         "value": round(step_bytes / (us_step * 1e-6) / 1e9, 1),
@@ -337,6 +380,7 @@ def main():
             "frac": round(app_flop / (app_us * 1e-6) / 1e12 / 78.6, 4),
             "bytes": 2 * B * n_new * Hkv * d * 2 + B * n_new * Hkv * INT2_BYTES_PER_TOKEN_HEAD,
         },
+        "prefill_128k_tokens": pf,
         "bytes": {"int2_kv": kv_bytes, "block_table": table_bytes, "q_and_out": qo_bytes,
                   "append": append_bytes, "step_total": step_bytes,
                   "bf16_kv_equivalent": int(lens.sum()) * Hkv * BF16_BYTES_PER_TOKEN_HEAD},

@@ -528,7 +528,11 @@ __device__ inline void append_body(float* Rs, double (*xs)[RW][kD], int is_v, in
   }
 }
 
-template <int RW, class Rows>
+// DEF: the default format (binary16 metadata, group-absmax clip, 32-channel
+// groups) as compile-time constants, so that its code has no format branches.
+__device__ inline QFmt pick(bool def, const QFmt& fmt) { return def ? QFmt{0, 0, 4} : fmt; }
+
+template <int RW, class Rows, bool DEF>
 __global__ __launch_bounds__(256) void append_kernel(uint8_t* __restrict__ pages, int Hkv,
                                                      Rows rows, int n_rows,
                                                      const float* __restrict__ Rk,
@@ -537,7 +541,7 @@ __global__ __launch_bounds__(256) void append_kernel(uint8_t* __restrict__ pages
   __shared__ float Rs[kD * kD];
   __shared__ double xs[kWaves][RW][kD];
   append_body<RW>(Rs, xs, blockIdx.y, blockIdx.x, gridDim.x, pages, Hkv, rows, n_rows, Rk, Rv,
-                  clip_k, clip_v, fmt);
+                  clip_k, clip_v, pick(DEF, fmt));
 }
 
 // ---------------------------------------------------------------------------
@@ -628,10 +632,11 @@ __device__ inline void store_row4(uint8_t* __restrict__ pages, int Hkv, int64_t 
   }
 }
 
-template <class Rows>
+template <class Rows, bool DEF>
 __global__ __launch_bounds__(512) void append_bulk_kernel(
     uint8_t* __restrict__ pages, int Hkv, Rows rows, int n_rows, const float* __restrict__ Rk,
-    const float* __restrict__ Rv, float clip_k, float clip_v, QFmt fmt) {
+    const float* __restrict__ Rv, float clip_k, float clip_v, QFmt fmt_arg) {
+  const QFmt fmt = pick(DEF, fmt_arg);
   // xs first: its reads use the 16-bit LDS offset field
   __shared__ double2 xs[kBulkWaves][kBulkRows][kD / 2];      // 64 KB
   __shared__ float4 Rq[kD][kD / 4];                          // 64 KB
@@ -718,10 +723,10 @@ __global__ __launch_bounds__(256) void prepare_kernel(const uint16_t* __restrict
 // One launch for a decode step's prologue: blockIdx.y 0/1 = K/V cache update
 // (append_blocks blocks), 2 = query rotation (prep_blocks blocks).  The two are
 // independent; the split kernel that follows needs both.
-template <int RW, class Rows>
+template <int RW, class Rows, bool DEF>
 __global__ __launch_bounds__(256) void prologue_kernel(
     uint8_t* __restrict__ pages, int Hkv, Rows rows, int n_rows, const float* __restrict__ Rk,
-    const float* __restrict__ Rv, float clip_k, float clip_v, QFmt fmt, int append_blocks,
+    const float* __restrict__ Rv, float clip_k, float clip_v, QFmt fmt_arg, int append_blocks,
     const uint16_t* __restrict__ q, int q_rows, float qscale, float* __restrict__ qt,
     int prep_blocks) {
   __shared__ float Rs[kD * kD];
@@ -730,7 +735,7 @@ __global__ __launch_bounds__(256) void prologue_kernel(
   if (blockIdx.y < 2) {
     if ((int)blockIdx.x < append_blocks)
       append_body<RW>(Rs, xs, blockIdx.y, blockIdx.x, append_blocks, pages, Hkv, rows, n_rows,
-                      Rk, Rv, clip_k, clip_v, fmt);
+                      Rk, Rv, clip_k, clip_v, pick(DEF, fmt_arg));
   } else if ((int)blockIdx.x < prep_blocks) {
     prepare_body(Rs, qs, blockIdx.x, q, q_rows, Rk, qscale, qt);
   }
@@ -745,21 +750,32 @@ int64_t append_blocks_for(int64_t n_rows, int rw) {
   return blocks > 1024 ? 1024 : blocks;
 }
 
+bool is_default(const QFmt& f) { return f.bf16 == 0 && f.quantile == 0 && f.ng == 4; }
+
 template <class Rows>
 hipError_t launch_rows(void* pages, int64_t Hkv, const Rows& rows, int64_t n_rows, const float* Rk,
                        const float* Rv, float clip_k, float clip_v, QFmt fmt, hipStream_t st) {
+  const bool def = is_default(fmt);
   if (n_rows <= 4096) {  // one decode step: many short waves
     const dim3 grid((unsigned)append_blocks_for(n_rows, 1), 2);
-    hipLaunchKernelGGL((append_kernel<1, Rows>), grid, dim3(256), 0, st, static_cast<uint8_t*>(pages),
-                       (int)Hkv, rows, (int)n_rows, Rk, Rv, clip_k, clip_v, fmt);
+    auto go = [&](auto kernel) {
+      hipLaunchKernelGGL(kernel, grid, dim3(256), 0, st, static_cast<uint8_t*>(pages), (int)Hkv,
+                         rows, (int)n_rows, Rk, Rv, clip_k, clip_v, fmt);
+    };
+    if (def) go(append_kernel<1, Rows, true>);
+    else go(append_kernel<1, Rows, false>);
   } else {  // bulk: one persistent 8-wave block per CU, half of them per tensor
     const int64_t items = (n_rows + kBulkRows - 1) / kBulkRows;
     int64_t nb = (items + kBulkWaves - 1) / kBulkWaves;
     const int64_t cap = std::max<int64_t>(1, device_cus() / 2);
     if (nb > cap) nb = cap;
-    hipLaunchKernelGGL(append_bulk_kernel<Rows>, dim3((unsigned)nb, 2), dim3(512), 0, st,
-                       static_cast<uint8_t*>(pages), (int)Hkv, rows, (int)n_rows, Rk, Rv, clip_k,
-                       clip_v, fmt);
+    auto go = [&](auto kernel) {
+      hipLaunchKernelGGL(kernel, dim3((unsigned)nb, 2), dim3(512), 0, st,
+                         static_cast<uint8_t*>(pages), (int)Hkv, rows, (int)n_rows, Rk, Rv,
+                         clip_k, clip_v, fmt);
+    };
+    if (def) go(append_bulk_kernel<Rows, true>);
+    else go(append_bulk_kernel<Rows, false>);
   }
   return hipGetLastError();
 }
@@ -773,14 +789,19 @@ hipError_t launch_prologue(void* pages, int64_t Hkv, const Rows& rows, int64_t n
   const int ab = n_rows > 0 ? (int)append_blocks_for(n_rows, rw) : 0;
   const int pb = (B * Hq + kPrepRows - 1) / kPrepRows;
   const dim3 grid((unsigned)(ab > pb ? ab : pb), 3);
-  if (rw == 1)
-    hipLaunchKernelGGL((prologue_kernel<1, Rows>), grid, dim3(256), 0, st,
-                       static_cast<uint8_t*>(pages), (int)Hkv, rows, (int)n_rows, Rk, Rv, clip_k,
-                       clip_v, fmt, ab, q, B * Hq, qscale, qt, pb);
-  else
-    hipLaunchKernelGGL((prologue_kernel<4, Rows>), grid, dim3(256), 0, st,
-                       static_cast<uint8_t*>(pages), (int)Hkv, rows, (int)n_rows, Rk, Rv, clip_k,
-                       clip_v, fmt, ab, q, B * Hq, qscale, qt, pb);
+  auto go = [&](auto kernel) {
+    hipLaunchKernelGGL(kernel, grid, dim3(256), 0, st, static_cast<uint8_t*>(pages), (int)Hkv,
+                       rows, (int)n_rows, Rk, Rv, clip_k, clip_v, fmt, ab, q, B * Hq, qscale, qt,
+                       pb);
+  };
+  const bool def = is_default(fmt);
+  if (rw == 1) {
+    if (def) go(prologue_kernel<1, Rows, true>);
+    else go(prologue_kernel<1, Rows, false>);
+  } else {
+    if (def) go(prologue_kernel<4, Rows, true>);
+    else go(prologue_kernel<4, Rows, false>);
+  }
   return hipGetLastError();
 }
 }  // namespace

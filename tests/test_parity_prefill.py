@@ -1,0 +1,90 @@
+"""GPU parity of the prefill-scale cache write (Alg. 1 Prefill; Sec. 4 "KV Cache
+Layout" and "KV Cache Update") against the oracle: one 131072-token prompt of 8
+KV heads written by a single oscar_mixed_append call, the launch the benchmark
+times (bulk append kernel, bf16 sink 64 and window 256, the 130752 tokens between
+them quantized to INT2), then decode attention over the whole cache with 96
+query heads.
+
+Compared on the whole cache, not a sample: every byte of the INT2 pool
+(bit-exact, with the near-boundary rule of helpers.compare_pools), every element
+of the segment store (bit-exact bf16 copies), and the decode output of every
+query head (2e-3 on fp32).  The oracle writes the same cache directly: segment
+rows by oracle.seg_write, history rows by oracle.kv_append (its pins show this
+equals its one-token-per-step loop).  Two formats: the default one (G = 32,
+binary16 scale/zero, group-absmax clip) and the paper's (G = 128, bf16
+scale/zero, per-token quantile clip)."""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import paper_2605_17757_amd as ok
+import workloads as W
+from helpers import DECODE_TOL, Case, bits, compare_pools, log, max_abs
+
+pytestmark = pytest.mark.gpu
+
+D, P = 128, 64
+S0, WIN = 64, 256
+
+# name -> (meta_dtype, clip_mode, group size)
+FORMATS = {"default": (0, 0, 32), "paper_format": (1, 1, 128)}
+
+
+@pytest.mark.parametrize("fmt", list(FORMATS))
+def test_prefill_131072_tokens_one_call(fmt):
+    meta, clip, G = FORMATS[fmt]
+    cfg = W.config(4, batch=1)  # 131072 tokens, 96/8 heads, Student-t(3) keys
+    n = int(cfg.lens[0])
+    Hkv, Hq = cfg.Hkv, cfg.Hq
+    table, num_pages = W.block_table(cfg)
+    lay = ok.Layout(num_kv_heads=Hkv, num_pages=num_pages, group_size=G, clip_mode=clip,
+                    meta_dtype=meta)
+    Rk_np, Rv_np = W.rotations(cfg)
+    kd, vd = W.cache_kv(cfg, 0, device="cuda")  # the same inputs reach both sides
+    k, v = kd.cpu(), vd.cpu()
+    q = W.queries(cfg)
+    log("prefill %s: tokens %d, kv heads %d, pages %d" % (fmt, n, Hkv, num_pages))
+
+    pool = ok.alloc_pool(lay)
+    seg = ok.alloc_seg(lay, 1, S0, WIN)
+    table_d = torch.from_numpy(table).cuda()
+    lens_d = torch.from_numpy(cfg.lens).cuda()
+    Rk, Rv = torch.from_numpy(Rk_np).cuda(), torch.from_numpy(Rv_np).cuda()
+    ok.mixed_append(lay, pool, seg, S0, WIN, kd, vd,
+                    torch.zeros(n, dtype=torch.int32, device="cuda"),
+                    torch.arange(n, dtype=torch.int64, device="cuda"), table_d, lens_d, Rk, Rv,
+                    cfg.clip_k, cfg.clip_v)
+    S = ok.default_num_splits(lay, 1, Hq, int(table.shape[1]) * P)
+    ws = ok.alloc_mixed_workspace(lay, 1, Hq, S)
+    out = torch.empty(1, Hq, D, dtype=torch.float32, device="cuda")
+    ok.decode_attn_mixed(lay, pool, seg, S0, WIN, q.cuda(), table_d, lens_d, Rk, Rv,
+                         cfg.sm_scale, S, ws, out)
+    torch.cuda.synchronize()
+    log("  gpu done, splits", S)
+
+    lo, hi = S0, n - WIN
+    ora = np.zeros(ok.pool_bytes(lay), np.uint8)
+    oseg = np.zeros(oracle.seg_elems(d=D, Hkv=Hkv, B=1, S0=S0, W=WIN), np.uint16)
+    keep = np.r_[0:lo, hi:n]
+    kt = torch.from_numpy(keep)
+    oracle.seg_write(oseg, d=D, Hkv=Hkv, B=1, S0=S0, W=WIN, k=bits(k[kt]), v=bits(v[kt]),
+                     seq_idx=np.zeros(keep.size, np.int32), pos=keep.astype(np.int64))
+    sl = W.slots_for(table, 0, np.arange(lo, hi))
+    oracle.kv_append(ora, d=D, Hkv=Hkv, P=P, G=G, k=bits(k[lo:hi]), v=bits(v[lo:hi]),
+                     slot_mapping=sl, Rk=Rk_np, Rv=Rv_np, clip_k=cfg.clip_k, clip_v=cfg.clip_v,
+                     meta=meta, clip=clip)
+    log("  oracle cache written")
+
+    gseg = seg.cpu().contiguous().view(torch.int16).numpy().view(np.uint16).reshape(-1)
+    assert np.array_equal(gseg, oseg)
+    case = Case(cfg, Rk_np, Rv_np, table, num_pages, q, k[lo:hi], v[lo:hi], sl)
+    nd, nt = compare_pools(pool.cpu().numpy(), ora, case, meta=meta, clip=clip, G=G)
+    log("  pool: differing bytes", nd, "tolerated near-boundary rows", nt)
+
+    ref = oracle.decode_mixed(ora, oseg, d=D, Hkv=Hkv, P=P, G=G, S0=S0, W=WIN, q=bits(q),
+                              block_table=table, seq_lens=cfg.lens, Rk=Rk_np, Rv=Rv_np,
+                              sm_scale=cfg.sm_scale, meta=meta)
+    err = max_abs(out, ref)
+    log("  decode max|err| over %d heads = %.3g" % (Hq, err))
+    assert err <= DECODE_TOL
