@@ -19,6 +19,14 @@ What it computes (arXiv 2605.17757):
                          window around the INT2 history, the per-step demotion of
                          the oldest window token (Alg. 1 DecodeStep) and decode
                          attention over all three segments.
+  * ``query_cov``, ``attn_rows``, ``score_cov``, ``hadamard``, ``bit_reversal``,
+    ``compose``, ``eigh_desc``, ``clip_errors``, ``calibrate`` -- the offline
+                         calibration of Sec. 3 and Alg. 1 Calibrate: the
+                         GQA-averaged query covariance C_Q, the score-aware value
+                         covariance C_S = V^T S^T S V / N, their eigenvectors
+                         (descending, sign fixed), R = U H_Had P_br, and the clip
+                         ratio with the smallest quantization error of the
+                         rotated rows.
 
 Quantizer variants (keyword arguments, defaults = the hot path's format):
 ``meta`` 0/1 stores scale and zero as binary16 / bfloat16; ``clip`` 0/1 takes the
@@ -99,6 +107,20 @@ def lib():
         L.oracle_decode_mixed.restype = i32
         L.oracle_decode_mixed.argtypes = [i32, i32, i32, i32, i32, i64, P, P, i32, i32, P, i32,
                                           i32, P, i32, P, P, P, f64, P, i32, P]
+        L.oracle_query_cov.restype = i32
+        L.oracle_query_cov.argtypes = [P, i64, i32, i32, i32, P]
+        L.oracle_attn_rows.restype = i32
+        L.oracle_attn_rows.argtypes = [P, P, P, i64, i32, i32, i32, i32, P, i64, P]
+        L.oracle_score_cov.restype = i32
+        L.oracle_score_cov.argtypes = [P, P, P, i64, i32, i32, i32, i32, P]
+        L.oracle_hadamard.restype = i32
+        L.oracle_hadamard.argtypes = [i32, P]
+        L.oracle_bit_reversal.restype = i32
+        L.oracle_bit_reversal.argtypes = [i32, P]
+        L.oracle_compose.restype = i32
+        L.oracle_compose.argtypes = [P, i32, P]
+        L.oracle_clip_errors.restype = i32
+        L.oracle_clip_errors.argtypes = [P, i64, i32, P, i32, i32, i32, P, i32, P]
         L.oracle_num_threads.restype = i32
         _lib = L
     return _lib
@@ -350,3 +372,127 @@ def decode_mixed(pages: np.ndarray, seg: np.ndarray, *, d: int, Hkv: int, P: int
     if rc:
         raise ValueError("oracle decode_mixed: bad page id, length or head")
     return out
+
+
+# ---------------------------------------------------------------------------
+# Offline calibration (Sec. 3 "Algorithm Design: Offline Calibration and
+# Justification"; App. worked example; Alg. 1 Calibrate)
+# ---------------------------------------------------------------------------
+
+def query_cov(q: np.ndarray, Hkv: int) -> np.ndarray:
+    """GQA-averaged C_Q of bf16 queries q [T, Hq, d] (uint16 bits): [d, d] fp64."""
+    q = _c(q, np.uint16)
+    T, Hq, d = q.shape
+    C = np.zeros((d, d), np.float64)
+    if lib().oracle_query_cov(_ptr(q), T, Hq, Hkv, d, _ptr(C)):
+        raise ValueError("oracle query_cov: bad shape")
+    return C
+
+
+def attn_rows(q: np.ndarray, k: np.ndarray, v: np.ndarray, *, causal: bool,
+              pairs=None) -> np.ndarray:
+    """Attention outputs o_{t,i} (fp64) of bf16 q [T, Hq, d], k, v [T, Hkv, d];
+    ``pairs`` (t, i) or None for all rows ([T, Hq, d])."""
+    q, k, v = _c(q, np.uint16), _c(k, np.uint16), _c(v, np.uint16)
+    T, Hq, d = q.shape
+    Hkv = k.shape[1]
+    if pairs is None:
+        out = np.zeros((T, Hq, d), np.float64)
+        pp, n = None, 0
+    else:
+        pr = _c(pairs, np.int32).reshape(-1, 2)
+        out = np.zeros((pr.shape[0], d), np.float64)
+        pp, n = _ptr(pr), pr.shape[0]
+    if lib().oracle_attn_rows(_ptr(q), _ptr(k), _ptr(v), T, Hq, Hkv, d, int(bool(causal)), pp, n,
+                              _ptr(out)):
+        raise ValueError("oracle attn_rows: bad shape or pair")
+    return out
+
+
+def score_cov(q: np.ndarray, k: np.ndarray, v: np.ndarray, *, causal: bool) -> np.ndarray:
+    """GQA-averaged C_S = (1/N) V^T S^T S V: [d, d] fp64."""
+    q, k, v = _c(q, np.uint16), _c(k, np.uint16), _c(v, np.uint16)
+    T, Hq, d = q.shape
+    C = np.zeros((d, d), np.float64)
+    if lib().oracle_score_cov(_ptr(q), _ptr(k), _ptr(v), T, Hq, k.shape[1], d, int(bool(causal)),
+                              _ptr(C)):
+        raise ValueError("oracle score_cov: bad shape")
+    return C
+
+
+def hadamard(d: int) -> np.ndarray:
+    H = np.zeros((d, d), np.float64)
+    if lib().oracle_hadamard(d, _ptr(H)):
+        raise ValueError("oracle hadamard: d must be a power of two")
+    return H
+
+
+def bit_reversal(d: int) -> np.ndarray:
+    P = np.zeros((d, d), np.float64)
+    if lib().oracle_bit_reversal(d, _ptr(P)):
+        raise ValueError("oracle bit_reversal: d must be a power of two")
+    return P
+
+
+def compose(U: np.ndarray) -> np.ndarray:
+    """R = U H_Had P_br (fp64)."""
+    U = _c(U, np.float64)
+    d = U.shape[0]
+    R = np.zeros((d, d), np.float64)
+    if lib().oracle_compose(_ptr(U), d, _ptr(R)):
+        raise ValueError("oracle compose: d must be a power of two")
+    return R
+
+
+def eigh_desc(C: np.ndarray):
+    """Eigen-decomposition C = U diag(lam) U^T of a symmetric fp64 matrix (LAPACK
+    through numpy), eigenvalues in descending order; each eigenvector's sign is
+    fixed so that its entry of largest magnitude (the first such) is positive."""
+    w, U = np.linalg.eigh(_c(C, np.float64))
+    order = np.argsort(-w, kind="stable")
+    w, U = w[order], U[:, order]
+    idx = np.argmax(np.abs(U), axis=0)
+    sign = np.where(U[idx, np.arange(U.shape[1])] < 0, -1.0, 1.0)
+    return w.copy(), np.ascontiguousarray(U * sign[None, :])
+
+
+def clip_errors(x: np.ndarray, R, *, G: int, cands, meta: int = 0, clip: int = 0) -> np.ndarray:
+    """Mean squared quantization error of the rotated rows x [n, d] (bf16 bits) for
+    each candidate clip ratio (fp32): [n_cands] fp64."""
+    x = _c(x, np.uint16)
+    d = x.shape[-1]
+    x = x.reshape(-1, d)
+    cd = _c(cands, np.float32)
+    err = np.zeros(cd.size, np.float64)
+    Ra, Rp = _rot(R)
+    if lib().oracle_clip_errors(_ptr(x), x.shape[0], d, Rp, G, int(meta), int(clip), _ptr(cd),
+                                cd.size, _ptr(err)):
+        raise ValueError("oracle clip_errors: bad shape")
+    return err
+
+
+def default_clip_candidates() -> np.ndarray:
+    """0.80, 0.81, ..., 1.00 as fp32."""
+    return np.array([round(0.80 + 0.01 * n, 2) for n in range(21)], np.float32)
+
+
+def calibrate(q: np.ndarray, k: np.ndarray, v: np.ndarray, *, causal: bool = True, G: int = 32,
+              meta: int = 0, clip: int = 0, cands=None) -> dict:
+    """Alg. 1 Calibrate for one layer from bf16 activations q [T, Hq, d], k, v
+    [T, Hkv, d]: C_Q, C_S, their descending eigen-decompositions, R_K and R_V
+    (fp64 and rounded to fp32), and the clip ratios c_K, c_V chosen among
+    ``cands`` (the first minimum of clip_errors) for rows rotated by the fp32
+    matrices the cache update uses."""
+    cands = default_clip_candidates() if cands is None else _c(cands, np.float32)
+    Hkv = k.shape[1]
+    CQ = query_cov(q, Hkv)
+    CS = score_cov(q, k, v, causal=causal)
+    lam_q, UQ = eigh_desc(CQ)
+    lam_s, US = eigh_desc(CS)
+    RK, RV = compose(UQ), compose(US)
+    RK32, RV32 = RK.astype(np.float32), RV.astype(np.float32)
+    err_k = clip_errors(k, RK32, G=G, cands=cands, meta=meta, clip=clip)
+    err_v = clip_errors(v, RV32, G=G, cands=cands, meta=meta, clip=clip)
+    return {"C_Q": CQ, "C_S": CS, "lam_Q": lam_q, "lam_S": lam_s, "U_Q": UQ, "U_S": US,
+            "R_K": RK, "R_V": RV, "R_K32": RK32, "R_V32": RV32, "err_K": err_k, "err_V": err_v,
+            "c_K": float(cands[int(np.argmin(err_k))]), "c_V": float(cands[int(np.argmin(err_v))])}

@@ -795,3 +795,220 @@ int oracle_num_threads(void) {
   return 1;
 #endif
 }
+
+/* ------------------------------------------------------------------------- */
+/* Offline calibration (Sec. 3 "Algorithm Design: Offline Calibration and     */
+/* Justification"; Alg. 1 Calibrate)                                          */
+/* ------------------------------------------------------------------------- */
+
+static double bf16d(uint16_t h) { return (double)oracle_bf16_to_f32(h); }
+
+/* Query-aware key target covariance, GQA-averaged as in the appendix worked
+ * example: C_Q = (1/Hkv) sum_h (1/(T g)) sum_{i in group h} sum_t q_{t,i}^T q_{t,i},
+ * g = Hq/Hkv query heads per KV head, q: bf16 [T][Hq][d].  C: [d][d].  Returns
+ * -1 on a bad shape. */
+int oracle_query_cov(const uint16_t *q, int64_t T, int Hq, int Hkv, int d, double *C) {
+  if (T < 1 || Hkv < 1 || Hq < Hkv || Hq % Hkv || d < 1) return -1;
+  const int g = Hq / Hkv;
+#pragma omp parallel for schedule(dynamic, 1)
+  for (int i = 0; i < d; ++i) {
+    double *outer = (double *)calloc((size_t)d, sizeof(double));
+    double *grp = (double *)malloc(sizeof(double) * (size_t)d);
+    for (int h = 0; h < Hkv; ++h) {
+      for (int j = 0; j < d; ++j) grp[j] = 0.0;
+      for (int qi = h * g; qi < (h + 1) * g; ++qi)
+        for (int64_t t = 0; t < T; ++t) {
+          const uint16_t *row = q + ((size_t)t * Hq + qi) * d;
+          const double xi = bf16d(row[i]);
+          for (int j = 0; j < d; ++j) grp[j] = grp[j] + xi * bf16d(row[j]);
+        }
+      for (int j = 0; j < d; ++j) outer[j] = outer[j] + grp[j] / ((double)T * (double)g);
+    }
+    for (int j = 0; j < d; ++j) C[(size_t)i * d + j] = outer[j] / (double)Hkv;
+    free(outer); free(grp);
+  }
+  return 0;
+}
+
+/* Attention output rows of the calibration pass (Alg. 1 Calibrate):
+ * S = softmax_row(Q_i K_h^T / sqrt(d) + M) for query head i and its KV head
+ * h = i / g, M = 0 on keys j <= t and -inf on j > t when causal (no mask
+ * otherwise), o_{t,i} = sum_j S[t][j] v_{j,h}.  fp64 throughout: scores summed
+ * in ascending channel order, softmax with the row maximum subtracted.
+ * q: bf16 [T][Hq][d], k, v: bf16 [T][Hkv][d].  pairs: (t, i) int32 pairs, or
+ * NULL for every (t, i) in t-major order.  out: [n][d].  Returns -1 on a bad
+ * shape or pair. */
+int oracle_attn_rows(const uint16_t *q, const uint16_t *k, const uint16_t *v, int64_t T, int Hq,
+                     int Hkv, int d, int causal, const int32_t *pairs, int64_t n_pairs,
+                     double *out) {
+  if (T < 1 || Hkv < 1 || Hq < Hkv || Hq % Hkv || d < 1) return -1;
+  const int g = Hq / Hkv;
+  const int64_t n = pairs ? n_pairs : T * Hq;
+  int64_t bad = 0;
+#pragma omp parallel for schedule(dynamic, 4) reduction(+ : bad)
+  for (int64_t p = 0; p < n; ++p) {
+    const int64_t t = pairs ? pairs[2 * p] : p / Hq;
+    const int i = pairs ? pairs[2 * p + 1] : (int)(p % Hq);
+    double *o = out + (size_t)p * d;
+    if (t < 0 || t >= T || i < 0 || i >= Hq) { bad += 1; continue; }
+    const int h = i / g;
+    const int64_t nk = causal ? t + 1 : T;
+    double *s = (double *)malloc(sizeof(double) * (size_t)nk);
+    const uint16_t *qr = q + ((size_t)t * Hq + i) * d;
+    double m = -INFINITY;
+    for (int64_t j = 0; j < nk; ++j) {
+      const uint16_t *kr = k + ((size_t)j * Hkv + h) * d;
+      double dot = 0.0;
+      for (int c = 0; c < d; ++c) dot = dot + bf16d(qr[c]) * bf16d(kr[c]);
+      s[j] = dot / sqrt((double)d);
+      if (s[j] > m) m = s[j];
+    }
+    double den = 0.0;
+    for (int64_t j = 0; j < nk; ++j) { s[j] = exp(s[j] - m); den = den + s[j]; }
+    for (int c = 0; c < d; ++c) o[c] = 0.0;
+    for (int64_t j = 0; j < nk; ++j) {
+      const uint16_t *vr = v + ((size_t)j * Hkv + h) * d;
+      const double w = s[j] / den;
+      for (int c = 0; c < d; ++c) o[c] = o[c] + w * bf16d(vr[c]);
+    }
+    free(s);
+  }
+  return bad ? -1 : 0;
+}
+
+/* Score-aware value target covariance (Sec. 3): C_S = (1/N) V^T S^T S V, i.e.
+ * the second moment of the attention outputs o = S V, GQA-averaged like C_Q:
+ * C_S = (1/Hkv) sum_h (1/(T g)) sum_{i in group h} sum_t o_{t,i}^T o_{t,i}. */
+int oracle_score_cov(const uint16_t *q, const uint16_t *k, const uint16_t *v, int64_t T, int Hq,
+                     int Hkv, int d, int causal, double *C) {
+  if (T < 1 || Hkv < 1 || Hq < Hkv || Hq % Hkv || d < 1) return -1;
+  const int g = Hq / Hkv;
+  double *O = (double *)malloc(sizeof(double) * (size_t)T * Hq * d);
+  if (!O) return -1;
+  if (oracle_attn_rows(q, k, v, T, Hq, Hkv, d, causal, NULL, 0, O)) { free(O); return -1; }
+#pragma omp parallel for schedule(dynamic, 1)
+  for (int i = 0; i < d; ++i) {
+    double *outer = (double *)calloc((size_t)d, sizeof(double));
+    double *grp = (double *)malloc(sizeof(double) * (size_t)d);
+    for (int h = 0; h < Hkv; ++h) {
+      for (int j = 0; j < d; ++j) grp[j] = 0.0;
+      for (int qi = h * g; qi < (h + 1) * g; ++qi)
+        for (int64_t t = 0; t < T; ++t) {
+          const double *row = O + ((size_t)t * Hq + qi) * d;
+          for (int j = 0; j < d; ++j) grp[j] = grp[j] + row[i] * row[j];
+        }
+      for (int j = 0; j < d; ++j) outer[j] = outer[j] + grp[j] / ((double)T * (double)g);
+    }
+    for (int j = 0; j < d; ++j) C[(size_t)i * d + j] = outer[j] / (double)Hkv;
+    free(outer); free(grp);
+  }
+  free(O);
+  return 0;
+}
+
+/* Normalized Walsh-Hadamard matrix by the Sylvester recursion of the appendix
+ * (App. "Hadamard transform"): H_1 = [1], H_2m = [[H_m, H_m], [H_m, -H_m]] / sqrt 2.
+ * d must be a power of two.  H: [d][d]. */
+int oracle_hadamard(int d, double *H) {
+  if (d < 1 || (d & (d - 1))) return -1;
+  H[0] = 1.0;
+  for (int m = 1; m < d; m *= 2) {
+    /* grow the leading m x m block in place, from the bottom-right corner */
+    for (int i = m - 1; i >= 0; --i)
+      for (int j = m - 1; j >= 0; --j) {
+        const double x = H[(size_t)i * d + j] / sqrt(2.0);
+        H[(size_t)i * d + j] = x;
+        H[(size_t)i * d + j + m] = x;
+        H[(size_t)(i + m) * d + j] = x;
+        H[(size_t)(i + m) * d + j + m] = -x;
+      }
+  }
+  return 0;
+}
+
+/* Bit reversal of k over log2(d) bits. */
+static int bitrev(int k, int d) {
+  int r = 0;
+  for (int b = 1; b < d; b <<= 1) { r = (r << 1) | (k & 1); k >>= 1; }
+  return r;
+}
+
+/* Permuted bit-reversal matrix P_br (App. "P_K"): the eigenvector of the k-th
+ * largest eigenvalue goes to position bitrev(k), i.e. (x P)_{bitrev(k)} = x_k:
+ * P[k][bitrev(k)] = 1.  P: [d][d]. */
+int oracle_bit_reversal(int d, double *P) {
+  if (d < 1 || (d & (d - 1))) return -1;
+  for (size_t i = 0; i < (size_t)d * d; ++i) P[i] = 0.0;
+  for (int kk = 0; kk < d; ++kk) P[(size_t)kk * d + bitrev(kk, d)] = 1.0;
+  return 0;
+}
+
+/* Composed rotation (Eq. method_composed_rot): R = U H_Had P_br, fp64 matrix
+ * products in ascending summation order.  U: [d][d], eigenvectors in columns
+ * sorted by descending eigenvalue.  R: [d][d]. */
+int oracle_compose(const double *U, int d, double *R) {
+  if (d < 1 || (d & (d - 1))) return -1;
+  double *H = (double *)malloc(sizeof(double) * (size_t)d * d);
+  double *P = (double *)malloc(sizeof(double) * (size_t)d * d);
+  double *UH = (double *)malloc(sizeof(double) * (size_t)d * d);
+  oracle_hadamard(d, H);
+  oracle_bit_reversal(d, P);
+  for (int i = 0; i < d; ++i)
+    for (int j = 0; j < d; ++j) {
+      double acc = 0.0;
+      for (int c = 0; c < d; ++c) acc = acc + U[(size_t)i * d + c] * H[(size_t)c * d + j];
+      UH[(size_t)i * d + j] = acc;
+    }
+  for (int i = 0; i < d; ++i)
+    for (int j = 0; j < d; ++j) {
+      double acc = 0.0;
+      for (int c = 0; c < d; ++c) acc = acc + UH[(size_t)i * d + c] * P[(size_t)c * d + j];
+      R[(size_t)i * d + j] = acc;
+    }
+  free(H); free(P); free(UH);
+  return 0;
+}
+
+/* Clip calibration (Alg. 1 CalibrateClip, whose procedure the paper leaves
+ * open; read here as: pick the candidate ratio with the smallest quantization
+ * error of the rotated calibration rows).  For each candidate ratio rho_n:
+ *   err[n] = mean over rows r and channels c of (x~_{r,c} - s_g (code_{r,c} - z_g))^2
+ * with x~ = x R rounded to fp32 (oracle_rotate_row) and (code, s, z) from
+ * oracle_quantize_row with rho_n, s and z read back from their stored format.
+ * x: bf16 [n_rows][d].  Rows are summed in order (deterministic).  Returns -1
+ * on a bad shape. */
+int oracle_clip_errors(const uint16_t *x, int64_t n_rows, int d, const float *R, int G, int meta,
+                       int clip, const float *cands, int n_cands, double *err) {
+  if (n_rows < 1 || d < 1 || G < 1 || d % G || n_cands < 1) return -1;
+  double *per = (double *)malloc(sizeof(double) * (size_t)n_rows * n_cands);
+  if (!per) return -1;
+#pragma omp parallel for schedule(static)
+  for (int64_t r = 0; r < n_rows; ++r) {
+    float *xr = (float *)malloc(sizeof(float) * (size_t)d);
+    float *xt = (float *)malloc(sizeof(float) * (size_t)d);
+    uint8_t *codes = (uint8_t *)malloc((size_t)d);
+    uint16_t *s16 = (uint16_t *)malloc(sizeof(uint16_t) * (size_t)(d / G));
+    uint16_t *z16 = (uint16_t *)malloc(sizeof(uint16_t) * (size_t)(d / G));
+    for (int c = 0; c < d; ++c) xr[c] = oracle_bf16_to_f32(x[(size_t)r * d + c]);
+    oracle_rotate_row(xr, R, d, xt);
+    for (int n = 0; n < n_cands; ++n) {
+      oracle_quantize_row(xt, d, G, cands[n], meta, clip, codes, s16, z16);
+      double e = 0.0;
+      for (int c = 0; c < d; ++c) {
+        const double s = (double)meta_load(meta, s16[c / G]);
+        const double z = (double)meta_load(meta, z16[c / G]);
+        const double diff = (double)xt[c] - s * ((double)codes[c] - z);
+        e = e + diff * diff;
+      }
+      per[(size_t)r * n_cands + n] = e;
+    }
+    free(xr); free(xt); free(codes); free(s16); free(z16);
+  }
+  for (int n = 0; n < n_cands; ++n) {
+    double acc = 0.0;
+    for (int64_t r = 0; r < n_rows; ++r) acc = acc + per[(size_t)r * n_cands + n];
+    err[n] = acc / ((double)n_rows * (double)d);
+  }
+  free(per);
+  return 0;
+}
