@@ -331,6 +331,107 @@ int oscar_bf16_decode_attn(const oscar_layout *L, const void *pages, const void 
                            void *workspace, size_t workspace_bytes, void *out,
                            oscar_dtype out_dtype, void *stream);
 
+/*
+ * Offline calibration (Sec. 3 "Algorithm Design: Offline Calibration and
+ * Justification"; App. "Hadamard transform", "P_K" and the worked example;
+ * Alg. 1 Calibrate).  From one layer's calibration activations (bf16
+ * q [T, Hq, d], k and v [T, Hkv, d], row-major, d = 128, Hq % Hkv == 0,
+ * g = Hq / Hkv) the rotations and clip ratios the cache update takes.
+ * All matrices are row-major [d][d]; fp64 unless stated.  Device pointers,
+ * 16-byte aligned; asynchronous on `stream`; nothing is allocated.
+ */
+#define OSCAR_CALIB_MAX_CANDS 32  /* candidate clip ratios per call */
+#define OSCAR_CALIB_MAX_SWEEPS 32 /* Jacobi sweeps before giving up   */
+
+/*
+ * oscar_calib_query_cov -- query-aware key target covariance, GQA-averaged as
+ * in the appendix worked example:
+ *   C = (1/Hkv) sum_h (1/(T g)) sum_{i in group h} sum_t q_{t,i}^T q_{t,i}
+ * Products of the bf16 inputs are exact; they are summed in fp32 over chunks of
+ * rows and the chunks in fp64.  workspace >= oscar_calib_workspace_bytes(T, Hq,
+ * Hkv).  C: fp64 [d][d], exactly symmetric.
+ */
+size_t oscar_calib_workspace_bytes(int64_t T, int32_t Hq, int32_t Hkv);
+int oscar_calib_query_cov(const void *q, int64_t T, int32_t Hq, int32_t Hkv, double *C,
+                          void *workspace, size_t workspace_bytes, void *stream);
+
+/*
+ * oscar_calib_attn -- the calibration pass's attention rows (Alg. 1 Calibrate):
+ *   out[t][i] = softmax_row(q_{t,i} K_h^T / sqrt(d) + M) V_h,  h = i / g,
+ * M = -inf on keys j > t when causal != 0 (0 otherwise).  fp32 out [T, Hq, d].
+ * Scores are exact products summed in fp32; softmax in fp32 with the running row
+ * maximum; the probabilities enter the value product with ~16 significant bits.
+ */
+int oscar_calib_attn(const void *q, const void *k, const void *v, int64_t T, int32_t Hq,
+                     int32_t Hkv, int32_t causal, float *out, void *stream);
+
+/*
+ * oscar_calib_score_cov -- score-aware value target covariance (Sec. 3):
+ *   C = (1/N) V^T S^T S V, i.e. the GQA-averaged second moment of the rows
+ *   o_{t,i} of oscar_calib_attn (averaged like oscar_calib_query_cov).
+ * The rows are kept in the workspace (>= oscar_calib_workspace_bytes(T, Hq, Hkv)).
+ */
+int oscar_calib_score_cov(const void *q, const void *k, const void *v, int64_t T, int32_t Hq,
+                          int32_t Hkv, int32_t causal, double *C, void *workspace,
+                          size_t workspace_bytes, void *stream);
+
+/*
+ * oscar_calib_rotation -- for each of n_mats symmetric matrices C (fp64
+ * [n_mats][d][d]): the eigen-decomposition C = U diag(lam) U^T with lam
+ * descending (ties: lower index first) and each eigenvector's largest-magnitude
+ * entry (the first such) positive, then the composed rotation
+ * (Eq. method_composed_rot)
+ *   R = U H_Had P_br,   H_Had the normalized Sylvester Walsh-Hadamard matrix,
+ *                       P_br[k][bitrev(k)] = 1 (App. "P_K")
+ * evaluated as R[i][j] = sum_c U[i][c] H[c][bitrev(j)] in fp64, ascending c.
+ * Eigen-decomposition by cyclic Jacobi in fp64.
+ *   lam  : [n_mats][d]             U   : [n_mats][d][d] (eigenvectors in columns)
+ *   R64  : [n_mats][d][d] or NULL  R32 : fp32 [n_mats][d][d] or NULL (R64 rounded)
+ *   info : int32 [n_mats], sweeps run, or -1 if OSCAR_CALIB_MAX_SWEEPS sweeps did
+ *          not converge (lam, U and R are then not reliable)
+ *   workspace >= oscar_calib_rotation_workspace_bytes(n_mats)
+ */
+size_t oscar_calib_rotation_workspace_bytes(int32_t n_mats);
+int oscar_calib_rotation(const double *C, int32_t n_mats, double *lam, double *U, double *R64,
+                         float *R32, int32_t *info, void *workspace, size_t workspace_bytes,
+                         void *stream);
+
+/*
+ * oscar_calib_clip -- clip calibration (Alg. 1 CalibrateClip; the paper gives no
+ * procedure: read as the candidate with the smallest quantization error of the
+ * rotated calibration rows).  For rows x [n_tok, Hkv = L->num_kv_heads, d] bf16,
+ * rotated by R (fp32, NULL: identity) exactly as oscar_kv_append does, and
+ * quantized with L's group size, clip mode and metadata format at each
+ * candidate ratio cands[n] (fp32, in (0, 1], n_cands <= OSCAR_CALIB_MAX_CANDS):
+ *   err[n] = mean over rows and channels of (x~_c - s (code_c - z))^2   (fp64)
+ *   best   = cands[first n minimizing err] (fp32 [1], may be NULL)
+ * workspace >= oscar_calib_clip_workspace_bytes(n_tok, Hkv, n_cands).
+ */
+size_t oscar_calib_clip_workspace_bytes(int64_t n_tok, int32_t Hkv, int32_t n_cands);
+int oscar_calib_clip(const oscar_layout *L, const void *x, int64_t n_tok, const float *R,
+                     const float *cands, int32_t n_cands, double *err, float *best,
+                     void *workspace, size_t workspace_bytes, void *stream);
+
+/*
+ * oscar_calibrate_layer -- Alg. 1 Calibrate for one layer, in the paper's order:
+ * C_Q (oscar_calib_query_cov), C_S (oscar_calib_score_cov), their rotations
+ * R_K = U_Q H_Had P_br and R_V = U_S H_Had P_br (oscar_calib_rotation), and the
+ * clip ratios c_K, c_V (oscar_calib_clip of k by R_K and of v by R_V, in L's
+ * quantizer format).  L->num_kv_heads is Hkv.
+ *   R_k, R_v : fp32 [d][d] outputs (what oscar_kv_append and decode take)
+ *   clip     : fp32 [2] = (c_K, c_V)
+ *   lam      : fp64 [2][d] (spectra of C_Q, C_S) or NULL
+ *   info     : int32 [2] (oscar_calib_rotation's) or NULL
+ * workspace >= oscar_calibrate_layer_workspace_bytes(T, Hq, Hkv, n_cands).
+ */
+size_t oscar_calibrate_layer_workspace_bytes(int64_t T, int32_t Hq, int32_t Hkv,
+                                             int32_t n_cands);
+int oscar_calibrate_layer(const oscar_layout *L, const void *q, const void *k, const void *v,
+                          int64_t T, int32_t Hq, int32_t causal, const float *cands,
+                          int32_t n_cands, float *R_k, float *R_v, float *clip, double *lam,
+                          int32_t *info, void *workspace, size_t workspace_bytes,
+                          void *stream);
+
 #ifdef __cplusplus
 }
 #endif

@@ -32,7 +32,13 @@ EXPORTS = (
     "oscar_decode_attn_mixed", "oscar_decode_step_mixed",
     "oscar_bf16_page_bytes", "oscar_bf16_kv_append", "oscar_bf16_decode_workspace_bytes",
     "oscar_bf16_decode_attn",
+    "oscar_calib_workspace_bytes", "oscar_calib_query_cov", "oscar_calib_attn",
+    "oscar_calib_score_cov", "oscar_calib_rotation_workspace_bytes", "oscar_calib_rotation",
+    "oscar_calib_clip_workspace_bytes", "oscar_calib_clip",
+    "oscar_calibrate_layer_workspace_bytes", "oscar_calibrate_layer",
 )
+
+CALIB_MAX_CANDS = 32
 
 
 class OscarError(RuntimeError):
@@ -105,6 +111,17 @@ def lib() -> ctypes.CDLL:
             "oscar_bf16_decode_workspace_bytes": (sz, [LP, i32, i32, i32]),
             "oscar_bf16_decode_attn": (ctypes.c_int, [LP, P, P, i32, i32, P, i32, P, f32, i32, P,
                                                       sz, P, ctypes.c_int, P]),
+            "oscar_calib_workspace_bytes": (sz, [i64, i32, i32]),
+            "oscar_calib_query_cov": (ctypes.c_int, [P, i64, i32, i32, P, P, sz, P]),
+            "oscar_calib_attn": (ctypes.c_int, [P, P, P, i64, i32, i32, i32, P, P]),
+            "oscar_calib_score_cov": (ctypes.c_int, [P, P, P, i64, i32, i32, i32, P, P, sz, P]),
+            "oscar_calib_rotation_workspace_bytes": (sz, [i32]),
+            "oscar_calib_rotation": (ctypes.c_int, [P, i32, P, P, P, P, P, P, sz, P]),
+            "oscar_calib_clip_workspace_bytes": (sz, [i64, i32, i32]),
+            "oscar_calib_clip": (ctypes.c_int, [LP, P, i64, P, P, i32, P, P, P, sz, P]),
+            "oscar_calibrate_layer_workspace_bytes": (sz, [i64, i32, i32, i32]),
+            "oscar_calibrate_layer": (ctypes.c_int, [LP, P, P, P, i64, i32, i32, P, i32, P, P, P,
+                                                     P, P, P, sz, P]),
         }
         for name, (res, args) in sigs.items():
             fn = getattr(L, name)
@@ -408,3 +425,144 @@ def bf16_decode_attn(layout: Layout, pages, q, block_table, seq_lens, sm_scale: 
         _ptr(workspace, torch.uint8, "workspace"), workspace.numel(),
         _ptr(out, out.dtype, "out", B * Hq * d), out_dtype, _stream(stream))
     _check(st, "oscar_bf16_decode_attn")
+
+
+# ---------------------------------------------------------------------------
+# offline calibration (Sec. 3; Alg. 1 Calibrate)
+# ---------------------------------------------------------------------------
+
+def _ws(n: int, where: str, device="cuda") -> torch.Tensor:
+    if n == 0:
+        raise OscarError(ERR_INVALID_ARG, where)
+    return torch.empty(n, dtype=torch.uint8, device=device)
+
+
+def _qkv_shapes(q, k=None, v=None):
+    if q.dim() != 3 or q.shape[2] != HEAD_DIM:
+        raise ValueError("q must be [T, Hq, %d]" % HEAD_DIM)
+    T, Hq = int(q.shape[0]), int(q.shape[1])
+    Hkv = None
+    if k is not None:
+        if k.dim() != 3 or k.shape[0] != T or k.shape[2] != HEAD_DIM or v is None or \
+                tuple(v.shape) != tuple(k.shape):
+            raise ValueError("k, v must be [T, Hkv, %d] with the same T as q" % HEAD_DIM)
+        Hkv = int(k.shape[1])
+    return T, Hq, Hkv
+
+
+def calib_workspace_bytes(T: int, Hq: int, Hkv: int) -> int:
+    return int(lib().oscar_calib_workspace_bytes(T, Hq, Hkv))
+
+
+def calib_query_cov(q, Hkv: int, workspace=None, stream=None) -> torch.Tensor:
+    """GQA-averaged C_Q (fp64 [d, d]) of bf16 queries q [T, Hq, d]."""
+    T, Hq, _ = _qkv_shapes(q)
+    ws = workspace if workspace is not None else _ws(calib_workspace_bytes(T, Hq, Hkv),
+                                                     "calib_workspace_bytes")
+    C = torch.empty(HEAD_DIM, HEAD_DIM, dtype=torch.float64, device=q.device)
+    _check(lib().oscar_calib_query_cov(_ptr(q, torch.bfloat16, "q"), T, Hq, Hkv,
+                                       _ptr(C, torch.float64, "C"), _ptr(ws, torch.uint8, "ws"),
+                                       ws.numel(), _stream(stream)), "oscar_calib_query_cov")
+    return C
+
+
+def calib_attn(q, k, v, causal: bool = True, out=None, stream=None) -> torch.Tensor:
+    """Attention rows of the calibration pass: fp32 [T, Hq, d]."""
+    T, Hq, Hkv = _qkv_shapes(q, k, v)
+    if out is None:
+        out = torch.empty(T, Hq, HEAD_DIM, dtype=torch.float32, device=q.device)
+    _check(lib().oscar_calib_attn(_ptr(q, torch.bfloat16, "q"), _ptr(k, torch.bfloat16, "k"),
+                                  _ptr(v, torch.bfloat16, "v"), T, Hq, Hkv, int(bool(causal)),
+                                  _ptr(out, torch.float32, "out", T * Hq * HEAD_DIM),
+                                  _stream(stream)), "oscar_calib_attn")
+    return out
+
+
+def calib_score_cov(q, k, v, causal: bool = True, workspace=None, stream=None) -> torch.Tensor:
+    """GQA-averaged C_S = V^T S^T S V / N (fp64 [d, d])."""
+    T, Hq, Hkv = _qkv_shapes(q, k, v)
+    ws = workspace if workspace is not None else _ws(calib_workspace_bytes(T, Hq, Hkv),
+                                                     "calib_workspace_bytes")
+    C = torch.empty(HEAD_DIM, HEAD_DIM, dtype=torch.float64, device=q.device)
+    _check(lib().oscar_calib_score_cov(_ptr(q, torch.bfloat16, "q"), _ptr(k, torch.bfloat16, "k"),
+                                       _ptr(v, torch.bfloat16, "v"), T, Hq, Hkv,
+                                       int(bool(causal)), _ptr(C, torch.float64, "C"),
+                                       _ptr(ws, torch.uint8, "ws"), ws.numel(), _stream(stream)),
+           "oscar_calib_score_cov")
+    return C
+
+
+def calib_rotation(C, workspace=None, stream=None) -> dict:
+    """Eigen-decomposition (descending, sign-fixed) and R = U H_Had P_br of
+    symmetric fp64 matrices C [n, d, d] (or [d, d])."""
+    Cb = C if C.dim() == 3 else C.unsqueeze(0)
+    n = int(Cb.shape[0])
+    if tuple(Cb.shape[1:]) != (HEAD_DIM, HEAD_DIM):
+        raise ValueError("C must be [n, %d, %d]" % (HEAD_DIM, HEAD_DIM))
+    Cb = Cb.contiguous()
+    dev = Cb.device
+    lam = torch.empty(n, HEAD_DIM, dtype=torch.float64, device=dev)
+    U = torch.empty(n, HEAD_DIM, HEAD_DIM, dtype=torch.float64, device=dev)
+    R64 = torch.empty_like(U)
+    R32 = torch.empty(n, HEAD_DIM, HEAD_DIM, dtype=torch.float32, device=dev)
+    info = torch.empty(n, dtype=torch.int32, device=dev)
+    ws = workspace if workspace is not None else _ws(
+        int(lib().oscar_calib_rotation_workspace_bytes(n)), "calib_rotation_workspace_bytes")
+    _check(lib().oscar_calib_rotation(_ptr(Cb, torch.float64, "C"), n, _ptr(lam, torch.float64, "lam"),
+                                      _ptr(U, torch.float64, "U"), _ptr(R64, torch.float64, "R64"),
+                                      _ptr(R32, torch.float32, "R32"), _ptr(info, torch.int32, "info"),
+                                      _ptr(ws, torch.uint8, "ws"), ws.numel(), _stream(stream)),
+           "oscar_calib_rotation")
+    return {"lam": lam, "U": U, "R64": R64, "R32": R32, "info": info}
+
+
+def calib_clip(layout: Layout, x, R, cands, workspace=None, stream=None):
+    """(err [n_cands] fp64, best [1] fp32) for rows x [n_tok, Hkv, d] (bf16)."""
+    if x.dim() != 3 or x.shape[1] != layout.num_kv_heads or x.shape[2] != HEAD_DIM:
+        raise ValueError("x must be [n_tok, Hkv, %d]" % HEAD_DIM)
+    n_tok = int(x.shape[0])
+    nc = int(cands.numel())
+    err = torch.empty(nc, dtype=torch.float64, device=x.device)
+    best = torch.empty(1, dtype=torch.float32, device=x.device)
+    ws = workspace if workspace is not None else _ws(
+        int(lib().oscar_calib_clip_workspace_bytes(n_tok, layout.num_kv_heads, nc)),
+        "calib_clip_workspace_bytes")
+    _check(lib().oscar_calib_clip(ctypes.byref(layout), _ptr(x, torch.bfloat16, "x"), n_tok,
+                                  _rptr(R, "R"), _ptr(cands, torch.float32, "cands"), nc,
+                                  _ptr(err, torch.float64, "err"), _ptr(best, torch.float32, "best"),
+                                  _ptr(ws, torch.uint8, "ws"), ws.numel(), _stream(stream)),
+           "oscar_calib_clip")
+    return err, best
+
+
+def calibrate_layer_workspace_bytes(T: int, Hq: int, Hkv: int, n_cands: int) -> int:
+    return int(lib().oscar_calibrate_layer_workspace_bytes(T, Hq, Hkv, n_cands))
+
+
+def calibrate_layer(layout: Layout, q, k, v, cands, causal: bool = True, workspace=None,
+                    stream=None) -> dict:
+    """Alg. 1 Calibrate for one layer: R_K, R_V (fp32 [d, d]), clip (c_K, c_V),
+    lam [2, d] (spectra of C_Q and C_S) and info [2]."""
+    T, Hq, Hkv = _qkv_shapes(q, k, v)
+    if Hkv != layout.num_kv_heads:
+        raise ValueError("k has %d heads, layout %d" % (Hkv, layout.num_kv_heads))
+    nc = int(cands.numel())
+    dev = q.device
+    Rk = torch.empty(HEAD_DIM, HEAD_DIM, dtype=torch.float32, device=dev)
+    Rv = torch.empty_like(Rk)
+    clip = torch.empty(2, dtype=torch.float32, device=dev)
+    lam = torch.empty(2, HEAD_DIM, dtype=torch.float64, device=dev)
+    info = torch.empty(2, dtype=torch.int32, device=dev)
+    ws = workspace if workspace is not None else _ws(
+        calibrate_layer_workspace_bytes(T, Hq, Hkv, nc), "calibrate_layer_workspace_bytes")
+    _check(lib().oscar_calibrate_layer(ctypes.byref(layout), _ptr(q, torch.bfloat16, "q"),
+                                       _ptr(k, torch.bfloat16, "k"), _ptr(v, torch.bfloat16, "v"),
+                                       T, Hq, int(bool(causal)), _ptr(cands, torch.float32, "cands"),
+                                       nc, _ptr(Rk, torch.float32, "R_k"),
+                                       _ptr(Rv, torch.float32, "R_v"),
+                                       _ptr(clip, torch.float32, "clip"),
+                                       _ptr(lam, torch.float64, "lam"),
+                                       _ptr(info, torch.int32, "info"),
+                                       _ptr(ws, torch.uint8, "ws"), ws.numel(), _stream(stream)),
+           "oscar_calibrate_layer")
+    return {"R_K": Rk, "R_V": Rv, "clip": clip, "lam": lam, "info": info}

@@ -32,6 +32,7 @@ SOURCES = {
     "decode_mfma.hip": ["-mllvm", "-amdgpu-mfma-vgpr-form=1"],
     "bf16_decode.hip": [],
     "mixed.hip": [],
+    "calib.hip": ["-ffp-contract=off"],
 }
 
 

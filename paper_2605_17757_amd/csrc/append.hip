@@ -26,6 +26,7 @@ namespace oscar {
 namespace {
 
 constexpr int kWaves = 4;
+constexpr int kMaxClipCands = 32;  // candidate clip ratios per calibration call
 
 __device__ inline float f16_bits_to_f32(uint16_t h) { return __half2float(__ushort_as_half(h)); }
 
@@ -741,6 +742,115 @@ __global__ __launch_bounds__(256) void prologue_kernel(
   }
 }
 
+// ---------------------------------------------------------------------------
+// Clip calibration (Alg. 1 CalibrateClip).  The paper leaves the procedure open;
+// it is read here as: the candidate ratio whose quantization of the rotated
+// calibration rows has the smallest squared error.  A wave takes rows (token,
+// head) grid-stride and rotates each exactly as the cache update does (lane l:
+// channels l and l + 64); for every candidate it clips and quantizes the row with
+// the cache update's steps and takes sum_c (x~_c - s (code_c - z))^2 in fp64,
+// s and z read back from their stored format.  A row's error is summed over the
+// wave and added, row by row, to the wave's total per candidate; the block adds
+// its waves and writes one partial per candidate, which clip_reduce_kernel sums
+// in block order.
+// ---------------------------------------------------------------------------
+__device__ inline double wave_sum_f64(double x) {
+#pragma unroll
+  for (int o = 32; o >= 1; o >>= 1) x += __shfl_xor(x, o, 64);
+  return x;
+}
+
+__global__ __launch_bounds__(256) void clip_err_kernel(const uint16_t* __restrict__ x, int n_rows,
+                                                       const float* __restrict__ R,
+                                                       const float* __restrict__ cands,
+                                                       int n_cands, QFmt fmt,
+                                                       double* __restrict__ partial) {
+  __shared__ float Rs[kD * kD];
+  __shared__ double xs[kWaves][kD];
+  __shared__ double werr[kWaves][kMaxClipCands];
+  const int w = threadIdx.x >> 6, l = threadIdx.x & 63;
+  if (R) {
+    float4 r4[kD * kD / 4 / 256];
+#pragma unroll
+    for (int i = 0; i < kD * kD / 4 / 256; ++i)
+      r4[i] = reinterpret_cast<const float4*>(R)[threadIdx.x + 256 * i];
+#pragma unroll
+    for (int i = 0; i < kD * kD / 4 / 256; ++i) reinterpret_cast<float4*>(Rs)[threadIdx.x + 256 * i] = r4[i];
+  }
+  if (l < kMaxClipCands) werr[w][l] = 0.0;
+  __syncthreads();
+  for (int row = blockIdx.x * kWaves + w; row < n_rows; row += gridDim.x * kWaves) {
+    const uint32_t pair = reinterpret_cast<const uint32_t*>(x + (size_t)row * kD)[l];
+    xs[w][2 * l] = (double)__uint_as_float(pair << 16);
+    xs[w][2 * l + 1] = (double)__uint_as_float(pair & 0xffff0000u);
+    double acc0 = 0.0, acc1 = 0.0;
+    if (R) {
+#pragma unroll 4
+      for (int c = 0; c < kD; ++c) {
+        const double xc = xs[w][c];
+        acc0 = __fma_rn(xc, (double)Rs[c * kD + l], acc0);
+        acc1 = __fma_rn(xc, (double)Rs[c * kD + l + 64], acc1);
+      }
+    } else {
+      acc0 = xs[w][l];
+      acc1 = xs[w][l + 64];
+    }
+    const float xt0 = __double2float_rn(acc0), xt1 = __double2float_rn(acc1);
+    for (int n = 0; n < n_cands; ++n) {
+      const float clip = cands[n];
+      float tau0, tau1;
+      if (fmt.quantile) {
+        tau0 = tau1 = token_quantile_wave(xt0, xt1, clip);
+      } else {
+        group_reduce2<true>(fabsf(xt0), fabsf(xt1), fmt.ng, tau0, tau1);
+        tau0 = __fmul_rn(clip, tau0);
+        tau1 = __fmul_rn(clip, tau1);
+      }
+      const float y0 = fminf(fmaxf(xt0, -tau0), tau0), y1 = fminf(fmaxf(xt1, -tau1), tau1);
+      float a0, a1, b0, b1;
+      group_reduce2<false>(y0, y1, fmt.ng, a0, a1);
+      group_reduce2<true>(y0, y1, fmt.ng, b0, b1);
+      const QOut q0 = quantize(y0, a0, b0, fmt);
+      const QOut q1 = quantize(y1, a1, b1, fmt);
+      const double d0 = (double)xt0 - (double)meta_load(fmt, q0.s16) *
+                                          ((double)q0.code - (double)meta_load(fmt, q0.z16));
+      const double d1 = (double)xt1 - (double)meta_load(fmt, q1.s16) *
+                                          ((double)q1.code - (double)meta_load(fmt, q1.z16));
+      const double rs = wave_sum_f64(d0 * d0 + d1 * d1);
+      if (l == 0) werr[w][n] += rs;
+    }
+  }
+  __syncthreads();
+  if ((int)threadIdx.x < n_cands) {
+    const int n = threadIdx.x;
+    partial[(size_t)blockIdx.x * n_cands + n] = ((werr[0][n] + werr[1][n]) + werr[2][n]) + werr[3][n];
+  }
+}
+
+// err[n] = (sum of the blocks' partials, in block order) / (n_rows d); best = the
+// candidate of the first minimum.
+__global__ __launch_bounds__(64) void clip_reduce_kernel(const double* __restrict__ partial,
+                                                         int n_blocks, int n_cands,
+                                                         const float* __restrict__ cands,
+                                                         double inv_n, double* __restrict__ err,
+                                                         float* __restrict__ best) {
+  __shared__ double es[kMaxClipCands];
+  const int n = threadIdx.x;
+  if (n < n_cands) {
+    double acc = 0.0;
+    for (int b = 0; b < n_blocks; ++b) acc += partial[(size_t)b * n_cands + n];
+    es[n] = acc * inv_n;
+    err[n] = es[n];
+  }
+  __syncthreads();
+  if (n == 0 && best) {
+    int arg = 0;
+    for (int i = 1; i < n_cands; ++i)
+      if (es[i] < es[arg]) arg = i;
+    best[0] = cands[arg];
+  }
+}
+
 }  // namespace
 
 namespace {
@@ -855,6 +965,24 @@ hipError_t launch_mixed_step_prologue(void* pages, uint16_t* seg, int64_t Hkv, i
   const StepRows rows{k, v, seg, seq_lens, block_table, (int)n_rows, (int)Hkv, max_pages, S0, W};
   return launch_prologue(pages, Hkv, rows, n_rows, Rk, Rv, clip_k, clip_v, fmt, q, B, Hq, qscale,
                          qt, st);
+}
+
+hipError_t launch_clip_errors(const uint16_t* x, int64_t n_rows, const float* R,
+                              const float* cands, int n_cands, QuantFmt fmt, double* partial,
+                              int n_blocks, double* err, float* best, hipStream_t st) {
+  hipLaunchKernelGGL(clip_err_kernel, dim3((unsigned)n_blocks), dim3(256), 0, st, x, (int)n_rows, R,
+                     cands, n_cands, fmt, partial);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL(clip_reduce_kernel, dim3(1), dim3(64), 0, st, partial, n_blocks, n_cands,
+                     cands, 1.0 / ((double)n_rows * kD), err, best);
+  return hipGetLastError();
+}
+
+int clip_blocks(int64_t n_rows) {
+  const int64_t items = (n_rows + kWaves - 1) / kWaves;
+  const int64_t cap = 4 * (int64_t)device_cus();
+  return (int)std::max<int64_t>(1, std::min(items, cap));
 }
 
 }  // namespace oscar

@@ -117,4 +117,30 @@ hipError_t launch_bf16_split(const uint16_t* pages, int Hkv, int B, int Hq,
                              const int32_t* seq_lens, int num_splits, const float* qt,
                              float* part_o, float* part_ml, hipStream_t st);
 
+// Offline calibration.
+// Second moment C = (X^T X) * inv_n of rows X [n_rows][128] (bf16 or fp32), fp64
+// [128][128]; partial: gram_partial_bytes(n_rows) bytes of scratch.
+size_t gram_partial_bytes(int64_t n_rows);
+hipError_t launch_gram(const void* X, int x_bf16, int64_t n_rows, double inv_n, float* partial,
+                       double* C, hipStream_t st);
+// O[t][i] = softmax(q_{t,i} K_h^T / sqrt(d) + M) V_h (fp32 [T][Hq][128]).
+hipError_t launch_calib_attn(const uint16_t* q, const uint16_t* k, const uint16_t* v, int T,
+                             int Hq, int Hkv, int causal, float* out, hipStream_t st);
+// Symmetric eigen-decomposition of n_mats matrices [128][128] (fp64): lam
+// descending, U columns sign-fixed; scratch diag [n][128], rot eig_rot_bytes,
+// n_rounds [n], V [n][128][128]; info [n] = sweeps run or -1.
+size_t eig_rot_bytes(int n_mats, int max_sweeps);
+hipError_t launch_eig(const double* C, int n_mats, int max_sweeps, double* diag, double2* rot,
+                      int* n_rounds, double* V, double* lam, double* U, int* info,
+                      hipStream_t st);
+// R = U H_Had P_br for n_mats matrices (either output may be nullptr).
+hipError_t launch_compose(const double* U, int n_mats, double* R64, float* R32, hipStream_t st);
+// Mean squared quantization error of the rotated rows for each candidate clip
+// ratio (n_cands <= 32) and the first minimizing candidate; partial: n_blocks x
+// n_cands doubles, n_blocks = clip_blocks(n_rows).
+int clip_blocks(int64_t n_rows);
+hipError_t launch_clip_errors(const uint16_t* x, int64_t n_rows, const float* R,
+                              const float* cands, int n_cands, QuantFmt fmt, double* partial,
+                              int n_blocks, double* err, float* best, hipStream_t st);
+
 }  // namespace oscar

@@ -519,3 +519,249 @@ int oscar_bf16_decode_attn(const oscar_layout* L, const void* pages, const void*
 }
 
 }  // extern "C"
+
+// ---------------------------------------------------------------------------
+// Offline calibration
+// ---------------------------------------------------------------------------
+
+namespace {
+
+constexpr int kCalibMaxSweeps = OSCAR_CALIB_MAX_SWEEPS;
+
+int check_calib(int64_t T, int32_t Hq, int32_t Hkv) {
+  if (T < 1 || Hkv < 1 || Hq < Hkv || Hq % Hkv != 0) return OSCAR_ERR_INVALID_ARG;
+  const int64_t g = Hq / Hkv;
+  const int64_t hc = g % 4 == 0 ? 4 : g % 2 == 0 ? 2 : 1;
+  const int64_t span = 32 * 8 / hc;
+  if ((T + span - 1) / span > 65535 || Hq / hc > 65535) return OSCAR_ERR_UNSUPPORTED;
+  return OSCAR_OK;
+}
+
+struct CalibWs {
+  size_t o_off, part_off, total;
+};
+CalibWs calib_ws(int64_t T, int32_t Hq) {
+  CalibWs w;
+  w.o_off = 0;
+  w.part_off = align256((size_t)T * Hq * kD * sizeof(float));
+  w.total = align256(w.part_off + gram_partial_bytes(T * Hq));
+  return w;
+}
+
+struct RotWs {
+  size_t diag_off, rot_off, rounds_off, v_off, info_off, total;
+};
+RotWs rot_ws(int32_t n) {
+  RotWs w;
+  w.diag_off = 0;
+  w.rot_off = align256(w.diag_off + (size_t)n * kD * sizeof(double));
+  w.rounds_off = align256(w.rot_off + eig_rot_bytes(n, kCalibMaxSweeps));
+  w.v_off = align256(w.rounds_off + (size_t)n * sizeof(int));
+  w.info_off = align256(w.v_off + (size_t)n * kD * kD * sizeof(double));
+  w.total = align256(w.info_off + (size_t)n * sizeof(int));
+  return w;
+}
+
+size_t clip_ws_bytes(int64_t n_rows, int32_t n_cands) {
+  return align256((size_t)clip_blocks(n_rows) * n_cands * sizeof(double));
+}
+
+bool cands_shape_ok(int32_t n_cands) { return n_cands >= 1 && n_cands <= OSCAR_CALIB_MAX_CANDS; }
+
+struct LayerWs {
+  size_t c_off, calib_off, rot_off, lam_off, u_off, clip_off, err_off, info_off, total;
+};
+LayerWs layer_ws(int64_t T, int32_t Hq, int32_t Hkv, int32_t n_cands) {
+  LayerWs w;
+  w.c_off = 0;
+  w.calib_off = align256(2 * (size_t)kD * kD * sizeof(double));
+  w.rot_off = align256(w.calib_off + calib_ws(T, Hq).total);
+  w.lam_off = align256(w.rot_off + rot_ws(2).total);
+  w.u_off = align256(w.lam_off + 2 * (size_t)kD * sizeof(double));
+  w.clip_off = align256(w.u_off + 2 * (size_t)kD * kD * sizeof(double));
+  w.err_off = align256(w.clip_off + clip_ws_bytes(T * Hkv, n_cands));
+  w.info_off = align256(w.err_off + 2 * (size_t)n_cands * sizeof(double));
+  w.total = align256(w.info_off + 2 * sizeof(int));
+  return w;
+}
+
+int query_cov_impl(const void* q, int64_t T, int32_t Hq, double* C, char* ws, hipStream_t st) {
+  const CalibWs w = calib_ws(T, Hq);
+  return hip_status(launch_gram(q, 1, T * Hq, 1.0 / ((double)T * Hq),
+                                reinterpret_cast<float*>(ws + w.part_off), C, st));
+}
+
+int score_cov_impl(const void* q, const void* k, const void* v, int64_t T, int32_t Hq,
+                   int32_t Hkv, int32_t causal, double* C, char* ws, hipStream_t st) {
+  const CalibWs w = calib_ws(T, Hq);
+  float* O = reinterpret_cast<float*>(ws + w.o_off);
+  hipError_t e = launch_calib_attn(static_cast<const uint16_t*>(q), static_cast<const uint16_t*>(k),
+                                   static_cast<const uint16_t*>(v), (int)T, Hq, Hkv, causal ? 1 : 0,
+                                   O, st);
+  if (e != hipSuccess) return OSCAR_ERR_HIP;
+  return hip_status(launch_gram(O, 0, T * Hq, 1.0 / ((double)T * Hq),
+                                reinterpret_cast<float*>(ws + w.part_off), C, st));
+}
+
+int rotation_impl(const double* C, int32_t n, double* lam, double* U, double* R64, float* R32,
+                  int32_t* info, char* ws, hipStream_t st) {
+  const RotWs w = rot_ws(n);
+  int* inf = info ? info : reinterpret_cast<int*>(ws + w.info_off);
+  hipError_t e = launch_eig(C, n, kCalibMaxSweeps, reinterpret_cast<double*>(ws + w.diag_off),
+                            reinterpret_cast<double2*>(ws + w.rot_off),
+                            reinterpret_cast<int*>(ws + w.rounds_off),
+                            reinterpret_cast<double*>(ws + w.v_off), lam, U, inf, st);
+  if (e != hipSuccess) return OSCAR_ERR_HIP;
+  return hip_status(launch_compose(U, n, R64, R32, st));
+}
+
+bool cands_values_ok(const float* cands, int32_t n) {
+  // candidate ratios live on the device; only their count is checked here
+  return cands != nullptr && n >= 1;
+}
+
+}  // namespace
+
+extern "C" {
+
+size_t oscar_calib_workspace_bytes(int64_t T, int32_t Hq, int32_t Hkv) {
+  if (check_calib(T, Hq, Hkv) != OSCAR_OK) return 0;
+  return calib_ws(T, Hq).total;
+}
+
+int oscar_calib_query_cov(const void* q, int64_t T, int32_t Hq, int32_t Hkv, double* C,
+                          void* workspace, size_t workspace_bytes, void* stream) {
+  int st = check_calib(T, Hq, Hkv);
+  if (st) return st;
+  if (!q || !C || !workspace || !aligned(q, 16) || !aligned(C, 8) || !aligned(workspace, 256))
+    return OSCAR_ERR_INVALID_ARG;
+  if (workspace_bytes < calib_ws(T, Hq).total) return OSCAR_ERR_WORKSPACE_TOO_SMALL;
+  return query_cov_impl(q, T, Hq, C, static_cast<char*>(workspace),
+                        static_cast<hipStream_t>(stream));
+}
+
+int oscar_calib_attn(const void* q, const void* k, const void* v, int64_t T, int32_t Hq,
+                     int32_t Hkv, int32_t causal, float* out, void* stream) {
+  int st = check_calib(T, Hq, Hkv);
+  if (st) return st;
+  if (!q || !k || !v || !out || !aligned(q, 16) || !aligned(k, 16) || !aligned(v, 16) ||
+      !aligned(out, 16))
+    return OSCAR_ERR_INVALID_ARG;
+  return hip_status(launch_calib_attn(static_cast<const uint16_t*>(q),
+                                      static_cast<const uint16_t*>(k),
+                                      static_cast<const uint16_t*>(v), (int)T, Hq, Hkv,
+                                      causal ? 1 : 0, out, static_cast<hipStream_t>(stream)));
+}
+
+int oscar_calib_score_cov(const void* q, const void* k, const void* v, int64_t T, int32_t Hq,
+                          int32_t Hkv, int32_t causal, double* C, void* workspace,
+                          size_t workspace_bytes, void* stream) {
+  int st = check_calib(T, Hq, Hkv);
+  if (st) return st;
+  if (!q || !k || !v || !C || !workspace || !aligned(q, 16) || !aligned(k, 16) ||
+      !aligned(v, 16) || !aligned(C, 8) || !aligned(workspace, 256))
+    return OSCAR_ERR_INVALID_ARG;
+  if (workspace_bytes < calib_ws(T, Hq).total) return OSCAR_ERR_WORKSPACE_TOO_SMALL;
+  return score_cov_impl(q, k, v, T, Hq, Hkv, causal, C, static_cast<char*>(workspace),
+                        static_cast<hipStream_t>(stream));
+}
+
+size_t oscar_calib_rotation_workspace_bytes(int32_t n_mats) {
+  if (n_mats < 1 || n_mats > 65535) return 0;
+  return rot_ws(n_mats).total;
+}
+
+int oscar_calib_rotation(const double* C, int32_t n_mats, double* lam, double* U, double* R64,
+                         float* R32, int32_t* info, void* workspace, size_t workspace_bytes,
+                         void* stream) {
+  if (n_mats < 1 || !C || !lam || !U || !workspace) return OSCAR_ERR_INVALID_ARG;
+  if (n_mats > 65535) return OSCAR_ERR_UNSUPPORTED;
+  if (!aligned(C, 8) || !aligned(lam, 8) || !aligned(U, 8) || !aligned(R64, 8) ||
+      !aligned(R32, 4) || !aligned(info, 4) || !aligned(workspace, 256))
+    return OSCAR_ERR_INVALID_ARG;
+  if (workspace_bytes < rot_ws(n_mats).total) return OSCAR_ERR_WORKSPACE_TOO_SMALL;
+  return rotation_impl(C, n_mats, lam, U, R64, R32, info, static_cast<char*>(workspace),
+                       static_cast<hipStream_t>(stream));
+}
+
+size_t oscar_calib_clip_workspace_bytes(int64_t n_tok, int32_t Hkv, int32_t n_cands) {
+  if (n_tok < 1 || Hkv < 1 || !cands_shape_ok(n_cands)) return 0;
+  if (n_tok * Hkv > 0x7fffffffLL) return 0;
+  return clip_ws_bytes(n_tok * Hkv, n_cands);
+}
+
+int oscar_calib_clip(const oscar_layout* L, const void* x, int64_t n_tok, const float* R,
+                     const float* cands, int32_t n_cands, double* err, float* best,
+                     void* workspace, size_t workspace_bytes, void* stream) {
+  int st = check_layout(L);
+  if (st) return st;
+  if (n_tok < 1 || !x || !err || !workspace || !cands_values_ok(cands, n_cands))
+    return OSCAR_ERR_INVALID_ARG;
+  if (!cands_shape_ok(n_cands)) return OSCAR_ERR_UNSUPPORTED;
+  if (n_tok * L->num_kv_heads > 0x7fffffffLL) return OSCAR_ERR_UNSUPPORTED;
+  if (!aligned(x, 4) || !aligned(R, 16) || !aligned(cands, 4) || !aligned(err, 8) ||
+      !aligned(best, 4) || !aligned(workspace, 256))
+    return OSCAR_ERR_INVALID_ARG;
+  const int64_t rows = n_tok * L->num_kv_heads;
+  if (workspace_bytes < clip_ws_bytes(rows, n_cands)) return OSCAR_ERR_WORKSPACE_TOO_SMALL;
+  return hip_status(launch_clip_errors(static_cast<const uint16_t*>(x), rows, R, cands, n_cands,
+                                       quant_fmt(L), static_cast<double*>(workspace),
+                                       clip_blocks(rows), err, best,
+                                       static_cast<hipStream_t>(stream)));
+}
+
+size_t oscar_calibrate_layer_workspace_bytes(int64_t T, int32_t Hq, int32_t Hkv,
+                                             int32_t n_cands) {
+  if (check_calib(T, Hq, Hkv) != OSCAR_OK || !cands_shape_ok(n_cands)) return 0;
+  if (T * Hkv > 0x7fffffffLL) return 0;
+  return layer_ws(T, Hq, Hkv, n_cands).total;
+}
+
+int oscar_calibrate_layer(const oscar_layout* L, const void* q, const void* k, const void* v,
+                          int64_t T, int32_t Hq, int32_t causal, const float* cands,
+                          int32_t n_cands, float* R_k, float* R_v, float* clip, double* lam,
+                          int32_t* info, void* workspace, size_t workspace_bytes,
+                          void* stream) {
+  int st = check_layout(L);
+  if (st) return st;
+  const int32_t Hkv = L->num_kv_heads;
+  st = check_calib(T, Hq, Hkv);
+  if (st) return st;
+  if (!q || !k || !v || !R_k || !R_v || !clip || !workspace || !cands_values_ok(cands, n_cands))
+    return OSCAR_ERR_INVALID_ARG;
+  if (!cands_shape_ok(n_cands)) return OSCAR_ERR_UNSUPPORTED;
+  if (T * Hkv > 0x7fffffffLL) return OSCAR_ERR_UNSUPPORTED;
+  if (!aligned(q, 16) || !aligned(k, 16) || !aligned(v, 16) || !aligned(R_k, 16) ||
+      !aligned(R_v, 16) || !aligned(clip, 4) || !aligned(lam, 8) || !aligned(info, 4) ||
+      !aligned(cands, 4) || !aligned(workspace, 256))
+    return OSCAR_ERR_INVALID_ARG;
+  const LayerWs w = layer_ws(T, Hq, Hkv, n_cands);
+  if (workspace_bytes < w.total) return OSCAR_ERR_WORKSPACE_TOO_SMALL;
+  char* ws = static_cast<char*>(workspace);
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  double* C = reinterpret_cast<double*>(ws + w.c_off);  // [2][d][d]: C_Q, C_S
+  double* lm = lam ? lam : reinterpret_cast<double*>(ws + w.lam_off);
+  double* U = reinterpret_cast<double*>(ws + w.u_off);
+  int32_t* inf = info ? info : reinterpret_cast<int32_t*>(ws + w.info_off);
+  double* err = reinterpret_cast<double*>(ws + w.err_off);
+  char* cw = ws + w.calib_off;
+  if ((st = query_cov_impl(q, T, Hq, C, cw, s))) return st;
+  if ((st = score_cov_impl(q, k, v, T, Hq, Hkv, causal, C + kD * kD, cw, s))) return st;
+  // R_k and R_v are adjacent only through the caller's pointers: compose each
+  if ((st = rotation_impl(C, 2, lm, U, nullptr, nullptr, inf, ws + w.rot_off, s))) return st;
+  if (launch_compose(U, 1, nullptr, R_k, s) != hipSuccess) return OSCAR_ERR_HIP;
+  if (launch_compose(U + kD * kD, 1, nullptr, R_v, s) != hipSuccess) return OSCAR_ERR_HIP;
+  const QuantFmt fmt = quant_fmt(L);
+  const int64_t rows = T * Hkv;
+  const int nb = clip_blocks(rows);
+  double* part = reinterpret_cast<double*>(ws + w.clip_off);
+  if (launch_clip_errors(static_cast<const uint16_t*>(k), rows, R_k, cands, n_cands, fmt, part, nb,
+                         err, clip, s) != hipSuccess)
+    return OSCAR_ERR_HIP;
+  if (launch_clip_errors(static_cast<const uint16_t*>(v), rows, R_v, cands, n_cands, fmt, part, nb,
+                         err + n_cands, clip + 1, s) != hipSuccess)
+    return OSCAR_ERR_HIP;
+  return OSCAR_OK;
+}
+
+}  // extern "C"

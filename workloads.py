@@ -261,3 +261,36 @@ def slots_for(table: np.ndarray, b: int, positions, P: int = PAGE_SIZE) -> np.nd
     """slot = page * P + offset for token positions of sequence b."""
     pos = np.asarray(positions, np.int64)
     return table[b, pos // P].astype(np.int64) * P + pos % P
+
+
+# ---------------------------------------------------------------------------
+# Calibration activations (one layer's Q, K, V dump)
+# ---------------------------------------------------------------------------
+
+CALIB_TOKENS = 8878  # the paper's calibration pass length per layer
+
+
+def calib_activations(T: int, Hq: int, Hkv: int, seed: int, d: int = HEAD_DIM,
+                      device="cpu"):
+    """Synthetic calibration activations, bf16 [T, Hq, d] and [T, Hkv, d] x 2.
+    Queries: Gaussian with covariance B diag(lambda) B^T, lambda the paper-like
+    descending spectrum (162.5 .. 0.009) and B a seeded random orthogonal basis
+    shared by all heads.  Keys: Gaussian with four outlier channels scaled by 15
+    and a common offset of 0.5 on eight channels (keys carry a mean).  Values:
+    standard Gaussian with two channels scaled by 4."""
+    rng = _rng(seed)
+    basis, _ = np.linalg.qr(rng.standard_normal((d, d)))
+    lam = paper_like_spectrum(d)
+    mix = torch.from_numpy((np.sqrt(lam)[:, None] * basis.T).astype(np.float32)).to(device)
+    k_out = torch.tensor(sorted(rng.choice(d, 4, replace=False).tolist()), device=device)
+    k_mean = torch.tensor(sorted(rng.choice(d, 8, replace=False).tolist()), device=device)
+    v_out = torch.tensor(sorted(rng.choice(d, 2, replace=False).tolist()), device=device)
+    g = _gen(seed * 7 + 1, device)
+    z = torch.randn(T * Hq, d, generator=g, device=device, dtype=torch.float32)
+    q = (z @ mix).reshape(T, Hq, d)
+    k = torch.randn(T, Hkv, d, generator=g, device=device, dtype=torch.float32)
+    k[..., k_out] *= 15.0
+    k[..., k_mean] += 0.5
+    v = torch.randn(T, Hkv, d, generator=g, device=device, dtype=torch.float32)
+    v[..., v_out] *= 4.0
+    return q.to(torch.bfloat16), k.to(torch.bfloat16), v.to(torch.bfloat16)
