@@ -22,7 +22,9 @@ sequences.  `mixed_cache_step` is oscar_decode_step_mixed on the same sequences
 with a bf16 sink of 64 and a bf16 window of 256 tokens around the INT2 history.
 `variants` times the same step with the cache in other quantizer formats: the
 paper's stated one (128-channel groups, bf16 scale/zero, per-token quantile clip)
-and identity R_V.
+and identity R_V.  `prefill_128k_tokens` times one 131072-token prompt written
+by oscar_mixed_append.  `calibration` times the offline calibration of one layer
+(oscar_calibrate_layer on 8878 synthetic calibration tokens) and its stages.
 """
 from __future__ import annotations
 
@@ -65,6 +67,8 @@ def parse():
                     help="skip the prefill-scale cache write (one 131072-token prompt)")
     ap.add_argument("--no-variants", action="store_true",
                     help="skip the quantizer-variant steps (paper format, identity R_V)")
+    ap.add_argument("--no-calib", action="store_true",
+                    help="skip the offline calibration of one layer (8878 tokens)")
     ap.add_argument("--no-mixed", action="store_true",
                     help="skip the mixed-precision cache step (bf16 sink + window)")
     ap.add_argument("--sink", type=int, default=64, help="mixed cache: bf16 sink tokens S0")
@@ -509,6 +513,62 @@ def main():
             "kv_footprint_ratio": round(BF16_BYTES_PER_TOKEN_HEAD / INT2_BYTES_PER_TOKEN_HEAD, 3),
         }
         del bf_pool
+
+    # ---- offline calibration of one layer (Alg. 1 Calibrate): 8878 calibration
+    # tokens of this layer shape, the paper's quantizer format for the clip ratios ----
+    if not args.no_calib:
+        torch.cuda.empty_cache()
+        Tc = W.CALIB_TOKENS
+        cq, ck, cv = (t.to(dev) for t in W.calib_activations(Tc, Hq, Hkv, 4242))
+        clay = ok.Layout(num_kv_heads=Hkv, num_pages=1, group_size=128,
+                         clip_mode=ok.CLIP_TOKEN_QUANTILE, meta_dtype=ok.META_BF16)
+        cands = torch.tensor([round(0.80 + 0.01 * n, 2) for n in range(21)],
+                             dtype=torch.float32, device=dev)
+        cws = torch.empty(ok.calibrate_layer_workspace_bytes(Tc, Hq, Hkv, cands.numel()),
+                          dtype=torch.uint8, device=dev)
+        cal = ok.calibrate_layer(clay, cq, ck, cv, cands, workspace=cws)
+        torch.cuda.synchronize()
+
+        def ev_time(fn, n):
+            for _ in range(2):
+                fn()
+            a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            torch.cuda.synchronize()
+            a.record(stream)
+            for _ in range(n):
+                fn()
+            b.record(stream)
+            torch.cuda.synchronize()
+            return a.elapsed_time(b) * 1e3 / n
+
+        layer_us = ev_time(lambda: ok.calibrate_layer(clay, cq, ck, cv, cands, workspace=cws), 5)
+        obuf = torch.empty(Tc, Hq, d, dtype=torch.float32, device=dev)
+        attn_us = ev_time(lambda: ok.calib_attn(cq, ck, cv, out=obuf), 10)
+        sws = torch.empty(ok.calib_workspace_bytes(Tc, Hq, Hkv), dtype=torch.uint8, device=dev)
+        cq_us = ev_time(lambda: ok.calib_query_cov(cq, Hkv, workspace=sws), 10)
+        cs_us = ev_time(lambda: ok.calib_score_cov(cq, ck, cv, workspace=sws), 5)
+        Cst = torch.stack([ok.calib_query_cov(cq, Hkv, workspace=sws),
+                           ok.calib_score_cov(cq, ck, cv, workspace=sws)])
+        rot_us = ev_time(lambda: ok.calib_rotation(Cst), 3)
+        clip_us = ev_time(lambda: ok.calib_clip(clay, ck, cal["R_K"], cands), 5)
+        pairs = Tc * (Tc + 1) // 2                 # causal (query, key) pairs per head
+        attn_flop = pairs * Hq * 4 * d             # q k^T and p v, 2 d each
+        res["calibration"] = {
+            "tokens": Tc, "q_heads": Hq, "kv_heads": Hkv, "causal": True,
+            "clip_format": "G=128, bf16 scale/zero, token quantile", "candidates": cands.numel(),
+            "us_per_layer": round(layer_us, 1),
+            "stages_us": {"query_cov": round(cq_us, 1), "score_cov": round(cs_us, 1),
+                          "attn": round(attn_us, 1), "rotation_2_matrices": round(rot_us, 1),
+                          "clip_one_tensor": round(clip_us, 1)},
+            "attn_roofline": {"bound": "mfma", "flop": attn_flop,
+                              "achieved_tflops": round(attn_flop / (attn_us * 1e-6) / 1e12, 1),
+                              "peak_tflops_bf16": 2500.0,
+                              "frac": round(attn_flop / (attn_us * 1e-6) / 1e12 / 2500.0, 4)},
+            "sweeps": [int(x) for x in cal["info"].tolist()],
+            "clip": [round(float(x), 2) for x in cal["clip"].tolist()],
+        }
+        del cq, ck, cv, cws, obuf, sws, Cst
+        torch.cuda.empty_cache()
 
     # ---- device copy probe (achievable HBM bandwidth) ----
     src = torch.empty(1 << 30, dtype=torch.uint8, device=dev)

@@ -748,16 +748,39 @@ __global__ __launch_bounds__(256) void prologue_kernel(
 // calibration rows has the smallest squared error.  A wave takes rows (token,
 // head) grid-stride and rotates each exactly as the cache update does (lane l:
 // channels l and l + 64); for every candidate it clips and quantizes the row with
-// the cache update's steps and takes sum_c (x~_c - s (code_c - z))^2 in fp64,
-// s and z read back from their stored format.  A row's error is summed over the
-// wave and added, row by row, to the wave's total per candidate; the block adds
-// its waves and writes one partial per candidate, which clip_reduce_kernel sums
-// in block order.
+// the cache update's steps and adds (x~_c - s (code_c - z))^2 in fp64, s and z
+// read back from their stored format, to the lane's sum for that candidate.  The
+// clip threshold is formed as in the cache update: ratio x group absmax (the
+// group maxima found once per row), or the token quantile a_k + f (a_{k+1} - a_k)
+// read from the row's |x~| sorted once per row (bitonic network over the wave).
+// At the end the lanes, the waves and then (clip_reduce_kernel) the blocks are
+// summed in a fixed order.
 // ---------------------------------------------------------------------------
 __device__ inline double wave_sum_f64(double x) {
 #pragma unroll
   for (int o = 32; o >= 1; o >>= 1) x += __shfl_xor(x, o, 64);
   return x;
+}
+
+// Ascending sort of the 128 values (element 2 l + s in slot s of lane l).
+__device__ inline void wave_sort128(float& v0, float& v1, int l) {
+#pragma unroll
+  for (int k = 2; k <= kD; k <<= 1) {
+#pragma unroll
+    for (int j = k >> 1; j >= 2; j >>= 1) {
+      const bool lower = ((2 * l) & j) == 0, asc = ((2 * l) & k) == 0;
+      const float o0 = __shfl_xor(v0, j >> 1, 64), o1 = __shfl_xor(v1, j >> 1, 64);
+      v0 = (lower == asc) ? fminf(v0, o0) : fmaxf(v0, o0);
+      v1 = (lower == asc) ? fminf(v1, o1) : fmaxf(v1, o1);
+    }
+    const bool asc = ((2 * l) & k) == 0;  // j = 1: the lane's own pair
+    const float lo = fminf(v0, v1), hi = fmaxf(v0, v1);
+    v0 = asc ? lo : hi;
+    v1 = asc ? hi : lo;
+  }
+}
+__device__ inline float sorted_at(float v0, float v1, int e) {  // e wave-uniform
+  return __int_as_float(__builtin_amdgcn_readlane(__float_as_int((e & 1) ? v1 : v0), e >> 1));
 }
 
 __global__ __launch_bounds__(256) void clip_err_kernel(const uint16_t* __restrict__ x, int n_rows,
@@ -777,8 +800,10 @@ __global__ __launch_bounds__(256) void clip_err_kernel(const uint16_t* __restric
 #pragma unroll
     for (int i = 0; i < kD * kD / 4 / 256; ++i) reinterpret_cast<float4*>(Rs)[threadIdx.x + 256 * i] = r4[i];
   }
-  if (l < kMaxClipCands) werr[w][l] = 0.0;
   __syncthreads();
+  double e[kMaxClipCands];
+#pragma unroll
+  for (int n = 0; n < kMaxClipCands; ++n) e[n] = 0.0;
   for (int row = blockIdx.x * kWaves + w; row < n_rows; row += gridDim.x * kWaves) {
     const uint32_t pair = reinterpret_cast<const uint32_t*>(x + (size_t)row * kD)[l];
     xs[w][2 * l] = (double)__uint_as_float(pair << 16);
@@ -796,15 +821,29 @@ __global__ __launch_bounds__(256) void clip_err_kernel(const uint16_t* __restric
       acc1 = xs[w][l + 64];
     }
     const float xt0 = __double2float_rn(acc0), xt1 = __double2float_rn(acc1);
-    for (int n = 0; n < n_cands; ++n) {
+    float g0, g1, s0 = 0.0f, s1 = 0.0f;
+    if (fmt.quantile) {
+      s0 = fabsf(xt0);
+      s1 = fabsf(xt1);
+      wave_sort128(s0, s1, l);
+    } else {
+      group_reduce2<true>(fabsf(xt0), fabsf(xt1), fmt.ng, g0, g1);
+    }
+#pragma clang loop unroll(full)
+    for (int n = 0; n < kMaxClipCands; ++n) {
+      if (n >= n_cands) continue;
       const float clip = cands[n];
       float tau0, tau1;
       if (fmt.quantile) {
-        tau0 = tau1 = token_quantile_wave(xt0, xt1, clip);
+        int k;
+        float f;
+        quantile_pos(clip, k, f);
+        k = __builtin_amdgcn_readfirstlane(k);
+        const float ak = sorted_at(s0, s1, k);
+        tau0 = tau1 = k >= kD - 1 ? ak : lerp_tau(ak, sorted_at(s0, s1, k + 1), f);
       } else {
-        group_reduce2<true>(fabsf(xt0), fabsf(xt1), fmt.ng, tau0, tau1);
-        tau0 = __fmul_rn(clip, tau0);
-        tau1 = __fmul_rn(clip, tau1);
+        tau0 = __fmul_rn(clip, g0);
+        tau1 = __fmul_rn(clip, g1);
       }
       const float y0 = fminf(fmaxf(xt0, -tau0), tau0), y1 = fminf(fmaxf(xt1, -tau1), tau1);
       float a0, a1, b0, b1;
@@ -816,9 +855,14 @@ __global__ __launch_bounds__(256) void clip_err_kernel(const uint16_t* __restric
                                           ((double)q0.code - (double)meta_load(fmt, q0.z16));
       const double d1 = (double)xt1 - (double)meta_load(fmt, q1.s16) *
                                           ((double)q1.code - (double)meta_load(fmt, q1.z16));
-      const double rs = wave_sum_f64(d0 * d0 + d1 * d1);
-      if (l == 0) werr[w][n] += rs;
+      e[n] += d0 * d0 + d1 * d1;
     }
+  }
+#pragma unroll
+  for (int n = 0; n < kMaxClipCands; ++n) {
+    if (n >= n_cands) continue;
+    const double t = wave_sum_f64(e[n]);
+    if (l == 0) werr[w][n] = t;
   }
   __syncthreads();
   if ((int)threadIdx.x < n_cands) {

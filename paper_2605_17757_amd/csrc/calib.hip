@@ -107,19 +107,31 @@ __global__ __launch_bounds__(kGramWaves * 64) void gram_kernel(const void* __res
   }
 }
 
-// C[i][j] = C[j][i] = (sum over blocks, in block order, in fp64) * inv_n.
+// C[i][j] = C[j][i] = (sum over the blocks' partial tiles, in fp64) * inv_n.  A
+// block takes 32 elements; thread (element e, part p) adds blocks p, p + 8, ...
+// in order, then part 0 adds the 8 sums in order (a fixed order: deterministic).
+constexpr int kRedParts = 8;
+
 __global__ __launch_bounds__(256) void gram_reduce_kernel(const float* __restrict__ partial,
                                                           int n_blocks, double inv_n,
                                                           double* __restrict__ C) {
-  const int e = blockIdx.x * 256 + threadIdx.x;  // tile * 1024 + element
-  if (e >= kGramTiles * 1024) return;
-  const int t = e >> 10, ij = e & 1023;
+  __shared__ double sums[kRedParts][32];
+  const int el = threadIdx.x & 31, part = threadIdx.x >> 5;
+  const int e = blockIdx.x * 32 + el;  // tile * 1024 + element
   double acc = 0.0;
-  for (int b = 0; b < n_blocks; ++b) acc += (double)partial[((size_t)b * kGramTiles + t) * 1024 + ij];
+  for (int b = part; b < n_blocks; b += kRedParts)
+    acc += (double)partial[((size_t)b * kGramTiles) * 1024 + e];
+  sums[part][el] = acc;
+  __syncthreads();
+  if (part != 0) return;
+  double tot = 0.0;
+#pragma unroll
+  for (int p = 0; p < kRedParts; ++p) tot += sums[p][el];
+  const int t = e >> 10, ij = e & 1023;
   int ti, tj;
   gram_tile(t, ti, tj);
   const int i = 32 * ti + (ij >> 5), j = 32 * tj + (ij & 31);
-  const double c = acc * inv_n;
+  const double c = tot * inv_n;
   C[i * kD + j] = c;
   C[j * kD + i] = c;
 }
@@ -300,7 +312,7 @@ __global__ __launch_bounds__(kAttnWaves * 64) void attn_kernel(
 
 // ---------------------------------------------------------------------------
 // Symmetric eigen-decomposition by cyclic Jacobi (round-robin ordering), fp64.
-// One block per matrix keeps the upper triangle in LDS (66 KB).  A sweep is 127
+// One block of 16 waves per matrix keeps the upper triangle in LDS (66 KB).  A sweep is 127
 // rounds of 64 disjoint pairs (p, q) (circle method: in round r the pairs are
 // (127, r) and ((r + k) mod 127, (r - k) mod 127), k = 1..63), so every
 // off-diagonal entry is visited once per sweep.  For each pair the rotation
@@ -335,9 +347,10 @@ __device__ inline void round_pair(int r, int kk, int& p, int& q) {
   q = max(a, b);
 }
 
-constexpr int kJacPerThread = (kJacBlocks + 255) / 256;
+constexpr int kJacThreads = 1024;  // 16 waves: the round's 2080 block updates, ~2 per thread
+constexpr int kJacPerThread = (kJacBlocks + kJacThreads - 1) / kJacThreads;
 
-__global__ __launch_bounds__(256) void jacobi_kernel(const double* __restrict__ C, int max_sweeps,
+__global__ __launch_bounds__(kJacThreads) void jacobi_kernel(const double* __restrict__ C, int max_sweeps,
                                                      double* __restrict__ diag,
                                                      double2* __restrict__ rot,
                                                      int* __restrict__ n_rounds,
@@ -348,13 +361,15 @@ __global__ __launch_bounds__(256) void jacobi_kernel(const double* __restrict__ 
   __shared__ int rotated;
   const int mtx = blockIdx.x, tid = threadIdx.x;
   const double* Cm = C + (size_t)mtx * kD * kD;
-  for (int i = 0; i < kD; ++i)
-    for (int j = i + tid; j < kD; j += 256) A[upk(i, j)] = Cm[i * kD + j];
+  for (int e = tid; e < kD * kD; e += kJacThreads) {
+    const int i = e >> 7, j = e & (kD - 1);
+    if (i <= j) A[upk(i, j)] = Cm[e];
+  }
   // this thread's 2x2 blocks (k1 <= k2), fixed for every round
   int bk1[kJacPerThread], bk2[kJacPerThread];
 #pragma unroll
   for (int n = 0; n < kJacPerThread; ++n) {
-    const int b = tid + 256 * n;
+    const int b = tid + kJacThreads * n;
     int k1 = 0, rem = b;
     while (k1 < kJacPairs && rem >= kJacPairs - k1) {
       rem -= kJacPairs - k1;
@@ -426,7 +441,7 @@ __global__ __launch_bounds__(256) void jacobi_kernel(const double* __restrict__ 
     sweeps = sw + 1;
   }
   __syncthreads();
-  for (int i = tid; i < kD; i += 256) diag[(size_t)mtx * kD + i] = A[upk(i, i)];
+  for (int i = tid; i < kD; i += kJacThreads) diag[(size_t)mtx * kD + i] = A[upk(i, i)];
   if (tid == 0) {
     n_rounds[mtx] = sweeps * kJacRounds;
     info[mtx] = converged ? sweeps + 1 : -1;
@@ -561,7 +576,7 @@ hipError_t launch_gram(const void* X, int x_bf16, int64_t n_rows, double inv_n, 
                        n_rows, per, partial);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL(gram_reduce_kernel, dim3(kGramTiles * 1024 / 256), dim3(256), 0, st,
+  hipLaunchKernelGGL(gram_reduce_kernel, dim3(kGramTiles * 1024 / 32), dim3(256), 0, st,
                      partial, (int)nb, inv_n, C);
   return hipGetLastError();
 }
@@ -586,7 +601,7 @@ size_t eig_rot_bytes(int n_mats, int max_sweeps) {
 hipError_t launch_eig(const double* C, int n_mats, int max_sweeps, double* diag, double2* rot,
                       int* n_rounds, double* V, double* lam, double* U, int* info,
                       hipStream_t st) {
-  hipLaunchKernelGGL(jacobi_kernel, dim3((unsigned)n_mats), dim3(256), 0, st, C, max_sweeps,
+  hipLaunchKernelGGL(jacobi_kernel, dim3((unsigned)n_mats), dim3(kJacThreads), 0, st, C, max_sweeps,
                      diag, rot, n_rounds, info);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;

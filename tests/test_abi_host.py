@@ -245,3 +245,59 @@ def test_null_rotations_pass_validation(L):
                              None) == ok.ERR_INVALID_ARG
     assert L.oscar_decode_attn(ctypes.byref(lay), FAKE, FAKE, 2, 32, FAKE, 4, FAKE, None, None,
                                0.088, 2, FAKE, 16, FAKE, 0, None) == ok.ERR_WORKSPACE_TOO_SMALL
+
+
+def test_calibration_sizes(L):
+    T, Hq, Hkv = 8878, 32, 8
+    ws = L.oscar_calib_workspace_bytes(T, Hq, Hkv)
+    o_bytes = T * Hq * 128 * 4
+    assert ws % 256 == 0 and ws >= o_bytes + 10 * 1024 * 4    # rows + >= one block's partials
+    assert L.oscar_calib_workspace_bytes(0, Hq, Hkv) == 0
+    assert L.oscar_calib_workspace_bytes(T, 12, 8) == 0          # 12 heads do not split into 8
+    assert L.oscar_calib_workspace_bytes(T, 4, 8) == 0           # fewer query than KV heads
+    rot1, rot2 = L.oscar_calib_rotation_workspace_bytes(1), L.oscar_calib_rotation_workspace_bytes(2)
+    # per matrix: 32 sweeps x 127 rounds x 64 (c, s) pairs, the vectors and the diagonal
+    per = 32 * 127 * 64 * 16 + 128 * 128 * 8 + 128 * 8
+    assert per <= rot1 <= per + 5 * 256 and 2 * per <= rot2 <= 2 * per + 5 * 256
+    assert L.oscar_calib_rotation_workspace_bytes(0) == 0
+    assert L.oscar_calib_clip_workspace_bytes(T, Hkv, 21) > 0
+    assert L.oscar_calib_clip_workspace_bytes(T, Hkv, 0) == 0
+    assert L.oscar_calib_clip_workspace_bytes(T, Hkv, 33) == 0
+    lw = L.oscar_calibrate_layer_workspace_bytes(T, Hq, Hkv, 21)
+    assert lw >= ws + rot2 + 2 * 128 * 128 * 8 * 2
+    assert L.oscar_calibrate_layer_workspace_bytes(T, Hq, Hkv, 40) == 0
+
+
+def test_calibration_rejects_invalid_arguments(L):
+    E, U, W = ok.ERR_INVALID_ARG, ok.ERR_UNSUPPORTED, ok.ERR_WORKSPACE_TOO_SMALL
+    ws_n = L.oscar_calib_workspace_bytes(100, 8, 2)
+    q = FAKE
+    assert L.oscar_calib_query_cov(None, 100, 8, 2, FAKE, FAKE, ws_n, None) == E
+    assert L.oscar_calib_query_cov(q, 0, 8, 2, FAKE, FAKE, ws_n, None) == E
+    assert L.oscar_calib_query_cov(q, 100, 8, 3, FAKE, FAKE, ws_n, None) == E
+    assert L.oscar_calib_query_cov(q, 100, 8, 2, FAKE, FAKE, ws_n - 1, None) == W
+    assert L.oscar_calib_query_cov(ctypes.c_void_p(0x10008), 100, 8, 2, FAKE, FAKE, ws_n, None) == E
+    assert L.oscar_calib_attn(q, q, None, 100, 8, 2, 1, FAKE, None) == E
+    assert L.oscar_calib_attn(q, q, q, 100, 8, 16, 1, FAKE, None) == E
+    assert L.oscar_calib_attn(q, q, q, 70000 * 64, 4, 1, 1, FAKE, None) == U   # > 65535 query tiles
+    assert L.oscar_calib_score_cov(q, q, q, 100, 8, 2, 1, FAKE, FAKE, ws_n - 256, None) == W
+    rw = L.oscar_calib_rotation_workspace_bytes(2)
+    assert L.oscar_calib_rotation(FAKE, 0, FAKE, FAKE, None, None, None, FAKE, rw, None) == E
+    assert L.oscar_calib_rotation(FAKE, 2, None, FAKE, None, None, None, FAKE, rw, None) == E
+    assert L.oscar_calib_rotation(FAKE, 2, FAKE, FAKE, None, None, None, FAKE, rw - 1, None) == W
+    lay = ok.Layout(num_kv_heads=2, num_pages=1)
+    cw = L.oscar_calib_clip_workspace_bytes(100, 2, 21)
+    assert L.oscar_calib_clip(ctypes.byref(lay), q, 100, None, FAKE, 0, FAKE, None, FAKE, cw, None) == E
+    assert L.oscar_calib_clip(ctypes.byref(lay), q, 100, None, FAKE, 33, FAKE, None, FAKE, cw, None) == U
+    assert L.oscar_calib_clip(ctypes.byref(lay), q, 100, None, None, 21, FAKE, None, FAKE, cw, None) == E
+    assert L.oscar_calib_clip(ctypes.byref(lay), q, 100, None, FAKE, 21, FAKE, None, FAKE, cw - 1, None) == W
+    bad = ok.Layout(num_kv_heads=2, num_pages=1, group_size=16)
+    assert L.oscar_calib_clip(ctypes.byref(bad), q, 100, None, FAKE, 21, FAKE, None, FAKE, cw, None) == U
+    lw = L.oscar_calibrate_layer_workspace_bytes(100, 8, 2, 21)
+    args = [q, q, q, 100, 8, 1, FAKE, 21, FAKE, FAKE, FAKE, None, None, FAKE]
+    assert L.oscar_calibrate_layer(ctypes.byref(lay), *args, lw - 1, None) == W
+    assert L.oscar_calibrate_layer(ctypes.byref(ok.Layout(num_kv_heads=3, num_pages=1)), *args, lw,
+                                   None) == E
+    args2 = list(args)
+    args2[9] = None  # R_v
+    assert L.oscar_calibrate_layer(ctypes.byref(lay), *args2, lw, None) == E
