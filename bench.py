@@ -550,6 +550,8 @@ def main():
         Cst = torch.stack([ok.calib_query_cov(cq, Hkv, workspace=sws),
                            ok.calib_score_cov(cq, ck, cv, workspace=sws)])
         rot_us = ev_time(lambda: ok.calib_rotation(Cst), 3)
+        C72 = Cst.repeat(36, 1, 1).contiguous()   # a 36-layer model's K and V matrices
+        rot72_us = ev_time(lambda: ok.calib_rotation(C72), 2)
         clip_us = ev_time(lambda: ok.calib_clip(clay, ck, cal["R_K"], cands), 5)
         pairs = Tc * (Tc + 1) // 2                 # causal (query, key) pairs per head
         attn_flop = pairs * Hq * 4 * d             # q k^T and p v, 2 d each
@@ -559,6 +561,7 @@ def main():
             "us_per_layer": round(layer_us, 1),
             "stages_us": {"query_cov": round(cq_us, 1), "score_cov": round(cs_us, 1),
                           "attn": round(attn_us, 1), "rotation_2_matrices": round(rot_us, 1),
+                          "rotation_72_matrices": round(rot72_us, 1),
                           "clip_one_tensor": round(clip_us, 1)},
             "attn_roofline": {"bound": "mfma", "flop": attn_flop,
                               "achieved_tflops": round(attn_flop / (attn_us * 1e-6) / 1e12, 1),
@@ -567,7 +570,7 @@ def main():
             "sweeps": [int(x) for x in cal["info"].tolist()],
             "clip": [round(float(x), 2) for x in cal["clip"].tolist()],
         }
-        del cq, ck, cv, cws, obuf, sws, Cst
+        del cq, ck, cv, cws, obuf, sws, Cst, C72
         torch.cuda.empty_cache()
 
     # ---- device copy probe (achievable HBM bandwidth) ----

@@ -26,6 +26,7 @@ namespace {
 
 typedef float f32x16 __attribute__((ext_vector_type(16)));
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
 
 // ---------------------------------------------------------------------------
 // Second-moment matrix X^T X of rows X [n][128] (bf16 or fp32) on fp32 MFMAs.
@@ -148,17 +149,14 @@ __global__ __launch_bounds__(256) void gram_reduce_kernel(const float* __restric
 // as A and B agree; V^T comes from LDS (staged transposed).  P enters the bf16
 // MFMA as a sum of two bf16 parts, p = hi + lo (16 significant bits), so that
 // the product with the bf16 values is kept to ~2^-17 relative; Q K^T of bf16
-// inputs is exact up to the fp32 accumulation.  Online softmax in base 2 with
-// the row maximum; O^T is kept in the accumulators and normalized at the end.
+// inputs is exact up to the fp32 accumulation.  Online softmax in base 2; the
+// running maximum is raised (and O^T, l rescaled) only when a tile's maximum
+// exceeds it by more than 8, the result being the same up to rounding; O^T is kept
+// in the accumulators and normalized at the end.
 // ---------------------------------------------------------------------------
 constexpr int kAttnWaves = 8;
 constexpr int kKPitch = kD + 8;  // bf16: 272-byte K rows (conflict-free 16-byte reads)
 constexpr int kVPitch = 64 + 4;  // bf16: 136-byte V^T rows (conflict-free 8-byte reads)
-
-__device__ inline uint32_t bf16_rne(float f) {  // finite inputs
-  const uint32_t u = __float_as_uint(f);
-  return (u + 0x7fffu + ((u >> 16) & 1u)) >> 16;
-}
 
 __global__ __launch_bounds__(kAttnWaves * 64) void attn_kernel(
     const uint16_t* __restrict__ q, const uint16_t* __restrict__ k, const uint16_t* __restrict__ v,
@@ -230,69 +228,106 @@ __global__ __launch_bounds__(kAttnWaves * 64) void attn_kernel(
     if (!active || kt >= wave_kt) continue;
 
     // S^T: lane holds query qrow, keys 64 kt + 32 kk + 8 (r / 4) + 4 h + r % 4
+    // the two 32-key halves as two interleaved MFMA chains; each step's K pieces
+    // are read from LDS one step ahead
     f32x16 s[2] = {};
+    const uint16_t* kb = Ks + li * kKPitch + 8 * h;
+    uint4 ka0 = *reinterpret_cast<const uint4*>(kb);
+    uint4 ka1 = *reinterpret_cast<const uint4*>(kb + 32 * kKPitch);
 #pragma unroll
-    for (int kk = 0; kk < 2; ++kk)
-#pragma unroll
-      for (int ks = 0; ks < 8; ++ks) {
-        const uint4 a = *reinterpret_cast<const uint4*>(Ks + (32 * kk + li) * kKPitch + 16 * ks + 8 * h);
-        s[kk] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, a), qf[ks], s[kk], 0, 0, 0);
+    for (int ks = 0; ks < 8; ++ks) {
+      uint4 kn0 = ka0, kn1 = ka1;
+      if (ks + 1 < 8) {
+        kn0 = *reinterpret_cast<const uint4*>(kb + 16 * (ks + 1));
+        kn1 = *reinterpret_cast<const uint4*>(kb + 32 * kKPitch + 16 * (ks + 1));
       }
+      s[0] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, ka0), qf[ks], s[0], 0, 0, 0);
+      s[1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, ka1), qf[ks], s[1], 0, 0, 0);
+      ka0 = kn0;
+      ka1 = kn1;
+    }
+    // keep the LDS reads one step ahead of the MFMAs that consume them
+    __builtin_amdgcn_sched_group_barrier(0x100, 4, 0);
+#pragma unroll
+    for (int ks = 0; ks < 7; ++ks) {
+      __builtin_amdgcn_sched_group_barrier(0x008, 2, 0);
+      if (ks < 6) __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);
+    }
+    __builtin_amdgcn_sched_group_barrier(0x008, 2, 0);
     const bool edge = (causal && 64 * kt + 63 > qw0) || 64 * kt + 64 > T;
     float mt = -INFINITY;
+    if (edge) {  // keys >= limit are masked
+      const int limit = causal ? min(T, qrow + 1) : T;
+#pragma unroll
+      for (int kk = 0; kk < 2; ++kk)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          const int key = 64 * kt + 32 * kk + 8 * (r >> 2) + 4 * h + (r & 3);
+          s[kk][r] = key < limit ? s[kk][r] : -INFINITY;
+        }
+    }
 #pragma unroll
     for (int kk = 0; kk < 2; ++kk)
 #pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        float x = s[kk][r] * scale_log2;
-        if (edge) {
-          const int key = 64 * kt + 32 * kk + 8 * (r >> 2) + 4 * h + (r & 3);
-          if (key >= T || (causal && key > qrow)) x = -INFINITY;
-        }
-        s[kk][r] = x;
-        mt = fmaxf(mt, x);
-      }
-    mt = fmaxf(mt, __shfl_xor(mt, 32, 64));
-    const float m_new = fmaxf(m, mt);  // finite: key 0 is visible to every query
-    const float alpha = __builtin_amdgcn_exp2f(m - m_new);
-    m = m_new;
+      for (int r = 0; r < 16; ++r) mt = fmaxf(mt, s[kk][r]);
+    mt = fmaxf(mt, __shfl_xor(mt, 32, 64)) * scale_log2;  // finite: key 0 is visible to every query
+    // The running maximum m (base-2 units) is raised only when a score exceeds it
+    // by more than 8, so most tiles skip the rescale; probabilities stay <= 2^8.
+    if (__ballot(mt > m + 8.0f)) {
+      const float m_new = fmaxf(m, mt);
+      const float alpha = __builtin_amdgcn_exp2f(m - m_new);
+      m = m_new;
+      lsum *= alpha;
+#pragma unroll
+      for (int dt = 0; dt < 4; ++dt)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) o[dt][r] *= alpha;
+    }
     float tsum = 0.0f;  // the tile's probabilities, added to the running sum once
+    // V^T pieces for step (kk, u): dims 32 dt + l % 32, keys 32 kk + 16 u + 4 h + 0..3
+    // and + 8; read one step ahead
+    auto vload = [&](int kk, int u, uint4 (&va)[4]) {
 #pragma unroll
-    for (int dt = 0; dt < 4; ++dt)
-#pragma unroll
-      for (int r = 0; r < 16; ++r) o[dt][r] *= alpha;
+      for (int dt = 0; dt < 4; ++dt) {
+        const uint16_t* vp = Vt + (32 * dt + li) * kVPitch + 32 * kk + 16 * u + 4 * h;
+        const uint2 v0 = *reinterpret_cast<const uint2*>(vp);
+        const uint2 v1 = *reinterpret_cast<const uint2*>(vp + 8);
+        va[dt] = make_uint4(v0.x, v0.y, v1.x, v1.y);
+      }
+    };
+    uint4 vcur[4], vnext[4];
+    vload(0, 0, vcur);
 #pragma unroll
     for (int kk = 0; kk < 2; ++kk)
 #pragma unroll
       for (int u = 0; u < 2; ++u) {
-        uint32_t hi[4], lo[4];
+        const int step = 2 * kk + u;
+        if (step + 1 < 4) vload((step + 1) >> 1, (step + 1) & 1, vnext);
+        uint32_t hw[4], lw[4];
 #pragma unroll
         for (int t2 = 0; t2 < 4; ++t2) {
-          uint32_t hb[2], lb[2];
-#pragma unroll
-          for (int e = 0; e < 2; ++e) {
-            const float p = __builtin_amdgcn_exp2f(s[kk][8 * u + 2 * t2 + e] - m_new);
-            tsum += p;
-            hb[e] = bf16_rne(p);
-            lb[e] = bf16_rne(p - __uint_as_float(hb[e] << 16));
-          }
-          hi[t2] = hb[0] | (hb[1] << 16);
-          lo[t2] = lb[0] | (lb[1] << 16);
+          const float p0 = __builtin_amdgcn_exp2f(fmaf(s[kk][8 * u + 2 * t2], scale_log2, -m));
+          const float p1 = __builtin_amdgcn_exp2f(fmaf(s[kk][8 * u + 2 * t2 + 1], scale_log2, -m));
+          tsum += p0;
+          tsum += p1;
+          const bf16x2 hb = {(__bf16)p0, (__bf16)p1};
+          hw[t2] = __builtin_bit_cast(uint32_t, hb);
+          const bf16x2 lb = {(__bf16)(p0 - __uint_as_float(hw[t2] << 16)),
+                             (__bf16)(p1 - __uint_as_float(hw[t2] & 0xffff0000u))};
+          lw[t2] = __builtin_bit_cast(uint32_t, lb);
         }
-        const bf16x8 phi = __builtin_bit_cast(bf16x8, make_uint4(hi[0], hi[1], hi[2], hi[3]));
-        const bf16x8 plo = __builtin_bit_cast(bf16x8, make_uint4(lo[0], lo[1], lo[2], lo[3]));
-        // A = V^T[dim 32 dt + l % 32][keys 32 kk + 16 u + 4 h + 0..3 and + 8]
+        const bf16x8 phi = __builtin_bit_cast(bf16x8, make_uint4(hw[0], hw[1], hw[2], hw[3]));
+        const bf16x8 plo = __builtin_bit_cast(bf16x8, make_uint4(lw[0], lw[1], lw[2], lw[3]));
 #pragma unroll
-        for (int dt = 0; dt < 4; ++dt) {
-          const uint16_t* vp = Vt + (32 * dt + li) * kVPitch + 32 * kk + 16 * u + 4 * h;
-          const uint2 v0 = *reinterpret_cast<const uint2*>(vp);
-          const uint2 v1 = *reinterpret_cast<const uint2*>(vp + 8);
-          const bf16x8 a = __builtin_bit_cast(bf16x8, make_uint4(v0.x, v0.y, v1.x, v1.y));
-          o[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, phi, o[dt], 0, 0, 0);
-          o[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, plo, o[dt], 0, 0, 0);
-        }
+        for (int dt = 0; dt < 4; ++dt)
+          o[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, vcur[dt]), phi, o[dt], 0, 0, 0);
+#pragma unroll
+        for (int dt = 0; dt < 4; ++dt)
+          o[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, vcur[dt]), plo, o[dt], 0, 0, 0);
+#pragma unroll
+        for (int dt = 0; dt < 4; ++dt) vcur[dt] = vnext[dt];
       }
-    lsum = lsum * alpha + tsum;
+    lsum += tsum;
   }
 
   if (!active || qrow >= T) return;
