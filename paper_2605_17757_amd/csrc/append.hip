@@ -871,23 +871,32 @@ __global__ __launch_bounds__(256) void clip_err_kernel(const uint16_t* __restric
   }
 }
 
-// err[n] = (sum of the blocks' partials, in block order) / (n_rows d); best = the
-// candidate of the first minimum.
-__global__ __launch_bounds__(64) void clip_reduce_kernel(const double* __restrict__ partial,
-                                                         int n_blocks, int n_cands,
-                                                         const float* __restrict__ cands,
-                                                         double inv_n, double* __restrict__ err,
-                                                         float* __restrict__ best) {
+// err[n] = (sum of the blocks' partials) / (n_rows d); best = the candidate of the
+// first minimum.  Thread (candidate n, part p) adds blocks p, p + 8, ... in order,
+// then the 8 part sums are added in order (a fixed order: deterministic).
+constexpr int kClipParts = 8;
+
+__global__ __launch_bounds__(kClipParts * kMaxClipCands) void clip_reduce_kernel(
+    const double* __restrict__ partial, int n_blocks, int n_cands,
+    const float* __restrict__ cands, double inv_n, double* __restrict__ err,
+    float* __restrict__ best) {
+  __shared__ double ps[kClipParts][kMaxClipCands];
   __shared__ double es[kMaxClipCands];
-  const int n = threadIdx.x;
-  if (n < n_cands) {
-    double acc = 0.0;
-    for (int b = 0; b < n_blocks; ++b) acc += partial[(size_t)b * n_cands + n];
-    es[n] = acc * inv_n;
+  const int n = threadIdx.x % kMaxClipCands, part = threadIdx.x / kMaxClipCands;
+  double acc = 0.0;
+  if (n < n_cands)
+    for (int b = part; b < n_blocks; b += kClipParts) acc += partial[(size_t)b * n_cands + n];
+  ps[part][n] = acc;
+  __syncthreads();
+  if (part == 0 && n < n_cands) {
+    double tot = 0.0;
+#pragma unroll
+    for (int p = 0; p < kClipParts; ++p) tot += ps[p][n];
+    es[n] = tot * inv_n;
     err[n] = es[n];
   }
   __syncthreads();
-  if (n == 0 && best) {
+  if (threadIdx.x == 0 && best) {
     int arg = 0;
     for (int i = 1; i < n_cands; ++i)
       if (es[i] < es[arg]) arg = i;
@@ -1018,7 +1027,8 @@ hipError_t launch_clip_errors(const uint16_t* x, int64_t n_rows, const float* R,
                      cands, n_cands, fmt, partial);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL(clip_reduce_kernel, dim3(1), dim3(64), 0, st, partial, n_blocks, n_cands,
+  hipLaunchKernelGGL(clip_reduce_kernel, dim3(1), dim3(kClipParts * kMaxClipCands), 0, st, partial,
+                     n_blocks, n_cands,
                      cands, 1.0 / ((double)n_rows * kD), err, best);
   return hipGetLastError();
 }
