@@ -78,14 +78,14 @@ def lib():
         L.oracle_token_quantile.argtypes = [P, i32, f32]
         L.oracle_kv_append.restype = i64
         L.oracle_kv_append.argtypes = [i32, i32, i32, i32, i32, i32, i64, P, P, P, P, i32, P, P,
-                                       f32, f32]
+                                       f32, f32, i32]
         L.oracle_read_token.argtypes = [i32, i32, i32, i32, P, i64, i32, i32, i32, P, P, P]
         L.oracle_decode.restype = i32
         L.oracle_decode.argtypes = [i32, i32, i32, i32, i32, i64, P, P, i32, i32, P, i32, P, P,
-                                    P, f64, P, i32, P]
+                                    P, f64, P, i32, P, i32]
         L.oracle_decode_brute.restype = i32
         L.oracle_decode_brute.argtypes = [i32, i32, i32, i32, i32, i64, P, P, i32, i32, P, i32,
-                                          P, P, P, f64, P]
+                                          P, P, P, f64, P, i32]
         L.oracle_bf16_decode.restype = i32
         L.oracle_bf16_decode.argtypes = [i32, i32, i32, i64, P, P, i32, i32, P, i32, P, f64,
                                          P, i32, P]
@@ -103,10 +103,10 @@ def lib():
         L.oracle_seg_write.argtypes = [i32, i32, i32, i32, i32, P, P, P, P, P, i32]
         L.oracle_mixed_update.restype = i64
         L.oracle_mixed_update.argtypes = [i32, i32, i32, i32, i32, i32, i64, P, P, i32, i32, i32,
-                                          P, P, P, i32, P, P, P, f32, f32]
+                                          P, P, P, i32, P, P, P, f32, f32, i32]
         L.oracle_decode_mixed.restype = i32
         L.oracle_decode_mixed.argtypes = [i32, i32, i32, i32, i32, i64, P, P, i32, i32, P, i32,
-                                          i32, P, i32, P, P, P, f64, P, i32, P]
+                                          i32, P, i32, P, P, P, f64, P, i32, P, i32]
         L.oracle_query_cov.restype = i32
         L.oracle_query_cov.argtypes = [P, i64, i32, i32, i32, P]
         L.oracle_attn_rows.restype = i32
@@ -120,7 +120,7 @@ def lib():
         L.oracle_compose.restype = i32
         L.oracle_compose.argtypes = [P, i32, P]
         L.oracle_clip_errors.restype = i32
-        L.oracle_clip_errors.argtypes = [P, i64, i32, P, i32, i32, i32, P, i32, P]
+        L.oracle_clip_errors.argtypes = [P, i64, i32, P, i32, i32, i32, P, i32, P, i32, i32]
         L.oracle_num_threads.restype = i32
         _lib = L
     return _lib
@@ -141,6 +141,15 @@ def _rot(R):
         return None, None
     a = _c(R, np.float32)
     return a, _ptr(a)
+
+
+def _rph(*Rs) -> int:
+    """1 when the rotations are per KV head ([Hkv, d, d]), 0 when shared ([d, d]);
+    None entries (identity) take either form."""
+    kinds = {np.ndim(R) for R in Rs if R is not None}
+    if len(kinds) > 1:
+        raise ValueError("R_k and R_v must both be shared [d, d] or both per head [Hkv, d, d]")
+    return int(kinds == {3})
 
 
 def num_threads() -> int:
@@ -212,7 +221,7 @@ def kv_append(pages: np.ndarray, *, d: int, Hkv: int, P: int, G: int, k: np.ndar
     Rva, Rvp = _rot(Rv)
     rc = lib().oracle_kv_append(d, Hkv, P, G, int(meta), int(clip), num_pages, _ptr(pages),
                                 _ptr(k), _ptr(v), _ptr(slots), n_tok, Rkp, Rvp, float(clip_k),
-                                float(clip_v))
+                                float(clip_v), _rph(Rk, Rv))
     if rc < 0:
         raise ValueError("oracle kv_append: slot outside the page pool")
     return int(rc)
@@ -249,7 +258,7 @@ def decode(pages: np.ndarray, *, d: int, Hkv: int, P: int, G: int, q: np.ndarray
     Rva, Rvp = _rot(Rv)
     rc = lib().oracle_decode(d, Hkv, P, G, int(meta), num_pages, _ptr(pages), _ptr(q), B, Hq,
                              _ptr(bt), bt.shape[1], _ptr(sl), Rkp, Rvp, float(sm_scale), pp, n,
-                             _ptr(out))
+                             _ptr(out), _rph(Rk, Rv))
     if rc:
         raise ValueError("oracle decode: bad page id, length or head")
     return out
@@ -268,7 +277,7 @@ def decode_brute(pages: np.ndarray, *, d: int, Hkv: int, P: int, G: int, q: np.n
     Rva, Rvp = _rot(Rv)
     rc = lib().oracle_decode_brute(d, Hkv, P, G, int(meta), num_pages, _ptr(pages), _ptr(q), B,
                                    Hq, _ptr(bt), bt.shape[1], _ptr(sl), Rkp, Rvp, float(sm_scale),
-                                   _ptr(out))
+                                   _ptr(out), _rph(Rk, Rv))
     if rc:
         raise ValueError("oracle decode_brute: bad page id or length")
     return out
@@ -341,7 +350,7 @@ def mixed_update(pages: np.ndarray, seg: np.ndarray, *, d: int, Hkv: int, P: int
     rc = lib().oracle_mixed_update(d, Hkv, P, G, int(meta), int(clip), num_pages, _ptr(pages),
                                    _ptr(seg), S0, W, B, _ptr(_c(k_new, np.uint16)),
                                    _ptr(_c(v_new, np.uint16)), _ptr(bt), bt.shape[1], _ptr(sl),
-                                   Rkp, Rvp, float(clip_k), float(clip_v))
+                                   Rkp, Rvp, float(clip_k), float(clip_v), _rph(Rk, Rv))
     if rc < 0:
         raise ValueError("oracle mixed_update: bad length or page")
     return int(rc)
@@ -368,7 +377,7 @@ def decode_mixed(pages: np.ndarray, seg: np.ndarray, *, d: int, Hkv: int, P: int
     rc = lib().oracle_decode_mixed(d, Hkv, P, G, int(meta), num_pages, _ptr(pages),
                                    _ptr(_c(seg, np.uint16)), S0, W, _ptr(q), B, Hq, _ptr(bt),
                                    bt.shape[1], _ptr(sl), Rkp, Rvp, float(sm_scale), pp, n,
-                                   _ptr(out))
+                                   _ptr(out), _rph(Rk, Rv))
     if rc:
         raise ValueError("oracle decode_mixed: bad page id, length or head")
     return out
@@ -457,16 +466,21 @@ def eigh_desc(C: np.ndarray):
 
 
 def clip_errors(x: np.ndarray, R, *, G: int, cands, meta: int = 0, clip: int = 0) -> np.ndarray:
-    """Mean squared quantization error of the rotated rows x [n, d] (bf16 bits) for
-    each candidate clip ratio (fp32): [n_cands] fp64."""
+    """Mean squared quantization error of the rotated rows x [n, d] or [n, Hkv, d]
+    (bf16 bits) for each candidate clip ratio (fp32): [n_cands] fp64.  R: [d, d],
+    [Hkv, d, d] (row (t, h) rotated by R[h]) or None."""
     x = _c(x, np.uint16)
     d = x.shape[-1]
+    Hkv = x.shape[1] if x.ndim == 3 else 1
+    rph = _rph(R)
+    if rph and (x.ndim != 3 or np.shape(R)[0] != Hkv):
+        raise ValueError("per-head R needs rows [n, Hkv, d] with Hkv = R.shape[0]")
     x = x.reshape(-1, d)
     cd = _c(cands, np.float32)
     err = np.zeros(cd.size, np.float64)
     Ra, Rp = _rot(R)
     if lib().oracle_clip_errors(_ptr(x), x.shape[0], d, Rp, G, int(meta), int(clip), _ptr(cd),
-                                cd.size, _ptr(err)):
+                                cd.size, _ptr(err), Hkv, rph):
         raise ValueError("oracle clip_errors: bad shape")
     return err
 
@@ -477,19 +491,32 @@ def default_clip_candidates() -> np.ndarray:
 
 
 def calibrate(q: np.ndarray, k: np.ndarray, v: np.ndarray, *, causal: bool = True, G: int = 32,
-              meta: int = 0, clip: int = 0, cands=None) -> dict:
+              meta: int = 0, clip: int = 0, cands=None, per_head: bool = False) -> dict:
     """Alg. 1 Calibrate for one layer from bf16 activations q [T, Hq, d], k, v
     [T, Hkv, d]: C_Q, C_S, their descending eigen-decompositions, R_K and R_V
     (fp64 and rounded to fp32), and the clip ratios c_K, c_V chosen among
     ``cands`` (the first minimum of clip_errors) for rows rotated by the fp32
-    matrices the cache update uses."""
+    matrices the cache update uses.  ``per_head``: one C_Q, C_S and rotation per
+    KV head (the average over its g query heads), stacked [Hkv, d, d]; one clip
+    ratio per tensor over all heads."""
     cands = default_clip_candidates() if cands is None else _c(cands, np.float32)
     Hkv = k.shape[1]
-    CQ = query_cov(q, Hkv)
-    CS = score_cov(q, k, v, causal=causal)
-    lam_q, UQ = eigh_desc(CQ)
-    lam_s, US = eigh_desc(CS)
-    RK, RV = compose(UQ), compose(US)
+    if per_head:
+        g = q.shape[1] // Hkv
+        CQ = np.stack([query_cov(q[:, h * g:(h + 1) * g], 1) for h in range(Hkv)])
+        CS = np.stack([score_cov(q[:, h * g:(h + 1) * g], k[:, h:h + 1], v[:, h:h + 1],
+                                 causal=causal) for h in range(Hkv)])
+        eq = [eigh_desc(C) for C in CQ]
+        es = [eigh_desc(C) for C in CS]
+        lam_q, UQ = np.stack([e[0] for e in eq]), np.stack([e[1] for e in eq])
+        lam_s, US = np.stack([e[0] for e in es]), np.stack([e[1] for e in es])
+        RK, RV = np.stack([compose(U) for U in UQ]), np.stack([compose(U) for U in US])
+    else:
+        CQ = query_cov(q, Hkv)
+        CS = score_cov(q, k, v, causal=causal)
+        lam_q, UQ = eigh_desc(CQ)
+        lam_s, US = eigh_desc(CS)
+        RK, RV = compose(UQ), compose(US)
     RK32, RV32 = RK.astype(np.float32), RV.astype(np.float32)
     err_k = clip_errors(k, RK32, G=G, cands=cands, meta=meta, clip=clip)
     err_v = clip_errors(v, RV32, G=G, cands=cands, meta=meta, clip=clip)

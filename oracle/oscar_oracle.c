@@ -169,6 +169,12 @@ size_t oracle_page_head_bytes(int d, int P, int G) {
 
 typedef struct { int d, Hkv, P, G, meta; } geo_t;
 
+/* Rotation of KV head h: one shared [d][d] matrix (rph = 0) or one per KV head,
+ * [Hkv][d][d] (rph = 1); NULL stays the identity. */
+static const float *head_rot(const float *R, int rph, int h, int d) {
+  return (R && rph) ? R + (size_t)h * d * d : R;
+}
+
 static size_t kcode_off(geo_t g, int t, int c) { return (size_t)t * (g.d / 4) + (size_t)(c / 4); }
 static size_t vcode_off(geo_t g, int t, int c) {
   return (size_t)g.P * (g.d / 4) + (size_t)(c / 4) * g.P + (size_t)t;
@@ -319,13 +325,14 @@ int oracle_quantize_row(const float *xt, int d, int G, float rho, int meta, int 
 
 /* Quantize n_tok new rows into the paged cache (Alg. 1 QuantizeAndWrite; the
  * fused cache-write of Sec. 4).  k, v: bf16 [n_tok, Hkv, d]; slot_mapping[i] =
- * page*P + offset.  Rk, Rv: fp32 [d, d] row-major, or NULL for the identity.
+ * page*P + offset.  Rk, Rv: fp32 [d, d] row-major (rph = 0) or [Hkv, d, d], one
+ * per KV head (rph = 1), or NULL for the identity.
  * meta, clip: metadata format and clip rule of oracle_quantize_row.  Returns the
  * number of saturated metadata stores, or -1 on a slot outside the pool. */
 int64_t oracle_kv_append(int d, int Hkv, int P, int G, int meta, int clip, int64_t num_pages,
                          uint8_t *pages, const uint16_t *k, const uint16_t *v,
                          const int64_t *slot_mapping, int n_tok, const float *Rk,
-                         const float *Rv, float clip_k, float clip_v) {
+                         const float *Rv, float clip_k, float clip_v, int rph) {
   geo_t g = {d, Hkv, P, G, meta};
   int64_t sat = 0, bad = 0;
 #pragma omp parallel for reduction(+ : sat, bad) schedule(static)
@@ -344,7 +351,7 @@ int64_t oracle_kv_append(int d, int Hkv, int P, int G, int meta, int clip, int64
       for (int is_v = 0; is_v < 2; ++is_v) {
         const uint16_t *src = (is_v ? v : k) + ((size_t)i * Hkv + (size_t)h) * d;
         for (int c = 0; c < d; ++c) x[c] = oracle_bf16_to_f32(src[c]);
-        oracle_rotate_row(x, is_v ? Rv : Rk, d, xt);
+        oracle_rotate_row(x, head_rot(is_v ? Rv : Rk, rph, h, d), d, xt);
         sat += oracle_quantize_row(xt, d, G, is_v ? clip_v : clip_k, meta, clip, codes, s16, z16);
         for (int c = 0; c < d; ++c) put_code(g, blk, is_v, t, c, codes[c]);
         for (int grp = 0; grp < d / G; ++grp) put_sz(g, blk, is_v, grp, t, s16[grp], z16[grp]);
@@ -394,8 +401,10 @@ static void dequant_rotated(geo_t g, const uint8_t *blk, int is_v, int t, double
 static int decode_pair(geo_t g, const uint8_t *pages, int64_t num_pages, const uint16_t *q,
                        int Hq, const int32_t *block_table, int max_pages,
                        const int32_t *seq_lens, const float *Rk, const float *Rv,
-                       double sm_scale, int b, int h, double *o) {
+                       double sm_scale, int b, int h, double *o, int rph) {
   int d = g.d, group = Hq / g.Hkv, kvh = h / group;
+  Rk = head_rot(Rk, rph, kvh, d);
+  Rv = head_rot(Rv, rph, kvh, d);
   int len = seq_lens[b];
   if (len < 1 || len > max_pages * g.P) return -1;
   double *qt = (double *)calloc((size_t)d, sizeof(double));
@@ -446,7 +455,7 @@ int oracle_decode(int d, int Hkv, int P, int G, int meta, int64_t num_pages,
                   const uint8_t *pages, const uint16_t *q, int B, int Hq,
                   const int32_t *block_table, int max_pages, const int32_t *seq_lens,
                   const float *Rk, const float *Rv, double sm_scale, const int32_t *pairs,
-                  int n_pairs, double *out) {
+                  int n_pairs, double *out, int rph) {
   geo_t g = {d, Hkv, P, G, meta};
   if (Hq % Hkv) return -1;
   int n = pairs ? n_pairs : B * Hq;
@@ -457,7 +466,7 @@ int oracle_decode(int d, int Hkv, int P, int G, int meta, int64_t num_pages,
     int h = pairs ? pairs[2 * i + 1] : i % Hq;
     if (b < 0 || b >= B || h < 0 || h >= Hq) { bad += 1; continue; }
     if (decode_pair(g, pages, num_pages, q, Hq, block_table, max_pages, seq_lens, Rk, Rv,
-                    sm_scale, b, h, out + (size_t)i * d))
+                    sm_scale, b, h, out + (size_t)i * d, rph))
       bad += 1;
   }
   return bad ? -1 : 0;
@@ -469,7 +478,8 @@ int oracle_decode(int d, int Hkv, int P, int G, int meta, int64_t num_pages,
 int oracle_decode_brute(int d, int Hkv, int P, int G, int meta, int64_t num_pages,
                         const uint8_t *pages, const uint16_t *q, int B, int Hq,
                         const int32_t *block_table, int max_pages, const int32_t *seq_lens,
-                        const float *Rk, const float *Rv, double sm_scale, double *out) {
+                        const float *Rk, const float *Rv, double sm_scale, double *out,
+                        int rph) {
   geo_t g = {d, Hkv, P, G, meta};
   if (Hq % Hkv) return -1;
   int group = Hq / Hkv;
@@ -483,6 +493,7 @@ int oracle_decode_brute(int d, int Hkv, int P, int G, int meta, int64_t num_page
     double *score = (double *)malloc(sizeof(double) * (size_t)len);
     for (int h = 0; h < Hq && !rc; ++h) {
       int kvh = h / group;
+      const float *Rkh = head_rot(Rk, rph, kvh, d), *Rvh = head_rot(Rv, rph, kvh, d);
       const uint16_t *qr = q + ((size_t)b * Hq + h) * d;
       double m = -INFINITY;
       for (int t = 0; t < len; ++t) {
@@ -492,17 +503,17 @@ int oracle_decode_brute(int d, int Hkv, int P, int G, int meta, int64_t num_page
         dequant_rotated(g, blk, 0, t % P, rot);
         for (int j = 0; j < d; ++j) {          /* k^_j = sum_c Q(k~)_c Rk[j][c] */
           double acc = 0.0;
-          if (!Rk) acc = rot[j];
+          if (!Rkh) acc = rot[j];
           else
-            for (int c = 0; c < d; ++c) acc += rot[c] * (double)Rk[(size_t)j * d + c];
+            for (int c = 0; c < d; ++c) acc += rot[c] * (double)Rkh[(size_t)j * d + c];
           khat[j] = acc;
         }
         dequant_rotated(g, blk, 1, t % P, rot);
         for (int j = 0; j < d; ++j) {
           double acc = 0.0;
-          if (!Rv) acc = rot[j];
+          if (!Rvh) acc = rot[j];
           else
-            for (int c = 0; c < d; ++c) acc += rot[c] * (double)Rv[(size_t)j * d + c];
+            for (int c = 0; c < d; ++c) acc += rot[c] * (double)Rvh[(size_t)j * d + c];
           vhat[(size_t)t * d + j] = acc;
         }
         double s = 0.0;
@@ -662,7 +673,7 @@ int64_t oracle_mixed_update(int d, int Hkv, int P, int G, int meta, int clip, in
                             uint16_t *seg, int S0, int W, int B, const uint16_t *k_new,
                             const uint16_t *v_new, const int32_t *block_table, int max_pages,
                             const int32_t *seq_lens, const float *Rk, const float *Rv,
-                            float clip_k, float clip_v) {
+                            float clip_k, float clip_v, int rph) {
   int64_t sat = 0;
   uint16_t *ko = (uint16_t *)malloc(sizeof(uint16_t) * (size_t)Hkv * d);
   uint16_t *vo = (uint16_t *)malloc(sizeof(uint16_t) * (size_t)Hkv * d);
@@ -688,7 +699,7 @@ int64_t oracle_mixed_update(int d, int Hkv, int P, int G, int meta, int clip, in
       int32_t page = block_table[(size_t)b * max_pages + quant_pos / P];
       int64_t slot = (int64_t)page * P + quant_pos % P;
       int64_t r = oracle_kv_append(d, Hkv, P, G, meta, clip, num_pages, pages, qk, qv, &slot, 1, Rk, Rv,
-                                   clip_k, clip_v);
+                                   clip_k, clip_v, rph);
       if (r < 0) { rc = -1; break; }
       sat += r;
     }
@@ -712,7 +723,7 @@ int oracle_decode_mixed(int d, int Hkv, int P, int G, int meta, int64_t num_page
                         const uint16_t *seg, int S0, int W, const uint16_t *q, int B, int Hq,
                         const int32_t *block_table, int max_pages, const int32_t *seq_lens,
                         const float *Rk, const float *Rv, double sm_scale, const int32_t *pairs,
-                        int n_pairs, double *out) {
+                        int n_pairs, double *out, int rph) {
   geo_t g = {d, Hkv, P, G, meta};
   if (Hq % Hkv || S0 < 0 || W < 0) return -1;
   int group = Hq / Hkv;
@@ -725,6 +736,7 @@ int oracle_decode_mixed(int d, int Hkv, int P, int G, int meta, int64_t num_page
     int len = (b >= 0 && b < B) ? seq_lens[b] : 0;
     if (h < 0 || h >= Hq || len < 1 || len > max_pages * P) { bad += 1; continue; }
     int kvh = h / group;
+    const float *Rkh = head_rot(Rk, rph, kvh, d), *Rvh = head_rot(Rv, rph, kvh, d);
     int lo = len < S0 ? len : S0;
     int hi = len - W > lo ? len - W : lo;
     const uint16_t *qr = q + ((size_t)b * Hq + h) * d;
@@ -737,9 +749,9 @@ int oracle_decode_mixed(int d, int Hkv, int P, int G, int meta, int64_t num_page
     for (int c = 0; c < d; ++c) qd[c] = (double)oracle_bf16_to_f32(qr[c]);
     for (int j = 0; j < d; ++j) {
       double acc = 0.0;
-      if (!Rk) acc = qd[j];
+      if (!Rkh) acc = qd[j];
       else
-        for (int c = 0; c < d; ++c) acc += qd[c] * (double)Rk[(size_t)c * d + j];
+        for (int c = 0; c < d; ++c) acc += qd[c] * (double)Rkh[(size_t)c * d + j];
       qt[j] = acc;
     }
     double m = -INFINITY;
@@ -775,9 +787,9 @@ int oracle_decode_mixed(int d, int Hkv, int P, int G, int meta, int64_t num_page
       double *o = out + (size_t)i * d;
       for (int j = 0; j < d; ++j) {
         double acc = 0.0;
-        if (!Rv) acc = ot[j];
+        if (!Rvh) acc = ot[j];
         else
-          for (int c = 0; c < d; ++c) acc += ot[c] * (double)Rv[(size_t)j * d + c];
+          for (int c = 0; c < d; ++c) acc += ot[c] * (double)Rvh[(size_t)j * d + c];
         o[j] = (acc + op[j]) / l;
       }
     } else {
@@ -975,11 +987,13 @@ int oracle_compose(const double *U, int d, double *R) {
  *   err[n] = mean over rows r and channels c of (x~_{r,c} - s_g (code_{r,c} - z_g))^2
  * with x~ = x R rounded to fp32 (oracle_rotate_row) and (code, s, z) from
  * oracle_quantize_row with rho_n, s and z read back from their stored format.
- * x: bf16 [n_rows][d].  Rows are summed in order (deterministic).  Returns -1
- * on a bad shape. */
+ * x: bf16 [n_rows][d], row r of KV head r % Hkv (rotated by that head's matrix
+ * when rph = 1).  Rows are summed in order (deterministic).  Returns -1 on a bad
+ * shape. */
 int oracle_clip_errors(const uint16_t *x, int64_t n_rows, int d, const float *R, int G, int meta,
-                       int clip, const float *cands, int n_cands, double *err) {
-  if (n_rows < 1 || d < 1 || G < 1 || d % G || n_cands < 1) return -1;
+                       int clip, const float *cands, int n_cands, double *err, int Hkv,
+                       int rph) {
+  if (n_rows < 1 || d < 1 || G < 1 || d % G || n_cands < 1 || Hkv < 1) return -1;
   double *per = (double *)malloc(sizeof(double) * (size_t)n_rows * n_cands);
   if (!per) return -1;
 #pragma omp parallel for schedule(static)
@@ -990,7 +1004,7 @@ int oracle_clip_errors(const uint16_t *x, int64_t n_rows, int d, const float *R,
     uint16_t *s16 = (uint16_t *)malloc(sizeof(uint16_t) * (size_t)(d / G));
     uint16_t *z16 = (uint16_t *)malloc(sizeof(uint16_t) * (size_t)(d / G));
     for (int c = 0; c < d; ++c) xr[c] = oracle_bf16_to_f32(x[(size_t)r * d + c]);
-    oracle_rotate_row(xr, R, d, xt);
+    oracle_rotate_row(xr, head_rot(R, rph, (int)(r % Hkv), d), d, xt);
     for (int n = 0; n < n_cands; ++n) {
       oracle_quantize_row(xt, d, G, cands[n], meta, clip, codes, s16, z16);
       double e = 0.0;

@@ -261,3 +261,99 @@ def test_null_rotation_is_identity(meta, clip):
             p = np.exp(sc - sc.max())
             ref = p @ deq[1] / p.sum()
             assert np.max(np.abs(got[b, hq] - ref)) < 1e-10
+
+
+# ---------------------------------------------------------------------------
+# one rotation per KV head
+# ---------------------------------------------------------------------------
+
+def _signed_perm(rng, d=D):
+    """R with x R = a signed permutation of x: R[perm[j], j] = sign[j]."""
+    perm = rng.permutation(d)
+    sign = rng.choice([-1.0, 1.0], d)
+    R = np.zeros((d, d), np.float32)
+    R[perm, np.arange(d)] = sign
+    return R, perm, sign
+
+
+def _cache(Rk, Rv, kb, vb, table, lens, Hkv, G=32, meta=0, clip=0):
+    pages = np.zeros(table.size * Hkv * oracle.page_head_bytes(D, P, G), np.uint8)
+    for b in range(len(lens)):
+        oracle.kv_append(pages, d=D, Hkv=Hkv, P=P, G=G, k=kb[b], v=vb[b],
+                         slot_mapping=W.slots_for(table, b, np.arange(lens[b])), Rk=Rk, Rv=Rv,
+                         clip_k=0.9, clip_v=0.95, meta=meta, clip=clip)
+    return pages
+
+
+def test_per_head_rotation_maps_each_head_to_its_matrix():
+    """With R_h a signed permutation per KV head, the cache of head h holds the
+    codes of the rows permuted by R_h (bit-exact against the identity-rotation
+    cache of those permuted rows), and decode equals the identity-rotation decode
+    of the permuted query, rotated back by R_h^T."""
+    B, Hq, Hkv, mp = 2, 6, 3, 3
+    lens = [70, 129]
+    rng = np.random.default_rng(41)
+    table = rng.permutation(B * mp).astype(np.int32).reshape(B, mp)
+    kb = [W.f32_to_bf16_bits((rng.standard_normal((n, Hkv, D)) * 2).astype(np.float32)) for n in lens]
+    vb = [W.f32_to_bf16_bits(rng.standard_normal((n, Hkv, D)).astype(np.float32)) for n in lens]
+    Rs = [_signed_perm(rng) for _ in range(2 * Hkv)]
+    Rk = np.stack([r[0] for r in Rs[:Hkv]])
+    Rv = np.stack([r[0] for r in Rs[Hkv:]])
+    pages = _cache(Rk, Rv, kb, vb, table, lens, Hkv)
+
+    def permuted(x, which):  # x~ = x R_h per head (exact: signed permutation of bf16)
+        out = np.empty_like(x)
+        for h in range(Hkv):
+            _, perm, sign = Rs[which * Hkv + h]
+            f = W.bf16_bits_to_f32(x[:, h])[:, perm] * sign
+            out[:, h] = W.f32_to_bf16_bits(f.astype(np.float32))
+        return out
+
+    ref = _cache(None, None, [permuted(k, 0) for k in kb], [permuted(v, 1) for v in vb], table,
+                 lens, Hkv)
+    assert np.array_equal(pages, ref)
+    q = W.f32_to_bf16_bits(rng.standard_normal((B, Hq, D)).astype(np.float32))
+    sm = 1.0 / math.sqrt(D)
+    got = oracle.decode(pages, d=D, Hkv=Hkv, P=P, G=32, q=q, block_table=table,
+                        seq_lens=np.array(lens, np.int32), Rk=Rk, Rv=Rv, sm_scale=sm)
+    g = Hq // Hkv
+    qp = np.empty_like(q)
+    for hq in range(Hq):
+        _, perm, sign = Rs[hq // g]
+        qp[:, hq] = W.f32_to_bf16_bits((W.bf16_bits_to_f32(q[:, hq])[:, perm] * sign).astype(np.float32))
+    base = oracle.decode(pages, d=D, Hkv=Hkv, P=P, G=32, q=qp, block_table=table,
+                         seq_lens=np.array(lens, np.int32), Rk=None, Rv=None, sm_scale=sm)
+    for hq in range(Hq):
+        Rvh = Rv[hq // g].astype(np.float64)
+        assert np.max(np.abs(got[:, hq] - base[:, hq] @ Rvh.T)) <= 1e-12
+    # the rotated-basis evaluation equals the original-basis brute force
+    brute = oracle.decode_brute(pages, d=D, Hkv=Hkv, P=P, G=32, q=q, block_table=table,
+                                seq_lens=np.array(lens, np.int32), Rk=Rk, Rv=Rv, sm_scale=sm)
+    assert np.max(np.abs(got - brute)) <= 1e-12
+    # equal matrices per head = the shared matrix
+    R1 = W.rotation(43)
+    same = _cache(np.stack([R1] * Hkv), np.stack([R1] * Hkv), kb, vb, table, lens, Hkv)
+    assert np.array_equal(same, _cache(R1, R1, kb, vb, table, lens, Hkv))
+    with pytest.raises(ValueError):
+        _cache(Rk, R1, kb, vb, table, lens, Hkv)   # mixed shared / per-head
+
+
+def test_per_head_calibration_averages_to_the_shared_one():
+    """The per-head C_Q, C_S are the GQA groups' averages, so their mean over the
+    heads is the shared (GQA-averaged) covariance; each head's rotation passes
+    Lemma 1 against its own covariance."""
+    rng = np.random.default_rng(47)
+    T, Hq, Hkv = 150, 6, 3
+    q = W.f32_to_bf16_bits((rng.standard_normal((T, Hq, D)) * np.linspace(0.2, 3, D)).astype(np.float32))
+    k = W.f32_to_bf16_bits(rng.standard_normal((T, Hkv, D)).astype(np.float32))
+    v = W.f32_to_bf16_bits(rng.standard_normal((T, Hkv, D)).astype(np.float32))
+    ph = oracle.calibrate(q, k, v, per_head=True)
+    sh = oracle.calibrate(q, k, v)
+    for key in ("C_Q", "C_S"):
+        assert ph[key].shape == (Hkv, D, D)
+        assert np.max(np.abs(ph[key].mean(axis=0) - sh[key])) <= 1e-13 * np.max(np.abs(sh[key]))
+    for h in range(Hkv):
+        R, C = ph["R_K"][h], ph["C_Q"][h]
+        dg = np.diag(R.T @ C @ R)
+        assert np.max(np.abs(dg - np.trace(C) / D)) <= 1e-12 * np.trace(C)
+    assert ph["R_K32"].shape == (Hkv, D, D) and ph["c_K"] in oracle.default_clip_candidates()
