@@ -33,6 +33,10 @@
  *   - A rotation matrix argument (R_k, R_v) may be NULL: the identity, e.g.
  *     R_V absorbed into the value and output projections (Sec. 4 "KV Cache
  *     Update").  The same choice must be used for the cache update and decode.
+ *   - L->rot_per_head = 1: every non-NULL R_k, R_v is an fp32 [Hkv][d][d] array,
+ *     one matrix per KV head (row (token, h) and the query heads of KV head h use
+ *     matrix h); 0 (default): one [d][d] matrix for all heads, as the paper
+ *     deploys it (one rotation per layer, GQA-averaged).
  *   - Supported shapes: head_dim 128, page_size 64, group_size 32, 64 or 128.  Other values
  *     return OSCAR_ERR_UNSUPPORTED; an unknown clip_mode or meta_dtype returns
  *     OSCAR_ERR_INVALID_ARG.
@@ -94,6 +98,7 @@ typedef struct {
   int64_t num_pages;    /* pages in the pool (>= 1)                   */
   int32_t clip_mode;    /* oscar_clip_mode (default GROUP_ABSMAX)     */
   int32_t meta_dtype;   /* oscar_meta_dtype (default F16)             */
+  int32_t rot_per_head; /* 0: one R_k, R_v per layer; 1: one per KV head */
 } oscar_layout;
 
 /* Human-readable name of a status code (static storage). */
@@ -400,7 +405,8 @@ int oscar_calib_rotation(const double *C, int32_t n_mats, double *lam, double *U
  * oscar_calib_clip -- clip calibration (Alg. 1 CalibrateClip; the paper gives no
  * procedure: read as the candidate with the smallest quantization error of the
  * rotated calibration rows).  For rows x [n_tok, Hkv = L->num_kv_heads, d] bf16,
- * rotated by R (fp32, NULL: identity) exactly as oscar_kv_append does, and
+ * rotated by R (fp32, [Hkv][d][d] when L->rot_per_head, NULL: identity) exactly
+ * as oscar_kv_append does, and
  * quantized with L's group size, clip mode and metadata format at each
  * candidate ratio cands[n] (fp32, in (0, 1], n_cands <= OSCAR_CALIB_MAX_CANDS):
  *   err[n] = mean over rows and channels of (x~_c - s (code_c - z))^2   (fp64)
@@ -417,14 +423,17 @@ int oscar_calib_clip(const oscar_layout *L, const void *x, int64_t n_tok, const 
  * C_Q (oscar_calib_query_cov), C_S (oscar_calib_score_cov), their rotations
  * R_K = U_Q H_Had P_br and R_V = U_S H_Had P_br (oscar_calib_rotation), and the
  * clip ratios c_K, c_V (oscar_calib_clip of k by R_K and of v by R_V, in L's
- * quantizer format).  L->num_kv_heads is Hkv.
- *   R_k, R_v : fp32 [d][d] outputs (what oscar_kv_append and decode take)
+ * quantizer format).  L->num_kv_heads is Hkv.  With L->rot_per_head = 1 every KV
+ * head h gets its own C_Q and C_S (the average over its g query heads only) and
+ * its own R_K, R_V; the clip ratios stay one per tensor (all heads' rows).
+ *   R_k, R_v : fp32 [d][d], or [Hkv][d][d] per head (what oscar_kv_append and
+ *              decode take)
  *   clip     : fp32 [2] = (c_K, c_V)
- *   lam      : fp64 [2][d] (spectra of C_Q, C_S) or NULL
- *   info     : int32 [2] (oscar_calib_rotation's) or NULL
- * workspace >= oscar_calibrate_layer_workspace_bytes(T, Hq, Hkv, n_cands).
+ *   lam      : fp64 [2][d] (spectra of C_Q, C_S), [2][Hkv][d] per head, or NULL
+ *   info     : int32 [2] (oscar_calib_rotation's), [2][Hkv] per head, or NULL
+ * workspace >= oscar_calibrate_layer_workspace_bytes(L, T, Hq, n_cands).
  */
-size_t oscar_calibrate_layer_workspace_bytes(int64_t T, int32_t Hq, int32_t Hkv,
+size_t oscar_calibrate_layer_workspace_bytes(const oscar_layout *L, int64_t T, int32_t Hq,
                                              int32_t n_cands);
 int oscar_calibrate_layer(const oscar_layout *L, const void *q, const void *k, const void *v,
                           int64_t T, int32_t Hq, int32_t causal, const float *cands,

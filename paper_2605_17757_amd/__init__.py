@@ -56,13 +56,14 @@ class Layout(ctypes.Structure):
     _fields_ = [("head_dim", ctypes.c_int32), ("num_kv_heads", ctypes.c_int32),
                 ("page_size", ctypes.c_int32), ("group_size", ctypes.c_int32),
                 ("num_pages", ctypes.c_int64), ("clip_mode", ctypes.c_int32),
-                ("meta_dtype", ctypes.c_int32)]
+                ("meta_dtype", ctypes.c_int32), ("rot_per_head", ctypes.c_int32)]
 
     def __init__(self, num_kv_heads: int, num_pages: int, head_dim: int = HEAD_DIM,
                  page_size: int = PAGE_SIZE, group_size: int = GROUP_SIZE,
-                 clip_mode: int = CLIP_GROUP_ABSMAX, meta_dtype: int = META_F16):
+                 clip_mode: int = CLIP_GROUP_ABSMAX, meta_dtype: int = META_F16,
+                 rot_per_head: int = 0):
         super().__init__(head_dim, num_kv_heads, page_size, group_size, num_pages, clip_mode,
-                         meta_dtype)
+                         meta_dtype, rot_per_head)
 
 
 _lib = None
@@ -119,7 +120,7 @@ def lib() -> ctypes.CDLL:
             "oscar_calib_rotation": (ctypes.c_int, [P, i32, P, P, P, P, P, P, sz, P]),
             "oscar_calib_clip_workspace_bytes": (sz, [i64, i32, i32]),
             "oscar_calib_clip": (ctypes.c_int, [LP, P, i64, P, P, i32, P, P, P, sz, P]),
-            "oscar_calibrate_layer_workspace_bytes": (sz, [i64, i32, i32, i32]),
+            "oscar_calibrate_layer_workspace_bytes": (sz, [LP, i64, i32, i32]),
             "oscar_calibrate_layer": (ctypes.c_int, [LP, P, P, P, i64, i32, i32, P, i32, P, P, P,
                                                      P, P, P, sz, P]),
         }
@@ -162,9 +163,13 @@ def _ptr(t: torch.Tensor, dtype, name: str, numel: int | None = None):
     return ctypes.c_void_p(t.data_ptr())
 
 
-def _rptr(R, name: str, d: int = HEAD_DIM):
-    """A rotation matrix (fp32 [d, d] on the GPU), or None for the identity."""
-    return None if R is None else _ptr(R, torch.float32, name, d * d)
+def _rptr(R, name: str, d: int = HEAD_DIM, layout=None):
+    """A rotation matrix (fp32 [d, d] on the GPU; [Hkv, d, d] when the layout has
+    one per KV head), or None for the identity."""
+    if R is None:
+        return None
+    n = d * d * (layout.num_kv_heads if layout is not None and layout.rot_per_head else 1)
+    return _ptr(R, torch.float32, name, n)
 
 
 # ---------------------------------------------------------------------------
@@ -217,7 +222,7 @@ def kv_append(layout: Layout, pages, k_new, v_new, slot_mapping, R_k, R_v, clip_
         _ptr(k_new, torch.bfloat16, "k_new", n_tok * hkv * d),
         _ptr(v_new, torch.bfloat16, "v_new", n_tok * hkv * d),
         _ptr(slot_mapping, torch.int64, "slot_mapping"), n_tok,
-        _rptr(R_k, "R_k", d), _rptr(R_v, "R_v", d),
+        _rptr(R_k, "R_k", d, layout), _rptr(R_v, "R_v", d, layout),
         float(clip_k), float(clip_v), _stream(stream))
     _check(st, "oscar_kv_append")
 
@@ -242,8 +247,8 @@ def decode_attn(layout: Layout, pages, q, block_table, seq_lens, R_k, R_v, sm_sc
         ctypes.byref(layout), _ptr(pages, torch.uint8, "pages", pool_bytes(layout)),
         _ptr(q, torch.bfloat16, "q", B * Hq * d), B, Hq,
         _ptr(block_table, torch.int32, "block_table", B * mp), mp,
-        _ptr(seq_lens, torch.int32, "seq_lens", B), _rptr(R_k, "R_k", d),
-        _rptr(R_v, "R_v", d), float(sm_scale), int(num_splits),
+        _ptr(seq_lens, torch.int32, "seq_lens", B), _rptr(R_k, "R_k", d, layout),
+        _rptr(R_v, "R_v", d, layout), float(sm_scale), int(num_splits),
         _ptr(workspace, torch.uint8, "workspace"), workspace.numel(),
         _ptr(out, out.dtype, "out", B * Hq * d), out_dtype, _stream(stream))
     _check(st, "oscar_decode_attn")
@@ -265,8 +270,8 @@ def decode_step(layout: Layout, pages, k_new, v_new, slot_mapping, clip_k: float
         ctypes.byref(layout), _ptr(pages, torch.uint8, "pages", pool_bytes(layout)), kp, vp, sp,
         n_new, float(clip_k), float(clip_v), _ptr(q, torch.bfloat16, "q", B * Hq * d), B, Hq,
         _ptr(block_table, torch.int32, "block_table", B * mp), mp,
-        _ptr(seq_lens, torch.int32, "seq_lens", B), _rptr(R_k, "R_k", d),
-        _rptr(R_v, "R_v", d), float(sm_scale), int(num_splits),
+        _ptr(seq_lens, torch.int32, "seq_lens", B), _rptr(R_k, "R_k", d, layout),
+        _rptr(R_v, "R_v", d, layout), float(sm_scale), int(num_splits),
         _ptr(workspace, torch.uint8, "workspace"), workspace.numel(),
         _ptr(out, out.dtype, "out", B * Hq * d), out_dtype, _stream(stream))
     _check(st, "oscar_decode_step")
@@ -277,7 +282,7 @@ def decode_prepare(layout: Layout, q, R_k, sm_scale: float, num_splits: int, wor
     B, Hq, d = int(q.shape[0]), int(q.shape[1]), layout.head_dim
     st = lib().oscar_decode_prepare(
         ctypes.byref(layout), _ptr(q, torch.bfloat16, "q", B * Hq * d), B, Hq,
-        _rptr(R_k, "R_k", d), float(sm_scale), int(num_splits),
+        _rptr(R_k, "R_k", d, layout), float(sm_scale), int(num_splits),
         _ptr(workspace, torch.uint8, "workspace"), workspace.numel(), _stream(stream))
     _check(st, "oscar_decode_prepare")
 
@@ -298,7 +303,7 @@ def decode_reduce(layout: Layout, B: int, Hq: int, R_v, num_splits: int, workspa
     d = layout.head_dim
     out_dtype = OUT_F32 if out.dtype == torch.float32 else OUT_BF16
     st = lib().oscar_decode_reduce(
-        ctypes.byref(layout), B, Hq, _rptr(R_v, "R_v", d), int(num_splits),
+        ctypes.byref(layout), B, Hq, _rptr(R_v, "R_v", d, layout), int(num_splits),
         _ptr(workspace, torch.uint8, "workspace"), workspace.numel(),
         _ptr(out, out.dtype, "out", B * Hq * d), out_dtype, _stream(stream))
     _check(st, "oscar_decode_reduce")
@@ -348,8 +353,8 @@ def mixed_append(layout: Layout, pages, seg, S0: int, W: int, k, v, seq_idx, pos
         _ptr(k, torch.bfloat16, "k", n_tok * hkv * d), _ptr(v, torch.bfloat16, "v", n_tok * hkv * d),
         _ptr(seq_idx, torch.int32, "seq_idx", n_tok), _ptr(pos, torch.int64, "pos", n_tok), n_tok,
         _ptr(block_table, torch.int32, "block_table", B * mp), mp,
-        _ptr(seq_lens, torch.int32, "seq_lens", B), _rptr(R_k, "R_k", d),
-        _rptr(R_v, "R_v", d), float(clip_k), float(clip_v), _stream(stream))
+        _ptr(seq_lens, torch.int32, "seq_lens", B), _rptr(R_k, "R_k", d, layout),
+        _rptr(R_v, "R_v", d, layout), float(clip_k), float(clip_v), _stream(stream))
     _check(st, "oscar_mixed_append")
 
 
@@ -364,8 +369,8 @@ def decode_attn_mixed(layout: Layout, pages, seg, S0: int, W: int, q, block_tabl
         _seg_ptr(layout, seg, B, S0, W), int(S0), int(W),
         _ptr(q, torch.bfloat16, "q", B * Hq * d), B, Hq,
         _ptr(block_table, torch.int32, "block_table", B * mp), mp,
-        _ptr(seq_lens, torch.int32, "seq_lens", B), _rptr(R_k, "R_k", d),
-        _rptr(R_v, "R_v", d), float(sm_scale), int(num_splits),
+        _ptr(seq_lens, torch.int32, "seq_lens", B), _rptr(R_k, "R_k", d, layout),
+        _rptr(R_v, "R_v", d, layout), float(sm_scale), int(num_splits),
         _ptr(workspace, torch.uint8, "workspace"), workspace.numel(),
         _ptr(out, out.dtype, "out", B * Hq * d), out_dtype, _stream(stream))
     _check(st, "oscar_decode_attn_mixed")
@@ -386,8 +391,8 @@ def decode_step_mixed(layout: Layout, pages, seg, S0: int, W: int, k_new, v_new,
         _ptr(v_new, torch.bfloat16, "v_new", B * hkv * d), float(clip_k), float(clip_v),
         _ptr(q, torch.bfloat16, "q", B * Hq * d), B, Hq,
         _ptr(block_table, torch.int32, "block_table", B * mp), mp,
-        _ptr(seq_lens, torch.int32, "seq_lens", B), _rptr(R_k, "R_k", d),
-        _rptr(R_v, "R_v", d), float(sm_scale), int(num_splits),
+        _ptr(seq_lens, torch.int32, "seq_lens", B), _rptr(R_k, "R_k", d, layout),
+        _rptr(R_v, "R_v", d, layout), float(sm_scale), int(num_splits),
         _ptr(workspace, torch.uint8, "workspace"), workspace.numel(),
         _ptr(out, out.dtype, "out", B * Hq * d), out_dtype, _stream(stream))
     _check(st, "oscar_decode_step_mixed")
@@ -528,33 +533,35 @@ def calib_clip(layout: Layout, x, R, cands, workspace=None, stream=None):
         int(lib().oscar_calib_clip_workspace_bytes(n_tok, layout.num_kv_heads, nc)),
         "calib_clip_workspace_bytes")
     _check(lib().oscar_calib_clip(ctypes.byref(layout), _ptr(x, torch.bfloat16, "x"), n_tok,
-                                  _rptr(R, "R"), _ptr(cands, torch.float32, "cands"), nc,
+                                  _rptr(R, "R", HEAD_DIM, layout), _ptr(cands, torch.float32, "cands"), nc,
                                   _ptr(err, torch.float64, "err"), _ptr(best, torch.float32, "best"),
                                   _ptr(ws, torch.uint8, "ws"), ws.numel(), _stream(stream)),
            "oscar_calib_clip")
     return err, best
 
 
-def calibrate_layer_workspace_bytes(T: int, Hq: int, Hkv: int, n_cands: int) -> int:
-    return int(lib().oscar_calibrate_layer_workspace_bytes(T, Hq, Hkv, n_cands))
+def calibrate_layer_workspace_bytes(layout: Layout, T: int, Hq: int, n_cands: int) -> int:
+    return int(lib().oscar_calibrate_layer_workspace_bytes(ctypes.byref(layout), T, Hq, n_cands))
 
 
 def calibrate_layer(layout: Layout, q, k, v, cands, causal: bool = True, workspace=None,
                     stream=None) -> dict:
-    """Alg. 1 Calibrate for one layer: R_K, R_V (fp32 [d, d]), clip (c_K, c_V),
-    lam [2, d] (spectra of C_Q and C_S) and info [2]."""
+    """Alg. 1 Calibrate for one layer: R_K, R_V (fp32 [d, d], or [Hkv, d, d] when
+    the layout has one rotation per KV head), clip (c_K, c_V), lam (spectra of
+    C_Q and C_S) and info."""
     T, Hq, Hkv = _qkv_shapes(q, k, v)
     if Hkv != layout.num_kv_heads:
         raise ValueError("k has %d heads, layout %d" % (Hkv, layout.num_kv_heads))
     nc = int(cands.numel())
     dev = q.device
-    Rk = torch.empty(HEAD_DIM, HEAD_DIM, dtype=torch.float32, device=dev)
+    hm = (Hkv,) if layout.rot_per_head else ()
+    Rk = torch.empty(*hm, HEAD_DIM, HEAD_DIM, dtype=torch.float32, device=dev)
     Rv = torch.empty_like(Rk)
     clip = torch.empty(2, dtype=torch.float32, device=dev)
-    lam = torch.empty(2, HEAD_DIM, dtype=torch.float64, device=dev)
-    info = torch.empty(2, dtype=torch.int32, device=dev)
+    lam = torch.empty(2, *hm, HEAD_DIM, dtype=torch.float64, device=dev)
+    info = torch.empty(2, *hm, dtype=torch.int32, device=dev)
     ws = workspace if workspace is not None else _ws(
-        calibrate_layer_workspace_bytes(T, Hq, Hkv, nc), "calibrate_layer_workspace_bytes")
+        calibrate_layer_workspace_bytes(layout, T, Hq, nc), "calibrate_layer_workspace_bytes")
     _check(lib().oscar_calibrate_layer(ctypes.byref(layout), _ptr(q, torch.bfloat16, "q"),
                                        _ptr(k, torch.bfloat16, "k"), _ptr(v, torch.bfloat16, "v"),
                                        T, Hq, int(bool(causal)), _ptr(cands, torch.float32, "cands"),

@@ -203,10 +203,12 @@ constexpr int kPrepRows = 8;
 __device__ inline void prepare_body(float* Rsf, float4 (*qs)[kD / 4], int bx,
                                     const uint16_t* __restrict__ q, int rows,
                                     const float* __restrict__ Rk, float qscale,
-                                    float* __restrict__ qt) {
+                                    float* __restrict__ qt, int rph, int Hq, int Hkv) {
   float4* Rs = reinterpret_cast<float4*>(Rsf);
-  const int r0 = bx * kPrepRows;
   const int t = threadIdx.x;
+  int kvh;
+  query_row(bx, 0, kPrepRows, rows, Hq, Hkv, rph, kvh);
+  if (Rk && rph) Rk += (size_t)kvh * kD * kD;  // the block's rows share a KV head
   if (Rk) {
     // 16 float4 per thread, all loads issued before the stores (no per-load wait)
     float4 v[kD * kD / 4 / 256];
@@ -217,9 +219,11 @@ __device__ inline void prepare_body(float* Rsf, float4 (*qs)[kD / 4], int bx,
   }
   {  // 8 rows x 128 bf16 = 256 threads x 4 values
     const int r = t >> 5, c4 = t & 31;
+    int kv_;
+    const int row = query_row(bx, r, kPrepRows, rows, Hq, Hkv, rph, kv_);
     float4 x = make_float4(0.0f, 0.0f, 0.0f, 0.0f);
-    if (r0 + r < rows) {
-      const uint2 w = reinterpret_cast<const uint2*>(q + (size_t)(r0 + r) * kD)[c4];
+    if (row >= 0) {
+      const uint2 w = reinterpret_cast<const uint2*>(q + (size_t)row * kD)[c4];
       x = make_float4(bf16_to_f32((uint16_t)(w.x & 0xffffu)), bf16_to_f32((uint16_t)(w.x >> 16)),
                       bf16_to_f32((uint16_t)(w.y & 0xffffu)), bf16_to_f32((uint16_t)(w.y >> 16)));
     }
@@ -250,8 +254,11 @@ __device__ inline void prepare_body(float* Rsf, float4 (*qs)[kD / 4], int bx,
     for (int i = 0; i < 4; ++i) acc[i] = Q[(rg + i) * kD + j];
   }
 #pragma unroll
-  for (int i = 0; i < 4; ++i)
-    if (r0 + rg + i < rows) qt[(size_t)(r0 + rg + i) * kD + j] = acc[i] * qscale;
+  for (int i = 0; i < 4; ++i) {
+    int kv_;
+    const int row = query_row(bx, rg + i, kPrepRows, rows, Hq, Hkv, rph, kv_);
+    if (row >= 0) qt[(size_t)row * kD + j] = acc[i] * qscale;
+  }
 }
 
 // ---------------------------------------------------------------------------
@@ -466,6 +473,17 @@ __device__ inline void append_body(float* Rs, double (*xs)[RW][kD], int is_v, in
                                    const QFmt& fmt) {
   const float* __restrict__ R = is_v ? Rv : Rk;  // nullptr: identity
   const float clip = is_v ? clip_v : clip_k;
+  // rph: the block takes the rows (token, h) of one KV head h, so that it stages
+  // that head's matrix; gx is then a multiple of Hkv
+  int h = 0;
+  if (fmt.rph) {
+    h = bx % Hkv;
+    bx /= Hkv;
+    gx /= Hkv;
+    if (R) R += (size_t)h * kD * kD;
+  }
+  const int n_seq = fmt.rph ? n_rows / Hkv : n_rows;
+  auto row_at = [&](int i) { return fmt.rph ? (i < n_seq ? i * Hkv + h : n_rows) : i; };
 
   if (R) {  // 16 float4 per thread, all loads issued before the stores
     float4 r4[kD * kD / 4 / 256];
@@ -479,13 +497,13 @@ __device__ inline void append_body(float* Rs, double (*xs)[RW][kD], int is_v, in
 
   const int w = threadIdx.x >> 6;
   const int l = threadIdx.x & 63;
-  const int n_items = (n_rows + RW - 1) / RW;
+  const int n_items = (n_seq + RW - 1) / RW;
 
   // each wave owns xs[w]: no block-level synchronization inside the loop
   for (int item = bx * kWaves + w; item < n_items; item += gx * kWaves) {
 #pragma unroll
     for (int rr = 0; rr < RW; ++rr) {
-      const int row = item * RW + rr;
+      const int row = row_at(item * RW + rr);
       double x0 = 0.0, x1 = 0.0;
       const uint16_t* src = rows.src(row, is_v);
       if (src) {
@@ -523,7 +541,7 @@ __device__ inline void append_body(float* Rs, double (*xs)[RW][kD], int is_v, in
 
 #pragma unroll
     for (int rr = 0; rr < RW; ++rr) {
-      const int row = item * RW + rr;
+      const int row = row_at(item * RW + rr);
       store_row(pages, Hkv, rows.slot(row), row, is_v, clip, fmt, acc0[rr], acc1[rr], l);
     }
   }
@@ -531,7 +549,7 @@ __device__ inline void append_body(float* Rs, double (*xs)[RW][kD], int is_v, in
 
 // DEF: the default format (binary16 metadata, group-absmax clip, 32-channel
 // groups) as compile-time constants, so that its code has no format branches.
-__device__ inline QFmt pick(bool def, const QFmt& fmt) { return def ? QFmt{0, 0, 4} : fmt; }
+__device__ inline QFmt pick(bool def, const QFmt& fmt) { return def ? QFmt{0, 0, 4, 0} : fmt; }
 
 template <int RW, class Rows, bool DEF>
 __global__ __launch_bounds__(256) void append_kernel(uint8_t* __restrict__ pages, int Hkv,
@@ -645,6 +663,16 @@ __global__ __launch_bounds__(512) void append_bulk_kernel(
   const float* __restrict__ R = is_v ? Rv : Rk;  // nullptr: identity
   const float clip = is_v ? clip_v : clip_k;
   const int t = threadIdx.x;
+  // rph: one KV head's rows per block (gridDim.x is then a multiple of Hkv)
+  int h = 0, bx = blockIdx.x, gx = gridDim.x;
+  if (fmt.rph) {
+    h = bx % Hkv;
+    bx /= Hkv;
+    gx /= Hkv;
+    if (R) R += (size_t)h * kD * kD;
+  }
+  const int n_seq = fmt.rph ? n_rows / Hkv : n_rows;
+  auto row_at = [&](int i) { return fmt.rph ? (i < n_seq ? i * Hkv + h : n_rows) : i; };
   if (R) {  // 8 float4 per thread, loads issued before the stores
     float4 r4[kD * kD / 4 / 512];
 #pragma unroll
@@ -662,11 +690,11 @@ __global__ __launch_bounds__(512) void append_bulk_kernel(
   }
   __syncthreads();
   const int w = t >> 6, l = t & 63, half = l >> 5, lp = l & 31;
-  const int n_items = (n_rows + kBulkRows - 1) / kBulkRows;
-  for (int item = blockIdx.x * kBulkWaves + w; item < n_items; item += gridDim.x * kBulkWaves) {
+  const int n_items = (n_seq + kBulkRows - 1) / kBulkRows;
+  for (int item = bx * kBulkWaves + w; item < n_items; item += gx * kBulkWaves) {
 #pragma unroll
     for (int rr = 0; rr < kBulkRows; ++rr) {
-      const int row = item * kBulkRows + rr;
+      const int row = row_at(item * kBulkRows + rr);
       double2 x = make_double2(0.0, 0.0);
       const uint16_t* src = rows.src(row, is_v);
       if (src) {
@@ -707,7 +735,7 @@ __global__ __launch_bounds__(512) void append_bulk_kernel(
     }
 #pragma unroll
     for (int p = 0; p < kBulkRows / 2; ++p) {
-      const int row = item * kBulkRows + 2 * p + half;
+      const int row = row_at(item * kBulkRows + 2 * p + half);
       store_row4(pages, Hkv, rows.slot(row), row, is_v, clip, fmt, acc[p], lp, half);
     }
   }
@@ -715,10 +743,11 @@ __global__ __launch_bounds__(512) void append_bulk_kernel(
 
 __global__ __launch_bounds__(256) void prepare_kernel(const uint16_t* __restrict__ q, int rows,
                                                       const float* __restrict__ Rk, float qscale,
-                                                      float* __restrict__ qt) {
+                                                      float* __restrict__ qt, int rph, int Hq,
+                                                      int Hkv) {
   __shared__ float Rs[kD * kD];
   __shared__ float4 qs[kPrepRows][kD / 4];
-  prepare_body(Rs, qs, blockIdx.x, q, rows, Rk, qscale, qt);
+  prepare_body(Rs, qs, blockIdx.x, q, rows, Rk, qscale, qt, rph, Hq, Hkv);
 }
 
 // One launch for a decode step's prologue: blockIdx.y 0/1 = K/V cache update
@@ -728,7 +757,7 @@ template <int RW, class Rows, bool DEF>
 __global__ __launch_bounds__(256) void prologue_kernel(
     uint8_t* __restrict__ pages, int Hkv, Rows rows, int n_rows, const float* __restrict__ Rk,
     const float* __restrict__ Rv, float clip_k, float clip_v, QFmt fmt_arg, int append_blocks,
-    const uint16_t* __restrict__ q, int q_rows, float qscale, float* __restrict__ qt,
+    const uint16_t* __restrict__ q, int q_rows, int Hq, float qscale, float* __restrict__ qt,
     int prep_blocks) {
   __shared__ float Rs[kD * kD];
   __shared__ double xs[kWaves][RW][kD];
@@ -738,7 +767,7 @@ __global__ __launch_bounds__(256) void prologue_kernel(
       append_body<RW>(Rs, xs, blockIdx.y, blockIdx.x, append_blocks, pages, Hkv, rows, n_rows,
                       Rk, Rv, clip_k, clip_v, pick(DEF, fmt_arg));
   } else if ((int)blockIdx.x < prep_blocks) {
-    prepare_body(Rs, qs, blockIdx.x, q, q_rows, Rk, qscale, qt);
+    prepare_body(Rs, qs, blockIdx.x, q, q_rows, Rk, qscale, qt, fmt_arg.rph, Hq, Hkv);
   }
 }
 
@@ -786,12 +815,21 @@ __device__ inline float sorted_at(float v0, float v1, int e) {  // e wave-unifor
 __global__ __launch_bounds__(256) void clip_err_kernel(const uint16_t* __restrict__ x, int n_rows,
                                                        const float* __restrict__ R,
                                                        const float* __restrict__ cands,
-                                                       int n_cands, QFmt fmt,
+                                                       int n_cands, QFmt fmt, int Hkv,
                                                        double* __restrict__ partial) {
   __shared__ float Rs[kD * kD];
   __shared__ double xs[kWaves][kD];
   __shared__ double werr[kWaves][kMaxClipCands];
   const int w = threadIdx.x >> 6, l = threadIdx.x & 63;
+  // rph: the block takes the rows (token, h) of one KV head h and its matrix
+  int h = 0, bx = blockIdx.x, gx = gridDim.x;
+  if (fmt.rph) {
+    h = bx % Hkv;
+    bx /= Hkv;
+    gx /= Hkv;
+    if (R) R += (size_t)h * kD * kD;
+  }
+  const int n_seq = fmt.rph ? n_rows / Hkv : n_rows;
   if (R) {
     float4 r4[kD * kD / 4 / 256];
 #pragma unroll
@@ -804,7 +842,8 @@ __global__ __launch_bounds__(256) void clip_err_kernel(const uint16_t* __restric
   double e[kMaxClipCands];
 #pragma unroll
   for (int n = 0; n < kMaxClipCands; ++n) e[n] = 0.0;
-  for (int row = blockIdx.x * kWaves + w; row < n_rows; row += gridDim.x * kWaves) {
+  for (int i = bx * kWaves + w; i < n_seq; i += gx * kWaves) {
+    const int row = fmt.rph ? i * Hkv + h : i;
     const uint32_t pair = reinterpret_cast<const uint32_t*>(x + (size_t)row * kD)[l];
     xs[w][2 * l] = (double)__uint_as_float(pair << 16);
     xs[w][2 * l + 1] = (double)__uint_as_float(pair & 0xffff0000u);
@@ -912,15 +951,24 @@ int64_t append_blocks_for(int64_t n_rows, int rw) {
   const int64_t blocks = (n_items + kWaves - 1) / kWaves;
   return blocks > 1024 ? 1024 : blocks;
 }
+// With one rotation per KV head a block takes one head's rows: a multiple of Hkv
+// blocks, each head's share sized for its n_rows / Hkv rows.
+int64_t append_blocks_rph(int64_t n_rows, int rw, int64_t Hkv, int rph) {
+  if (!rph) return append_blocks_for(n_rows, rw);
+  const int64_t n_items = (n_rows / Hkv + rw - 1) / rw;
+  int64_t per = (n_items + kWaves - 1) / kWaves;
+  per = std::max<int64_t>(1, std::min(per, std::max<int64_t>(1, 1024 / Hkv)));
+  return per * Hkv;
+}
 
-bool is_default(const QFmt& f) { return f.bf16 == 0 && f.quantile == 0 && f.ng == 4; }
+bool is_default(const QFmt& f) { return f.bf16 == 0 && f.quantile == 0 && f.ng == 4 && f.rph == 0; }
 
 template <class Rows>
 hipError_t launch_rows(void* pages, int64_t Hkv, const Rows& rows, int64_t n_rows, const float* Rk,
                        const float* Rv, float clip_k, float clip_v, QFmt fmt, hipStream_t st) {
   const bool def = is_default(fmt);
   if (n_rows <= 4096) {  // one decode step: many short waves
-    const dim3 grid((unsigned)append_blocks_for(n_rows, 1), 2);
+    const dim3 grid((unsigned)append_blocks_rph(n_rows, 1, Hkv, fmt.rph), 2);
     auto go = [&](auto kernel) {
       hipLaunchKernelGGL(kernel, grid, dim3(256), 0, st, static_cast<uint8_t*>(pages), (int)Hkv,
                          rows, (int)n_rows, Rk, Rv, clip_k, clip_v, fmt);
@@ -928,10 +976,12 @@ hipError_t launch_rows(void* pages, int64_t Hkv, const Rows& rows, int64_t n_row
     if (def) go(append_kernel<1, Rows, true>);
     else go(append_kernel<1, Rows, false>);
   } else {  // bulk: one persistent 8-wave block per CU, half of them per tensor
-    const int64_t items = (n_rows + kBulkRows - 1) / kBulkRows;
+    const int64_t heads = fmt.rph ? Hkv : 1;  // rph: a block per head's share
+    const int64_t items = (n_rows / heads + kBulkRows - 1) / kBulkRows;
     int64_t nb = (items + kBulkWaves - 1) / kBulkWaves;
-    const int64_t cap = std::max<int64_t>(1, device_cus() / 2);
+    const int64_t cap = std::max<int64_t>(1, device_cus() / 2 / heads);
     if (nb > cap) nb = cap;
+    nb *= heads;
     auto go = [&](auto kernel) {
       hipLaunchKernelGGL(kernel, dim3((unsigned)nb, 2), dim3(512), 0, st,
                          static_cast<uint8_t*>(pages), (int)Hkv, rows, (int)n_rows, Rk, Rv,
@@ -949,13 +999,13 @@ hipError_t launch_prologue(void* pages, int64_t Hkv, const Rows& rows, int64_t n
                            QFmt fmt, const uint16_t* q, int B, int Hq, float qscale, float* qt,
                            hipStream_t st) {
   const int rw = n_rows <= 4096 ? 1 : 4;
-  const int ab = n_rows > 0 ? (int)append_blocks_for(n_rows, rw) : 0;
-  const int pb = (B * Hq + kPrepRows - 1) / kPrepRows;
+  const int ab = n_rows > 0 ? (int)append_blocks_rph(n_rows, rw, Hkv, fmt.rph) : 0;
+  const int pb = query_blocks(B, Hq, (int)Hkv, fmt.rph, kPrepRows);
   const dim3 grid((unsigned)(ab > pb ? ab : pb), 3);
   auto go = [&](auto kernel) {
     hipLaunchKernelGGL(kernel, grid, dim3(256), 0, st, static_cast<uint8_t*>(pages), (int)Hkv,
-                       rows, (int)n_rows, Rk, Rv, clip_k, clip_v, fmt, ab, q, B * Hq, qscale, qt,
-                       pb);
+                       rows, (int)n_rows, Rk, Rv, clip_k, clip_v, fmt, ab, q, B * Hq, Hq, qscale,
+                       qt, pb);
   };
   const bool def = is_default(fmt);
   if (rw == 1) {
@@ -990,10 +1040,10 @@ hipError_t launch_mixed_append(void* pages, uint16_t* seg, int64_t Hkv, int S0, 
 }
 
 hipError_t launch_decode_prepare(const uint16_t* q, int B, int Hq, const float* Rk,
-                                 float qscale, float* qt, hipStream_t st) {
+                                 float qscale, float* qt, hipStream_t st, int rph, int Hkv) {
   const int rows = B * Hq;
-  hipLaunchKernelGGL(prepare_kernel, dim3((rows + kPrepRows - 1) / kPrepRows), dim3(256), 0, st,
-                     q, rows, Rk, qscale, qt);
+  hipLaunchKernelGGL(prepare_kernel, dim3(query_blocks(B, Hq, Hkv, rph, kPrepRows)), dim3(256), 0,
+                     st, q, rows, Rk, qscale, qt, rph, Hq, Hkv);
   return hipGetLastError();
 }
 
@@ -1021,10 +1071,11 @@ hipError_t launch_mixed_step_prologue(void* pages, uint16_t* seg, int64_t Hkv, i
 }
 
 hipError_t launch_clip_errors(const uint16_t* x, int64_t n_rows, const float* R,
-                              const float* cands, int n_cands, QuantFmt fmt, double* partial,
-                              int n_blocks, double* err, float* best, hipStream_t st) {
+                              const float* cands, int n_cands, QuantFmt fmt, int Hkv,
+                              double* partial, int n_blocks, double* err, float* best,
+                              hipStream_t st) {
   hipLaunchKernelGGL(clip_err_kernel, dim3((unsigned)n_blocks), dim3(256), 0, st, x, (int)n_rows, R,
-                     cands, n_cands, fmt, partial);
+                     cands, n_cands, fmt, Hkv, partial);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   hipLaunchKernelGGL(clip_reduce_kernel, dim3(1), dim3(kClipParts * kMaxClipCands), 0, st, partial,
@@ -1033,10 +1084,11 @@ hipError_t launch_clip_errors(const uint16_t* x, int64_t n_rows, const float* R,
   return hipGetLastError();
 }
 
-int clip_blocks(int64_t n_rows) {
-  const int64_t items = (n_rows + kWaves - 1) / kWaves;
-  const int64_t cap = 4 * (int64_t)device_cus();
-  return (int)std::max<int64_t>(1, std::min(items, cap));
+int clip_blocks(int64_t n_rows, int Hkv, int rph) {
+  const int64_t heads = rph ? Hkv : 1;  // rph: blocks per head, times Hkv
+  const int64_t items = (n_rows / heads + kWaves - 1) / kWaves;
+  const int64_t cap = std::max<int64_t>(1, 4 * (int64_t)device_cus() / heads);
+  return (int)(std::max<int64_t>(1, std::min(items, cap)) * heads);
 }
 
 }  // namespace oscar

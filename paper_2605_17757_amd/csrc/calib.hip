@@ -49,10 +49,17 @@ __device__ inline void gram_tile(int t, int& ti, int& tj) {
   tj = ti + (t - first);
 }
 
+// Row r of X is at element (r / rpt) * tok_stride + (r % rpt) * 128: rpt
+// consecutive rows per token (one KV head's query heads), tokens tok_stride apart.
+__device__ inline int64_t gram_row(int64_t r, int64_t rpt, int64_t tok_stride) {
+  return (r / rpt) * tok_stride + (r % rpt) * kD;
+}
+
 template <bool BF16>
 __global__ __launch_bounds__(kGramWaves * 64) void gram_kernel(const void* __restrict__ X,
                                                               int64_t n_rows,
                                                               int64_t rows_per_block,
+                                                              int64_t rpt, int64_t tok_stride,
                                                               float* __restrict__ partial) {
   __shared__ float xs[kGramRows * kGramPitch];
   const int tid = threadIdx.x, w = tid >> 6, l = tid & 63, h = l >> 5, li = l & 31;
@@ -69,7 +76,8 @@ __global__ __launch_bounds__(kGramWaves * 64) void gram_kernel(const void* __res
       for (int idx = tid; idx < kGramRows * 16; idx += kGramWaves * 64) {
         const int row = idx >> 4, c8 = idx & 15;
         uint4 u = make_uint4(0, 0, 0, 0);
-        if (base + row < r1) u = *reinterpret_cast<const uint4*>(x + (base + row) * kD + c8 * 8);
+        if (base + row < r1)
+          u = *reinterpret_cast<const uint4*>(x + gram_row(base + row, rpt, tok_stride) + c8 * 8);
         float* dst = xs + row * kGramPitch + c8 * 8;
         const uint32_t wd[4] = {u.x, u.y, u.z, u.w};
 #pragma unroll
@@ -83,7 +91,8 @@ __global__ __launch_bounds__(kGramWaves * 64) void gram_kernel(const void* __res
       for (int idx = tid; idx < kGramRows * 32; idx += kGramWaves * 64) {
         const int row = idx >> 5, c4 = idx & 31;
         float4 f = make_float4(0.0f, 0.0f, 0.0f, 0.0f);
-        if (base + row < r1) f = *reinterpret_cast<const float4*>(x + (base + row) * kD + c4 * 4);
+        if (base + row < r1)
+          f = *reinterpret_cast<const float4*>(x + gram_row(base + row, rpt, tok_stride) + c4 * 4);
         *reinterpret_cast<float4*>(xs + row * kGramPitch + c4 * 4) = f;
       }
     }
@@ -599,16 +608,16 @@ size_t gram_partial_bytes(int64_t n_rows) {
 }
 
 hipError_t launch_gram(const void* X, int x_bf16, int64_t n_rows, double inv_n, float* partial,
-                       double* C, hipStream_t st) {
+                       double* C, hipStream_t st, int64_t rpt, int64_t tok_stride) {
   const int64_t nb = gram_blocks(n_rows);
   int64_t per = (n_rows + nb - 1) / nb;
   per = (per + kGramRows - 1) / kGramRows * kGramRows;
   if (x_bf16)
     hipLaunchKernelGGL(gram_kernel<true>, dim3((unsigned)nb), dim3(kGramWaves * 64), 0, st, X,
-                       n_rows, per, partial);
+                       n_rows, per, rpt, tok_stride, partial);
   else
     hipLaunchKernelGGL(gram_kernel<false>, dim3((unsigned)nb), dim3(kGramWaves * 64), 0, st, X,
-                       n_rows, per, partial);
+                       n_rows, per, rpt, tok_stride, partial);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   hipLaunchKernelGGL(gram_reduce_kernel, dim3(kGramTiles * 1024 / 32), dim3(256), 0, st,

@@ -40,20 +40,30 @@ constexpr int kRvPitch4 = kD / 4 + 1;  // row pitch of the LDS copy in float4
 
 // MIXED: a row has num_splits + 1 slots; the last holds the bf16 tokens' state
 // in the original basis, o = (sum_s e_s o~_s R_v^T + e_b o_b) / L.
+// Rows are taken 8 per block in the natural order, or (rph: one R_v per KV head)
+// 8 rows of one KV head per block.
 template <bool MIXED>
 __global__ __launch_bounds__(256) void reduce_kernel(int rows, int num_splits,
                                                      const float* __restrict__ part_o,
                                                      const float* __restrict__ part_ml,
                                                      const float* __restrict__ Rv,
-                                                     void* __restrict__ out, int out_f32) {
+                                                     void* __restrict__ out, int out_f32, int rph,
+                                                     int Hq, int Hkv) {
   __shared__ float4 Rs[kD * kRvPitch4];
   __shared__ float4 om[kRedRows][kD / 4];
   __shared__ float eb_il[kRedRows];  // MIXED: e_b / L per row
   const int stride = MIXED ? num_splits + 1 : num_splits;
-  const int r0 = blockIdx.x * kRedRows;
   const int t = threadIdx.x;
+  int kvh;
+  query_row(blockIdx.x, 0, kRedRows, rows, Hq, Hkv, rph, kvh);
+  if (Rv && rph) Rv += (size_t)kvh * kD * kD;
+  auto row_of = [&](int r) {  // the block's r-th row, or rows (past the end)
+    int kv_;
+    const int x = query_row(blockIdx.x, r, kRedRows, rows, Hq, Hkv, rph, kv_);
+    return x < 0 ? rows : x;
+  };
   {  // 8 rows x 32 float4 columns: one (row, float4) per thread
-    const int rr = t >> 5, c4 = t & 31, r = r0 + rr;
+    const int rr = t >> 5, c4 = t & 31, r = row_of(rr);
     float4 o = make_float4(0.0f, 0.0f, 0.0f, 0.0f);
     const float2* ml = reinterpret_cast<const float2*>(part_ml + (size_t)r * stride * 2);
     // live slots lead (empty ones only follow the end of a sequence): n_live is
@@ -158,7 +168,7 @@ __global__ __launch_bounds__(256) void reduce_kernel(int rows, int num_splits,
   if (MIXED) {  // the bf16 tokens' part, already in the original basis
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
-      const int r = r0 + rg + i;
+      const int r = row_of(rg + i);
       const float e = eb_il[rg + i];
       if (r < rows && e != 0.0f)
         acc[i] = fmaf(e, part_o[((size_t)r * stride + num_splits) * kD + j], acc[i]);
@@ -166,7 +176,7 @@ __global__ __launch_bounds__(256) void reduce_kernel(int rows, int num_splits,
   }
 #pragma unroll
   for (int i = 0; i < 4; ++i) {
-    const int r = r0 + rg + i;
+    const int r = row_of(rg + i);
     if (r >= rows) continue;
     if (out_f32) static_cast<float*>(out)[(size_t)r * kD + j] = acc[i];
     else static_cast<uint16_t*>(out)[(size_t)r * kD + j] = f32_to_bf16_rne(acc[i]);
@@ -188,15 +198,15 @@ hipError_t launch_decode_split(const uint8_t* pages, int Hkv, int B, int Hq,
 
 hipError_t launch_decode_reduce(int B, int Hq, int num_splits, const float* part_o,
                                 const float* part_ml, const float* Rv, void* out, int out_f32,
-                                hipStream_t st, const MixedSpec* mixed) {
+                                hipStream_t st, const MixedSpec* mixed, int rph, int Hkv) {
   const int rows = B * Hq;
-  const dim3 grid((rows + kRedRows - 1) / kRedRows);
+  const dim3 grid(query_blocks(B, Hq, Hkv, rph, kRedRows));
   if (mixed)
     hipLaunchKernelGGL(reduce_kernel<true>, grid, dim3(256), 0, st, rows, num_splits, part_o,
-                       part_ml, Rv, out, out_f32);
+                       part_ml, Rv, out, out_f32, rph, Hq, Hkv);
   else
     hipLaunchKernelGGL(reduce_kernel<false>, grid, dim3(256), 0, st, rows, num_splits, part_o,
-                       part_ml, Rv, out, out_f32);
+                       part_ml, Rv, out, out_f32, rph, Hq, Hkv);
   return hipGetLastError();
 }
 

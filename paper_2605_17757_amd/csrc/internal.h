@@ -49,8 +49,30 @@ struct MixedSpec {
 struct QuantFmt {
   int bf16;
   int quantile;
-  int ng;  // groups per head (128 / G)
+  int ng;   // groups per head (128 / G)
+  int rph;  // one rotation matrix per KV head ([Hkv][128][128]) instead of one shared
 };
+
+// Query rows (b, head) = b * Hq + head, taken n per block: block bx takes rows
+// bx * n + r in the natural order, or (rph) the rows of one KV head per block,
+// kvh = bx % Hkv, local rows (bx / Hkv) * n + r enumerating (b, head in the KV
+// head's group).  Returns the row, or -1 past the end.
+__device__ inline int query_row(int bx, int r, int n, int rows, int Hq, int Hkv, int rph,
+                                int& kvh) {
+  if (!rph) {
+    kvh = 0;
+    const int idx = bx * n + r;
+    return idx < rows ? idx : -1;
+  }
+  const int g = Hq / Hkv;
+  kvh = bx % Hkv;
+  const int idx = (bx / Hkv) * n + r;
+  return idx < (rows / Hq) * g ? (idx / g) * Hq + kvh * g + idx % g : -1;
+}
+// Blocks of n query rows: natural order, or (rph) per KV head.
+inline int query_blocks(int B, int Hq, int Hkv, int rph, int n) {
+  return rph ? Hkv * ((B * (Hq / Hkv) + n - 1) / n) : (B * Hq + n - 1) / n;
+}
 
 // Kernel launchers (each returns the hipError_t of its launch).
 // Rk or Rv nullptr: identity rotation.
@@ -59,7 +81,8 @@ hipError_t launch_append(void* pages, int64_t Hkv, const uint16_t* k, const uint
                          float clip_k, float clip_v, QuantFmt fmt, hipStream_t st);
 
 hipError_t launch_decode_prepare(const uint16_t* q, int B, int Hq, const float* Rk,
-                                 float qscale, float* qt, hipStream_t st);
+                                 float qscale, float* qt, hipStream_t st, int rph = 0,
+                                 int Hkv = 1);
 // Cache update of n_tok tokens and query rotation in one launch (decode step prologue).
 hipError_t launch_step_prologue(void* pages, int64_t Hkv, const uint16_t* k, const uint16_t* v,
                                 const int64_t* slots, int n_tok, const float* Rk,
@@ -108,7 +131,8 @@ int device_cus();  // compute units of the current device (cached)
 // basis (added after the back-rotation).
 hipError_t launch_decode_reduce(int B, int Hq, int num_splits, const float* part_o,
                                 const float* part_ml, const float* Rv, void* out, int out_f32,
-                                hipStream_t st, const MixedSpec* mixed = nullptr);
+                                hipStream_t st, const MixedSpec* mixed = nullptr, int rph = 0,
+                                int Hkv = 1);
 
 hipError_t launch_bf16_append(void* pages, int64_t Hkv, const uint16_t* k, const uint16_t* v,
                               const int64_t* slots, int n_tok, hipStream_t st);
@@ -121,8 +145,10 @@ hipError_t launch_bf16_split(const uint16_t* pages, int Hkv, int B, int Hq,
 // Second moment C = (X^T X) * inv_n of rows X [n_rows][128] (bf16 or fp32), fp64
 // [128][128]; partial: gram_partial_bytes(n_rows) bytes of scratch.
 size_t gram_partial_bytes(int64_t n_rows);
+// Row r of X at element (r / rpt) * tok_stride + (r % rpt) * 128 (rpt = 1,
+// tok_stride = 128: consecutive rows).
 hipError_t launch_gram(const void* X, int x_bf16, int64_t n_rows, double inv_n, float* partial,
-                       double* C, hipStream_t st);
+                       double* C, hipStream_t st, int64_t rpt = 1, int64_t tok_stride = kD);
 // O[t][i] = softmax(q_{t,i} K_h^T / sqrt(d) + M) V_h (fp32 [T][Hq][128]).
 hipError_t launch_calib_attn(const uint16_t* q, const uint16_t* k, const uint16_t* v, int T,
                              int Hq, int Hkv, int causal, float* out, hipStream_t st);
@@ -138,9 +164,11 @@ hipError_t launch_compose(const double* U, int n_mats, double* R64, float* R32, 
 // Mean squared quantization error of the rotated rows for each candidate clip
 // ratio (n_cands <= 32) and the first minimizing candidate; partial: n_blocks x
 // n_cands doubles, n_blocks = clip_blocks(n_rows).
-int clip_blocks(int64_t n_rows);
+// Rows x [n_rows / Hkv][Hkv][128]; with fmt.rph, R is [Hkv][128][128].
+int clip_blocks(int64_t n_rows, int Hkv, int rph);
 hipError_t launch_clip_errors(const uint16_t* x, int64_t n_rows, const float* R,
-                              const float* cands, int n_cands, QuantFmt fmt, double* partial,
-                              int n_blocks, double* err, float* best, hipStream_t st);
+                              const float* cands, int n_cands, QuantFmt fmt, int Hkv,
+                              double* partial, int n_blocks, double* err, float* best,
+                              hipStream_t st);
 
 }  // namespace oscar

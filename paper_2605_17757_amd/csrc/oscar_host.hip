@@ -42,6 +42,7 @@ int check_layout(const oscar_layout* L) {
   if (L->clip_mode != OSCAR_CLIP_GROUP_ABSMAX && L->clip_mode != OSCAR_CLIP_TOKEN_QUANTILE)
     return OSCAR_ERR_INVALID_ARG;
   if (L->meta_dtype != OSCAR_META_F16 && L->meta_dtype != OSCAR_META_BF16) return OSCAR_ERR_INVALID_ARG;
+  if (L->rot_per_head != 0 && L->rot_per_head != 1) return OSCAR_ERR_INVALID_ARG;
   if (L->head_dim != kD || L->page_size != kP ||
       (L->group_size != 32 && L->group_size != 64 && L->group_size != 128))
     return OSCAR_ERR_UNSUPPORTED;
@@ -79,7 +80,8 @@ bool aligned(const void* p, size_t a) { return (reinterpret_cast<uintptr_t>(p) &
 
 QuantFmt quant_fmt(const oscar_layout* L) {
   return QuantFmt{L->meta_dtype == OSCAR_META_BF16 ? 1 : 0,
-                  L->clip_mode == OSCAR_CLIP_TOKEN_QUANTILE ? 1 : 0, kD / L->group_size};
+                  L->clip_mode == OSCAR_CLIP_TOKEN_QUANTILE ? 1 : 0, kD / L->group_size,
+                  L->rot_per_head};
 }
 int meta_bf16(const oscar_layout* L) { return L->meta_dtype == OSCAR_META_BF16 ? 1 : 0; }
 int groups(const oscar_layout* L) { return kD / L->group_size; }
@@ -176,7 +178,8 @@ int oscar_decode_prepare(const oscar_layout* L, const void* q, int32_t B, int32_
   float* qt = reinterpret_cast<float*>(static_cast<uint8_t*>(workspace) + ws.qt_off);
   return hip_status(launch_decode_prepare(static_cast<const uint16_t*>(q), B, Hq, R_k,
                                           sm_scale * kLog2e, qt,
-                                          static_cast<hipStream_t>(stream)));
+                                          static_cast<hipStream_t>(stream), L->rot_per_head,
+                                          L->num_kv_heads));
 }
 
 int oscar_decode_split(const oscar_layout* L, const void* pages, int32_t B, int32_t Hq,
@@ -214,7 +217,8 @@ int oscar_decode_reduce(const oscar_layout* L, int32_t B, int32_t Hq, const floa
                                          reinterpret_cast<const float*>(base + ws.po_off),
                                          reinterpret_cast<const float*>(base + ws.pml_off), R_v,
                                          out, out_dtype == OSCAR_OUT_F32 ? 1 : 0,
-                                         static_cast<hipStream_t>(stream)));
+                                         static_cast<hipStream_t>(stream), nullptr,
+                                         L->rot_per_head, L->num_kv_heads));
 }
 
 int oscar_decode_attn(const oscar_layout* L, const void* pages, const void* q, int32_t B,
@@ -299,7 +303,8 @@ int oscar_decode_step(const oscar_layout* L, void* pages, const void* k_new, con
   return hip_status(launch_decode_reduce(B, Hq, num_splits,
                                          reinterpret_cast<const float*>(base + ws.po_off),
                                          reinterpret_cast<const float*>(base + ws.pml_off), R_v,
-                                         out, out_dtype == OSCAR_OUT_F32 ? 1 : 0, hs));
+                                         out, out_dtype == OSCAR_OUT_F32 ? 1 : 0, hs, nullptr,
+                                         L->rot_per_head, L->num_kv_heads));
 }
 
 // ---------------------------------------------------------------------------
@@ -397,7 +402,8 @@ int launch_mixed_rest(const oscar_layout* L, const void* pages, const void* seg,
                                      num_splits, po, pml, hs));
   if (st) return st;
   return hip_status(launch_decode_reduce(B, Hq, num_splits, po, pml, R_v, out,
-                                         out_dtype == OSCAR_OUT_F32 ? 1 : 0, hs, &mx));
+                                         out_dtype == OSCAR_OUT_F32 ? 1 : 0, hs, &mx,
+                                         L->rot_per_head, L->num_kv_heads));
 }
 
 }  // namespace
@@ -417,7 +423,8 @@ int oscar_decode_attn_mixed(const oscar_layout* L, const void* pages, const void
   const DecodeWs ws = decode_ws(B, Hq, (int64_t)num_splits + 1);
   float* qt = reinterpret_cast<float*>(static_cast<uint8_t*>(workspace) + ws.qt_off);
   st = hip_status(launch_decode_prepare(static_cast<const uint16_t*>(q), B, Hq, R_k,
-                                        sm_scale * kLog2e, qt, hs));
+                                        sm_scale * kLog2e, qt, hs,
+                                        L->rot_per_head, L->num_kv_heads));
   if (st) return st;
   return launch_mixed_rest(L, pages, seg, S0, W, q, B, Hq, block_table, max_pages_per_seq,
                            seq_lens, R_v, sm_scale, num_splits, workspace, out, out_dtype, hs);
@@ -562,8 +569,10 @@ RotWs rot_ws(int32_t n) {
   return w;
 }
 
-size_t clip_ws_bytes(int64_t n_rows, int32_t n_cands) {
-  return align256((size_t)clip_blocks(n_rows) * n_cands * sizeof(double));
+size_t clip_ws_bytes(int64_t n_rows, int32_t Hkv, int32_t n_cands) {
+  // enough partials for either block schedule (shared or per-head rotation)
+  const int nb = std::max(clip_blocks(n_rows, Hkv, 0), clip_blocks(n_rows, Hkv, 1));
+  return align256((size_t)nb * n_cands * sizeof(double));
 }
 
 bool cands_shape_ok(int32_t n_cands) { return n_cands >= 1 && n_cands <= OSCAR_CALIB_MAX_CANDS; }
@@ -571,36 +580,55 @@ bool cands_shape_ok(int32_t n_cands) { return n_cands >= 1 && n_cands <= OSCAR_C
 struct LayerWs {
   size_t c_off, calib_off, rot_off, lam_off, u_off, clip_off, err_off, info_off, total;
 };
-LayerWs layer_ws(int64_t T, int32_t Hq, int32_t Hkv, int32_t n_cands) {
+// nm = 2 (C_Q, C_S) shared, or 2 Hkv with one rotation per KV head.
+LayerWs layer_ws(int64_t T, int32_t Hq, int32_t Hkv, int32_t n_cands, int32_t nm) {
   LayerWs w;
   w.c_off = 0;
-  w.calib_off = align256(2 * (size_t)kD * kD * sizeof(double));
+  w.calib_off = align256((size_t)nm * kD * kD * sizeof(double));
   w.rot_off = align256(w.calib_off + calib_ws(T, Hq).total);
-  w.lam_off = align256(w.rot_off + rot_ws(2).total);
-  w.u_off = align256(w.lam_off + 2 * (size_t)kD * sizeof(double));
-  w.clip_off = align256(w.u_off + 2 * (size_t)kD * kD * sizeof(double));
-  w.err_off = align256(w.clip_off + clip_ws_bytes(T * Hkv, n_cands));
+  w.lam_off = align256(w.rot_off + rot_ws(nm).total);
+  w.u_off = align256(w.lam_off + (size_t)nm * kD * sizeof(double));
+  w.clip_off = align256(w.u_off + (size_t)nm * kD * kD * sizeof(double));
+  w.err_off = align256(w.clip_off + clip_ws_bytes(T * Hkv, Hkv, n_cands));
   w.info_off = align256(w.err_off + 2 * (size_t)n_cands * sizeof(double));
-  w.total = align256(w.info_off + 2 * sizeof(int));
+  w.total = align256(w.info_off + (size_t)nm * sizeof(int));
   return w;
 }
 
-int query_cov_impl(const void* q, int64_t T, int32_t Hq, double* C, char* ws, hipStream_t st) {
+// C_Q over all query heads (Hkv_mats = 1), or one per KV head over its g query
+// heads (Hkv_mats = Hkv: C + h d^2 for head h).
+int query_cov_impl(const void* q, int64_t T, int32_t Hq, int32_t Hkv, int32_t Hkv_mats,
+                   double* C, char* ws, hipStream_t st) {
   const CalibWs w = calib_ws(T, Hq);
-  return hip_status(launch_gram(q, 1, T * Hq, 1.0 / ((double)T * Hq),
-                                reinterpret_cast<float*>(ws + w.part_off), C, st));
+  const int64_t g = Hq / Hkv_mats;  // query heads per matrix
+  for (int h = 0; h < Hkv_mats; ++h) {
+    const uint16_t* x = static_cast<const uint16_t*>(q) + (size_t)h * g * kD;
+    const int rc = hip_status(launch_gram(x, 1, T * g, 1.0 / ((double)T * g),
+                                          reinterpret_cast<float*>(ws + w.part_off),
+                                          C + (size_t)h * kD * kD, st, g, (int64_t)Hq * kD));
+    if (rc) return rc;
+  }
+  (void)Hkv;
+  return OSCAR_OK;
 }
 
 int score_cov_impl(const void* q, const void* k, const void* v, int64_t T, int32_t Hq,
-                   int32_t Hkv, int32_t causal, double* C, char* ws, hipStream_t st) {
+                   int32_t Hkv, int32_t Hkv_mats, int32_t causal, double* C, char* ws,
+                   hipStream_t st) {
   const CalibWs w = calib_ws(T, Hq);
   float* O = reinterpret_cast<float*>(ws + w.o_off);
   hipError_t e = launch_calib_attn(static_cast<const uint16_t*>(q), static_cast<const uint16_t*>(k),
                                    static_cast<const uint16_t*>(v), (int)T, Hq, Hkv, causal ? 1 : 0,
                                    O, st);
   if (e != hipSuccess) return OSCAR_ERR_HIP;
-  return hip_status(launch_gram(O, 0, T * Hq, 1.0 / ((double)T * Hq),
-                                reinterpret_cast<float*>(ws + w.part_off), C, st));
+  const int64_t g = Hq / Hkv_mats;
+  for (int h = 0; h < Hkv_mats; ++h) {
+    const int rc = hip_status(launch_gram(O + (size_t)h * g * kD, 0, T * g, 1.0 / ((double)T * g),
+                                          reinterpret_cast<float*>(ws + w.part_off),
+                                          C + (size_t)h * kD * kD, st, g, (int64_t)Hq * kD));
+    if (rc) return rc;
+  }
+  return OSCAR_OK;
 }
 
 int rotation_impl(const double* C, int32_t n, double* lam, double* U, double* R64, float* R32,
@@ -636,7 +664,7 @@ int oscar_calib_query_cov(const void* q, int64_t T, int32_t Hq, int32_t Hkv, dou
   if (!q || !C || !workspace || !aligned(q, 16) || !aligned(C, 8) || !aligned(workspace, 256))
     return OSCAR_ERR_INVALID_ARG;
   if (workspace_bytes < calib_ws(T, Hq).total) return OSCAR_ERR_WORKSPACE_TOO_SMALL;
-  return query_cov_impl(q, T, Hq, C, static_cast<char*>(workspace),
+  return query_cov_impl(q, T, Hq, Hkv, 1, C, static_cast<char*>(workspace),
                         static_cast<hipStream_t>(stream));
 }
 
@@ -662,7 +690,7 @@ int oscar_calib_score_cov(const void* q, const void* k, const void* v, int64_t T
       !aligned(v, 16) || !aligned(C, 8) || !aligned(workspace, 256))
     return OSCAR_ERR_INVALID_ARG;
   if (workspace_bytes < calib_ws(T, Hq).total) return OSCAR_ERR_WORKSPACE_TOO_SMALL;
-  return score_cov_impl(q, k, v, T, Hq, Hkv, causal, C, static_cast<char*>(workspace),
+  return score_cov_impl(q, k, v, T, Hq, Hkv, 1, causal, C, static_cast<char*>(workspace),
                         static_cast<hipStream_t>(stream));
 }
 
@@ -687,7 +715,7 @@ int oscar_calib_rotation(const double* C, int32_t n_mats, double* lam, double* U
 size_t oscar_calib_clip_workspace_bytes(int64_t n_tok, int32_t Hkv, int32_t n_cands) {
   if (n_tok < 1 || Hkv < 1 || !cands_shape_ok(n_cands)) return 0;
   if (n_tok * Hkv > 0x7fffffffLL) return 0;
-  return clip_ws_bytes(n_tok * Hkv, n_cands);
+  return clip_ws_bytes(n_tok * Hkv, Hkv, n_cands);
 }
 
 int oscar_calib_clip(const oscar_layout* L, const void* x, int64_t n_tok, const float* R,
@@ -703,18 +731,22 @@ int oscar_calib_clip(const oscar_layout* L, const void* x, int64_t n_tok, const 
       !aligned(best, 4) || !aligned(workspace, 256))
     return OSCAR_ERR_INVALID_ARG;
   const int64_t rows = n_tok * L->num_kv_heads;
-  if (workspace_bytes < clip_ws_bytes(rows, n_cands)) return OSCAR_ERR_WORKSPACE_TOO_SMALL;
+  if (workspace_bytes < clip_ws_bytes(rows, L->num_kv_heads, n_cands))
+    return OSCAR_ERR_WORKSPACE_TOO_SMALL;
   return hip_status(launch_clip_errors(static_cast<const uint16_t*>(x), rows, R, cands, n_cands,
-                                       quant_fmt(L), static_cast<double*>(workspace),
-                                       clip_blocks(rows), err, best,
-                                       static_cast<hipStream_t>(stream)));
+                                       quant_fmt(L), L->num_kv_heads,
+                                       static_cast<double*>(workspace),
+                                       clip_blocks(rows, L->num_kv_heads, L->rot_per_head), err,
+                                       best, static_cast<hipStream_t>(stream)));
 }
 
-size_t oscar_calibrate_layer_workspace_bytes(int64_t T, int32_t Hq, int32_t Hkv,
+size_t oscar_calibrate_layer_workspace_bytes(const oscar_layout* L, int64_t T, int32_t Hq,
                                              int32_t n_cands) {
+  if (check_layout(L) != OSCAR_OK) return 0;
+  const int32_t Hkv = L->num_kv_heads;
   if (check_calib(T, Hq, Hkv) != OSCAR_OK || !cands_shape_ok(n_cands)) return 0;
   if (T * Hkv > 0x7fffffffLL) return 0;
-  return layer_ws(T, Hq, Hkv, n_cands).total;
+  return layer_ws(T, Hq, Hkv, n_cands, L->rot_per_head ? 2 * Hkv : 2).total;
 }
 
 int oscar_calibrate_layer(const oscar_layout* L, const void* q, const void* k, const void* v,
@@ -735,31 +767,33 @@ int oscar_calibrate_layer(const oscar_layout* L, const void* q, const void* k, c
       !aligned(R_v, 16) || !aligned(clip, 4) || !aligned(lam, 8) || !aligned(info, 4) ||
       !aligned(cands, 4) || !aligned(workspace, 256))
     return OSCAR_ERR_INVALID_ARG;
-  const LayerWs w = layer_ws(T, Hq, Hkv, n_cands);
+  const int32_t hm = L->rot_per_head ? Hkv : 1;  // matrices per tensor
+  const LayerWs w = layer_ws(T, Hq, Hkv, n_cands, 2 * hm);
   if (workspace_bytes < w.total) return OSCAR_ERR_WORKSPACE_TOO_SMALL;
   char* ws = static_cast<char*>(workspace);
   hipStream_t s = static_cast<hipStream_t>(stream);
-  double* C = reinterpret_cast<double*>(ws + w.c_off);  // [2][d][d]: C_Q, C_S
+  const size_t dd = (size_t)kD * kD;
+  double* C = reinterpret_cast<double*>(ws + w.c_off);  // [2][hm][d][d]: C_Q, C_S
   double* lm = lam ? lam : reinterpret_cast<double*>(ws + w.lam_off);
   double* U = reinterpret_cast<double*>(ws + w.u_off);
   int32_t* inf = info ? info : reinterpret_cast<int32_t*>(ws + w.info_off);
   double* err = reinterpret_cast<double*>(ws + w.err_off);
   char* cw = ws + w.calib_off;
-  if ((st = query_cov_impl(q, T, Hq, C, cw, s))) return st;
-  if ((st = score_cov_impl(q, k, v, T, Hq, Hkv, causal, C + kD * kD, cw, s))) return st;
+  if ((st = query_cov_impl(q, T, Hq, Hkv, hm, C, cw, s))) return st;
+  if ((st = score_cov_impl(q, k, v, T, Hq, Hkv, hm, causal, C + hm * dd, cw, s))) return st;
   // R_k and R_v are adjacent only through the caller's pointers: compose each
-  if ((st = rotation_impl(C, 2, lm, U, nullptr, nullptr, inf, ws + w.rot_off, s))) return st;
-  if (launch_compose(U, 1, nullptr, R_k, s) != hipSuccess) return OSCAR_ERR_HIP;
-  if (launch_compose(U + kD * kD, 1, nullptr, R_v, s) != hipSuccess) return OSCAR_ERR_HIP;
+  if ((st = rotation_impl(C, 2 * hm, lm, U, nullptr, nullptr, inf, ws + w.rot_off, s))) return st;
+  if (launch_compose(U, hm, nullptr, R_k, s) != hipSuccess) return OSCAR_ERR_HIP;
+  if (launch_compose(U + hm * dd, hm, nullptr, R_v, s) != hipSuccess) return OSCAR_ERR_HIP;
   const QuantFmt fmt = quant_fmt(L);
   const int64_t rows = T * Hkv;
-  const int nb = clip_blocks(rows);
+  const int nb = clip_blocks(rows, Hkv, L->rot_per_head);
   double* part = reinterpret_cast<double*>(ws + w.clip_off);
-  if (launch_clip_errors(static_cast<const uint16_t*>(k), rows, R_k, cands, n_cands, fmt, part, nb,
-                         err, clip, s) != hipSuccess)
+  if (launch_clip_errors(static_cast<const uint16_t*>(k), rows, R_k, cands, n_cands, fmt, Hkv, part,
+                         nb, err, clip, s) != hipSuccess)
     return OSCAR_ERR_HIP;
-  if (launch_clip_errors(static_cast<const uint16_t*>(v), rows, R_v, cands, n_cands, fmt, part, nb,
-                         err + n_cands, clip + 1, s) != hipSuccess)
+  if (launch_clip_errors(static_cast<const uint16_t*>(v), rows, R_v, cands, n_cands, fmt, Hkv, part,
+                         nb, err + n_cands, clip + 1, s) != hipSuccess)
     return OSCAR_ERR_HIP;
   return OSCAR_OK;
 }

@@ -184,7 +184,10 @@ def compare_pools(gpu_pool: np.ndarray, ora_pool: np.ndarray, case: Case, meta: 
             continue
         src = case.v if is_v else case.k
         x = W.bf16_bits_to_f32(bits(src[i, h]))
-        xt = oracle.rotate_row(x, case.Rv if is_v else case.Rk)
+        R = case.Rv if is_v else case.Rk
+        if R is not None and np.ndim(R) == 3:  # one rotation per KV head
+            R = R[h]
+        xt = oracle.rotate_row(x, R)
         if not row_near_boundary(xt, case.cfg.clip_v if is_v else case.cfg.clip_k, G=G,
                                  meta=meta, clip=clip):
             untolerated.append((slot, h, is_v, "not near a rounding boundary"))

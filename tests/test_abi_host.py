@@ -231,7 +231,10 @@ def test_quantizer_format_fields(L):
     assert ok.layout_check(ok.Layout(8, 10, clip_mode=2)) == ok.ERR_INVALID_ARG
     assert ok.layout_check(ok.Layout(8, 10, meta_dtype=-1)) == ok.ERR_INVALID_ARG
     assert _append(L, ok.Layout(8, 10, meta_dtype=7)) == ok.ERR_INVALID_ARG
-    assert ctypes.sizeof(ok.Layout) == 32
+    # one rotation per KV head: 0 or 1
+    assert ok.layout_check(ok.Layout(8, 10, rot_per_head=1)) == ok.OK
+    assert ok.layout_check(ok.Layout(8, 10, rot_per_head=2)) == ok.ERR_INVALID_ARG
+    assert ctypes.sizeof(ok.Layout) == 40      # 8 x int32 + 1 x int64, 8-byte aligned
 
 
 def test_null_rotations_pass_validation(L):
@@ -263,9 +266,14 @@ def test_calibration_sizes(L):
     assert L.oscar_calib_clip_workspace_bytes(T, Hkv, 21) > 0
     assert L.oscar_calib_clip_workspace_bytes(T, Hkv, 0) == 0
     assert L.oscar_calib_clip_workspace_bytes(T, Hkv, 33) == 0
-    lw = L.oscar_calibrate_layer_workspace_bytes(T, Hq, Hkv, 21)
+    lay = ok.Layout(num_kv_heads=Hkv, num_pages=1)
+    lw = L.oscar_calibrate_layer_workspace_bytes(ctypes.byref(lay), T, Hq, 21)
     assert lw >= ws + rot2 + 2 * 128 * 128 * 8 * 2
-    assert L.oscar_calibrate_layer_workspace_bytes(T, Hq, Hkv, 40) == 0
+    assert L.oscar_calibrate_layer_workspace_bytes(ctypes.byref(lay), T, Hq, 40) == 0
+    # one rotation per KV head: 2 Hkv matrices
+    lph = ok.Layout(num_kv_heads=Hkv, num_pages=1, rot_per_head=1)
+    lw_ph = L.oscar_calibrate_layer_workspace_bytes(ctypes.byref(lph), T, Hq, 21)
+    assert lw_ph >= ws + L.oscar_calib_rotation_workspace_bytes(2 * Hkv)
 
 
 def test_calibration_rejects_invalid_arguments(L):
@@ -293,7 +301,7 @@ def test_calibration_rejects_invalid_arguments(L):
     assert L.oscar_calib_clip(ctypes.byref(lay), q, 100, None, FAKE, 21, FAKE, None, FAKE, cw - 1, None) == W
     bad = ok.Layout(num_kv_heads=2, num_pages=1, group_size=16)
     assert L.oscar_calib_clip(ctypes.byref(bad), q, 100, None, FAKE, 21, FAKE, None, FAKE, cw, None) == U
-    lw = L.oscar_calibrate_layer_workspace_bytes(100, 8, 2, 21)
+    lw = L.oscar_calibrate_layer_workspace_bytes(ctypes.byref(lay), 100, 8, 21)
     args = [q, q, q, 100, 8, 1, FAKE, 21, FAKE, FAKE, FAKE, None, None, FAKE]
     assert L.oscar_calibrate_layer(ctypes.byref(lay), *args, lw - 1, None) == W
     assert L.oscar_calibrate_layer(ctypes.byref(ok.Layout(num_kv_heads=3, num_pages=1)), *args, lw,

@@ -277,3 +277,36 @@ def test_calibrate_layer_paper_format_and_full_size_sampled():
         _check_rotation(C, rot, i)
     assert torch.equal(rot["R32"][0], cal["R_K"]) and torch.equal(rot["R32"][1], cal["R_V"])
     _layer_checks(cal, q, k, v, T, Hq, Hkv, (meta, clip, G), True, True)
+
+
+def test_calibrate_layer_one_rotation_per_kv_head():
+    """L->rot_per_head: each KV head's C_Q and C_S over its own query heads, its own
+    R_K and R_V, one clip ratio per tensor over all heads' rows."""
+    T, Hq, Hkv = 300, 8, 2
+    q, k, v = _acts(T, Hq, Hkv, 650)
+    lay = ok.Layout(num_kv_heads=Hkv, num_pages=1, rot_per_head=1)
+    cands_np = oracle.default_clip_candidates()
+    cal = ok.calibrate_layer(lay, q.cuda(), k.cuda(), v.cuda(), torch.from_numpy(cands_np).cuda())
+    torch.cuda.synchronize()
+    ora = oracle.calibrate(bits(q), bits(k), bits(v), per_head=True)
+    Rk = cal["R_K"].cpu().numpy().astype(np.float64)
+    Rv = cal["R_V"].cpu().numpy().astype(np.float64)
+    lam = cal["lam"].cpu().numpy()
+    assert Rk.shape == (Hkv, D, D) and lam.shape == (2, Hkv, D)
+    assert np.all(cal["info"].cpu().numpy() >= 1)
+    for h in range(Hkv):
+        for R in (Rk[h], Rv[h]):
+            assert np.max(np.abs(R.T @ R - np.eye(D))) <= 2e-6
+        lq = ora["lam_Q"][h]
+        assert np.max(np.abs(lam[0, h] - lq)) <= 1024 * U24 * D * lq[0]
+        ls = ora["lam_S"][h]
+        assert np.max(np.abs(lam[1, h] - ls)) <= 4e-4 * D * ls[0]
+        C = ora["C_Q"][h]
+        dg = np.diag(Rk[h].T @ C @ Rk[h])                  # Lemma 1, head by head
+        assert np.max(np.abs(dg - np.trace(C) / D)) <= 1e-5 * np.trace(C)
+    for x, R, c in ((k, cal["R_K"], cal["clip"][0]), (v, cal["R_V"], cal["clip"][1])):
+        ref = oracle.clip_errors(bits(x), R.cpu().numpy(), G=32, cands=cands_np)
+        srt = np.sort(ref)
+        log("  per-head clip %.2f (oracle on the GPU's R: %.2f)" % (float(c), cands_np[np.argmin(ref)]))
+        if srt[1] - srt[0] > 1e-9 * srt[0]:
+            assert float(c) == float(cands_np[np.argmin(ref)])

@@ -19,30 +19,40 @@ pytestmark = pytest.mark.gpu
 
 D, P = 128, 64
 
-# name -> (meta_dtype, clip_mode, rotate K, rotate V, group size).  The paper's
-# stated format: groups of 128 channels, bf16 scale/zero, per-token quantile clip.
+# name -> (meta_dtype, clip_mode, rotate K, rotate V, group size, one rotation per
+# KV head).  The paper's stated format: groups of 128 channels, bf16 scale/zero,
+# per-token quantile clip.
 VARIANTS = {
-    "bf16_meta": (1, 0, True, True, 32),
-    "token_quantile": (0, 1, True, True, 32),
-    "g64": (0, 0, True, True, 64),
-    "g128": (0, 0, True, True, 128),
-    "paper_format": (1, 1, True, True, 128),
-    "paper_format_g64": (1, 1, True, True, 64),
-    "identity_v": (0, 0, True, False, 32),
-    "identity_kv_paper_format": (1, 1, False, False, 128),
+    "bf16_meta": (1, 0, True, True, 32, 0),
+    "token_quantile": (0, 1, True, True, 32, 0),
+    "g64": (0, 0, True, True, 64, 0),
+    "g128": (0, 0, True, True, 128, 0),
+    "paper_format": (1, 1, True, True, 128, 0),
+    "paper_format_g64": (1, 1, True, True, 64, 0),
+    "identity_v": (0, 0, True, False, 32, 0),
+    "identity_kv_paper_format": (1, 1, False, False, 128, 0),
+    "per_head_r": (0, 0, True, True, 32, 1),
+    "per_head_paper_format": (1, 1, True, True, 128, 1),
+    "per_head_k_identity_v": (0, 0, True, False, 32, 1),
 }
+
+
+def per_head_rotations(cfg: W.Config):
+    """One seeded rotation per KV head for K and for V: [Hkv, d, d] each."""
+    return (np.stack([W.rotation(cfg.seed + W.S_RK + 7919 * h, cfg.d) for h in range(cfg.Hkv)]),
+            np.stack([W.rotation(cfg.seed + W.S_RV + 7919 * h, cfg.d) for h in range(cfg.Hkv)]))
 
 
 class VCase:
     def __init__(self, cfg: W.Config, variant: str):
         self.cfg = cfg
-        self.meta, self.clip, rk, rv, self.G = VARIANTS[variant]
-        Rk, Rv = W.rotations(cfg)
+        self.meta, self.clip, rk, rv, self.G, self.rph = VARIANTS[variant]
+        Rk, Rv = per_head_rotations(cfg) if self.rph else W.rotations(cfg)
         self.Rk = Rk if rk else None
         self.Rv = Rv if rv else None
         self.table, self.num_pages = W.block_table(cfg)
         self.lay = ok.Layout(num_kv_heads=cfg.Hkv, num_pages=self.num_pages, group_size=self.G,
-                             clip_mode=self.clip, meta_dtype=self.meta)
+                             clip_mode=self.clip, meta_dtype=self.meta, rot_per_head=self.rph)
         self.kv = [W.cache_kv(cfg, b) for b in range(cfg.B)]
         self.q = W.queries(cfg)
         self.Rk_d = None if self.Rk is None else torch.from_numpy(self.Rk).cuda()
@@ -122,7 +132,8 @@ def test_variant_append_and_decode_small(variant):
 
 
 @pytest.mark.parametrize("variant", ["token_quantile", "g64", "paper_format",
-                                     "identity_kv_paper_format"])
+                                     "identity_kv_paper_format", "per_head_r",
+                                     "per_head_paper_format"])
 def test_variant_bulk_append_qwen3_4b_shape(variant):
     """8192 tokens x 8 KV heads: the bulk cache update (two rows per wave, the
     quantile searched per wave half)."""
@@ -137,7 +148,8 @@ def test_variant_bulk_append_qwen3_4b_shape(variant):
     assert err <= DECODE_TOL
 
 
-@pytest.mark.parametrize("variant", ["paper_format", "g64", "identity_v"])
+@pytest.mark.parametrize("variant", ["paper_format", "g64", "identity_v", "per_head_r",
+                                     "per_head_k_identity_v"])
 def test_variant_decode_step(variant):
     """oscar_decode_step (cache update of the newest token + decode) in the variant
     format equals the oracle's append of every token + decode."""
@@ -162,15 +174,16 @@ def test_variant_decode_step(variant):
     assert err <= DECODE_TOL
 
 
-def test_variant_mixed_cache_paper_format():
+@pytest.mark.parametrize("variant", ["paper_format", "per_head_paper_format"])
+def test_variant_mixed_cache_paper_format(variant):
     """The mixed-precision cache in the paper's format: bf16 sink 64 and window 256
     around an INT2 history with 128-channel groups, bf16 metadata and the
-    per-token quantile clip;
+    per-token quantile clip (and with one rotation per KV head);
     prompt by oscar_mixed_append, newest token by oscar_decode_step_mixed (with
     demotion), against the oracle's one-token-per-step loop."""
     S0, W_ = 64, 256
     vc = VCase(W.custom("var_mixed", 4, 8, 2, [30, 320, 321, 900], seed_index=245,
-                        k_outliers=(5, 90), v_outliers=(17,)), "paper_format")
+                        k_outliers=(5, 90), v_outliers=(17,)), variant)
     cfg = vc.cfg
     lens = cfg.lens
     pool = ok.alloc_pool(vc.lay)
