@@ -21,8 +21,8 @@ workload.  `bf16_baseline` is the bf16 paged-decode kernel on the same
 sequences.  `mixed_cache_step` is oscar_decode_step_mixed on the same sequences
 with a bf16 sink of 64 and a bf16 window of 256 tokens around the INT2 history.
 `variants` times the same step with the cache in other quantizer formats: the
-paper's stated one (128-channel groups, bf16 scale/zero, per-token quantile clip)
-and identity R_V.  `prefill_128k_tokens` times one 131072-token prompt written
+paper's stated one (128-channel groups, bf16 scale/zero, per-token quantile clip),
+identity R_V, and one rotation per KV head.  `prefill_128k_tokens` times one 131072-token prompt written
 by oscar_mixed_append.  `calibration` times the offline calibration of one layer
 (oscar_calibrate_layer on 8878 synthetic calibration tokens) and its stages.
 """
@@ -440,19 +440,26 @@ def main():
         del pool  # the INT2 pool of the main step is no longer needed
         torch.cuda.empty_cache()
         res["variants"] = {}
-        for vname, (clip_mode, meta, use_rv, G) in {
-                "paper_format": (ok.CLIP_TOKEN_QUANTILE, ok.META_BF16, True, 128),
-                "identity_v": (ok.CLIP_GROUP_ABSMAX, ok.META_F16, False, 32)}.items():
+        # per-head rotations: one seeded matrix per KV head for K and V
+        Rk_ph = torch.from_numpy(np.stack([W.rotation(cfg.seed + W.S_RK + 7919 * h)
+                                           for h in range(Hkv)])).to(dev)
+        Rv_ph = torch.from_numpy(np.stack([W.rotation(cfg.seed + W.S_RV + 7919 * h)
+                                           for h in range(Hkv)])).to(dev)
+        for vname, (clip_mode, meta, use_rv, G, rph) in {
+                "paper_format": (ok.CLIP_TOKEN_QUANTILE, ok.META_BF16, True, 128, 0),
+                "identity_v": (ok.CLIP_GROUP_ABSMAX, ok.META_F16, False, 32, 0),
+                "per_head_r": (ok.CLIP_GROUP_ABSMAX, ok.META_F16, True, 32, 1)}.items():
             vlay = ok.Layout(num_kv_heads=Hkv, num_pages=num_pages, group_size=G,
-                             clip_mode=clip_mode, meta_dtype=meta)
-            vRv = Rv if use_rv else None
+                             clip_mode=clip_mode, meta_dtype=meta, rot_per_head=rph)
+            vRk = Rk_ph if rph else Rk
+            vRv = (Rv_ph if rph else Rv) if use_rv else None
             vpool = ok.alloc_pool(vlay)
             t0 = time.time()
             for b in range(B):
                 k, v = W.cache_kv(cfg, b, device=dev)
                 n = int(lens[b])
                 slots = torch.from_numpy(W.slots_for(table, b, np.arange(n - 1))).to(dev)
-                ok.kv_append(vlay, vpool, k[:n - 1], v[:n - 1], slots, Rk, vRv, cfg.clip_k,
+                ok.kv_append(vlay, vpool, k[:n - 1], v[:n - 1], slots, vRk, vRv, cfg.clip_k,
                              cfg.clip_v)
                 del k, v
             torch.cuda.synchronize()
@@ -460,7 +467,7 @@ def main():
 
             def step_v():
                 ok.decode_step(vlay, vpool, new_k, new_v, new_slots_t, cfg.clip_k, cfg.clip_v, q,
-                               bt, sl, Rk, vRv, cfg.sm_scale, S, ws, out)
+                               bt, sl, vRk, vRv, cfg.sm_scale, S, ws, out)
 
             for _ in range(args.warmup):
                 step_v()
@@ -475,10 +482,12 @@ def main():
             tok_b = 64 + 2 * (d // G) * 4
             vbytes = (step_bytes - kv_bytes + int(lens.sum()) * Hkv * tok_b
                       - B * Hkv * (INT2_BYTES_PER_TOKEN_HEAD - tok_b)
-                      - (0 if use_rv else 2 * d * d * 4))
+                      - (0 if use_rv else 2 * d * d * 4)
+                      + (2 * (Hkv - 1) * 2 * d * d * 4 if rph else 0))  # R_k, R_v read per head
             res["variants"][vname] = {
                 "clip_mode": "token_quantile" if clip_mode else "group_absmax",
                 "meta_dtype": "bf16" if meta else "f16", "R_v": "given" if use_rv else "identity",
+                "rotation_per_kv_head": bool(rph),
                 "group_size": G, "bytes_per_token_head": tok_b, "step_bytes": vbytes,
                 "us_per_step": round(v_wall_us, 2), "us_per_step_events": round(v_ev_us, 2),
                 "GBps": round(vbytes / (v_wall_us * 1e-6) / 1e9, 1),
@@ -524,7 +533,7 @@ def main():
                          clip_mode=ok.CLIP_TOKEN_QUANTILE, meta_dtype=ok.META_BF16)
         cands = torch.tensor([round(0.80 + 0.01 * n, 2) for n in range(21)],
                              dtype=torch.float32, device=dev)
-        cws = torch.empty(ok.calibrate_layer_workspace_bytes(Tc, Hq, Hkv, cands.numel()),
+        cws = torch.empty(ok.calibrate_layer_workspace_bytes(clay, Tc, Hq, cands.numel()),
                           dtype=torch.uint8, device=dev)
         cal = ok.calibrate_layer(clay, cq, ck, cv, cands, workspace=cws)
         torch.cuda.synchronize()
