@@ -148,8 +148,10 @@ __global__ __launch_bounds__(256) void gram_reduce_kernel(const float* __restric
 
 // ---------------------------------------------------------------------------
 // Calibration attention, O = softmax_row(Q K^T / sqrt(d) + M) V, M causal or 0.
-// A block of 8 waves covers one KV head's key/value tiles for hc of its query
-// heads and 32 * 8 / hc queries; wave w takes head (w % hc) and 32 queries.
+// A block of kCalibAttnWaves (8) waves covers one KV head's key/value tiles for hc
+// of its query heads and 32 * 8 / hc queries; wave w takes head (w % hc) and 32
+// queries (blocks of 4 waves, two per CU, measured 1.34x slower: each K/V tile then
+// serves half as many waves).
 // Per 64-key tile the wave computes S^T = K Q^T (v_mfma_f32_32x32x16_bf16,
 // A = K rows from LDS, B = the wave's queries held in registers), so that a lane
 // owns one query and 32 of the tile's keys: the row maximum is a lane maximum and
@@ -163,7 +165,7 @@ __global__ __launch_bounds__(256) void gram_reduce_kernel(const float* __restric
 // exceeds it by more than 8, the result being the same up to rounding; O^T is kept
 // in the accumulators and normalized at the end.
 // ---------------------------------------------------------------------------
-constexpr int kAttnWaves = 8;
+constexpr int kAttnWaves = kCalibAttnWaves;
 constexpr int kKPitch = kD + 8;  // bf16: 272-byte K rows (conflict-free 16-byte reads)
 constexpr int kVPitch = 64 + 4;  // bf16: 136-byte V^T rows (conflict-free 8-byte reads)
 
@@ -198,20 +200,29 @@ __global__ __launch_bounds__(kAttnWaves * 64) void attn_kernel(
   f32x16 o[4] = {};
   float m = -INFINITY, lsum = 0.0f;
 
-  // tile staging: K as two 16-byte pieces per thread; V as keys (2 kp, 2 kp + 1),
-  // dims 8 dq .. 8 dq + 7 per thread, written transposed (key pairs per dword)
-  const int kp = tid & 31, dq = tid >> 5;
-  uint4 kr[2], vr[2];
+  // tile staging: K as 16-byte pieces (64 rows x 16) spread over the threads; V as
+  // items (key pair kp: keys 2 kp, 2 kp + 1; dims 8 dq .. 8 dq + 7), written
+  // transposed (key pairs per dword)
+  constexpr int kNT = kAttnWaves * 64;
+  constexpr int kKPer = 1024 / kNT, kVPer = 512 / kNT;
+  uint4 kr[kKPer], vr[kVPer][2];
   auto load_tile = [&](int kt) {
 #pragma unroll
-    for (int i = 0; i < 2; ++i) {
-      const int idx = tid + 512 * i, row = idx >> 4, c8 = idx & 15;
+    for (int i = 0; i < kKPer; ++i) {
+      const int idx = tid + kNT * i, row = idx >> 4, c8 = idx & 15;
       const int key = 64 * kt + row;
       kr[i] = key < T ? *reinterpret_cast<const uint4*>(k + ((size_t)key * Hkv + kvh) * kD + c8 * 8)
                       : make_uint4(0, 0, 0, 0);
-      const int vkey = 64 * kt + 2 * kp + i;
-      vr[i] = vkey < T ? *reinterpret_cast<const uint4*>(v + ((size_t)vkey * Hkv + kvh) * kD + dq * 8)
-                       : make_uint4(0, 0, 0, 0);
+    }
+#pragma unroll
+    for (int j = 0; j < kVPer; ++j) {
+      const int item = tid + kNT * j, kp = item & 31, dq = item >> 5;
+#pragma unroll
+      for (int e = 0; e < 2; ++e) {
+        const int vkey = 64 * kt + 2 * kp + e;
+        vr[j][e] = vkey < T ? *reinterpret_cast<const uint4*>(v + ((size_t)vkey * Hkv + kvh) * kD + dq * 8)
+                            : make_uint4(0, 0, 0, 0);
+      }
     }
   };
   load_tile(0);
@@ -219,13 +230,15 @@ __global__ __launch_bounds__(kAttnWaves * 64) void attn_kernel(
   for (int kt = 0; kt < n_kt; ++kt) {
     __syncthreads();
 #pragma unroll
-    for (int i = 0; i < 2; ++i) {
-      const int idx = tid + 512 * i, row = idx >> 4, c8 = idx & 15;
+    for (int i = 0; i < kKPer; ++i) {
+      const int idx = tid + kNT * i, row = idx >> 4, c8 = idx & 15;
       *reinterpret_cast<uint4*>(Ks + row * kKPitch + c8 * 8) = kr[i];
     }
-    {
-      const uint32_t a[4] = {vr[0].x, vr[0].y, vr[0].z, vr[0].w};
-      const uint32_t b[4] = {vr[1].x, vr[1].y, vr[1].z, vr[1].w};
+#pragma unroll
+    for (int j = 0; j < kVPer; ++j) {
+      const int item = tid + kNT * j, kp = item & 31, dq = item >> 5;
+      const uint32_t a[4] = {vr[j][0].x, vr[j][0].y, vr[j][0].z, vr[j][0].w};
+      const uint32_t b[4] = {vr[j][1].x, vr[j][1].y, vr[j][1].z, vr[j][1].w};
 #pragma unroll
       for (int c = 0; c < 8; ++c) {
         const uint32_t word = __builtin_amdgcn_perm(b[c >> 1], a[c >> 1], (c & 1) ? 0x07060302u : 0x05040100u);

@@ -142,6 +142,9 @@ hipError_t launch_bf16_split(const uint16_t* pages, int Hkv, int B, int Hq,
                              float* part_o, float* part_ml, hipStream_t st);
 
 // Offline calibration.
+// Waves per block of the calibration attention kernel (32 queries each); a block
+// covers 32 * kCalibAttnWaves / hc queries of hc query heads.
+constexpr int kCalibAttnWaves = 8;
 // Second moment C = (X^T X) * inv_n of rows X [n_rows][128] (bf16 or fp32), fp64
 // [128][128]; partial: gram_partial_bytes(n_rows) bytes of scratch.
 size_t gram_partial_bytes(int64_t n_rows);

@@ -539,7 +539,7 @@ int check_calib(int64_t T, int32_t Hq, int32_t Hkv) {
   if (T < 1 || Hkv < 1 || Hq < Hkv || Hq % Hkv != 0) return OSCAR_ERR_INVALID_ARG;
   const int64_t g = Hq / Hkv;
   const int64_t hc = g % 4 == 0 ? 4 : g % 2 == 0 ? 2 : 1;
-  const int64_t span = 32 * 8 / hc;
+  const int64_t span = 32 * kCalibAttnWaves / hc;
   if ((T + span - 1) / span > 65535 || Hq / hc > 65535) return OSCAR_ERR_UNSUPPORTED;
   return OSCAR_OK;
 }
