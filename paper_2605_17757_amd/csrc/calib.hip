@@ -151,7 +151,9 @@ __global__ __launch_bounds__(256) void gram_reduce_kernel(const float* __restric
 // A block of kCalibAttnWaves (8) waves covers one KV head's key/value tiles for hc
 // of its query heads and 32 * 8 / hc queries; wave w takes head (w % hc) and 32
 // queries (blocks of 4 waves, two per CU, measured 1.34x slower: each K/V tile then
-// serves half as many waves).
+// serves half as many waves; a double-buffered version that issues the next tile's
+// score MFMAs before the current tile's softmax needs more than 256 registers per
+// lane and spills: 1.16x slower).
 // Per 64-key tile the wave computes S^T = K Q^T (v_mfma_f32_32x32x16_bf16,
 // A = K rows from LDS, B = the wave's queries held in registers), so that a lane
 // owns one query and 32 of the tile's keys: the row maximum is a lane maximum and
@@ -249,6 +251,9 @@ __global__ __launch_bounds__(kAttnWaves * 64) void attn_kernel(
     if (kt + 1 < n_kt) load_tile(kt + 1);
     if (!active || kt >= wave_kt) continue;
 
+    // issue priority: high while a wave feeds the matrix cores, low in its softmax,
+    // so that a SIMD's other wave fills the gaps
+    __builtin_amdgcn_s_setprio(1);
     // S^T: lane holds query qrow, keys 64 kt + 32 kk + 8 (r / 4) + 4 h + r % 4
     // the two 32-key halves as two interleaved MFMA chains; each step's K pieces
     // are read from LDS one step ahead
@@ -276,6 +281,7 @@ __global__ __launch_bounds__(kAttnWaves * 64) void attn_kernel(
       if (ks < 6) __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);
     }
     __builtin_amdgcn_sched_group_barrier(0x008, 2, 0);
+    __builtin_amdgcn_s_setprio(0);
     const bool edge = (causal && 64 * kt + 63 > qw0) || 64 * kt + 64 > T;
     float mt = -INFINITY;
     if (edge) {  // keys >= limit are masked
@@ -305,6 +311,7 @@ __global__ __launch_bounds__(kAttnWaves * 64) void attn_kernel(
 #pragma unroll
         for (int r = 0; r < 16; ++r) o[dt][r] *= alpha;
     }
+    __builtin_amdgcn_s_setprio(1);
     float tsum = 0.0f;  // the tile's probabilities, added to the running sum once
     // V^T pieces for step (kk, u): dims 32 dt + l % 32, keys 32 kk + 16 u + 4 h + 0..3
     // and + 8; read one step ahead
@@ -350,6 +357,7 @@ __global__ __launch_bounds__(kAttnWaves * 64) void attn_kernel(
         for (int dt = 0; dt < 4; ++dt) vcur[dt] = vnext[dt];
       }
     lsum += tsum;
+    __builtin_amdgcn_s_setprio(0);
   }
 
   if (!active || qrow >= T) return;
