@@ -377,7 +377,8 @@ __global__ __launch_bounds__(kAttnWaves * 64) void attn_kernel(
 
 // ---------------------------------------------------------------------------
 // Symmetric eigen-decomposition by cyclic Jacobi (round-robin ordering), fp64.
-// One block of 16 waves per matrix keeps the upper triangle in LDS (66 KB).  A sweep is 127
+// One block of 16 waves per matrix keeps the whole matrix in LDS (130 KB, both
+// triangles: plain row-major addressing for the block updates).  A sweep is 127
 // rounds of 64 disjoint pairs (p, q) (circle method: in round r the pairs are
 // (127, r) and ((r + k) mod 127, (r - k) mod 127), k = 1..63), so every
 // off-diagonal entry is visited once per sweep.  For each pair the rotation
@@ -391,14 +392,10 @@ __global__ __launch_bounds__(kAttnWaves * 64) void attn_kernel(
 // ---------------------------------------------------------------------------
 constexpr int kJacRounds = kD - 1;
 constexpr int kJacPairs = kD / 2;
-constexpr int kJacPacked = kD * (kD + 1) / 2;
+constexpr int kJacPitch = kD + 2;  // doubles: rows of the LDS copy, 8 bytes of padding
 constexpr int kJacBlocks = kJacPairs * (kJacPairs + 1) / 2;  // 2x2 blocks with k1 <= k2
 constexpr double kJacTol = 1e-15;
 
-__device__ inline int upk(int i, int j) {  // i <= j
-  return i * kD - (i * (i - 1)) / 2 + (j - i);
-}
-__device__ inline double& sym(double* A, int i, int j) { return i <= j ? A[upk(i, j)] : A[upk(j, i)]; }
 __device__ inline void round_pair(int r, int kk, int& p, int& q) {
   int a, b;
   if (kk == 0) {
@@ -420,7 +417,7 @@ __global__ __launch_bounds__(kJacThreads) void jacobi_kernel(const double* __res
                                                      double2* __restrict__ rot,
                                                      int* __restrict__ n_rounds,
                                                      int* __restrict__ info) {
-  __shared__ double A[kJacPacked];
+  __shared__ double A[kD * kJacPitch];  // both triangles (130 KB)
   __shared__ double2 cs[kJacPairs];
   __shared__ int pp[kJacPairs], qq[kJacPairs];
   __shared__ int rotated;
@@ -428,7 +425,7 @@ __global__ __launch_bounds__(kJacThreads) void jacobi_kernel(const double* __res
   const double* Cm = C + (size_t)mtx * kD * kD;
   for (int e = tid; e < kD * kD; e += kJacThreads) {
     const int i = e >> 7, j = e & (kD - 1);
-    if (i <= j) A[upk(i, j)] = Cm[e];
+    A[i * kJacPitch + j] = Cm[e];
   }
   // this thread's 2x2 blocks (k1 <= k2), fixed for every round
   int bk1[kJacPerThread], bk2[kJacPerThread];
@@ -453,7 +450,8 @@ __global__ __launch_bounds__(kJacThreads) void jacobi_kernel(const double* __res
       if (tid < kJacPairs) {
         int p, q;
         round_pair(r, tid, p, q);
-        const double app = A[upk(p, p)], aqq = A[upk(q, q)], apq = A[upk(p, q)];
+        const double app = A[p * kJacPitch + p], aqq = A[q * kJacPitch + q];
+        const double apq = A[p * kJacPitch + q];
         double c = 1.0, s = 0.0;
         if (apq != 0.0 && fabs(apq) > kJacTol * sqrt(fabs(app * aqq))) {
           const double tau = (aqq - app) / (2.0 * apq);
@@ -476,25 +474,31 @@ __global__ __launch_bounds__(kJacThreads) void jacobi_kernel(const double* __res
         if (c1.y == 0.0 && c2.y == 0.0) continue;
         const int p1 = pp[k1], q1 = qq[k1], p2 = pp[k2], q2 = qq[k2];
         if (k1 == k2) {
-          const double app = A[upk(p1, p1)], aqq = A[upk(q1, q1)], apq = A[upk(p1, q1)];
+          const double app = A[p1 * kJacPitch + p1], aqq = A[q1 * kJacPitch + q1];
+          const double apq = A[p1 * kJacPitch + q1];
           const double c = c1.x, s = c1.y;
           // J^T M J with M symmetric; the off-diagonal entry is zero by construction
           const double t00 = c * app - s * apq, t01 = c * apq - s * aqq;
           const double t10 = s * app + c * apq, t11 = s * apq + c * aqq;
-          A[upk(p1, p1)] = t00 * c - t01 * s;
-          A[upk(q1, q1)] = t10 * s + t11 * c;
-          A[upk(p1, q1)] = 0.0;
-        } else {
-          double& m00 = sym(A, p1, p2);
-          double& m01 = sym(A, p1, q2);
-          double& m10 = sym(A, q1, p2);
-          double& m11 = sym(A, q1, q2);
+          A[p1 * kJacPitch + p1] = t00 * c - t01 * s;
+          A[q1 * kJacPitch + q1] = t10 * s + t11 * c;
+          A[p1 * kJacPitch + q1] = 0.0;
+          A[q1 * kJacPitch + p1] = 0.0;
+        } else {  // rows (p1, q1) x columns (p2, q2), mirrored to the transposed block
+          const double m00 = A[p1 * kJacPitch + p2], m01 = A[p1 * kJacPitch + q2];
+          const double m10 = A[q1 * kJacPitch + p2], m11 = A[q1 * kJacPitch + q2];
           const double t00 = c1.x * m00 - c1.y * m10, t01 = c1.x * m01 - c1.y * m11;
           const double t10 = c1.y * m00 + c1.x * m10, t11 = c1.y * m01 + c1.x * m11;
-          m00 = t00 * c2.x - t01 * c2.y;
-          m01 = t00 * c2.y + t01 * c2.x;
-          m10 = t10 * c2.x - t11 * c2.y;
-          m11 = t10 * c2.y + t11 * c2.x;
+          const double n00 = t00 * c2.x - t01 * c2.y, n01 = t00 * c2.y + t01 * c2.x;
+          const double n10 = t10 * c2.x - t11 * c2.y, n11 = t10 * c2.y + t11 * c2.x;
+          A[p1 * kJacPitch + p2] = n00;
+          A[p1 * kJacPitch + q2] = n01;
+          A[q1 * kJacPitch + p2] = n10;
+          A[q1 * kJacPitch + q2] = n11;
+          A[p2 * kJacPitch + p1] = n00;
+          A[q2 * kJacPitch + p1] = n01;
+          A[p2 * kJacPitch + q1] = n10;
+          A[q2 * kJacPitch + q1] = n11;
         }
       }
     }
@@ -506,7 +510,7 @@ __global__ __launch_bounds__(kJacThreads) void jacobi_kernel(const double* __res
     sweeps = sw + 1;
   }
   __syncthreads();
-  for (int i = tid; i < kD; i += kJacThreads) diag[(size_t)mtx * kD + i] = A[upk(i, i)];
+  for (int i = tid; i < kD; i += kJacThreads) diag[(size_t)mtx * kD + i] = A[i * kJacPitch + i];
   if (tid == 0) {
     n_rounds[mtx] = sweeps * kJacRounds;
     info[mtx] = converged ? sweeps + 1 : -1;
