@@ -163,6 +163,11 @@ __device__ inline float quad_max(float x) {
   x = fmaxf(x, __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(x), 0x4E, 0xF, 0xF, false)));
   return x;
 }
+__device__ inline float quad_sum(float x) {
+  x += __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(x), 0xB1, 0xF, 0xF, false));
+  x += __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(x), 0x4E, 0xF, 0xF, false));
+  return x;
+}
 // Reductions over lanes l, l^16, l^32, l^48 with the gfx950 row-swap permutes:
 // swapping a value with itself across the wave halves / odd-even rows leaves
 // x[l] and x[l^32] (then x[l^16]) in the two outputs.
@@ -324,61 +329,97 @@ __device__ inline void compute_page(WaveState& st, WaveLds& L, int t0, int t1, i
   // ---- P.V weights w = p * s_v of (head lo>>2, group lo&3), tokens 16*hi + e ----
   const int wh = lo >> 2, wg = lo & 3;
   const float2 hsw = L.hs[wh];
-  float4 pw[4];
-  uint4 vz[4];
-#pragma unroll
-  for (int j = 0; j < 4; ++j) {
-    pw[j] = L.p[wh][4 * hi + j];
-    vz[j] = *reinterpret_cast<const uint4*>(pb + kLdsVSz + 272 * wg + 64 * hi + 16 * j);
-  }
-  uint32_t sz[16];
-#pragma unroll
-  for (int e = 0; e < 16; ++e) {
-    sz[e] = comp(vz[e >> 2], e & 3);
-    if (!FULL && (16 * hi + e < t0 || 16 * hi + e >= t1)) sz[e] = 0u;  // (0, 0): w = 0, z = 0
-    if (NG < 4 && wg >= NG) sz[e] = 0u;  // no such group: lanes idle
-  }
-  // largest V scale of the group on this page: scales are positive binary16 or
-  // bfloat16, so their bit patterns order like their values (high halves, the
-  // zero points, ignored)
-  uint32_t m5[6];
-#pragma unroll
-  for (int e = 0; e < 5; ++e) m5[e] = max3_lo16(sz[3 * e], sz[3 * e + 1], sz[3 * e + 2]);
-  m5[5] = sz[15];
-  const uint32_t smax = max3_lo16(max3_lo16(m5[0], m5[1], m5[2]), max3_lo16(m5[3], m5[4], m5[5]), 0u);
-  const float svmax = rows_max(BF ? __uint_as_float(smax << 16) : h_lo(smax));
-  const float sig = hsw.y * svmax;  // >= every w of the row on this page
-  const float inv = sig > 0.0f ? kWMax * __builtin_amdgcn_rcpf(sig) : 0.0f;
-  L.ws[lo] = sig * (1.0f / kWMax);
   float zp = 0.0f;
-  uint32_t aw[kNDig][4];
+  if (NG == 1) {
+    // one group per head: lane (head wh, quarter wg) forms the weights of tokens
+    // 16*hi + 4*wg + (0..3), dword wg of the head's k-group hi operand (every lane
+    // busy, a quarter of the work per lane of the per-group layout)
+    const float4 pw = L.p[wh][4 * hi + wg];
+    const uint4 vz = *reinterpret_cast<const uint4*>(pb + kLdsVSz + 64 * hi + 16 * wg);
+    uint32_t sz[4];
 #pragma unroll
-  for (int j = 0; j < 4; ++j) {
+    for (int b = 0; b < 4; ++b) {
+      const int tok = 16 * hi + 4 * wg + b;
+      sz[b] = comp(vz, b);
+      if (!FULL && (tok < t0 || tok >= t1)) sz[b] = 0u;  // (0, 0): w = 0, z = 0
+    }
+    // largest V scale of the head on this page (bit patterns of positive scales)
+    const uint32_t smax = max3_lo16(max3_lo16(sz[0], sz[1], sz[2]), sz[3], 0u);
+    const float svmax = rows_max(quad_max(BF ? __uint_as_float(smax << 16) : h_lo(smax)));
+    const float sig = hsw.y * svmax;
+    const float inv = sig > 0.0f ? kWMax * __builtin_amdgcn_rcpf(sig) : 0.0f;
+    L.ws[lo] = sig * (1.0f / kWMax);  // equal for the 16 lanes of head wh
     uint32_t f[4];
 #pragma unroll
     for (int b = 0; b < 4; ++b) {
-      const int e = 4 * j + b;
-      const float w = sz_s_fma<BF>(sz[e], compf(pw[j], b), 0.0f);
-      // mantissa of rne(w * inv) + 2^23 + 32896 = k + 32896, k in [0, 2^21]:
-      // k = 65536 d_0 + 256 d_1 + d_2 with d_2, d_1 = (bytes 0, 1) ^ 0x80, d_0 = byte 2
+      const float w = sz_s_fma<BF>(sz[b], compf(pw, b), 0.0f);
       f[b] = __float_as_uint(fmaf(w, inv, kMagic + kDigitBias));
-      zp = sz_z_fma<BF>(sz[e], w, zp);  // unquantized w: differs from the quantized by <= 2^-22 sig
+      zp = sz_z_fma<BF>(sz[b], w, zp);
     }
-    const uint32_t t01 = __builtin_amdgcn_perm(f[1], f[0], 0x05010400u) ^ 0x80808080u;  // [f0.0 f1.0 f0.1 f1.1]
+    const uint32_t t01 = __builtin_amdgcn_perm(f[1], f[0], 0x05010400u) ^ 0x80808080u;
     const uint32_t t23 = __builtin_amdgcn_perm(f[3], f[2], 0x05010400u) ^ 0x80808080u;
-    const uint32_t h01 = __builtin_amdgcn_perm(f[1], f[0], 0x0c0c0602u);                // [f0.2 f1.2 0 0]
+    const uint32_t h01 = __builtin_amdgcn_perm(f[1], f[0], 0x0c0c0602u);
     const uint32_t h23 = __builtin_amdgcn_perm(f[3], f[2], 0x0c0c0602u);
-    aw[2][j] = __builtin_amdgcn_perm(t23, t01, 0x05040100u);
-    aw[1][j] = __builtin_amdgcn_perm(t23, t01, 0x07060302u);
-    aw[0][j] = __builtin_amdgcn_perm(h23, h01, 0x05040100u);
+    char* wp = pb + 16 * (w_base(0) + w_slot(wh, hi)) + 4 * wg;
+    *reinterpret_cast<uint32_t*>(wp) = __builtin_amdgcn_perm(h23, h01, 0x05040100u);       // digit 0
+    *reinterpret_cast<uint32_t*>(wp + 16) = __builtin_amdgcn_perm(t23, t01, 0x07060302u);  // digit 1
+    *reinterpret_cast<uint32_t*>(wp + 32) = __builtin_amdgcn_perm(t23, t01, 0x05040100u);  // digit 2
+  } else {
+    float4 pw[4];
+    uint4 vz[4];
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      pw[j] = L.p[wh][4 * hi + j];
+      vz[j] = *reinterpret_cast<const uint4*>(pb + kLdsVSz + 272 * wg + 64 * hi + 16 * j);
+    }
+    uint32_t sz[16];
+#pragma unroll
+    for (int e = 0; e < 16; ++e) {
+      sz[e] = comp(vz[e >> 2], e & 3);
+      if (!FULL && (16 * hi + e < t0 || 16 * hi + e >= t1)) sz[e] = 0u;  // (0, 0): w = 0, z = 0
+      if (NG < 4 && wg >= NG) sz[e] = 0u;  // no such group: lanes idle
+    }
+    // largest V scale of the group on this page: scales are positive binary16 or
+    // bfloat16, so their bit patterns order like their values (high halves, the
+    // zero points, ignored)
+    uint32_t m5[6];
+#pragma unroll
+    for (int e = 0; e < 5; ++e) m5[e] = max3_lo16(sz[3 * e], sz[3 * e + 1], sz[3 * e + 2]);
+    m5[5] = sz[15];
+    const uint32_t smax = max3_lo16(max3_lo16(m5[0], m5[1], m5[2]), max3_lo16(m5[3], m5[4], m5[5]), 0u);
+    const float svmax = rows_max(BF ? __uint_as_float(smax << 16) : h_lo(smax));
+    const float sig = hsw.y * svmax;  // >= every w of the row on this page
+    const float inv = sig > 0.0f ? kWMax * __builtin_amdgcn_rcpf(sig) : 0.0f;
+    L.ws[lo] = sig * (1.0f / kWMax);
+    uint32_t aw[kNDig][4];
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      uint32_t f[4];
+#pragma unroll
+      for (int b = 0; b < 4; ++b) {
+        const int e = 4 * j + b;
+        const float w = sz_s_fma<BF>(sz[e], compf(pw[j], b), 0.0f);
+        // mantissa of rne(w * inv) + 2^23 + 32896 = k + 32896, k in [0, 2^21]:
+        // k = 65536 d_0 + 256 d_1 + d_2 with d_2, d_1 = (bytes 0, 1) ^ 0x80, d_0 = byte 2
+        f[b] = __float_as_uint(fmaf(w, inv, kMagic + kDigitBias));
+        zp = sz_z_fma<BF>(sz[e], w, zp);  // unquantized w: differs from the quantized by <= 2^-22 sig
+      }
+      const uint32_t t01 = __builtin_amdgcn_perm(f[1], f[0], 0x05010400u) ^ 0x80808080u;  // [f0.0 f1.0 f0.1 f1.1]
+      const uint32_t t23 = __builtin_amdgcn_perm(f[3], f[2], 0x05010400u) ^ 0x80808080u;
+      const uint32_t h01 = __builtin_amdgcn_perm(f[1], f[0], 0x0c0c0602u);                // [f0.2 f1.2 0 0]
+      const uint32_t h23 = __builtin_amdgcn_perm(f[3], f[2], 0x0c0c0602u);
+      aw[2][j] = __builtin_amdgcn_perm(t23, t01, 0x05040100u);
+      aw[1][j] = __builtin_amdgcn_perm(t23, t01, 0x07060302u);
+      aw[0][j] = __builtin_amdgcn_perm(h23, h01, 0x05040100u);
+    }
+    if (NG == 4 || wg < NG) {  // digit operands to LDS: group wg, rows 3*wh + digit, k-group hi
+      char* wp = pb + 16 * (w_base(wg) + w_slot(wh, hi));
+#pragma unroll
+      for (int dg = 0; dg < kNDig; ++dg)
+        *reinterpret_cast<uint4*>(wp + 16 * dg) = make_uint4(aw[dg][0], aw[dg][1], aw[dg][2], aw[dg][3]);
+    }
   }
   st.zacc = fmaf(st.zacc, hsw.x, zp);
-  if (NG == 4 || wg < NG) {  // digit operands to LDS: group wg, rows 3*wh + digit, k-group hi
-    char* wp = pb + 16 * (w_base(wg) + w_slot(wh, hi));
-#pragma unroll
-    for (int dg = 0; dg < kNDig; ++dg)
-      *reinterpret_cast<uint4*>(wp + 16 * dg) = make_uint4(aw[dg][0], aw[dg][1], aw[dg][2], aw[dg][3]);
-  }
 
   // ---- P.V on the matrix cores: lane (channel column, head hi) ----
   const float4 ws = *reinterpret_cast<const float4*>(&L.ws[4 * hi]);
@@ -565,7 +606,8 @@ __device__ __attribute__((always_inline)) inline void process_piece(WaveLds& L, 
 
   // ---- write the split's partial state ----
   const float ltot = row16_sum(st.lsum);  // head hi
-  const float ztot = rows_sum(st.zacc);   // (head lo>>2, group lo&3)
+  float ztot = rows_sum(st.zacc);         // (head lo>>2, group lo&3)
+  if (NG == 1) ztot = quad_sum(ztot);     // the head's quarters: its one group
   L.ws[lo] = ztot;                        // lanes of equal lo write equal values
   const float4 zh = *reinterpret_cast<const float4*>(&L.ws[4 * hi]);
   const int hout = 4 * chunk + hi;        // head of this lane's accumulators
