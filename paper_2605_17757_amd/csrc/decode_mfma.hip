@@ -310,8 +310,9 @@ __device__ inline void compute_page(WaveState& st, WaveLds& L, int t0, int t1, i
     if (valid(u)) mx = fmaxf(mx, S[u]);
   mx = row16_max(mx) * st.sq;  // sq > 0; at least one valid token per page
   const float mn = fmaxf(st.m, mx);
-  // the running maxima of the wave's heads change on few pages: when none does,
-  // alpha = 1 and the rescaling below is skipped (same results)
+  // alpha rescales the head's running sums (1 on the pages where the maximum
+  // stays, which is most of them; the multiplies are kept, as a wave-uniform skip
+  // would save about 1 % of the page's VALU)
   const float alpha = ex2(st.m - mn);  // m = -inf on the first page -> 0
   const float pmax = ex2(mx - mn);
   float p[4];
