@@ -94,6 +94,9 @@ __device__ inline v4i mfma32(long a, long b) {
   const v4i z = {0, 0, 0, 0};
   return __builtin_amdgcn_mfma_i32_16x16x32_i8(a, b, z, 0, 0, 0);
 }
+__device__ inline v4i mfma32acc(long a, long b, v4i c) {
+  return __builtin_amdgcn_mfma_i32_16x16x32_i8(a, b, c, 0, 0, 0);
+}
 
 // raw v_exp_f32 (results below 2^-126 flush to 0: negligible softmax weights)
 __device__ inline float ex2(float x) { return __builtin_amdgcn_exp2f(x); }
@@ -273,31 +276,36 @@ __device__ inline void compute_page(WaveState& st, WaveLds& L, int t0, int t1, i
 #pragma unroll
   for (int u = 0; u < 4; ++u) {
     float acc = 0.0f;
-    int tg[4];
+    v4i dg[NG];  // NG < 4: the digit sums of a group's slices accumulate in one MFMA chain
 #pragma unroll
     for (int g = 0; g < 4; ++g) {
       const uint32_t y = kc[8 * u + 2 * g] >> sh4;  // fields 2(hi&1), 2(hi&1)+1 of each byte
       const uint32_t msk = 0x03030303u;
       const long b = (long)((uint64_t)(y & msk) | ((uint64_t)((y >> 2) & msk) << 32));
-      const v4i d = mfma32(st.aq[g], b);
-      const int t = combine3(d[0], d[1], d[2]);
       if (NG == 4) {
+        const v4i d = mfma32(st.aq[g], b);
+        const int t = combine3(d[0], d[1], d[2]);
         const uint32_t sz = comp(ksz[g], u);
         // s * (acc - z * sum q_int) with s, z read from the packed pair
         acc = sz_s_fma<BF>(sz, sz_nz_fma<BF>(sz, st.qs[g], (float)t), acc);
       } else {
-        tg[g] = t;
+        const int j = g * NG / 4;  // the slice's group
+        if (g % (4 / NG) == 0) dg[j] = mfma32(st.aq[g], b);
+        else dg[j] = mfma32acc(st.aq[g], b, dg[j]);
       }
     }
-    if (NG == 2) {  // slices of a group added in int32 (|sum| < 2^31)
+    if (NG == 2) {  // 64 channels: |digit sums| <= 64 * 128 * 3, the combined sum < 2^31
 #pragma unroll
       for (int j = 0; j < 2; ++j) {
         const uint32_t sz = comp(ksz[j], u);
-        acc = sz_s_fma<BF>(sz, sz_nz_fma<BF>(sz, st.qs[j], (float)(tg[2 * j] + tg[2 * j + 1])), acc);
+        const int t = combine3(dg[j][0], dg[j][1], dg[j][2]);
+        acc = sz_s_fma<BF>(sz, sz_nz_fma<BF>(sz, st.qs[j], (float)t), acc);
       }
-    } else if (NG == 1) {  // four slices: two int32 pair sums, added in fp32
+    } else if (NG == 1) {
+      // 128 channels: the combined sum can exceed int32, so the digits are combined
+      // in fp32: 256 d_1 + d_2 is exact (< 2^24), and one rounding adds 65536 d_0
       const uint32_t sz = comp(ksz[0], u);
-      const float T = (float)(tg[0] + tg[1]) + (float)(tg[2] + tg[3]);
+      const float T = fmaf((float)dg[0][0], 65536.0f, fmaf((float)dg[0][1], 256.0f, (float)dg[0][2]));
       acc = sz_s_fma<BF>(sz, sz_nz_fma<BF>(sz, st.qs[0], T), 0.0f);
     }
     S[u] = acc;
