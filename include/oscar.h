@@ -24,9 +24,17 @@
  *     launch); asynchronous faults surface at the caller's next synchronization.
  *   - Host arguments are validated before anything is launched; on any error
  *     nothing is launched and no memory is touched.  Device-resident indices
- *     (slot_mapping, block_table, seq_lens) are not validated: they must lie in
- *     range (slot < num_pages*page_size, 0 <= page id < num_pages,
- *     1 <= seq_lens[b] <= max_pages_per_seq*page_size).
+ *     (slot_mapping, block_table, seq_lens, seq_idx) are not validated by
+ *     default: they must lie in range (slot < num_pages*page_size, 0 <= page id
+ *     < num_pages, 1 <= seq_lens[b] <= max_pages_per_seq*page_size, 0 <=
+ *     seq_idx < B).  With the environment variable OSCAR_DEBUG set (and not
+ *     "0", read at every call) the entry points that take them synchronize the
+ *     stream, copy them to host memory and check them first: seq_lens[b] in
+ *     [0, max_pages_per_seq*page_size], the block-table entries of the pages a
+ *     sequence uses in [0, num_pages), slots below num_pages*page_size
+ *     (negative slots are skipped by the cache update), seq_idx in [0, B); an
+ *     index out of range returns OSCAR_ERR_INVALID_ARG with nothing launched,
+ *     a failed copy OSCAR_ERR_HIP.
  *   - Inputs must be finite.  Scales and zeros that fall outside the range of
  *     their storage format are saturated to its largest finite value (+-65504
  *     for binary16).

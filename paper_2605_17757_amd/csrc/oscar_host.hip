@@ -1,9 +1,12 @@
 // liboscar C ABI: argument validation, workspace carving and kernel launches.
 // Every entry point validates all host arguments before launching anything.
 #include <math.h>
+#include <stdlib.h>
+#include <string.h>
 
 #include <algorithm>
 #include <atomic>
+#include <vector>
 
 #include "../../include/oscar.h"
 #include "internal.h"
@@ -53,6 +56,67 @@ int check_layout(const oscar_layout* L) {
 bool clip_ok(float c) { return isfinite(c) && c > 0.0f && c <= 1.0f; }
 
 int hip_status(hipError_t e) { return e == hipSuccess ? OSCAR_OK : OSCAR_ERR_HIP; }
+
+// ---------------------------------------------------------------------------
+// OSCAR_DEBUG (environment variable, read at every call; set and not "0"): the
+// entry points that take device-resident indices synchronize the stream, copy
+// the indices to host memory and check them before launching anything:
+//   seq_lens[b] in [0, max_pages_per_seq * page_size], the block-table entries
+//   of the pages a sequence uses (ceil(seq_lens[b] / page_size)) in
+//   [0, num_pages), slots below num_pages * page_size (negative slots are
+//   skipped by the cache update), seq_idx in [0, B).
+// An index out of range returns OSCAR_ERR_INVALID_ARG with nothing launched; a
+// failed copy (e.g. a host pointer) returns OSCAR_ERR_HIP.
+// ---------------------------------------------------------------------------
+bool debug_on() {
+  const char* e = getenv("OSCAR_DEBUG");
+  return e && e[0] && strcmp(e, "0") != 0;
+}
+
+template <class T>
+int copy_to_host(std::vector<T>& h, const T* d, int64_t n) {
+  h.resize((size_t)n);
+  if (n == 0) return OSCAR_OK;
+  return hip_status(hipMemcpy(h.data(), d, (size_t)n * sizeof(T), hipMemcpyDeviceToHost));
+}
+
+// Any of the index arrays may be null (not part of the call).
+int debug_check(const oscar_layout* L, void* stream, int32_t B, const int32_t* block_table,
+                int32_t max_pages_per_seq, const int32_t* seq_lens, const int64_t* slots,
+                int64_t n_slots, const int32_t* seq_idx, int64_t n_idx) {
+  if (!debug_on()) return OSCAR_OK;
+  int st = hip_status(hipStreamSynchronize(static_cast<hipStream_t>(stream)));
+  if (st) return st;
+  const int64_t P = L->page_size;
+  if (seq_lens) {
+    std::vector<int32_t> lens, bt;
+    if ((st = copy_to_host(lens, seq_lens, B))) return st;
+    if (block_table && (st = copy_to_host(bt, block_table, (int64_t)B * max_pages_per_seq)))
+      return st;
+    for (int32_t b = 0; b < B; ++b) {
+      const int64_t len = lens[(size_t)b];
+      if (len < 0 || len > (int64_t)max_pages_per_seq * P) return OSCAR_ERR_INVALID_ARG;
+      if (!block_table) continue;
+      for (int64_t i = 0; i < (len + P - 1) / P; ++i) {
+        const int32_t pg = bt[(size_t)b * max_pages_per_seq + (size_t)i];
+        if (pg < 0 || pg >= L->num_pages) return OSCAR_ERR_INVALID_ARG;
+      }
+    }
+  }
+  if (slots) {
+    std::vector<int64_t> sl;
+    if ((st = copy_to_host(sl, slots, n_slots))) return st;
+    for (int64_t s : sl)
+      if (s >= L->num_pages * P) return OSCAR_ERR_INVALID_ARG;
+  }
+  if (seq_idx) {
+    std::vector<int32_t> si;
+    if ((st = copy_to_host(si, seq_idx, n_idx))) return st;
+    for (int32_t x : si)
+      if (x < 0 || x >= B) return OSCAR_ERR_INVALID_ARG;
+  }
+  return OSCAR_OK;
+}
 
 int check_decode_common(const oscar_layout* L, int32_t B, int32_t Hq, int32_t num_splits) {
   int st = check_layout(L);
@@ -160,6 +224,8 @@ int oscar_kv_append(const oscar_layout* L, void* pages, const void* k_new, const
       !aligned(pages, 16) || !aligned(slot_mapping, 8))
     return OSCAR_ERR_INVALID_ARG;
   if ((int64_t)n_tok * L->num_kv_heads > 0x7fffffffLL) return OSCAR_ERR_UNSUPPORTED;
+  st = debug_check(L, stream, 0, nullptr, 0, nullptr, slot_mapping, n_tok, nullptr, 0);
+  if (st) return st;
   return hip_status(launch_append(pages, L->num_kv_heads, static_cast<const uint16_t*>(k_new),
                                   static_cast<const uint16_t*>(v_new), slot_mapping, n_tok, R_k,
                                   R_v, clip_k, clip_v, quant_fmt(L),
@@ -193,6 +259,8 @@ int oscar_decode_split(const oscar_layout* L, const void* pages, int32_t B, int3
   if (!aligned(workspace, 256) || !aligned(pages, 16)) return OSCAR_ERR_INVALID_ARG;
   const DecodeWs ws = decode_ws(B, Hq, num_splits);
   if (workspace_bytes < ws.total) return OSCAR_ERR_WORKSPACE_TOO_SMALL;
+  st = debug_check(L, stream, B, block_table, max_pages_per_seq, seq_lens, nullptr, 0, nullptr, 0);
+  if (st) return st;
   uint8_t* base = static_cast<uint8_t*>(workspace);
   return hip_status(launch_decode_split(
       static_cast<const uint8_t*>(pages), L->num_kv_heads, B, Hq, block_table, max_pages_per_seq,
@@ -242,6 +310,8 @@ int oscar_decode_attn(const oscar_layout* L, const void* pages, const void* q, i
       !aligned(out, out_dtype == OSCAR_OUT_F32 ? 4 : 2))
     return OSCAR_ERR_INVALID_ARG;
   if (workspace_bytes < decode_ws(B, Hq, num_splits).total) return OSCAR_ERR_WORKSPACE_TOO_SMALL;
+  st = debug_check(L, stream, B, block_table, max_pages_per_seq, seq_lens, nullptr, 0, nullptr, 0);
+  if (st) return st;
   st = oscar_decode_prepare(L, q, B, Hq, R_k, sm_scale, num_splits, workspace, workspace_bytes,
                             stream);
   if (st) return st;
@@ -285,6 +355,9 @@ int oscar_decode_step(const oscar_layout* L, void* pages, const void* k_new, con
     return OSCAR_ERR_INVALID_ARG;
   const DecodeWs ws = decode_ws(B, Hq, num_splits);
   if (workspace_bytes < ws.total) return OSCAR_ERR_WORKSPACE_TOO_SMALL;
+  st = debug_check(L, stream, B, block_table, max_pages_per_seq, seq_lens,
+                   n_new > 0 ? slot_mapping : nullptr, n_new, nullptr, 0);
+  if (st) return st;
   hipStream_t hs = static_cast<hipStream_t>(stream);
   uint8_t* base = static_cast<uint8_t*>(workspace);
   float* qt = reinterpret_cast<float*>(base + ws.qt_off);
@@ -342,6 +415,9 @@ int oscar_mixed_append(const oscar_layout* L, void* pages, void* seg, int32_t B,
   if ((int64_t)n_tok * L->num_kv_heads > 0x7fffffffLL ||
       (int64_t)max_pages_per_seq * L->page_size > 0x7fffffffLL)
     return OSCAR_ERR_UNSUPPORTED;
+  st = debug_check(L, stream, B, block_table, max_pages_per_seq, seq_lens, nullptr, 0, seq_idx,
+                   n_tok);
+  if (st) return st;
   return hip_status(launch_mixed_append(
       pages, static_cast<uint16_t*>(seg), L->num_kv_heads, S0, W, static_cast<const uint16_t*>(k),
       static_cast<const uint16_t*>(v), seq_idx, pos, n_tok, seq_lens, block_table,
@@ -419,6 +495,8 @@ int oscar_decode_attn_mixed(const oscar_layout* L, const void* pages, const void
                               seq_lens, R_k, R_v, sm_scale, &num_splits, workspace,
                               workspace_bytes, out, out_dtype);
   if (st) return st;
+  st = debug_check(L, stream, B, block_table, max_pages_per_seq, seq_lens, nullptr, 0, nullptr, 0);
+  if (st) return st;
   hipStream_t hs = static_cast<hipStream_t>(stream);
   const DecodeWs ws = decode_ws(B, Hq, (int64_t)num_splits + 1);
   float* qt = reinterpret_cast<float*>(static_cast<uint8_t*>(workspace) + ws.qt_off);
@@ -441,6 +519,8 @@ int oscar_decode_step_mixed(const oscar_layout* L, void* pages, void* seg, int32
   int st = check_mixed_decode(L, pages, seg, S0, W, q, B, Hq, block_table, max_pages_per_seq,
                               seq_lens, R_k, R_v, sm_scale, &num_splits, workspace,
                               workspace_bytes, out, out_dtype);
+  if (st) return st;
+  st = debug_check(L, stream, B, block_table, max_pages_per_seq, seq_lens, nullptr, 0, nullptr, 0);
   if (st) return st;
   if (!k_new || !v_new || !clip_ok(clip_k) || !clip_ok(clip_v)) return OSCAR_ERR_INVALID_ARG;
   if (!aligned(k_new, 4) || !aligned(v_new, 4)) return OSCAR_ERR_INVALID_ARG;
@@ -476,6 +556,8 @@ int oscar_bf16_kv_append(const oscar_layout* L, void* pages, const void* k_new,
   if (n_tok == 0) return OSCAR_OK;
   if (!pages || !k_new || !v_new || !slot_mapping) return OSCAR_ERR_INVALID_ARG;
   if (!aligned(pages, 16) || !aligned(k_new, 4) || !aligned(v_new, 4)) return OSCAR_ERR_INVALID_ARG;
+  st = debug_check(L, stream, 0, nullptr, 0, nullptr, slot_mapping, n_tok, nullptr, 0);
+  if (st) return st;
   return hip_status(launch_bf16_append(pages, L->num_kv_heads,
                                        static_cast<const uint16_t*>(k_new),
                                        static_cast<const uint16_t*>(v_new), slot_mapping, n_tok,
@@ -508,6 +590,8 @@ int oscar_bf16_decode_attn(const oscar_layout* L, const void* pages, const void*
     return OSCAR_ERR_INVALID_ARG;
   const DecodeWs ws = decode_ws(B, Hq, num_splits);
   if (workspace_bytes < ws.total) return OSCAR_ERR_WORKSPACE_TOO_SMALL;
+  st = debug_check(L, stream, B, block_table, max_pages_per_seq, seq_lens, nullptr, 0, nullptr, 0);
+  if (st) return st;
   uint8_t* base = static_cast<uint8_t*>(workspace);
   float* qt = reinterpret_cast<float*>(base + ws.qt_off);
   float* po = reinterpret_cast<float*>(base + ws.po_off);
