@@ -594,7 +594,29 @@ def main():
     e1.record(stream)
     torch.cuda.synchronize()
     res["copy_probe_GBps"] = round(2 * src.numel() * 10 / (e0.elapsed_time(e1) * 1e-3) / 1e9, 1)
-    del src, dst
+    del dst
+    # ---- plain streaming read of 2 GiB (the reference for the split kernel's reads) ----
+    src = torch.empty(2 << 30, dtype=torch.uint8, device=dev)
+    src.fill_(1)
+    cus = torch.cuda.get_device_properties(0).multi_processor_count
+    rp = {}
+    for mult in (4, 8, 16, 32):
+        nb = mult * cus
+        sink = torch.empty(nb * 256, dtype=torch.int32, device=dev)
+        for _ in range(2):
+            ok.hbm_read_probe(src, nb, sink)
+        ts = []
+        for _ in range(10):
+            a, z = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            a.record(stream)
+            ok.hbm_read_probe(src, nb, sink)
+            z.record(stream)
+            z.synchronize()
+            ts.append(a.elapsed_time(z))
+        rp["%d_blocks" % nb] = round(src.numel() / (sorted(ts)[5] * 1e-3) / 1e9, 1)
+    res["read_probe_GBps"] = rp
+    res["read_probe_best_GBps"] = max(rp.values())
+    del src, sink
 
     # ---- CPU oracle baseline on a bounded sample ----
     if not args.no_cpu_baseline:

@@ -449,6 +449,22 @@ int oscar_calibrate_layer(const oscar_layout *L, const void *q, const void *k, c
                           int32_t *info, void *workspace, size_t workspace_bytes,
                           void *stream);
 
+/* ------------------------------------------------------------------------- */
+/* Measurement helper (not part of the method)                                */
+/* ------------------------------------------------------------------------- */
+
+/*
+ * oscar_hbm_read_probe -- a plain streaming read of `bytes` bytes at src (device,
+ * 16-byte aligned, bytes a multiple of 16) by `blocks` blocks of 256 threads,
+ * each thread reading 16-byte words grid-stride and writing the xor of its words
+ * to sink[thread] (device, uint32 [blocks * 256], caller-owned).  The xor of all
+ * sink words is the xor of all source words.  Its rate is the reference for the
+ * decode kernel's HBM read rate.  Asynchronous on `stream`; invalid arguments
+ * return OSCAR_ERR_INVALID_ARG with nothing launched.
+ */
+int oscar_hbm_read_probe(const void *src, size_t bytes, uint32_t *sink, int32_t blocks,
+                         void *stream);
+
 #ifdef __cplusplus
 }
 #endif

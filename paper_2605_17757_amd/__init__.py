@@ -36,6 +36,7 @@ EXPORTS = (
     "oscar_calib_score_cov", "oscar_calib_rotation_workspace_bytes", "oscar_calib_rotation",
     "oscar_calib_clip_workspace_bytes", "oscar_calib_clip",
     "oscar_calibrate_layer_workspace_bytes", "oscar_calibrate_layer",
+    "oscar_hbm_read_probe",
 )
 
 CALIB_MAX_CANDS = 32
@@ -123,6 +124,7 @@ def lib() -> ctypes.CDLL:
             "oscar_calibrate_layer_workspace_bytes": (sz, [LP, i64, i32, i32]),
             "oscar_calibrate_layer": (ctypes.c_int, [LP, P, P, P, i64, i32, i32, P, i32, P, P, P,
                                                      P, P, P, sz, P]),
+            "oscar_hbm_read_probe": (ctypes.c_int, [P, sz, P, i32, P]),
         }
         for name, (res, args) in sigs.items():
             fn = getattr(L, name)
@@ -573,3 +575,22 @@ def calibrate_layer(layout: Layout, q, k, v, cands, causal: bool = True, workspa
                                        _ptr(ws, torch.uint8, "ws"), ws.numel(), _stream(stream)),
            "oscar_calibrate_layer")
     return {"R_K": Rk, "R_V": Rv, "clip": clip, "lam": lam, "info": info}
+
+
+# ---------------------------------------------------------------------------
+# measurement helper
+# ---------------------------------------------------------------------------
+
+def hbm_read_probe(src, blocks: int, sink=None, stream=None) -> torch.Tensor:
+    """Plain streaming read of the bytes of ``src`` (a contiguous GPU tensor, size a
+    multiple of 16 bytes) by ``blocks`` blocks of 256 threads; returns the uint32
+    sink [blocks * 256] whose xor is the xor of the source words."""
+    if not isinstance(src, torch.Tensor) or not src.is_cuda or not src.is_contiguous():
+        raise ValueError("src must be a contiguous GPU tensor")
+    nbytes = src.numel() * src.element_size()
+    if sink is None:
+        sink = torch.empty(int(blocks) * 256, dtype=torch.int32, device=src.device)
+    _check(lib().oscar_hbm_read_probe(ctypes.c_void_p(src.data_ptr()), nbytes,
+                                      _ptr(sink, torch.int32, "sink", int(blocks) * 256),
+                                      int(blocks), _stream(stream)), "oscar_hbm_read_probe")
+    return sink

@@ -33,6 +33,7 @@ SOURCES = {
     "bf16_decode.hip": [],
     "mixed.hip": [],
     "calib.hip": ["-ffp-contract=off"],
+    "probe.hip": [],
 }
 
 

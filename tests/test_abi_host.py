@@ -309,3 +309,15 @@ def test_calibration_rejects_invalid_arguments(L):
     args2 = list(args)
     args2[9] = None  # R_v
     assert L.oscar_calibrate_layer(ctypes.byref(lay), *args2, lw, None) == E
+
+
+def test_read_probe_rejects_invalid_arguments(L):
+    # every case returns before any HIP call (no device needed)
+    buf = ctypes.c_void_p(1 << 20)  # 16-byte aligned, never dereferenced
+    sink = ctypes.c_void_p(1 << 21)
+    assert L.oscar_hbm_read_probe(None, 16, sink, 1, None) == ok.ERR_INVALID_ARG
+    assert L.oscar_hbm_read_probe(buf, 16, None, 1, None) == ok.ERR_INVALID_ARG
+    assert L.oscar_hbm_read_probe(buf, 16, sink, 0, None) == ok.ERR_INVALID_ARG
+    assert L.oscar_hbm_read_probe(buf, 0, sink, 1, None) == ok.ERR_INVALID_ARG
+    assert L.oscar_hbm_read_probe(buf, 24, sink, 1, None) == ok.ERR_INVALID_ARG      # not x16
+    assert L.oscar_hbm_read_probe(ctypes.c_void_p((1 << 20) + 8), 16, sink, 1, None) == ok.ERR_INVALID_ARG
