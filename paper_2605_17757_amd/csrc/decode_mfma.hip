@@ -373,6 +373,58 @@ __device__ inline void compute_page(WaveState& st, WaveLds& L, int t0, int t1, i
     *reinterpret_cast<uint32_t*>(wp) = __builtin_amdgcn_perm(h23, h01, 0x05040100u);       // digit 0
     *reinterpret_cast<uint32_t*>(wp + 16) = __builtin_amdgcn_perm(t23, t01, 0x07060302u);  // digit 1
     *reinterpret_cast<uint32_t*>(wp + 32) = __builtin_amdgcn_perm(t23, t01, 0x05040100u);  // digit 2
+  } else if (NG == 2) {
+    // two groups per head: lane (head wh, group wg & 1, half wg >> 1) forms the
+    // weights of tokens 16*hi + 8*(wg >> 1) + (0..7) of its group, dwords
+    // 2*(wg >> 1) + (0, 1) of the group's k-group hi operand
+    const int gq = wg & 1, hf = wg >> 1;
+    float4 pw[2];
+    uint4 vz[2];
+#pragma unroll
+    for (int j = 0; j < 2; ++j) {
+      pw[j] = L.p[wh][4 * hi + 2 * hf + j];
+      vz[j] = *reinterpret_cast<const uint4*>(pb + kLdsVSz + 272 * gq + 64 * hi + 16 * (2 * hf + j));
+    }
+    uint32_t sz[8];
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      const int tok = 16 * hi + 8 * hf + e;
+      sz[e] = comp(vz[e >> 2], e & 3);
+      if (!FULL && (tok < t0 || tok >= t1)) sz[e] = 0u;  // (0, 0): w = 0, z = 0
+    }
+    // largest V scale of the group on this page: this lane's 8 tokens, the other
+    // half's lane (wg ^ 2) and the k-groups hi
+    const uint32_t smax = max3_lo16(max3_lo16(sz[0], sz[1], sz[2]), max3_lo16(sz[3], sz[4], sz[5]),
+                                    max3_lo16(sz[6], sz[7], 0u));
+    float sv = BF ? __uint_as_float(smax << 16) : h_lo(smax);
+    sv = fmaxf(sv, __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(sv), 0x4E, 0xF, 0xF, false)));
+    const float svmax = rows_max(sv);
+    const float sig = hsw.y * svmax;
+    const float inv = sig > 0.0f ? kWMax * __builtin_amdgcn_rcpf(sig) : 0.0f;
+    L.ws[lo] = sig * (1.0f / kWMax);  // lanes wg and wg ^ 2: group wg & 1 of head wh
+    uint32_t aw[kNDig][2];
+#pragma unroll
+    for (int j = 0; j < 2; ++j) {
+      uint32_t f[4];
+#pragma unroll
+      for (int b = 0; b < 4; ++b) {
+        const int e = 4 * j + b;
+        const float w = sz_s_fma<BF>(sz[e], compf(pw[j], b), 0.0f);
+        f[b] = __float_as_uint(fmaf(w, inv, kMagic + kDigitBias));
+        zp = sz_z_fma<BF>(sz[e], w, zp);
+      }
+      const uint32_t t01 = __builtin_amdgcn_perm(f[1], f[0], 0x05010400u) ^ 0x80808080u;
+      const uint32_t t23 = __builtin_amdgcn_perm(f[3], f[2], 0x05010400u) ^ 0x80808080u;
+      const uint32_t h01 = __builtin_amdgcn_perm(f[1], f[0], 0x0c0c0602u);
+      const uint32_t h23 = __builtin_amdgcn_perm(f[3], f[2], 0x0c0c0602u);
+      aw[2][j] = __builtin_amdgcn_perm(t23, t01, 0x05040100u);
+      aw[1][j] = __builtin_amdgcn_perm(t23, t01, 0x07060302u);
+      aw[0][j] = __builtin_amdgcn_perm(h23, h01, 0x05040100u);
+    }
+    char* wp = pb + 16 * (w_base(gq) + w_slot(wh, hi)) + 8 * hf;
+#pragma unroll
+    for (int dg = 0; dg < kNDig; ++dg)
+      *reinterpret_cast<uint2*>(wp + 16 * dg) = make_uint2(aw[dg][0], aw[dg][1]);
   } else {
     float4 pw[4];
     uint4 vz[4];
@@ -386,7 +438,6 @@ __device__ inline void compute_page(WaveState& st, WaveLds& L, int t0, int t1, i
     for (int e = 0; e < 16; ++e) {
       sz[e] = comp(vz[e >> 2], e & 3);
       if (!FULL && (16 * hi + e < t0 || 16 * hi + e >= t1)) sz[e] = 0u;  // (0, 0): w = 0, z = 0
-      if (NG < 4 && wg >= NG) sz[e] = 0u;  // no such group: lanes idle
     }
     // largest V scale of the group on this page: scales are positive binary16 or
     // bfloat16, so their bit patterns order like their values (high halves, the
@@ -421,7 +472,7 @@ __device__ inline void compute_page(WaveState& st, WaveLds& L, int t0, int t1, i
       aw[1][j] = __builtin_amdgcn_perm(t23, t01, 0x07060302u);
       aw[0][j] = __builtin_amdgcn_perm(h23, h01, 0x05040100u);
     }
-    if (NG == 4 || wg < NG) {  // digit operands to LDS: group wg, rows 3*wh + digit, k-group hi
+    {  // digit operands to LDS: group wg, rows 3*wh + digit, k-group hi
       char* wp = pb + 16 * (w_base(wg) + w_slot(wh, hi));
 #pragma unroll
       for (int dg = 0; dg < kNDig; ++dg)
@@ -617,6 +668,8 @@ __device__ __attribute__((always_inline)) inline void process_piece(WaveLds& L, 
   const float ltot = row16_sum(st.lsum);  // head hi
   float ztot = rows_sum(st.zacc);         // (head lo>>2, group lo&3)
   if (NG == 1) ztot = quad_sum(ztot);     // the head's quarters: its one group
+  if (NG == 2)                            // the group's halves: lanes wg and wg ^ 2
+    ztot += __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(ztot), 0x4E, 0xF, 0xF, false));
   L.ws[lo] = ztot;                        // lanes of equal lo write equal values
   const float4 zh = *reinterpret_cast<const float4*>(&L.ws[4 * hi]);
   const int hout = 4 * chunk + hi;        // head of this lane's accumulators
