@@ -66,7 +66,7 @@ def parse():
     ap.add_argument("--no-prefill", action="store_true",
                     help="skip the prefill-scale cache write (one 131072-token prompt)")
     ap.add_argument("--no-variants", action="store_true",
-                    help="skip the quantizer-variant steps (paper format, identity R_V)")
+                    help="skip the quantizer-variant steps (paper format at G = 128 and 64, identity R_V, per-head R)")
     ap.add_argument("--no-calib", action="store_true",
                     help="skip the offline calibration of one layer (8878 tokens)")
     ap.add_argument("--no-mixed", action="store_true",
@@ -447,6 +447,7 @@ def main():
                                            for h in range(Hkv)])).to(dev)
         for vname, (clip_mode, meta, use_rv, G, rph) in {
                 "paper_format": (ok.CLIP_TOKEN_QUANTILE, ok.META_BF16, True, 128, 0),
+                "paper_format_g64": (ok.CLIP_TOKEN_QUANTILE, ok.META_BF16, True, 64, 0),
                 "identity_v": (ok.CLIP_GROUP_ABSMAX, ok.META_F16, False, 32, 0),
                 "per_head_r": (ok.CLIP_GROUP_ABSMAX, ok.META_F16, True, 32, 1)}.items():
             vlay = ok.Layout(num_kv_heads=Hkv, num_pages=num_pages, group_size=G,
