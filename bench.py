@@ -21,10 +21,20 @@ workload.  `bf16_baseline` is the bf16 paged-decode kernel on the same
 sequences.  `mixed_cache_step` is oscar_decode_step_mixed on the same sequences
 with a bf16 sink of 64 and a bf16 window of 256 tokens around the INT2 history.
 `variants` times the same step with the cache in other quantizer formats: the
-paper's stated one (128-channel groups, bf16 scale/zero, per-token quantile clip),
-identity R_V, and one rotation per KV head.  `prefill_128k_tokens` times one 131072-token prompt written
-by oscar_mixed_append.  `calibration` times the offline calibration of one layer
+paper's stated one (128-channel groups, bf16 scale/zero, per-token quantile
+clip), the same at 64-channel groups, identity R_V, and one rotation per KV head.
+`prefill_128k_tokens` times one 131072-token prompt written by
+oscar_mixed_append.  `calibration` times the offline calibration of one layer
 (oscar_calibrate_layer on 8878 synthetic calibration tokens) and its stages.
+`c3_qwen3_32b_b128` and `c4_longctx_b16` time the same step on the Qwen3-32B
+shaped layer (64/8 heads, batch 128, 32768 tokens; with its bf16 baseline) and
+the long-context layer (96/8 heads, batch 16, 131072 tokens, Student-t keys,
+64 splits), each with its split kernel's roofline and the pieces per sequence
+the split produces.  `small_configs` times the cache-resident workloads (tiny
+4/1 x 256, Qwen3-4B 8192, Qwen3-8B batch 1) warm and cold (a 1 GiB buffer
+written between the calls, outside the events), with the oracle on one host
+thread and on all of them.  `read_probe_ex` is the streaming-read probe over
+access patterns (loads in flight, non-temporal loads, per-wave chunks).
 """
 from __future__ import annotations
 
@@ -71,6 +81,10 @@ def parse():
                     help="skip the offline calibration of one layer (8878 tokens)")
     ap.add_argument("--no-mixed", action="store_true",
                     help="skip the mixed-precision cache step (bf16 sink + window)")
+    ap.add_argument("--no-configs", action="store_true",
+                    help="skip the Qwen3-32B (config 3) and long-context (config 4) rows")
+    ap.add_argument("--no-small", action="store_true",
+                    help="skip the warm/cold rows of the cache-resident configs 0, 1, 2 (B=1)")
     ap.add_argument("--sink", type=int, default=64, help="mixed cache: bf16 sink tokens S0")
     ap.add_argument("--window", type=int, default=256, help="mixed cache: bf16 window tokens W")
     return ap.parse_args()
@@ -268,6 +282,7 @@ def main():
     torch.cuda.synchronize()
     split_us = e0.elapsed_time(e1) * 1e3 / args.steps
     achieved = split_bytes / (split_us * 1e-6) / 1e9
+    pieces_main = pieces_per_sequence(ws, B, Hq, S)
 
     # ---- the 64-token-per-sequence cache update (4096 tokens x 8 KV heads) ----
     # into each sequence's spare slots len_b .. len_b + 63 (never read by the
@@ -596,34 +611,348 @@ def main():
     torch.cuda.synchronize()
     res["copy_probe_GBps"] = round(2 * src.numel() * 10 / (e0.elapsed_time(e1) * 1e-3) / 1e9, 1)
     del dst
-    # ---- plain streaming read of 2 GiB (the reference for the split kernel's reads) ----
+    # ---- streaming reads of 2 GiB (the reference for the split kernel's reads):
+    # the plain probe at four grid sizes, then the access-pattern sweep ----
     src = torch.empty(2 << 30, dtype=torch.uint8, device=dev)
     src.fill_(1)
     cus = torch.cuda.get_device_properties(0).multi_processor_count
-    rp = {}
-    for mult in (4, 8, 16, 32):
-        nb = mult * cus
+
+    def probe_rate(nb, loads=None, flags=0):
         sink = torch.empty(nb * 256, dtype=torch.int32, device=dev)
         for _ in range(2):
-            ok.hbm_read_probe(src, nb, sink)
+            ok.hbm_read_probe(src, nb, sink, loads=loads, flags=flags)
         ts = []
         for _ in range(10):
             a, z = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
             a.record(stream)
-            ok.hbm_read_probe(src, nb, sink)
+            ok.hbm_read_probe(src, nb, sink, loads=loads, flags=flags)
             z.record(stream)
             z.synchronize()
             ts.append(a.elapsed_time(z))
-        rp["%d_blocks" % nb] = round(src.numel() / (sorted(ts)[5] * 1e-3) / 1e9, 1)
+        return round(src.numel() / (sorted(ts)[5] * 1e-3) / 1e9, 1)
+
+    rp = {"%d_blocks" % (m * cus): probe_rate(m * cus) for m in (4, 8, 16, 32)}
     res["read_probe_GBps"] = rp
-    res["read_probe_best_GBps"] = max(rp.values())
-    del src, sink
+    sweep = {}
+    for loads in (4, 8, 16):
+        for flags, fname in ((0, "plain"), (ok.PROBE_NONTEMPORAL, "nt"),
+                             (ok.PROBE_WAVE_CHUNKS, "chunks"),
+                             (ok.PROBE_NONTEMPORAL | ok.PROBE_WAVE_CHUNKS, "nt_chunks")):
+            for m in (8, 16, 32):
+                sweep["%s_x%d_%dpercu" % (fname, loads, m)] = probe_rate(m * cus, loads, flags)
+    best = max(sweep, key=sweep.get)
+    res["read_probe_ex"] = {"best": best, "best_GBps": sweep[best], "GBps": sweep}
+    res["read_probe_best_GBps"] = max(max(rp.values()), sweep[best])
+    res["roofline"]["frac_of_read_probe"] = round(achieved / res["read_probe_best_GBps"], 4)
+    del src
+
+    # ---- the Qwen3-32B-shaped and long-context layers, and the cache-resident
+    # workloads warm and cold ----
+    res["pieces_per_sequence"] = pieces_main
+    if not args.no_configs:
+        torch.cuda.empty_cache()
+        res["c3_qwen3_32b_b128"] = config_row(args, 3, not args.no_bf16_baseline)
+        torch.cuda.empty_cache()
+        res["c4_longctx_b16"] = config_row(args, 4, not args.no_bf16_baseline)
+        torch.cuda.empty_cache()
+    if not args.no_small:
+        res["small_configs"] = small_config_rows(args, not args.no_cpu_baseline)
+        torch.cuda.empty_cache()
 
     # ---- CPU oracle baseline on a bounded sample ----
     if not args.no_cpu_baseline:
         res["cpu_baseline"] = cpu_baseline(cfg, table, Rk_np, Rv_np, q, args.cpu_seconds)
 
     print(json.dumps(res), flush=True)
+
+
+def _a256(x: int) -> int:
+    return (x + 255) & ~255
+
+
+def pieces_per_sequence(ws, B: int, Hq: int, S: int) -> dict:
+    """Partial states the split wrote per sequence after a decode, read from the
+    workspace's (m, l) slots (q~ fp32 [B*Hq, 128], o~ fp32 [B*Hq*S, 128], (m, l)
+    fp32 [B*Hq*S, 2], 256-byte aligned regions; an unused slot holds m = -inf)."""
+    import torch
+    off = _a256(B * Hq * 128 * 4)
+    off += _a256(B * Hq * S * 128 * 4)
+    ml = ws[off:off + B * Hq * S * 8].view(torch.float32).view(B, Hq, S, 2)
+    live = (ml[..., 0] > float("-inf")).sum(-1)[:, 0].cpu().numpy()  # head 0 of each sequence
+    return {"min": int(live.min()), "mean": round(float(live.mean()), 2), "max": int(live.max()),
+            "slots": S}
+
+
+def _events(n):
+    import torch
+    return [torch.cuda.Event(enable_timing=True) for _ in range(n)]
+
+
+def _back_to_back_us(fn, n, stream):
+    """n calls of fn between two HIP events on `stream`; mean microseconds per call."""
+    import torch
+    e0, e1 = _events(2)
+    torch.cuda.synchronize()
+    e0.record(stream)
+    for _ in range(n):
+        fn()
+    e1.record(stream)
+    torch.cuda.synchronize()
+    return e0.elapsed_time(e1) * 1e3 / n
+
+
+def _build_cache(ok, W, cfg, dev, with_bf16: bool):
+    """INT2 pool with tokens 0..n-2 of every sequence (token n-1 is the step's new
+    token), the optional bf16 pool with all n tokens, and the new rows/slots."""
+    import torch
+    B, Hkv, d = cfg.B, cfg.Hkv, cfg.d
+    table, num_pages = W.block_table(cfg)
+    lay = ok.Layout(num_kv_heads=Hkv, num_pages=num_pages)
+    Rk_np, Rv_np = W.rotations(cfg)
+    Rk, Rv = torch.from_numpy(Rk_np).to(dev), torch.from_numpy(Rv_np).to(dev)
+    pool = ok.alloc_pool(lay)
+    bf_pool = (torch.zeros(ok.bf16_pool_bytes(lay) // 2, dtype=torch.bfloat16, device=dev)
+               if with_bf16 else None)
+    new_k = torch.empty(B, Hkv, d, dtype=torch.bfloat16, device=dev)
+    new_v = torch.empty_like(new_k)
+    new_slots = np.zeros(B, np.int64)
+    for b in range(B):
+        k, v = W.cache_kv(cfg, b, device=dev)
+        n = int(cfg.lens[b])
+        slots = torch.from_numpy(W.slots_for(table, b, np.arange(n))).to(dev)
+        if n > 1:
+            ok.kv_append(lay, pool, k[:n - 1], v[:n - 1], slots[:n - 1], Rk, Rv, cfg.clip_k,
+                         cfg.clip_v)
+        if bf_pool is not None:
+            ok.bf16_kv_append(lay, bf_pool, k, v, slots)
+        new_k[b] = k[n - 1]
+        new_v[b] = v[n - 1]
+        new_slots[b] = int(W.slots_for(table, b, [n - 1])[0])
+        del k, v
+    torch.cuda.synchronize()
+    return dict(table=table, lay=lay, Rk=Rk, Rv=Rv, Rk_np=Rk_np, Rv_np=Rv_np, pool=pool,
+                bf_pool=bf_pool, new_k=new_k, new_v=new_v,
+                new_slots=torch.from_numpy(new_slots).to(dev),
+                bt=torch.from_numpy(table).to(dev), sl=torch.from_numpy(cfg.lens).to(dev),
+                q=W.queries(cfg, device=dev))
+
+
+def _step_bytes(cfg):
+    """Algorithmic bytes of one decode step (split, q/out, the new tokens' update,
+    R_k and R_v) and of the split alone."""
+    lens = cfg.lens.astype(np.int64)
+    B, Hq, Hkv, d = cfg.B, cfg.Hq, cfg.Hkv, cfg.d
+    split = int(lens.sum()) * Hkv * INT2_BYTES_PER_TOKEN_HEAD + int(np.sum((lens + 63) // 64)) * 4 + B * 4
+    qo = 2 * B * Hq * d * 2
+    app = 2 * B * Hkv * d * 2 + B * Hkv * INT2_BYTES_PER_TOKEN_HEAD + B * 8 + 2 * d * d * 4
+    return split + qo + app + 2 * d * d * 4, split, qo
+
+
+def config_row(args, index: int, with_bf16: bool) -> dict:
+    """The decode step on workload `index` (3: Qwen3-32B shape, 4: long context):
+    step time, split roofline, stage breakdown, pieces per sequence, bf16 baseline."""
+    import torch
+
+    import paper_2605_17757_amd as ok
+    import workloads as W
+    dev = "cuda"
+    stream = torch.cuda.current_stream()
+    cfg = W.config(index)
+    B, Hq, Hkv, d = cfg.B, cfg.Hq, cfg.Hkv, cfg.d
+    t0 = time.time()
+    c = _build_cache(ok, W, cfg, dev, with_bf16)
+    lay = c["lay"]
+    S = args.num_splits or ok.default_num_splits(lay, B, Hq, int(c["table"].shape[1]) * 64)
+    if cfg.min_splits and S < cfg.min_splits:
+        S = cfg.min_splits
+    ws = ok.alloc_workspace(lay, B, Hq, S)
+    out = torch.empty(B, Hq, d, dtype=torch.bfloat16, device=dev)
+    print("setup %.1fs: %s B=%d Hq=%d Hkv=%d splits=%d" % (time.time() - t0, cfg.name, B, Hq, Hkv,
+                                                          S), file=sys.stderr, flush=True)
+
+    def step():
+        ok.decode_step(lay, c["pool"], c["new_k"], c["new_v"], c["new_slots"], cfg.clip_k,
+                       cfg.clip_v, c["q"], c["bt"], c["sl"], c["Rk"], c["Rv"], cfg.sm_scale, S,
+                       ws, out)
+
+    for _ in range(args.warmup):
+        step()
+    t_settle = time.perf_counter()
+    while (time.perf_counter() - t_settle) * 1e3 < args.settle_ms:
+        for _ in range(10):
+            step()
+        torch.cuda.synchronize()
+    torch.cuda.synchronize()
+    w0 = time.perf_counter()
+    for _ in range(args.steps):
+        step()
+    torch.cuda.synchronize()
+    us = (time.perf_counter() - w0) / args.steps * 1e6
+    step_b, split_b, qo_b = _step_bytes(cfg)
+    # stage breakdown (events between the decode stages)
+    ev = [_events(4) for _ in range(args.steps)]
+    for i in range(args.steps):
+        ev[i][0].record(stream)
+        ok.decode_prepare(lay, c["q"], c["Rk"], cfg.sm_scale, S, ws)
+        ev[i][1].record(stream)
+        ok.decode_split(lay, c["pool"], B, Hq, c["bt"], c["sl"], S, ws)
+        ev[i][2].record(stream)
+        ok.decode_reduce(lay, B, Hq, c["Rv"], S, ws, out)
+        ev[i][3].record(stream)
+    torch.cuda.synchronize()
+    seg = np.array([[ev[i][j].elapsed_time(ev[i][j + 1]) for j in range(3)]
+                    for i in range(args.steps)]) * 1e3
+    split_us = _back_to_back_us(lambda: ok.decode_split(lay, c["pool"], B, Hq, c["bt"], c["sl"],
+                                                        S, ws), args.steps, stream)
+    ach = split_b / (split_us * 1e-6) / 1e9
+    row = {
+        "workload": cfg.name, "batch": B, "q_heads": Hq, "kv_heads": Hkv,
+        "seq_len": int(cfg.lens.max()), "k_dist": cfg.k_dist, "num_splits": S,
+        "us_per_step": round(us, 2), "GBps": round(step_b / (us * 1e-6) / 1e9, 1),
+        "frac_of_peak": round(step_b / (us * 1e-6) / 1e9 / HBM_PEAK_GBS, 4),
+        "tokens_per_s": round(B / (us * 1e-6), 1),
+        "stages_us": {"decode_prepare": round(float(np.mean(seg[:, 0])), 2),
+                      "decode_split": round(float(np.mean(seg[:, 1])), 2),
+                      "decode_reduce": round(float(np.mean(seg[:, 2])), 2)},
+        "roofline": {"kernel": "decode_split", "bound": "hbm", "achieved": round(ach, 1),
+                     "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                     "frac": round(ach / HBM_PEAK_GBS, 4), "us": round(split_us, 2),
+                     "bytes_per_launch": split_b},
+        "pieces_per_sequence": pieces_per_sequence(ws, B, Hq, S),
+        "bytes": {"step_total": step_b, "int2_kv": int(cfg.lens.astype(np.int64).sum()) * Hkv *
+                  INT2_BYTES_PER_TOKEN_HEAD,
+                  "bf16_kv_equivalent": int(cfg.lens.astype(np.int64).sum()) * Hkv *
+                  BF16_BYTES_PER_TOKEN_HEAD},
+    }
+    if c["bf_pool"] is not None:
+        bws = torch.empty(ok.decode_workspace_bytes(lay, B, Hq, S), dtype=torch.uint8,
+                          device=dev)
+        bout = torch.empty_like(out)
+
+        def bf16():
+            ok.bf16_decode_attn(lay, c["bf_pool"], c["q"], c["bt"], c["sl"], cfg.sm_scale, S,
+                                bws, bout)
+
+        for _ in range(3):
+            bf16()
+        bus = _back_to_back_us(bf16, max(5, args.steps // 4), stream)
+        bbytes = row["bytes"]["bf16_kv_equivalent"] + split_b - row["bytes"]["int2_kv"] + qo_b
+        int2_us = float(np.mean(seg.sum(axis=1)))
+        row["bf16_baseline"] = {
+            "us_per_decode": round(bus, 2), "GBps": round(bbytes / (bus * 1e-6) / 1e9, 1),
+            "frac_of_peak": round(bbytes / (bus * 1e-6) / 1e9 / HBM_PEAK_GBS, 4),
+            "int2_decode_us": round(int2_us, 2), "int2_speedup": round(bus / int2_us, 3),
+            "kv_footprint_ratio": round(BF16_BYTES_PER_TOKEN_HEAD / INT2_BYTES_PER_TOKEN_HEAD, 3)}
+        del bws
+    del c, ws
+    return row
+
+
+def small_config_rows(args, with_oracle: bool) -> dict:
+    """Cache-resident workloads (tiny 4/1 x 256, Qwen3-4B 8192, Qwen3-8B batch 1):
+    the decode step warm (back to back, and per call between events) and cold
+    (a 1 GiB buffer written between the calls, outside the events), and the
+    oracle's decode of the same cache on one host thread and on all of them."""
+    import torch
+
+    import oracle
+    import paper_2605_17757_amd as ok
+    import workloads as W
+    dev = "cuda"
+    stream = torch.cuda.current_stream()
+    flush = torch.empty(1 << 30, dtype=torch.uint8, device=dev)
+    rows = {}
+    for index, batch in ((0, None), (1, None), (2, 1)):
+        cfg = W.config(index, batch=batch)
+        B, Hq, Hkv, d = cfg.B, cfg.Hq, cfg.Hkv, cfg.d
+        c = _build_cache(ok, W, cfg, dev, False)
+        lay = c["lay"]
+        S = ok.default_num_splits(lay, B, Hq, int(c["table"].shape[1]) * 64)
+        ws = ok.alloc_workspace(lay, B, Hq, S)
+        out = torch.empty(B, Hq, d, dtype=torch.bfloat16, device=dev)
+
+        def step():
+            ok.decode_step(lay, c["pool"], c["new_k"], c["new_v"], c["new_slots"], cfg.clip_k,
+                           cfg.clip_v, c["q"], c["bt"], c["sl"], c["Rk"], c["Rv"], cfg.sm_scale,
+                           S, ws, out)
+
+        for _ in range(20):
+            step()
+        b2b = _back_to_back_us(step, 200, stream)
+        ev = [_events(2) for _ in range(100)]
+        torch.cuda.synchronize()
+        for e in ev:
+            e[0].record(stream)
+            step()
+            e[1].record(stream)
+        torch.cuda.synchronize()
+        warm = np.array([e[0].elapsed_time(e[1]) for e in ev]) * 1e3
+        cold = []
+        for i in range(30):
+            flush.fill_(i & 0xff)
+            e = _events(2)
+            e[0].record(stream)
+            step()
+            e[1].record(stream)
+            torch.cuda.synchronize()
+            cold.append(e[0].elapsed_time(e[1]) * 1e3)
+        cold = np.array(cold)
+        step_b, split_b, _ = _step_bytes(cfg)
+
+        def pct(x):
+            return {"median": round(float(np.median(x)), 2), "p10": round(float(np.percentile(x, 10)), 2),
+                    "p90": round(float(np.percentile(x, 90)), 2)}
+
+        row = {"workload": cfg.name, "batch": B, "q_heads": Hq, "kv_heads": Hkv,
+               "seq_len": int(cfg.lens.max()), "num_splits": S, "step_bytes": step_b,
+               "int2_kv_bytes": int(cfg.lens.astype(np.int64).sum()) * Hkv * INT2_BYTES_PER_TOKEN_HEAD,
+               "warm_us_back_to_back": round(b2b, 2), "warm_us_per_call": pct(warm),
+               "cold_us_per_call": pct(cold),
+               "cold_GBps": round(step_b / (np.median(cold) * 1e-6) / 1e9, 1),
+               "cold_frac_of_peak": round(step_b / (np.median(cold) * 1e-6) / 1e9 / HBM_PEAK_GBS, 4),
+               "tokens_per_s_warm": round(B / (b2b * 1e-6), 1)}
+        if with_oracle:
+            row["oracle"] = _oracle_small(oracle, W, cfg, c)
+        rows[cfg.name] = row
+        del c, ws
+    del flush
+    return rows
+
+
+def _oracle_small(oracle, W, cfg, c) -> dict:
+    """The oracle's decode of the whole workload (its own cache, built untimed),
+    median of 3 runs on one thread and on all of them."""
+    import torch
+
+    def u16(t):
+        return t.detach().contiguous().cpu().view(torch.int16).numpy().view(np.uint16)
+
+    Hkv, d = cfg.Hkv, cfg.d
+    table, lens = c["table"], cfg.lens
+    bph = oracle.page_head_bytes(d, 64, 32)
+    pool = np.zeros(table.size * Hkv * bph, np.uint8)
+    for b in range(cfg.B):
+        n = int(lens[b])
+        k, v = W.cache_kv(cfg, b, device="cuda")
+        oracle.kv_append(pool, d=d, Hkv=Hkv, P=64, G=32, k=u16(k), v=u16(v),
+                         slot_mapping=W.slots_for(table, b, np.arange(n)), Rk=c["Rk_np"],
+                         Rv=c["Rv_np"], clip_k=cfg.clip_k, clip_v=cfg.clip_v)
+    qh = u16(c["q"])
+    all_threads = oracle.num_threads()
+    res = {}
+    for name, nt in (("one_thread", 1), ("all_threads", all_threads)):
+        oracle.set_num_threads(nt)
+        ts = []
+        for _ in range(3):
+            t0 = time.perf_counter()
+            oracle.decode(pool, d=d, Hkv=Hkv, P=64, G=32, q=qh, block_table=table,
+                          seq_lens=lens, Rk=c["Rk_np"], Rv=c["Rv_np"], sm_scale=cfg.sm_scale)
+            ts.append(time.perf_counter() - t0)
+        t = float(np.median(ts))
+        res[name] = {"threads": nt, "us_per_step": round(t * 1e6, 1),
+                     "tokens_per_s": round(cfg.B / t, 3)}
+    oracle.set_num_threads(all_threads)
+    return res
 
 
 def split_traffic():

@@ -465,6 +465,25 @@ int oscar_calibrate_layer(const oscar_layout *L, const void *q, const void *k, c
 int oscar_hbm_read_probe(const void *src, size_t bytes, uint32_t *sink, int32_t blocks,
                          void *stream);
 
+/* Access-pattern flags of oscar_hbm_read_probe_ex. */
+enum {
+  OSCAR_PROBE_NONTEMPORAL = 1, /* non-temporal loads (lines not kept for reuse)     */
+  OSCAR_PROBE_WAVE_CHUNKS = 2  /* each wave reads loads_per_thread KiB contiguous   */
+};
+
+/*
+ * oscar_hbm_read_probe_ex -- the same read with a chosen access pattern:
+ * loads_per_thread (4, 8 or 16) independent 16-byte loads in flight per thread
+ * and iteration; flags a combination of OSCAR_PROBE_* (0: grid-stride words,
+ * plain loads, as oscar_hbm_read_probe with 4 loads).  With
+ * OSCAR_PROBE_WAVE_CHUNKS wave w reads words [w*64*U, (w+1)*64*U) of each
+ * iteration's span of 64*U words per wave (lane l, load u: word 64u + l).
+ * The sink contract is the one above.  Any other loads_per_thread or flag bit
+ * returns OSCAR_ERR_INVALID_ARG with nothing launched.
+ */
+int oscar_hbm_read_probe_ex(const void *src, size_t bytes, uint32_t *sink, int32_t blocks,
+                            int32_t loads_per_thread, int32_t flags, void *stream);
+
 #ifdef __cplusplus
 }
 #endif

@@ -122,6 +122,8 @@ def lib():
         L.oracle_clip_errors.restype = i32
         L.oracle_clip_errors.argtypes = [P, i64, i32, P, i32, i32, i32, P, i32, P, i32, i32]
         L.oracle_num_threads.restype = i32
+        L.oracle_set_num_threads.restype = None
+        L.oracle_set_num_threads.argtypes = [i32]
         _lib = L
     return _lib
 
@@ -154,6 +156,11 @@ def _rph(*Rs) -> int:
 
 def num_threads() -> int:
     return int(lib().oracle_num_threads())
+
+
+def set_num_threads(n: int) -> None:
+    """Thread count of the oracle's parallel loops from here on (timing only)."""
+    lib().oracle_set_num_threads(int(n))
 
 
 def page_head_bytes(d: int, P: int, G: int) -> int:

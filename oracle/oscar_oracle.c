@@ -808,6 +808,15 @@ int oracle_num_threads(void) {
 #endif
 }
 
+/* Thread count of the parallel loops that follow (n >= 1); timing only. */
+void oracle_set_num_threads(int n) {
+#ifdef _OPENMP
+  if (n >= 1) omp_set_num_threads(n);
+#else
+  (void)n;
+#endif
+}
+
 /* ------------------------------------------------------------------------- */
 /* Offline calibration (Sec. 3 "Algorithm Design: Offline Calibration and     */
 /* Justification"; Alg. 1 Calibrate)                                          */

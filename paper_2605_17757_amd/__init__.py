@@ -36,7 +36,7 @@ EXPORTS = (
     "oscar_calib_score_cov", "oscar_calib_rotation_workspace_bytes", "oscar_calib_rotation",
     "oscar_calib_clip_workspace_bytes", "oscar_calib_clip",
     "oscar_calibrate_layer_workspace_bytes", "oscar_calibrate_layer",
-    "oscar_hbm_read_probe",
+    "oscar_hbm_read_probe", "oscar_hbm_read_probe_ex",
 )
 
 CALIB_MAX_CANDS = 32
@@ -125,6 +125,7 @@ def lib() -> ctypes.CDLL:
             "oscar_calibrate_layer": (ctypes.c_int, [LP, P, P, P, i64, i32, i32, P, i32, P, P, P,
                                                      P, P, P, sz, P]),
             "oscar_hbm_read_probe": (ctypes.c_int, [P, sz, P, i32, P]),
+            "oscar_hbm_read_probe_ex": (ctypes.c_int, [P, sz, P, i32, i32, i32, P]),
         }
         for name, (res, args) in sigs.items():
             fn = getattr(L, name)
@@ -581,16 +582,28 @@ def calibrate_layer(layout: Layout, q, k, v, cands, causal: bool = True, workspa
 # measurement helper
 # ---------------------------------------------------------------------------
 
-def hbm_read_probe(src, blocks: int, sink=None, stream=None) -> torch.Tensor:
+PROBE_NONTEMPORAL, PROBE_WAVE_CHUNKS = 1, 2
+
+
+def hbm_read_probe(src, blocks: int, sink=None, stream=None, loads: int | None = None,
+                   flags: int = 0) -> torch.Tensor:
     """Plain streaming read of the bytes of ``src`` (a contiguous GPU tensor, size a
     multiple of 16 bytes) by ``blocks`` blocks of 256 threads; returns the uint32
-    sink [blocks * 256] whose xor is the xor of the source words."""
+    sink [blocks * 256] whose xor is the xor of the source words.  ``loads`` (4, 8
+    or 16 loads in flight per thread) and ``flags`` (PROBE_NONTEMPORAL,
+    PROBE_WAVE_CHUNKS) select oscar_hbm_read_probe_ex; both None/0 call
+    oscar_hbm_read_probe."""
     if not isinstance(src, torch.Tensor) or not src.is_cuda or not src.is_contiguous():
         raise ValueError("src must be a contiguous GPU tensor")
     nbytes = src.numel() * src.element_size()
     if sink is None:
         sink = torch.empty(int(blocks) * 256, dtype=torch.int32, device=src.device)
-    _check(lib().oscar_hbm_read_probe(ctypes.c_void_p(src.data_ptr()), nbytes,
-                                      _ptr(sink, torch.int32, "sink", int(blocks) * 256),
-                                      int(blocks), _stream(stream)), "oscar_hbm_read_probe")
+    sp = _ptr(sink, torch.int32, "sink", int(blocks) * 256)
+    if loads is None and not flags:
+        _check(lib().oscar_hbm_read_probe(ctypes.c_void_p(src.data_ptr()), nbytes, sp,
+                                          int(blocks), _stream(stream)), "oscar_hbm_read_probe")
+    else:
+        _check(lib().oscar_hbm_read_probe_ex(ctypes.c_void_p(src.data_ptr()), nbytes, sp,
+                                             int(blocks), int(loads or 4), int(flags),
+                                             _stream(stream)), "oscar_hbm_read_probe_ex")
     return sink

@@ -289,26 +289,46 @@ int oscar_decode_reduce(const oscar_layout* L, int32_t B, int32_t Hq, const floa
                                          L->rot_per_head, L->num_kv_heads));
 }
 
+}  // extern "C"
+
+namespace {
+
+// Host-argument checks of oscar_decode_attn (all three stages), with num_splits
+// == 0 resolved to the default; the workspace is checked separately.
+int check_decode_attn(const oscar_layout* L, const void* pages, const void* q, int32_t B,
+                      int32_t Hq, const int32_t* block_table, int32_t max_pages_per_seq,
+                      const int32_t* seq_lens, float sm_scale, int32_t* num_splits,
+                      const void* out, oscar_dtype out_dtype) {
+  if (*num_splits < 0) return OSCAR_ERR_INVALID_ARG;
+  if (*num_splits == 0) {
+    *num_splits = resolve_default_splits(L, B, Hq, max_pages_per_seq);
+    if (*num_splits < 1) return *num_splits == 0 ? OSCAR_ERR_INVALID_ARG : -*num_splits;
+  }
+  int st = check_decode_common(L, B, Hq, *num_splits);
+  if (st) return st;
+  if (!pages || !q || !block_table || !seq_lens || !out || max_pages_per_seq < 1 ||
+      !isfinite(sm_scale))
+    return OSCAR_ERR_INVALID_ARG;
+  if (out_dtype != OSCAR_OUT_BF16 && out_dtype != OSCAR_OUT_F32) return OSCAR_ERR_INVALID_ARG;
+  if (!aligned(pages, 16) || !aligned(q, 4) || !aligned(out, out_dtype == OSCAR_OUT_F32 ? 4 : 2))
+    return OSCAR_ERR_INVALID_ARG;
+  return OSCAR_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
 int oscar_decode_attn(const oscar_layout* L, const void* pages, const void* q, int32_t B,
                       int32_t Hq, const int32_t* block_table, int32_t max_pages_per_seq,
                       const int32_t* seq_lens, const float* R_k, const float* R_v,
                       float sm_scale, int32_t num_splits, void* workspace,
                       size_t workspace_bytes, void* out, oscar_dtype out_dtype, void* stream) {
-  if (num_splits < 0) return OSCAR_ERR_INVALID_ARG;
-  if (num_splits == 0) {
-    num_splits = resolve_default_splits(L, B, Hq, max_pages_per_seq);
-    if (num_splits < 1) return num_splits == 0 ? OSCAR_ERR_INVALID_ARG : -num_splits;
-  }
   // validate every argument of all three stages before launching any of them
-  int st = check_decode_common(L, B, Hq, num_splits);
+  int st = check_decode_attn(L, pages, q, B, Hq, block_table, max_pages_per_seq, seq_lens,
+                             sm_scale, &num_splits, out, out_dtype);
   if (st) return st;
-  if (!pages || !q || !block_table || !seq_lens || !workspace || !out ||
-      max_pages_per_seq < 1 || !isfinite(sm_scale))
-    return OSCAR_ERR_INVALID_ARG;
-  if (out_dtype != OSCAR_OUT_BF16 && out_dtype != OSCAR_OUT_F32) return OSCAR_ERR_INVALID_ARG;
-  if (!aligned(workspace, 256) || !aligned(pages, 16) || !aligned(q, 4) ||
-      !aligned(out, out_dtype == OSCAR_OUT_F32 ? 4 : 2))
-    return OSCAR_ERR_INVALID_ARG;
+  if (!workspace || !aligned(workspace, 256)) return OSCAR_ERR_INVALID_ARG;
   if (workspace_bytes < decode_ws(B, Hq, num_splits).total) return OSCAR_ERR_WORKSPACE_TOO_SMALL;
   st = debug_check(L, stream, B, block_table, max_pages_per_seq, seq_lens, nullptr, 0, nullptr, 0);
   if (st) return st;

@@ -321,3 +321,10 @@ def test_read_probe_rejects_invalid_arguments(L):
     assert L.oscar_hbm_read_probe(buf, 0, sink, 1, None) == ok.ERR_INVALID_ARG
     assert L.oscar_hbm_read_probe(buf, 24, sink, 1, None) == ok.ERR_INVALID_ARG      # not x16
     assert L.oscar_hbm_read_probe(ctypes.c_void_p((1 << 20) + 8), 16, sink, 1, None) == ok.ERR_INVALID_ARG
+    X = L.oscar_hbm_read_probe_ex
+    assert X(None, 16, sink, 1, 8, 0, None) == ok.ERR_INVALID_ARG
+    assert X(buf, 16, sink, 1, 5, 0, None) == ok.ERR_INVALID_ARG          # 4, 8 or 16 loads
+    assert X(buf, 16, sink, 1, 32, 0, None) == ok.ERR_INVALID_ARG
+    assert X(buf, 16, sink, 1, 8, 4, None) == ok.ERR_INVALID_ARG          # unknown flag bit
+    assert X(buf, 24, sink, 1, 8, 3, None) == ok.ERR_INVALID_ARG
+
