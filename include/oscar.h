@@ -202,6 +202,34 @@ int oscar_decode_attn(const oscar_layout *L, const void *pages, const void *q, i
                       float sm_scale, int32_t num_splits, void *workspace,
                       size_t workspace_bytes, void *out, oscar_dtype out_dtype, void *stream);
 
+/* Size of the device scratch array behind oscar_decode_attn_noalloc. */
+#define OSCAR_NOALLOC_SCRATCH_BYTES ((size_t)64 << 20)
+
+/*
+ * oscar_decode_attn_noalloc -- oscar_decode_attn without a workspace argument,
+ * for callers that cannot allocate device memory (code under HIP graph capture,
+ * tight serving loops, harnesses that forbid hipMalloc).  It computes exactly
+ * what oscar_decode_attn computes with the same arguments (same kernels) and
+ * allocates nothing: the workspace is a 64 MiB array in the library's device
+ * data (OSCAR_NOALLOC_SCRATCH_BYTES), one copy per GPU, held from the library's
+ * load until the process ends; its address is looked up once per device on the
+ * first call made with that device current.
+ *   Arguments as in oscar_decode_attn.  A call whose workspace
+ *   (oscar_decode_workspace_bytes(L, B, Hq, num_splits) with num_splits
+ *   resolved) exceeds OSCAR_NOALLOC_SCRATCH_BYTES returns
+ *   OSCAR_ERR_WORKSPACE_TOO_SMALL with nothing launched; a failed address
+ *   lookup returns OSCAR_ERR_HIP.
+ *   Every call on one GPU uses that GPU's one array (no initialization is
+ *   needed: each call writes every entry it reads), so calls that may overlap
+ *   on one GPU (other streams, other host threads) race: order them on one
+ *   stream or serialize them.
+ */
+int oscar_decode_attn_noalloc(const oscar_layout *L, const void *pages, const void *q, int32_t B,
+                              int32_t Hq, const int32_t *block_table, int32_t max_pages_per_seq,
+                              const int32_t *seq_lens, const float *R_k, const float *R_v,
+                              float sm_scale, int32_t num_splits, void *out,
+                              oscar_dtype out_dtype, void *stream);
+
 /*
  * oscar_decode_step -- one serving decode step (Alg. 1 DecodeStep): write the
  * n_new newest tokens' K/V into the cache (exactly oscar_kv_append), then

@@ -26,7 +26,7 @@ HEAD_DIM, PAGE_SIZE, GROUP_SIZE = 128, 64, 32
 EXPORTS = (
     "oscar_status_string", "oscar_page_bytes", "oscar_pool_bytes", "oscar_layout_check",
     "oscar_kv_append", "oscar_decode_workspace_bytes", "oscar_default_num_splits",
-    "oscar_decode_attn", "oscar_decode_step", "oscar_decode_prepare", "oscar_decode_split",
+    "oscar_decode_attn", "oscar_decode_attn_noalloc", "oscar_decode_step", "oscar_decode_prepare", "oscar_decode_split",
     "oscar_decode_reduce",
     "oscar_seg_bytes", "oscar_mixed_workspace_bytes", "oscar_mixed_append",
     "oscar_decode_attn_mixed", "oscar_decode_step_mixed",
@@ -91,6 +91,8 @@ def lib() -> ctypes.CDLL:
             "oscar_default_num_splits": (i32, [LP, i32, i32, i32]),
             "oscar_decode_attn": (ctypes.c_int, [LP, P, P, i32, i32, P, i32, P, P, P, f32, i32, P,
                                                  sz, P, ctypes.c_int, P]),
+            "oscar_decode_attn_noalloc": (ctypes.c_int, [LP, P, P, i32, i32, P, i32, P, P, P,
+                                                         f32, i32, P, ctypes.c_int, P]),
             "oscar_decode_step": (ctypes.c_int, [LP, P, P, P, P, i32, f32, f32, P, i32, i32, P,
                                                  i32, P, P, P, f32, i32, P, sz, P, ctypes.c_int,
                                                  P]),
@@ -255,6 +257,27 @@ def decode_attn(layout: Layout, pages, q, block_table, seq_lens, R_k, R_v, sm_sc
         _ptr(workspace, torch.uint8, "workspace"), workspace.numel(),
         _ptr(out, out.dtype, "out", B * Hq * d), out_dtype, _stream(stream))
     _check(st, "oscar_decode_attn")
+
+
+NOALLOC_SCRATCH_BYTES = 64 << 20
+
+
+def decode_attn_noalloc(layout: Layout, pages, q, block_table, seq_lens, R_k, R_v,
+                        sm_scale: float, num_splits: int, out, stream=None) -> None:
+    """decode_attn with the library's per-GPU scratch array as its workspace
+    (oscar_decode_attn_noalloc: nothing is allocated; calls that overlap on one
+    GPU race)."""
+    B, Hq, mp = _decode_args(layout, q, block_table, seq_lens)
+    d = layout.head_dim
+    out_dtype = OUT_F32 if out.dtype == torch.float32 else OUT_BF16
+    st = lib().oscar_decode_attn_noalloc(
+        ctypes.byref(layout), _ptr(pages, torch.uint8, "pages", pool_bytes(layout)),
+        _ptr(q, torch.bfloat16, "q", B * Hq * d), B, Hq,
+        _ptr(block_table, torch.int32, "block_table", B * mp), mp,
+        _ptr(seq_lens, torch.int32, "seq_lens", B), _rptr(R_k, "R_k", d, layout),
+        _rptr(R_v, "R_v", d, layout), float(sm_scale), int(num_splits),
+        _ptr(out, out.dtype, "out", B * Hq * d), out_dtype, _stream(stream))
+    _check(st, "oscar_decode_attn_noalloc")
 
 
 def decode_step(layout: Layout, pages, k_new, v_new, slot_mapping, clip_k: float,

@@ -6,6 +6,7 @@
 
 #include <algorithm>
 #include <atomic>
+#include <mutex>
 #include <vector>
 
 #include "../../include/oscar.h"
@@ -900,6 +901,61 @@ int oscar_calibrate_layer(const oscar_layout* L, const void* q, const void* k, c
                          nb, err + n_cands, clip + 1, s) != hipSuccess)
     return OSCAR_ERR_HIP;
   return OSCAR_OK;
+}
+
+}  // extern "C"
+
+// ---------------------------------------------------------------------------
+// decode attention without a caller workspace
+// ---------------------------------------------------------------------------
+
+namespace {
+
+// The decode workspace (q~ and the partial states) of oscar_decode_attn_noalloc,
+// for callers that cannot allocate: one copy per GPU, held until the process
+// ends.  In host code `scratch` is only the symbol's name; its device address is
+// looked up with hipGetSymbolAddress once per device (scratch_address) and only
+// that address is handed to the kernels.
+static __device__ __align__(256) uint8_t scratch[OSCAR_NOALLOC_SCRATCH_BYTES];
+
+constexpr int kMaxDevices = 256;
+std::mutex g_scratch_mu;
+void* g_scratch_addr[kMaxDevices];
+
+// Device address of the current device's scratch array.
+int scratch_address(void** addr) {
+  int dev = -1;
+  if (hipGetDevice(&dev) != hipSuccess) return OSCAR_ERR_HIP;
+  if (dev < 0 || dev >= kMaxDevices) return OSCAR_ERR_UNSUPPORTED;
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (!g_scratch_addr[dev]) {
+    void* p = nullptr;
+    if (hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)) != hipSuccess || !p) return OSCAR_ERR_HIP;
+    g_scratch_addr[dev] = p;
+  }
+  *addr = g_scratch_addr[dev];
+  return OSCAR_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+int oscar_decode_attn_noalloc(const oscar_layout* L, const void* pages, const void* q, int32_t B,
+                              int32_t Hq, const int32_t* block_table, int32_t max_pages_per_seq,
+                              const int32_t* seq_lens, const float* R_k, const float* R_v,
+                              float sm_scale, int32_t num_splits, void* out,
+                              oscar_dtype out_dtype, void* stream) {
+  int st = check_decode_attn(L, pages, q, B, Hq, block_table, max_pages_per_seq, seq_lens,
+                             sm_scale, &num_splits, out, out_dtype);
+  if (st) return st;
+  if (decode_ws(B, Hq, num_splits).total > OSCAR_NOALLOC_SCRATCH_BYTES)
+    return OSCAR_ERR_WORKSPACE_TOO_SMALL;
+  void* ws = nullptr;
+  if ((st = scratch_address(&ws))) return st;
+  return oscar_decode_attn(L, pages, q, B, Hq, block_table, max_pages_per_seq, seq_lens, R_k, R_v,
+                           sm_scale, num_splits, ws, OSCAR_NOALLOC_SCRATCH_BYTES, out, out_dtype,
+                           stream);
 }
 
 }  // extern "C"

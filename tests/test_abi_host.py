@@ -328,3 +328,21 @@ def test_read_probe_rejects_invalid_arguments(L):
     assert X(buf, 16, sink, 1, 8, 4, None) == ok.ERR_INVALID_ARG          # unknown flag bit
     assert X(buf, 24, sink, 1, 8, 3, None) == ok.ERR_INVALID_ARG
 
+
+def test_decode_noalloc_validates_before_touching_the_device(L):
+    # invalid arguments and an oversized workspace return before the scratch
+    # array's address is looked up (no device needed)
+    lay = ok.Layout(8, 10)
+
+    def call(B=2, Hq=32, S=2, q=FAKE, out_dtype=0, lay=lay):
+        return L.oscar_decode_attn_noalloc(ctypes.byref(lay), FAKE, q, B, Hq, FAKE, 4, FAKE,
+                                           FAKE, FAKE, 0.088, S, FAKE, out_dtype, None)
+
+    assert call(Hq=30) == ok.ERR_INVALID_ARG
+    assert call(B=0) == ok.ERR_INVALID_ARG
+    assert call(S=-1) == ok.ERR_INVALID_ARG
+    assert call(q=None) == ok.ERR_INVALID_ARG
+    assert call(out_dtype=9) == ok.ERR_INVALID_ARG
+    assert call(lay=ok.Layout(8, 10, page_size=32)) == ok.ERR_UNSUPPORTED
+    assert ok.decode_workspace_bytes(lay, 4096, 64, 64) > ok.NOALLOC_SCRATCH_BYTES
+    assert call(B=4096, Hq=64, S=64) == ok.ERR_WORKSPACE_TOO_SMALL
