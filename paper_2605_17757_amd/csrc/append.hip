@@ -78,25 +78,44 @@ struct QOut {
   uint16_t s16, z16;
 };
 
+// Scale and zero point of a group with (clipped) minimum a and maximum b, as
+// stored (s16, z16) and as used for the codes (sf, zf); a group whose stored
+// scale is 0 stores s = 1, z = M(-a) and codes 0 (deg).
+struct QParams {
+  uint16_t s16, z16;
+  float sf, zf;
+  bool deg;
+};
+__device__ inline QParams quant_params(float a, float b, const QFmt& fmt) {
+  QParams p;
+  const float s = __fdiv_rn(__fsub_rn(b, a), 3.0f);
+  p.s16 = meta_store(fmt, s);
+  p.deg = (p.s16 & 0x7fffu) == 0;
+  if (p.deg) {
+    p.s16 = fmt.bf16 ? 0x3f80u : 0x3c00u;  // 1.0
+    p.z16 = plus_zero(meta_store(fmt, -a));
+    p.sf = p.zf = 0.0f;
+  } else {
+    p.sf = meta_load(fmt, p.s16);
+    p.z16 = plus_zero(meta_store(fmt, __fdiv_rn(-a, p.sf)));
+    p.zf = meta_load(fmt, p.z16);
+  }
+  return p;
+}
+// Code of one clipped channel value y: clamp(round_half_even(y / s + z), 0, 3).
+__device__ inline uint32_t quant_code(float y, const QParams& p) {
+  if (p.deg) return 0u;
+  const float r = rintf(__fadd_rn(__fdiv_rn(y, p.sf), p.zf));
+  return (uint32_t)fminf(fmaxf(r, 0.0f), 3.0f);
+}
+
 // Quantize one clipped channel value y of a group with minimum a and maximum b.
 __device__ inline QOut quantize(float y, float a, float b, const QFmt& fmt) {
+  const QParams p = quant_params(a, b, fmt);
   QOut o;
-  const float s = __fdiv_rn(__fsub_rn(b, a), 3.0f);
-  uint16_t s16 = meta_store(fmt, s);
-  if ((s16 & 0x7fffu) == 0) {
-    o.s16 = fmt.bf16 ? 0x3f80u : 0x3c00u;  // 1.0
-    o.z16 = plus_zero(meta_store(fmt, -a));
-    o.code = 0;
-  } else {
-    const float sf = meta_load(fmt, s16);
-    const uint16_t z16 = plus_zero(meta_store(fmt, __fdiv_rn(-a, sf)));
-    const float zf = meta_load(fmt, z16);
-    float r = rintf(__fadd_rn(__fdiv_rn(y, sf), zf));
-    r = fminf(fmaxf(r, 0.0f), 3.0f);
-    o.s16 = s16;
-    o.z16 = z16;
-    o.code = (uint32_t)r;
-  }
+  o.s16 = p.s16;
+  o.z16 = p.z16;
+  o.code = quant_code(y, p);
   return o;
 }
 
@@ -279,6 +298,9 @@ struct PlainRows {  // oscar_kv_append: token i -> slot_mapping[i]
   }
   __device__ int64_t slot(int row) const { return row < n_rows ? slots[row / Hkv] : -1; }
   __device__ void copy(int, int, int) const {}
+  // the row's bf16 input (whatever its destination), and its bf16 copy destination
+  __device__ const uint16_t* data(int row, int is_v) const { return src(row, is_v); }
+  __device__ uint32_t* seg_dst(int, int) const { return nullptr; }
 };
 
 // Segment store of the mixed cache: [B][Hkv][K, V][S0 + W][d] bf16; position p
@@ -330,6 +352,14 @@ struct PrefillRows {
     const int h = row % Hkv;
     seg_row(seg, Hkv, S0, W, b, h, is_v, seg_slot(S0, W, p))[l] =
         reinterpret_cast<const uint32_t*>((is_v ? v : k) + (size_t)row * kD)[l];
+  }
+  __device__ const uint16_t* data(int row, int is_v) const {
+    return row < n_rows ? (is_v ? v : k) + (size_t)row * kD : nullptr;
+  }
+  __device__ uint32_t* seg_dst(int row, int is_v) const {
+    int b, p;
+    if (route(row, b, p) != 1) return nullptr;
+    return seg_row(seg, Hkv, S0, W, b, row % Hkv, is_v, seg_slot(S0, W, p));
   }
 };
 
@@ -563,18 +593,10 @@ __global__ __launch_bounds__(256) void append_kernel(uint8_t* __restrict__ pages
                   clip_k, clip_v, pick(DEF, fmt));
 }
 
-// ---------------------------------------------------------------------------
-// Bulk cache update (large appends): persistent blocks of 8 waves, one per CU;
-// blockIdx.y selects K or V.  A wave takes 8 rows at a time as 4 row pairs: the
-// two halves of the wave hold rows 2p and 2p + 1 of pair p, and lane l' = l & 31
-// of a half computes channels l' + 32 q (q = 0..3), so each group of 32 channels
-// is one half wave as in the small-append path.  The matrix is staged once per
-// block as Rq[c][l'] = R[c][l' + 32 q], q = 0..3; the rows are kept in LDS as
-// fp64 (channels 2i, 2i + 1 in one 16-byte read), and every lane runs its 16 fp64
-// chains (4 pairs x 4 channels) in ascending channel order.
-// ---------------------------------------------------------------------------
-constexpr int kBulkWaves = 8;
-constexpr int kBulkRows = 8;
+// Row-pair layout of the bulk cache update: the two halves of a wave hold rows
+// 2p and 2p + 1, and lane l' = l & 31 of a half holds channels l' + 32 q
+// (q = 0..3), so each group of 32 channels is one half wave as in the per-row
+// path.
 
 // store_row for the pair layout: lane l' of the half holds channels l' + 32 q;
 // slot is uniform across the half wave.
@@ -651,21 +673,121 @@ __device__ inline void store_row4(uint8_t* __restrict__ pages, int Hkv, int64_t 
   }
 }
 
+// ---------------------------------------------------------------------------
+// Bulk cache update on the fp64 matrix cores (large appends; every format).  A
+// wave rotates 16 rows at a time as one 16 x 128 x 128 product of
+// v_mfma_f64_16x16x4_f64 steps: step s takes channels 4 s .. 4 s + 3, A = the 16
+// rows' bf16 values of those channels (lane l: row l % 16, channel 4 s + l / 16),
+// B = rows 4 s .. 4 s + 3 of R (lane l: row 4 s + l / 16), over eight column
+// tiles whose column j is channel 8 j + t (tile t).  A step adds its four
+// products to the running fp64 sum one after another in channel order (lane
+// group l / 16 = position in that order) and the steps run s = 0..31 in turn,
+// so each x~ is the fp64 sum of the 128 exact products in ascending channel
+// order rounded once to fp32, bit for bit the value of the row-per-lane path.
+// Output lane l, register i of tile t holds row l / 16 + 4 i, channel 8 (l % 16)
+// + t; the 16 rows go through LDS (fp32) to the layout of the quantizer: lane
+// (row, 32-channel slice) for the group-absmax clip (store_slice32), two rows per
+// wave (store_row4) for the token-quantile clip.  R is staged once per block
+// as fp32 (64 KB) and read as two 16-byte words per lane and step.
+// ---------------------------------------------------------------------------
+constexpr int kMfmaWaves = 8;
+constexpr int kMfmaRows = 16;
+constexpr int kStagePitch = 66;   // dwords per staged bf16 row (8-byte reads of 16 rows: all banks)
+constexpr int kXtPitch = 132;     // floats per x~ row
+constexpr int kAreaWords = kMfmaRows * kXtPitch;  // per wave: staged rows, then x~
+
+typedef double d4v __attribute__((ext_vector_type(4)));
+
+// Clip, quantize and pack the 16 rows of a bulk item under the group-absmax
+// clip: lane l takes row l / 4, channels 32 q .. 32 q + 31 (q = l % 4) in x; a
+// group of G channels is the G / 32 lanes q of one row with equal q / (G / 32)
+// (quad-lane reductions for G = 64, 128).  Same steps and operation order as
+// store_row4.
+__device__ inline float quad_group_max(float v, int ng) {
+  if (ng <= 2) v = fmaxf(v, __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), 0xB1, 0xF, 0xF, false)));
+  if (ng == 1) v = fmaxf(v, __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), 0x4E, 0xF, 0xF, false)));
+  return v;
+}
+__device__ inline float quad_group_min(float v, int ng) {
+  if (ng <= 2) v = fminf(v, __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), 0xB1, 0xF, 0xF, false)));
+  if (ng == 1) v = fminf(v, __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), 0x4E, 0xF, 0xF, false)));
+  return v;
+}
+
+__device__ inline void store_slice32(uint8_t* __restrict__ pages, int Hkv, int64_t slot, int row,
+                                     int is_v, float clip, const QFmt& fmt, const float (&x)[32],
+                                     int q) {
+  float m = 0.0f;
+#pragma unroll
+  for (int i = 0; i < 32; ++i) m = fmaxf(m, fabsf(x[i]));
+  const float tau = __fmul_rn(clip, quad_group_max(m, fmt.ng));
+  float y[32];
+  float a = INFINITY, b = -INFINITY;
+#pragma unroll
+  for (int i = 0; i < 32; ++i) {
+    y[i] = fminf(fmaxf(x[i], -tau), tau);
+    a = fminf(a, y[i]);
+    b = fmaxf(b, y[i]);
+  }
+  a = quad_group_min(a, fmt.ng);
+  b = quad_group_max(b, fmt.ng);
+  const QParams p = quant_params(a, b, fmt);
+  uint32_t w[8];
+#pragma unroll
+  for (int jb = 0; jb < 8; ++jb) {
+    uint32_t byte = 0;
+#pragma unroll
+    for (int e = 0; e < 4; ++e) byte |= quant_code(y[4 * jb + e], p) << (2 * e);
+    w[jb] = byte;
+  }
+  if (slot < 0) return;
+  const int h = row % Hkv;
+  const int64_t page = slot / kP;
+  const int t = (int)(slot - page * kP);
+  uint8_t* blk = pages + ((size_t)page * Hkv + h) * block_bytes(fmt.ng);
+  if (is_v) {
+#pragma unroll
+    for (int jb = 0; jb < 8; ++jb) blk[kOffVCodes + (8 * q + jb) * kP + t] = (uint8_t)w[jb];
+  } else {
+    *reinterpret_cast<uint2*>(blk + kOffKCodes + t * (kD / 4) + 8 * q) =
+        make_uint2(w[0] | (w[1] << 8) | (w[2] << 16) | (w[3] << 24),
+                   w[4] | (w[5] << 8) | (w[6] << 16) | (w[7] << 24));
+  }
+  const int per = 4 / fmt.ng;  // slices per group
+  if (q % per == 0) {
+    const uint32_t sz_base = is_v ? off_vsz(fmt.ng) : kOffKSz;
+    *reinterpret_cast<uint32_t*>(blk + sz_base + ((q / per) * kP + t) * 4) =
+        (uint32_t)p.s16 | ((uint32_t)p.z16 << 16);
+  }
+}
+
+// 64-bit value of lane src (any source lane, per-lane index).  The halves are
+// moved as 32-bit ints and widened as unsigned (a sign-extended low half would
+// set every bit of the high half).
+__device__ inline int64_t shfl64(int64_t v, int src) {
+  const int lo = __shfl((int)(uint32_t)v, src, 64), hi = __shfl((int)(v >> 32), src, 64);
+  return (int64_t)(((uint64_t)(uint32_t)hi << 32) | (uint32_t)lo);
+}
+// 64-bit value of lane `lane` (wave-uniform index), widened the same way.
+__device__ inline uint64_t readlane64(uint64_t v, int lane) {
+  const uint32_t lo = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)v, lane);
+  const uint32_t hi = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)(v >> 32), lane);
+  return ((uint64_t)hi << 32) | lo;
+}
+
 template <class Rows, bool DEF>
-__global__ __launch_bounds__(512) void append_bulk_kernel(
+__global__ __launch_bounds__(512) void append_mfma_kernel(
     uint8_t* __restrict__ pages, int Hkv, Rows rows, int n_rows, const float* __restrict__ Rk,
     const float* __restrict__ Rv, float clip_k, float clip_v, QFmt fmt_arg) {
   const QFmt fmt = pick(DEF, fmt_arg);
-  // xs first: its reads use the 16-bit LDS offset field
-  __shared__ double2 xs[kBulkWaves][kBulkRows][kD / 2];      // 64 KB
-  __shared__ float4 Rq[kD][kD / 4];                          // 64 KB
+  __shared__ float4 Rs4[kD][kD / 4];                        // R[c][j], 64 KB
+  __shared__ uint32_t area_all[kMfmaWaves][kAreaWords];     // 66 KB
   const int is_v = blockIdx.y;
   const float* __restrict__ R = is_v ? Rv : Rk;  // nullptr: identity
   const float clip = is_v ? clip_v : clip_k;
   const int t = threadIdx.x;
-  // rph: one KV head's rows per block (gridDim.x is then a multiple of Hkv)
   int h = 0, bx = blockIdx.x, gx = gridDim.x;
-  if (fmt.rph) {
+  if (fmt.rph) {  // one KV head's rows per block (gridDim.x is a multiple of Hkv)
     h = bx % Hkv;
     bx /= Hkv;
     gx /= Hkv;
@@ -677,66 +799,114 @@ __global__ __launch_bounds__(512) void append_bulk_kernel(
     float4 r4[kD * kD / 4 / 512];
 #pragma unroll
     for (int i = 0; i < kD * kD / 4 / 512; ++i) r4[i] = reinterpret_cast<const float4*>(R)[t + 512 * i];
-    float* rq = reinterpret_cast<float*>(Rq);
 #pragma unroll
-    for (int i = 0; i < kD * kD / 4 / 512; ++i) {
-      const int f = t + 512 * i, c = f >> 5, j = 4 * (f & 31);  // R[c][j..j+3]
-      const int q = j >> 5, lp = j & 31;                          // channel j = lp + 32 q
-      rq[(c * 32 + lp + 0) * 4 + q] = r4[i].x;
-      rq[(c * 32 + lp + 1) * 4 + q] = r4[i].y;
-      rq[(c * 32 + lp + 2) * 4 + q] = r4[i].z;
-      rq[(c * 32 + lp + 3) * 4 + q] = r4[i].w;
-    }
+    for (int i = 0; i < kD * kD / 4 / 512; ++i) (&Rs4[0][0])[t + 512 * i] = r4[i];
   }
   __syncthreads();
   const int w = t >> 6, l = t & 63, half = l >> 5, lp = l & 31;
-  const int n_items = (n_seq + kBulkRows - 1) / kBulkRows;
-  for (int item = bx * kBulkWaves + w; item < n_items; item += gx * kBulkWaves) {
+  const int kq = l >> 4, j = l & 15;
+  uint32_t* area = area_all[w];
+  float* xt = reinterpret_cast<float*>(area);
+  // v_perm selector: the bf16 of channel 4 s + kq (of the 8 bytes read) into the
+  // high half of a dword, zeros below: an fp32 with the same value
+  const uint32_t asel = 0x01000C0Cu + 0x02020000u * (uint32_t)kq;
+  const int n_items = (n_seq + kMfmaRows - 1) / kMfmaRows;
+  const int stride = gx * kMfmaWaves;
+  // Rows of an item: their bf16 words (lane l: channels 2 l, 2 l + 1 of each
+  // row), loaded one item ahead into registers, and their destinations, resolved
+  // by lane r % 16 for row r (in parallel: the routing may take several
+  // dependent loads).
+  uint32_t nxt[kMfmaRows];
+  int64_t slot_n = -1;
+  uint32_t* seg_n = nullptr;
+  auto fetch = [&](int it) {
 #pragma unroll
-    for (int rr = 0; rr < kBulkRows; ++rr) {
-      const int row = row_at(item * kBulkRows + rr);
-      double2 x = make_double2(0.0, 0.0);
-      const uint16_t* src = rows.src(row, is_v);
-      if (src) {
-        const uint32_t pair = reinterpret_cast<const uint32_t*>(src)[l];
-        x = make_double2((double)__uint_as_float(pair << 16), (double)__uint_as_float(pair & 0xffff0000u));
-      }
-      xs[w][rr][l] = x;  // channels 2l, 2l + 1
-      rows.copy(row, is_v, l);
+    for (int rr = 0; rr < kMfmaRows; ++rr) {
+      const uint16_t* src = rows.data(row_at(it * kMfmaRows + rr), is_v);
+      nxt[rr] = src ? reinterpret_cast<const uint32_t*>(src)[l] : 0u;
     }
-    double acc[kBulkRows / 2][4];
+    const int row = row_at(it * kMfmaRows + (l & 15));
+    slot_n = rows.slot(row);
+    seg_n = rows.seg_dst(row, is_v);
+  };
+  int item = bx * kMfmaWaves + w;
+  if (item < n_items) fetch(item);
+  for (; item < n_items; item += stride) {
+    // stage the item's rows (and their bf16 copies, if any), then fetch the next
+    const int64_t slot_l = slot_n;
+#pragma unroll
+    for (int rr = 0; rr < kMfmaRows; ++rr) {
+      area[rr * kStagePitch + l] = nxt[rr];
+      uint32_t* d = reinterpret_cast<uint32_t*>(
+          (uintptr_t)readlane64((uint64_t)reinterpret_cast<uintptr_t>(seg_n), rr));
+      if (d) d[l] = nxt[rr];
+    }
+    if (item + stride < n_items) fetch(item + stride);
     if (R) {
+      d4v acc[8];
 #pragma unroll
-      for (int p = 0; p < kBulkRows / 2; ++p)
-#pragma unroll
-        for (int q = 0; q < 4; ++q) acc[p][q] = 0.0;
+      for (int tt = 0; tt < 8; ++tt) acc[tt] = d4v{0.0, 0.0, 0.0, 0.0};
 #pragma unroll 2
-      for (int c2 = 0; c2 < kD / 2; ++c2) {
-        const float4 ra = Rq[2 * c2][lp], rb = Rq[2 * c2 + 1][lp];
-        const double a[4] = {ra.x, ra.y, ra.z, ra.w}, b[4] = {rb.x, rb.y, rb.z, rb.w};
+      for (int s2 = 0; s2 < kD / 4; ++s2) {
+        const uint2 xa = *reinterpret_cast<const uint2*>(&area[j * kStagePitch + 2 * s2]);
+        const double a = (double)__uint_as_float(__builtin_amdgcn_perm(xa.y, xa.x, asel));
+        const float4 r0 = Rs4[4 * s2 + kq][2 * j], r1 = Rs4[4 * s2 + kq][2 * j + 1];
+        const float rb[8] = {r0.x, r0.y, r0.z, r0.w, r1.x, r1.y, r1.z, r1.w};
 #pragma unroll
-        for (int p = 0; p < kBulkRows / 2; ++p) {
-          const double2 x = xs[w][2 * p + half][c2];  // channels 2 c2, 2 c2 + 1 of the row
+        for (int tt = 0; tt < 8; ++tt)
+          acc[tt] = __builtin_amdgcn_mfma_f64_16x16x4f64(a, (double)rb[tt], acc[tt], 0, 0, 0);
+      }
+      // x~ rows to LDS as fp32 (the staged rows are no longer read)
 #pragma unroll
-          for (int q = 0; q < 4; ++q) {
-            acc[p][q] = __fma_rn(x.x, a[q], acc[p][q]);
-            acc[p][q] = __fma_rn(x.y, b[q], acc[p][q]);
-          }
+      for (int i = 0; i < 4; ++i) {
+        float* dst = xt + (kq + 4 * i) * kXtPitch + 8 * j;
+        *reinterpret_cast<float4*>(dst) =
+            make_float4(__double2float_rn(acc[0][i]), __double2float_rn(acc[1][i]),
+                        __double2float_rn(acc[2][i]), __double2float_rn(acc[3][i]));
+        *reinterpret_cast<float4*>(dst + 4) =
+            make_float4(__double2float_rn(acc[4][i]), __double2float_rn(acc[5][i]),
+                        __double2float_rn(acc[6][i]), __double2float_rn(acc[7][i]));
+      }
+    }
+    if (!fmt.quantile) {  // lane l: row l / 4, channels 32 (l % 4) .. + 31
+      const int rr = l >> 2, q = l & 3;
+      float x[32];
+      if (R) {
+#pragma unroll
+        for (int i = 0; i < 8; ++i) {
+          const float4 v = *reinterpret_cast<const float4*>(xt + rr * kXtPitch + 32 * q + 4 * i);
+          x[4 * i] = v.x; x[4 * i + 1] = v.y; x[4 * i + 2] = v.z; x[4 * i + 3] = v.w;
+        }
+      } else {  // identity: the staged bf16 values
+#pragma unroll
+        for (int i = 0; i < 16; ++i) {
+          const uint32_t pr = area[rr * kStagePitch + 16 * q + i];
+          x[2 * i] = __uint_as_float(pr << 16);
+          x[2 * i + 1] = __uint_as_float(pr & 0xffff0000u);
         }
       }
-    } else {  // identity: channel l' + 32 q of the row
-#pragma unroll
-      for (int p = 0; p < kBulkRows / 2; ++p)
-#pragma unroll
-        for (int q = 0; q < 4; ++q) {
-          const double2 x = xs[w][2 * p + half][(lp + 32 * q) >> 1];
-          acc[p][q] = (lp & 1) ? x.y : x.x;
-        }
+      const int row = row_at(item * kMfmaRows + rr);
+      store_slice32(pages, Hkv, shfl64(slot_l, rr), row, is_v, clip, fmt, x, q);
+      continue;
     }
+    // token-quantile clip: row pairs, half `half` takes row 2 p + half; lane lp
+    // holds channels lp + 32 q
+#pragma unroll 1
+    for (int p = 0; p < kMfmaRows / 2; ++p) {
+      const int rr = 2 * p + half;
+      double x4[4];
 #pragma unroll
-    for (int p = 0; p < kBulkRows / 2; ++p) {
-      const int row = row_at(item * kBulkRows + 2 * p + half);
-      store_row4(pages, Hkv, rows.slot(row), row, is_v, clip, fmt, acc[p], lp, half);
+      for (int q = 0; q < 4; ++q) {
+        const int c = lp + 32 * q;
+        if (R) {
+          x4[q] = (double)xt[rr * kXtPitch + c];
+        } else {  // identity: the staged bf16 value
+          const uint32_t pr = area[rr * kStagePitch + (c >> 1)];
+          x4[q] = (double)__uint_as_float((c & 1) ? (pr & 0xffff0000u) : (pr << 16));
+        }
+      }
+      const int row = row_at(item * kMfmaRows + rr);
+      store_row4(pages, Hkv, shfl64(slot_l, rr), row, is_v, clip, fmt, x4, lp, half);
     }
   }
 }
@@ -975,10 +1145,10 @@ hipError_t launch_rows(void* pages, int64_t Hkv, const Rows& rows, int64_t n_row
     };
     if (def) go(append_kernel<1, Rows, true>);
     else go(append_kernel<1, Rows, false>);
-  } else {  // bulk: one persistent 8-wave block per CU, half of them per tensor
+  } else {  // bulk: one persistent 8-wave block per CU (fp64 MFMA), half of them per tensor
     const int64_t heads = fmt.rph ? Hkv : 1;  // rph: a block per head's share
-    const int64_t items = (n_rows / heads + kBulkRows - 1) / kBulkRows;
-    int64_t nb = (items + kBulkWaves - 1) / kBulkWaves;
+    const int64_t items = (n_rows / heads + kMfmaRows - 1) / kMfmaRows;
+    int64_t nb = (items + kMfmaWaves - 1) / kMfmaWaves;
     const int64_t cap = std::max<int64_t>(1, device_cus() / 2 / heads);
     if (nb > cap) nb = cap;
     nb *= heads;
@@ -987,8 +1157,8 @@ hipError_t launch_rows(void* pages, int64_t Hkv, const Rows& rows, int64_t n_row
                          static_cast<uint8_t*>(pages), (int)Hkv, rows, (int)n_rows, Rk, Rv,
                          clip_k, clip_v, fmt);
     };
-    if (def) go(append_bulk_kernel<Rows, true>);
-    else go(append_bulk_kernel<Rows, false>);
+    if (def) go(append_mfma_kernel<Rows, true>);
+    else go(append_mfma_kernel<Rows, false>);
   }
   return hipGetLastError();
 }

@@ -2,11 +2,12 @@
 (liboscar on the GPU, the CPU oracle on the host) from the same seeded inputs,
 and compare the results under the parity rules:
 
-  * append: page bytes bit-exact.  A differing byte is tolerated only when its
-    row is within 1e-6 of a rounding boundary in the oracle's own arithmetic
-    (the fp64 value of (b-a)/3 or -a/s within 1e-6 relative of a binary16
-    rounding midpoint, or a code's y/s + z within 1e-6 of k + 0.5); tolerated
-    rows are counted and reported.
+  * append: page bytes bit-exact.  Every differing element (code, scale, zero
+    point) is tolerated only when its own decision lies within 1e-6 of a
+    rounding boundary in the oracle's own arithmetic (the fp64 value of (b-a)/3
+    or -a/s within 1e-6 relative of a rounding midpoint of the metadata format,
+    or a code's y/s + z within 1e-6 of k + 0.5; the codes of a tolerated (s, z)
+    follow it); tolerated elements are counted and reported.
   * decode: max |o_gpu - o_oracle| <= 2e-3 on the fp32 output (fp32
     accumulation against the fp64 oracle); the bf16 output equals the
     round-to-nearest-even of the same kernel's fp32 output.
@@ -118,44 +119,75 @@ def _bf16_midpoint_close(x: float, rel: float = 1e-6) -> bool:
     return abs(k - (2 * math.floor(k / 2) + 1)) * half <= rel * abs(x)
 
 
-def row_near_boundary(xt: np.ndarray, rho: float, G: int = 32, meta: int = 0,
-                      clip: int = 0) -> bool:
-    """True if quantizing this rotated row involves a decision within 1e-6 of a
-    rounding boundary (evaluated from the oracle's fp32 row in fp64).  meta, clip:
-    the metadata format (0 binary16, 1 bfloat16) and clip rule (0 group absmax,
-    1 token quantile)."""
+def _meta_value(bits16: int, meta: int) -> float:
+    """The stored scale or zero point from its 16 bits (binary16 or bfloat16)."""
+    if meta:
+        return float(np.array([bits16 << 16], np.uint32).view(np.float32)[0])
+    return float(np.array([bits16], np.uint16).view(np.float16)[0])
+
+
+def _row_fields(pool: np.ndarray, base: int, t: int, is_v: int, G: int):
+    """Codes [128] and (s, z) bit patterns [d/G, 2] of token slot t of the
+    page-head block at byte `base` (the page layout of include/oscar.h)."""
+    ng = 128 // G
+    if is_v:
+        cb = pool[base + 2048 + np.arange(32) * 64 + t]
+    else:
+        cb = pool[base + t * 32: base + t * 32 + 32]
+    codes = ((cb[:, None].astype(np.int32) >> (2 * np.arange(4))) & 3).reshape(128)
+    off = base + 4096 + (ng * 64 * 4 if is_v else 0) + (np.arange(ng) * 64 + t) * 4
+    e = pool[off[:, None] + np.arange(4)].astype(np.int64)
+    sz = np.stack([e[:, 0] | (e[:, 1] << 8), e[:, 2] | (e[:, 3] << 8)], axis=1)
+    return codes, sz
+
+
+def row_tolerated_elements(xt: np.ndarray, rho: float, gpu_codes, gpu_sz, ora_codes, ora_sz,
+                           G: int = 32, meta: int = 0, clip: int = 0):
+    """Differing elements (codes, scales, zero points) of one quantized row and
+    whether each is a near-boundary case in the oracle's own arithmetic (from its
+    fp32 rotated row xt, evaluated in fp64): a scale that differs is tolerated
+    only if (b - a)/3 lies within 1e-6 relative of a rounding midpoint of the
+    metadata format, a zero point (same scale) only if -a/s does; the codes of
+    such a group follow from the other (s, z) and are tolerated with it; a code of
+    a group whose (s, z) agree only if its y/s + z lies within 1e-6 of k + 0.5.
+    Returns (n_differing_elements, n_untolerated)."""
     close = _bf16_midpoint_close if meta else _f16_midpoint_close
-    rnd = _bf16_round if meta else (lambda v: float(np.float16(v)))
     tau_tok = np.float32(oracle.token_quantile(xt, rho)) if clip else None
-    for g in range(len(xt) // G):
-        x = xt[g * G:(g + 1) * G].astype(np.float32)
+    n_diff = n_bad = 0
+    for g in range(128 // G):
+        sl = slice(g * G, (g + 1) * G)
+        dc = np.nonzero(gpu_codes[sl] != ora_codes[sl])[0]
+        ds, dz = gpu_sz[g, 0] != ora_sz[g, 0], gpu_sz[g, 1] != ora_sz[g, 1]
+        n_here = len(dc) + int(ds) + int(dz)
+        if n_here == 0:
+            continue
+        n_diff += n_here
+        x = xt[sl].astype(np.float32)
         if clip:
             tau = tau_tok
         else:
-            m = np.float32(np.abs(x).max())
-            tau = np.float32(np.float32(rho) * m)
+            tau = np.float32(np.float32(rho) * np.float32(np.abs(x).max()))
         y = np.minimum(np.maximum(x, -tau), tau)
         a, b = float(y.min()), float(y.max())
-        s_exact = (b - a) / 3.0
-        if close(s_exact):
-            return True
-        s16 = rnd(float(np.float32(np.float32(b - a) / np.float32(3.0))))
-        if s16 == 0.0:
+        s16 = _meta_value(int(ora_sz[g, 0]), meta)
+        if ds or dz:
+            ok_group = close((b - a) / 3.0) if ds else (s16 != 0.0 and close(-a / s16))
+            if not ok_group:
+                n_bad += n_here
             continue
-        z_exact = -a / s16
-        if close(z_exact):
-            return True
-        z16 = rnd(float(np.float32(-a) / np.float32(s16)))
+        z16 = _meta_value(int(ora_sz[g, 1]), meta)
         u = y.astype(np.float64) / s16 + z16
-        if np.any(np.abs(u - (np.floor(u) + 0.5)) <= 1e-6):
-            return True
-    return False
+        for c in dc:
+            if abs(u[c] - (np.floor(u[c]) + 0.5)) > 1e-6:
+                n_bad += 1
+    return n_diff, n_bad
 
 
 def compare_pools(gpu_pool: np.ndarray, ora_pool: np.ndarray, case: Case, meta: int = 0,
                   clip: int = 0, G: int = 32):
-    """Returns (n_diff_bytes, n_tolerated_rows); raises AssertionError on any
-    difference that the near-boundary rule does not cover."""
+    """Returns (n_diff_bytes, n_tolerated_elements): every differing code, scale
+    or zero point must be a near-boundary case (row_tolerated_elements); raises
+    AssertionError on any other difference."""
     diff = np.nonzero(gpu_pool != ora_pool)[0]
     if diff.size == 0:
         return 0, 0
@@ -176,7 +208,7 @@ def compare_pools(gpu_pool: np.ndarray, ora_pool: np.ndarray, case: Case, meta: 
         else:
             t, is_v = ((inner - 4096 - szb) // 4) % 64, 1
         bad_rows.add((page * 64 + t, h, is_v))
-    untolerated = []
+    untolerated, n_tol = [], 0
     for slot, h, is_v in sorted(bad_rows):
         i = slot_to_tok.get(slot)
         if i is None:
@@ -188,12 +220,20 @@ def compare_pools(gpu_pool: np.ndarray, ora_pool: np.ndarray, case: Case, meta: 
         if R is not None and np.ndim(R) == 3:  # one rotation per KV head
             R = R[h]
         xt = oracle.rotate_row(x, R)
-        if not row_near_boundary(xt, case.cfg.clip_v if is_v else case.cfg.clip_k, G=G,
-                                 meta=meta, clip=clip):
-            untolerated.append((slot, h, is_v, "not near a rounding boundary"))
+        page, t = divmod(slot, 64)
+        base = (page * hkv + h) * bph
+        gc, gsz = _row_fields(gpu_pool, base, t, is_v, G)
+        oc, osz = _row_fields(ora_pool, base, t, is_v, G)
+        n_diff, n_bad = row_tolerated_elements(
+            xt, case.cfg.clip_v if is_v else case.cfg.clip_k, gc, gsz, oc, osz, G=G, meta=meta,
+            clip=clip)
+        if n_bad:
+            untolerated.append((slot, h, is_v, "%d of %d differing elements not near a rounding "
+                                "boundary" % (n_bad, n_diff)))
+        n_tol += n_diff - n_bad
     assert not untolerated, "append mismatches: %s (first of %d rows)" % (untolerated[:5],
                                                                            len(untolerated))
-    return int(diff.size), len(bad_rows)
+    return int(diff.size), n_tol
 
 
 # ---------------------------------------------------------------------------

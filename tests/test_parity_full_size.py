@@ -5,10 +5,11 @@ configs 3 and 4 at their full shapes, in the launch configuration bench.py
 times: the cache holds tokens 0..len-2 of every sequence, then one
 oscar_decode_step appends each sequence's newest token and decodes the whole
 batch with the default split count.  The GPU runs the whole batch; the oracle
-appends and decodes only the sampled sequences (all query heads of each),
-which is all that their outputs and pages depend on.  Compared: every output
-element of the sampled sequences (2e-3 on fp32) and every byte of their pages
-(bit-exact, near-boundary rule of helpers.compare_pools)."""
+appends the sampled sequences and decodes a subset of them (all query heads of
+each), which is all that those outputs and pages depend on.  Compared: every
+output element of the decoded sequences (2e-3 on fp32) and every byte of the
+pages of all sampled sequences (bit-exact, near-boundary rule of
+helpers.compare_pools)."""
 import numpy as np
 import pytest
 import torch
@@ -21,7 +22,8 @@ from helpers import DECODE_TOL, Case, bits, compare_pools, log, max_abs
 pytestmark = pytest.mark.gpu
 
 
-def _full_size(cfg: W.Config, sample_b):
+def _full_size(cfg: W.Config, decode_b, page_b=()):
+    sample_b = sorted(set(decode_b) | set(page_b))
     B, Hq, Hkv, d = cfg.B, cfg.Hq, cfg.Hkv, cfg.d
     lens = cfg.lens.astype(np.int64)
     table, num_pages = W.block_table(cfg)
@@ -30,7 +32,7 @@ def _full_size(cfg: W.Config, sample_b):
     Rk = torch.from_numpy(Rk_np).cuda()
     Rv = torch.from_numpy(Rv_np).cuda()
     log("full size", cfg.name, "B", B, "Hq", Hq, "Hkv", Hkv, "pages", num_pages,
-        "sampled", list(sample_b))
+        "decoded", list(decode_b), "page bytes", list(sample_b))
 
     # The sampled sequences' rows are drawn once on the CPU and used by both sides;
     # the other sequences (which the sampled outputs do not read) are drawn on the
@@ -75,10 +77,10 @@ def _full_size(cfg: W.Config, sample_b):
         ks.append(k)
         vs.append(v)
         ss.append(slots)
-    pairs = np.array([(b, h) for b in sample_b for h in range(Hq)], np.int32)
+    pairs = np.array([(b, h) for b in decode_b for h in range(Hq)], np.int32)
     ref = oracle.decode(ora, d=d, Hkv=Hkv, P=64, G=32, q=bits(q), block_table=table,
                         seq_lens=cfg.lens, Rk=Rk_np, Rv=Rv_np, sm_scale=cfg.sm_scale, pairs=pairs)
-    got = out[torch.as_tensor(np.asarray(sample_b))].reshape(-1, d)
+    got = out[torch.as_tensor(np.asarray(decode_b))].reshape(-1, d)
     err = max_abs(got, ref)
     log("  decode max|err| over %d (seq, head) rows = %.3g" % (len(pairs), err))
     assert err <= DECODE_TOL
@@ -93,7 +95,7 @@ def _full_size(cfg: W.Config, sample_b):
     case = Case(cfg, Rk_np, Rv_np, table, num_pages, q, torch.cat(ks), torch.cat(vs),
                 np.concatenate(ss))
     nd, nt = compare_pools(gpu_sel, ora, case)
-    log("  append: differing bytes", nd, "tolerated near-boundary rows", nt)
+    log("  append: differing bytes", nd, "tolerated near-boundary elements", nt)
 
 
 def test_full_size_bench_workload_qwen3_8b_b64():
@@ -103,8 +105,10 @@ def test_full_size_bench_workload_qwen3_8b_b64():
 
 
 def test_full_size_qwen3_32b_b128_ctx32k():
-    _full_size(W.config(3), [0, 127])
+    # decode 2 sequences; page bytes of 8 spread over the batch
+    _full_size(W.config(3), [0, 127], [0, 17, 38, 55, 64, 91, 110, 127])
 
 
 def test_full_size_longctx_b16_ctx128k():
-    _full_size(W.config(4), [5])
+    # decode 1 sequence; page bytes of 4
+    _full_size(W.config(4), [5], [0, 5, 10, 15])

@@ -22,7 +22,7 @@ def _run_full(case: Case, num_splits: int = 0, check_bf16: bool = True):
     pool = gpu_append(case)
     ora = oracle_append(case)
     nd, nt = compare_pools(pool.cpu().numpy(), ora, case)
-    log("  append: differing bytes", nd, "tolerated near-boundary rows", nt)
+    log("  append: differing bytes", nd, "tolerated near-boundary elements", nt)
     ref = oracle_decode(case, ora)
     out = gpu_decode(case, pool, num_splits)
     err = max_abs(out, ref)
@@ -198,7 +198,7 @@ def test_append_fuzz_edge_rows():
         pool = gpu_append(case)
         ora = oracle_append(case)
         nd, nt = compare_pools(pool.cpu().numpy(), ora, case)
-        log("fuzz compose=%s differing bytes %d tolerated rows %d" % (compose, nd, nt))
+        log("fuzz compose=%s differing bytes %d tolerated elements %d" % (compose, nd, nt))
 
 
 def test_append_only_touches_addressed_slots():

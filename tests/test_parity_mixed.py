@@ -133,7 +133,7 @@ class Mixed:
 
     def compare_state(self, pool, seg, ora_pages, ora_seg, lens):
         nd, nt = compare_pools(pool.cpu().numpy(), ora_pages, self.history_case(lens))
-        log("  pool: differing bytes", nd, "tolerated near-boundary rows", nt)
+        log("  pool: differing bytes", nd, "tolerated near-boundary elements", nt)
         gs = _seg_np(seg)
         assert gs.shape == ora_seg.shape
         bad = np.nonzero(gs != ora_seg)[0]
@@ -386,4 +386,4 @@ def test_mixed_full_size_bench_workload_sampled():
     case = Case(cfg, Rk_np, Rv_np, table, num_pages, q, torch.cat(ks), torch.cat(vs),
                 np.concatenate(ss))
     nd, nt = compare_pools(gpu_sel, ora, case)
-    log("  pool: differing bytes", nd, "tolerated near-boundary rows", nt)
+    log("  pool: differing bytes", nd, "tolerated near-boundary elements", nt)

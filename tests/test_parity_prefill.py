@@ -80,7 +80,7 @@ def test_prefill_131072_tokens_one_call(fmt):
     assert np.array_equal(gseg, oseg)
     case = Case(cfg, Rk_np, Rv_np, table, num_pages, q, k[lo:hi], v[lo:hi], sl)
     nd, nt = compare_pools(pool.cpu().numpy(), ora, case, meta=meta, clip=clip, G=G)
-    log("  pool: differing bytes", nd, "tolerated near-boundary rows", nt)
+    log("  pool: differing bytes", nd, "tolerated near-boundary elements", nt)
 
     ref = oracle.decode_mixed(ora, oseg, d=D, Hkv=Hkv, P=P, G=G, S0=S0, W=WIN, q=bits(q),
                               block_table=table, seq_lens=cfg.lens, Rk=Rk_np, Rv=Rv_np,

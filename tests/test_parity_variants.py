@@ -104,7 +104,7 @@ class VCase:
     def compare(self, gpu_pool, ora_pool, upto):
         nd, nt = compare_pools(gpu_pool.cpu().numpy(), ora_pool, self.case(upto), meta=self.meta,
                                clip=self.clip, G=self.G)
-        log("  pool: differing bytes", nd, "tolerated near-boundary rows", nt)
+        log("  pool: differing bytes", nd, "tolerated near-boundary elements", nt)
 
 
 def _small_cfg(name, seed):
