@@ -390,7 +390,7 @@ def main():
         "roofline": {
             "kernel": "decode_split", "bound": "hbm", "achieved": round(achieved, 1),
             "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4),
-            "traffic": split_traffic(), "bytes_per_launch": split_bytes,
+            "traffic": split_traffic(cfg.name), "bytes_per_launch": split_bytes,
         },
         "append_64_tokens_per_seq": {
             "tokens": B * n_new, "rows": app_rows, "us": round(app_us, 2),
@@ -817,7 +817,7 @@ def config_row(args, index: int, with_bf16: bool) -> dict:
         "roofline": {"kernel": "decode_split", "bound": "hbm", "achieved": round(ach, 1),
                      "peak": HBM_PEAK_GBS, "unit": "GB/s",
                      "frac": round(ach / HBM_PEAK_GBS, 4), "us": round(split_us, 2),
-                     "bytes_per_launch": split_b},
+                     "bytes_per_launch": split_b, "traffic": split_traffic(cfg.name)},
         "pieces_per_sequence": pieces_per_sequence(ws, B, Hq, S),
         "bytes": {"step_total": step_b, "int2_kv": int(cfg.lens.astype(np.int64).sum()) * Hkv *
                   INT2_BYTES_PER_TOKEN_HEAD,
@@ -955,20 +955,23 @@ def _oracle_small(oracle, W, cfg, c) -> dict:
     return res
 
 
-def split_traffic():
-    """HBM bytes per split launch from the committed rocprofv3 FETCH_SIZE /
-    WRITE_SIZE passes (scaled by a 1 GiB copy's counters), or None when the
-    split kernel's source has changed since those counters were taken."""
+def split_traffic(workload: str = "qwen3_8b_b64_ctx32k"):
+    """HBM bytes per split launch on `workload` from the committed rocprofv3
+    FETCH_SIZE / WRITE_SIZE passes (FETCH_SIZE scaled by what it reads for a 1 GiB
+    copy and a 2 GiB streaming read of known size), or None when the split
+    kernel's source has changed since those counters were taken or the workload
+    has no record."""
     import hashlib
     rec_path = os.path.join(ROOT, "profiles", "split_mfma_kernel_traffic.json")
     try:
         rec = json.load(open(rec_path))
         src = open(os.path.join(ROOT, rec["source"]), "rb").read()
+        entry = rec["workloads"][workload]
     except (OSError, ValueError, KeyError):
         return None
     if hashlib.sha256(src).hexdigest() != rec.get("source_sha256"):
         return None
-    return int(rec["traffic_bytes_per_launch"])
+    return int(entry["traffic_bytes_per_launch"])
 
 
 def cpu_baseline(cfg, table, Rk_np, Rv_np, q, seconds, max_seqs=4):
