@@ -190,9 +190,8 @@ hipError_t launch_decode_split(const uint8_t* pages, int Hkv, int B, int Hq,
                                const int32_t* seq_lens, int num_splits, const float* qt,
                                float* part_o, float* part_ml, hipStream_t st, int meta_bf16,
                                int ng, const MixedSpec* mixed) {
-  // one resident wave per SIMD slot: 4 waves per SIMD, 4 SIMDs per CU
   return launch_decode_split_mfma(pages, Hkv, B, Hq, block_table, max_pages, seq_lens,
-                                  num_splits, 16 * device_cus(), qt, part_o, part_ml, st,
+                                  num_splits, device_cus(), qt, part_o, part_ml, st,
                                   meta_bf16, ng, mixed);
 }
 

@@ -1,8 +1,8 @@
 // Split kernel of INT2 decode attention on the matrix cores (gfx950 int8 MFMA).
-// Persistent waves: each wave owns one (page range, kv-head, chunk of 4 query
-// heads), walks the range's pages (64 tokens each) and keeps the online-softmax
-// state of its 4 heads in registers; a range that crosses sequence boundaries
-// writes one partial state per sequence piece (see split_mfma_kernel).
+// Persistent waves: each wave owns one (page range, kv-head), walks the range's
+// pages (64 tokens each) and keeps the online-softmax state of the kv-head's
+// query heads in registers, in chunks of 4; a range that crosses sequence
+// boundaries writes one partial state per sequence piece (see split_mfma_kernel).
 //
 // Arithmetic (Sec. 2: K^ = Q(K R) R^T; Alg. 1 DecodeStep), per 32-channel group g
 // with Q(x~)_c = s_g (code_c - z_g):
@@ -199,14 +199,19 @@ __device__ inline int combine3(int a, int b, int c) {
   return (int)((t << 8) + (uint32_t)c);
 }
 
-// Per-wave LDS: the page copy and the exchanges between lane roles.
+// Per-wave LDS: the page copy and the exchanges between lane roles.  The weight
+// digits of chunk 0 go over the page's spent K codes and K scales, those of
+// chunks 1..NCH-1 to areas of their own (same slot placement).
+constexpr int kWSlots = 208;  // slots of one chunk's weight digits (the K area of the page)
+template <int NCH>
 struct WaveLds {
-  uint4 page[kSlots];   // page-head block (slot placement above)
-  float4 p[4][17];      // softmax weights of the page, [head][token / 4] (pitch 17)
-  float2 hs[4];         // (alpha, p_max) per head
-  float ws[16];         // P.V scale per (head, group); at the end, sum w z per (head, group)
-  int qs[16];           // sum of q_int per (head, 32-channel slice)
-  float sq[4];          // q scale per head
+  uint4 page[kSlots];                 // page-head block (slot placement above)
+  uint4 wdig[NCH - 1][kWSlots];       // weight digits of chunks 1..NCH-1
+  float4 p[4][17];                    // softmax weights of the page, [head][token / 4] (pitch 17)
+  float2 hs[4];                       // (alpha, p_max) per head
+  float ws[NCH][16];                  // P.V scale per (head, group) and chunk; at the end, sum w z
+  int qs[16];                         // sum of q_int per (head, 32-channel slice)
+  float sq[4];                        // q scale per head
 };
 
 typedef uint32_t u4 __attribute__((ext_vector_type(4)));
@@ -217,11 +222,9 @@ struct Stage {  // chunks 64 i + lane of the next page, i = 0..5
 
 // A page-head block has 256 + 32 NG chunks of 16 bytes (NG groups per head): the
 // codes, then 16 NG chunks of K (s, z) and 16 NG of V (s, z).  Chunks past the
-// block are not loaded.  NT: non-temporal loads, for blocks that exactly one wave
-// reads (the lines are not kept for reuse, which raised the read rate from 5.3
-// to 5.6 TB/s on the Qwen3-8B-shaped batch); with several query-head chunks per
-// KV head the chunks' waves read the same block and the later ones hit L2 on
-// plain loads.
+// block are not loaded.  NT: non-temporal loads (every block is read by exactly
+// one wave, so its lines are not kept for reuse; this raised the read rate from
+// 5.3 to 5.8 TB/s on the Qwen3-8B-shaped batch).
 template <bool NT>
 __device__ inline u4 ld16(const u4* p) {
   if (NT) return __builtin_nontemporal_load(p);
@@ -271,90 +274,78 @@ struct WaveState {
 // [t0, t1) (the partial first or last page of a token range).
 // NG groups of 128 / NG channels per head: a group spans 4 / NG of the 32-channel
 // slices that the MFMA tiles use, which share its (s, z) and its P.V weights.
-template <bool FULL, bool BF, int NG>
-__device__ inline void compute_page(WaveState& st, WaveLds& L, int t0, int t1, int lo, int hi) {
+// NCH chunks of 4 query heads share the page: the K-code operands of the score
+// MFMAs, the V scales (and their page maximum) and the V-code operands of the P.V
+// MFMAs are formed once; everything per head runs once per chunk.
+template <bool FULL, bool BF, int NG, int NCH>
+__device__ inline void compute_page(WaveState (&st)[NCH], WaveLds<NCH>& L, int t0, int t1, int lo,
+                                    int hi) {
   char* pb = reinterpret_cast<char*>(L.page);
-  // ---- scores of head hi for tokens 4*lo + u ----
+  // ---- scores of head hi of every chunk for tokens 4*lo + u ----
   // code dword 2g + (hi>>1) of token 4*lo + u at byte 32u + 8g from the lane base
   const uint32_t* kc = reinterpret_cast<const uint32_t*>(pb + kLdsKCodes + 144 * lo + 4 * (hi >> 1));
   const uint32_t sh4 = 4u * (uint32_t)(hi & 1);
   uint4 ksz[NG];  // (s, z) of tokens 4*lo + (0..3), group i
 #pragma unroll
   for (int i = 0; i < NG; ++i) ksz[i] = *reinterpret_cast<const uint4*>(pb + kLdsKSz + 256 * i + 16 * lo);
-  float S[4];
+  float S[NCH][4];
 #pragma unroll
   for (int u = 0; u < 4; ++u) {
-    float acc = 0.0f;
-    v4i dg[NG];  // NG < 4: the digit sums of a group's slices accumulate in one MFMA chain
+    float acc[NCH];
+    v4i dg[NCH][NG];  // NG < 4: the digit sums of a group's slices accumulate in one MFMA chain
+#pragma unroll
+    for (int c = 0; c < NCH; ++c) acc[c] = 0.0f;
 #pragma unroll
     for (int g = 0; g < 4; ++g) {
       const uint32_t y = kc[8 * u + 2 * g] >> sh4;  // fields 2(hi&1), 2(hi&1)+1 of each byte
       const uint32_t msk = 0x03030303u;
       const long b = (long)((uint64_t)(y & msk) | ((uint64_t)((y >> 2) & msk) << 32));
-      if (NG == 4) {
-        const v4i d = mfma32(st.aq[g], b);
-        const int t = combine3(d[0], d[1], d[2]);
-        const uint32_t sz = comp(ksz[g], u);
-        // s * (acc - z * sum q_int) with s, z read from the packed pair
-        acc = sz_s_fma<BF>(sz, sz_nz_fma<BF>(sz, st.qs[g], (float)t), acc);
-      } else {
-        const int j = g * NG / 4;  // the slice's group
-        if (g % (4 / NG) == 0) dg[j] = mfma32(st.aq[g], b);
-        else dg[j] = mfma32acc(st.aq[g], b, dg[j]);
+#pragma unroll
+      for (int c = 0; c < NCH; ++c) {
+        if (NG == 4) {
+          const v4i d = mfma32(st[c].aq[g], b);
+          const int t = combine3(d[0], d[1], d[2]);
+          const uint32_t sz = comp(ksz[g], u);
+          // s * (acc - z * sum q_int) with s, z read from the packed pair
+          acc[c] = sz_s_fma<BF>(sz, sz_nz_fma<BF>(sz, st[c].qs[g], (float)t), acc[c]);
+        } else {
+          const int j = g * NG / 4;  // the slice's group
+          if (g % (4 / NG) == 0) dg[c][j] = mfma32(st[c].aq[g], b);
+          else dg[c][j] = mfma32acc(st[c].aq[g], b, dg[c][j]);
+        }
       }
     }
-    if (NG == 2) {  // 64 channels: |digit sums| <= 64 * 128 * 3, the combined sum < 2^31
 #pragma unroll
-      for (int j = 0; j < 2; ++j) {
-        const uint32_t sz = comp(ksz[j], u);
-        const int t = combine3(dg[j][0], dg[j][1], dg[j][2]);
-        acc = sz_s_fma<BF>(sz, sz_nz_fma<BF>(sz, st.qs[j], (float)t), acc);
+    for (int c = 0; c < NCH; ++c) {
+      if (NG == 2) {  // 64 channels: |digit sums| <= 64 * 128 * 3, the combined sum < 2^31
+#pragma unroll
+        for (int j = 0; j < 2; ++j) {
+          const uint32_t sz = comp(ksz[j], u);
+          const int t = combine3(dg[c][j][0], dg[c][j][1], dg[c][j][2]);
+          acc[c] = sz_s_fma<BF>(sz, sz_nz_fma<BF>(sz, st[c].qs[j], (float)t), acc[c]);
+        }
+      } else if (NG == 1) {
+        // 128 channels: the combined sum can exceed int32, so the digits are combined
+        // in fp32: 256 d_1 + d_2 is exact (< 2^24), and one rounding adds 65536 d_0
+        const uint32_t sz = comp(ksz[0], u);
+        const float T = fmaf((float)dg[c][0][0], 65536.0f, fmaf((float)dg[c][0][1], 256.0f, (float)dg[c][0][2]));
+        acc[c] = sz_s_fma<BF>(sz, sz_nz_fma<BF>(sz, st[c].qs[0], T), 0.0f);
       }
-    } else if (NG == 1) {
-      // 128 channels: the combined sum can exceed int32, so the digits are combined
-      // in fp32: 256 d_1 + d_2 is exact (< 2^24), and one rounding adds 65536 d_0
-      const uint32_t sz = comp(ksz[0], u);
-      const float T = fmaf((float)dg[0][0], 65536.0f, fmaf((float)dg[0][1], 256.0f, (float)dg[0][2]));
-      acc = sz_s_fma<BF>(sz, sz_nz_fma<BF>(sz, st.qs[0], T), 0.0f);
+      S[c][u] = acc[c];
     }
-    S[u] = acc;
   }
-  // ---- online softmax, head hi ----
-  auto valid = [&](int u) { return FULL || (4 * lo + u >= t0 && 4 * lo + u < t1); };
-  float mx = -INFINITY;
-#pragma unroll
-  for (int u = 0; u < 4; ++u)
-    if (valid(u)) mx = fmaxf(mx, S[u]);
-  mx = row16_max(mx) * st.sq;  // sq > 0; at least one valid token per page
-  const float mn = fmaxf(st.m, mx);
-  // alpha rescales the head's running sums (1 on the pages where the maximum
-  // stays, which is most of them; the multiplies are kept, as a wave-uniform skip
-  // would save about 1 % of the page's VALU)
-  const float alpha = ex2(st.m - mn);  // m = -inf on the first page -> 0
-  const float pmax = ex2(mx - mn);
-  float p[4];
-  float ls = 0.0f;
-#pragma unroll
-  for (int u = 0; u < 4; ++u) {
-    p[u] = valid(u) ? ex2(fmaf(st.sq, S[u], -mn)) : 0.0f;
-    ls += p[u];
-  }
-  st.lsum = fmaf(st.lsum, alpha, ls);
-  st.m = mn;
-  L.p[hi][lo] = make_float4(p[0], p[1], p[2], p[3]);
-  L.hs[hi] = make_float2(alpha, pmax);  // every lane of the row writes the same value
 
-  // ---- P.V weights w = p * s_v of (head lo>>2, group lo&3), tokens 16*hi + e ----
+  // ---- V scales of the weight layout, shared by the chunks ----
+  // lane (head wh = lo>>2, group wg = lo&3); their largest value on this page
   const int wh = lo >> 2, wg = lo & 3;
-  const float2 hsw = L.hs[wh];
-  float zp = 0.0f;
+  constexpr int NE = NG == 1 ? 4 : NG == 2 ? 8 : 16;  // tokens whose weights a lane forms
+  uint32_t sz[NE];
+  float svmax;
   if (NG == 1) {
     // one group per head: lane (head wh, quarter wg) forms the weights of tokens
     // 16*hi + 4*wg + (0..3), dword wg of the head's k-group hi operand (every lane
     // busy, a quarter of the work per lane of the per-group layout)
-    const float4 pw = L.p[wh][4 * hi + wg];
     const uint4 vz = *reinterpret_cast<const uint4*>(pb + kLdsVSz + 64 * hi + 16 * wg);
-    uint32_t sz[4];
 #pragma unroll
     for (int b = 0; b < 4; ++b) {
       const int tok = 16 * hi + 4 * wg + b;
@@ -363,38 +354,16 @@ __device__ inline void compute_page(WaveState& st, WaveLds& L, int t0, int t1, i
     }
     // largest V scale of the head on this page (bit patterns of positive scales)
     const uint32_t smax = max3_lo16(max3_lo16(sz[0], sz[1], sz[2]), sz[3], 0u);
-    const float svmax = rows_max(quad_max(BF ? __uint_as_float(smax << 16) : h_lo(smax)));
-    const float sig = hsw.y * svmax;
-    const float inv = sig > 0.0f ? kWMax * __builtin_amdgcn_rcpf(sig) : 0.0f;
-    L.ws[lo] = sig * (1.0f / kWMax);  // equal for the 16 lanes of head wh
-    uint32_t f[4];
-#pragma unroll
-    for (int b = 0; b < 4; ++b) {
-      const float w = sz_s_fma<BF>(sz[b], compf(pw, b), 0.0f);
-      f[b] = __float_as_uint(fmaf(w, inv, kMagic + kDigitBias));
-      zp = sz_z_fma<BF>(sz[b], w, zp);
-    }
-    const uint32_t t01 = __builtin_amdgcn_perm(f[1], f[0], 0x05010400u) ^ 0x80808080u;
-    const uint32_t t23 = __builtin_amdgcn_perm(f[3], f[2], 0x05010400u) ^ 0x80808080u;
-    const uint32_t h01 = __builtin_amdgcn_perm(f[1], f[0], 0x0c0c0602u);
-    const uint32_t h23 = __builtin_amdgcn_perm(f[3], f[2], 0x0c0c0602u);
-    char* wp = pb + 16 * (w_base(0) + w_slot(wh, hi)) + 4 * wg;
-    *reinterpret_cast<uint32_t*>(wp) = __builtin_amdgcn_perm(h23, h01, 0x05040100u);       // digit 0
-    *reinterpret_cast<uint32_t*>(wp + 16) = __builtin_amdgcn_perm(t23, t01, 0x07060302u);  // digit 1
-    *reinterpret_cast<uint32_t*>(wp + 32) = __builtin_amdgcn_perm(t23, t01, 0x05040100u);  // digit 2
+    svmax = rows_max(quad_max(BF ? __uint_as_float(smax << 16) : h_lo(smax)));
   } else if (NG == 2) {
     // two groups per head: lane (head wh, group wg & 1, half wg >> 1) forms the
     // weights of tokens 16*hi + 8*(wg >> 1) + (0..7) of its group, dwords
     // 2*(wg >> 1) + (0, 1) of the group's k-group hi operand
     const int gq = wg & 1, hf = wg >> 1;
-    float4 pw[2];
     uint4 vz[2];
 #pragma unroll
-    for (int j = 0; j < 2; ++j) {
-      pw[j] = L.p[wh][4 * hi + 2 * hf + j];
+    for (int j = 0; j < 2; ++j)
       vz[j] = *reinterpret_cast<const uint4*>(pb + kLdsVSz + 272 * gq + 64 * hi + 16 * (2 * hf + j));
-    }
-    uint32_t sz[8];
 #pragma unroll
     for (int e = 0; e < 8; ++e) {
       const int tok = 16 * hi + 8 * hf + e;
@@ -407,42 +376,12 @@ __device__ inline void compute_page(WaveState& st, WaveLds& L, int t0, int t1, i
                                     max3_lo16(sz[6], sz[7], 0u));
     float sv = BF ? __uint_as_float(smax << 16) : h_lo(smax);
     sv = fmaxf(sv, __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(sv), 0x4E, 0xF, 0xF, false)));
-    const float svmax = rows_max(sv);
-    const float sig = hsw.y * svmax;
-    const float inv = sig > 0.0f ? kWMax * __builtin_amdgcn_rcpf(sig) : 0.0f;
-    L.ws[lo] = sig * (1.0f / kWMax);  // lanes wg and wg ^ 2: group wg & 1 of head wh
-    uint32_t aw[kNDig][2];
-#pragma unroll
-    for (int j = 0; j < 2; ++j) {
-      uint32_t f[4];
-#pragma unroll
-      for (int b = 0; b < 4; ++b) {
-        const int e = 4 * j + b;
-        const float w = sz_s_fma<BF>(sz[e], compf(pw[j], b), 0.0f);
-        f[b] = __float_as_uint(fmaf(w, inv, kMagic + kDigitBias));
-        zp = sz_z_fma<BF>(sz[e], w, zp);
-      }
-      const uint32_t t01 = __builtin_amdgcn_perm(f[1], f[0], 0x05010400u) ^ 0x80808080u;
-      const uint32_t t23 = __builtin_amdgcn_perm(f[3], f[2], 0x05010400u) ^ 0x80808080u;
-      const uint32_t h01 = __builtin_amdgcn_perm(f[1], f[0], 0x0c0c0602u);
-      const uint32_t h23 = __builtin_amdgcn_perm(f[3], f[2], 0x0c0c0602u);
-      aw[2][j] = __builtin_amdgcn_perm(t23, t01, 0x05040100u);
-      aw[1][j] = __builtin_amdgcn_perm(t23, t01, 0x07060302u);
-      aw[0][j] = __builtin_amdgcn_perm(h23, h01, 0x05040100u);
-    }
-    char* wp = pb + 16 * (w_base(gq) + w_slot(wh, hi)) + 8 * hf;
-#pragma unroll
-    for (int dg = 0; dg < kNDig; ++dg)
-      *reinterpret_cast<uint2*>(wp + 16 * dg) = make_uint2(aw[dg][0], aw[dg][1]);
+    svmax = rows_max(sv);
   } else {
-    float4 pw[4];
     uint4 vz[4];
 #pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      pw[j] = L.p[wh][4 * hi + j];
+    for (int j = 0; j < 4; ++j)
       vz[j] = *reinterpret_cast<const uint4*>(pb + kLdsVSz + 272 * wg + 64 * hi + 16 * j);
-    }
-    uint32_t sz[16];
 #pragma unroll
     for (int e = 0; e < 16; ++e) {
       sz[e] = comp(vz[e >> 2], e & 3);
@@ -456,18 +395,55 @@ __device__ inline void compute_page(WaveState& st, WaveLds& L, int t0, int t1, i
     for (int e = 0; e < 5; ++e) m5[e] = max3_lo16(sz[3 * e], sz[3 * e + 1], sz[3 * e + 2]);
     m5[5] = sz[15];
     const uint32_t smax = max3_lo16(max3_lo16(m5[0], m5[1], m5[2]), max3_lo16(m5[3], m5[4], m5[5]), 0u);
-    const float svmax = rows_max(BF ? __uint_as_float(smax << 16) : h_lo(smax));
+    svmax = rows_max(BF ? __uint_as_float(smax << 16) : h_lo(smax));
+  }
+
+  // ---- per chunk: online softmax of head hi, then the P.V weights w = p * s_v of
+  // (head wh, group wg) as three int8 digit operands in the chunk's LDS area ----
+  auto valid = [&](int u) { return FULL || (4 * lo + u >= t0 && 4 * lo + u < t1); };
+  float alpha[NCH];
+#pragma unroll
+  for (int c = 0; c < NCH; ++c) {
+    float mx = -INFINITY;
+#pragma unroll
+    for (int u = 0; u < 4; ++u)
+      if (valid(u)) mx = fmaxf(mx, S[c][u]);
+    mx = row16_max(mx) * st[c].sq;  // sq > 0; at least one valid token per page
+    const float mn = fmaxf(st[c].m, mx);
+    // alpha rescales the head's running sums (1 on the pages where the maximum
+    // stays, which is most of them; the multiplies are kept, as a wave-uniform skip
+    // would save about 1 % of the page's VALU)
+    alpha[c] = ex2(st[c].m - mn);  // m = -inf on the first page -> 0
+    const float pmax = ex2(mx - mn);
+    float p[4];
+    float ls = 0.0f;
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      p[u] = valid(u) ? ex2(fmaf(st[c].sq, S[c][u], -mn)) : 0.0f;
+      ls += p[u];
+    }
+    st[c].lsum = fmaf(st[c].lsum, alpha[c], ls);
+    st[c].m = mn;
+    L.p[hi][lo] = make_float4(p[0], p[1], p[2], p[3]);
+    L.hs[hi] = make_float2(alpha[c], pmax);  // every lane of the row writes the same value
+
+    char* wbase = c == 0 ? pb : reinterpret_cast<char*>(L.wdig[c == 0 ? 0 : c - 1]);
+    const float2 hsw = L.hs[wh];
     const float sig = hsw.y * svmax;  // >= every w of the row on this page
     const float inv = sig > 0.0f ? kWMax * __builtin_amdgcn_rcpf(sig) : 0.0f;
-    L.ws[lo] = sig * (1.0f / kWMax);
-    uint32_t aw[kNDig][4];
+    float zp = 0.0f;
+    constexpr int NJ = NE / 4;  // dwords of digits per lane and digit row
+    uint32_t aw[kNDig][NJ];
 #pragma unroll
-    for (int j = 0; j < 4; ++j) {
+    for (int j = 0; j < NJ; ++j) {
+      // p of tokens 4*(4*hi + q) + (0..3): q = wg (NG 1), 2*(wg>>1) + j (NG 2), j (NG 4)
+      const int q = NG == 1 ? wg : NG == 2 ? 2 * (wg >> 1) + j : j;
+      const float4 pw = L.p[wh][4 * hi + q];
       uint32_t f[4];
 #pragma unroll
       for (int b = 0; b < 4; ++b) {
         const int e = 4 * j + b;
-        const float w = sz_s_fma<BF>(sz[e], compf(pw[j], b), 0.0f);
+        const float w = sz_s_fma<BF>(sz[e], compf(pw, b), 0.0f);
         // mantissa of rne(w * inv) + 2^23 + 32896 = k + 32896, k in [0, 2^21]:
         // k = 65536 d_0 + 256 d_1 + d_2 with d_2, d_1 = (bytes 0, 1) ^ 0x80, d_0 = byte 2
         f[b] = __float_as_uint(fmaf(w, inv, kMagic + kDigitBias));
@@ -481,37 +457,59 @@ __device__ inline void compute_page(WaveState& st, WaveLds& L, int t0, int t1, i
       aw[1][j] = __builtin_amdgcn_perm(t23, t01, 0x07060302u);
       aw[0][j] = __builtin_amdgcn_perm(h23, h01, 0x05040100u);
     }
-    {  // digit operands to LDS: group wg, rows 3*wh + digit, k-group hi
-      char* wp = pb + 16 * (w_base(wg) + w_slot(wh, hi));
+    if (NG == 1) {  // dword wg of the head's k-group hi operand
+      L.ws[c][lo] = sig * (1.0f / kWMax);  // equal for the 16 lanes of head wh
+      char* wp = wbase + 16 * (w_base(0) + w_slot(wh, hi)) + 4 * wg;
+#pragma unroll
+      for (int dg = 0; dg < kNDig; ++dg) *reinterpret_cast<uint32_t*>(wp + 16 * dg) = aw[dg][0];
+    } else if (NG == 2) {  // dwords 2*(wg>>1) + (0, 1) of group wg & 1
+      L.ws[c][lo] = sig * (1.0f / kWMax);  // lanes wg and wg ^ 2: group wg & 1 of head wh
+      char* wp = wbase + 16 * (w_base(wg & 1) + w_slot(wh, hi)) + 8 * (wg >> 1);
+#pragma unroll
+      for (int dg = 0; dg < kNDig; ++dg)
+        *reinterpret_cast<uint2*>(wp + 16 * dg) = make_uint2(aw[dg][0], aw[dg][1]);
+    } else {  // group wg, rows 3*wh + digit, k-group hi
+      L.ws[c][lo] = sig * (1.0f / kWMax);
+      char* wp = wbase + 16 * (w_base(wg) + w_slot(wh, hi));
 #pragma unroll
       for (int dg = 0; dg < kNDig; ++dg)
         *reinterpret_cast<uint4*>(wp + 16 * dg) = make_uint4(aw[dg][0], aw[dg][1], aw[dg][2], aw[dg][3]);
     }
+    st[c].zacc = fmaf(st[c].zacc, hsw.x, zp);
   }
-  st.zacc = fmaf(st.zacc, hsw.x, zp);
 
-  // ---- P.V on the matrix cores: lane (channel column, head hi) ----
-  const float4 ws = *reinterpret_cast<const float4*>(&L.ws[4 * hi]);
+  // ---- P.V on the matrix cores: lane (channel column, head hi), every chunk ----
   // B operand: field 2F + (lo>>3) of each token's byte, taken in place by the mask
   // mk = 3 << 2(lo>>3): columns lo >= 8 hold 4 x code (undone when the state is written)
   const uint32_t mk = 0x03030303u << (2 * (lo >> 3));
   // V codes of quad 8G + (lo&7), tokens 16*hi + (0..15)
   const char* vb = pb + kLdsVCodes + 16 * (4 * (lo & 7) + (hi ^ (((lo >> 2) & 1) << 1)));
   // A operand row (head lo>>2, digit lo&3); the padding digit row reads digit 2
-  const char* ab = pb + 16 * (w_slot(lo >> 2, hi) + min(lo & 3, 2));
+  const int arow = 16 * (w_slot(lo >> 2, hi) + min(lo & 3, 2));
+  float4 ws[NCH];
+#pragma unroll
+  for (int c = 0; c < NCH; ++c) ws[c] = *reinterpret_cast<const float4*>(&L.ws[c][4 * hi]);
 #pragma unroll
   for (int G = 0; G < 4; ++G) {
-    const uint4 a4 = *reinterpret_cast<const uint4*>(ab + 16 * w_base(G * NG / 4));  // its group's digits
-    const v4i aop = {(int)a4.x, (int)a4.y, (int)a4.z, (int)a4.w};
+    v4i aop[NCH];
+#pragma unroll
+    for (int c = 0; c < NCH; ++c) {
+      const char* wbase = c == 0 ? pb : reinterpret_cast<const char*>(L.wdig[c == 0 ? 0 : c - 1]);
+      const uint4 a4 = *reinterpret_cast<const uint4*>(wbase + arow + 16 * w_base(G * NG / 4));
+      aop[c] = v4i{(int)a4.x, (int)a4.y, (int)a4.z, (int)a4.w};
+    }
     const uint4 x = *reinterpret_cast<const uint4*>(vb + 512 * G);  // quad 8G + (lo&7)
 #pragma unroll
     for (int F = 0; F < 2; ++F) {
       const v4i bv = {(int)((x.x >> (4 * F)) & mk), (int)((x.y >> (4 * F)) & mk),
                       (int)((x.z >> (4 * F)) & mk), (int)((x.w >> (4 * F)) & mk)};
-      const v4i d = mfma64(aop, bv);
-      const int t = combine3(d[0], d[1], d[2]);
-      float& o = st.of[2 * G + F];
-      o = fmaf((float)t, compf(ws, G * NG / 4), o * alpha);
+#pragma unroll
+      for (int c = 0; c < NCH; ++c) {
+        const v4i d = mfma64(aop[c], bv);
+        const int t = combine3(d[0], d[1], d[2]);
+        float& o = st[c].of[2 * G + F];
+        o = fmaf((float)t, compf(ws[c], G * NG / 4), o * alpha[c]);
+      }
     }
   }
 }
@@ -539,10 +537,10 @@ __device__ inline TokRange tok_range(int lo, int hi) {
 // piece + 1 .. num_splits - 1 are marked empty.  The wave has done `done0` of its
 // `total` pages before this piece (issue-priority bands).  Without MIXED the
 // range starts at token 0 (R.t0 = 0).
-template <bool MIXED, bool BF, int NG, bool NT>
-__device__ __attribute__((always_inline)) inline void process_piece(WaveLds& L, const uint8_t* __restrict__ pages, int Hkv, int Hq,
+template <bool MIXED, bool BF, int NG, int NCH>
+__device__ __attribute__((always_inline)) inline void process_piece(WaveLds<NCH>& L, const uint8_t* __restrict__ pages, int Hkv, int Hq,
                                      const int32_t* __restrict__ block_table, int max_pages, int b,
-                                     TokRange R, int kvh, int chunk, int p0, int p1, int piece,
+                                     TokRange R, int kvh, int p0, int p1, int piece,
                                      bool last, int num_splits, int row_stride,
                                      const float* __restrict__ qt,
                                      float* __restrict__ part_o, float* __restrict__ part_ml,
@@ -554,11 +552,14 @@ __device__ __attribute__((always_inline)) inline void process_piece(WaveLds& L, 
   const uint8_t* __restrict__ base = pages + (size_t)kvh * block_bytes(NG);
   const size_t page_stride = (size_t)Hkv * block_bytes(NG);
 
-  WaveState st;
+  WaveState st[NCH];
   // ---- query operands: q_int = rne(q~ * Q / max|q~|), three int8 digits ----
   // Lane (head lo>>2, digit lo&3, k-group hi) holds, for group g, element e of
-  // the k-group: channel 32g + 16(hi>>1) + 4(e&3) + 2(hi&1) + (e>>2).
-  {
+  // the k-group: channel 32g + 16(hi>>1) + 4(e&3) + 2(hi&1) + (e>>2).  Chunk c
+  // holds query heads 4c .. 4c + 3 of the KV head.
+#pragma unroll
+  for (int chunk = 0; chunk < NCH; ++chunk) {
+    WaveState& sc = st[chunk];
     const int h = lo >> 2, dsel = lo & 3;
     const int hloc = 4 * chunk + h;
     float qv[4][8];
@@ -602,7 +603,7 @@ __device__ __attribute__((always_inline)) inline void process_piece(WaveLds& L, 
         const int dv = dsel == 0 ? d0 : dsel == 1 ? d1 : dsel == 2 ? d2 : 0;
         w[e >> 2] |= ((uint32_t)dv & 0xffu) << (8 * (e & 3));
       }
-      st.aq[g] = (long)((uint64_t)w[0] | ((uint64_t)w[1] << 32));
+      sc.aq[g] = (long)((uint64_t)w[0] | ((uint64_t)w[1] << 32));
       // sum over the group's 32 channels (k-groups hi), exact in int
       sum += __shfl_xor(sum, 16, 64);
       sum += __shfl_xor(sum, 32, 64);
@@ -612,20 +613,20 @@ __device__ __attribute__((always_inline)) inline void process_piece(WaveLds& L, 
     L.sq[h] = sq;  // lanes of equal h write equal values
     const int4 q4 = *reinterpret_cast<const int4*>(&L.qs[4 * hi]);
     if (NG == 4) {
-      st.qs[0] = (float)q4.x; st.qs[1] = (float)q4.y; st.qs[2] = (float)q4.z; st.qs[3] = (float)q4.w;
+      sc.qs[0] = (float)q4.x; sc.qs[1] = (float)q4.y; sc.qs[2] = (float)q4.z; sc.qs[3] = (float)q4.w;
     } else if (NG == 2) {  // sums over the group's slices, in int32 (|sum| < 2^31)
-      st.qs[0] = (float)(q4.x + q4.y); st.qs[1] = (float)(q4.z + q4.w);
-      st.qs[2] = st.qs[3] = 0.0f;
+      sc.qs[0] = (float)(q4.x + q4.y); sc.qs[1] = (float)(q4.z + q4.w);
+      sc.qs[2] = sc.qs[3] = 0.0f;
     } else {
-      st.qs[0] = (float)(q4.x + q4.y + q4.z + q4.w);
-      st.qs[1] = st.qs[2] = st.qs[3] = 0.0f;
+      sc.qs[0] = (float)(q4.x + q4.y + q4.z + q4.w);
+      sc.qs[1] = sc.qs[2] = sc.qs[3] = 0.0f;
     }
-    st.sq = L.sq[hi];
-    st.m = -INFINITY;
-    st.lsum = 0.0f;
-    st.zacc = 0.0f;
+    sc.sq = L.sq[hi];
+    sc.m = -INFINITY;
+    sc.lsum = 0.0f;
+    sc.zacc = 0.0f;
 #pragma unroll
-    for (int k = 0; k < 8; ++k) st.of[k] = 0.0f;
+    for (int k = 0; k < 8; ++k) sc.of[k] = 0.0f;
   }
 
   // Block-table entries of the split, 64 pages at a time: lane i holds the entry
@@ -633,14 +634,14 @@ __device__ __attribute__((always_inline)) inline void process_piece(WaveLds& L, 
   int cb = p0;
   int btv = (p0 + l < p1) ? bt[p0 + l] : 0;
   Stage sg;
-  if (p0 < p1) stage_load<NG, NT>(sg, base + (size_t)__builtin_amdgcn_readlane(btv, 0) * page_stride, l);
+  if (p0 < p1) stage_load<NG, true>(sg, base + (size_t)__builtin_amdgcn_readlane(btv, 0) * page_stride, l);
   // pages [p0, pf) are full; page pf (if < p1) is the range's partial last page
   int pf = (p0 < p1 && p1 == npg && R.t1 != kP) ? p1 - 1 : p1;
   int pg = p0;
   if (MIXED && p0 == 0 && p0 < p1 && R.t0 != 0) {  // the range's partial first page
     stage_store<NG>(L.page, sg, l);
-    stage_load<NG, NT>(sg, base + (size_t)__builtin_amdgcn_readlane(btv, min(1, p1 - 1)) * page_stride, l);
-    compute_page<false, BF, NG>(st, L, R.t0, npg == 1 ? R.t1 : kP, lo, hi);
+    stage_load<NG, true>(sg, base + (size_t)__builtin_amdgcn_readlane(btv, min(1, p1 - 1)) * page_stride, l);
+    compute_page<false, BF, NG, NCH>(st, L, R.t0, npg == 1 ? R.t1 : kP, lo, hi);
     pg = 1;
     pf = max(pf, 1);  // a one-page range is done
   }
@@ -659,8 +660,8 @@ __device__ __attribute__((always_inline)) inline void process_piece(WaveLds& L, 
         cb += 64;
         btv = (cb + l < p1) ? bt[cb + l] : 0;
       }
-      stage_load<NG, NT>(sg, base + (size_t)__builtin_amdgcn_readlane(btv, nx - cb) * page_stride, l);
-      compute_page<true, BF, NG>(st, L, 0, kP, lo, hi);
+      stage_load<NG, true>(sg, base + (size_t)__builtin_amdgcn_readlane(btv, nx - cb) * page_stride, l);
+      compute_page<true, BF, NG, NCH>(st, L, 0, kP, lo, hi);
     }
     if (band < 4 && lim > p0 && lim <= pf) {  // the band ended inside this piece
       if (band == 1) __builtin_amdgcn_s_setprio(2);
@@ -670,38 +671,42 @@ __device__ __attribute__((always_inline)) inline void process_piece(WaveLds& L, 
   }
   if (pf < p1) {  // the partial last page; the stage holds it
     stage_store<NG>(L.page, sg, l);
-    compute_page<false, BF, NG>(st, L, 0, R.t1, lo, hi);
+    compute_page<false, BF, NG, NCH>(st, L, 0, R.t1, lo, hi);
   }
 
-  // ---- write the split's partial state ----
-  const float ltot = row16_sum(st.lsum);  // head hi
-  float ztot = rows_sum(st.zacc);         // (head lo>>2, group lo&3)
-  if (NG == 1) ztot = quad_sum(ztot);     // the head's quarters: its one group
-  if (NG == 2)                            // the group's halves: lanes wg and wg ^ 2
-    ztot += __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(ztot), 0x4E, 0xF, 0xF, false));
-  L.ws[lo] = ztot;                        // lanes of equal lo write equal values
-  const float4 zh = *reinterpret_cast<const float4*>(&L.ws[4 * hi]);
-  const int hout = 4 * chunk + hi;        // head of this lane's accumulators
-  if (hout >= g_heads) return;            // padding head
-  const size_t row = ((size_t)b * Hq + kvh * g_heads + hout) * (MIXED ? row_stride : num_splits) + piece;
-  if (last && lo == 0)  // the range's last piece: the remaining slots hold nothing
-    for (int s2 = piece + 1; s2 < num_splits; ++s2) {
-      part_ml[(row + s2 - piece) * 2] = -INFINITY;
-      part_ml[(row + s2 - piece) * 2 + 1] = 0.0f;
-    }
-  const bool empty = st.m == -INFINITY;
-  const float cs = lo >= 8 ? 0.25f : 1.0f;  // P.V columns lo >= 8 accumulate 4 x code
+  // ---- write the split's partial state, per chunk ----
 #pragma unroll
-  for (int G = 0; G < 4; ++G) {
+  for (int chunk = 0; chunk < NCH; ++chunk) {
+    const WaveState& sc = st[chunk];
+    const float ltot = row16_sum(sc.lsum);  // head hi
+    float ztot = rows_sum(sc.zacc);         // (head lo>>2, group lo&3)
+    if (NG == 1) ztot = quad_sum(ztot);     // the head's quarters: its one group
+    if (NG == 2)                            // the group's halves: lanes wg and wg ^ 2
+      ztot += __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(ztot), 0x4E, 0xF, 0xF, false));
+    L.ws[0][lo] = ztot;                     // lanes of equal lo write equal values
+    const float4 zh = *reinterpret_cast<const float4*>(&L.ws[0][4 * hi]);
+    const int hout = 4 * chunk + hi;        // head of this lane's accumulators
+    if (hout >= g_heads) continue;          // padding head
+    const size_t row = ((size_t)b * Hq + kvh * g_heads + hout) * (MIXED ? row_stride : num_splits) + piece;
+    if (last && lo == 0)  // the range's last piece: the remaining slots hold nothing
+      for (int s2 = piece + 1; s2 < num_splits; ++s2) {
+        part_ml[(row + s2 - piece) * 2] = -INFINITY;
+        part_ml[(row + s2 - piece) * 2 + 1] = 0.0f;
+      }
+    const bool empty = sc.m == -INFINITY;
+    const float cs = lo >= 8 ? 0.25f : 1.0f;  // P.V columns lo >= 8 accumulate 4 x code
 #pragma unroll
-    for (int F = 0; F < 2; ++F) {
-      const int ch = 32 * G + 4 * (lo & 7) + 2 * F + (lo >> 3);
-      part_o[row * kD + ch] = empty ? 0.0f : fmaf(st.of[2 * G + F], cs, -compf(zh, G * NG / 4));
+    for (int G = 0; G < 4; ++G) {
+#pragma unroll
+      for (int F = 0; F < 2; ++F) {
+        const int ch = 32 * G + 4 * (lo & 7) + 2 * F + (lo >> 3);
+        part_o[row * kD + ch] = empty ? 0.0f : fmaf(sc.of[2 * G + F], cs, -compf(zh, G * NG / 4));
+      }
     }
-  }
-  if (lo == 0) {
-    part_ml[row * 2] = st.m;
-    part_ml[row * 2 + 1] = ltot;
+    if (lo == 0) {
+      part_ml[row * 2] = sc.m;
+      part_ml[row * 2 + 1] = ltot;
+    }
   }
 }
 
@@ -710,16 +715,20 @@ __device__ __attribute__((always_inline)) inline void process_piece(WaveLds& L, 
 // [r*pw, (r+1)*pw) with pw = max(ceil(T / n_ranges), ceil(max_pages / (S - 1)),
 // kMinRange), so every wave reads the same number of pages and a sequence is cut
 // into at most S pieces (piece = r - first range of the sequence).  Each range
-// runs one wave per (kv-head, chunk of query heads): the waves of a range read
-// the blocks of the same pages at the same time (each page's Hkv blocks are
-// contiguous).  With S = 1 each range is one whole sequence.  With MIXED a
-// sequence's pages are those of its INT2 history only, and a row's slots are
-// row_stride apart (the slots after the S history slots belong to other kernels).
-// Grid: ceil(n_ranges * Hkv / 8) * 8 * nch one-wave workgroups; workgroup id ->
-// (xcd = id % 8, slot = id / 8); chunk = slot % nch; u = (slot / nch) * 8 + xcd;
-// (range, kv-head) = (u / Hkv, u % Hkv): the chunks of one (range, kv-head)
-// share an XCD (and its L2) under round-robin dispatch.
+// runs one wave per kv-head, which handles all NCH chunks of 4 query heads of
+// that kv-head, so every page-head block is read by exactly one wave; the waves
+// of a range read the blocks of the same pages at the same time (each page's Hkv
+// blocks are contiguous).  With S = 1 each range is one whole sequence.  With
+// MIXED a sequence's pages are those of its INT2 history only, and a row's slots
+// are row_stride apart (the slots after the S history slots belong to other
+// kernels).  Grid: n_ranges * Hkv one-wave workgroups, workgroup u = (range u /
+// Hkv, kv-head u % Hkv).  Waves per SIMD: 4 for one chunk (128 VGPRs), 3 for two,
+// 2 for three or four (the chunks' softmax states and query operands).
 constexpr int kMinRange = 4;
+template <int NCH>
+struct SplitWaves {
+  static constexpr int per_simd = NCH == 1 ? 4 : NCH == 2 ? 3 : 2;
+};
 
 __device__ inline int wave_sum_i(int x) {
 #pragma unroll
@@ -727,19 +736,15 @@ __device__ inline int wave_sum_i(int x) {
   return x;
 }
 
-template <bool MIXED, bool BF, int NG, bool NT>
-__global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(4, 4))) void split_mfma_kernel(
+template <bool MIXED, bool BF, int NG, int NCH>
+__global__ __launch_bounds__(64) __attribute__((
+    amdgpu_waves_per_eu(SplitWaves<NCH>::per_simd, SplitWaves<NCH>::per_simd))) void split_mfma_kernel(
     const uint8_t* __restrict__ pages, int Hkv, int Hq, const int32_t* __restrict__ block_table,
     int max_pages, const int32_t* __restrict__ seq_lens, int num_splits, int n_ranges, int B,
     const float* __restrict__ qt, float* __restrict__ part_o, float* __restrict__ part_ml,
     int S0, int W, int row_stride) {
-  __shared__ WaveLds L;
-  const int g_heads = Hq / Hkv;
-  const int nch = (g_heads + 3) >> 2;
-  const int xcd = blockIdx.x & 7;
-  const int slot = blockIdx.x >> 3;
-  const int chunk = slot % nch;
-  const int64_t u = (int64_t)(slot / nch) * 8 + xcd;
+  __shared__ WaveLds<NCH> L;
+  const int64_t u = blockIdx.x;
   if (u >= (int64_t)n_ranges * Hkv) return;
   const int r = (int)(u / Hkv), kvh = (int)(u % Hkv);
   const int l = threadIdx.x;
@@ -755,7 +760,7 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(4, 4))) void
   };
   if (num_splits == 1) {  // one range per sequence
     const TokRange R = range_of(r);
-    process_piece<MIXED, BF, NG, NT>(L, pages, Hkv, Hq, block_table, max_pages, r, R, kvh, chunk, 0, R.npg,
+    process_piece<MIXED, BF, NG, NCH>(L, pages, Hkv, Hq, block_table, max_pages, r, R, kvh, 0, R.npg,
                          0, true, 1, stride, qt, part_o, part_ml, 0, 1 << 20);
     return;
   }
@@ -772,7 +777,7 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(4, 4))) void
   const int64_t xe = min(T, x + pw);
   // a sequence with no pages gets empty slots from the (range b mod n_ranges,
   // kv-head 0, chunk 0) wave, for all its heads
-  if (kvh == 0 && chunk == 0)
+  if (kvh == 0)
     for (int bb = r; bb < B; bb += n_ranges)
       if (range_of(bb).npg == 0)
         for (int i = l; i < Hq * num_splits; i += 64) {
@@ -810,7 +815,7 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(4, 4))) void
   while (true) {
     const int64_t end = min(xe, before + npg_b);
     const int piece = (int)(r - before / pw);
-    process_piece<MIXED, BF, NG, NT>(L, pages, Hkv, Hq, block_table, max_pages, b, range_of(b), kvh, chunk,
+    process_piece<MIXED, BF, NG, NCH>(L, pages, Hkv, Hq, block_table, max_pages, b, range_of(b), kvh,
                          (int)(x - before), (int)(end - before), piece, end == before + npg_b,
                          num_splits, stride, qt, part_o, part_ml, (int)(x - x0), (int)(xe - x0));
     x = end;
@@ -827,16 +832,16 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(4, 4))) void
 
 hipError_t launch_decode_split_mfma(const uint8_t* pages, int Hkv, int B, int Hq,
                                     const int32_t* block_table, int max_pages,
-                                    const int32_t* seq_lens, int num_splits, int resident_waves,
+                                    const int32_t* seq_lens, int num_splits, int cus,
                                     const float* qt, float* part_o, float* part_ml,
                                     hipStream_t st, int meta_bf16, int ng,
                                     const MixedSpec* mixed) {
-  const int g = Hq / Hkv;
-  const int nch = (g + 3) / 4;
-  // one range per resident wave group (each range runs Hkv * nch waves)
+  const int nch = split_chunks(Hq / Hkv);
+  // one range per resident group of Hkv waves
   const int64_t ranges =
-      num_splits == 1 ? (int64_t)B : std::max<int64_t>(1, resident_waves / (nch * Hkv));
-  const int64_t blocks = (ranges * Hkv + 7) / 8 * 8 * nch;
+      num_splits == 1 ? (int64_t)B
+                      : std::max<int64_t>(1, (int64_t)split_waves_per_cu(nch) * cus / Hkv);
+  const int64_t blocks = ranges * Hkv;
   if (blocks > 0x7fffffffLL) return hipErrorInvalidConfiguration;
   const int S0 = mixed ? mixed->S0 : 0, W = mixed ? mixed->W : 0;
   const int stride = mixed ? mixed->row_stride : num_splits;
@@ -845,17 +850,18 @@ hipError_t launch_decode_split_mfma(const uint8_t* pages, int Hkv, int B, int Hq
                        block_table, max_pages, seq_lens, num_splits, (int)ranges, B, qt, part_o,
                        part_ml, S0, W, stride);
   };
-  // one wave per page-head block (at most 4 query heads per KV head): streamed
-  auto by_nt = [&](auto mixed_c, auto bf_c, auto ng_c) {
+  auto by_nch = [&](auto mixed_c, auto bf_c, auto ng_c) {
     constexpr bool M = decltype(mixed_c)::value, BFV = decltype(bf_c)::value;
     constexpr int NGV = decltype(ng_c)::value;
-    if (nch == 1) go(split_mfma_kernel<M, BFV, NGV, true>);
-    else go(split_mfma_kernel<M, BFV, NGV, false>);
+    if (nch == 1) go(split_mfma_kernel<M, BFV, NGV, 1>);
+    else if (nch == 2) go(split_mfma_kernel<M, BFV, NGV, 2>);
+    else if (nch == 3) go(split_mfma_kernel<M, BFV, NGV, 3>);
+    else go(split_mfma_kernel<M, BFV, NGV, 4>);
   };
   auto by_ng = [&](auto mixed_c, auto bf_c) {
-    if (ng == 4) by_nt(mixed_c, bf_c, std::integral_constant<int, 4>{});
-    else if (ng == 2) by_nt(mixed_c, bf_c, std::integral_constant<int, 2>{});
-    else by_nt(mixed_c, bf_c, std::integral_constant<int, 1>{});
+    if (ng == 4) by_nch(mixed_c, bf_c, std::integral_constant<int, 4>{});
+    else if (ng == 2) by_nch(mixed_c, bf_c, std::integral_constant<int, 2>{});
+    else by_nch(mixed_c, bf_c, std::integral_constant<int, 1>{});
   };
   using T = std::true_type;
   using F = std::false_type;

@@ -22,6 +22,11 @@ __host__ __device__ constexpr int off_vsz(int ng) { return kOffKSz + sz_bytes(ng
 __host__ __device__ constexpr int block_bytes(int ng) { return 2 * kCodeBytes + 2 * sz_bytes(ng); }
 constexpr int kMaxGroupHeads = 16;                 // query heads per kv-head
 
+// Split kernel geometry: a wave handles all query heads of its kv-head in chunks
+// of 4, and the number of chunks sets its registers, hence the waves per CU.
+inline int split_chunks(int heads_per_kv) { return (heads_per_kv + 3) / 4; }
+inline int split_waves_per_cu(int nch) { return nch == 1 ? 16 : nch == 2 ? 12 : 8; }
+
 // Workspace carving for decode (byte offsets, 256-aligned).
 struct DecodeWs {
   size_t qt_off, po_off, pml_off, total;
@@ -118,11 +123,11 @@ hipError_t launch_decode_split(const uint8_t* pages, int Hkv, int B, int Hq,
                                const int32_t* seq_lens, int num_splits, const float* qt,
                                float* part_o, float* part_ml, hipStream_t st, int meta_bf16,
                                int ng, const MixedSpec* mixed = nullptr);
-// Balanced split kernel: `resident_waves` waves share the pages equally; a
-// (sequence, head) row gets at most num_splits partial states.
+// Balanced split kernel: split_waves_per_cu(chunks) * cus resident waves share
+// the pages equally; a (sequence, head) row gets at most num_splits partial states.
 hipError_t launch_decode_split_mfma(const uint8_t* pages, int Hkv, int B, int Hq,
                                     const int32_t* block_table, int max_pages,
-                                    const int32_t* seq_lens, int num_splits, int resident_waves,
+                                    const int32_t* seq_lens, int num_splits, int cus,
                                     const float* qt, float* part_o, float* part_ml,
                                     hipStream_t st, int meta_bf16, int ng,
                                     const MixedSpec* mixed);

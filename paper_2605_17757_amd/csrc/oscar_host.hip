@@ -198,13 +198,15 @@ int32_t oscar_default_num_splits(const oscar_layout* L, int32_t B, int32_t Hq,
   if (check_layout(L) != OSCAR_OK || B < 1 || Hq < 1 || max_seq_len < 1) return 1;
   const int64_t pages = (max_seq_len + L->page_size - 1) / L->page_size;
   if (pages < 4) return 1;
-  // The split kernel gives each of its ~16 waves per CU an equal share of all
-  // pages (ranges of >= 4 pages); a (sequence, head) row is cut into at most
-  // num_splits pieces.  Assuming sequences average half the longest, the range
-  // is ~B * Hkv * pages / 2 / waves pages; allow one more piece than the longest
-  // sequence needs at that range.
-  const int64_t chunks = (Hq % L->num_kv_heads == 0) ? (Hq / L->num_kv_heads + 3) / 4 : 1;
-  const int64_t ranges = std::max<int64_t>(1, 16LL * device_cus() / (chunks * L->num_kv_heads));
+  // The split kernel gives each of its resident waves (8 to 16 per CU, by the
+  // query heads per kv-head) an equal share of all pages (ranges of >= 4 pages);
+  // a (sequence, head) row is cut into at most num_splits pieces.  Assuming
+  // sequences average half the longest, the range is ~B * Hkv * pages / 2 /
+  // waves pages; allow one more piece than the longest sequence needs at that
+  // range.
+  const int chunks = (Hq % L->num_kv_heads == 0) ? split_chunks(Hq / L->num_kv_heads) : 1;
+  const int64_t ranges = std::max<int64_t>(
+      1, (int64_t)split_waves_per_cu(chunks) * device_cus() / L->num_kv_heads);
   int64_t range = ((int64_t)B * pages / 2 + ranges - 1) / ranges;
   if (range < 4) range = 4;
   int64_t s = (pages + range - 1) / range + 1;
