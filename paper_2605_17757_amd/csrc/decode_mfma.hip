@@ -135,6 +135,14 @@ __device__ inline float sz_nz_fma(uint32_t h, float b, float c) {  // -z * b + c
   return BF ? fmaf(-__uint_as_float(h & 0xffff0000u), b, c) : mix_nhi(h, b, c);
 }
 
+// s * b + c with s read from a packed (scale, zero) word, in plain C (v_fma_mix_f32
+// for binary16): for operands that come straight from an MFMA, whose read-after-
+// write wait states the compiler inserts only before instructions it knows.
+template <bool BF>
+__device__ inline float sz_s_fma_c(uint32_t h, float b, float c) {
+  return fmaf(BF ? __uint_as_float(h << 16) : __half2float(__ushort_as_half((uint16_t)(h & 0xffffu))), b, c);
+}
+
 // unsigned maximum of the low halves of three words (high half of the result unused)
 __device__ inline uint32_t max3_lo16(uint32_t a, uint32_t b, uint32_t c) {
   uint32_t r;
@@ -170,6 +178,62 @@ __device__ inline float quad_sum(float x) {
   x += __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(x), 0xB1, 0xF, 0xF, false));
   x += __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(x), 0x4E, 0xF, 0xF, false));
   return x;
+}
+// Max over the 16 lanes of a row for four values at once: v_max_f32 with DPP
+// operands (quad swaps, then row rotations by 4 and 8), the four chains
+// interleaved so that every DPP read is 3 instructions after the write it reads
+// (2 wait states required; the leading s_nop covers the inputs' writes).
+__device__ inline void row16_max4(float& a, float& b, float& c, float& d) {
+  asm volatile(
+      "s_nop 1\n"
+      "v_max_f32_dpp %0, %0, %0 quad_perm:[1,0,3,2] row_mask:0xf bank_mask:0xf\n"
+      "v_max_f32_dpp %1, %1, %1 quad_perm:[1,0,3,2] row_mask:0xf bank_mask:0xf\n"
+      "v_max_f32_dpp %2, %2, %2 quad_perm:[1,0,3,2] row_mask:0xf bank_mask:0xf\n"
+      "v_max_f32_dpp %3, %3, %3 quad_perm:[1,0,3,2] row_mask:0xf bank_mask:0xf\n"
+      "v_max_f32_dpp %0, %0, %0 quad_perm:[2,3,0,1] row_mask:0xf bank_mask:0xf\n"
+      "v_max_f32_dpp %1, %1, %1 quad_perm:[2,3,0,1] row_mask:0xf bank_mask:0xf\n"
+      "v_max_f32_dpp %2, %2, %2 quad_perm:[2,3,0,1] row_mask:0xf bank_mask:0xf\n"
+      "v_max_f32_dpp %3, %3, %3 quad_perm:[2,3,0,1] row_mask:0xf bank_mask:0xf\n"
+      "v_max_f32_dpp %0, %0, %0 row_ror:4 row_mask:0xf bank_mask:0xf\n"
+      "v_max_f32_dpp %1, %1, %1 row_ror:4 row_mask:0xf bank_mask:0xf\n"
+      "v_max_f32_dpp %2, %2, %2 row_ror:4 row_mask:0xf bank_mask:0xf\n"
+      "v_max_f32_dpp %3, %3, %3 row_ror:4 row_mask:0xf bank_mask:0xf\n"
+      "v_max_f32_dpp %0, %0, %0 row_ror:8 row_mask:0xf bank_mask:0xf\n"
+      "v_max_f32_dpp %1, %1, %1 row_ror:8 row_mask:0xf bank_mask:0xf\n"
+      "v_max_f32_dpp %2, %2, %2 row_ror:8 row_mask:0xf bank_mask:0xf\n"
+      "v_max_f32_dpp %3, %3, %3 row_ror:8 row_mask:0xf bank_mask:0xf\n"
+      : "+v"(a), "+v"(b), "+v"(c), "+v"(d));
+}
+// The same for two values (s_nop between the dependent pairs).
+__device__ inline void row16_max2(float& a, float& b) {
+  asm volatile(
+      "s_nop 1\n"
+      "v_max_f32_dpp %0, %0, %0 quad_perm:[1,0,3,2] row_mask:0xf bank_mask:0xf\n"
+      "v_max_f32_dpp %1, %1, %1 quad_perm:[1,0,3,2] row_mask:0xf bank_mask:0xf\n"
+      "s_nop 0\n"
+      "v_max_f32_dpp %0, %0, %0 quad_perm:[2,3,0,1] row_mask:0xf bank_mask:0xf\n"
+      "v_max_f32_dpp %1, %1, %1 quad_perm:[2,3,0,1] row_mask:0xf bank_mask:0xf\n"
+      "s_nop 0\n"
+      "v_max_f32_dpp %0, %0, %0 row_ror:4 row_mask:0xf bank_mask:0xf\n"
+      "v_max_f32_dpp %1, %1, %1 row_ror:4 row_mask:0xf bank_mask:0xf\n"
+      "s_nop 0\n"
+      "v_max_f32_dpp %0, %0, %0 row_ror:8 row_mask:0xf bank_mask:0xf\n"
+      "v_max_f32_dpp %1, %1, %1 row_ror:8 row_mask:0xf bank_mask:0xf\n"
+      : "+v"(a), "+v"(b));
+}
+// The same for one value (s_nop between the dependent steps).
+__device__ inline float row16_max1(float a) {
+  asm volatile(
+      "s_nop 1\n"
+      "v_max_f32_dpp %0, %0, %0 quad_perm:[1,0,3,2] row_mask:0xf bank_mask:0xf\n"
+      "s_nop 1\n"
+      "v_max_f32_dpp %0, %0, %0 quad_perm:[2,3,0,1] row_mask:0xf bank_mask:0xf\n"
+      "s_nop 1\n"
+      "v_max_f32_dpp %0, %0, %0 row_ror:4 row_mask:0xf bank_mask:0xf\n"
+      "s_nop 1\n"
+      "v_max_f32_dpp %0, %0, %0 row_ror:8 row_mask:0xf bank_mask:0xf\n"
+      : "+v"(a));
+  return a;
 }
 // Reductions over lanes l, l^16, l^32, l^48 with the gfx950 row-swap permutes:
 // swapping a value with itself across the wave halves / odd-even rows leaves
@@ -514,6 +578,407 @@ __device__ inline void compute_page(WaveState (&st)[NCH], WaveLds<NCH>& L, int t
   }
 }
 
+// ---------------------------------------------------------------------------
+// Wide instances (5 to 16 query heads per kv-head).  The scores of all the
+// kv-head's query heads come from one set of fp16 MFMAs, so the per-(token, head,
+// group) work after them is one scale FMA (two with 8 heads, below); the P.V
+// products stay on the int8 MFMAs in chunks of 4 heads (as above).  Up to 8
+// heads (RPH = 2 rows per head) the hi and lo halves of q~ are two MFMA rows of
+// the head (row lo: head lo>>1, half lo&1), one MFMA per slice and tile, and
+// the lane's D registers hold heads 2hi + (i>>1) whose halves add up; from 9
+// heads (RPH = 1) a row is a head and the halves are two chained MFMAs.
+//
+// v_mfma_f32_16x16x32_f16: A row = head lo, k-slots 8*hi + e; B column lo,
+// k-slots 8*hi + e; D lane l, register i = (head 4*hi + i, column lo).  A K code
+// enters B as a binary16 subnormal: its two bits, masked in place at field j of
+// a byte (bits c * 4^j), are the value c * 4^j * 2^-24, exactly.  The A side
+// holds q~ * E / 4^j as a hi + lo pair of binary16 values (E a power of two per
+// head that puts max|q~| * E in [2^14, 2^15)), so every product is exactly
+// q~ * c * E * 2^-24 and a slice's sum is exact up to the fp32 accumulation.
+// Token tile u: column lo is token 4*lo + u.  Slice g (32 channels), k-group hi:
+// the codes of bytes A = 8g + 2hi and A + 1 of the token (channels 32g + 8hi + f
+// and 32g + 8hi + 4 + f for field f), Y = byte A | byte (A + 1) << 16 and
+// P_f = Y & (0x00030003 << 2f); B dwords (P_0, P_1, P_2, P_3), so k-slot e is
+// field e>>1 of byte A (e even) or A + 1 (e odd).  Two chained MFMAs per slice
+// and tile take the hi and the lo halves of q~ against the same B.  The
+// zero-point term sum_g s_g z_g Q_g(h) of a tile is one fp32
+// MFMA (16x16x4: A row = head, k = group: Q_g E 2^-24; B k = group, column =
+// token: s_g z_g, exact in fp32) that seeds the sum of the scaled slices.
+//
+// Softmax per page: p' = 2^(score - page max + 21 - e), with svmax < 2^e the
+// largest V scale of the page, so that every weight s_v p' lies in [0, 2^21]
+// and is quantized as it is (no per-(head, group) rescale).  The true weight is
+// p' s_v ws, ws = 2^(page max - m - 21 + e), with m a reference maximum per head
+// that only moves when a page's maximum exceeds it by more than kSlack (sums
+// relative to m then stay below 2^kSlack times their true size; the running
+// sums are rescaled only on those pages).
+constexpr float kSlack = 10.0f;
+
+typedef _Float16 h8 __attribute__((ext_vector_type(8)));
+typedef float f4v __attribute__((ext_vector_type(4)));
+
+__device__ inline f4v mfma_h(u4 a, u4 b, f4v c) {
+  return __builtin_amdgcn_mfma_f32_16x16x32_f16(__builtin_bit_cast(h8, a), __builtin_bit_cast(h8, b), c,
+                                                0, 0, 0);
+}
+__device__ inline f4v mfma_f(float a, float b) {
+  const f4v z = {0.0f, 0.0f, 0.0f, 0.0f};
+  return __builtin_amdgcn_mfma_f32_16x16x4f32(a, b, z, 0, 0, 0);
+}
+// s * z of a packed (scale, zero) word (exact in fp32), in plain C like every
+// operation next to the wide path's MFMAs: the compiler inserts the MFMA
+// read/write wait states only around instructions it sees, not inline asm.
+template <bool BF>
+__device__ inline float sz_prod(uint32_t h) {
+  if (BF) return __uint_as_float(h << 16) * __uint_as_float(h & 0xffff0000u);
+  return fmaf(__half2float(__ushort_as_half((uint16_t)(h & 0xffffu))),
+              __half2float(__ushort_as_half((uint16_t)(h >> 16))), 0.0f);
+}
+
+// p' of a page for the chunks' weight lanes: [head][token / 4] float4, pitch 17.
+// Up to 12 heads it lies over the page's K area (spent once the scores are done).
+template <int NCH>
+struct WideLdsX {};
+template <>
+struct WideLdsX<4> {
+  uint4 pqx[16 * 17];
+};
+template <int NCH>
+struct WideLds : WideLdsX<NCH> {
+  uint4 page[kSlots];            // page-head block (slot placement above)
+  uint4 wdig[NCH][kWSlots];      // weight digits of each chunk
+  float2 hs[16];                 // per head on this page: (PV scale ws, rescale factor)
+};
+template <int NCH>
+__device__ inline float4* wide_pq(WideLds<NCH>& L) {
+  if constexpr (NCH == 4) return reinterpret_cast<float4*>(L.pqx);
+  else return reinterpret_cast<float4*>(L.page);
+}
+
+template <int NCH>
+struct WideRows {
+  static constexpr int RPH = NCH <= 2 ? 2 : 1;  // MFMA rows per head
+  static constexpr int HPL = 4 / RPH;           // heads per lane in the score layout
+};
+template <int NCH>
+struct WideState {
+  static constexpr int RPH = WideRows<NCH>::RPH, HPL = WideRows<NCH>::HPL;
+  u4 aq[4][3 - RPH]; // score A operands: slice g; RPH 1: hi (0) / lo (1) halves of head lo;
+                     // RPH 2: the half lo&1 of head lo>>1 (k-group hi)
+  float az;          // zero-point MFMA A operand of row lo, group hi: E 2^-24 sum of q~
+  float sq[HPL];     // 2^24 / E of head HPL hi + j (log2 units per accumulated score)
+  float m[HPL];      // reference maximum (log2 units) of head HPL hi + j
+  float lsum[HPL];   // partial sum of p relative to m over this lane's tokens, head HPL hi + j
+  float zacc[NCH];   // partial sum of w z_v of (head 4c + (lo>>2), group lo&3)
+  float of[NCH][8];  // unnormalized o~ of head 4c + hi, tile (G, F) at of[c][2G + F]
+};
+
+template <bool FULL, bool BF, int NG, int NCH>
+__device__ inline void compute_page_wide(WideState<NCH>& st, WideLds<NCH>& L, int t0, int t1, int lo,
+                                         int hi) {
+  char* pb = reinterpret_cast<char*>(L.page);
+  const int l = threadIdx.x & 63;
+  __builtin_assume(hi >= 0 && hi < 4);
+  __builtin_assume(lo >= 0 && lo < 16);
+  auto valid = [&](int u) { return FULL || (4 * lo + u >= t0 && 4 * lo + u < t1); };
+
+  // ---- largest V scale of the page over its valid tokens: lane l < 16 NG reads V
+  // (s, z) chunk l (tokens 4(l&15) + b of group l>>4) ----
+  int esv;
+  {
+    uint32_t mloc = 0u;
+    if (NG == 4 || l < 16 * NG) {
+      const uint4 w = *reinterpret_cast<const uint4*>(pb + kLdsVSz + 16 * (l + (l >> 4)));
+      uint32_t x[4] = {w.x, w.y, w.z, w.w};
+#pragma unroll
+      for (int b = 0; b < 4; ++b)
+        if (!FULL && (4 * (l & 15) + b < t0 || 4 * (l & 15) + b >= t1)) x[b] = 0u;
+      mloc = max(max(x[0] & 0xffffu, x[1] & 0xffffu), max(x[2] & 0xffffu, x[3] & 0xffffu));
+    }
+    const float sv = rows_max(row16_max1(BF ? __uint_as_float(mloc << 16) : h_lo(mloc)));
+    frexpf(sv, &esv);  // sv < 2^esv
+  }
+  const float cw = (float)(21 - esv);
+
+  // ---- scores of heads 4hi + i for tokens 4lo + u ----
+  const uint32_t* kc = reinterpret_cast<const uint32_t*>(pb + kLdsKCodes + 144 * lo + 4 * (hi >> 1));
+  const uint32_t sel = (hi & 1) ? 0x0C030C02u : 0x0C010C00u;  // bytes 2(hi&1), +1 to the two halves
+  constexpr int RPH = WideRows<NCH>::RPH, HPL = WideRows<NCH>::HPL;
+  // zero-point terms of the tiles: dz[u] = sum_g Q_g s_g z_g (B: group hi of token 4lo + u)
+  f4v dz[4];
+  {
+    const uint4 kszb = *reinterpret_cast<const uint4*>(pb + kLdsKSz + 256 * (hi < NG ? hi : 0) + 16 * lo);
+#pragma unroll
+    for (int u = 0; u < 4; ++u) dz[u] = mfma_f(st.az, hi < NG ? sz_prod<BF>(comp(kszb, u)) : 0.0f);
+  }
+  // slices g (outer) for the four token tiles; a group's slices chain in the MFMA
+  // accumulator and its scale is applied after the last one
+  float acc[4][HPL];
+  f4v d[4];
+#pragma unroll
+  for (int g = 0; g < 4; ++g) {
+    const bool first = (g % (4 / NG)) == 0, lastg = (g + 1) % (4 / NG) == 0;
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      const uint32_t D = kc[8 * u + 2 * g];
+      const uint32_t Y = __builtin_amdgcn_perm(D, D, sel);
+      const u4 bk = {Y & 0x00030003u, Y & 0x000C000Cu, Y & 0x00300030u, Y & 0x00C000C0u};
+      const f4v zero = {0.0f, 0.0f, 0.0f, 0.0f};
+      d[u] = mfma_h(st.aq[g][0], bk, first ? zero : d[u]);
+      if (RPH == 1) d[u] = mfma_h(st.aq[g][1], bk, d[u]);
+    }
+    if (lastg) {  // (s, z) of tokens 4lo + (0..3) of the group
+      const uint4 kg = *reinterpret_cast<const uint4*>(pb + kLdsKSz + 256 * (g * NG / 4) + 16 * lo);
+#pragma unroll
+      for (int u = 0; u < 4; ++u)
+#pragma unroll
+        for (int j = 0; j < HPL; ++j) {
+          const float x = RPH == 1 ? d[u][j] : d[u][2 * j] + d[u][2 * j + 1];
+          acc[u][j] = sz_s_fma_c<BF>(comp(kg, u), x, g + 1 == 4 / NG ? -dz[u][RPH * j] : acc[u][j]);
+        }
+    }
+  }
+
+  // ---- online softmax of heads HPL hi + j ----
+  float mx[HPL];
+#pragma unroll
+  for (int j = 0; j < HPL; ++j) {
+    float x = -INFINITY;
+#pragma unroll
+    for (int u = 0; u < 4; ++u)
+      if (valid(u)) x = fmaxf(x, acc[u][j]);
+    mx[j] = x;
+  }
+  if (HPL == 4) row16_max4(mx[0], mx[HPL > 1 ? 1 : 0], mx[HPL > 2 ? 2 : 0], mx[HPL > 3 ? 3 : 0]);
+  else row16_max2(mx[0], mx[HPL > 1 ? 1 : 0]);  // at least one valid token per page
+  bool need = false;
+#pragma unroll
+  for (int j = 0; j < HPL; ++j) {
+    mx[j] *= st.sq[j];
+    need = need || !(mx[j] <= st.m[j] + kSlack);
+  }
+  const bool resc = __ballot(need) != 0ull;  // wave-uniform
+  float alpha[HPL];
+#pragma unroll
+  for (int j = 0; j < HPL; ++j) alpha[j] = 1.0f;
+  if (resc) {
+#pragma unroll
+    for (int j = 0; j < HPL; ++j) {
+      const float mn = fmaxf(st.m[j], mx[j]);
+      alpha[j] = ex2(st.m[j] - mn);  // m = -inf on the first page -> 0
+      st.m[j] = mn;
+      st.lsum[j] *= alpha[j];
+    }
+  }
+  float4* pq = wide_pq(L);
+#pragma unroll
+  for (int j = 0; j < HPL; ++j) {
+    const int hh = HPL * hi + j;
+    const float c = cw - mx[j];
+    const float ws = ex2(mx[j] - st.m[j] - cw);
+    float pv[4];
+    float ls = 0.0f;
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      pv[u] = valid(u) ? ex2(fmaf(st.sq[j], acc[u][j], c)) : 0.0f;
+      ls += pv[u];
+    }
+    st.lsum[j] = fmaf(ls, ws, st.lsum[j]);
+    if (hh < 4 * NCH) {
+      pq[hh * 17 + lo] = make_float4(pv[0], pv[1], pv[2], pv[3]);
+      if (lo == 0) L.hs[hh] = make_float2(ws, alpha[j]);
+    }
+  }
+
+  const int wh = lo >> 2, wg = lo & 3;
+  if constexpr (NCH >= 3) {
+  // ---- per chunk: the P.V weights w' = s_v p' of (head 4c + wh, group wg) as three
+  // int8 digit operands in the chunk's LDS area ----
+  constexpr int NE = NG == 1 ? 4 : NG == 2 ? 8 : 16;  // tokens whose weights a lane forms
+  uint32_t sz[NE];
+  if (NG == 1) {  // lane (head wh, quarter wg): tokens 16*hi + 4*wg + (0..3)
+    const uint4 vz = *reinterpret_cast<const uint4*>(pb + kLdsVSz + 64 * hi + 16 * wg);
+#pragma unroll
+    for (int b = 0; b < 4; ++b) {
+      const int tok = 16 * hi + 4 * wg + b;
+      sz[b] = comp(vz, b);
+      if (!FULL && (tok < t0 || tok >= t1)) sz[b] = 0u;
+    }
+  } else if (NG == 2) {  // lane (head wh, group wg & 1, half wg >> 1): tokens 16*hi + 8*(wg >> 1) + (0..7)
+    const int gq = wg & 1, hf = wg >> 1;
+#pragma unroll
+    for (int j = 0; j < 2; ++j) {
+      const uint4 vz = *reinterpret_cast<const uint4*>(pb + kLdsVSz + 272 * gq + 64 * hi + 16 * (2 * hf + j));
+#pragma unroll
+      for (int b = 0; b < 4; ++b) {
+        const int tok = 16 * hi + 8 * hf + 4 * j + b;
+        sz[4 * j + b] = comp(vz, b);
+        if (!FULL && (tok < t0 || tok >= t1)) sz[4 * j + b] = 0u;
+      }
+    }
+  } else {  // lane (head wh, group wg): tokens 16*hi + (0..15)
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const uint4 vz = *reinterpret_cast<const uint4*>(pb + kLdsVSz + 272 * wg + 64 * hi + 16 * j);
+#pragma unroll
+      for (int b = 0; b < 4; ++b) {
+        sz[4 * j + b] = comp(vz, b);
+        if (!FULL && (16 * hi + 4 * j + b < t0 || 16 * hi + 4 * j + b >= t1)) sz[4 * j + b] = 0u;
+      }
+    }
+  }
+  float szp[NE];
+#pragma unroll
+  for (int e = 0; e < NE; ++e) szp[e] = sz_prod<BF>(sz[e]);
+  // the digit bias as a register operand (a literal would split the mixed-precision
+  // FMA into a conversion and an FMA)
+  float magic = kMagic + kDigitBias;
+  asm("" : "+v"(magic));
+#pragma unroll
+  for (int c = 0; c < NCH; ++c) {
+    const int hh = 4 * c + wh;
+    const float2 hsw = L.hs[hh];
+    char* wbase = reinterpret_cast<char*>(L.wdig[c]);
+    float zp = 0.0f;
+    constexpr int NJ = NE / 4;
+    uint32_t aw[kNDig][NJ];
+#pragma unroll
+    for (int j = 0; j < NJ; ++j) {
+      const int q = NG == 1 ? wg : NG == 2 ? 2 * (wg >> 1) + j : j;
+      const float4 pw = pq[hh * 17 + 4 * hi + q];
+      uint32_t f[4];
+#pragma unroll
+      for (int b = 0; b < 4; ++b) {
+        const int e = 4 * j + b;
+        // mantissa of rne(w') + 2^23 + 32896 = k + 32896, k in [0, 2^21] (as above)
+        f[b] = __float_as_uint(sz_s_fma_c<BF>(sz[e], compf(pw, b), magic));
+        zp = fmaf(szp[e], compf(pw, b), zp);
+      }
+      const uint32_t t01 = __builtin_amdgcn_perm(f[1], f[0], 0x05010400u) ^ 0x80808080u;
+      const uint32_t t23 = __builtin_amdgcn_perm(f[3], f[2], 0x05010400u) ^ 0x80808080u;
+      const uint32_t h01 = __builtin_amdgcn_perm(f[1], f[0], 0x0c0c0602u);
+      const uint32_t h23 = __builtin_amdgcn_perm(f[3], f[2], 0x0c0c0602u);
+      aw[2][j] = __builtin_amdgcn_perm(t23, t01, 0x05040100u);
+      aw[1][j] = __builtin_amdgcn_perm(t23, t01, 0x07060302u);
+      aw[0][j] = __builtin_amdgcn_perm(h23, h01, 0x05040100u);
+    }
+    if (NG == 1) {
+      char* wp = wbase + 16 * (w_base(0) + w_slot(wh, hi)) + 4 * wg;
+#pragma unroll
+      for (int dg = 0; dg < kNDig; ++dg) *reinterpret_cast<uint32_t*>(wp + 16 * dg) = aw[dg][0];
+    } else if (NG == 2) {
+      char* wp = wbase + 16 * (w_base(wg & 1) + w_slot(wh, hi)) + 8 * (wg >> 1);
+#pragma unroll
+      for (int dg = 0; dg < kNDig; ++dg)
+        *reinterpret_cast<uint2*>(wp + 16 * dg) = make_uint2(aw[dg][0], aw[dg][1]);
+    } else {
+      char* wp = wbase + 16 * (w_base(wg) + w_slot(wh, hi));
+#pragma unroll
+      for (int dg = 0; dg < kNDig; ++dg)
+        *reinterpret_cast<uint4*>(wp + 16 * dg) = make_uint4(aw[dg][0], aw[dg][1], aw[dg][2], aw[dg][3]);
+    }
+    st.zacc[c] = fmaf(zp, hsw.x, st.zacc[c] * hsw.y);
+  }
+
+  } else {
+  // ---- the P.V weights w' = s_v p' of (head 4c + wh, group wg) as three int8
+  // digit operands in each chunk's LDS area, four tokens at a time (quad j of the
+  // lane's tokens, all chunks), so that few V scales are live at once ----
+  constexpr int NJ = NG == 1 ? 1 : NG == 2 ? 2 : 4;  // token quads whose weights a lane forms
+  // the digit bias as a register operand (a literal would split the mixed-precision
+  // FMA into a conversion and an FMA)
+  float magic = kMagic + kDigitBias;
+  asm("" : "+v"(magic));
+  float zp[NCH];
+#pragma unroll
+  for (int c = 0; c < NCH; ++c) zp[c] = 0.0f;
+#pragma unroll
+  for (int j = 0; j < NJ; ++j) {
+    // V (s, z) of the lane's tokens 16hi + 4q + b, q = wg (NG 1), 2(wg>>1) + j (NG 2),
+    // j (NG 4), of group wg (NG 4), wg & 1 (NG 2) or the head's one group (NG 1)
+    const int q = NG == 1 ? wg : NG == 2 ? 2 * (wg >> 1) + j : j;
+    const int grp = NG == 1 ? 0 : NG == 2 ? (wg & 1) : wg;
+    const uint4 vz = *reinterpret_cast<const uint4*>(pb + kLdsVSz + 272 * grp + 64 * hi + 16 * q);
+    uint32_t sz[4];
+    float szp[4];
+#pragma unroll
+    for (int bb = 0; bb < 4; ++bb) {
+      const int tok = 16 * hi + 4 * q + bb;
+      sz[bb] = comp(vz, bb);
+      if (!FULL && (tok < t0 || tok >= t1)) sz[bb] = 0u;  // (0, 0): w = 0, z = 0
+      szp[bb] = sz_prod<BF>(sz[bb]);
+    }
+#pragma unroll
+    for (int c = 0; c < NCH; ++c) {
+      const int hh = 4 * c + wh;
+      const float4 pw = pq[hh * 17 + 4 * hi + q];
+      uint32_t f[4];
+#pragma unroll
+      for (int bb = 0; bb < 4; ++bb) {
+        // mantissa of rne(w') + 2^23 + 32896 = k + 32896, k in [0, 2^21] (as above)
+        f[bb] = __float_as_uint(sz_s_fma_c<BF>(sz[bb], compf(pw, bb), magic));
+        zp[c] = fmaf(szp[bb], compf(pw, bb), zp[c]);
+      }
+      const uint32_t t01 = __builtin_amdgcn_perm(f[1], f[0], 0x05010400u) ^ 0x80808080u;
+      const uint32_t t23 = __builtin_amdgcn_perm(f[3], f[2], 0x05010400u) ^ 0x80808080u;
+      const uint32_t h01 = __builtin_amdgcn_perm(f[1], f[0], 0x0c0c0602u);
+      const uint32_t h23 = __builtin_amdgcn_perm(f[3], f[2], 0x0c0c0602u);
+      uint32_t aw[kNDig];
+      aw[2] = __builtin_amdgcn_perm(t23, t01, 0x05040100u);
+      aw[1] = __builtin_amdgcn_perm(t23, t01, 0x07060302u);
+      aw[0] = __builtin_amdgcn_perm(h23, h01, 0x05040100u);
+      // dword j of the lane's 16-byte digit rows (NG 4: k-group hi's 16 tokens of
+      // (head wh, group wg); NG 2: half wg>>1 of them; NG 1: quarter wg)
+      char* wp = reinterpret_cast<char*>(L.wdig[c]) + 16 * (w_base(grp) + w_slot(wh, hi)) +
+                 (NG == 1 ? 4 * wg : NG == 2 ? 8 * (wg >> 1) + 4 * j : 4 * j);
+#pragma unroll
+      for (int dg = 0; dg < kNDig; ++dg) *reinterpret_cast<uint32_t*>(wp + 16 * dg) = aw[dg];
+    }
+  }
+#pragma unroll
+  for (int c = 0; c < NCH; ++c) {
+    const float2 hsw = L.hs[4 * c + wh];
+    st.zacc[c] = fmaf(zp[c], hsw.x, st.zacc[c] * hsw.y);
+  }
+
+  }
+  // ---- P.V on the int8 matrix cores: lane (channel column, head hi), every chunk ----
+  const uint32_t mk = 0x03030303u << (2 * (lo >> 3));
+  const char* vb = pb + kLdsVCodes + 16 * (4 * (lo & 7) + (hi ^ (((lo >> 2) & 1) << 1)));
+  const int arow = 16 * (w_slot(lo >> 2, hi) + min(lo & 3, 2));
+  float wsc[NCH];
+#pragma unroll
+  for (int c = 0; c < NCH; ++c) {
+    const float2 h = L.hs[4 * c + hi];
+    wsc[c] = h.x;
+    if (resc)
+#pragma unroll
+      for (int k = 0; k < 8; ++k) st.of[c][k] *= h.y;
+  }
+#pragma unroll
+  for (int G = 0; G < 4; ++G) {
+    v4i aop[NCH];
+#pragma unroll
+    for (int c = 0; c < NCH; ++c) {
+      const uint4 a4 = *reinterpret_cast<const uint4*>(reinterpret_cast<const char*>(L.wdig[c]) + arow +
+                                                       16 * w_base(G * NG / 4));
+      aop[c] = v4i{(int)a4.x, (int)a4.y, (int)a4.z, (int)a4.w};
+    }
+    const uint4 x = *reinterpret_cast<const uint4*>(vb + 512 * G);
+#pragma unroll
+    for (int F = 0; F < 2; ++F) {
+      const v4i bv = {(int)((x.x >> (4 * F)) & mk), (int)((x.y >> (4 * F)) & mk),
+                      (int)((x.z >> (4 * F)) & mk), (int)((x.w >> (4 * F)) & mk)};
+#pragma unroll
+      for (int c = 0; c < NCH; ++c) {
+        const v4i d = mfma64(aop[c], bv);
+        const int t = combine3(d[0], d[1], d[2]);
+        st.of[c][2 * G + F] = fmaf((float)t, wsc[c], st.of[c][2 * G + F]);
+      }
+    }
+  }
+}
+
 // The INT2 token range of a sequence in page terms: pages [first, first + npg)
 // of its block-table row; token slots [t0, 64) of the range's first page and
 // [0, t1) of its last page are in the range (t0 = 0, t1 = 64 when aligned).
@@ -531,12 +996,72 @@ __device__ inline TokRange tok_range(int lo, int hi) {
 }
 
 // Pages [p0, p1) of the token range R of sequence b (page indices relative to
-// R.first), kv-head kvh, query-head chunk `chunk`: online softmax over the pages
-// and the partial state written to slot `piece` of the (sequence, head) rows,
-// whose slots are row_stride apart.  `last`: the piece ends the range, so slots
-// piece + 1 .. num_splits - 1 are marked empty.  The wave has done `done0` of its
-// `total` pages before this piece (issue-priority bands).  Without MIXED the
-// range starts at token 0 (R.t0 = 0).
+// R.first), kv-head kvh: each page-head block is staged into `page` and handed to
+// compute(full, t0, t1) (full: all 64 token slots; otherwise slots [t0, t1)).
+// The wave has done `done0` of its `total` pages before these (issue-priority
+// bands).  Without MIXED the range starts at token 0 (R.t0 = 0).
+template <bool MIXED, int NG, typename Compute>
+__device__ __attribute__((always_inline)) inline void walk_pages(uint4* page, const uint8_t* __restrict__ pages,
+                                                                 int Hkv, const int32_t* __restrict__ block_table,
+                                                                 int max_pages, int b, TokRange R, int kvh, int p0,
+                                                                 int p1, int done0, int total, Compute&& compute) {
+  const int l = threadIdx.x;
+  const int npg = R.npg;
+  const int32_t* __restrict__ bt = block_table + (size_t)b * max_pages + (MIXED ? R.first : 0);
+  const uint8_t* __restrict__ base = pages + (size_t)kvh * block_bytes(NG);
+  const size_t page_stride = (size_t)Hkv * block_bytes(NG);
+  // Block-table entries of the split, 64 pages at a time: lane i holds the entry
+  // of page cb + i (a vector load, so that waiting for it never waits on LDS).
+  int cb = p0;
+  int btv = (p0 + l < p1) ? bt[p0 + l] : 0;
+  Stage sg;
+  if (p0 < p1) stage_load<NG, true>(sg, base + (size_t)__builtin_amdgcn_readlane(btv, 0) * page_stride, l);
+  // pages [p0, pf) are full; page pf (if < p1) is the range's partial last page
+  int pf = (p0 < p1 && p1 == npg && R.t1 != kP) ? p1 - 1 : p1;
+  int pg = p0;
+  if (MIXED && p0 == 0 && p0 < p1 && R.t0 != 0) {  // the range's partial first page
+    stage_store<NG>(page, sg, l);
+    stage_load<NG, true>(sg, base + (size_t)__builtin_amdgcn_readlane(btv, min(1, p1 - 1)) * page_stride, l);
+    compute(std::false_type{}, R.t0, npg == 1 ? R.t1 : kP);
+    pg = 1;
+    pf = max(pf, 1);  // a one-page range is done
+  }
+  // Full pages in four bands of the wave's whole page count (done0 pages of it
+  // before this piece, total in all): the wave lowers its issue priority at
+  // 25 %, 50 % and 75 % of its pages.  Waves sharing a SIMD otherwise issue in age
+  // order, and the youngest of them finished up to 1.7x later than the oldest
+  // with the same page count; waves that are behind now go first.
+  for (int band = 1; band <= 4; ++band) {
+    const int lim = (int)(((int64_t)(25 * band) * total + 99) / 100) - done0 + p0;  // band end
+    const int e = min(max(lim, pg), pf);
+    for (; pg < e; ++pg) {
+      stage_store<NG>(page, sg, l);
+      const int nx = min(pg + 1, p1 - 1);  // page pg+1 (the last page again at the end)
+      if (nx - cb >= 64) {                 // uniform: next 64 entries
+        cb += 64;
+        btv = (cb + l < p1) ? bt[cb + l] : 0;
+      }
+      stage_load<NG, true>(sg, base + (size_t)__builtin_amdgcn_readlane(btv, nx - cb) * page_stride, l);
+      compute(std::true_type{}, 0, kP);
+    }
+    if (band < 4 && lim > p0 && lim <= pf) {  // the band ended inside this piece
+      if (band == 1) __builtin_amdgcn_s_setprio(2);
+      else if (band == 2) __builtin_amdgcn_s_setprio(1);
+      else __builtin_amdgcn_s_setprio(0);
+    }
+  }
+  if (pf < p1) {  // the partial last page; the stage holds it
+    stage_store<NG>(page, sg, l);
+    compute(std::false_type{}, 0, R.t1);
+  }
+
+}
+
+// Pages [p0, p1) of the token range R of sequence b, kv-head kvh, one chunk of
+// at most 4 query heads: online softmax over the pages and the partial state
+// written to slot `piece` of the (sequence, head) rows, whose slots are
+// row_stride apart.  `last`: the piece ends the range, so slots piece + 1 ..
+// num_splits - 1 are marked empty.
 template <bool MIXED, bool BF, int NG, int NCH>
 __device__ __attribute__((always_inline)) inline void process_piece(WaveLds<NCH>& L, const uint8_t* __restrict__ pages, int Hkv, int Hq,
                                      const int32_t* __restrict__ block_table, int max_pages, int b,
@@ -547,10 +1072,6 @@ __device__ __attribute__((always_inline)) inline void process_piece(WaveLds<NCH>
                                      int done0, int total) {
   const int g_heads = Hq / Hkv;
   const int l = threadIdx.x, lo = l & 15, hi = l >> 4;
-  const int npg = R.npg;
-  const int32_t* __restrict__ bt = block_table + (size_t)b * max_pages + (MIXED ? R.first : 0);
-  const uint8_t* __restrict__ base = pages + (size_t)kvh * block_bytes(NG);
-  const size_t page_stride = (size_t)Hkv * block_bytes(NG);
 
   WaveState st[NCH];
   // ---- query operands: q_int = rne(q~ * Q / max|q~|), three int8 digits ----
@@ -629,50 +1150,10 @@ __device__ __attribute__((always_inline)) inline void process_piece(WaveLds<NCH>
     for (int k = 0; k < 8; ++k) sc.of[k] = 0.0f;
   }
 
-  // Block-table entries of the split, 64 pages at a time: lane i holds the entry
-  // of page cb + i (a vector load, so that waiting for it never waits on LDS).
-  int cb = p0;
-  int btv = (p0 + l < p1) ? bt[p0 + l] : 0;
-  Stage sg;
-  if (p0 < p1) stage_load<NG, true>(sg, base + (size_t)__builtin_amdgcn_readlane(btv, 0) * page_stride, l);
-  // pages [p0, pf) are full; page pf (if < p1) is the range's partial last page
-  int pf = (p0 < p1 && p1 == npg && R.t1 != kP) ? p1 - 1 : p1;
-  int pg = p0;
-  if (MIXED && p0 == 0 && p0 < p1 && R.t0 != 0) {  // the range's partial first page
-    stage_store<NG>(L.page, sg, l);
-    stage_load<NG, true>(sg, base + (size_t)__builtin_amdgcn_readlane(btv, min(1, p1 - 1)) * page_stride, l);
-    compute_page<false, BF, NG, NCH>(st, L, R.t0, npg == 1 ? R.t1 : kP, lo, hi);
-    pg = 1;
-    pf = max(pf, 1);  // a one-page range is done
-  }
-  // Full pages in four bands of the wave's whole page count (done0 pages of it
-  // before this piece, total in all): the wave lowers its issue priority at
-  // 25 %, 50 % and 75 % of its pages.  Waves sharing a SIMD otherwise issue in age
-  // order, and the youngest of them finished up to 1.7x later than the oldest
-  // with the same page count; waves that are behind now go first.
-  for (int band = 1; band <= 4; ++band) {
-    const int lim = (int)(((int64_t)(25 * band) * total + 99) / 100) - done0 + p0;  // band end
-    const int e = min(max(lim, pg), pf);
-    for (; pg < e; ++pg) {
-      stage_store<NG>(L.page, sg, l);
-      const int nx = min(pg + 1, p1 - 1);  // page pg+1 (the last page again at the end)
-      if (nx - cb >= 64) {                 // uniform: next 64 entries
-        cb += 64;
-        btv = (cb + l < p1) ? bt[cb + l] : 0;
-      }
-      stage_load<NG, true>(sg, base + (size_t)__builtin_amdgcn_readlane(btv, nx - cb) * page_stride, l);
-      compute_page<true, BF, NG, NCH>(st, L, 0, kP, lo, hi);
-    }
-    if (band < 4 && lim > p0 && lim <= pf) {  // the band ended inside this piece
-      if (band == 1) __builtin_amdgcn_s_setprio(2);
-      else if (band == 2) __builtin_amdgcn_s_setprio(1);
-      else __builtin_amdgcn_s_setprio(0);
-    }
-  }
-  if (pf < p1) {  // the partial last page; the stage holds it
-    stage_store<NG>(L.page, sg, l);
-    compute_page<false, BF, NG, NCH>(st, L, 0, R.t1, lo, hi);
-  }
+  walk_pages<MIXED, NG>(L.page, pages, Hkv, block_table, max_pages, b, R, kvh, p0, p1, done0, total,
+                        [&](auto full, int t0, int t1) {
+                          compute_page<decltype(full)::value, BF, NG, NCH>(st, L, t0, t1, lo, hi);
+                        });
 
   // ---- write the split's partial state, per chunk ----
 #pragma unroll
@@ -710,6 +1191,149 @@ __device__ __attribute__((always_inline)) inline void process_piece(WaveLds<NCH>
   }
 }
 
+// The same for 5 to 16 query heads per kv-head (all of them in one wave: scores
+// with one MFMA row per head, P.V in chunks of 4 heads).
+template <bool MIXED, bool BF, int NG, int NCH>
+__device__ __attribute__((always_inline)) inline void process_piece_wide(
+    WideLds<NCH>& L, const uint8_t* __restrict__ pages, int Hkv, int Hq, const int32_t* __restrict__ block_table,
+    int max_pages, int b, TokRange R, int kvh, int p0, int p1, int piece, bool last, int num_splits,
+    int row_stride, const float* __restrict__ qt, float* __restrict__ part_o, float* __restrict__ part_ml,
+    int done0, int total) {
+  const int g_heads = Hq / Hkv;
+  const int l = threadIdx.x & 63, lo = l & 15, hi = l >> 4;
+  const size_t stride = MIXED ? row_stride : num_splits;
+
+  WideState<NCH> st;
+  constexpr int RPH = WideRows<NCH>::RPH, HPL = WideRows<NCH>::HPL;
+  // ---- query operands of head hq = lo / RPH: lane k-group hi holds channels
+  // 32g + 8hi + (0..7) of slice g ----
+  {
+    const int hq = lo / RPH;
+    float qv[4][8];
+    float amax = 0.0f;
+#pragma unroll
+    for (int g = 0; g < 4; ++g)
+#pragma unroll
+      for (int e = 0; e < 8; ++e) qv[g][e] = 0.0f;
+    if (hq < g_heads) {
+      const float* src = qt + ((size_t)b * Hq + kvh * g_heads + hq) * kD + 8 * hi;
+#pragma unroll
+      for (int g = 0; g < 4; ++g) {
+        const float4 x0 = *reinterpret_cast<const float4*>(src + 32 * g);
+        const float4 x1 = *reinterpret_cast<const float4*>(src + 32 * g + 4);
+        qv[g][0] = x0.x; qv[g][1] = x0.y; qv[g][2] = x0.z; qv[g][3] = x0.w;
+        qv[g][4] = x1.x; qv[g][5] = x1.y; qv[g][6] = x1.z; qv[g][7] = x1.w;
+      }
+#pragma unroll
+      for (int g = 0; g < 4; ++g)
+#pragma unroll
+        for (int e = 0; e < 8; ++e) amax = fmaxf(amax, fabsf(qv[g][e]));
+    }
+    amax = rows_max(amax);  // all 128 channels of the head
+    int ex = 0;
+    if (amax > 0.0f) frexpf(amax, &ex);  // amax in [2^(ex-1), 2^ex)
+    const float E = amax > 0.0f ? ldexpf(1.0f, 15 - ex) : 1.0f;
+    const float sqv = amax > 0.0f ? ldexpf(1.0f, 9 + ex) : 1.0f;  // 2^24 / E
+#pragma unroll
+    for (int g = 0; g < 4; ++g) {
+      uint32_t hw[8], lw[8];
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {  // k-slot e: channel 32g + 8hi + (e>>1) + 4(e&1), field e>>1
+        const int f = e >> 1;
+        const float v = qv[g][f + 4 * (e & 1)] * ldexpf(E, -2 * f);
+        const __half h = __float2half_rn(v);
+        hw[e] = __half_as_ushort(h);
+        lw[e] = __half_as_ushort(__float2half_rn(v - __half2float(h)));
+        if (RPH == 2 && (lo & 1)) hw[e] = lw[e];  // the lo-half row of the head
+      }
+      st.aq[g][0] = u4{hw[0] | (hw[1] << 16), hw[2] | (hw[3] << 16), hw[4] | (hw[5] << 16), hw[6] | (hw[7] << 16)};
+      if (RPH == 1)
+        st.aq[g][RPH == 1 ? 1 : 0] =
+            u4{lw[0] | (lw[1] << 16), lw[2] | (lw[3] << 16), lw[4] | (lw[5] << 16), lw[6] | (lw[7] << 16)};
+    }
+    // zero-point MFMA operand: the sum of q~ over group hi (slice sums over the k-groups)
+    float ps[4];
+#pragma unroll
+    for (int g = 0; g < 4; ++g) {
+      float t = 0.0f;
+#pragma unroll
+      for (int e = 0; e < 8; ++e) t += qv[g][e];
+      ps[g] = rows_sum(t);
+    }
+    float gsum;
+    if (NG == 4) gsum = hi == 0 ? ps[0] : hi == 1 ? ps[1] : hi == 2 ? ps[2] : ps[3];
+    else if (NG == 2) gsum = hi == 0 ? ps[0] + ps[1] : hi == 1 ? ps[2] + ps[3] : 0.0f;
+    else gsum = hi == 0 ? (ps[0] + ps[1]) + (ps[2] + ps[3]) : 0.0f;
+    st.az = RPH == 2 && (lo & 1) ? 0.0f : gsum * E * (1.0f / 16777216.0f);  // one row per head
+    float* sqh = reinterpret_cast<float*>(L.page);  // the page is staged after this
+    if (hi == 0) sqh[hq] = sqv;                      // lanes of equal hq write equal values
+#pragma unroll
+    for (int j = 0; j < HPL; ++j) {
+      st.sq[j] = sqh[HPL * hi + j];
+      st.m[j] = -INFINITY;
+      st.lsum[j] = 0.0f;
+    }
+#pragma unroll
+    for (int c = 0; c < NCH; ++c) {
+      st.zacc[c] = 0.0f;
+#pragma unroll
+      for (int k = 0; k < 8; ++k) st.of[c][k] = 0.0f;
+    }
+  }
+
+  walk_pages<MIXED, NG>(L.page, pages, Hkv, block_table, max_pages, b, R, kvh, p0, p1, done0, total,
+                        [&](auto full, int t0, int t1) {
+                          compute_page_wide<decltype(full)::value, BF, NG, NCH>(st, L, t0, t1, lo, hi);
+                        });
+
+  // ---- the piece's partial state: (m, l) of heads HPL hi + j ----
+#pragma unroll
+  for (int j = 0; j < HPL; ++j) {
+    const float ltot = row16_sum(st.lsum[j]);
+    const int hh = HPL * hi + j;
+    if (hh < g_heads && lo == 0) {
+      const size_t row = ((size_t)b * Hq + kvh * g_heads + hh) * stride + piece;
+      part_ml[row * 2] = st.m[j];
+      part_ml[row * 2 + 1] = ltot;
+      if (last)  // the range's last piece: the remaining slots hold nothing
+        for (int s2 = piece + 1; s2 < num_splits; ++s2) {
+          part_ml[(row + s2 - piece) * 2] = -INFINITY;
+          part_ml[(row + s2 - piece) * 2 + 1] = 0.0f;
+        }
+    }
+  }
+  // ---- o~ of head 4c + hi per chunk (sum w z_v per (head, group) through LDS) ----
+  float* zx = reinterpret_cast<float*>(L.page);  // the last page is done
+#pragma unroll
+  for (int c = 0; c < NCH; ++c) {
+    float ztot = rows_sum(st.zacc[c]);  // (head 4c + (lo>>2), group lo&3)
+    if (NG == 1) ztot = quad_sum(ztot);
+    if (NG == 2) ztot += __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(ztot), 0x4E, 0xF, 0xF, false));
+    zx[16 * c + lo] = ztot;  // lanes of equal lo write equal values
+  }
+  const bool empty = p0 >= p1;
+  const float cs = lo >= 8 ? 0.25f : 1.0f;  // P.V columns lo >= 8 accumulate 4 x code
+#pragma unroll
+  for (int c = 0; c < NCH; ++c) {
+    const float4 zh = *reinterpret_cast<const float4*>(&zx[16 * c + 4 * hi]);
+    const int hout = 4 * c + hi;
+    if (hout >= g_heads) continue;  // padding head
+    const size_t row = ((size_t)b * Hq + kvh * g_heads + hout) * stride + piece;
+#pragma unroll
+    for (int G = 0; G < 4; ++G) {
+#pragma unroll
+      for (int F = 0; F < 2; ++F) {
+        const int ch = 32 * G + 4 * (lo & 7) + 2 * F + (lo >> 3);
+        part_o[row * kD + ch] = empty ? 0.0f : fmaf(st.of[c][2 * G + F], cs, -compf(zh, G * NG / 4));
+      }
+    }
+  }
+}
+
+// LDS of a split wave: one chunk of 4 heads, or the wide layout.
+template <int NCH>
+using SplitLds = typename std::conditional<NCH == 1, WaveLds<1>, WideLds<NCH>>::type;
+
 // Balanced split (persistent waves over equal page ranges).  The sequences'
 // pages are laid end to end, T pages in total; range r covers pages
 // [r*pw, (r+1)*pw) with pw = max(ceil(T / n_ranges), ceil(max_pages / (S - 1)),
@@ -722,12 +1346,13 @@ __device__ __attribute__((always_inline)) inline void process_piece(WaveLds<NCH>
 // MIXED a sequence's pages are those of its INT2 history only, and a row's slots
 // are row_stride apart (the slots after the S history slots belong to other
 // kernels).  Grid: n_ranges * Hkv one-wave workgroups, workgroup u = (range u /
-// Hkv, kv-head u % Hkv).  Waves per SIMD: 4 for one chunk (128 VGPRs), 3 for two,
-// 2 for three or four (the chunks' softmax states and query operands).
+// Hkv, kv-head u % Hkv).  Waves per SIMD: 4 for one chunk (128 VGPRs), 2 for the
+// wide instances (their query operands, chunk states and prefetched page; at 3
+// waves the prefetched page spills to scratch).
 constexpr int kMinRange = 4;
 template <int NCH>
 struct SplitWaves {
-  static constexpr int per_simd = NCH == 1 ? 4 : NCH == 2 ? 3 : 2;
+  static constexpr int per_simd = NCH == 1 ? 4 : 2;
 };
 
 __device__ inline int wave_sum_i(int x) {
@@ -743,7 +1368,7 @@ __global__ __launch_bounds__(64) __attribute__((
     int max_pages, const int32_t* __restrict__ seq_lens, int num_splits, int n_ranges, int B,
     const float* __restrict__ qt, float* __restrict__ part_o, float* __restrict__ part_ml,
     int S0, int W, int row_stride) {
-  __shared__ WaveLds<NCH> L;
+  __shared__ SplitLds<NCH> L;
   const int64_t u = blockIdx.x;
   if (u >= (int64_t)n_ranges * Hkv) return;
   const int r = (int)(u / Hkv), kvh = (int)(u % Hkv);
@@ -758,10 +1383,18 @@ __global__ __launch_bounds__(64) __attribute__((
     const int lo = min(S0, len);
     return tok_range(lo, max(lo, len - W));
   };
+  auto run_piece = [&](int bb, TokRange R, int p0, int p1, int piece, bool last, int done0, int total) {
+    if constexpr (NCH == 1)
+      process_piece<MIXED, BF, NG, NCH>(L, pages, Hkv, Hq, block_table, max_pages, bb, R, kvh, p0, p1, piece,
+                                        last, num_splits, stride, qt, part_o, part_ml, done0, total);
+    else
+      process_piece_wide<MIXED, BF, NG, NCH>(L, pages, Hkv, Hq, block_table, max_pages, bb, R, kvh, p0, p1,
+                                             piece, last, num_splits, stride, qt, part_o, part_ml, done0,
+                                             total);
+  };
   if (num_splits == 1) {  // one range per sequence
     const TokRange R = range_of(r);
-    process_piece<MIXED, BF, NG, NCH>(L, pages, Hkv, Hq, block_table, max_pages, r, R, kvh, 0, R.npg,
-                         0, true, 1, stride, qt, part_o, part_ml, 0, 1 << 20);
+    run_piece(r, R, 0, R.npg, 0, true, 0, 1 << 20);
     return;
   }
   // total pages over all sequences
@@ -815,9 +1448,8 @@ __global__ __launch_bounds__(64) __attribute__((
   while (true) {
     const int64_t end = min(xe, before + npg_b);
     const int piece = (int)(r - before / pw);
-    process_piece<MIXED, BF, NG, NCH>(L, pages, Hkv, Hq, block_table, max_pages, b, range_of(b), kvh,
-                         (int)(x - before), (int)(end - before), piece, end == before + npg_b,
-                         num_splits, stride, qt, part_o, part_ml, (int)(x - x0), (int)(xe - x0));
+    run_piece(b, range_of(b), (int)(x - before), (int)(end - before), piece, end == before + npg_b,
+              (int)(x - x0), (int)(xe - x0));
     x = end;
     if (x >= xe) break;
     before += npg_b;

@@ -25,7 +25,7 @@ constexpr int kMaxGroupHeads = 16;                 // query heads per kv-head
 // Split kernel geometry: a wave handles all query heads of its kv-head in chunks
 // of 4, and the number of chunks sets its registers, hence the waves per CU.
 inline int split_chunks(int heads_per_kv) { return (heads_per_kv + 3) / 4; }
-inline int split_waves_per_cu(int nch) { return nch == 1 ? 16 : nch == 2 ? 12 : 8; }
+inline int split_waves_per_cu(int nch) { return nch == 1 ? 16 : 8; }
 
 // Workspace carving for decode (byte offsets, 256-aligned).
 struct DecodeWs {
