@@ -357,8 +357,14 @@ int oscar_decode_step_mixed(const oscar_layout *L, void *pages, void *seg, int32
 /*
  * bf16 paged-decode baseline (same paging, uncompressed cache), for comparing
  * against the INT2 path on the same GPU.  A bf16 page-head block (page p,
- * kv-head h) starts at element (p*Hkv + h) * 2*P*d and holds
- * [K: P x d bf16, token-major][V: P x d bf16, token-major].
+ * kv-head h) starts at element (p*Hkv + h) * 2*P*d and holds K then V in the
+ * order of the decode's matrix-core operands (P = 64, d = 128; each of K and V
+ * is 16 tiles of 64 lanes x 8 elements, one contiguous 1 KB load per tile):
+ *   K(t, c) at ((u*4 + kc)*64 + lo + 16*hi)*8 + e,
+ *           t = 4*lo + u, c = 32*hi + 8*kc + e;
+ *   V(t, c) at P*d + ((ct*2 + kt)*64 + lo + 16*hi)*8 + e,
+ *           t = 16*hi + 8*kt + e, c = 16*ct + lo.
+ * Token slots never written are read as 0 weight (their V is masked).
  */
 size_t oscar_bf16_page_bytes(const oscar_layout *L);
 int oscar_bf16_kv_append(const oscar_layout *L, void *pages, const void *k_new,

@@ -541,13 +541,25 @@ int oracle_decode_brute(int d, int Hkv, int P, int G, int meta, int64_t num_page
 /* ------------------------------------------------------------------------- */
 /* bf16 baseline: plain attention over a bf16 paged cache                     */
 /* ------------------------------------------------------------------------- */
-/* bf16 page-head block (page p, kv-head h) at element (p*Hkv + h) * 2*P*d:
- * [K: P x d bf16, token-major][V: P x d bf16, token-major]. */
+/* bf16 page-head block (page p, kv-head h) at element (p*Hkv + h) * 2*P*d, for
+ * P = 64, d = 128, in the library's tiled order (K then V, each as 16 tiles of
+ * 64 x 8 elements):
+ *   K(t, c) at ((u*4 + kc)*64 + lo + 16*hi)*8 + e,   t = 4*lo + u, c = 32*hi + 8*kc + e
+ *   V(t, c) at P*d + ((ct*2 + kt)*64 + lo + 16*hi)*8 + e,
+ *                                                  t = 16*hi + 8*kt + e, c = 16*ct + lo */
+static size_t bf16_k_index(int t, int c) {
+  int u = t & 3, lo = t >> 2, hi = c >> 5, kc = (c >> 3) & 3, e = c & 7;
+  return ((size_t)(u * 4 + kc) * 64 + lo + 16 * hi) * 8 + e;
+}
+static size_t bf16_v_index(int t, int c) {
+  int hi = t >> 4, kt = (t >> 3) & 1, e = t & 7, ct = c >> 4, lo = c & 15;
+  return (size_t)64 * 128 + ((size_t)(ct * 2 + kt) * 64 + lo + 16 * hi) * 8 + e;
+}
 int oracle_bf16_decode(int d, int Hkv, int P, int64_t num_pages, const uint16_t *pages,
                        const uint16_t *q, int B, int Hq, const int32_t *block_table,
                        int max_pages, const int32_t *seq_lens, double sm_scale,
                        const int32_t *pairs, int n_pairs, double *out) {
-  if (Hq % Hkv) return -1;
+  if (Hq % Hkv || d != 128 || P != 64) return -1;
   int group = Hq / Hkv;
   int n = pairs ? n_pairs : B * Hq;
   int bad = 0;
@@ -566,9 +578,10 @@ int oracle_bf16_decode(int d, int Hkv, int P, int64_t num_pages, const uint16_t 
     for (int t = 0; t < len && ok; ++t) {
       int32_t page = block_table[(size_t)b * max_pages + t / P];
       if (page < 0 || page >= num_pages) { ok = 0; break; }
-      const uint16_t *kr = pages + (((size_t)page * Hkv + kvh) * 2 * P + (size_t)(t % P)) * d;
+      const uint16_t *kb = pages + ((size_t)page * Hkv + kvh) * 2 * P * d;
       double s = 0.0;
-      for (int c = 0; c < d; ++c) s += (double)oracle_bf16_to_f32(qr[c]) * (double)oracle_bf16_to_f32(kr[c]);
+      for (int c = 0; c < d; ++c)
+        s += (double)oracle_bf16_to_f32(qr[c]) * (double)oracle_bf16_to_f32(kb[bf16_k_index(t % P, c)]);
       score[t] = sm_scale * s;
       if (score[t] > m) m = score[t];
     }
@@ -577,10 +590,10 @@ int oracle_bf16_decode(int d, int Hkv, int P, int64_t num_pages, const uint16_t 
       for (int j = 0; j < d; ++j) o[j] = 0.0;
       for (int t = 0; t < len; ++t) {
         int32_t page = block_table[(size_t)b * max_pages + t / P];
-        const uint16_t *vr = pages + (((size_t)page * Hkv + kvh) * 2 * P + P + (size_t)(t % P)) * d;
+        const uint16_t *vb = pages + ((size_t)page * Hkv + kvh) * 2 * P * d;
         double p = exp(score[t] - m);
         l += p;
-        for (int j = 0; j < d; ++j) o[j] += p * (double)oracle_bf16_to_f32(vr[j]);
+        for (int j = 0; j < d; ++j) o[j] += p * (double)oracle_bf16_to_f32(vb[bf16_v_index(t % P, j)]);
       }
       for (int j = 0; j < d; ++j) o[j] /= l;
     } else {
@@ -595,16 +608,20 @@ int oracle_bf16_decode(int d, int Hkv, int P, int64_t num_pages, const uint16_t 
 int oracle_bf16_append(int d, int Hkv, int P, int64_t num_pages, uint16_t *pages,
                        const uint16_t *k, const uint16_t *v, const int64_t *slot_mapping,
                        int n_tok) {
+  if (d != 128 || P != 64) return -1;
   for (int i = 0; i < n_tok; ++i) {
     int64_t slot = slot_mapping[i];
     if (slot < 0 || slot >= num_pages * (int64_t)P) return -1;
     int64_t page = slot / P;
     int t = (int)(slot % P);
     for (int h = 0; h < Hkv; ++h) {
-      uint16_t *kd = pages + (((size_t)page * Hkv + h) * 2 * P + (size_t)t) * d;
-      uint16_t *vd = pages + (((size_t)page * Hkv + h) * 2 * P + P + (size_t)t) * d;
-      memcpy(kd, k + ((size_t)i * Hkv + h) * d, sizeof(uint16_t) * (size_t)d);
-      memcpy(vd, v + ((size_t)i * Hkv + h) * d, sizeof(uint16_t) * (size_t)d);
+      uint16_t *blk = pages + ((size_t)page * Hkv + h) * 2 * P * d;
+      const uint16_t *ks = k + ((size_t)i * Hkv + h) * d;
+      const uint16_t *vs = v + ((size_t)i * Hkv + h) * d;
+      for (int c = 0; c < d; ++c) {
+        blk[bf16_k_index(t, c)] = ks[c];
+        blk[bf16_v_index(t, c)] = vs[c];
+      }
     }
   }
   return 0;

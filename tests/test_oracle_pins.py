@@ -515,3 +515,28 @@ def test_bf16_decode_equals_plain_attention():
                              seq_lens=np.array(lens, np.int32), sm_scale=0.088)
     ref = _plain_attention(q, K, V, lens, Hq, Hkv, 0.088)
     assert np.max(np.abs(got - ref)) <= 1e-12
+
+
+def test_bf16_append_layout_hand_positions():
+    """The bf16 baseline's page-head block in its tiled operand order:
+    hand-computed element positions for one token (page 2, token 37)."""
+    d, P, Hkv = 128, 64, 2
+    pages = np.zeros(3 * Hkv * 2 * P * d, np.uint16)
+    k = (np.arange(Hkv * d, dtype=np.uint16) + 1).reshape(1, Hkv, d)
+    v = (np.arange(Hkv * d, dtype=np.uint16) + 1001).reshape(1, Hkv, d)
+    slot = 2 * P + 37
+    oracle.bf16_append(pages, d=d, Hkv=Hkv, P=P, k=k, v=v, slot_mapping=np.array([slot]))
+    # t = 37: K tile (u = 1, kc), lane lo = 9; V tile (kt = 0), element e = 5, hi = 2
+    hand = {0: (1 * 4 + 0) * 64 * 8 + 9 * 8 + 0,              # c = 0: hi 0, kc 0, e 0
+            45: (1 * 4 + 1) * 64 * 8 + (9 + 16) * 8 + 5,      # c = 45: hi 1, kc 1, e 5
+            127: (1 * 4 + 3) * 64 * 8 + (9 + 48) * 8 + 7}     # c = 127: hi 3, kc 3, e 7
+    hand_v = {0: P * d + (0 * 2 + 0) * 64 * 8 + (0 + 32) * 8 + 5,       # c = 0: ct 0, lo 0
+              45: P * d + (2 * 2 + 0) * 64 * 8 + (13 + 32) * 8 + 5,     # c = 45: ct 2, lo 13
+              127: P * d + (7 * 2 + 0) * 64 * 8 + (15 + 32) * 8 + 5}    # c = 127: ct 7, lo 15
+    for h in range(Hkv):
+        base = (2 * Hkv + h) * 2 * P * d
+        for c, off in hand.items():
+            assert pages[base + off] == k[0, h, c]
+        for c, off in hand_v.items():
+            assert pages[base + off] == v[0, h, c]
+    assert np.count_nonzero(pages) == 2 * Hkv * d
