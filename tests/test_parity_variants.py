@@ -131,6 +131,28 @@ def test_variant_append_and_decode_small(variant):
     assert torch.equal(outb.cpu(), vc.gpu_decode(pool, lens, 3).cpu().to(torch.bfloat16))
 
 
+@pytest.mark.parametrize("variant", ["g64", "paper_format_g64", "paper_format", "bf16_meta",
+                                     "token_quantile", "per_head_r"])
+@pytest.mark.parametrize("g", [6, 12])
+def test_variant_gqa_6_and_12(variant, g):
+    """Query heads per KV head that are not a multiple of 4 (padding heads) and the
+    wide score path (5-8 and 9-16 heads per KV head) in every group size and
+    metadata format, ragged lengths, 1 and 3 splits."""
+    cfg = W.custom("var_g%d_%s" % (g, variant), 4, 2 * g, 2, [1, 65, 200, 777],
+                   seed_index=260 + g + list(VARIANTS).index(variant), k_outliers=(5, 90),
+                   v_outliers=(17,))
+    vc = VCase(cfg, variant)
+    lens = cfg.lens
+    pool = vc.gpu_append(lens)
+    ora = vc.oracle_append(lens)
+    vc.compare(pool, ora, lens)
+    ref = vc.oracle_decode(ora, lens)
+    for S in (1, 3):
+        err = max_abs(vc.gpu_decode(pool, lens, S), ref)
+        log("variant", variant, "g", g, "splits %d max|err| = %.3g" % (S, err))
+        assert err <= DECODE_TOL
+
+
 @pytest.mark.parametrize("variant", ["token_quantile", "g64", "paper_format",
                                      "identity_kv_paper_format", "per_head_r",
                                      "per_head_paper_format"])
@@ -174,7 +196,7 @@ def test_variant_decode_step(variant):
     assert err <= DECODE_TOL
 
 
-@pytest.mark.parametrize("variant", ["paper_format", "per_head_paper_format"])
+@pytest.mark.parametrize("variant", ["paper_format", "paper_format_g64", "g64", "per_head_paper_format"])
 def test_variant_mixed_cache_paper_format(variant):
     """The mixed-precision cache in the paper's format: bf16 sink 64 and window 256
     around an INT2 history with 128-channel groups, bf16 metadata and the
