@@ -204,6 +204,25 @@ __device__ inline void row16_max4(float& a, float& b, float& c, float& d) {
       "v_max_f32_dpp %3, %3, %3 row_ror:8 row_mask:0xf bank_mask:0xf\n"
       : "+v"(a), "+v"(b), "+v"(c), "+v"(d));
 }
+// The same for three values (three interleaved chains: every read is 2
+// instructions after its write).
+__device__ inline void row16_max3(float& a, float& b, float& c) {
+  asm volatile(
+      "s_nop 1\n"
+      "v_max_f32_dpp %0, %0, %0 quad_perm:[1,0,3,2] row_mask:0xf bank_mask:0xf\n"
+      "v_max_f32_dpp %1, %1, %1 quad_perm:[1,0,3,2] row_mask:0xf bank_mask:0xf\n"
+      "v_max_f32_dpp %2, %2, %2 quad_perm:[1,0,3,2] row_mask:0xf bank_mask:0xf\n"
+      "v_max_f32_dpp %0, %0, %0 quad_perm:[2,3,0,1] row_mask:0xf bank_mask:0xf\n"
+      "v_max_f32_dpp %1, %1, %1 quad_perm:[2,3,0,1] row_mask:0xf bank_mask:0xf\n"
+      "v_max_f32_dpp %2, %2, %2 quad_perm:[2,3,0,1] row_mask:0xf bank_mask:0xf\n"
+      "v_max_f32_dpp %0, %0, %0 row_ror:4 row_mask:0xf bank_mask:0xf\n"
+      "v_max_f32_dpp %1, %1, %1 row_ror:4 row_mask:0xf bank_mask:0xf\n"
+      "v_max_f32_dpp %2, %2, %2 row_ror:4 row_mask:0xf bank_mask:0xf\n"
+      "v_max_f32_dpp %0, %0, %0 row_ror:8 row_mask:0xf bank_mask:0xf\n"
+      "v_max_f32_dpp %1, %1, %1 row_ror:8 row_mask:0xf bank_mask:0xf\n"
+      "v_max_f32_dpp %2, %2, %2 row_ror:8 row_mask:0xf bank_mask:0xf\n"
+      : "+v"(a), "+v"(b), "+v"(c));
+}
 // The same for two values (s_nop between the dependent pairs).
 __device__ inline void row16_max2(float& a, float& b) {
   asm volatile(
@@ -655,20 +674,27 @@ __device__ inline float4* wide_pq(WideLds<NCH>& L) {
   else return reinterpret_cast<float4*>(L.page);
 }
 
+// Score rows: (head, half) pairs at 2 rows per head (RPH 2: row r holds head
+// r >> 1), or one row per head (RPH 1: row r holds head (r >> 2) + 4 (r & 3), so
+// that D register j of lane (hi, lo) is head hi + 4j and, at 9 to 12 heads, the
+// padding heads 12..15 are register 3 of every lane: that register is skipped).
 template <int NCH>
 struct WideRows {
   static constexpr int RPH = NCH <= 2 ? 2 : 1;  // MFMA rows per head
   static constexpr int HPL = 4 / RPH;           // heads per lane in the score layout
+  static constexpr int NJ = NCH == 3 ? 3 : HPL; // of them, those that can be real heads
+  __device__ static int row_head(int r) { return RPH == 1 ? (r >> 2) + 4 * (r & 3) : r >> 1; }
+  __device__ static int lane_head(int hi, int j) { return RPH == 1 ? hi + 4 * j : HPL * hi + j; }
 };
 template <int NCH>
 struct WideState {
   static constexpr int RPH = WideRows<NCH>::RPH, HPL = WideRows<NCH>::HPL;
-  u4 aq[4][3 - RPH]; // score A operands: slice g; RPH 1: hi (0) / lo (1) halves of head lo;
-                     // RPH 2: the half lo&1 of head lo>>1 (k-group hi)
+  u4 aq[4][3 - RPH]; // score A operands of row lo (head row_head(lo)), slice g, k-group hi:
+                     // RPH 1: its hi (0) and lo (1) halves; RPH 2: the half lo&1
   float az;          // zero-point MFMA A operand of row lo, group hi: E 2^-24 sum of q~
-  float sq[HPL];     // 2^24 / E of head HPL hi + j (log2 units per accumulated score)
-  float m[HPL];      // reference maximum (log2 units) of head HPL hi + j
-  float lsum[HPL];   // partial sum of p relative to m over this lane's tokens, head HPL hi + j
+  float sq[HPL];     // 2^24 / E of head lane_head(hi, j) (log2 units per accumulated score)
+  float m[HPL];      // reference maximum (log2 units) of that head
+  float lsum[HPL];   // partial sum of p relative to m over this lane's tokens, that head
   float zacc[NCH];   // partial sum of w z_v of (head 4c + (lo>>2), group lo&3)
   float of[NCH][8];  // unnormalized o~ of head 4c + hi, tile (G, F) at of[c][2G + F]
 };
@@ -700,10 +726,10 @@ __device__ inline void compute_page_wide(WideState<NCH>& st, WideLds<NCH>& L, in
   }
   const float cw = (float)(21 - esv);
 
-  // ---- scores of heads 4hi + i for tokens 4lo + u ----
+  // ---- scores of heads lane_head(hi, j) for tokens 4lo + u ----
   const uint32_t* kc = reinterpret_cast<const uint32_t*>(pb + kLdsKCodes + 144 * lo + 4 * (hi >> 1));
   const uint32_t sel = (hi & 1) ? 0x0C030C02u : 0x0C010C00u;  // bytes 2(hi&1), +1 to the two halves
-  constexpr int RPH = WideRows<NCH>::RPH, HPL = WideRows<NCH>::HPL;
+  constexpr int RPH = WideRows<NCH>::RPH, HPL = WideRows<NCH>::HPL, NJ = WideRows<NCH>::NJ;
   // zero-point terms of the tiles: dz[u] = sum_g Q_g s_g z_g (B: group hi of token 4lo + u)
   f4v dz[4];
   {
@@ -732,38 +758,40 @@ __device__ inline void compute_page_wide(WideState<NCH>& st, WideLds<NCH>& L, in
 #pragma unroll
       for (int u = 0; u < 4; ++u)
 #pragma unroll
-        for (int j = 0; j < HPL; ++j) {
+        for (int j = 0; j < NJ; ++j) {
           const float x = RPH == 1 ? d[u][j] : d[u][2 * j] + d[u][2 * j + 1];
           acc[u][j] = sz_s_fma_c<BF>(comp(kg, u), x, g + 1 == 4 / NG ? -dz[u][RPH * j] : acc[u][j]);
         }
     }
   }
 
-  // ---- online softmax of heads HPL hi + j ----
+  // ---- online softmax of heads lane_head(hi, j) ----
   float mx[HPL];
 #pragma unroll
-  for (int j = 0; j < HPL; ++j) {
+  for (int j = 0; j < NJ; ++j) {
     float x = -INFINITY;
 #pragma unroll
     for (int u = 0; u < 4; ++u)
       if (valid(u)) x = fmaxf(x, acc[u][j]);
     mx[j] = x;
   }
-  if (HPL == 4) row16_max4(mx[0], mx[HPL > 1 ? 1 : 0], mx[HPL > 2 ? 2 : 0], mx[HPL > 3 ? 3 : 0]);
-  else row16_max2(mx[0], mx[HPL > 1 ? 1 : 0]);  // at least one valid token per page
+  // at least one valid token per page
+  if (NJ == 4) row16_max4(mx[0], mx[NJ > 1 ? 1 : 0], mx[NJ > 2 ? 2 : 0], mx[NJ > 3 ? 3 : 0]);
+  else if (NJ == 3) row16_max3(mx[0], mx[NJ > 1 ? 1 : 0], mx[NJ > 2 ? 2 : 0]);
+  else row16_max2(mx[0], mx[NJ > 1 ? 1 : 0]);
   bool need = false;
 #pragma unroll
-  for (int j = 0; j < HPL; ++j) {
+  for (int j = 0; j < NJ; ++j) {
     mx[j] *= st.sq[j];
     need = need || !(mx[j] <= st.m[j] + kSlack);
   }
   const bool resc = __ballot(need) != 0ull;  // wave-uniform
   float alpha[HPL];
 #pragma unroll
-  for (int j = 0; j < HPL; ++j) alpha[j] = 1.0f;
+  for (int j = 0; j < NJ; ++j) alpha[j] = 1.0f;
   if (resc) {
 #pragma unroll
-    for (int j = 0; j < HPL; ++j) {
+    for (int j = 0; j < NJ; ++j) {
       const float mn = fmaxf(st.m[j], mx[j]);
       alpha[j] = ex2(st.m[j] - mn);  // m = -inf on the first page -> 0
       st.m[j] = mn;
@@ -772,8 +800,8 @@ __device__ inline void compute_page_wide(WideState<NCH>& st, WideLds<NCH>& L, in
   }
   float4* pq = wide_pq(L);
 #pragma unroll
-  for (int j = 0; j < HPL; ++j) {
-    const int hh = HPL * hi + j;
+  for (int j = 0; j < NJ; ++j) {
+    const int hh = WideRows<NCH>::lane_head(hi, j);
     const float c = cw - mx[j];
     const float ws = ex2(mx[j] - st.m[j] - cw);
     float pv[4];
@@ -1204,11 +1232,11 @@ __device__ __attribute__((always_inline)) inline void process_piece_wide(
   const size_t stride = MIXED ? row_stride : num_splits;
 
   WideState<NCH> st;
-  constexpr int RPH = WideRows<NCH>::RPH, HPL = WideRows<NCH>::HPL;
-  // ---- query operands of head hq = lo / RPH: lane k-group hi holds channels
+  constexpr int RPH = WideRows<NCH>::RPH, HPL = WideRows<NCH>::HPL, NJ = WideRows<NCH>::NJ;
+  // ---- query operands of head hq = row_head(lo): lane k-group hi holds channels
   // 32g + 8hi + (0..7) of slice g ----
   {
-    const int hq = lo / RPH;
+    const int hq = WideRows<NCH>::row_head(lo);
     float qv[4][8];
     float amax = 0.0f;
 #pragma unroll
@@ -1269,7 +1297,7 @@ __device__ __attribute__((always_inline)) inline void process_piece_wide(
     if (hi == 0) sqh[hq] = sqv;                      // lanes of equal hq write equal values
 #pragma unroll
     for (int j = 0; j < HPL; ++j) {
-      st.sq[j] = sqh[HPL * hi + j];
+      st.sq[j] = sqh[j < NJ ? WideRows<NCH>::lane_head(hi, j) : 0];
       st.m[j] = -INFINITY;
       st.lsum[j] = 0.0f;
     }
@@ -1286,11 +1314,11 @@ __device__ __attribute__((always_inline)) inline void process_piece_wide(
                           compute_page_wide<decltype(full)::value, BF, NG, NCH>(st, L, t0, t1, lo, hi);
                         });
 
-  // ---- the piece's partial state: (m, l) of heads HPL hi + j ----
+  // ---- the piece's partial state: (m, l) of heads lane_head(hi, j) ----
 #pragma unroll
-  for (int j = 0; j < HPL; ++j) {
+  for (int j = 0; j < NJ; ++j) {
     const float ltot = row16_sum(st.lsum[j]);
-    const int hh = HPL * hi + j;
+    const int hh = WideRows<NCH>::lane_head(hi, j);
     if (hh < g_heads && lo == 0) {
       const size_t row = ((size_t)b * Hq + kvh * g_heads + hh) * stride + piece;
       part_ml[row * 2] = st.m[j];
