@@ -213,70 +213,72 @@ __device__ inline uint32_t pack_quad(uint32_t code, int lane) {
 __device__ inline float bf16_to_f32(uint16_t h) { return __uint_as_float(((uint32_t)h) << 16); }
 
 // ---------------------------------------------------------------------------
-// prepare: 8 query rows per block.  R_k (64 KB) is copied to LDS once per block;
-// thread (channel j, row group) computes 4 rows of column j, reading R_k[c][j]
-// (consecutive j: no bank conflicts) and the rows' q[c..c+3] (broadcast).
+// prepare: q~ = q R_k (times the logit scale) on the fp32 matrix cores, 16 query
+// rows per block.  Wave w computes column tiles 2w and 2w + 1 (16 channels each)
+// of the block's rows as 32 chained 16x16x4 MFMAs per tile: step s takes channels
+// c = 32k + s in k-slot k, so lane (row lo, k-slot hi) holds q[row][32hi + s] (one
+// 64-byte run of the row) and lane (column lo, k-slot hi) R_k[32hi + s][16t + lo]
+// (16 lanes read 64 contiguous bytes of a row of R_k).  R_k is read straight from
+// L2 (no LDS copy, no barrier); all loads of a wave are issued before its MFMAs.
+// D lane (column lo, hi): rows 4hi + i.
 // ---------------------------------------------------------------------------
-constexpr int kPrepRows = 8;
+constexpr int kPrepRows = 16;
 
-__device__ inline void prepare_body(float* Rsf, float4 (*qs)[kD / 4], int bx,
-                                    const uint16_t* __restrict__ q, int rows,
+typedef float prep_f4 __attribute__((ext_vector_type(4)));
+
+__device__ inline void prepare_body(int bx, const uint16_t* __restrict__ q, int rows,
                                     const float* __restrict__ Rk, float qscale,
                                     float* __restrict__ qt, int rph, int Hq, int Hkv) {
-  float4* Rs = reinterpret_cast<float4*>(Rsf);
-  const int t = threadIdx.x;
+  const int t = threadIdx.x, w = t >> 6, lo = t & 15, hi = (t >> 4) & 3;
   int kvh;
   query_row(bx, 0, kPrepRows, rows, Hq, Hkv, rph, kvh);
   if (Rk && rph) Rk += (size_t)kvh * kD * kD;  // the block's rows share a KV head
-  if (Rk) {
-    // 16 float4 per thread, all loads issued before the stores (no per-load wait)
-    float4 v[kD * kD / 4 / 256];
+  int kv_;
+  const int arow = query_row(bx, lo, kPrepRows, rows, Hq, Hkv, rph, kv_);
+  if (!Rk) {  // R = I (bf16 baseline): a scaled copy, rows 4w + (0..3), lane: 2 channels
 #pragma unroll
-    for (int k = 0; k < kD * kD / 4 / 256; ++k) v[k] = reinterpret_cast<const float4*>(Rk)[t + 256 * k];
-#pragma unroll
-    for (int k = 0; k < kD * kD / 4 / 256; ++k) Rs[t + 256 * k] = v[k];
-  }
-  {  // 8 rows x 128 bf16 = 256 threads x 4 values
-    const int r = t >> 5, c4 = t & 31;
-    int kv_;
-    const int row = query_row(bx, r, kPrepRows, rows, Hq, Hkv, rph, kv_);
-    float4 x = make_float4(0.0f, 0.0f, 0.0f, 0.0f);
-    if (row >= 0) {
-      const uint2 w = reinterpret_cast<const uint2*>(q + (size_t)row * kD)[c4];
-      x = make_float4(bf16_to_f32((uint16_t)(w.x & 0xffffu)), bf16_to_f32((uint16_t)(w.x >> 16)),
-                      bf16_to_f32((uint16_t)(w.y & 0xffffu)), bf16_to_f32((uint16_t)(w.y >> 16)));
+    for (int i = 0; i < 4; ++i) {
+      const int row = query_row(bx, 4 * w + i, kPrepRows, rows, Hq, Hkv, rph, kv_);
+      if (row < 0) continue;
+      const int c = 2 * (t & 63);
+      const uint32_t v = *reinterpret_cast<const uint32_t*>(q + (size_t)row * kD + c);
+      qt[(size_t)row * kD + c] = bf16_to_f32((uint16_t)(v & 0xffffu)) * qscale;
+      qt[(size_t)row * kD + c + 1] = bf16_to_f32((uint16_t)(v >> 16)) * qscale;
     }
-    qs[r][c4] = x;
+    return;
   }
-  __syncthreads();
-  const int j = t & (kD - 1);
-  const int rg = (t >> 7) * 4;
-  float acc[4] = {0.0f, 0.0f, 0.0f, 0.0f};
-  if (Rk) {
-    const float* R = reinterpret_cast<const float*>(Rs);
-#pragma unroll 4
-    for (int c4 = 0; c4 < kD / 4; ++c4) {
-      const float r_0 = R[(4 * c4 + 0) * kD + j], r_1 = R[(4 * c4 + 1) * kD + j];
-      const float r_2 = R[(4 * c4 + 2) * kD + j], r_3 = R[(4 * c4 + 3) * kD + j];
+  float a[32];
+  if (arow >= 0) {
+    const uint4* src = reinterpret_cast<const uint4*>(q + (size_t)arow * kD + 32 * hi);
 #pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        const float4 x = qs[rg + i][c4];
-        acc[i] = fmaf(x.x, r_0, acc[i]);
-        acc[i] = fmaf(x.y, r_1, acc[i]);
-        acc[i] = fmaf(x.z, r_2, acc[i]);
-        acc[i] = fmaf(x.w, r_3, acc[i]);
+    for (int k = 0; k < 4; ++k) {
+      const uint4 v = src[k];
+      const uint32_t u[4] = {v.x, v.y, v.z, v.w};
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        a[8 * k + 2 * e] = bf16_to_f32((uint16_t)(u[e] & 0xffffu));
+        a[8 * k + 2 * e + 1] = bf16_to_f32((uint16_t)(u[e] >> 16));
       }
     }
-  } else {  // R = I (bf16 baseline)
-    const float* Q = reinterpret_cast<const float*>(qs);
+  } else {
 #pragma unroll
-    for (int i = 0; i < 4; ++i) acc[i] = Q[(rg + i) * kD + j];
+    for (int s = 0; s < 32; ++s) a[s] = 0.0f;
   }
+  float b[2][32];
 #pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    int kv_;
-    const int row = query_row(bx, rg + i, kPrepRows, rows, Hq, Hkv, rph, kv_);
-    if (row >= 0) qt[(size_t)row * kD + j] = acc[i] * qscale;
+  for (int tt = 0; tt < 2; ++tt)
+#pragma unroll
+    for (int s = 0; s < 32; ++s) b[tt][s] = Rk[(size_t)(32 * hi + s) * kD + 16 * (2 * w + tt) + lo];
+#pragma unroll
+  for (int tt = 0; tt < 2; ++tt) {
+    prep_f4 d = {0.0f, 0.0f, 0.0f, 0.0f};
+#pragma unroll
+    for (int s = 0; s < 32; ++s) d = __builtin_amdgcn_mfma_f32_16x16x4f32(a[s], b[tt][s], d, 0, 0, 0);
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int row = query_row(bx, 4 * hi + i, kPrepRows, rows, Hq, Hkv, rph, kv_);
+      if (row >= 0) qt[(size_t)row * kD + 16 * (2 * w + tt) + lo] = d[i] * qscale;
+    }
   }
 }
 
@@ -915,9 +917,7 @@ __global__ __launch_bounds__(256) void prepare_kernel(const uint16_t* __restrict
                                                       const float* __restrict__ Rk, float qscale,
                                                       float* __restrict__ qt, int rph, int Hq,
                                                       int Hkv) {
-  __shared__ float Rs[kD * kD];
-  __shared__ float4 qs[kPrepRows][kD / 4];
-  prepare_body(Rs, qs, blockIdx.x, q, rows, Rk, qscale, qt, rph, Hq, Hkv);
+  prepare_body(blockIdx.x, q, rows, Rk, qscale, qt, rph, Hq, Hkv);
 }
 
 // One launch for a decode step's prologue: blockIdx.y 0/1 = K/V cache update
@@ -931,13 +931,12 @@ __global__ __launch_bounds__(256) void prologue_kernel(
     int prep_blocks) {
   __shared__ float Rs[kD * kD];
   __shared__ double xs[kWaves][RW][kD];
-  __shared__ float4 qs[kPrepRows][kD / 4];
   if (blockIdx.y < 2) {
     if ((int)blockIdx.x < append_blocks)
       append_body<RW>(Rs, xs, blockIdx.y, blockIdx.x, append_blocks, pages, Hkv, rows, n_rows,
                       Rk, Rv, clip_k, clip_v, pick(DEF, fmt_arg));
   } else if ((int)blockIdx.x < prep_blocks) {
-    prepare_body(Rs, qs, blockIdx.x, q, q_rows, Rk, qscale, qt, fmt_arg.rph, Hq, Hkv);
+    prepare_body(blockIdx.x, q, q_rows, Rk, qscale, qt, fmt_arg.rph, Hq, Hkv);
   }
 }
 
