@@ -181,8 +181,10 @@ __global__ __launch_bounds__(256) void reduce_kernel(int rows, int num_splits,
       for (int i = 0; i < 4; ++i) store(tt, i, om[(4 * hi + i) * kOmPitch + 16 * (2 * w + tt) + lo]);
     return;
   }
-  // Both tiles' products first, then their stores: the results are read in the
-  // block that ends the MFMA chains.
+  // Both tiles' products first, then their stores, on a path no other branch
+  // joins: with the identity case as the other arm of an if/else whose join read
+  // the MFMA results, the compiler put no wait states between the last MFMA and
+  // the first read of its result (wrong values in one result register).
   red_f4 d[2];
 #pragma unroll
   for (int tt = 0; tt < 2; ++tt) {
