@@ -153,6 +153,32 @@ def test_variant_gqa_6_and_12(variant, g):
         assert err <= DECODE_TOL
 
 
+@pytest.mark.parametrize("variant", ["bf16_meta", "g64", "g128", "identity_v", "per_head_r"])
+def test_bf16_output_is_rne_of_fp32_every_instance(variant):
+    """For every split-kernel instance (1 to 16 query heads per KV head: one chunk,
+    the two-row and the one-row-per-head score tiles; each group size and metadata
+    format) and both reduce instances (8 and 16 rows per block), with 1 and 3
+    splits, the bf16 output is the round-to-nearest-even of the fp32 output of the
+    same call: the two differ only in the final store."""
+    for g in (1, 4, 6, 8, 12, 16):
+        cfg = W.custom("rne_g%d_%s" % (g, variant), 3, 2 * g, 2, [5, 130, 300],
+                       seed_index=300 + g + list(VARIANTS).index(variant))
+        vc = VCase(cfg, variant)
+        pool = vc.gpu_append(cfg.lens)
+        for S in (1, 3):
+            o32 = vc.gpu_decode(pool, cfg.lens, S)
+            o16 = vc.gpu_decode(pool, cfg.lens, S, out_dtype=torch.bfloat16)
+            log("rne", variant, "g", g, "splits", S)
+            assert torch.equal(o16.cpu(), o32.cpu().to(torch.bfloat16)), (g, S)
+    # 4096 rows: the reduce's 16-row blocks
+    cfg = W.custom("rne_rows_%s" % variant, 128, 32, 8, np.full(128, 100), seed_index=330)
+    vc = VCase(cfg, variant)
+    pool = vc.gpu_append(cfg.lens)
+    o32 = vc.gpu_decode(pool, cfg.lens, 2)
+    o16 = vc.gpu_decode(pool, cfg.lens, 2, out_dtype=torch.bfloat16)
+    assert torch.equal(o16.cpu(), o32.cpu().to(torch.bfloat16))
+
+
 @pytest.mark.parametrize("variant", ["token_quantile", "g64", "paper_format",
                                      "identity_kv_paper_format", "per_head_r",
                                      "per_head_paper_format"])
