@@ -1,8 +1,11 @@
-// Split kernel of INT2 decode attention on the matrix cores (gfx950 int8 MFMA).
+// Split kernel of INT2 decode attention on the matrix cores (gfx950 MFMA).
 // Persistent waves: each wave owns one (page range, kv-head), walks the range's
 // pages (64 tokens each) and keeps the online-softmax state of the kv-head's
-// query heads in registers, in chunks of 4; a range that crosses sequence
-// boundaries writes one partial state per sequence piece (see split_mfma_kernel).
+// query heads in registers; a range that crosses sequence boundaries writes one
+// partial state per sequence piece (see split_mfma_kernel).  Up to 4 query heads
+// per kv-head: int8 products for the scores and P.V, as below.  5 to 16: the scores
+// on fp16 products with one or two rows per head, P.V on int8 in chunks of 4 heads
+// (compute_page_wide, further down).
 //
 // Arithmetic (Sec. 2: K^ = Q(K R) R^T; Alg. 1 DecodeStep), per 32-channel group g
 // with Q(x~)_c = s_g (code_c - z_g):
@@ -357,9 +360,11 @@ struct WaveState {
 // [t0, t1) (the partial first or last page of a token range).
 // NG groups of 128 / NG channels per head: a group spans 4 / NG of the 32-channel
 // slices that the MFMA tiles use, which share its (s, z) and its P.V weights.
-// NCH chunks of 4 query heads share the page: the K-code operands of the score
-// MFMAs, the V scales (and their page maximum) and the V-code operands of the P.V
-// MFMAs are formed once; everything per head runs once per chunk.
+// NCH chunks of 4 query heads would share the page (the K-code operands of the
+// score MFMAs, the V scales and the V-code operands of the P.V MFMAs formed once,
+// everything per head once per chunk); the kernel instantiates NCH = 1 only: 5 to
+// 16 query heads per KV head take the wide path (compute_page_wide), whose score
+// tiles hold one or two rows per head.
 template <bool FULL, bool BF, int NG, int NCH>
 __device__ inline void compute_page(WaveState (&st)[NCH], WaveLds<NCH>& L, int t0, int t1, int lo,
                                     int hi) {
