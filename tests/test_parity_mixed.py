@@ -202,6 +202,28 @@ def test_mixed_gqa_ratios(g):
     assert err <= DECODE_TOL
 
 
+def test_mixed_reduce_16_row_blocks():
+    """4096 (sequence, head) rows, so that the merge runs 16 rows per block, with the
+    bf16 segments' slot (sink 4, window 8) added after the back-rotation."""
+    S0, W_ = 4, 8
+    lens = np.random.default_rng(220).integers(1, 81, size=128).astype(np.int32)
+    cfg = W.custom("mixed_rows4096", 128, 32, 8, lens, seed_index=220, k_outliers=(5, 90),
+                   v_outliers=(17,))
+    m = Mixed(cfg, S0, W_)
+    pool, seg = m.gpu_prefill(lens - 1)
+    out = m.gpu_step(pool, seg, lens, num_splits=3)
+    ora_pages, ora_seg = m.oracle_build(lens)
+    m.compare_state(pool, seg, ora_pages, ora_seg, lens)
+    ref = m.oracle_decode(ora_pages, ora_seg, lens)
+    err = max_abs(out, ref)
+    log("  rows 4096 max|err| = %.3g" % err)
+    assert err <= DECODE_TOL
+    ob = m.gpu_decode(pool, seg, lens, num_splits=3, out_dtype=torch.bfloat16)
+    o3 = m.gpu_decode(pool, seg, lens, num_splits=3)
+    assert max_abs(o3, ref) <= DECODE_TOL
+    assert torch.equal(ob.cpu(), o3.cpu().to(torch.bfloat16))
+
+
 def test_mixed_many_steps_demote_in_order():
     """A decode loop on the GPU: prefill, then 150 steps, each compared with the
     oracle's loop (the window wraps, pages fill, tokens are demoted one by one)."""
