@@ -94,7 +94,7 @@ def main():
     args = parse()
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
-        print("bench.py measures one GPU only: this build runs the decode path on a single "
+        print("bench.py measures one GPU only: liboscar runs the decode path on a single "
               "MI355X (no multi-GPU path); run with --gpus 1", file=sys.stderr)
         sys.exit(2)
 

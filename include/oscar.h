@@ -118,7 +118,7 @@ size_t oscar_page_bytes(const oscar_layout *L);
 /* Bytes of the whole pool: num_pages * oscar_page_bytes(L). */
 size_t oscar_pool_bytes(const oscar_layout *L);
 
-/* Check a layout; OSCAR_OK if this build supports it. */
+/* Check a layout; OSCAR_OK if the library supports it. */
 int oscar_layout_check(const oscar_layout *L);
 
 /*
