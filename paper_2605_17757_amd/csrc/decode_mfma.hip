@@ -824,7 +824,6 @@ __device__ inline void compute_page_wide(WideState<NCH>& st, WideLds<NCH>& L, in
   }
 
   const int wh = lo >> 2, wg = lo & 3;
-  if constexpr (NCH >= 3) {
   // ---- per chunk: the P.V weights w' = s_v p' of (head 4c + wh, group wg) as three
   // int8 digit operands in the chunk's LDS area ----
   constexpr int NE = NG == 1 ? 4 : NG == 2 ? 8 : 16;  // tokens whose weights a lane forms
@@ -913,68 +912,6 @@ __device__ inline void compute_page_wide(WideState<NCH>& st, WideLds<NCH>& L, in
     st.zacc[c] = fmaf(zp, hsw.x, st.zacc[c] * hsw.y);
   }
 
-  } else {
-  // ---- the P.V weights w' = s_v p' of (head 4c + wh, group wg) as three int8
-  // digit operands in each chunk's LDS area, four tokens at a time (quad j of the
-  // lane's tokens, all chunks), so that few V scales are live at once ----
-  constexpr int NJ = NG == 1 ? 1 : NG == 2 ? 2 : 4;  // token quads whose weights a lane forms
-  // the digit bias as a register operand (a literal would split the mixed-precision
-  // FMA into a conversion and an FMA)
-  float magic = kMagic + kDigitBias;
-  asm("" : "+v"(magic));
-  float zp[NCH];
-#pragma unroll
-  for (int c = 0; c < NCH; ++c) zp[c] = 0.0f;
-#pragma unroll
-  for (int j = 0; j < NJ; ++j) {
-    // V (s, z) of the lane's tokens 16hi + 4q + b, q = wg (NG 1), 2(wg>>1) + j (NG 2),
-    // j (NG 4), of group wg (NG 4), wg & 1 (NG 2) or the head's one group (NG 1)
-    const int q = NG == 1 ? wg : NG == 2 ? 2 * (wg >> 1) + j : j;
-    const int grp = NG == 1 ? 0 : NG == 2 ? (wg & 1) : wg;
-    const uint4 vz = *reinterpret_cast<const uint4*>(pb + kLdsVSz + 272 * grp + 64 * hi + 16 * q);
-    uint32_t sz[4];
-    float szp[4];
-#pragma unroll
-    for (int bb = 0; bb < 4; ++bb) {
-      const int tok = 16 * hi + 4 * q + bb;
-      sz[bb] = comp(vz, bb);
-      if (!FULL && (tok < t0 || tok >= t1)) sz[bb] = 0u;  // (0, 0): w = 0, z = 0
-      szp[bb] = sz_prod<BF>(sz[bb]);
-    }
-#pragma unroll
-    for (int c = 0; c < NCH; ++c) {
-      const int hh = 4 * c + wh;
-      const float4 pw = pq[hh * 17 + 4 * hi + q];
-      uint32_t f[4];
-#pragma unroll
-      for (int bb = 0; bb < 4; ++bb) {
-        // mantissa of rne(w') + 2^23 + 32896 = k + 32896, k in [0, 2^21] (as above)
-        f[bb] = __float_as_uint(sz_s_fma_c<BF>(sz[bb], compf(pw, bb), magic));
-        zp[c] = fmaf(szp[bb], compf(pw, bb), zp[c]);
-      }
-      const uint32_t t01 = __builtin_amdgcn_perm(f[1], f[0], 0x05010400u) ^ 0x80808080u;
-      const uint32_t t23 = __builtin_amdgcn_perm(f[3], f[2], 0x05010400u) ^ 0x80808080u;
-      const uint32_t h01 = __builtin_amdgcn_perm(f[1], f[0], 0x0c0c0602u);
-      const uint32_t h23 = __builtin_amdgcn_perm(f[3], f[2], 0x0c0c0602u);
-      uint32_t aw[kNDig];
-      aw[2] = __builtin_amdgcn_perm(t23, t01, 0x05040100u);
-      aw[1] = __builtin_amdgcn_perm(t23, t01, 0x07060302u);
-      aw[0] = __builtin_amdgcn_perm(h23, h01, 0x05040100u);
-      // dword j of the lane's 16-byte digit rows (NG 4: k-group hi's 16 tokens of
-      // (head wh, group wg); NG 2: half wg>>1 of them; NG 1: quarter wg)
-      char* wp = reinterpret_cast<char*>(L.wdig[c]) + 16 * (w_base(grp) + w_slot(wh, hi)) +
-                 (NG == 1 ? 4 * wg : NG == 2 ? 8 * (wg >> 1) + 4 * j : 4 * j);
-#pragma unroll
-      for (int dg = 0; dg < kNDig; ++dg) *reinterpret_cast<uint32_t*>(wp + 16 * dg) = aw[dg];
-    }
-  }
-#pragma unroll
-  for (int c = 0; c < NCH; ++c) {
-    const float2 hsw = L.hs[4 * c + wh];
-    st.zacc[c] = fmaf(zp[c], hsw.x, st.zacc[c] * hsw.y);
-  }
-
-  }
   // ---- P.V on the int8 matrix cores: lane (channel column, head hi), every chunk ----
   const uint32_t mk = 0x03030303u << (2 * (lo >> 3));
   const char* vb = pb + kLdsVCodes + 16 * (4 * (lo & 7) + (hi ^ (((lo >> 2) & 1) << 1)));
