@@ -85,6 +85,8 @@ constexpr int kLdsVSz = kSlotVSz * 16;
 // slot kWBase[G] + 13 k + 3 perm_k(head) + digit, where perm_k is the identity for
 // even k and (0, 2, 3, 1) for odd k.
 __device__ inline int w_base(int G) { return G == 0 ? 0 : G == 1 ? 51 : G == 2 ? 103 : 156; }
+// The same as arithmetic, for a lane-varying G (no branches in the page loop).
+__device__ inline int w_base_v(int G) { return 51 * G + ((G * (G - 1)) >> 1); }
 __device__ inline int w_slot(int head, int k) {
   return 13 * k + 3 * ((k & 1) ? (0x1320 >> (4 * head)) & 0xf : head);
 }
@@ -883,7 +885,10 @@ __device__ inline void compute_page_wide(WideState<NCH>& st, WideLds<NCH>& L, in
       for (int b = 0; b < 4; ++b) {
         const int e = 4 * j + b;
         // mantissa of rne(w') + 2^23 + 32896 = k + 32896, k in [0, 2^21] (as above)
-        f[b] = __float_as_uint(sz_s_fma_c<BF>(sz[e], compf(pw, b), magic));
+        // (inline asm: its inputs and result are LDS and VALU values, never MFMA
+        // operands or results; as plain C the compiler converts s once for all
+        // chunks and then needs a conversion and an FMA where one mixed FMA does)
+        f[b] = __float_as_uint(sz_s_fma<BF>(sz[e], compf(pw, b), magic));
         zp = fmaf(szp[e], compf(pw, b), zp);
       }
       const uint32_t t01 = __builtin_amdgcn_perm(f[1], f[0], 0x05010400u) ^ 0x80808080u;
@@ -899,12 +904,12 @@ __device__ inline void compute_page_wide(WideState<NCH>& st, WideLds<NCH>& L, in
 #pragma unroll
       for (int dg = 0; dg < kNDig; ++dg) *reinterpret_cast<uint32_t*>(wp + 16 * dg) = aw[dg][0];
     } else if (NG == 2) {
-      char* wp = wbase + 16 * (w_base(wg & 1) + w_slot(wh, hi)) + 8 * (wg >> 1);
+      char* wp = wbase + 16 * (w_base_v(wg & 1) + w_slot(wh, hi)) + 8 * (wg >> 1);
 #pragma unroll
       for (int dg = 0; dg < kNDig; ++dg)
         *reinterpret_cast<uint2*>(wp + 16 * dg) = make_uint2(aw[dg][0], aw[dg][1]);
     } else {
-      char* wp = wbase + 16 * (w_base(wg) + w_slot(wh, hi));
+      char* wp = wbase + 16 * (w_base_v(wg) + w_slot(wh, hi));
 #pragma unroll
       for (int dg = 0; dg < kNDig; ++dg)
         *reinterpret_cast<uint4*>(wp + 16 * dg) = make_uint4(aw[dg][0], aw[dg][1], aw[dg][2], aw[dg][3]);
