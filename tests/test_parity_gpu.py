@@ -75,6 +75,30 @@ def test_gqa_ratios_and_ragged_lengths(g):
     _run_full(make_case(cfg), num_splits=3)
 
 
+@pytest.mark.parametrize("g", [4, 8, 12])
+@pytest.mark.parametrize("num_splits", [1, 3])
+def test_zero_length_sequences(g, num_splits):
+    """Sequences of length 0 between live ones (a length-0 sequence decodes to a zero
+    row): their rows are exactly zero and every other row matches the oracle, in the
+    int8 instance (4 query heads per KV head) and the wide ones (8, 12)."""
+    Hkv = 2
+    lens = np.array([0, 130, 0, 700, 64, 0], np.int32)
+    cfg = W.custom("zero_len_g%d" % g, len(lens), g * Hkv, Hkv, lens, seed_index=230 + g)
+    case = make_case(cfg)
+    log("case", cfg.name, "lens", list(lens), "splits", num_splits)
+    pool = gpu_append(case)
+    ora = oracle_append(case)
+    compare_pools(pool.cpu().numpy(), ora, case)
+    live = np.nonzero(lens > 0)[0]
+    pairs = np.array([(b, h) for b in live for h in range(cfg.Hq)], np.int32)
+    ref = oracle_decode(case, ora, pairs=pairs)
+    out = gpu_decode(case, pool, num_splits).cpu().numpy()
+    err = max_abs(out[live].reshape(-1, 128), ref)
+    log("  decode max|err| = %.3g" % err)
+    assert err <= DECODE_TOL
+    assert np.all(out[lens == 0] == 0.0)
+
+
 def test_split_count_invariance():
     cfg = W.config(1)
     cfg.lens = np.array([5000], np.int32)
