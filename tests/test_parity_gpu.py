@@ -99,6 +99,22 @@ def test_zero_length_sequences(g, num_splits):
     assert np.all(out[lens == 0] == 0.0)
 
 
+def test_lengths_outside_the_table_are_clamped(monkeypatch):
+    """Without the debug checks a length is clamped to [0, the block-table row's
+    capacity]: past the capacity the output equals the one at the capacity, bit for
+    bit, and a negative length decodes to a zero row."""
+    monkeypatch.delenv("OSCAR_DEBUG", raising=False)
+    cfg = W.custom("clamp", 3, 8, 2, [256, 300, 128], seed_index=240)
+    case = make_case(cfg)
+    pool = gpu_append(case)
+    cap = case.table.shape[1] * 64
+    for S in (1, 3):
+        at_cap = gpu_decode(case, pool, S, lens=np.array([cap, cap, 0], np.int32))
+        past = gpu_decode(case, pool, S, lens=np.array([cap + 50, cap + 100000, -5], np.int32))
+        assert torch.equal(at_cap, past)
+        assert bool((past[2] == 0.0).all())
+
+
 def test_split_count_invariance():
     cfg = W.config(1)
     cfg.lens = np.array([5000], np.int32)
