@@ -159,14 +159,7 @@ __device__ inline float h_lo(uint32_t w) { return __half2float(__ushort_as_half(
 __device__ inline uint32_t comp(uint4 v, int i) { return i == 0 ? v.x : i == 1 ? v.y : i == 2 ? v.z : v.w; }
 __device__ inline float compf(float4 v, int i) { return i == 0 ? v.x : i == 1 ? v.y : i == 2 ? v.z : v.w; }
 
-// Max / sum over the 16 lanes of a row (quad swaps, then row rotations by 4 and 8).
-__device__ inline float row16_max(float x) {
-  x = fmaxf(x, __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(x), 0xB1, 0xF, 0xF, false)));
-  x = fmaxf(x, __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(x), 0x4E, 0xF, 0xF, false)));
-  x = fmaxf(x, __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(x), 0x124, 0xF, 0xF, false)));
-  x = fmaxf(x, __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(x), 0x128, 0xF, 0xF, false)));
-  return x;
-}
+// Sum over the 16 lanes of a row (quad swaps, then row rotations by 4 and 8).
 __device__ inline float row16_sum(float x) {
   x += __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(x), 0xB1, 0xF, 0xF, false));
   x += __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(x), 0x4E, 0xF, 0xF, false));
@@ -174,10 +167,25 @@ __device__ inline float row16_sum(float x) {
   x += __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(x), 0x128, 0xF, 0xF, false));
   return x;
 }
-__device__ inline float quad_max(float x) {
-  x = fmaxf(x, __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(x), 0xB1, 0xF, 0xF, false)));
-  x = fmaxf(x, __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(x), 0x4E, 0xF, 0xF, false)));
-  return x;
+// Max over the lanes l and l ^ 2 of a quad, and over all four lanes of a quad,
+// of non-negative floats (their bit patterns order like their values, so the
+// integer maximum needs no NaN quieting); v_max_u32 with DPP operands, an s_nop
+// before each DPP read of a fresh VALU result.
+__device__ inline float quad_pair_max_pos(float a) {
+  asm volatile(
+      "s_nop 1\n"
+      "v_max_u32_dpp %0, %0, %0 quad_perm:[2,3,0,1] row_mask:0xf bank_mask:0xf\n"
+      : "+v"(a));
+  return a;
+}
+__device__ inline float quad_max_pos(float a) {
+  asm volatile(
+      "s_nop 1\n"
+      "v_max_u32_dpp %0, %0, %0 quad_perm:[1,0,3,2] row_mask:0xf bank_mask:0xf\n"
+      "s_nop 1\n"
+      "v_max_u32_dpp %0, %0, %0 quad_perm:[2,3,0,1] row_mask:0xf bank_mask:0xf\n"
+      : "+v"(a));
+  return a;
 }
 __device__ inline float quad_sum(float x) {
   x += __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(x), 0xB1, 0xF, 0xF, false));
@@ -269,6 +277,14 @@ __device__ inline float rows_max(float x) {
   u = __float_as_uint(x);
   auto b = __builtin_amdgcn_permlane16_swap(u, u, false, false);
   return fmaxf(__uint_as_float(b[0]), __uint_as_float(b[1]));
+}
+// The same maximum for non-negative floats, on their bit patterns.
+__device__ inline float rows_max_pos(float x) {
+  uint32_t u = __float_as_uint(x);
+  auto a = __builtin_amdgcn_permlane32_swap(u, u, false, false);
+  u = max(a[0], a[1]);
+  auto b = __builtin_amdgcn_permlane16_swap(u, u, false, false);
+  return __uint_as_float(max(b[0], b[1]));
 }
 __device__ inline float rows_sum(float x) {
   uint32_t u = __float_as_uint(x);
@@ -444,7 +460,7 @@ __device__ inline void compute_page(WaveState (&st)[NCH], WaveLds<NCH>& L, int t
     }
     // largest V scale of the head on this page (bit patterns of positive scales)
     const uint32_t smax = max3_lo16(max3_lo16(sz[0], sz[1], sz[2]), sz[3], 0u);
-    svmax = rows_max(quad_max(BF ? __uint_as_float(smax << 16) : h_lo(smax)));
+    svmax = rows_max_pos(quad_max_pos(BF ? __uint_as_float(smax << 16) : h_lo(smax)));
   } else if (NG == 2) {
     // two groups per head: lane (head wh, group wg & 1, half wg >> 1) forms the
     // weights of tokens 16*hi + 8*(wg >> 1) + (0..7) of its group, dwords
@@ -465,8 +481,7 @@ __device__ inline void compute_page(WaveState (&st)[NCH], WaveLds<NCH>& L, int t
     const uint32_t smax = max3_lo16(max3_lo16(sz[0], sz[1], sz[2]), max3_lo16(sz[3], sz[4], sz[5]),
                                     max3_lo16(sz[6], sz[7], 0u));
     float sv = BF ? __uint_as_float(smax << 16) : h_lo(smax);
-    sv = fmaxf(sv, __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(sv), 0x4E, 0xF, 0xF, false)));
-    svmax = rows_max(sv);
+    svmax = rows_max_pos(quad_pair_max_pos(sv));
   } else {
     uint4 vz[4];
 #pragma unroll
@@ -485,7 +500,7 @@ __device__ inline void compute_page(WaveState (&st)[NCH], WaveLds<NCH>& L, int t
     for (int e = 0; e < 5; ++e) m5[e] = max3_lo16(sz[3 * e], sz[3 * e + 1], sz[3 * e + 2]);
     m5[5] = sz[15];
     const uint32_t smax = max3_lo16(max3_lo16(m5[0], m5[1], m5[2]), max3_lo16(m5[3], m5[4], m5[5]), 0u);
-    svmax = rows_max(BF ? __uint_as_float(smax << 16) : h_lo(smax));
+    svmax = rows_max_pos(BF ? __uint_as_float(smax << 16) : h_lo(smax));
   }
 
   // ---- per chunk: online softmax of head hi, then the P.V weights w = p * s_v of
@@ -498,7 +513,7 @@ __device__ inline void compute_page(WaveState (&st)[NCH], WaveLds<NCH>& L, int t
 #pragma unroll
     for (int u = 0; u < 4; ++u)
       if (valid(u)) mx = fmaxf(mx, S[c][u]);
-    mx = row16_max(mx) * st[c].sq;  // sq > 0; at least one valid token per page
+    mx = row16_max1(mx) * st[c].sq;  // sq > 0; at least one valid token per page
     const float mn = fmaxf(st[c].m, mx);
     // alpha rescales the head's running sums (1 on the pages where the maximum
     // stays, which is most of them; the multiplies are kept, as a wave-uniform skip
@@ -728,7 +743,7 @@ __device__ inline void compute_page_wide(WideState<NCH>& st, WideLds<NCH>& L, in
         if (!FULL && (4 * (l & 15) + b < t0 || 4 * (l & 15) + b >= t1)) x[b] = 0u;
       mloc = max(max(x[0] & 0xffffu, x[1] & 0xffffu), max(x[2] & 0xffffu, x[3] & 0xffffu));
     }
-    const float sv = rows_max(row16_max1(BF ? __uint_as_float(mloc << 16) : h_lo(mloc)));
+    const float sv = rows_max_pos(row16_max1(BF ? __uint_as_float(mloc << 16) : h_lo(mloc)));
     frexpf(sv, &esv);  // sv < 2^esv
   }
   const float cw = (float)(21 - esv);
