@@ -63,6 +63,11 @@ constexpr float kWMax = 2097152.0f;        // w scale 2^21: 64 * 12 * 2^21 < 2^3
 constexpr float kMagic = 8388608.0f;       // 2^23: x + 2^23 (0 <= x < 2^23) has x in its mantissa
 constexpr float kDigitBias = 32896.0f;     // 128 + 128 * 256 (offset of the two low digits)
 constexpr int kNDig = 3;                   // int8 digits per scaled value (most significant first)
+// A head's reference maximum m moves only on a page whose maximum exceeds it by
+// more than kSlack (log2 units): p and the running sums are relative to m, at most
+// 2^kSlack times their size relative to the true maximum, and they are rescaled on
+// those pages only (a wave-uniform branch).
+constexpr float kSlack = 10.0f;
 // LDS copy of a page-head block, in 16-byte slots.  The placement keeps every LDS
 // instruction of the page loop free of bank conflicts on gfx950, whose ds_read_b128
 // serves a wave in four passes of 16 lanes (4-lane blocks {0,3,5,6}, {1,2,4,7} of
@@ -107,37 +112,62 @@ __device__ inline v4i mfma32acc(long a, long b, v4i c) {
 __device__ inline float ex2(float x) { return __builtin_amdgcn_exp2f(x); }
 
 // v_fma_mix_f32 with one binary16 operand taken from the low / high half of a
-// packed (scale, zero) word: no separate conversion instructions.
-__device__ inline float mix_lo(uint32_t h, float b, float c) {  // lo(h) * b + c
+// packed (scale, zero) word (no conversion instructions), in inline asm whose
+// result overwrites its own addend or multiplicand register.  The compiler places
+// no wait states around inline asm: a result written to a free register could land
+// in one that an MFMA still in flight reads (its operands are dead to the compiler
+// once the MFMA has issued), so every helper writes only a register that holds one
+// of its own live inputs, an LDS or VALU value that is never an MFMA operand or
+// result.  Plain C gives the same instructions here but converts the scales of a
+// whole page at once and spills at 128 VGPRs.
+__device__ inline void mix_lo_acc(uint32_t h, float b, float& acc) {  // acc += lo(h) * b
+  asm("v_fma_mix_f32 %0, %1, %2, %0 op_sel:[0,0,0] op_sel_hi:[1,0,0]" : "+v"(acc) : "v"(h), "v"(b));
+}
+__device__ inline void mix_hi_acc(uint32_t h, float b, float& acc) {  // acc += hi(h) * b
+  asm("v_fma_mix_f32 %0, %1, %2, %0 op_sel:[1,0,0] op_sel_hi:[1,0,0]" : "+v"(acc) : "v"(h), "v"(b));
+}
+__device__ inline void mix_nhi_acc(uint32_t h, float b, float& acc) {  // acc -= hi(h) * b
+  asm("v_fma_mix_f32 %0, -%1, %2, %0 op_sel:[1,0,0] op_sel_hi:[1,0,0]" : "+v"(acc) : "v"(h), "v"(b));
+}
+__device__ inline void mix_lo_mul(uint32_t h, float& b) {  // b = lo(h) * b
+  asm("v_fma_mix_f32 %0, %1, %0, 0 op_sel:[0,0,0] op_sel_hi:[1,0,0]" : "+v"(b) : "v"(h));
+}
+
+// The same for either metadata format: binary16 as above, bfloat16 as the upper
+// bits of a binary32 (a shift or a mask) in plain C.
+template <bool BF>
+__device__ inline void sz_s_acc(uint32_t h, float b, float& acc) {  // acc += s * b
+  if (BF) acc = fmaf(__uint_as_float(h << 16), b, acc);
+  else mix_lo_acc(h, b, acc);
+}
+template <bool BF>
+__device__ inline void sz_z_acc(uint32_t h, float b, float& acc) {  // acc += z * b
+  if (BF) acc = fmaf(__uint_as_float(h & 0xffff0000u), b, acc);
+  else mix_hi_acc(h, b, acc);
+}
+template <bool BF>
+__device__ inline void sz_nz_acc(uint32_t h, float b, float& acc) {  // acc -= z * b
+  if (BF) acc = fmaf(-__uint_as_float(h & 0xffff0000u), b, acc);
+  else mix_nhi_acc(h, b, acc);
+}
+template <bool BF>
+__device__ inline void sz_s_mul(uint32_t h, float& b) {  // b *= s
+  if (BF) b *= __uint_as_float(h << 16);
+  else mix_lo_mul(h, b);
+}
+
+// s * b + c for a binary16 s as one v_fma_mix_f32 in inline asm, for the P.V
+// weights of the wide path: plain C converts a scale once for all chunks and then
+// needs an FMA per chunk as well.  The compiler places no wait states around inline
+// asm, so this is used only where no MFMA can be in flight: after every score MFMA
+// result has been read (the weights depend on the softmax), before the P.V MFMAs
+// (a later basic block).
+template <bool BF>
+__device__ inline float sz_s_fma_asm(uint32_t h, float b, float c) {
+  if (BF) return fmaf(__uint_as_float(h << 16), b, c);
   float r;
   asm("v_fma_mix_f32 %0, %1, %2, %3 op_sel:[0,0,0] op_sel_hi:[1,0,0]" : "=v"(r) : "v"(h), "v"(b), "v"(c));
   return r;
-}
-__device__ inline float mix_hi(uint32_t h, float b, float c) {  // hi(h) * b + c
-  float r;
-  asm("v_fma_mix_f32 %0, %1, %2, %3 op_sel:[1,0,0] op_sel_hi:[1,0,0]" : "=v"(r) : "v"(h), "v"(b), "v"(c));
-  return r;
-}
-__device__ inline float mix_nhi(uint32_t h, float b, float c) {  // -hi(h) * b + c
-  float r;
-  asm("v_fma_mix_f32 %0, -%1, %2, %3 op_sel:[1,0,0] op_sel_hi:[1,0,0]" : "=v"(r) : "v"(h), "v"(b), "v"(c));
-  return r;
-}
-
-// Reads of a packed (scale, zero) word in either metadata format: binary16 via
-// v_fma_mix_f32 (no conversion instructions), bfloat16 as the upper bits of a
-// binary32 (a shift or a mask).
-template <bool BF>
-__device__ inline float sz_s_fma(uint32_t h, float b, float c) {  // s * b + c
-  return BF ? fmaf(__uint_as_float(h << 16), b, c) : mix_lo(h, b, c);
-}
-template <bool BF>
-__device__ inline float sz_z_fma(uint32_t h, float b, float c) {  // z * b + c
-  return BF ? fmaf(__uint_as_float(h & 0xffff0000u), b, c) : mix_hi(h, b, c);
-}
-template <bool BF>
-__device__ inline float sz_nz_fma(uint32_t h, float b, float c) {  // -z * b + c
-  return BF ? fmaf(-__uint_as_float(h & 0xffff0000u), b, c) : mix_nhi(h, b, c);
 }
 
 // s * b + c with s read from a packed (scale, zero) word, in plain C (v_fma_mix_f32
@@ -150,9 +180,8 @@ __device__ inline float sz_s_fma_c(uint32_t h, float b, float c) {
 
 // unsigned maximum of the low halves of three words (high half of the result unused)
 __device__ inline uint32_t max3_lo16(uint32_t a, uint32_t b, uint32_t c) {
-  uint32_t r;
-  asm("v_max3_u16 %0, %1, %2, %3" : "=v"(r) : "v"(a), "v"(b), "v"(c));
-  return r;
+  const uint16_t m = max(max((uint16_t)a, (uint16_t)b), (uint16_t)c);
+  return m;
 }
 
 __device__ inline float h_lo(uint32_t w) { return __half2float(__ushort_as_half((uint16_t)(w & 0xffffu))); }
@@ -169,18 +198,20 @@ __device__ inline float row16_sum(float x) {
 }
 // Max over the lanes l and l ^ 2 of a quad, and over all four lanes of a quad,
 // of non-negative floats (their bit patterns order like their values, so the
-// integer maximum needs no NaN quieting); v_max_u32 with DPP operands, an s_nop
-// before each DPP read of a fresh VALU result.
+// integer maximum needs no NaN quieting); v_max_u32 with DPP operands.  The asm
+// DPP helpers start with s_nop 4: the compiler does not see their DPP reads, and
+// an EXEC write by a scalar instruction needs 5 wait states before one (a VALU
+// result 2); the later s_nops cover the dependent steps.
 __device__ inline float quad_pair_max_pos(float a) {
   asm volatile(
-      "s_nop 1\n"
+      "s_nop 4\n"
       "v_max_u32_dpp %0, %0, %0 quad_perm:[2,3,0,1] row_mask:0xf bank_mask:0xf\n"
       : "+v"(a));
   return a;
 }
 __device__ inline float quad_max_pos(float a) {
   asm volatile(
-      "s_nop 1\n"
+      "s_nop 4\n"
       "v_max_u32_dpp %0, %0, %0 quad_perm:[1,0,3,2] row_mask:0xf bank_mask:0xf\n"
       "s_nop 1\n"
       "v_max_u32_dpp %0, %0, %0 quad_perm:[2,3,0,1] row_mask:0xf bank_mask:0xf\n"
@@ -195,10 +226,10 @@ __device__ inline float quad_sum(float x) {
 // Max over the 16 lanes of a row for four values at once: v_max_f32 with DPP
 // operands (quad swaps, then row rotations by 4 and 8), the four chains
 // interleaved so that every DPP read is 3 instructions after the write it reads
-// (2 wait states required; the leading s_nop covers the inputs' writes).
+// (2 wait states required).
 __device__ inline void row16_max4(float& a, float& b, float& c, float& d) {
   asm volatile(
-      "s_nop 1\n"
+      "s_nop 4\n"
       "v_max_f32_dpp %0, %0, %0 quad_perm:[1,0,3,2] row_mask:0xf bank_mask:0xf\n"
       "v_max_f32_dpp %1, %1, %1 quad_perm:[1,0,3,2] row_mask:0xf bank_mask:0xf\n"
       "v_max_f32_dpp %2, %2, %2 quad_perm:[1,0,3,2] row_mask:0xf bank_mask:0xf\n"
@@ -221,7 +252,7 @@ __device__ inline void row16_max4(float& a, float& b, float& c, float& d) {
 // instructions after its write).
 __device__ inline void row16_max3(float& a, float& b, float& c) {
   asm volatile(
-      "s_nop 1\n"
+      "s_nop 4\n"
       "v_max_f32_dpp %0, %0, %0 quad_perm:[1,0,3,2] row_mask:0xf bank_mask:0xf\n"
       "v_max_f32_dpp %1, %1, %1 quad_perm:[1,0,3,2] row_mask:0xf bank_mask:0xf\n"
       "v_max_f32_dpp %2, %2, %2 quad_perm:[1,0,3,2] row_mask:0xf bank_mask:0xf\n"
@@ -239,7 +270,7 @@ __device__ inline void row16_max3(float& a, float& b, float& c) {
 // The same for two values (s_nop between the dependent pairs).
 __device__ inline void row16_max2(float& a, float& b) {
   asm volatile(
-      "s_nop 1\n"
+      "s_nop 4\n"
       "v_max_f32_dpp %0, %0, %0 quad_perm:[1,0,3,2] row_mask:0xf bank_mask:0xf\n"
       "v_max_f32_dpp %1, %1, %1 quad_perm:[1,0,3,2] row_mask:0xf bank_mask:0xf\n"
       "s_nop 0\n"
@@ -256,7 +287,7 @@ __device__ inline void row16_max2(float& a, float& b) {
 // The same for one value (s_nop between the dependent steps).
 __device__ inline float row16_max1(float a) {
   asm volatile(
-      "s_nop 1\n"
+      "s_nop 4\n"
       "v_max_f32_dpp %0, %0, %0 quad_perm:[1,0,3,2] row_mask:0xf bank_mask:0xf\n"
       "s_nop 1\n"
       "v_max_f32_dpp %0, %0, %0 quad_perm:[2,3,0,1] row_mask:0xf bank_mask:0xf\n"
@@ -413,7 +444,14 @@ __device__ inline void compute_page(WaveState (&st)[NCH], WaveLds<NCH>& L, int t
           const int t = combine3(d[0], d[1], d[2]);
           const uint32_t sz = comp(ksz[g], u);
           // s * (acc - z * sum q_int) with s, z read from the packed pair
-          acc[c] = sz_s_fma<BF>(sz, sz_nz_fma<BF>(sz, st[c].qs[g], (float)t), acc[c]);
+          float y = (float)t;
+          sz_nz_acc<BF>(sz, st[c].qs[g], y);
+          if (g == 0) {
+            sz_s_mul<BF>(sz, y);
+            acc[c] = y;
+          } else {
+            sz_s_acc<BF>(sz, y, acc[c]);
+          }
         } else {
           const int j = g * NG / 4;  // the slice's group
           if (g % (4 / NG) == 0) dg[c][j] = mfma32(st[c].aq[g], b);
@@ -428,14 +466,24 @@ __device__ inline void compute_page(WaveState (&st)[NCH], WaveLds<NCH>& L, int t
         for (int j = 0; j < 2; ++j) {
           const uint32_t sz = comp(ksz[j], u);
           const int t = combine3(dg[c][j][0], dg[c][j][1], dg[c][j][2]);
-          acc[c] = sz_s_fma<BF>(sz, sz_nz_fma<BF>(sz, st[c].qs[j], (float)t), acc[c]);
+          float y = (float)t;
+          sz_nz_acc<BF>(sz, st[c].qs[j], y);
+          if (j == 0) {
+            sz_s_mul<BF>(sz, y);
+            acc[c] = y;
+          } else {
+            sz_s_acc<BF>(sz, y, acc[c]);
+          }
         }
       } else if (NG == 1) {
         // 128 channels: the combined sum can exceed int32, so the digits are combined
         // in fp32: 256 d_1 + d_2 is exact (< 2^24), and one rounding adds 65536 d_0
         const uint32_t sz = comp(ksz[0], u);
         const float T = fmaf((float)dg[c][0][0], 65536.0f, fmaf((float)dg[c][0][1], 256.0f, (float)dg[c][0][2]));
-        acc[c] = sz_s_fma<BF>(sz, sz_nz_fma<BF>(sz, st[c].qs[0], T), 0.0f);
+        float y = T;
+        sz_nz_acc<BF>(sz, st[c].qs[0], y);
+        sz_s_mul<BF>(sz, y);
+        acc[c] = y;
       }
       S[c][u] = acc[c];
     }
@@ -516,8 +564,9 @@ __device__ inline void compute_page(WaveState (&st)[NCH], WaveLds<NCH>& L, int t
     mx = row16_max1(mx) * st[c].sq;  // sq > 0; at least one valid token per page
     const float mn = fmaxf(st[c].m, mx);
     // alpha rescales the head's running sums (1 on the pages where the maximum
-    // stays, which is most of them; the multiplies are kept, as a wave-uniform skip
-    // would save about 1 % of the page's VALU)
+    // stays, which is most of them; the multiplies are kept: a wave-uniform skip
+    // with a reference maximum that moves lazily needs registers that the
+    // 4-waves-per-SIMD budget does not have)
     alpha[c] = ex2(st[c].m - mn);  // m = -inf on the first page -> 0
     const float pmax = ex2(mx - mn);
     float p[4];
@@ -548,11 +597,12 @@ __device__ inline void compute_page(WaveState (&st)[NCH], WaveLds<NCH>& L, int t
 #pragma unroll
       for (int b = 0; b < 4; ++b) {
         const int e = 4 * j + b;
-        const float w = sz_s_fma<BF>(sz[e], compf(pw, b), 0.0f);
+        float w = compf(pw, b);
+        sz_s_mul<BF>(sz[e], w);
         // mantissa of rne(w * inv) + 2^23 + 32896 = k + 32896, k in [0, 2^21]:
         // k = 65536 d_0 + 256 d_1 + d_2 with d_2, d_1 = (bytes 0, 1) ^ 0x80, d_0 = byte 2
         f[b] = __float_as_uint(fmaf(w, inv, kMagic + kDigitBias));
-        zp = sz_z_fma<BF>(sz[e], w, zp);  // unquantized w: differs from the quantized by <= 2^-22 sig
+        sz_z_acc<BF>(sz[e], w, zp);  // unquantized w: differs from the quantized by <= 2^-22 sig
       }
       const uint32_t t01 = __builtin_amdgcn_perm(f[1], f[0], 0x05010400u) ^ 0x80808080u;  // [f0.0 f1.0 f0.1 f1.1]
       const uint32_t t23 = __builtin_amdgcn_perm(f[3], f[2], 0x05010400u) ^ 0x80808080u;
@@ -653,7 +703,6 @@ __device__ inline void compute_page(WaveState (&st)[NCH], WaveLds<NCH>& L, int t
 // that only moves when a page's maximum exceeds it by more than kSlack (sums
 // relative to m then stay below 2^kSlack times their true size; the running
 // sums are rescaled only on those pages).
-constexpr float kSlack = 10.0f;
 
 typedef _Float16 h8 __attribute__((ext_vector_type(8)));
 typedef float f4v __attribute__((ext_vector_type(4)));
@@ -900,10 +949,7 @@ __device__ inline void compute_page_wide(WideState<NCH>& st, WideLds<NCH>& L, in
       for (int b = 0; b < 4; ++b) {
         const int e = 4 * j + b;
         // mantissa of rne(w') + 2^23 + 32896 = k + 32896, k in [0, 2^21] (as above)
-        // (inline asm: its inputs and result are LDS and VALU values, never MFMA
-        // operands or results; as plain C the compiler converts s once for all
-        // chunks and then needs a conversion and an FMA where one mixed FMA does)
-        f[b] = __float_as_uint(sz_s_fma<BF>(sz[e], compf(pw, b), magic));
+        f[b] = __float_as_uint(sz_s_fma_asm<BF>(sz[e], compf(pw, b), magic));
         zp = fmaf(szp[e], compf(pw, b), zp);
       }
       const uint32_t t01 = __builtin_amdgcn_perm(f[1], f[0], 0x05010400u) ^ 0x80808080u;
