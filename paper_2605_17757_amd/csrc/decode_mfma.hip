@@ -111,6 +111,13 @@ __device__ inline v4i mfma32acc(long a, long b, v4i c) {
 // raw v_exp_f32 (results below 2^-126 flush to 0: negligible softmax weights)
 __device__ inline float ex2(float x) { return __builtin_amdgcn_exp2f(x); }
 
+// Lanes of a wave hand values to each other through LDS (one lane writes, others
+// read).  A wave's LDS operations run in order, so no instruction is needed, but to
+// the compiler each lane is a thread of its own: without this wavefront-scope fence
+// it may move a lane's read of another lane's value above that lane's write (it did
+// for a write made by one lane of each row).
+__device__ inline void lane_exchange() { __builtin_amdgcn_fence(__ATOMIC_ACQ_REL, "wavefront"); }
+
 // v_fma_mix_f32 with one binary16 operand taken from the low / high half of a
 // packed (scale, zero) word (no conversion instructions), in inline asm whose
 // result overwrites its own addend or multiplicand register.  The compiler places
@@ -377,6 +384,7 @@ __device__ inline void stage_load(Stage& s, const uint8_t* __restrict__ blk, int
 }
 template <int NG>
 __device__ inline void stage_store(uint4* page, const Stage& s, int l) {
+  lane_exchange();  // after every lane's reads of the previous page
   u4* dst = reinterpret_cast<u4*>(page);
   const int a = l + (l >> 3);                  // K codes
   const int v = l ^ (((l >> 4) & 1) << 1);     // V codes
@@ -393,6 +401,7 @@ __device__ inline void stage_store(uint4* page, const Stage& s, int l) {
   } else if (l < 32) {   // chunk 256 + l: K (s, z) for l < 16, V (s, z) chunk l - 16
     dst[l < 16 ? kSlotKSz + l : kSlotVSz + l - 16] = s.v4;
   }
+  lane_exchange();  // before any lane reads the page
 }
 
 struct WaveState {
@@ -570,16 +579,14 @@ __device__ inline void compute_page(WaveState (&st)[NCH], WaveLds<NCH>& L, int t
     alpha[c] = ex2(st[c].m - mn);  // m = -inf on the first page -> 0
     const float pmax = ex2(mx - mn);
     float p[4];
-    float ls = 0.0f;
 #pragma unroll
-    for (int u = 0; u < 4; ++u) {
-      p[u] = valid(u) ? ex2(fmaf(st[c].sq, S[c][u], -mn)) : 0.0f;
-      ls += p[u];
-    }
+    for (int u = 0; u < 4; ++u) p[u] = valid(u) ? ex2(fmaf(st[c].sq, S[c][u], -mn)) : 0.0f;
+    const float ls = ((p[0] + p[1]) + p[2]) + p[3];  // p >= 0: the sum from 0 without the 0 + p[0]
     st[c].lsum = fmaf(st[c].lsum, alpha[c], ls);
     st[c].m = mn;
     L.p[hi][lo] = make_float4(p[0], p[1], p[2], p[3]);
     L.hs[hi] = make_float2(alpha[c], pmax);  // every lane of the row writes the same value
+    lane_exchange();
 
     char* wbase = c == 0 ? pb : reinterpret_cast<char*>(L.wdig[c == 0 ? 0 : c - 1]);
     const float2 hsw = L.hs[wh];
@@ -633,6 +640,7 @@ __device__ inline void compute_page(WaveState (&st)[NCH], WaveLds<NCH>& L, int t
     st[c].zacc = fmaf(st[c].zacc, hsw.x, zp);
   }
 
+  lane_exchange();
   // ---- P.V on the matrix cores: lane (channel column, head hi), every chunk ----
   // B operand: field 2F + (lo>>3) of each token's byte, taken in place by the mask
   // mk = 3 << 2(lo>>3): columns lo >= 8 hold 4 x code (undone when the state is written)
@@ -737,7 +745,8 @@ template <int NCH>
 struct WideLds : WideLdsX<NCH> {
   uint4 page[kSlots];            // page-head block (slot placement above)
   uint4 wdig[NCH][kWSlots];      // weight digits of each chunk
-  float2 hs[16];                 // per head on this page: (PV scale ws, rescale factor)
+  float wsh[16];                 // per head on this page: P.V scale ws
+  float alh[16];                 // per head: rescale factor alpha (pages that move m)
 };
 template <int NCH>
 __device__ inline float4* wide_pq(WideLds<NCH>& L) {
@@ -856,17 +865,29 @@ __device__ inline void compute_page_wide(WideState<NCH>& st, WideLds<NCH>& L, in
     mx[j] *= st.sq[j];
     need = need || !(mx[j] <= st.m[j] + kSlack);
   }
-  const bool resc = __ballot(need) != 0ull;  // wave-uniform
-  float alpha[HPL];
-#pragma unroll
-  for (int j = 0; j < NJ; ++j) alpha[j] = 1.0f;
-  if (resc) {
+  if (__ballot(need) != 0ull) {  // wave-uniform
+    float alpha[HPL];
 #pragma unroll
     for (int j = 0; j < NJ; ++j) {
       const float mn = fmaxf(st.m[j], mx[j]);
       alpha[j] = ex2(st.m[j] - mn);  // m = -inf on the first page -> 0
       st.m[j] = mn;
       st.lsum[j] *= alpha[j];
+    }
+    // each head's alpha through LDS to the zero-point sums (head 4c + (lo>>2)) and
+    // the o~ accumulators (head 4c + hi) of the lane
+#pragma unroll
+    for (int j = 0; j < NJ; ++j) {
+      const int hh = WideRows<NCH>::lane_head(hi, j);
+      if (hh < 4 * NCH) L.alh[hh] = alpha[j];  // every lane of the row writes the same value
+    }
+    lane_exchange();
+#pragma unroll
+    for (int c = 0; c < NCH; ++c) {
+      st.zacc[c] *= L.alh[4 * c + (lo >> 2)];
+      const float a = L.alh[4 * c + hi];
+#pragma unroll
+      for (int k = 0; k < 8; ++k) st.of[c][k] *= a;
     }
   }
   float4* pq = wide_pq(L);
@@ -876,18 +897,16 @@ __device__ inline void compute_page_wide(WideState<NCH>& st, WideLds<NCH>& L, in
     const float c = cw - mx[j];
     const float ws = ex2(mx[j] - st.m[j] - cw);
     float pv[4];
-    float ls = 0.0f;
 #pragma unroll
-    for (int u = 0; u < 4; ++u) {
-      pv[u] = valid(u) ? ex2(fmaf(st.sq[j], acc[u][j], c)) : 0.0f;
-      ls += pv[u];
-    }
+    for (int u = 0; u < 4; ++u) pv[u] = valid(u) ? ex2(fmaf(st.sq[j], acc[u][j], c)) : 0.0f;
+    const float ls = ((pv[0] + pv[1]) + pv[2]) + pv[3];
     st.lsum[j] = fmaf(ls, ws, st.lsum[j]);
     if (hh < 4 * NCH) {
       pq[hh * 17 + lo] = make_float4(pv[0], pv[1], pv[2], pv[3]);
-      if (lo == 0) L.hs[hh] = make_float2(ws, alpha[j]);
+      L.wsh[hh] = ws;  // every lane of the row writes the same value
     }
   }
+  lane_exchange();
 
   const int wh = lo >> 2, wg = lo & 3;
   // ---- per chunk: the P.V weights w' = s_v p' of (head 4c + wh, group wg) as three
@@ -935,7 +954,7 @@ __device__ inline void compute_page_wide(WideState<NCH>& st, WideLds<NCH>& L, in
 #pragma unroll
   for (int c = 0; c < NCH; ++c) {
     const int hh = 4 * c + wh;
-    const float2 hsw = L.hs[hh];
+    const float wsv = L.wsh[hh];
     char* wbase = reinterpret_cast<char*>(L.wdig[c]);
     float zp = 0.0f;
     constexpr int NJ = NE / 4;
@@ -975,22 +994,17 @@ __device__ inline void compute_page_wide(WideState<NCH>& st, WideLds<NCH>& L, in
       for (int dg = 0; dg < kNDig; ++dg)
         *reinterpret_cast<uint4*>(wp + 16 * dg) = make_uint4(aw[dg][0], aw[dg][1], aw[dg][2], aw[dg][3]);
     }
-    st.zacc[c] = fmaf(zp, hsw.x, st.zacc[c] * hsw.y);
+    st.zacc[c] = fmaf(zp, wsv, st.zacc[c]);
   }
 
+  lane_exchange();
   // ---- P.V on the int8 matrix cores: lane (channel column, head hi), every chunk ----
   const uint32_t mk = 0x03030303u << (2 * (lo >> 3));
   const char* vb = pb + kLdsVCodes + 16 * (4 * (lo & 7) + (hi ^ (((lo >> 2) & 1) << 1)));
   const int arow = 16 * (w_slot(lo >> 2, hi) + min(lo & 3, 2));
   float wsc[NCH];
 #pragma unroll
-  for (int c = 0; c < NCH; ++c) {
-    const float2 h = L.hs[4 * c + hi];
-    wsc[c] = h.x;
-    if (resc)
-#pragma unroll
-      for (int k = 0; k < 8; ++k) st.of[c][k] *= h.y;
-  }
+  for (int c = 0; c < NCH; ++c) wsc[c] = L.wsh[4 * c + hi];
 #pragma unroll
   for (int G = 0; G < 4; ++G) {
     v4i aop[NCH];
@@ -1168,6 +1182,7 @@ __device__ __attribute__((always_inline)) inline void process_piece(WaveLds<NCH>
     }
     L.qs[lo] = dsel == 0 ? qsum[0] : dsel == 1 ? qsum[1] : dsel == 2 ? qsum[2] : qsum[3];  // (head h, group dsel)
     L.sq[h] = sq;  // lanes of equal h write equal values
+    lane_exchange();
     const int4 q4 = *reinterpret_cast<const int4*>(&L.qs[4 * hi]);
     if (NG == 4) {
       sc.qs[0] = (float)q4.x; sc.qs[1] = (float)q4.y; sc.qs[2] = (float)q4.z; sc.qs[3] = (float)q4.w;
@@ -1201,6 +1216,7 @@ __device__ __attribute__((always_inline)) inline void process_piece(WaveLds<NCH>
     if (NG == 2)                            // the group's halves: lanes wg and wg ^ 2
       ztot += __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(ztot), 0x4E, 0xF, 0xF, false));
     L.ws[0][lo] = ztot;                     // lanes of equal lo write equal values
+    lane_exchange();
     const float4 zh = *reinterpret_cast<const float4*>(&L.ws[0][4 * hi]);
     const int hout = 4 * chunk + hi;        // head of this lane's accumulators
     if (hout >= g_heads) continue;          // padding head
@@ -1302,7 +1318,8 @@ __device__ __attribute__((always_inline)) inline void process_piece_wide(
     else gsum = hi == 0 ? (ps[0] + ps[1]) + (ps[2] + ps[3]) : 0.0f;
     st.az = RPH == 2 && (lo & 1) ? 0.0f : gsum * E * (1.0f / 16777216.0f);  // one row per head
     float* sqh = reinterpret_cast<float*>(L.page);  // the page is staged after this
-    if (hi == 0) sqh[hq] = sqv;                      // lanes of equal hq write equal values
+    sqh[hq] = sqv;  // lanes of equal hq write equal values
+    lane_exchange();
 #pragma unroll
     for (int j = 0; j < HPL; ++j) {
       st.sq[j] = sqh[j < NJ ? WideRows<NCH>::lane_head(hi, j) : 0];
@@ -1347,6 +1364,7 @@ __device__ __attribute__((always_inline)) inline void process_piece_wide(
     if (NG == 2) ztot += __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(ztot), 0x4E, 0xF, 0xF, false));
     zx[16 * c + lo] = ztot;  // lanes of equal lo write equal values
   }
+  lane_exchange();
   const bool empty = p0 >= p1;
   const float cs = lo >= 8 ? 0.25f : 1.0f;  // P.V columns lo >= 8 accumulate 4 x code
 #pragma unroll
