@@ -531,8 +531,10 @@ __device__ inline void append_body(float* Rs, double (*xs)[RW][kD], int is_v, in
   const int l = threadIdx.x & 63;
   const int n_items = (n_seq + RW - 1) / RW;
 
-  // each wave owns xs[w]: no block-level synchronization inside the loop
+  // each wave owns xs[w]: no block-level synchronization inside the loop, only
+  // fences around the exchange between its lanes
   for (int item = bx * kWaves + w; item < n_items; item += gx * kWaves) {
+    lane_exchange();  // the previous item's reads of xs[w] come first
 #pragma unroll
     for (int rr = 0; rr < RW; ++rr) {
       const int row = row_at(item * RW + rr);
@@ -547,6 +549,7 @@ __device__ inline void append_body(float* Rs, double (*xs)[RW][kD], int is_v, in
       xs[w][rr][2 * l + 1] = x1;
       rows.copy(row, is_v, l);
     }
+    lane_exchange();
 
     double acc0[RW], acc1[RW];
     if (R) {
@@ -836,6 +839,7 @@ __global__ __launch_bounds__(512) void append_mfma_kernel(
   for (; item < n_items; item += stride) {
     // stage the item's rows (and their bf16 copies, if any), then fetch the next
     const int64_t slot_l = slot_n;
+    lane_exchange();  // the previous item's reads of the wave's area come first
 #pragma unroll
     for (int rr = 0; rr < kMfmaRows; ++rr) {
       area[rr * kStagePitch + l] = nxt[rr];
@@ -844,6 +848,7 @@ __global__ __launch_bounds__(512) void append_mfma_kernel(
       if (d) d[l] = nxt[rr];
     }
     if (item + stride < n_items) fetch(item + stride);
+    lane_exchange();
     if (R) {
       d4v acc[8];
 #pragma unroll
@@ -859,6 +864,7 @@ __global__ __launch_bounds__(512) void append_mfma_kernel(
           acc[tt] = __builtin_amdgcn_mfma_f64_16x16x4f64(a, (double)rb[tt], acc[tt], 0, 0, 0);
       }
       // x~ rows to LDS as fp32 (the staged rows are no longer read)
+      lane_exchange();
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
         float* dst = xt + (kq + 4 * i) * kXtPitch + 8 * j;
@@ -870,6 +876,7 @@ __global__ __launch_bounds__(512) void append_mfma_kernel(
                         __double2float_rn(acc[6][i]), __double2float_rn(acc[7][i]));
       }
     }
+    lane_exchange();  // x~ (or the staged rows) before the quantizer's reads
     if (!fmt.quantile) {  // lane l: row l / 4, channels 32 (l % 4) .. + 31
       const int rr = l >> 2, q = l & 3;
       float x[32];
@@ -1014,8 +1021,10 @@ __global__ __launch_bounds__(256) void clip_err_kernel(const uint16_t* __restric
   for (int i = bx * kWaves + w; i < n_seq; i += gx * kWaves) {
     const int row = fmt.rph ? i * Hkv + h : i;
     const uint32_t pair = reinterpret_cast<const uint32_t*>(x + (size_t)row * kD)[l];
+    lane_exchange();  // the previous row's reads of xs[w] come first
     xs[w][2 * l] = (double)__uint_as_float(pair << 16);
     xs[w][2 * l + 1] = (double)__uint_as_float(pair & 0xffff0000u);
+    lane_exchange();
     double acc0 = 0.0, acc1 = 0.0;
     if (R) {
 #pragma unroll 4

@@ -210,6 +210,7 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(3, 3))) void
         for (int ct = 0; ct < 8; ++ct) o[ct][i] *= alpha;
       }
     }
+    lane_exchange();  // after every lane's reads of the previous page's p
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
       float pv[4];
@@ -220,6 +221,7 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(3, 3))) void
       }
       ps[4 * hi + i][lo] = make_float4(pv[0], pv[1], pv[2], pv[3]);
     }
+    lane_exchange();
     // ---- P.V: p of head lo, tokens 16hi + 8kt + (0..7) ----
 #pragma unroll
     for (int kt = 0; kt < 2; ++kt) {

@@ -547,16 +547,19 @@ __global__ __launch_bounds__(kVecWaves * 64) void jacobi_vectors_kernel(
         round_pair(t % kJacRounds, l, p, q);
         const double2 c = buf[i];
         __builtin_amdgcn_wave_barrier();
+        lane_exchange();
         const double vp = vr[w][p], vq = vr[w][q];
         vr[w][p] = c.x * vp - c.y * vq;
         vr[w][q] = c.y * vp + c.x * vq;
         __builtin_amdgcn_wave_barrier();
+        lane_exchange();
         const int tn = t + kVecAhead;
         buf[i] = tn < R ? rm[(size_t)tn * kJacPairs + l] : make_double2(1.0, 0.0);
       }
     }
   }
   __builtin_amdgcn_wave_barrier();
+  lane_exchange();
   double* vo = V + ((size_t)mtx * kD + row) * kD;
   vo[l] = vr[w][l];
   vo[l + 64] = vr[w][l + 64];

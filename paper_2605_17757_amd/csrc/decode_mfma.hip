@@ -111,13 +111,6 @@ __device__ inline v4i mfma32acc(long a, long b, v4i c) {
 // raw v_exp_f32 (results below 2^-126 flush to 0: negligible softmax weights)
 __device__ inline float ex2(float x) { return __builtin_amdgcn_exp2f(x); }
 
-// Lanes of a wave hand values to each other through LDS (one lane writes, others
-// read).  A wave's LDS operations run in order, so no instruction is needed, but to
-// the compiler each lane is a thread of its own: without this wavefront-scope fence
-// it may move a lane's read of another lane's value above that lane's write (it did
-// for a write made by one lane of each row).
-__device__ inline void lane_exchange() { __builtin_amdgcn_fence(__ATOMIC_ACQ_REL, "wavefront"); }
-
 // v_fma_mix_f32 with one binary16 operand taken from the low / high half of a
 // packed (scale, zero) word (no conversion instructions), in inline asm whose
 // result overwrites its own addend or multiplicand register.  The compiler places

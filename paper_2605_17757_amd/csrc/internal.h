@@ -22,6 +22,13 @@ __host__ __device__ constexpr int off_vsz(int ng) { return kOffKSz + sz_bytes(ng
 __host__ __device__ constexpr int block_bytes(int ng) { return 2 * kCodeBytes + 2 * sz_bytes(ng); }
 constexpr int kMaxGroupHeads = 16;                 // query heads per kv-head
 
+// Lanes of one wave hand values to each other through LDS.  The hardware runs a
+// wave's LDS operations in order, so no instruction is needed, but to the compiler
+// each lane is a thread of its own: without a wavefront-scope fence between the
+// writes and the reads it may move a lane's read of another lane's value above
+// that lane's write.
+__device__ inline void lane_exchange() { __builtin_amdgcn_fence(__ATOMIC_ACQ_REL, "wavefront"); }
+
 // Split kernel geometry: a wave handles all query heads of its kv-head in chunks
 // of 4, and the number of chunks sets its registers, hence the waves per CU.
 inline int split_chunks(int heads_per_kv) { return (heads_per_kv + 3) / 4; }

@@ -151,12 +151,14 @@ __attribute__((amdgpu_waves_per_eu(NH > 8 ? 2 : 4, NH > 8 ? 2 : 4))) void seg_pa
 #pragma unroll
     for (int half = 0; half < 2; ++half) {
       __builtin_amdgcn_wave_barrier();
+      lane_exchange();
       {  // half rows of this channel half: row 8 i + l / 8, piece l % 8
         u4v* dst = kr + kPitch * (l >> 3) + (l & 7);
 #pragma unroll
         for (int i = 0; i < 8; ++i) dst[8 * kPitch * i] = kv[8 * half + i];
       }
       __builtin_amdgcn_wave_barrier();
+      lane_exchange();
       if (half == 1) {  // the K registers are free: the remaining V dwords
         __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
@@ -175,6 +177,7 @@ __attribute__((amdgpu_waves_per_eu(NH > 8 ? 2 : 4, NH > 8 ? 2 : 4))) void seg_pa
       }
     }
     __builtin_amdgcn_wave_barrier();
+    lane_exchange();
     float alpha[NH];
 #pragma unroll
     for (int h = 0; h < NH; ++h) {
@@ -188,6 +191,7 @@ __attribute__((amdgpu_waves_per_eu(NH > 8 ? 2 : 4, NH > 8 ? 2 : 4))) void seg_pa
       pw[l * NH + h] = p;  // over the staged rows: a wave's LDS accesses run in order
     }
     __builtin_amdgcn_wave_barrier();
+    lane_exchange();
 #pragma unroll
     for (int h = 0; h < NH; ++h) { a0[h] *= alpha[h]; a1[h] *= alpha[h]; }
 #pragma unroll
@@ -201,6 +205,7 @@ __attribute__((amdgpu_waves_per_eu(NH > 8 ? 2 : 4, NH > 8 ? 2 : 4))) void seg_pa
       }
     }
     __builtin_amdgcn_wave_barrier();
+    lane_exchange();
   }
 
   __syncthreads();  // the staging area becomes the merge area
