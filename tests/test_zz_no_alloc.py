@@ -48,6 +48,14 @@ def test_noalloc_matches_workspace_entry_point_two_calls():
     _check(make_case(small), 3)
 
 
+def test_noalloc_wide_instances():
+    """8 and 12 query heads per KV head (the wide split instances), after each other."""
+    for g, seed in ((8, 73), (12, 74)):
+        case = make_case(W.custom("noalloc_g%d" % g, 3, 2 * g, 2, [1500, 64, 333], seed_index=seed,
+                                  k_outliers=(3, 40)))
+        _check(case, 4)
+
+
 def test_noalloc_rejects_oversized_workspace():
     lay = ok.Layout(num_kv_heads=8, num_pages=1)
     B, Hq, S = 512, 64, 64
