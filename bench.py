@@ -30,7 +30,9 @@ oscar_mixed_append.  `calibration` times the offline calibration of one layer
 shaped layer (64/8 heads, batch 128, 32768 tokens; with its bf16 baseline) and
 the long-context layer (96/8 heads, batch 16, 131072 tokens, Student-t keys,
 64 splits), each with its split kernel's roofline and the pieces per sequence
-the split produces.  `small_configs` times the cache-resident workloads (tiny
+the split produces; `c3_tp8_share` is one GPU's share of the Qwen3-32B-shaped
+layer under 8-way KV-head sharding (one KV head, 8 query heads, batch 128, 32768
+tokens).  `small_configs` times the cache-resident workloads (tiny
 4/1 x 256, Qwen3-4B 8192, Qwen3-8B batch 1) warm and cold (a 1 GiB buffer
 written between the calls, outside the events), with the oracle on one host
 thread and on all of them.  `read_probe_ex` is the streaming-read probe over
@@ -61,7 +63,7 @@ def parse():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=50)
     ap.add_argument("--warmup", type=int, default=10)
-    ap.add_argument("--config", type=int, default=2, help="workload index 0..4 (default 2)")
+    ap.add_argument("--config", type=int, default=2, help="workload index 0..5 (default 2)")
     ap.add_argument("--batch", type=int, default=None, help="batch override (config 2: 64)")
     ap.add_argument("--num-splits", type=int, default=0, help="0 = library default")
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -654,6 +656,8 @@ def main():
         res["c3_qwen3_32b_b128"] = config_row(args, 3, not args.no_bf16_baseline)
         torch.cuda.empty_cache()
         res["c4_longctx_b16"] = config_row(args, 4, not args.no_bf16_baseline)
+        torch.cuda.empty_cache()
+        res["c3_tp8_share"] = config_row(args, 5, False)
         torch.cuda.empty_cache()
     if not args.no_small:
         res["small_configs"] = small_config_rows(args, not args.no_cpu_baseline)

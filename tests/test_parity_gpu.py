@@ -53,6 +53,15 @@ def test_config3_shape_reduced_batch_and_length():
     _run_full(make_case(cfg))
 
 
+def test_config5_tp8_share_single_kv_head():
+    # one GPU's share of the Qwen3-32B heads under 8-way KV-head sharding: one KV
+    # head and its 8 query heads, at batch 5 and ragged 1k-4k tokens
+    cfg = W.config(5, batch=5)
+    cfg.lens = np.array([4096, 1, 2049, 1000, 3007], np.int32)
+    _run_full(make_case(cfg))
+    _run_full(make_case(cfg), num_splits=7)
+
+
 def test_config4_shape_student_t_many_splits():
     # 96/8 heads (GQA 12), Student-t keys, distinct rotations, >= 64 splits
     cfg = W.config(4, batch=2)

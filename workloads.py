@@ -80,7 +80,9 @@ def _outlier_channels(seed: int, n: int, d: int) -> tuple:
 
 
 def config(index: int, batch: int | None = None) -> Config:
-    """The five workloads.  ``batch`` selects batch 1 or 64 for config 2."""
+    """The workloads (0-4: the five of the hot-path table; 5: one GPU's share of
+    workload 3 under 8-way KV-head sharding).  ``batch`` selects batch 1 or 64 for
+    config 2."""
     base = BASE_SEED + 1000 * index
     if index == 0:
         # Tiny single layer: 4/1 heads, 256 tokens, K channels 3 and 77 x20.
@@ -112,7 +114,14 @@ def config(index: int, batch: int | None = None) -> Config:
         B = 16 if batch is None else int(batch)
         return Config("longctx_b%d_h96x8_ctx128k" % B, 4, B, 96, 8,
                       np.full(B, 131072, np.int32), k_dist="student_t3", min_splits=64)
-    raise ValueError("config index must be 0..4")
+    if index == 5:
+        # One GPU's share of the Qwen3-32B-shaped layer under 8-way KV-head sharding:
+        # one KV head and its 8 query heads, batch 128, 32768 tokens.
+        B = 128 if batch is None else int(batch)
+        return Config("qwen3_32b_tp8_share_b%d_ctx32k" % B, 5, B, 8, 1, np.full(B, 32768, np.int32),
+                      k_outliers=_outlier_channels(base + S_OUTLIER, 4, HEAD_DIM),
+                      v_outliers=_outlier_channels(base + S_OUTLIER + 500, 4, HEAD_DIM))
+    raise ValueError("config index must be 0..5")
 
 
 def custom(name: str, B: int, Hq: int, Hkv: int, lens, seed_index: int = 90, **kw) -> Config:
