@@ -183,10 +183,11 @@ def test_mixed_prefill_then_step(S0, W_, lens):
     assert torch.equal(ob.cpu(), o3.cpu().to(torch.bfloat16))
 
 
-@pytest.mark.parametrize("g", [1, 3, 8, 12, 16])
+@pytest.mark.parametrize("g", [1, 3, 6, 8, 10, 12, 14, 16])
 def test_mixed_gqa_ratios(g):
-    """Every query-head grouping the kernels specialize for (4, 8 and 16 heads per
-    block), with ragged lengths and a window that spans several 64-slot chunks."""
+    """Every query-head grouping the kernels specialize for (4, 8, 12 and 16 heads
+    per block, the wide ones also with padding heads), with ragged lengths and a
+    window that spans several 64-slot chunks."""
     S0, W_ = 20, 300
     lens = [1, 19, 21, 320, 321, 333, 900]
     cfg = W.custom("mixed_gqa%d" % g, len(lens), 2 * g, 2, lens, seed_index=210 + g,

@@ -49,8 +49,8 @@ def test_noalloc_matches_workspace_entry_point_two_calls():
 
 
 def test_noalloc_wide_instances():
-    """8 and 12 query heads per KV head (the wide split instances), after each other."""
-    for g, seed in ((8, 73), (12, 74)):
+    """8, 12 and 16 query heads per KV head (the wide split instances), after each other."""
+    for g, seed in ((8, 73), (12, 74), (16, 97)):
         case = make_case(W.custom("noalloc_g%d" % g, 3, 2 * g, 2, [1500, 64, 333], seed_index=seed,
                                   k_outliers=(3, 40)))
         _check(case, 4)
