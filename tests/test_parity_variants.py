@@ -133,10 +133,10 @@ def test_variant_append_and_decode_small(variant):
 
 @pytest.mark.parametrize("variant", ["g64", "paper_format_g64", "paper_format", "bf16_meta",
                                      "token_quantile", "per_head_r"])
-@pytest.mark.parametrize("g", [6, 12])
-def test_variant_gqa_6_and_12(variant, g):
+@pytest.mark.parametrize("g", [6, 12, 15])
+def test_variant_gqa_wide(variant, g):
     """Query heads per KV head that are not a multiple of 4 (padding heads) and the
-    wide score path (5-8 and 9-16 heads per KV head) in every group size and
+    wide score path (5-8, 9-12 and 13-16 heads per KV head) in every group size and
     metadata format, ragged lengths, 1 and 3 splits."""
     cfg = W.custom("var_g%d_%s" % (g, variant), 4, 2 * g, 2, [1, 65, 200, 777],
                    seed_index=260 + g + list(VARIANTS).index(variant), k_outliers=(5, 90),
