@@ -30,6 +30,9 @@ SOURCES = {
     "decode.hip": [],
     # keep MFMA accumulators in VGPRs: the kernel shifts and reads them with VALU ops
     "decode_mfma.hip": ["-mllvm", "-amdgpu-mfma-vgpr-form=1"],
+    # the two-chunk split instances: the same flags and the max-ilp scheduler
+    "decode_mfma_wide2.hip": ["-mllvm", "-amdgpu-mfma-vgpr-form=1", "-mllvm",
+                              "-amdgpu-sched-strategy=max-ilp"],
     "bf16_decode.hip": [],
     "mixed.hip": [],
     "calib.hip": ["-ffp-contract=off"],

@@ -1507,8 +1507,38 @@ __global__ __launch_bounds__(64) __attribute__((
   }
 }
 
+// The launches of the NCH-chunk instances for the given quantizer format.
+template <int NCH>
+void launch_split_nch(const SplitLaunch& a, bool mixed, int meta_bf16, int ng) {
+  auto go = [&](auto kernel) {
+    hipLaunchKernelGGL(kernel, dim3((unsigned)a.blocks), dim3(64), 0, a.stream, a.pages, a.Hkv, a.Hq,
+                       a.block_table, a.max_pages, a.seq_lens, a.num_splits, a.ranges, a.B, a.qt,
+                       a.part_o, a.part_ml, a.S0, a.W, a.row_stride);
+  };
+  auto by_ng = [&](auto mixed_c, auto bf_c) {
+    constexpr bool M = decltype(mixed_c)::value, BFV = decltype(bf_c)::value;
+    if (ng == 4) go(split_mfma_kernel<M, BFV, 4, NCH>);
+    else if (ng == 2) go(split_mfma_kernel<M, BFV, 2, NCH>);
+    else go(split_mfma_kernel<M, BFV, 1, NCH>);
+  };
+  using T = std::true_type;
+  using F = std::false_type;
+  if (mixed) {
+    if (meta_bf16) by_ng(T{}, T{});
+    else by_ng(T{}, F{});
+  } else {
+    if (meta_bf16) by_ng(F{}, T{});
+    else by_ng(F{}, F{});
+  }
+}
+
 }  // namespace
 
+#ifdef OSCAR_SPLIT_TWO_CHUNK_UNIT
+void launch_split_two_chunk(const SplitLaunch& a, bool mixed, int meta_bf16, int ng) {
+  launch_split_nch<2>(a, mixed, meta_bf16, ng);
+}
+#else
 hipError_t launch_decode_split_mfma(const uint8_t* pages, int Hkv, int B, int Hq,
                                     const int32_t* block_table, int max_pages,
                                     const int32_t* seq_lens, int num_splits, int cus,
@@ -1522,36 +1552,31 @@ hipError_t launch_decode_split_mfma(const uint8_t* pages, int Hkv, int B, int Hq
                       : std::max<int64_t>(1, (int64_t)split_waves_per_cu(nch) * cus / Hkv);
   const int64_t blocks = ranges * Hkv;
   if (blocks > 0x7fffffffLL) return hipErrorInvalidConfiguration;
-  const int S0 = mixed ? mixed->S0 : 0, W = mixed ? mixed->W : 0;
-  const int stride = mixed ? mixed->row_stride : num_splits;
-  auto go = [&](auto kernel) {
-    hipLaunchKernelGGL(kernel, dim3((unsigned)blocks), dim3(64), 0, st, pages, Hkv, Hq,
-                       block_table, max_pages, seq_lens, num_splits, (int)ranges, B, qt, part_o,
-                       part_ml, S0, W, stride);
-  };
-  auto by_nch = [&](auto mixed_c, auto bf_c, auto ng_c) {
-    constexpr bool M = decltype(mixed_c)::value, BFV = decltype(bf_c)::value;
-    constexpr int NGV = decltype(ng_c)::value;
-    if (nch == 1) go(split_mfma_kernel<M, BFV, NGV, 1>);
-    else if (nch == 2) go(split_mfma_kernel<M, BFV, NGV, 2>);
-    else if (nch == 3) go(split_mfma_kernel<M, BFV, NGV, 3>);
-    else go(split_mfma_kernel<M, BFV, NGV, 4>);
-  };
-  auto by_ng = [&](auto mixed_c, auto bf_c) {
-    if (ng == 4) by_nch(mixed_c, bf_c, std::integral_constant<int, 4>{});
-    else if (ng == 2) by_nch(mixed_c, bf_c, std::integral_constant<int, 2>{});
-    else by_nch(mixed_c, bf_c, std::integral_constant<int, 1>{});
-  };
-  using T = std::true_type;
-  using F = std::false_type;
-  if (mixed) {
-    if (meta_bf16) by_ng(T{}, T{});
-    else by_ng(T{}, F{});
-  } else {
-    if (meta_bf16) by_ng(F{}, T{});
-    else by_ng(F{}, F{});
-  }
+  SplitLaunch a;
+  a.pages = pages;
+  a.Hkv = Hkv;
+  a.Hq = Hq;
+  a.block_table = block_table;
+  a.max_pages = max_pages;
+  a.seq_lens = seq_lens;
+  a.num_splits = num_splits;
+  a.ranges = (int)ranges;
+  a.B = B;
+  a.qt = qt;
+  a.part_o = part_o;
+  a.part_ml = part_ml;
+  a.S0 = mixed ? mixed->S0 : 0;
+  a.W = mixed ? mixed->W : 0;
+  a.row_stride = mixed ? mixed->row_stride : num_splits;
+  a.blocks = blocks;
+  a.stream = st;
+  const bool mx = mixed != nullptr;
+  if (nch == 1) launch_split_nch<1>(a, mx, meta_bf16, ng);
+  else if (nch == 2) launch_split_two_chunk(a, mx, meta_bf16, ng);
+  else if (nch == 3) launch_split_nch<3>(a, mx, meta_bf16, ng);
+  else launch_split_nch<4>(a, mx, meta_bf16, ng);
   return hipGetLastError();
 }
+#endif
 
 }  // namespace oscar

@@ -138,6 +138,24 @@ hipError_t launch_decode_split_mfma(const uint8_t* pages, int Hkv, int B, int Hq
                                     const float* qt, float* part_o, float* part_ml,
                                     hipStream_t st, int meta_bf16, int ng,
                                     const MixedSpec* mixed);
+// One launch of the split kernel: its arguments and grid (blocks one-wave groups).
+struct SplitLaunch {
+  const uint8_t* pages;
+  int Hkv, Hq;
+  const int32_t* block_table;
+  int max_pages;
+  const int32_t* seq_lens;
+  int num_splits, ranges, B;
+  const float* qt;
+  float* part_o;
+  float* part_ml;
+  int S0, W, row_stride;
+  int64_t blocks;
+  hipStream_t stream;
+};
+// The instances for 5 to 8 query heads per kv-head, compiled in a unit of their own
+// (decode_mfma_wide2.hip) with another instruction scheduler.
+void launch_split_two_chunk(const SplitLaunch& a, bool mixed, int meta_bf16, int ng);
 int device_cus();  // compute units of the current device (cached)
 // mixed != nullptr: rows of num_splits + 1 slots, the last one in the original
 // basis (added after the back-rotation).

@@ -12,6 +12,8 @@ from asm_scan import scan
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
 CSRC = os.path.join(ROOT, "paper_2605_17757_amd", "csrc")
 SCANNED = {"decode_mfma.hip"}
+# the units built from it (the second with the two-chunk instances only)
+UNITS = ["decode_mfma.hip", "decode_mfma_wide2.hip"]
 
 
 def test_inline_asm_only_in_scanned_sources():
@@ -28,15 +30,15 @@ def test_inline_asm_only_in_scanned_sources():
 
 @pytest.mark.skipif(shutil.which("hipcc") is None and not os.path.exists("/opt/rocm/bin/hipcc"),
                     reason="hipcc not installed")
-def test_inline_asm_respects_mfma_wait_states(tmp_path):
+@pytest.mark.parametrize("unit", UNITS)
+def test_inline_asm_respects_mfma_wait_states(tmp_path, unit):
     from paper_2605_17757_amd import build as B
-    (src,) = SCANNED
-    out = tmp_path / "decode_mfma.s"
-    cmd = [B.HIPCC, *B.COMMON, *B.SOURCES[src], "--cuda-device-only", "-S",
-           os.path.join(B.CSRC, src), "-o", str(out)]
+    out = tmp_path / unit.replace(".hip", ".s")
+    cmd = [B.HIPCC, *B.COMMON, *B.SOURCES[unit], "--cuda-device-only", "-S",
+           os.path.join(B.CSRC, unit), "-o", str(out)]
     subprocess.run(cmd, check=True, stderr=subprocess.DEVNULL)
     r = scan(out.read_text())
-    assert r["blocks"] > 100  # the helpers are inlined into every instance
+    assert r["blocks"] > 20  # the helpers are inlined into every instance
     assert r["war"] == [], r["war"][:5]
     assert r["raw"] == [], r["raw"][:5]
     assert r["dpp"] == [], r["dpp"][:5]
